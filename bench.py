@@ -1,0 +1,132 @@
+#!/usr/bin/env python3
+"""Derived tuples/s to fixpoint on one MI355X.
+
+Workload: transitive closure plus per-source reach count over an R-MAT graph
+(2^14 nodes, 2^18 distinct edges, a=0.57 b=0.19 c=0.19 d=0.05, seed 5) -- the
+largest of the engine's five workloads.  One step is one complete
+xl_fixpoint_run of the program (index build, seed, every semi-naive round,
+the count stratum) with the input edges already resident in device memory;
+derived relations are cleared before each step.
+
+Prints one JSON line.  `roofline` covers the dominant kernel (the fused
+delta-expand / probe / insert kernel), timed live with HIP events on the
+engine's stream; `cpu_baseline` times the CPU oracle on a bounded sample of
+the same workload (the closure rows of a few sources).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+
+
+def _algorithmic_bytes(st: dict) -> float:
+    """Bytes the fused join/insert kernel must move, by its definition.
+
+    Per source (delta) row: the row (8 B) and its index range (8 B).  Per
+    candidate: the matched edge's target (4 B) and one probe of the packed key
+    (8 B).  Per new tuple: the key written to the table (8 B) and the row
+    appended to the relation (8 B).
+    """
+    return 16.0 * st["emit_source_rows"] + 12.0 * st["emit_candidates"] + 16.0 * st["emit_new"]
+
+
+def cpu_baseline(wl, n_sources: int, seed: int = 7) -> dict:
+    from oracle import evaluate
+    from paper_2609_27203_amd import workloads as W
+    src = wl.edb["edge"][1][0]
+    rng = np.random.default_rng(seed)
+    pick = np.sort(rng.choice(np.unique(src), n_sources, replace=False)).astype(np.int32)
+    idb = {"path": ("i32", "i32"), "reach_count": ("i32", "i32")}
+    t0 = time.perf_counter()
+    res = evaluate(W.TC_COUNT_RULES, wl.edb, idb, restrict={"path": (0, pick)})
+    dt = time.perf_counter() - t0
+    rows = sum(len(r[1][0]) for r in res.relations.values())
+    return {"value": rows / dt, "unit": "derived tuples/s", "cores": 1, "kind": "oracle",
+            "sample": f"naive evaluation restricted to the closure of {n_sources} sampled sources "
+                      f"({rows} derived rows in {dt:.2f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workspace-gb", type=float, default=24.0)
+    ap.add_argument("--cpu-sources", type=int, default=48)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this engine "
+              "(the multi-GPU partitioning is design only)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_27203_amd import workloads as W
+    from paper_2609_27203_amd import xlh
+
+    wl = W.tc_rmat()
+    ctx = xlh.Context(device=0, workspace_bytes=int(args.workspace_gb * (1 << 30)))
+    ctx.set_option("profile", 1)
+    for name, (types, cols) in wl.edb.items():
+        ctx.relation(name, types).load(cols)
+    for name, types in wl.idb.items():
+        ctx.relation(name, types)
+    prog = ctx.compile(wl.rules)
+
+    def step():
+        for name in wl.idb:
+            ctx.relations[name].clear()
+        return prog.run()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        stats.append(step())
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = 1e3 * dt / args.steps
+    derived = stats[-1]["derived_tuples"]
+
+    emit_ms = sum(s["emit_ms"] for s in stats)
+    emit_launches = sum(s["emit_launches"] for s in stats)
+    ab = sum(_algorithmic_bytes(s) for s in stats)
+    achieved = ab / (emit_ms * 1e-3) / 1e9 if emit_ms > 0 else 0.0
+    roofline = {
+        "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+        "kernel": "stage_k<EM_SET, index> (fused delta expand + probe + insert)",
+        "launches_per_step": emit_launches / args.steps,
+        "avg_launch_ms": emit_ms / max(emit_launches, 1),
+        "algorithmic_bytes_per_step": ab / args.steps,
+    }
+    line = {
+        "metric": "derived tuples/sec to fixpoint (1 MI355X)",
+        "value": derived / (ms_per_step * 1e-3),
+        "unit": "derived tuples/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32", "data": "synthetic",
+        "config": {"workload": "R-MAT transitive closure + reach_count (2^14 nodes, 2^18 edges, seed 5)",
+                   "derived_tuples": derived, "iterations": stats[-1]["iterations"],
+                   "candidates": stats[-1]["candidates_total"], "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sources)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    main()

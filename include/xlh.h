@@ -1,0 +1,211 @@
+/*
+ * xlh -- semi-naive fixpoint evaluation of recursive Datalog rules on one
+ * AMD Instinct MI355X (gfx950).  Plain C ABI: opaque handles, plain pointers
+ * and sizes, no C++ or framework types.
+ *
+ * What is computed.  Relations are sets of typed tuples over int32 and
+ * IEEE-754 binary32 columns (the paper's typed predicates, Sec. 3.1-3.2).
+ * Rules use the paper's surface syntax (Sec. 3.1, 3.3, 3.5):
+ *
+ *     head(X, Y) :- body1(X, Z), body2(Z, Y), X != Y.
+ *     dist(S, Y, min(D)) :- dist(S, Z, D1), edge(Z, Y, W), D is D1 + W.
+ *
+ * Body literals are atoms (variables, '_' or integer constants as arguments),
+ * comparisons (!= == < <= > >=) and 'V is T (+|- T)*' arithmetic.  A head may
+ * carry one aggregate -- count, sum, min, max, logsumexp -- in its last
+ * position (Sec. 3.5).  xl_fixpoint_run evaluates the program stratum by
+ * stratum; each recursive stratum runs semi-naive iteration (Sec. 4.1,
+ * Algorithm 1): seed the delta from the rules, then repeatedly join the delta
+ * against the full relations, project the head tuples, deduplicate or
+ * aggregate them by key, take the difference with the full relation and
+ * merge, until every delta is empty.
+ *
+ * Aggregates inside recursion go beyond the paper (its stratifier rejects
+ * them, Sec. 3.5).  They are accepted as follows: min and max in any
+ * recursive rule (the delta holds keys that are new or strictly improved);
+ * sum and logsumexp only when every recursive rule of the stratum is linear
+ * (the delta of round k holds the fold of the contributions derived from the
+ * delta of round k-1, and the full relation accumulates them -- finite only
+ * when derivations are acyclic, otherwise the iteration cap is reached);
+ * count never (XL_UNSUPPORTED).
+ *
+ * Memory.  The caller owns a device workspace and a HIP stream; the library
+ * sub-allocates every relation, index, hash table and delta buffer from that
+ * workspace and never allocates device memory of its own (it allocates one
+ * small pinned host block per context for control reads).  Exceeding the
+ * workspace is XL_RESOURCE_EXHAUSTED (Sec. 2.2: byte budget), exceeding a
+ * relation's max_rows is XL_CAPACITY_EXCEEDED, reaching the iteration cap is
+ * XL_CONVERGENCE_FAILURE.  There is no host fallback: every step of
+ * evaluation runs in the library's HIP kernels.
+ *
+ * Threading.  Calls are blocking and a context must be used from one thread
+ * at a time.  Every call returns an xl_status; out-parameters are written
+ * only on XL_OK except where stated.  xl_last_error() describes the most
+ * recent failure on a context.
+ */
+#ifndef XLH_H
+#define XLH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    XL_OK = 0,
+    XL_INVALID_ARGUMENT = 1,   /* null handle, bad size, wrong relation, ... */
+    XL_TYPE_MISMATCH = 2,      /* a variable used at two column types (Sec. 3.2) */
+    XL_UNSUPPORTED = 3,        /* a rule form outside the accepted subset */
+    XL_RESOURCE_EXHAUSTED = 4, /* the workspace byte budget is exceeded (Sec. 2.2) */
+    XL_CAPACITY_EXCEEDED = 5,  /* a fixed row capacity is exceeded (Sec. 2.2) */
+    XL_CONVERGENCE_FAILURE = 6,/* the iteration cap was reached (Sec. 2.2, Alg. 1) */
+    XL_DEVICE_ERROR = 7,       /* a HIP runtime call failed */
+    XL_PARSE_ERROR = 8         /* the rule text does not parse */
+} xl_status;
+
+typedef enum { XL_I32 = 1, XL_F32 = 2 } xl_type;
+
+typedef struct xl_context xl_context;
+typedef struct xl_relation xl_relation;
+typedef struct xl_program xl_program;
+
+#define XL_MAX_ARITY 4
+#define XL_STATS_ROUNDS 256
+
+/*
+ * Terminal receipt of one xl_fixpoint_run (the paper's bounded terminal
+ * receipt, Sec. 4).  Always written by xl_fixpoint_run, also on failure.
+ *   iterations       semi-naive passes over all recursive strata; the seed is
+ *                    not a pass, the final pass that finds every delta empty is
+ *   delta_rows[i]    rows in the delta after the i-th recorded round: for each
+ *                    recursive stratum its seed then each pass; for each
+ *                    non-recursive stratum the rows it produced (first
+ *                    XL_STATS_ROUNDS rounds; rounds_recorded counts them all)
+ *   candidates_total head tuples emitted by the join/project step, all rounds
+ *   derived_tuples   final rows over all derived relations
+ *   control_bytes_read  device->host bytes read to drive the loop
+ *   ms_total         device time of the whole run (HIP events on the stream)
+ */
+typedef struct {
+    int32_t status;
+    int32_t iterations;
+    int32_t strata;
+    int32_t rounds_recorded;
+    int64_t delta_rows[XL_STATS_ROUNDS];
+    int64_t candidates_total;
+    int64_t new_tuples_total;
+    int64_t derived_tuples;
+    int64_t peak_workspace_bytes;
+    int64_t control_bytes_read;
+    int64_t table_grows;
+    double ms_total;
+    /* Fused join/insert kernels (set, min and max heads), timed with HIP
+     * events on the context's stream when the "profile" option is 1. */
+    double emit_ms;
+    int64_t emit_launches;
+    int64_t emit_source_rows;   /* delta or driver rows those launches read */
+    int64_t emit_candidates;    /* head tuples they produced */
+    int64_t emit_new;           /* keys they inserted (new or improved rows) */
+} xl_fixpoint_stats;
+
+/*
+ * Create a context on HIP device `device` that enqueues all work on
+ * `hip_stream` (a hipStream_t, may be NULL for the null stream) and
+ * sub-allocates from `workspace` (device memory of `workspace_bytes` bytes,
+ * owned by the caller; it and the stream must outlive the context).
+ * device = -1 creates a planning-only context: relations can be declared and
+ * rules compiled (no device work), but loads and runs fail with
+ * XL_INVALID_ARGUMENT.
+ */
+xl_status xl_context_create(int device, void* hip_stream, void* workspace,
+                            size_t workspace_bytes, xl_context** out);
+
+/*
+ * Tunables (key, value):
+ *   "hash_min_log2"   log2 of the smallest hash table (default 22)
+ *   "index_mode"      0 = automatic, 1 = always open-addressing hash tables,
+ *                     2 = prefer dense key-domain tables where they fit
+ *   "profile"         1 = time the fused join/insert kernels (receipt emit_*)
+ * XL_INVALID_ARGUMENT for an unknown key or value.
+ */
+xl_status xl_context_set_option(xl_context* ctx, const char* key, int64_t value);
+
+/*
+ * Declare relation `name` with `arity` columns of types `cols[0..arity)`.
+ * max_rows bounds the rows it may hold (0 = bounded only by the workspace);
+ * a load or a run that would exceed it fails with XL_CAPACITY_EXCEEDED.
+ * The handle belongs to the context.
+ */
+xl_status xl_relation_create(xl_context* ctx, const char* name, int arity,
+                             const xl_type* cols, int64_t max_rows, xl_relation** out);
+
+/*
+ * Replace the relation's contents with `nrows` rows given column-wise:
+ * cols[j] points at nrows int32 or float32 values (host memory, or device
+ * memory when cols_on_device != 0).  The data is copied into the workspace;
+ * the pointers are only borrowed for the call.  Duplicate rows are removed
+ * (relations are sets).  Returns after the copy has completed.
+ */
+xl_status xl_relation_load(xl_relation* rel, const void* const* cols, int64_t nrows,
+                           int cols_on_device);
+
+/* Empty the relation (O(1); its storage returns to the workspace). */
+xl_status xl_relation_clear(xl_relation* rel);
+
+/* Number of rows currently held. */
+xl_status xl_relation_size(const xl_relation* rel, int64_t* out_rows);
+
+/*
+ * Copy the relation out in canonical order: rows ascending lexicographically
+ * by column (int32 signed, float32 by IEEE totalOrder).  cols[j] receives
+ * the j-th column (host or device memory per cols_on_device) and must hold
+ * capacity_rows values.  If the relation has more rows, nothing is copied,
+ * *out_rows is set to the number needed and XL_CAPACITY_EXCEEDED returned.
+ */
+xl_status xl_relation_read(const xl_relation* rel, void* const* cols, int64_t capacity_rows,
+                           int64_t* out_rows, int cols_on_device);
+
+/*
+ * Compile rule text against the context's relations (every predicate must
+ * have been declared with xl_relation_create).  Host-only work: parse, type
+ * check, stratify (strongly connected components of the dependency graph),
+ * derive the delta variants of recursive rules and plan each rule as a
+ * pipeline of index joins.  XL_PARSE_ERROR, XL_TYPE_MISMATCH or
+ * XL_UNSUPPORTED on failure, with the reason in xl_last_error().
+ */
+xl_status xl_rule_compile(xl_context* ctx, const char* rules_text, xl_program** out);
+
+/*
+ * Human-readable plan (strata, delta variants, join steps).  Writes at most
+ * cap bytes including the terminating NUL; *needed receives the full size.
+ */
+xl_status xl_program_explain(const xl_program* prog, char* buf, size_t cap, size_t* needed);
+
+/*
+ * Evaluate the program to its fixpoint.  Set, min and max heads start from
+ * their current contents (empty after xl_relation_clear; loaded rows act as
+ * extra facts, so a loaded fixpoint is a resume point); count, sum and
+ * logsumexp heads are recomputed from empty.  Relations that are not rule
+ * heads are read only.
+ * max_iterations caps the semi-naive passes of each recursive stratum;
+ * reaching it returns XL_CONVERGENCE_FAILURE and leaves derived relations
+ * unspecified.  out_stats (may be NULL) is written on success and failure.
+ */
+xl_status xl_fixpoint_run(xl_program* prog, int64_t max_iterations,
+                          xl_fixpoint_stats* out_stats);
+
+const char* xl_last_error(const xl_context* ctx);
+const char* xl_status_string(xl_status status);
+
+void xl_program_destroy(xl_program* prog);
+void xl_relation_destroy(xl_relation* rel);
+/* Destroys the context and every relation and program created on it. */
+void xl_context_destroy(xl_context* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XLH_H */

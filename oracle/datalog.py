@@ -274,7 +274,10 @@ def _eval_body(rule, rels, var_types):
             if v not in binding:
                 binding[v] = rows[j][ri]
         n = li.size
+    atom_vars = {t[1] for _, terms in rule.atoms for t in terms if t[0] == "var"}
     for var, parts in rule.assigns:
+        if var in atom_vars:
+            raise ValueError(f"{var} is both an 'is' result and an atom argument")
         ptypes = set()
         vals = []
         for sign, t in parts:

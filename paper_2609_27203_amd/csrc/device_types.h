@@ -1,0 +1,132 @@
+// Plain descriptors passed by value to the HIP kernels.  The host planner
+// fills them; the kernels interpret them uniformly across a wavefront (every
+// field is the same for all lanes, so the interpretation costs only scalar
+// instructions).
+#pragma once
+#include <stdint.h>
+
+namespace xlh {
+
+constexpr int MAXV = 8;     // variable slots per rule
+constexpr int MAXC = 4;     // columns per relation (XL_MAX_ARITY)
+constexpr int MAXOPS = 12;  // micro-ops (comparisons / arithmetic) per stage
+constexpr int MAXK = 8;     // constants per stage
+
+enum ValType : uint8_t { T_I32 = 1, T_F32 = 2 };
+
+// What to do with one column of a row source or an index relation.
+enum ColActKind : int8_t { CA_NONE = 0, CA_BIND = 1, CA_CHECK_SLOT = 2, CA_CHECK_CONST = 3 };
+struct ColAct {
+  int8_t kind;
+  int8_t slot;
+  uint8_t type;   // ValType of the column (equality is IEEE for f32)
+  int8_t pad;
+  uint32_t cval;  // constant bits for CA_CHECK_CONST
+};
+
+// Micro-ops run after all columns of a stage are bound.
+enum OpKind : uint8_t { OP_CMP = 1, OP_ADD = 2, OP_SUB = 3, OP_MOV = 4 };
+enum CmpKind : uint8_t { CMP_NE = 0, CMP_EQ, CMP_LT, CMP_LE, CMP_GT, CMP_GE };
+// Operand encoding: >= 0 is a slot, < 0 is constant index (-1 - k).
+struct MicroOp {
+  uint8_t kind, cmp, type, pad;
+  int8_t dst, a, b, pad2;
+};
+
+// Rows that drive a stage: a relation, a delta, or materialized bindings
+// (up to one column per variable slot).
+struct RowSource {
+  const uint32_t* col[MAXV];
+  int64_t n;
+  int32_t ncols;
+  ColAct act[MAXV];
+};
+
+// Index join: the rows of a relation whose key column equals slot key_slot.
+// off[k] .. off[k+1] delimit rows with key value key_lo + k; col[] are the
+// relation's columns permuted into key order.
+struct IndexProbe {
+  const uint32_t* off;
+  const uint32_t* col[MAXC];
+  int32_t ncols;
+  int32_t key_lo;
+  uint32_t key_range;
+  int8_t key_slot;
+  ColAct act[MAXC];
+};
+
+// Head key packing: ((v0 - lo0) << shift) | (v1 - lo1), both as unsigned.
+struct KeyPack {
+  int32_t nkey;
+  int8_t slot[2];
+  int32_t lo[2];
+  int32_t shift;
+};
+
+// Open-addressing slot for keyed values (min/max/sum/logsumexp/count heads).
+struct Slot16 {
+  unsigned long long key;
+  uint32_t val;
+  uint32_t stamp;
+};
+
+constexpr unsigned long long EMPTY_KEY = ~0ull;
+
+enum EmitMode : int32_t {
+  EM_COUNT = 0,   // count the rows each chunk would emit
+  EM_MAT = 1,     // write bindings or (packed key, value) at scanned offsets
+  EM_SET = 2,     // insert-if-absent into a key set; winners append head rows
+  EM_MINMAX = 3,  // atomic improvement in a keyed table; improved keys to delta
+};
+
+// Device-side counters of one emission (cleared per round).
+enum Counter : int32_t {
+  CNT_APPENDED = 0,   // rows appended to the output list
+  CNT_INSERTED = 1,   // keys newly inserted into the table
+  CNT_OVERFLOW = 2,   // set when inserted keys pass the table's load limit
+  CNT_CANDIDATES = 3, // head tuples produced by the join/project step
+  CNT_FATAL = 4,      // probe sequence exhausted (must never happen)
+  CNT_N = 8
+};
+
+struct EmitSpec {
+  int32_t mode;
+  KeyPack key;
+  int8_t val_slot;
+  uint8_t val_type;
+  uint8_t is_max;        // EM_MINMAX: fold is max (stored complemented)
+  uint8_t mat_packed;    // EM_MAT: write (packed key, value) instead of slots
+  int32_t nout;
+  int8_t out_slot[MAXV];
+  uint32_t* out_col[MAXV];
+  unsigned long long* out_key;
+  uint32_t* out_val;
+  const unsigned long long* chunk_off;  // EM_MAT: exclusive offsets per chunk
+  int64_t mat_base;                     // EM_MAT: added to every output position
+  unsigned long long* chunk_cnt;        // EM_COUNT: rows per chunk
+  // EM_SET
+  unsigned long long* table;
+  unsigned long long mask;   // capacity - 1 (capacity is a power of two)
+  uint32_t* row_col[2];      // head row list (key columns), written at row_base + k
+  int64_t row_base;
+  int64_t row_cap;
+  // EM_MINMAX
+  Slot16* table16;
+  uint32_t round;
+  uint32_t* delta_idx;
+  // shared
+  unsigned long long* counters;
+  unsigned long long limit;  // overflow threshold on CNT_INSERTED
+};
+
+struct StageArgs {
+  RowSource src;
+  int32_t has_index;
+  IndexProbe idx;
+  int32_t nops;
+  MicroOp ops[MAXOPS];
+  uint32_t consts[MAXK];
+  EmitSpec emit;
+};
+
+}  // namespace xlh

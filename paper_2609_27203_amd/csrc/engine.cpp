@@ -1,0 +1,1026 @@
+// Workspace arena, relation storage, index builds and the semi-naive
+// fixpoint driver (host orchestration; every data-plane step is a kernel).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <memory>
+
+#include "engine.h"
+#include "kernels.h"
+
+namespace xlh {
+
+typedef unsigned long long u64;
+
+// Grid cap (blocks of four wavefronts) of the insert-or-improve emission kernels.
+constexpr int EMIT_GRID = 2048;
+
+// ================================================================== arena
+void Arena::init(char* base, size_t size) {
+  base_ = base;
+  size_ = size & ~(size_t)255;
+  free_.clear();
+  used_.clear();
+  if (size_) free_[0] = size_;
+  in_use_ = peak_ = 0;
+}
+
+void* Arena::alloc(size_t bytes) {
+  bytes = (std::max<size_t>(bytes, 1) + 255) & ~(size_t)255;
+  for (auto it = free_.begin(); it != free_.end(); ++it) {
+    if (it->second < bytes) continue;
+    size_t off = it->first, sz = it->second;
+    free_.erase(it);
+    if (sz > bytes) free_[off + bytes] = sz - bytes;
+    used_[off] = bytes;
+    in_use_ += bytes;
+    peak_ = std::max(peak_, in_use_);
+    return base_ + off;
+  }
+  return nullptr;
+}
+
+void Arena::release(void* p) {
+  if (!p) return;
+  size_t off = (size_t)((char*)p - base_);
+  auto it = used_.find(off);
+  if (it == used_.end()) return;
+  size_t sz = it->second;
+  used_.erase(it);
+  in_use_ -= sz;
+  auto nx = free_.lower_bound(off);
+  if (nx != free_.end() && nx->first == off + sz) {
+    sz += nx->second;
+    free_.erase(nx);
+  }
+  auto pv = free_.lower_bound(off);
+  if (pv != free_.begin()) {
+    --pv;
+    if (pv->first + pv->second == off) {
+      pv->second += sz;
+      return;
+    }
+  }
+  free_[off] = sz;
+}
+
+size_t Arena::largest_free() const {
+  size_t m = 0;
+  for (auto& kv : free_) m = std::max(m, kv.second);
+  return m;
+}
+
+// ================================================================== helpers
+#define XL_TRY(x)                        \
+  do {                                   \
+    xl_status _s = (x);                  \
+    if (_s != XL_OK) return _s;          \
+  } while (0)
+
+#define HIP_TRY(ctx, x)                                                                  \
+  do {                                                                                   \
+    hipError_t _e = (x);                                                                 \
+    if (_e != hipSuccess)                                                                \
+      return (ctx)->fail(XL_DEVICE_ERROR, std::string(#x) + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+namespace {
+
+// Arena block released on scope exit unless kept.
+struct Buf {
+  Context* c = nullptr;
+  void* p = nullptr;
+  Buf() = default;
+  explicit Buf(Context* cc) : c(cc) {}
+  Buf(const Buf&) = delete;
+  Buf& operator=(const Buf&) = delete;
+  ~Buf() { reset(); }
+  void reset() {
+    if (c && p) c->arena.release(p);
+    p = nullptr;
+  }
+  void* keep() {
+    void* q = p;
+    p = nullptr;
+    return q;
+  }
+  template <typename T>
+  T* as() const {
+    return (T*)p;
+  }
+};
+
+xl_status dalloc(Context* c, size_t bytes, Buf* b, const char* what) {
+  b->c = c;
+  b->reset();
+  b->p = c->arena.alloc(bytes);
+  if (!b->p)
+    return c->fail(XL_RESOURCE_EXHAUSTED,
+                   std::string("workspace exhausted allocating ") + std::to_string(bytes) +
+                       " bytes for " + what + " (in use " + std::to_string(c->arena.in_use()) +
+                       " of " + std::to_string(c->arena.capacity()) + ", largest free block " +
+                       std::to_string(c->arena.largest_free()) + ")");
+  return XL_OK;
+}
+
+xl_status ctl_read(Context* c, const void* dev, size_t bytes, void* host) {
+  HIP_TRY(c, hipMemcpyAsync(c->pinned, dev, bytes, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  memcpy(host, c->pinned, bytes);
+  c->control_bytes += (int64_t)bytes;
+  return XL_OK;
+}
+
+int bitlen(uint64_t x) {  // bits needed to represent values 0..x
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+uint64_t next_pow2(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Permutation sorting the rows lexicographically (int32 signed, float32
+// totalOrder), built as successive stable radix sorts from the last column.
+xl_status lex_perm(Context* c, uint32_t* const* cols, const uint8_t* types, int arity, int64_t n,
+                   Buf* perm_out) {
+  Buf pa, pb, ka, kb, tmp;
+  XL_TRY(dalloc(c, (size_t)n * 4, &pa, "sort permutation"));
+  XL_TRY(dalloc(c, (size_t)n * 4, &pb, "sort permutation"));
+  XL_TRY(dalloc(c, (size_t)n * 4, &ka, "sort keys"));
+  XL_TRY(dalloc(c, (size_t)n * 4, &kb, "sort keys"));
+  XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
+  HIP_TRY(c, k::iota_u32(pa.as<uint32_t>(), n, c->stream));
+  for (int j = arity - 1; j >= 0; --j) {
+    HIP_TRY(c, k::ordered_key(cols[j], types[j], pa.as<uint32_t>(), ka.as<uint32_t>(), n, c->stream));
+    int alt = 0;
+    HIP_TRY(c, k::radix_sort_u32(ka.as<uint32_t>(), pa.as<uint32_t>(), kb.as<uint32_t>(),
+                                 pb.as<uint32_t>(), n, 32, tmp.p, c->stream, &alt));
+    if (alt) std::swap(pa.p, pb.p);
+  }
+  std::swap(perm_out->p, pa.p);
+  perm_out->c = c;
+  return XL_OK;
+}
+
+xl_status compute_bounds(Context* c, Relation* r) {
+  if (r->nrows == 0) return XL_OK;
+  Buf mm;
+  XL_TRY(dalloc(c, 8 * MAXC, &mm, "bounds"));
+  int32_t init[2 * MAXC];
+  for (int j = 0; j < MAXC; ++j) {
+    init[2 * j] = INT32_MAX;
+    init[2 * j + 1] = INT32_MIN;
+  }
+  HIP_TRY(c, hipMemcpyAsync(mm.p, init, sizeof(init), hipMemcpyHostToDevice, c->stream));
+  for (int j = 0; j < r->arity; ++j)
+    if (r->types[j] == T_I32)
+      HIP_TRY(c, k::minmax_i32((const int32_t*)r->col[j], r->nrows, mm.as<int32_t>() + 2 * j, c->stream));
+  int32_t out[2 * MAXC];
+  XL_TRY(ctl_read(c, mm.p, sizeof(out), out));
+  for (int j = 0; j < r->arity; ++j) {
+    r->lo[j] = out[2 * j];
+    r->hi[j] = out[2 * j + 1];
+  }
+  return XL_OK;
+}
+
+}  // namespace
+
+void relation_free_storage(Relation* r) {
+  for (int j = 0; j < MAXC; ++j) {
+    if (r->col[j]) r->ctx->arena.release(r->col[j]);
+    r->col[j] = nullptr;
+  }
+  r->nrows = 0;
+}
+
+xl_status relation_clear(Relation* r) {
+  relation_free_storage(r);
+  return XL_OK;
+}
+
+// ================================================================== load / read
+xl_status relation_load(Relation* r, const void* const* cols, int64_t n, int on_device) {
+  Context* c = r->ctx;
+  if (c->device < 0) return c->fail(XL_INVALID_ARGUMENT, "planning-only context cannot hold data");
+  if (n < 0 || (n > 0 && !cols)) return c->fail(XL_INVALID_ARGUMENT, "bad row count or column pointers");
+  if (n >= (int64_t)1 << 31) return c->fail(XL_CAPACITY_EXCEEDED, "relations hold fewer than 2^31 rows");
+  for (int j = 0; j < r->arity && n > 0; ++j)
+    if (!cols[j]) return c->fail(XL_INVALID_ARGUMENT, "null column pointer");
+  if (n == 0) {
+    relation_free_storage(r);
+    return XL_OK;
+  }
+  Buf raw[MAXC];
+  for (int j = 0; j < r->arity; ++j) {
+    XL_TRY(dalloc(c, (size_t)n * 4, &raw[j], "loaded column"));
+    HIP_TRY(c, hipMemcpyAsync(raw[j].p, cols[j], (size_t)n * 4,
+                              on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+  }
+  int64_t m = n;
+  Buf fin[MAXC];
+  if (n == 1) {
+    for (int j = 0; j < r->arity; ++j) std::swap(fin[j].p, raw[j].p), fin[j].c = c;
+  } else {
+    // sets: sort rows, flag rows that differ from their predecessor, compact
+    uint32_t* rc[MAXC] = {};
+    for (int j = 0; j < r->arity; ++j) rc[j] = raw[j].as<uint32_t>();
+    Buf perm;
+    XL_TRY(lex_perm(c, rc, r->types, r->arity, n, &perm));
+    Buf sorted[MAXC];
+    const uint32_t* sc[MAXC] = {};
+    for (int j = 0; j < r->arity; ++j) {
+      XL_TRY(dalloc(c, (size_t)n * 4, &sorted[j], "sorted column"));
+      HIP_TRY(c, k::gather_u32(rc[j], perm.as<uint32_t>(), sorted[j].as<uint32_t>(), n, c->stream));
+      sc[j] = sorted[j].as<uint32_t>();
+      raw[j].reset();
+    }
+    Buf flag, pos, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)n * 4, &flag, "dedup flags"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &pos, "dedup positions"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(n), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    HIP_TRY(c, k::row_change_flags(sc, r->arity, n, flag.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), n, tot.as<uint32_t>(),
+                                     tmp.p, c->stream));
+    uint32_t mm = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &mm));
+    m = mm;
+    for (int j = 0; j < r->arity; ++j) {
+      XL_TRY(dalloc(c, (size_t)m * 4, &fin[j], "relation column"));
+      HIP_TRY(c, k::compact_u32(sc[j], flag.as<uint32_t>(), pos.as<uint32_t>(), fin[j].as<uint32_t>(),
+                                n, c->stream));
+    }
+  }
+  if (r->max_rows > 0 && m > r->max_rows)
+    return c->fail(XL_CAPACITY_EXCEEDED, "relation " + r->name + " holds at most " +
+                                             std::to_string(r->max_rows) + " rows, load has " +
+                                             std::to_string(m));
+  relation_free_storage(r);
+  for (int j = 0; j < r->arity; ++j) r->col[j] = (uint32_t*)fin[j].keep();
+  r->nrows = m;
+  XL_TRY(compute_bounds(c, r));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return XL_OK;
+}
+
+xl_status relation_read(const Relation* r, void* const* cols, int64_t cap, int64_t* out_rows,
+                        int on_device) {
+  Context* c = r->ctx;
+  if (cap < r->nrows) {
+    if (out_rows) *out_rows = r->nrows;
+    return c->fail(XL_CAPACITY_EXCEEDED, "output capacity " + std::to_string(cap) + " < " +
+                                             std::to_string(r->nrows) + " rows of " + r->name);
+  }
+  const int64_t n = r->nrows;
+  if (n > 0) {
+    if (!cols) return c->fail(XL_INVALID_ARGUMENT, "null column pointers");
+    for (int j = 0; j < r->arity; ++j)
+      if (!cols[j]) return c->fail(XL_INVALID_ARGUMENT, "null column pointer");
+    Buf perm;
+    XL_TRY(lex_perm(c, r->col, r->types, r->arity, n, &perm));
+    Buf stage;
+    if (!on_device) XL_TRY(dalloc(c, (size_t)n * 4, &stage, "readout staging"));
+    for (int j = 0; j < r->arity; ++j) {
+      uint32_t* dst = on_device ? (uint32_t*)cols[j] : stage.as<uint32_t>();
+      HIP_TRY(c, k::gather_u32(r->col[j], perm.as<uint32_t>(), dst, n, c->stream));
+      if (!on_device) {
+        HIP_TRY(c, hipMemcpyAsync(cols[j], dst, (size_t)n * 4, hipMemcpyDeviceToHost, c->stream));
+        HIP_TRY(c, hipStreamSynchronize(c->stream));
+      }
+    }
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+  }
+  if (out_rows) *out_rows = n;
+  return XL_OK;
+}
+
+// ================================================================== fixpoint run
+namespace {
+
+struct Interval {
+  int64_t lo = INT64_MAX, hi = INT64_MIN;
+  bool empty() const { return lo > hi; }
+  void join(const Interval& o) {
+    lo = std::min(lo, o.lo);
+    hi = std::max(hi, o.hi);
+  }
+  static Interval full() { return {INT32_MIN, INT32_MAX}; }
+};
+
+struct DevIndex {
+  Relation* rel = nullptr;
+  int col = 0;
+  IndexProbe probe{};
+  std::vector<std::unique_ptr<Buf>> owned;
+};
+
+struct HeadRun {
+  Relation* rel = nullptr;
+  Agg agg = Agg::NONE;
+  int fold = k::FOLD_NONE;
+  bool is_set = false, is_minmax = false, is_sortagg = false;
+  int nkey = 1;
+  KeyPack kp{};
+  int bits0 = 1;      // width of the first packed key component
+  double domain = 0;  // number of possible keys
+  Buf table;
+  int64_t cap = 0, keys = 0;
+  // set heads: append-only row list of every tuple; the delta is a range
+  Buf rows[2];
+  int64_t rows_cap = 0, nrows = 0, dbeg = 0, dend = 0, round_begin = 0;
+  // aggregate heads: delta rows (k0[, k1], value)
+  Buf drow[3];
+  int64_t dcap = 0, dn = 0;
+  Buf didx;
+  int64_t didx_n = 0;
+  Buf ckey, cval;
+  int64_t ccap = 0, cn = 0;
+  uint32_t round = 0;
+  int64_t preloaded = 0;
+};
+
+struct Runner {
+  Context* c;
+  Program* prog;
+  xl_fixpoint_stats* st;
+  std::vector<std::unique_ptr<DevIndex>> indexes;
+  std::vector<std::unique_ptr<HeadRun>> heads;
+  int64_t cands = 0;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  ~Runner() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+
+  HeadRun* head_of(const Relation* r) {
+    for (auto& h : heads)
+      if (h->rel == r) return h.get();
+    return nullptr;
+  }
+
+  void record(int64_t rows) {
+    if (st->rounds_recorded < XL_STATS_ROUNDS) st->delta_rows[st->rounds_recorded] = rows;
+    st->rounds_recorded++;
+  }
+
+  // ------------------------------------------------------------ indexes
+  xl_status get_index(Relation* rel, int col, IndexProbe* out) {
+    for (auto& ix : indexes)
+      if (ix->rel == rel && ix->col == col) {
+        *out = ix->probe;
+        return XL_OK;
+      }
+    auto ix = std::make_unique<DevIndex>();
+    ix->rel = rel;
+    ix->col = col;
+    IndexProbe& p = ix->probe;
+    const int64_t n = rel->nrows;
+    p.ncols = rel->arity;
+    auto own = [&](size_t bytes, const char* what, void** ptr) -> xl_status {
+      ix->owned.push_back(std::make_unique<Buf>());
+      XL_TRY(dalloc(c, bytes, ix->owned.back().get(), what));
+      *ptr = ix->owned.back()->p;
+      return XL_OK;
+    };
+    if (n == 0) {
+      void* off;
+      XL_TRY(own(8, "index offsets", &off));
+      HIP_TRY(c, hipMemsetAsync(off, 0, 8, c->stream));
+      p.off = (uint32_t*)off;
+      p.key_lo = 0;
+      p.key_range = 0;
+    } else {
+      if (rel->types[col] != T_I32) return c->fail(XL_UNSUPPORTED, "index key columns must be int32");
+      if (n > ((int64_t)1 << 25))
+        return c->fail(XL_UNSUPPORTED, "indexed relation " + rel->name + " exceeds 2^25 rows");
+      const int64_t range = (int64_t)rel->hi[col] - rel->lo[col] + 1;
+      if (range > ((int64_t)1 << 30))
+        return c->fail(XL_UNSUPPORTED, "key range of " + rel->name + " column " + std::to_string(col) +
+                                           " exceeds 2^30 values");
+      Buf keys, keys2, perm, perm2, tmp;
+      XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+      XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
+      XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));
+      XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
+      XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
+      HIP_TRY(c, k::sub_lo(rel->col[col], rel->lo[col], keys.as<uint32_t>(), n, c->stream));
+      HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
+      int alt = 0;
+      HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(),
+                                   perm2.as<uint32_t>(), n, std::max(1, bitlen((uint64_t)range - 1)),
+                                   tmp.p, c->stream, &alt));
+      uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
+      uint32_t* sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+      for (int j = 0; j < rel->arity; ++j) {
+        void* cj;
+        XL_TRY(own((size_t)n * 4, "index column", &cj));
+        HIP_TRY(c, k::gather_u32(rel->col[j], sp, (uint32_t*)cj, n, c->stream));
+        p.col[j] = (uint32_t*)cj;
+      }
+      void* off;
+      XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
+      HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
+      p.off = (uint32_t*)off;
+      p.key_lo = rel->lo[col];
+      p.key_range = (uint32_t)range;
+    }
+    *out = p;
+    indexes.push_back(std::move(ix));
+    return XL_OK;
+  }
+
+  // ------------------------------------------------------------ domains / heads
+  Interval col_interval(Relation* rel, int col, const std::map<Relation*, std::vector<Interval>>& dom) {
+    auto it = dom.find(rel);
+    if (it != dom.end()) {
+      if (col < (int)it->second.size()) return it->second[col];
+      return Interval::full();
+    }
+    if (rel->nrows == 0) return Interval{};
+    if (rel->types[col] != T_I32) return Interval::full();
+    return Interval{rel->lo[col], rel->hi[col]};
+  }
+
+  xl_status setup_heads(Stratum& s) {
+    std::map<Relation*, std::vector<Interval>> dom;
+    for (Relation* h : s.heads) {
+      const Agg a = prog->head_agg(h);
+      const int nkey = h->arity - (a != Agg::NONE ? 1 : 0);
+      std::vector<Interval> d(nkey);
+      const bool keep = a == Agg::NONE || a == Agg::MIN || a == Agg::MAX;
+      if (keep && h->nrows > 0)
+        for (int j = 0; j < nkey; ++j) d[j] = Interval{h->lo[j], h->hi[j]};
+      dom[h] = d;
+    }
+    for (int iter = 0; iter < 64; ++iter) {
+      bool changed = false;
+      for (RulePlan& p : s.full) {
+        std::vector<Interval>& d = dom[p.head];
+        for (int j = 0; j < p.nkey; ++j) {
+          const int sl = p.key_slot[j];
+          Interval iv;
+          if (p.var_is_arith[sl]) {
+            iv = Interval::full();
+          } else {
+            iv = Interval::full();
+            for (auto& src : p.var_sources[sl]) {
+              Interval o = col_interval(src.first, src.second, dom);
+              iv.lo = std::max(iv.lo, o.lo);
+              iv.hi = std::min(iv.hi, o.hi);
+            }
+          }
+          if (iv.empty()) continue;
+          Interval before = d[j];
+          d[j].join(iv);
+          changed = changed || before.lo != d[j].lo || before.hi != d[j].hi;
+        }
+      }
+      if (!changed) break;
+    }
+    for (Relation* h : s.heads) {
+      auto hr = std::make_unique<HeadRun>();
+      hr->rel = h;
+      hr->agg = prog->head_agg(h);
+      hr->nkey = h->arity - (hr->agg != Agg::NONE ? 1 : 0);
+      hr->is_set = hr->agg == Agg::NONE;
+      hr->is_minmax = hr->agg == Agg::MIN || hr->agg == Agg::MAX;
+      hr->is_sortagg = !hr->is_set && !hr->is_minmax;
+      switch (hr->agg) {
+        case Agg::COUNT: hr->fold = k::FOLD_COUNT; break;
+        case Agg::SUM: hr->fold = k::FOLD_SUM; break;
+        case Agg::MIN: hr->fold = k::FOLD_MIN; break;
+        case Agg::MAX: hr->fold = k::FOLD_MAX; break;
+        case Agg::LSE: hr->fold = k::FOLD_LSE; break;
+        default: hr->fold = k::FOLD_NONE;
+      }
+      std::vector<Interval>& d = dom[h];
+      KeyPack kp{};
+      kp.nkey = hr->nkey;
+      int bits0 = 1;
+      double dsize = 1;
+      for (int j = 0; j < hr->nkey; ++j) {
+        Interval iv = d[j].empty() ? Interval{0, 0} : d[j];
+        kp.lo[j] = (int32_t)iv.lo;
+        const int b = std::max(1, bitlen((uint64_t)(iv.hi - iv.lo)));
+        if (j == 0) bits0 = b; else kp.shift = b;
+        dsize *= (double)(iv.hi - iv.lo + 1);
+      }
+      if (hr->nkey == 2 && bits0 + kp.shift > 63)
+        return c->fail(XL_UNSUPPORTED, "key domain of " + h->name + " is wider than 63 bits");
+      hr->kp = kp;
+      hr->bits0 = bits0;
+      hr->domain = dsize;
+      hr->preloaded = (hr->is_set || hr->is_minmax) ? h->nrows : 0;
+      XL_TRY(init_head(hr.get()));
+      heads.push_back(std::move(hr));
+    }
+    return XL_OK;
+  }
+
+  size_t slot_bytes(const HeadRun* h) const { return h->is_set ? 8 : sizeof(Slot16); }
+
+  xl_status alloc_table(HeadRun* h, int64_t cap, Buf* out) {
+    XL_TRY(dalloc(c, (size_t)cap * slot_bytes(h), out, "hash table"));
+    HIP_TRY(c, hipMemsetAsync(out->p, 0xff, (size_t)cap * slot_bytes(h), c->stream));
+    return XL_OK;
+  }
+
+  int64_t initial_cap(int64_t expect) {
+    int64_t cap = (int64_t)1 << c->hash_min_log2;
+    return (int64_t)std::max<uint64_t>(cap, next_pow2((uint64_t)std::max<int64_t>(expect, 1) * 4));
+  }
+
+  xl_status init_head(HeadRun* h) {
+    Relation* r = h->rel;
+    h->cap = initial_cap(h->preloaded);
+    XL_TRY(alloc_table(h, h->cap, &h->table));
+    if (h->is_set) {
+      h->rows_cap = h->cap;
+      for (int j = 0; j < h->nkey; ++j) {
+        XL_TRY(dalloc(c, (size_t)h->rows_cap * 4, &h->rows[j], "relation rows"));
+        if (h->preloaded)
+          HIP_TRY(c, hipMemcpyAsync(h->rows[j].p, r->col[j], (size_t)h->preloaded * 4,
+                                    hipMemcpyDeviceToDevice, c->stream));
+      }
+      if (h->preloaded)
+        HIP_TRY(c, k::set_insert_rows(h->table.as<u64>(), (u64)h->cap - 1, h->rows[0].as<uint32_t>(),
+                                      h->nkey == 2 ? h->rows[1].as<uint32_t>() : nullptr, h->preloaded,
+                                      h->kp, c->dcounters, c->stream));
+      h->nrows = h->keys = h->preloaded;
+      h->dbeg = h->dend = 0;
+    } else {
+      if (h->is_minmax) {
+        XL_TRY(dalloc(c, (size_t)h->cap * 4, &h->didx, "delta slot list"));
+        h->keys = 0;
+        if (h->preloaded) {  // several loaded rows may share a key: count distinct keys
+          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+          HIP_TRY(c, k::table16_insert_rows(h->table.as<Slot16>(), (u64)h->cap - 1, r->col[0],
+                                            h->nkey == 2 ? r->col[1] : nullptr, r->col[h->nkey],
+                                            h->preloaded, h->kp, r->types[h->nkey],
+                                            h->agg == Agg::MAX, c->dcounters, c->stream));
+          u64 cnt[CNT_N];
+          XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+          if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "hash table probe exhausted (internal)");
+          h->keys = (int64_t)cnt[CNT_INSERTED];
+        }
+      }
+    }
+    return XL_OK;
+  }
+
+  // Grow the head's table (and row list) so it holds at least `need` keys.
+  xl_status grow(HeadRun* h, int64_t need) {
+    int64_t ncap = h->cap * 4;
+    while (ncap / 2 < need || ncap - need < 64 * 4 * EMIT_GRID + 1024) ncap *= 2;
+    Buf nt;
+    XL_TRY(alloc_table(h, ncap, &nt));
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (h->is_set) {
+      Buf nr[2];
+      for (int j = 0; j < h->nkey; ++j) {
+        XL_TRY(dalloc(c, (size_t)ncap * 4, &nr[j], "relation rows"));
+        HIP_TRY(c, hipMemcpyAsync(nr[j].p, h->rows[j].p, (size_t)h->nrows * 4, hipMemcpyDeviceToDevice,
+                                  c->stream));
+      }
+      HIP_TRY(c, k::set_insert_rows(nt.as<u64>(), (u64)ncap - 1, nr[0].as<uint32_t>(),
+                                    h->nkey == 2 ? nr[1].as<uint32_t>() : nullptr, h->nrows, h->kp,
+                                    c->dcounters, c->stream));
+      for (int j = 0; j < h->nkey; ++j) std::swap(h->rows[j].p, nr[j].p);
+      h->rows_cap = ncap;
+    } else {
+      HIP_TRY(c, k::table16_rehash(h->table.as<Slot16>(), h->cap, nt.as<Slot16>(), (u64)ncap - 1,
+                                   c->dcounters, c->stream));
+      if (h->is_minmax) {
+        Buf nd;
+        XL_TRY(dalloc(c, (size_t)ncap * 4, &nd, "delta slot list"));
+        std::swap(h->didx.p, nd.p);
+      }
+    }
+    std::swap(h->table.p, nt.p);
+    h->cap = ncap;
+    st->table_grows++;
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "hash table rebuild failed");
+    return XL_OK;
+  }
+
+  // ------------------------------------------------------------ rule evaluation
+  struct Source {
+    const uint32_t* col[MAXV];
+    int64_t n;
+  };
+
+  Source resolve_driver(const RulePlan& p) {
+    Source s{};
+    HeadRun* h = head_of(p.driver);
+    if (h && p.driver_delta) {
+      if (h->is_set) {
+        for (int j = 0; j < h->nkey; ++j) s.col[j] = h->rows[j].as<uint32_t>() + h->dbeg;
+        s.n = h->dend - h->dbeg;
+      } else {
+        for (int j = 0; j < p.driver->arity; ++j) s.col[j] = h->drow[j].as<uint32_t>();
+        s.n = h->dn;
+      }
+    } else if (h && h->is_set) {  // full scan of a head of this stratum (seed)
+      for (int j = 0; j < h->nkey; ++j) s.col[j] = h->rows[j].as<uint32_t>();
+      s.n = h->preloaded;
+    } else {
+      for (int j = 0; j < p.driver->arity; ++j) s.col[j] = p.driver->col[j];
+      s.n = h ? h->preloaded : p.driver->nrows;
+    }
+    return s;
+  }
+
+  void fill_ops(StageArgs& a, const RulePlan& p, int ks) {
+    a.nops = (int)p.stage_ops[ks].size();
+    for (int i = 0; i < a.nops; ++i) a.ops[i] = p.stage_ops[ks][i];
+    for (size_t i = 0; i < p.stage_consts[ks].size(); ++i) a.consts[i] = p.stage_consts[ks][i];
+  }
+
+  xl_status counted_pass(StageArgs& a, int64_t* total, Buf* offs) {
+    const int64_t nchunks = (a.src.n + 63) / 64;
+    Buf cnt, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)nchunks * 8, &cnt, "chunk counts"));
+    XL_TRY(dalloc(c, (size_t)nchunks * 8, offs, "chunk offsets"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(nchunks), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    StageArgs ca = a;
+    ca.emit.mode = EM_COUNT;
+    ca.emit.chunk_cnt = cnt.as<u64>();
+    HIP_TRY(c, k::stage_launch(ca, c->stream, 1 << 16));
+    HIP_TRY(c, k::scan_exclusive_u64(cnt.as<u64>(), offs->as<u64>(), nchunks, tot.as<u64>(), tmp.p,
+                                     c->stream));
+    u64 t = 0;
+    XL_TRY(ctl_read(c, tot.p, 8, &t));
+    *total = (int64_t)t;
+    return XL_OK;
+  }
+
+  xl_status eval_plan(const RulePlan& p) {
+    HeadRun* h = head_of(p.head);
+    const int nst = (int)p.steps.size();
+    const int nkst = nst > 0 ? nst : 1;
+    Source src = resolve_driver(p);
+    if (src.n == 0) return XL_OK;
+    // materialized bindings between stages
+    std::vector<std::unique_ptr<Buf>> live_bufs;
+    RowSource rs{};
+    rs.n = src.n;
+    rs.ncols = p.driver->arity;
+    for (int j = 0; j < rs.ncols; ++j) {
+      rs.col[j] = src.col[j];
+      rs.act[j] = p.driver_act[j];
+    }
+    for (int ks = 0; ks < nkst; ++ks) {
+      StageArgs a{};
+      a.src = rs;
+      a.has_index = nst > 0;
+      if (nst > 0) {
+        const StepPlan& sp = p.steps[ks];
+        XL_TRY(get_index(sp.rel, sp.key_col, &a.idx));
+        a.idx.key_slot = (int8_t)sp.key_slot;
+        for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
+      }
+      fill_ops(a, p, ks);
+      a.emit.counters = c->dcounters;
+      if (ks + 1 < nkst) {
+        // intermediate: count -> scan -> materialize the live slots
+        const std::vector<int>& live = p.live_after[ks];
+        a.emit.mode = EM_MAT;
+        a.emit.nout = (int)live.size();
+        int64_t total = 0;
+        Buf offs;
+        XL_TRY(counted_pass(a, &total, &offs));
+        RowSource next{};
+        next.n = total;
+        next.ncols = (int)live.size();
+        for (size_t q = 0; q < live.size(); ++q) {
+          live_bufs.push_back(std::make_unique<Buf>());
+          XL_TRY(dalloc(c, (size_t)std::max<int64_t>(total, 1) * 4, live_bufs.back().get(), "join bindings"));
+          a.emit.out_slot[q] = (int8_t)live[q];
+          a.emit.out_col[q] = live_bufs.back()->as<uint32_t>();
+          next.col[q] = a.emit.out_col[q];
+          next.act[q].kind = CA_BIND;
+          next.act[q].slot = (int8_t)live[q];
+        }
+        a.emit.chunk_off = offs.as<u64>();
+        a.emit.mat_base = 0;
+        if (total > 0) HIP_TRY(c, k::stage_launch(a, c->stream, 1 << 16));
+        rs = next;
+        if (total == 0) return XL_OK;
+        continue;
+      }
+      // final stage: emit into the head
+      a.emit.key.nkey = p.nkey;
+      a.emit.key.slot[0] = (int8_t)p.key_slot[0];
+      a.emit.key.slot[1] = (int8_t)(p.nkey == 2 ? p.key_slot[1] : p.key_slot[0]);
+      a.emit.key.lo[0] = h->kp.lo[0];
+      a.emit.key.lo[1] = h->kp.lo[1];
+      a.emit.key.shift = h->kp.shift;
+      a.emit.val_slot = (int8_t)p.val_slot;
+      a.emit.val_type = p.val_type;
+      if (h->is_sortagg) {
+        a.emit.mode = EM_MAT;
+        a.emit.mat_packed = 1;
+        int64_t total = 0;
+        Buf offs;
+        XL_TRY(counted_pass(a, &total, &offs));
+        cands += total;
+        if (total == 0) return XL_OK;
+        if (h->cn + total > h->ccap) {
+          const int64_t ncap = std::max<int64_t>(h->cn + total, h->ccap * 2);
+          Buf nk, nv;
+          XL_TRY(dalloc(c, (size_t)ncap * 8, &nk, "aggregate candidates"));
+          XL_TRY(dalloc(c, (size_t)ncap * 4, &nv, "aggregate candidates"));
+          if (h->cn) {
+            HIP_TRY(c, hipMemcpyAsync(nk.p, h->ckey.p, (size_t)h->cn * 8, hipMemcpyDeviceToDevice, c->stream));
+            HIP_TRY(c, hipMemcpyAsync(nv.p, h->cval.p, (size_t)h->cn * 4, hipMemcpyDeviceToDevice, c->stream));
+          }
+          std::swap(h->ckey.p, nk.p);
+          std::swap(h->cval.p, nv.p);
+          h->ckey.c = h->cval.c = c;
+          h->ccap = ncap;
+        }
+        a.emit.out_key = h->ckey.as<u64>();
+        a.emit.out_val = h->cval.as<uint32_t>();
+        a.emit.chunk_off = offs.as<u64>();
+        a.emit.mat_base = h->cn;
+        HIP_TRY(c, k::stage_launch(a, c->stream, 1 << 16));
+        h->cn += total;
+        return XL_OK;
+      }
+      // set / min / max: single pass with insert-or-improve, retried after growth
+      for (int attempt = 0;; ++attempt) {
+        if (attempt > 8) return c->fail(XL_DEVICE_ERROR, "hash table growth did not converge");
+        if (nst == 0 || ks == 0) {  // the driver may live in this head's row list
+          Source s2 = resolve_driver(p);
+          for (int j = 0; j < a.src.ncols && ks == 0; ++j) a.src.col[j] = s2.col[j];
+        }
+        // Every wavefront may insert one more batch of 64 keys after the load
+        // limit is crossed, so the limit leaves room for all of them: the
+        // table can never fill and the row list never overflows.
+        const int64_t waves = std::min<int64_t>((a.src.n + 63) / 64, (int64_t)EMIT_GRID * 4);
+        const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - 64 * waves - 1024);
+        if (h->keys >= max_keys) {
+          XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + 64 * waves + 1024)));
+          continue;
+        }
+        HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+        a.emit.limit = (u64)(max_keys - h->keys);
+        a.emit.mask = (u64)h->cap - 1;
+        if (h->is_set) {
+          a.emit.mode = EM_SET;
+          a.emit.table = h->table.as<u64>();
+          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
+          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
+          a.emit.row_base = h->nrows;
+          a.emit.row_cap = h->rows_cap;
+        } else {
+          a.emit.mode = EM_MINMAX;
+          a.emit.table16 = h->table.as<Slot16>();
+          a.emit.is_max = h->agg == Agg::MAX;
+          a.emit.round = h->round;
+          a.emit.delta_idx = h->didx.as<uint32_t>() + h->didx_n;
+        }
+        if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+        HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
+        if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+        u64 cnt[CNT_N];
+        XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+        if (c->profile) {
+          float ms = 0;
+          HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+          st->emit_ms += ms;
+          st->emit_launches++;
+          st->emit_source_rows += a.src.n;
+          st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+          st->emit_new += (int64_t)(h->is_set ? cnt[CNT_APPENDED] : cnt[CNT_INSERTED] + cnt[CNT_APPENDED]);
+        }
+        if (cnt[CNT_FATAL])
+          return c->fail(XL_DEVICE_ERROR, "hash table probe exhausted or row list overflow (internal)");
+        cands += (int64_t)cnt[CNT_CANDIDATES];
+        if (h->is_set) {
+          h->nrows += (int64_t)cnt[CNT_APPENDED];
+          h->keys += (int64_t)cnt[CNT_APPENDED];
+        } else {
+          h->keys += (int64_t)cnt[CNT_INSERTED];
+          h->didx_n += (int64_t)cnt[CNT_APPENDED];
+        }
+        if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+          return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                                   std::to_string(h->rel->max_rows));
+        if (!cnt[CNT_OVERFLOW]) break;
+        XL_TRY(grow(h, h->keys * 2 + 1));
+        if (h->is_minmax) {  // slot indices moved: rebuild this round's delta list
+          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+          HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(),
+                                        c->dcounters, c->stream));
+          u64 n2 = 0;
+          XL_TRY(ctl_read(c, c->dcounters, 8, &n2));
+          h->didx_n = (int64_t)n2;
+        }
+      }
+    }
+    return XL_OK;
+  }
+
+  xl_status ensure_drow(HeadRun* h, int64_t n) {
+    if (n <= h->dcap) return XL_OK;
+    const int64_t ncap = std::max<int64_t>(n, h->dcap * 2);
+    for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)ncap * 4, &h->drow[j], "delta rows"));
+    h->dcap = ncap;
+    return XL_OK;
+  }
+
+  void begin_round(HeadRun* h) {
+    h->round++;
+    h->round_begin = h->nrows;
+    h->didx_n = 0;
+    h->cn = 0;
+  }
+
+  xl_status finish_round(HeadRun* h, int64_t* delta) {
+    if (h->is_set) {
+      h->dbeg = h->round_begin;
+      h->dend = h->nrows;
+      *delta = h->dend - h->dbeg;
+      return XL_OK;
+    }
+    if (h->is_minmax) {
+      XL_TRY(ensure_drow(h, h->didx_n));
+      HIP_TRY(c, k::table16_rows_from_idx(h->table.as<Slot16>(), h->didx.as<uint32_t>(), h->didx_n,
+                                          h->kp, h->rel->types[h->nkey], h->fold, h->drow[0].as<uint32_t>(),
+                                          h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
+                                          h->drow[h->nkey].as<uint32_t>(), c->stream));
+      h->dn = h->didx_n;
+      *delta = h->dn;
+      return XL_OK;
+    }
+    // sorted aggregation of this round's candidates
+    const int64_t n = h->cn;
+    if (n == 0) {
+      h->dn = 0;
+      *delta = 0;
+      return XL_OK;
+    }
+    const int kbits = h->nkey == 2 ? h->bits0 + h->kp.shift : h->bits0;
+    Buf k2, v2, tmp, flag, pos, tot;
+    XL_TRY(dalloc(c, (size_t)n * 8, &k2, "sort keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &v2, "sort values"));
+    XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
+    int alt = 0;
+    HIP_TRY(c, k::radix_sort_u64(h->ckey.as<u64>(), h->cval.as<uint32_t>(), k2.as<u64>(), v2.as<uint32_t>(),
+                                 n, kbits, tmp.p, c->stream, &alt));
+    u64* sk = alt ? k2.as<u64>() : h->ckey.as<u64>();
+    uint32_t* sv = alt ? v2.as<uint32_t>() : h->cval.as<uint32_t>();
+    XL_TRY(dalloc(c, (size_t)n * 4, &flag, "segment flags"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &pos, "segment ids"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    tmp.reset();
+    XL_TRY(dalloc(c, k::scan_temp_bytes(n), &tmp, "scan scratch"));
+    HIP_TRY(c, k::seg_heads(sk, n, flag.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), n, tot.as<uint32_t>(), tmp.p,
+                                     c->stream));
+    uint32_t nseg = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &nseg));
+    Buf starts;
+    XL_TRY(dalloc(c, (size_t)nseg * 4, &starts, "segment starts"));
+    HIP_TRY(c, k::seg_starts(flag.as<uint32_t>(), pos.as<uint32_t>(), n, starts.as<uint32_t>(), c->stream));
+    XL_TRY(ensure_drow(h, nseg));
+    HIP_TRY(c, k::seg_reduce(sk, sv, starts.as<uint32_t>(), nseg, n, h->kp, h->rel->types[h->nkey], h->fold,
+                             h->drow[0].as<uint32_t>(), h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
+                             h->drow[h->nkey].as<uint32_t>(), c->stream));
+    if (h->keys + (int64_t)nseg > h->cap / 2) XL_TRY(grow(h, h->keys + nseg));
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    HIP_TRY(c, k::agg_merge(h->table.as<Slot16>(), (u64)h->cap - 1, h->drow[0].as<uint32_t>(),
+                            h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr, h->drow[h->nkey].as<uint32_t>(),
+                            nseg, h->kp, h->rel->types[h->nkey], h->fold, c->dcounters, c->stream));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "hash table probe exhausted (internal)");
+    h->keys += (int64_t)cnt[CNT_INSERTED];
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows");
+    h->dn = nseg;
+    h->cn = 0;
+    *delta = nseg;
+    return XL_OK;
+  }
+
+  xl_status materialize(HeadRun* h) {
+    Relation* r = h->rel;
+    if (h->is_set) {
+      relation_free_storage(r);
+      for (int j = 0; j < h->nkey; ++j) r->col[j] = (uint32_t*)h->rows[j].keep();
+      r->nrows = h->nrows;
+    } else {
+      Buf out[3];
+      const int64_t n = h->keys;
+      for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      HIP_TRY(c, k::table16_compact(h->table.as<Slot16>(), h->cap, h->kp, r->types[h->nkey], h->fold,
+                                    out[0].as<uint32_t>(), h->nkey == 2 ? out[1].as<uint32_t>() : nullptr,
+                                    out[h->nkey].as<uint32_t>(), std::max<int64_t>(n, 1), c->dcounters,
+                                    c->stream));
+      u64 m = 0;
+      XL_TRY(ctl_read(c, c->dcounters, 8, &m));
+      if ((int64_t)m != n) return c->fail(XL_DEVICE_ERROR, "table compaction count mismatch (internal)");
+      relation_free_storage(r);
+      for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
+      r->nrows = n;
+    }
+    return compute_bounds(c, r);
+  }
+
+  // ------------------------------------------------------------ strata
+  xl_status run_stratum(Stratum& s, int64_t max_iterations) {
+    heads.clear();
+    XL_TRY(setup_heads(s));
+    for (auto& h : heads) begin_round(h.get());
+    for (RulePlan& p : s.full) XL_TRY(eval_plan(p));
+    int64_t total = 0;
+    for (auto& h : heads) {
+      int64_t d = 0;
+      XL_TRY(finish_round(h.get(), &d));
+      total += d;
+      st->new_tuples_total += d;
+    }
+    record(total);
+    if (s.recursive) {
+      int64_t pass = 0;
+      while (total > 0) {
+        if (pass >= max_iterations)
+          return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                     " reached before the fixpoint");
+        ++pass;
+        st->iterations++;
+        for (auto& h : heads) begin_round(h.get());
+        for (RulePlan& p : s.variants) XL_TRY(eval_plan(p));
+        total = 0;
+        for (auto& h : heads) {
+          int64_t d = 0;
+          XL_TRY(finish_round(h.get(), &d));
+          total += d;
+          st->new_tuples_total += d;
+        }
+        record(total);
+      }
+    }
+    for (auto& h : heads) XL_TRY(materialize(h.get()));
+    heads.clear();
+    indexes.clear();
+    return XL_OK;
+  }
+};
+
+}  // namespace
+
+xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st) {
+  Context* c = p->ctx;
+  memset(st, 0, sizeof(*st));
+  if (c->device < 0) return c->fail(XL_INVALID_ARGUMENT, "planning-only context cannot run programs");
+  if (max_iterations < 0) return c->fail(XL_INVALID_ARGUMENT, "negative iteration cap");
+  c->arena.reset_peak();
+  const int64_t ctl0 = c->control_bytes;
+  hipEvent_t e0, e1;
+  HIP_TRY(c, hipEventCreate(&e0));
+  HIP_TRY(c, hipEventCreate(&e1));
+  HIP_TRY(c, hipEventRecord(e0, c->stream));
+  xl_status s = XL_OK;
+  {
+    Runner run{c, p, st};
+    if (c->profile) {
+      HIP_TRY(c, hipEventCreate(&run.ev[0]));
+      HIP_TRY(c, hipEventCreate(&run.ev[1]));
+    }
+    for (Stratum& str : p->strata) {
+      s = run.run_stratum(str, max_iterations);
+      if (s != XL_OK) break;
+    }
+    st->candidates_total = run.cands;
+  }
+  (void)hipEventRecord(e1, c->stream);
+  (void)hipEventSynchronize(e1);
+  float ms = 0;
+  (void)hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  st->ms_total = ms;
+  st->strata = (int32_t)p->strata.size();
+  for (auto& h : p->heads) st->derived_tuples += h.rel->nrows;
+  st->peak_workspace_bytes = (int64_t)c->arena.peak();
+  st->control_bytes_read = c->control_bytes - ctl0;
+  st->status = s;
+  return s;
+}
+
+}  // namespace xlh

@@ -1,0 +1,181 @@
+// Internal host-side structures of the fixpoint engine: workspace arena,
+// context, relations, compiled programs and their per-rule join plans.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/xlh.h"
+#include "device_types.h"
+
+namespace xlh {
+
+// ------------------------------------------------------------------ arena
+// First-fit allocator over the caller's workspace.  Blocks are 256-byte
+// aligned; freed neighbours coalesce.  Host-side bookkeeping only.
+class Arena {
+ public:
+  void init(char* base, size_t size);
+  void* alloc(size_t bytes);  // nullptr when no free block is large enough
+  void release(void* p);
+  size_t in_use() const { return in_use_; }
+  size_t peak() const { return peak_; }
+  void reset_peak() { peak_ = in_use_; }
+  size_t capacity() const { return size_; }
+  size_t largest_free() const;
+
+ private:
+  char* base_ = nullptr;
+  size_t size_ = 0;
+  std::map<size_t, size_t> free_;  // offset -> size
+  std::map<size_t, size_t> used_;  // offset -> size
+  size_t in_use_ = 0, peak_ = 0;
+};
+
+struct Program;
+
+struct Relation {
+  struct Context* ctx = nullptr;
+  std::string name;
+  int arity = 0;
+  uint8_t types[MAXC] = {};
+  int64_t max_rows = 0;
+  uint32_t* col[MAXC] = {};  // device columns (arena), nrows valid rows
+  int64_t nrows = 0;
+  int32_t lo[MAXC] = {}, hi[MAXC] = {};  // bounds of i32 columns when nrows > 0
+};
+
+struct Context {
+  int device = -1;
+  hipStream_t stream = nullptr;
+  Arena arena;
+  std::string err;
+  void* pinned = nullptr;                  // host control block
+  unsigned long long* dcounters = nullptr; // device counters (arena)
+  std::vector<Relation*> rels;
+  std::vector<Program*> progs;
+  int hash_min_log2 = 22;
+  int index_mode = 0;
+  int profile = 0;
+  int64_t control_bytes = 0;
+
+  xl_status fail(xl_status st, const std::string& msg) {
+    err = msg;
+    return st;
+  }
+  Relation* find(const std::string& name) const {
+    for (Relation* r : rels)
+      if (r->name == name) return r;
+    return nullptr;
+  }
+};
+
+// ------------------------------------------------------------------ AST
+enum class Agg { NONE, COUNT, SUM, MIN, MAX, LSE };
+
+struct Term {
+  enum Kind { VAR, ANON, INT, FLOAT } kind = ANON;
+  std::string name;
+  int64_t ival = 0;
+  double fval = 0.0;
+};
+
+struct AtomAst {
+  std::string pred;
+  std::vector<Term> args;
+};
+
+struct RuleAst {
+  std::string head;
+  std::vector<Term> head_args;  // key arguments (aggregate excluded)
+  Agg agg = Agg::NONE;
+  std::string agg_var;
+  std::vector<AtomAst> atoms;
+  struct Assign {
+    std::string var;
+    std::vector<std::pair<int, Term>> parts;  // (+1 / -1, term)
+  };
+  std::vector<Assign> assigns;
+  struct Cmp {
+    int op;
+    Term lhs, rhs;
+  };
+  std::vector<Cmp> cmps;
+  std::string text;
+};
+
+// ------------------------------------------------------------------ plans
+struct StepPlan {        // index join against a full relation
+  Relation* rel = nullptr;
+  int key_col = 0;
+  int key_slot = 0;
+  ColAct act[MAXC] = {};
+};
+
+struct RulePlan {
+  int rule = 0;
+  Relation* head = nullptr;
+  Relation* driver = nullptr;   // relation scanned first
+  bool driver_delta = false;    // scan the driver's delta instead of all rows
+  ColAct driver_act[MAXC] = {};
+  std::vector<StepPlan> steps;
+  // micro-ops executed by kernel stage k (k = max(0, #steps - 1) when no steps)
+  std::vector<std::vector<MicroOp>> stage_ops;
+  std::vector<std::vector<uint32_t>> stage_consts;
+  std::vector<std::vector<int>> live_after;  // slots materialized after stage k
+  int nkey = 0;
+  int key_slot[2] = {0, 0};
+  int val_slot = -1;
+  uint8_t val_type = T_I32;
+  // column -> (var slot or -1 for an is-result) binding source, for domains
+  std::vector<std::pair<Relation*, int>> var_sources[MAXV];
+  bool var_is_arith[MAXV] = {};
+};
+
+struct HeadInfo {
+  Relation* rel = nullptr;
+  Agg agg = Agg::NONE;
+};
+
+struct Stratum {
+  std::vector<Relation*> heads;
+  bool recursive = false;
+  std::vector<RulePlan> full;      // every rule, all atoms over full relations
+  std::vector<RulePlan> variants;  // recursive strata: one per recursive atom
+};
+
+struct Program {
+  Context* ctx = nullptr;
+  std::vector<RuleAst> rules;
+  std::vector<HeadInfo> heads;
+  std::vector<Stratum> strata;
+  Agg head_agg(const Relation* r) const {
+    for (const HeadInfo& h : heads)
+      if (h.rel == r) return h.agg;
+    return Agg::NONE;
+  }
+  bool is_head(const Relation* r) const {
+    for (const HeadInfo& h : heads)
+      if (h.rel == r) return true;
+    return false;
+  }
+};
+
+// frontend.cpp
+xl_status compile_program(Context* ctx, const char* text, Program** out);
+std::string explain_program(const Program* p);
+
+// engine.cpp
+xl_status relation_load(Relation* r, const void* const* cols, int64_t n, int on_device);
+xl_status relation_read(const Relation* r, void* const* cols, int64_t cap, int64_t* out_rows,
+                        int on_device);
+xl_status relation_clear(Relation* r);
+xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st);
+void relation_free_storage(Relation* r);
+
+const char* agg_name(Agg a);
+
+}  // namespace xlh

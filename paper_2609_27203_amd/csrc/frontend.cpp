@@ -1,0 +1,656 @@
+// Rule text -> typed rules -> strata -> per-rule join plans.  Host-only.
+//
+// Accepted subset of the paper's surface syntax (Sec. 3.1, 3.3, 3.5):
+//   rule    := head ':-' literal (',' literal)* '.'
+//   head    := name '(' Var (',' Var)* [',' agg '(' Var ')'] ')'
+//   literal := name '(' term (',' term)* ')'
+//            | Var 'is' term (('+' | '-') term)*
+//            | term cmp term            cmp in != == < <= > >=
+//   term    := Var | '_' | integer | float
+// Variables start with an upper-case letter or '_'; '//' starts a comment.
+#include <algorithm>
+#include <cctype>
+#include <cstring>
+#include <functional>
+#include <set>
+#include <sstream>
+
+#include "engine.h"
+
+namespace xlh {
+
+const char* agg_name(Agg a) {
+  switch (a) {
+    case Agg::COUNT: return "count";
+    case Agg::SUM: return "sum";
+    case Agg::MIN: return "min";
+    case Agg::MAX: return "max";
+    case Agg::LSE: return "logsumexp";
+    default: return "set";
+  }
+}
+
+namespace {
+
+struct Tok {
+  enum Kind { NAME, NUM, OP, END } kind;
+  std::string s;
+  int line;
+};
+
+struct Lexer {
+  std::vector<Tok> toks;
+  std::string err;
+  bool run(const char* text) {
+    int line = 1;
+    const char* p = text;
+    while (*p) {
+      if (*p == '\n') { ++line; ++p; continue; }
+      if (isspace((unsigned char)*p)) { ++p; continue; }
+      if (p[0] == '/' && p[1] == '/') { while (*p && *p != '\n') ++p; continue; }
+      if (isalpha((unsigned char)*p) || *p == '_') {
+        const char* b = p;
+        while (isalnum((unsigned char)*p) || *p == '_') ++p;
+        toks.push_back({Tok::NAME, std::string(b, p), line});
+        continue;
+      }
+      if (isdigit((unsigned char)*p)) {
+        const char* b = p;
+        while (isdigit((unsigned char)*p)) ++p;
+        if (*p == '.' && isdigit((unsigned char)p[1])) {
+          ++p;
+          while (isdigit((unsigned char)*p)) ++p;
+        }
+        if (*p == 'e' || *p == 'E') {
+          const char* q = p + 1;
+          if (*q == '+' || *q == '-') ++q;
+          if (isdigit((unsigned char)*q)) {
+            p = q;
+            while (isdigit((unsigned char)*p)) ++p;
+          }
+        }
+        toks.push_back({Tok::NUM, std::string(b, p), line});
+        continue;
+      }
+      static const char* ops2[] = {":-", "!=", "==", "<=", ">="};
+      bool two = false;
+      for (const char* o : ops2)
+        if (p[0] == o[0] && p[1] == o[1]) {
+          toks.push_back({Tok::OP, std::string(o), line});
+          p += 2;
+          two = true;
+          break;
+        }
+      if (two) continue;
+      if (strchr("(),.+-<>", *p)) {
+        toks.push_back({Tok::OP, std::string(1, *p), line});
+        ++p;
+        continue;
+      }
+      err = "line " + std::to_string(line) + ": unexpected character '" + std::string(1, *p) + "'";
+      return false;
+    }
+    toks.push_back({Tok::END, "", line});
+    return true;
+  }
+};
+
+bool is_var_name(const std::string& s) { return !s.empty() && (isupper((unsigned char)s[0]) || s[0] == '_'); }
+
+struct Parser {
+  std::vector<Tok>& t;
+  size_t i = 0;
+  std::string err;
+  explicit Parser(std::vector<Tok>& tt) : t(tt) {}
+
+  bool fail(const std::string& m) {
+    if (err.empty()) err = "line " + std::to_string(t[i].line) + ": " + m;
+    return false;
+  }
+  bool expect(const char* s) {
+    if (t[i].s == s && t[i].kind != Tok::END) { ++i; return true; }
+    return fail(std::string("expected '") + s + "' but found '" + t[i].s + "'");
+  }
+  bool term(Term* out) {
+    bool neg = false;
+    if (t[i].kind == Tok::OP && t[i].s == "-" && t[i + 1].kind == Tok::NUM) { neg = true; ++i; }
+    const Tok& k = t[i];
+    if (k.kind == Tok::NUM) {
+      ++i;
+      if (k.s.find_first_of(".eE") != std::string::npos) {
+        out->kind = Term::FLOAT;
+        out->fval = strtod(k.s.c_str(), nullptr) * (neg ? -1.0 : 1.0);
+      } else {
+        out->kind = Term::INT;
+        out->ival = strtoll(k.s.c_str(), nullptr, 10) * (neg ? -1 : 1);
+        if (out->ival < INT32_MIN || out->ival > INT32_MAX) return fail("integer constant out of int32 range");
+      }
+      return true;
+    }
+    if (k.kind == Tok::NAME) {
+      ++i;
+      if (k.s == "_") { out->kind = Term::ANON; return true; }
+      if (is_var_name(k.s)) { out->kind = Term::VAR; out->name = k.s; return true; }
+      return fail("expected a variable or constant, found '" + k.s + "'");
+    }
+    return fail("expected a term, found '" + k.s + "'");
+  }
+  static Agg agg_of(const std::string& s) {
+    if (s == "count") return Agg::COUNT;
+    if (s == "sum") return Agg::SUM;
+    if (s == "min") return Agg::MIN;
+    if (s == "max") return Agg::MAX;
+    if (s == "logsumexp") return Agg::LSE;
+    return Agg::NONE;
+  }
+  bool rule(RuleAst* r) {
+    size_t start = i;
+    if (t[i].kind != Tok::NAME || is_var_name(t[i].s)) return fail("expected a rule head");
+    r->head = t[i++].s;
+    if (!expect("(")) return false;
+    while (true) {
+      Agg a = t[i].kind == Tok::NAME ? agg_of(t[i].s) : Agg::NONE;
+      if (a != Agg::NONE && t[i + 1].s == "(") {
+        if (r->agg != Agg::NONE) return fail("at most one aggregate per head");
+        r->agg = a;
+        i += 2;
+        Term v;
+        if (!term(&v)) return false;
+        if (v.kind != Term::VAR) return fail("an aggregate takes one variable");
+        r->agg_var = v.name;
+        if (!expect(")")) return false;
+      } else {
+        if (r->agg != Agg::NONE) return fail("the aggregate must be the last head argument");
+        Term v;
+        if (!term(&v)) return false;
+        r->head_args.push_back(v);
+      }
+      if (t[i].s == ")") { ++i; break; }
+      if (!expect(",")) return false;
+    }
+    if (t[i].s == ".") return fail("facts are not accepted in rule text; load them as relation rows");
+    if (!expect(":-")) return false;
+    while (true) {
+      if (t[i].kind == Tok::NAME && !is_var_name(t[i].s) && t[i + 1].s == "(") {
+        AtomAst a;
+        a.pred = t[i].s;
+        i += 2;
+        while (true) {
+          Term v;
+          if (!term(&v)) return false;
+          a.args.push_back(v);
+          if (t[i].s == ")") { ++i; break; }
+          if (!expect(",")) return false;
+        }
+        r->atoms.push_back(a);
+      } else if (t[i].kind == Tok::NAME && t[i + 1].kind == Tok::NAME && t[i + 1].s == "is") {
+        if (!is_var_name(t[i].s) || t[i].s == "_") return fail("the left side of 'is' must be a variable");
+        RuleAst::Assign as;
+        as.var = t[i].s;
+        i += 2;
+        Term v;
+        if (!term(&v)) return false;
+        as.parts.push_back({1, v});
+        while (t[i].kind == Tok::OP && (t[i].s == "+" || t[i].s == "-")) {
+          int sign = t[i].s == "+" ? 1 : -1;
+          ++i;
+          if (!term(&v)) return false;
+          as.parts.push_back({sign, v});
+        }
+        r->assigns.push_back(as);
+      } else {
+        RuleAst::Cmp c;
+        if (!term(&c.lhs)) return false;
+        static const char* names[] = {"!=", "==", "<", "<=", ">", ">="};
+        int op = -1;
+        for (int k = 0; k < 6; ++k)
+          if (t[i].s == names[k]) op = k;
+        if (op < 0) return fail("expected a comparison operator, found '" + t[i].s + "'");
+        ++i;
+        c.op = op;
+        if (!term(&c.rhs)) return false;
+        r->cmps.push_back(c);
+      }
+      if (t[i].s == ".") { ++i; break; }
+      if (!expect(",")) return false;
+    }
+    std::ostringstream os;
+    for (size_t k = start; k < i; ++k) os << t[k].s << (k + 1 < i && t[k].kind == Tok::NAME && t[k + 1].kind == Tok::NAME ? " " : "");
+    r->text = os.str();
+    return true;
+  }
+};
+
+// ------------------------------------------------------------------ planning
+struct Planner {
+  Context* ctx;
+  std::string err;
+  xl_status status = XL_OK;
+
+  bool fail(xl_status st, const std::string& m) {
+    if (status == XL_OK) { status = st; err = m; }
+    return false;
+  }
+
+  static uint8_t term_type(const Term& t) { return t.kind == Term::FLOAT ? T_F32 : T_I32; }
+  static uint32_t term_bits(const Term& t) {
+    if (t.kind == Term::FLOAT) {
+      float f = (float)t.fval;
+      uint32_t b;
+      memcpy(&b, &f, 4);
+      return b;
+    }
+    return (uint32_t)(int32_t)t.ival;
+  }
+
+  // Plan one rule with atom `drv` scanned first.
+  bool plan(const RuleAst& r, int rule_id, int drv, bool delta, RulePlan* out) {
+    RulePlan p;
+    p.rule = rule_id;
+    p.head = ctx->find(r.head);
+    std::map<std::string, int> slot;
+    std::map<std::string, uint8_t> vtype;
+    std::map<std::string, int> bstage;  // binding stage (0 = driver, k+1 = step k)
+    std::set<std::string> assigned;
+    for (auto& a : r.assigns) {
+      if (assigned.count(a.var)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + a.var + " is assigned twice");
+      assigned.insert(a.var);
+    }
+    auto new_slot = [&](const std::string& v) -> int {
+      auto it = slot.find(v);
+      if (it != slot.end()) return it->second;
+      int s = (int)slot.size();
+      slot[v] = s;
+      return s;
+    };
+    auto bind_atom = [&](const AtomAst& a, Relation* rel, int stage, int key_col, ColAct* act) -> bool {
+      for (int j = 0; j < rel->arity; ++j) {
+        const Term& t = a.args[j];
+        ColAct c{};
+        c.type = rel->types[j];
+        if (j == key_col) {
+          act[j] = c;
+          continue;
+        }
+        if (t.kind == Term::ANON) {
+          c.kind = CA_NONE;
+        } else if (t.kind == Term::INT || t.kind == Term::FLOAT) {
+          if (term_type(t) != rel->types[j])
+            return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': constant does not match column " + std::to_string(j) + " of " + rel->name);
+          c.kind = CA_CHECK_CONST;
+          c.cval = term_bits(t);
+        } else {
+          if (assigned.count(t.name))
+            return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " is both an 'is' result and an atom argument");
+          auto vt = vtype.find(t.name);
+          if (vt != vtype.end() && vt->second != rel->types[j])
+            return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': variable " + t.name + " is used at two column types");
+          if (bstage.count(t.name)) {
+            c.kind = CA_CHECK_SLOT;
+            c.slot = (int8_t)slot[t.name];
+          } else {
+            c.kind = CA_BIND;
+            c.slot = (int8_t)new_slot(t.name);
+            bstage[t.name] = stage;
+            vtype[t.name] = rel->types[j];
+          }
+          p.var_sources[slot[t.name]].push_back({rel, j});
+        }
+        act[j] = c;
+      }
+      return true;
+    };
+
+    // driver
+    const AtomAst& da = r.atoms[drv];
+    p.driver = ctx->find(da.pred);
+    p.driver_delta = delta;
+    if (!bind_atom(da, p.driver, 0, -1, p.driver_act)) return false;
+    // join order: first remaining atom that shares a bound variable
+    std::vector<int> rest;
+    for (int k = 0; k < (int)r.atoms.size(); ++k)
+      if (k != drv) rest.push_back(k);
+    while (!rest.empty()) {
+      int pick = -1, key_col = -1;
+      for (size_t q = 0; q < rest.size() && pick < 0; ++q) {
+        const AtomAst& a = r.atoms[rest[q]];
+        Relation* rel = ctx->find(a.pred);
+        for (int j = 0; j < rel->arity; ++j) {
+          const Term& t = a.args[j];
+          if (t.kind == Term::VAR && bstage.count(t.name) && rel->types[j] == T_I32) {
+            pick = (int)q;
+            key_col = j;
+            break;
+          }
+        }
+      }
+      if (pick < 0)
+        return fail(XL_UNSUPPORTED, "rule '" + r.text + "': an atom shares no bound int32 variable with the atoms before it (cross products are not supported)");
+      const AtomAst& a = r.atoms[rest[pick]];
+      StepPlan st;
+      st.rel = ctx->find(a.pred);
+      st.key_col = key_col;
+      const std::string& kv = a.args[key_col].name;
+      if (vtype[kv] != T_I32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': join variable " + kv + " has two types");
+      st.key_slot = slot[kv];
+      p.var_sources[st.key_slot].push_back({st.rel, key_col});
+      int stage = (int)p.steps.size() + 1;
+      if (!bind_atom(a, st.rel, stage, key_col, st.act)) return false;
+      p.steps.push_back(st);
+      rest.erase(rest.begin() + pick);
+    }
+    const int nst = (int)p.steps.size();
+    const int nkst = nst > 0 ? nst : 1;  // kernel stages
+    p.stage_ops.assign(nkst, {});
+    p.stage_consts.assign(nkst, {});
+    auto kstage_of = [&](int bind_stage) { return bind_stage > 0 ? bind_stage - 1 : 0; };
+    std::map<std::string, int> avail;  // var -> kernel stage where available
+    for (auto& kv : bstage) avail[kv.first] = kstage_of(kv.second);
+
+    auto operand = [&](int ks, const Term& t, uint8_t* ty, int8_t* enc) -> bool {
+      if (t.kind == Term::VAR) {
+        if (!avail.count(t.name)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " is not bound before it is used");
+        *ty = vtype[t.name];
+        *enc = (int8_t)slot[t.name];
+        return true;
+      }
+      if (t.kind == Term::ANON) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': '_' cannot be used in arithmetic or comparisons");
+      auto& cs = p.stage_consts[ks];
+      if (cs.size() >= (size_t)MAXK) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': too many constants");
+      cs.push_back(term_bits(t));
+      *ty = term_type(t);
+      *enc = (int8_t)(-(int)cs.size());
+      return true;
+    };
+    auto stage_needed = [&](const std::vector<const Term*>& ts) -> int {
+      int s = 0;
+      for (const Term* t : ts)
+        if (t->kind == Term::VAR && avail.count(t->name)) s = std::max(s, avail[t->name]);
+      return s;
+    };
+    for (auto& as : r.assigns) {
+      std::vector<const Term*> ts;
+      for (auto& pt : as.parts) ts.push_back(&pt.second);
+      int ks = stage_needed(ts);
+      int s = new_slot(as.var);
+      uint8_t ty = 0;
+      for (size_t q = 0; q < as.parts.size(); ++q) {
+        uint8_t t1;
+        int8_t e1;
+        if (!operand(ks, as.parts[q].second, &t1, &e1)) return false;
+        if (q == 0) ty = t1;
+        else if (t1 != ty) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': 'is' mixes int32 and float32 operands");
+        MicroOp op{};
+        op.type = t1;
+        op.dst = (int8_t)s;
+        if (q == 0) {
+          if (as.parts[0].first > 0) {
+            op.kind = OP_MOV;
+            op.a = e1;
+          } else {  // 0 - x
+            Term zero;
+            zero.kind = t1 == T_F32 ? Term::FLOAT : Term::INT;
+            uint8_t tz;
+            int8_t ez;
+            if (!operand(ks, zero, &tz, &ez)) return false;
+            op.kind = OP_SUB;
+            op.a = ez;
+            op.b = e1;
+          }
+        } else {
+          op.kind = as.parts[q].first > 0 ? OP_ADD : OP_SUB;
+          op.a = (int8_t)s;
+          op.b = e1;
+        }
+        p.stage_ops[ks].push_back(op);
+      }
+      vtype[as.var] = ty;
+      avail[as.var] = ks;
+      p.var_is_arith[s] = true;
+    }
+    for (auto& c : r.cmps) {
+      int ks = stage_needed({&c.lhs, &c.rhs});
+      MicroOp op{};
+      op.kind = OP_CMP;
+      op.cmp = (uint8_t)c.op;
+      uint8_t t1, t2;
+      if (!operand(ks, c.lhs, &t1, &op.a) || !operand(ks, c.rhs, &t2, &op.b)) return false;
+      if (t1 != t2) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': comparison between int32 and float32");
+      op.type = t1;
+      p.stage_ops[ks].push_back(op);
+    }
+    if ((int)slot.size() > MAXV) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': more than 8 variables");
+    for (int k = 0; k < nkst; ++k)
+      if (p.stage_ops[k].size() > (size_t)MAXOPS) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': too many comparisons/arithmetic terms");
+
+    // head
+    Relation* h = p.head;
+    const int nkey = (int)r.head_args.size();
+    p.nkey = nkey;
+    for (int j = 0; j < nkey; ++j) {
+      const Term& t = r.head_args[j];
+      if (t.kind != Term::VAR) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': head arguments must be variables");
+      if (!avail.count(t.name)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': head variable " + t.name + " does not occur in the body");
+      if (vtype[t.name] != h->types[j]) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': head argument " + t.name + " does not match column " + std::to_string(j) + " of " + h->name);
+      p.key_slot[j] = slot[t.name];
+    }
+    if (r.agg != Agg::NONE) {
+      if (!avail.count(r.agg_var)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': aggregated variable " + r.agg_var + " does not occur in the body");
+      const uint8_t vt = h->types[nkey];
+      if (r.agg == Agg::COUNT) {
+        if (vt != T_I32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': count produces an int32 column");
+        p.val_slot = -1;
+      } else {
+        if (vtype[r.agg_var] != vt) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': aggregated variable does not match the head's value column");
+        if (r.agg == Agg::LSE && vt != T_F32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': logsumexp needs a float32 column");
+        p.val_slot = slot[r.agg_var];
+      }
+      p.val_type = vt;
+    }
+    // live slots between kernel stages
+    p.live_after.assign(nkst, {});
+    for (int k = 0; k + 1 < nkst; ++k) {
+      std::set<int> used;
+      for (int q = k + 1; q < nst; ++q) {
+        used.insert(p.steps[q].key_slot);
+        for (int j = 0; j < p.steps[q].rel->arity; ++j)
+          if (p.steps[q].act[j].kind == CA_CHECK_SLOT) used.insert(p.steps[q].act[j].slot);
+      }
+      for (int q = k + 1; q < nkst; ++q)
+        for (auto& op : p.stage_ops[q]) {
+          if (op.kind == OP_MOV || op.kind == OP_ADD || op.kind == OP_SUB || op.kind == OP_CMP) {
+            if (op.a >= 0) used.insert(op.a);
+            if (op.kind != OP_MOV && op.b >= 0) used.insert(op.b);
+          }
+        }
+      for (int j = 0; j < nkey; ++j) used.insert(p.key_slot[j]);
+      if (p.val_slot >= 0) used.insert(p.val_slot);
+      for (auto& kv : avail)
+        if (kv.second <= k && used.count(slot[kv.first])) p.live_after[k].push_back(slot[kv.first]);
+      std::sort(p.live_after[k].begin(), p.live_after[k].end());
+    }
+    *out = p;
+    return true;
+  }
+};
+
+}  // namespace
+
+xl_status compile_program(Context* ctx, const char* text, Program** out) {
+  Lexer lx;
+  if (!lx.run(text)) return ctx->fail(XL_PARSE_ERROR, lx.err);
+  Parser ps(lx.toks);
+  auto prog = new Program();
+  prog->ctx = ctx;
+  while (lx.toks[ps.i].kind != Tok::END) {
+    RuleAst r;
+    if (!ps.rule(&r)) {
+      delete prog;
+      return ctx->fail(XL_PARSE_ERROR, ps.err);
+    }
+    prog->rules.push_back(r);
+  }
+  auto bad = [&](xl_status st, const std::string& m) {
+    delete prog;
+    return ctx->fail(st, m);
+  };
+  if (prog->rules.empty()) return bad(XL_INVALID_ARGUMENT, "no rules");
+  // declarations, arity, head kinds
+  for (auto& r : prog->rules) {
+    Relation* h = ctx->find(r.head);
+    if (!h) return bad(XL_INVALID_ARGUMENT, "relation '" + r.head + "' is not declared");
+    const int want = (int)r.head_args.size() + (r.agg != Agg::NONE ? 1 : 0);
+    if (want != h->arity) return bad(XL_INVALID_ARGUMENT, "rule '" + r.text + "': head has " + std::to_string(want) + " arguments but " + h->name + " has arity " + std::to_string(h->arity));
+    if (r.head_args.empty() || r.head_args.size() > 2)
+      return bad(XL_UNSUPPORTED, "rule '" + r.text + "': derived relations need one or two key columns");
+    for (size_t j = 0; j < r.head_args.size(); ++j)
+      if (h->types[j] != T_I32) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': key columns of derived relations must be int32");
+    for (auto& a : r.atoms) {
+      Relation* rel = ctx->find(a.pred);
+      if (!rel) return bad(XL_INVALID_ARGUMENT, "relation '" + a.pred + "' is not declared");
+      if ((int)a.args.size() != rel->arity)
+        return bad(XL_INVALID_ARGUMENT, "rule '" + r.text + "': " + a.pred + " used with " + std::to_string(a.args.size()) + " arguments but has arity " + std::to_string(rel->arity));
+    }
+    if (r.atoms.empty()) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': a rule needs at least one body atom");
+    bool found = false;
+    for (auto& hi : prog->heads)
+      if (hi.rel == h) {
+        found = true;
+        if (hi.agg != r.agg) return bad(XL_UNSUPPORTED, "relation " + h->name + " is derived with two different aggregates");
+      }
+    if (!found) prog->heads.push_back({h, r.agg});
+  }
+  // dependency graph between derived relations and Tarjan's SCC algorithm
+  const int nh = (int)prog->heads.size();
+  auto hid = [&](Relation* r) {
+    for (int k = 0; k < nh; ++k)
+      if (prog->heads[k].rel == r) return k;
+    return -1;
+  };
+  std::vector<std::set<int>> deps(nh);
+  for (auto& r : prog->rules)
+    for (auto& a : r.atoms) {
+      int d = hid(ctx->find(a.pred));
+      if (d >= 0) deps[hid(ctx->find(r.head))].insert(d);
+    }
+  std::vector<int> index(nh, -1), low(nh, 0), stack;
+  std::vector<bool> on(nh, false);
+  std::vector<std::vector<int>> comps;
+  int counter = 0;
+  std::function<void(int)> visit = [&](int v) {
+    index[v] = low[v] = counter++;
+    stack.push_back(v);
+    on[v] = true;
+    for (int w : deps[v]) {
+      if (index[w] < 0) {
+        visit(w);
+        low[v] = std::min(low[v], low[w]);
+      } else if (on[w]) {
+        low[v] = std::min(low[v], index[w]);
+      }
+    }
+    if (low[v] == index[v]) {
+      std::vector<int> c;
+      while (true) {
+        int w = stack.back();
+        stack.pop_back();
+        on[w] = false;
+        c.push_back(w);
+        if (w == v) break;
+      }
+      comps.push_back(c);
+    }
+  };
+  for (int v = 0; v < nh; ++v)
+    if (index[v] < 0) visit(v);
+  // Tarjan emits components after everything they depend on.
+  Planner pl{ctx};
+  for (auto& c : comps) {
+    Stratum st;
+    std::set<Relation*> in;
+    for (int v : c) {
+      st.heads.push_back(prog->heads[v].rel);
+      in.insert(prog->heads[v].rel);
+    }
+    st.recursive = c.size() > 1 || deps[c[0]].count(c[0]);
+    bool has_agg = false;
+    for (int v : c) has_agg = has_agg || prog->heads[v].agg != Agg::NONE;
+    if (st.recursive && has_agg) {
+      if (c.size() > 1)
+        return bad(XL_UNSUPPORTED, "aggregate relation " + prog->heads[c[0]].rel->name + " is mutually recursive with another relation");
+      if (prog->heads[c[0]].agg == Agg::COUNT)
+        return bad(XL_UNSUPPORTED, "count inside recursion is not supported (relation " + prog->heads[c[0]].rel->name + ")");
+    }
+    for (int ri = 0; ri < (int)prog->rules.size(); ++ri) {
+      const RuleAst& r = prog->rules[ri];
+      if (!in.count(ctx->find(r.head))) continue;
+      std::vector<int> rec;
+      for (int k = 0; k < (int)r.atoms.size(); ++k)
+        if (in.count(ctx->find(r.atoms[k].pred))) rec.push_back(k);
+      if (rec.size() > 1)
+        return bad(XL_UNSUPPORTED, "rule '" + r.text + "': non-linear recursion (more than one recursive atom) is not supported yet");
+      RulePlan full;
+      if (!pl.plan(r, ri, rec.empty() ? 0 : rec[0], false, &full)) return bad(pl.status, pl.err);
+      st.full.push_back(full);
+      if (!rec.empty()) {
+        RulePlan var;
+        if (!pl.plan(r, ri, rec[0], true, &var)) return bad(pl.status, pl.err);
+        st.variants.push_back(var);
+      }
+    }
+    // every index join must target a relation outside the stratum
+    for (auto* plans : {&st.full, &st.variants})
+      for (auto& p : *plans)
+        for (auto& s : p.steps)
+          if (in.count(s.rel))
+            return bad(XL_UNSUPPORTED, "rule '" + prog->rules[p.rule].text + "': non-linear recursion is not supported yet");
+    prog->strata.push_back(st);
+  }
+  *out = prog;
+  return XL_OK;
+}
+
+std::string explain_program(const Program* p) {
+  std::ostringstream os;
+  auto acts = [&](const ColAct* a, int n) {
+    std::ostringstream o;
+    for (int j = 0; j < n; ++j) {
+      if (j) o << ",";
+      switch (a[j].kind) {
+        case CA_BIND: o << "v" << (int)a[j].slot; break;
+        case CA_CHECK_SLOT: o << "=v" << (int)a[j].slot; break;
+        case CA_CHECK_CONST: o << "=#" << a[j].cval; break;
+        default: o << "_";
+      }
+    }
+    return o.str();
+  };
+  for (size_t s = 0; s < p->strata.size(); ++s) {
+    const Stratum& st = p->strata[s];
+    os << "stratum " << s << (st.recursive ? " recursive" : " non-recursive") << " heads:";
+    for (Relation* h : st.heads) os << " " << h->name << "[" << agg_name(p->head_agg(h)) << "]";
+    os << "\n";
+    for (int pass = 0; pass < 2; ++pass) {
+      const auto& plans = pass == 0 ? st.full : st.variants;
+      for (const RulePlan& rp : plans) {
+        os << "  " << (pass == 0 ? (st.recursive ? "seed " : "eval ") : "delta ") << "rule " << rp.rule << ": ";
+        os << (rp.driver_delta ? "delta " : "scan ") << rp.driver->name << "(" << acts(rp.driver_act, rp.driver->arity) << ")";
+        for (size_t k = 0; k < rp.steps.size(); ++k) {
+          const StepPlan& sp = rp.steps[k];
+          os << " -> join " << sp.rel->name << " on col " << sp.key_col << "=v" << sp.key_slot << " ("
+             << acts(sp.act, sp.rel->arity) << ")";
+        }
+        int nops = 0;
+        for (auto& v : rp.stage_ops) nops += (int)v.size();
+        os << " ops=" << nops << " -> " << rp.head->name << " key(v" << rp.key_slot[0];
+        if (rp.nkey == 2) os << ",v" << rp.key_slot[1];
+        os << ")";
+        if (rp.val_slot >= 0) os << " val v" << rp.val_slot;
+        os << "\n";
+      }
+    }
+  }
+  return os.str();
+}
+
+}  // namespace xlh

@@ -1,0 +1,90 @@
+// Host-side launchers for the HIP kernels (all enqueue on the given stream and
+// return the launch status; none synchronizes).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "device_types.h"
+
+namespace xlh {
+namespace k {
+
+typedef unsigned long long u64;
+
+// ---- device-wide exclusive prefix sum (in place allowed) ----
+size_t scan_temp_bytes(int64_t n);
+hipError_t scan_exclusive_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total,
+                              void* temp, hipStream_t s);
+hipError_t scan_exclusive_u64(const u64* in, u64* out, int64_t n, u64* total, void* temp,
+                              hipStream_t s);
+
+// ---- LSD radix sort of (key, u32 value) pairs on bits [0, bits) ----
+// Ping-pongs between (keys, vals) and (keys_alt, vals_alt); *in_alt tells
+// which pair holds the result.  vals may be null (keys only).
+size_t radix_temp_bytes(int64_t n);
+hipError_t radix_sort_u32(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt,
+                          int64_t n, int bits, void* temp, hipStream_t s, int* in_alt);
+hipError_t radix_sort_u64(u64* keys, uint32_t* vals, u64* keys_alt, uint32_t* vals_alt,
+                          int64_t n, int bits, void* temp, hipStream_t s, int* in_alt);
+
+// ---- small helpers ----
+hipError_t iota_u32(uint32_t* out, int64_t n, hipStream_t s);
+hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n,
+                      hipStream_t s);
+// Order-preserving u32 image of a column: i32 signed order, f32 totalOrder.
+hipError_t ordered_key(const uint32_t* col, int type, const uint32_t* perm, uint32_t* out,
+                       int64_t n, hipStream_t s);
+// out[0] = min, out[1] = max over an i32 column (out must be initialised by caller
+// to {INT32_MAX, INT32_MIN}).
+hipError_t minmax_i32(const int32_t* col, int64_t n, int32_t* out, hipStream_t s);
+// key[i] = col[i] - lo as unsigned.
+hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hipStream_t s);
+// off[k] = first i with sorted[i] >= k, for k in [0, range].
+hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
+                       hipStream_t s);
+// flag[i] = 1 if row i differs (bitwise) from row i-1 in any column (or i == 0).
+hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
+                            hipStream_t s);
+// dst[pos[i]] = src[i] where flag[i] != 0.
+hipError_t compact_u32(const uint32_t* src, const uint32_t* flag, const uint32_t* pos,
+                       uint32_t* dst, int64_t n, hipStream_t s);
+
+// ---- join / project / emit stage ----
+hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap);
+
+// ---- hash tables ----
+hipError_t set_insert_rows(u64* table, u64 mask, const uint32_t* c0, const uint32_t* c1,
+                           int64_t n, KeyPack kp, unsigned long long* counters, hipStream_t s);
+hipError_t table16_insert_rows(Slot16* table, u64 mask, const uint32_t* c0, const uint32_t* c1,
+                               const uint32_t* v, int64_t n, KeyPack kp, int type, int is_max,
+                               unsigned long long* counters, hipStream_t s);
+hipError_t table16_rehash(const Slot16* old, int64_t old_cap, Slot16* nt, u64 mask,
+                          unsigned long long* counters, hipStream_t s);
+hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_t* delta_idx,
+                           unsigned long long* counter, hipStream_t s);
+// Rows (k0[, k1], v) of the given slots; folds are decoded (min/max transform).
+hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n, KeyPack kp,
+                                 int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                                 uint32_t* v, hipStream_t s);
+hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
+                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap,
+                           unsigned long long* counter, hipStream_t s);
+
+// ---- sorted-candidate aggregation (sum / logsumexp / count) ----
+hipError_t seg_heads(const u64* keys, int64_t n, uint32_t* flag, hipStream_t s);
+hipError_t seg_starts(const uint32_t* flag, const uint32_t* pos, int64_t n, uint32_t* start,
+                      hipStream_t s);
+// fold_kind: FOLD_SUM / FOLD_LSE / FOLD_COUNT / FOLD_MIN / FOLD_MAX
+hipError_t seg_reduce(const u64* keys, const uint32_t* vals, const uint32_t* start, int64_t nseg,
+                      int64_t n, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      uint32_t* v, hipStream_t s);
+// S(key) = S(key) (+) delta for every delta row (keys unique within the call).
+hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1,
+                     const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
+                     unsigned long long* counters, hipStream_t s);
+
+enum FoldKind { FOLD_NONE = 0, FOLD_COUNT, FOLD_SUM, FOLD_MIN, FOLD_MAX, FOLD_LSE };
+
+}  // namespace k
+}  // namespace xlh

@@ -1,0 +1,1044 @@
+// HIP kernels for gfx950 (CDNA4, wave64).  Every hot loop here is bound by
+// memory traffic or by atomics, never by arithmetic; nothing is a dense
+// contraction, so no matrix-core instructions are used.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace xlh {
+namespace k {
+
+// ============================================================ wave helpers
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ u64 lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t t = __shfl_up(x, d, 64);
+    if (lane >= d) x += t;
+  }
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan_t(T x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    T t = __shfl_up(x, d, 64);
+    if (lane >= d) x += t;
+  }
+  return x;
+}
+
+// Wavefront-local LDS ordering: LDS operations of one wave complete in issue
+// order; this keeps the compiler from moving accesses across the point.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// SplitMix64 finalizer (Steele, Lea, Flood 2014): a bijective 64-bit mixer.
+__device__ __forceinline__ u64 mix64(u64 x) {
+  x ^= x >> 30;
+  x *= 0xbf58476d1ce4e5b9ull;
+  x ^= x >> 27;
+  x *= 0x94d049bb133111ebull;
+  x ^= x >> 31;
+  return x;
+}
+
+__device__ __forceinline__ u64 atomic_load_agent(const u64* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+static inline unsigned grid_for(int64_t n, int per_block, int cap = 1 << 20) {
+  int64_t g = (n + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (unsigned)g;
+}
+
+// ============================================================ scan
+constexpr int SC_THREADS = 256;
+constexpr int SC_ITEMS = 16;
+constexpr int SC_TILE = SC_THREADS * SC_ITEMS;
+
+template <typename T>
+__device__ T block_excl_scan(T x, T* total) {
+  __shared__ T s_w[SC_THREADS / 64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  T incl = wave_incl_scan_t<T>(x);
+  if (lane == 63) s_w[w] = incl;
+  __syncthreads();
+  T pre = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < SC_THREADS / 64; ++i) {
+    T y = s_w[i];
+    if (i < w) pre += y;
+    tot += y;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + incl - x;
+}
+
+template <typename T>
+__global__ __launch_bounds__(SC_THREADS) void scan_reduce_k(const T* in, int64_t n, T* partial) {
+  const int64_t base = (int64_t)blockIdx.x * SC_TILE;
+  T acc = 0;
+#pragma unroll
+  for (int i = 0; i < SC_ITEMS; ++i) {
+    int64_t idx = base + (int64_t)i * SC_THREADS + threadIdx.x;
+    if (idx < n) acc += in[idx];
+  }
+  T tot;
+  block_excl_scan<T>(acc, &tot);
+  if (threadIdx.x == 0) partial[blockIdx.x] = tot;
+}
+
+// Each thread owns SC_ITEMS consecutive elements.
+template <typename T>
+__global__ __launch_bounds__(SC_THREADS) void scan_apply_k(const T* in, T* out, int64_t n,
+                                                            const T* partial, T* total) {
+  const int64_t base = (int64_t)blockIdx.x * SC_TILE + (int64_t)threadIdx.x * SC_ITEMS;
+  T v[SC_ITEMS];
+  T acc = 0;
+#pragma unroll
+  for (int i = 0; i < SC_ITEMS; ++i) {
+    int64_t idx = base + i;
+    v[i] = idx < n ? in[idx] : (T)0;
+    acc += v[i];
+  }
+  T tot;
+  T pre = block_excl_scan<T>(acc, &tot);
+  pre += partial ? partial[blockIdx.x] : (T)0;
+#pragma unroll
+  for (int i = 0; i < SC_ITEMS; ++i) {
+    int64_t idx = base + i;
+    if (idx < n) out[idx] = pre;
+    pre += v[i];
+  }
+  if (total && blockIdx.x == gridDim.x - 1 && threadIdx.x == SC_THREADS - 1) *total = pre;
+}
+
+size_t scan_temp_bytes(int64_t n) {
+  size_t bytes = 0;
+  int64_t m = n;
+  while (m > SC_TILE) {
+    m = (m + SC_TILE - 1) / SC_TILE;
+    bytes += ((size_t)m * 8 + 255) & ~(size_t)255;
+  }
+  return bytes + 256;
+}
+
+template <typename T>
+static hipError_t scan_rec(const T* in, T* out, int64_t n, T* total, char* temp, hipStream_t s) {
+  if (n <= 0) {
+    if (total) return hipMemsetAsync(total, 0, sizeof(T), s);
+    return hipSuccess;
+  }
+  if (n <= SC_TILE) {
+    scan_apply_k<T><<<1, SC_THREADS, 0, s>>>(in, out, n, nullptr, total);
+    return hipGetLastError();
+  }
+  int64_t nb = (n + SC_TILE - 1) / SC_TILE;
+  T* partial = (T*)temp;
+  char* next = temp + (((size_t)nb * 8 + 255) & ~(size_t)255);
+  scan_reduce_k<T><<<(unsigned)nb, SC_THREADS, 0, s>>>(in, n, partial);
+  hipError_t e = scan_rec<T>(partial, partial, nb, nullptr, next, s);
+  if (e != hipSuccess) return e;
+  scan_apply_k<T><<<(unsigned)nb, SC_THREADS, 0, s>>>(in, out, n, partial, total);
+  return hipGetLastError();
+}
+
+hipError_t scan_exclusive_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total,
+                              void* temp, hipStream_t s) {
+  return scan_rec<uint32_t>(in, out, n, total, (char*)temp, s);
+}
+hipError_t scan_exclusive_u64(const u64* in, u64* out, int64_t n, u64* total, void* temp,
+                              hipStream_t s) {
+  return scan_rec<u64>(in, out, n, total, (char*)temp, s);
+}
+
+// ============================================================ radix sort
+// LSD radix sort with 8-bit digits.  Per pass: a per-tile digit histogram
+// (LDS atomics), a device-wide scan of the digit-major histogram table, and a
+// stable scatter.  In the scatter each wavefront ranks its keys with a
+// ballot-based match of equal digits and running per-wave digit counters in
+// LDS, so the pass is stable without a block-wide sort.
+constexpr int RS_THREADS = 256;
+constexpr int RS_WAVES = RS_THREADS / 64;
+constexpr int RS_ITEMS = 16;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
+
+template <typename K>
+__global__ __launch_bounds__(RS_THREADS) void rs_hist_k(const K* keys, int64_t n, int shift,
+                                                         uint32_t dmask, uint32_t* hist,
+                                                         uint32_t nblocks) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+#pragma unroll
+  for (int i = 0; i < RS_ITEMS; ++i) {
+    int64_t idx = base + (int64_t)i * RS_THREADS + threadIdx.x;
+    if (idx < n) atomicAdd(&h[(uint32_t)(keys[idx] >> shift) & dmask], 1u);
+  }
+  __syncthreads();
+  hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+template <typename K>
+__global__ __launch_bounds__(RS_THREADS) void rs_scatter_k(const K* kin, const uint32_t* vin,
+                                                            K* kout, uint32_t* vout, int64_t n,
+                                                            int shift, int nbits,
+                                                            const uint32_t* off,
+                                                            uint32_t nblocks) {
+  __shared__ uint32_t cnt[RS_WAVES][256];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < RS_WAVES * 256; i += RS_THREADS) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  const uint32_t dmask = (1u << nbits) - 1u;
+  const int64_t sub = (int64_t)blockIdx.x * RS_TILE + (int64_t)w * 64 * RS_ITEMS;
+  K key[RS_ITEMS];
+  uint32_t val[RS_ITEMS], rank[RS_ITEMS], dig[RS_ITEMS];
+#pragma unroll
+  for (int i = 0; i < RS_ITEMS; ++i) {
+    const int64_t idx = sub + (int64_t)i * 64 + lane;
+    const bool valid = idx < n;
+    key[i] = valid ? kin[idx] : (K)0;
+    val[i] = (valid && vin) ? vin[idx] : 0u;
+    const uint32_t d = (uint32_t)(key[i] >> shift) & dmask;
+    u64 peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const u64 bal = __ballot(bit);
+      peers &= bit ? bal : ~bal;
+    }
+    if (!valid) peers = 0;
+    const uint32_t lt = __popcll(peers & lanemask_lt());
+    const uint32_t before = cnt[w][d];
+    wave_lds_sync();
+    rank[i] = before + lt;
+    dig[i] = valid ? d : 0xffffffffu;
+    if (valid && lt == 0) cnt[w][d] = before + (uint32_t)__popcll(peers);
+    wave_lds_sync();
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < RS_ITEMS; ++i) {
+    const uint32_t d = dig[i];
+    if (d == 0xffffffffu) continue;
+    uint32_t pre = 0;
+    for (int ww = 0; ww < w; ++ww) pre += cnt[ww][d];
+    const uint32_t pos = off[(size_t)d * nblocks + blockIdx.x] + pre + rank[i];
+    kout[pos] = key[i];
+    if (vout) vout[pos] = val[i];
+  }
+}
+
+size_t radix_temp_bytes(int64_t n) {
+  int64_t nb = (n + RS_TILE - 1) / RS_TILE;
+  if (nb < 1) nb = 1;
+  size_t hist = (((size_t)nb * 256 * 4) + 255) & ~(size_t)255;
+  return hist + scan_temp_bytes(nb * 256);
+}
+
+template <typename K>
+static hipError_t radix_sort_t(K* keys, uint32_t* vals, K* keys_alt, uint32_t* vals_alt,
+                               int64_t n, int bits, void* temp, hipStream_t s, int* in_alt) {
+  *in_alt = 0;
+  if (n <= 1 || bits <= 0) return hipSuccess;
+  const uint32_t nb = (uint32_t)((n + RS_TILE - 1) / RS_TILE);
+  uint32_t* hist = (uint32_t*)temp;
+  char* stemp = (char*)temp + ((((size_t)nb * 256 * 4) + 255) & ~(size_t)255);
+  K* ka = keys;
+  K* kb = keys_alt;
+  uint32_t* va = vals;
+  uint32_t* vb = vals ? vals_alt : nullptr;
+  for (int shift = 0; shift < bits; shift += 8) {
+    const int nbits = bits - shift < 8 ? bits - shift : 8;
+    rs_hist_k<K><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
+    hipError_t e = scan_exclusive_u32(hist, hist, (int64_t)nb * 256, nullptr, stemp, s);
+    if (e != hipSuccess) return e;
+    rs_scatter_k<K><<<nb, RS_THREADS, 0, s>>>(ka, va, kb, vb, n, shift, nbits, hist, nb);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    K* tk = ka; ka = kb; kb = tk;
+    uint32_t* tv = va; va = vb; vb = tv;
+    *in_alt ^= 1;
+  }
+  return hipSuccess;
+}
+
+hipError_t radix_sort_u32(uint32_t* keys, uint32_t* vals, uint32_t* keys_alt, uint32_t* vals_alt,
+                          int64_t n, int bits, void* temp, hipStream_t s, int* in_alt) {
+  return radix_sort_t<uint32_t>(keys, vals, keys_alt, vals_alt, n, bits, temp, s, in_alt);
+}
+hipError_t radix_sort_u64(u64* keys, uint32_t* vals, u64* keys_alt, uint32_t* vals_alt, int64_t n,
+                          int bits, void* temp, hipStream_t s, int* in_alt) {
+  return radix_sort_t<u64>(keys, vals, keys_alt, vals_alt, n, bits, temp, s, in_alt);
+}
+
+// ============================================================ small helpers
+__global__ void iota_k(uint32_t* out, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = (uint32_t)i;
+}
+hipError_t iota_u32(uint32_t* out, int64_t n, hipStream_t s) {
+  iota_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(out, n);
+  return hipGetLastError();
+}
+
+__global__ void gather_k(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[perm[i]];
+}
+hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n,
+                      hipStream_t s) {
+  gather_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(src, perm, dst, n);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ uint32_t order_bits(uint32_t x, int type) {
+  if (type == T_F32) return x ^ ((x >> 31) ? 0xffffffffu : 0x80000000u);  // totalOrder
+  return x ^ 0x80000000u;                                                  // signed int
+}
+
+__global__ void ordered_key_k(const uint32_t* col, int type, const uint32_t* perm,
+                              uint32_t* out, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = order_bits(col[perm ? perm[i] : i], type);
+}
+hipError_t ordered_key(const uint32_t* col, int type, const uint32_t* perm, uint32_t* out,
+                       int64_t n, hipStream_t s) {
+  ordered_key_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(col, type, perm, out, n);
+  return hipGetLastError();
+}
+
+__global__ void minmax_k(const int32_t* col, int64_t n, int32_t* out) {
+  int32_t lo = INT32_MAX, hi = INT32_MIN;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    lo = min(lo, col[i]);
+    hi = max(hi, col[i]);
+  }
+  for (int d = 32; d > 0; d >>= 1) {
+    lo = min(lo, __shfl_xor(lo, d, 64));
+    hi = max(hi, __shfl_xor(hi, d, 64));
+  }
+  if (lane_id() == 0) {
+    atomicMin(&out[0], lo);
+    atomicMax(&out[1], hi);
+  }
+}
+hipError_t minmax_i32(const int32_t* col, int64_t n, int32_t* out, hipStream_t s) {
+  minmax_k<<<grid_for(n, 256, 2048), 256, 0, s>>>(col, n, out);
+  return hipGetLastError();
+}
+
+__global__ void sub_lo_k(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = col[i] - (uint32_t)lo;
+}
+hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hipStream_t s) {
+  sub_lo_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(col, lo, out, n);
+  return hipGetLastError();
+}
+
+__global__ void csr_offsets_k(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k <= (int64_t)range;
+       k += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo = 0, hi = n;  // first i with sorted[i] >= k
+    while (lo < hi) {
+      int64_t mid = (lo + hi) >> 1;
+      if ((int64_t)sorted[mid] < k) lo = mid + 1; else hi = mid;
+    }
+    off[k] = (uint32_t)lo;
+  }
+}
+hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
+                       hipStream_t s) {
+  csr_offsets_k<<<grid_for((int64_t)range + 1, 256, 65536), 256, 0, s>>>(sorted, n, range, off);
+  return hipGetLastError();
+}
+
+struct ColPtrs { const uint32_t* c[MAXC]; };
+
+__global__ void row_change_k(ColPtrs cols, int ncols, int64_t n, uint32_t* flag) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t f = (i == 0);
+    if (i > 0)
+      for (int c = 0; c < ncols; ++c) f |= cols.c[c][i] != cols.c[c][i - 1];
+    flag[i] = f;
+  }
+}
+hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
+                            hipStream_t s) {
+  ColPtrs p{};
+  for (int c = 0; c < ncols; ++c) p.c[c] = cols[c];
+  row_change_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(p, ncols, n, flag);
+  return hipGetLastError();
+}
+
+__global__ void compact_k(const uint32_t* src, const uint32_t* flag, const uint32_t* pos,
+                          uint32_t* dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    if (flag[i]) dst[pos[i]] = src[i];
+}
+hipError_t compact_u32(const uint32_t* src, const uint32_t* flag, const uint32_t* pos,
+                       uint32_t* dst, int64_t n, hipStream_t s) {
+  compact_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(src, flag, pos, dst, n);
+  return hipGetLastError();
+}
+
+// ============================================================ hash tables
+// Open addressing over a power-of-two array with linear probing, so a probe
+// sequence walks consecutive 8- or 16-byte slots of the same 128-byte line.
+// A slot only ever changes from EMPTY to a key, so a plain (possibly stale)
+// read is a safe filter: a stale EMPTY is resolved by the compare-and-swap.
+__device__ __forceinline__ int set_insert(u64* table, u64 mask, u64 key, u64* counters) {
+  u64 i = mix64(key) & mask;
+  for (u64 probe = 0; probe <= mask; ++probe) {
+    const u64 cur = table[i];
+    if (cur == key) return 0;
+    if (cur == EMPTY_KEY) {
+      const u64 prev = atomicCAS(&table[i], EMPTY_KEY, key);
+      if (prev == EMPTY_KEY) return 1;
+      if (prev == key) return 0;
+    }
+    i = (i + 1) & mask;
+  }
+  atomicOr(&counters[CNT_FATAL], 1ull);
+  return 0;
+}
+
+// Returns the slot index of key (inserting it if absent); *ins = newly inserted.
+__device__ __forceinline__ u64 slot_find_or_insert(Slot16* t, u64 mask, u64 key, bool* ins,
+                                                   u64* counters) {
+  u64 i = mix64(key) & mask;
+  *ins = false;
+  for (u64 probe = 0; probe <= mask; ++probe) {
+    const u64 cur = t[i].key;
+    if (cur == key) return i;
+    if (cur == EMPTY_KEY) {
+      const u64 prev = atomicCAS(&t[i].key, EMPTY_KEY, key);
+      if (prev == EMPTY_KEY) {
+        *ins = true;
+        return i;
+      }
+      if (prev == key) return i;
+    }
+    i = (i + 1) & mask;
+  }
+  atomicOr(&counters[CNT_FATAL], 1ull);
+  return ~0ull;
+}
+
+template <typename KP>
+__device__ __forceinline__ u64 pack_key(KP& kp, uint32_t a, uint32_t b) {
+  u64 k = (uint32_t)(a - (uint32_t)kp.lo[0]);
+  if (kp.nkey == 2) k = (k << kp.shift) | (uint32_t)(b - (uint32_t)kp.lo[1]);
+  return k;
+}
+__device__ __forceinline__ void unpack_key(const KeyPack& kp, u64 key, uint32_t* a, uint32_t* b) {
+  if (kp.nkey == 2) {
+    *a = (uint32_t)(key >> kp.shift) + (uint32_t)kp.lo[0];
+    *b = (uint32_t)(key & ((1ull << kp.shift) - 1ull)) + (uint32_t)kp.lo[1];
+  } else {
+    *a = (uint32_t)key + (uint32_t)kp.lo[0];
+    *b = 0;
+  }
+}
+
+// Min/max are kept as an order-preserving unsigned image so a single
+// atomicMin implements both (max stores the complement).
+__device__ __forceinline__ uint32_t fold_encode(uint32_t x, int type, int is_max) {
+  const uint32_t o = order_bits(x, type);
+  return is_max ? ~o : o;
+}
+__device__ __forceinline__ uint32_t fold_decode(uint32_t e, int type, int is_max) {
+  const uint32_t o = is_max ? ~e : e;
+  if (type == T_F32) return (o & 0x80000000u) ? (o ^ 0x80000000u) : ~o;
+  return o ^ 0x80000000u;
+}
+
+__global__ void set_insert_rows_k(u64* table, u64 mask, const uint32_t* c0, const uint32_t* c1,
+                                  int64_t n, KeyPack kp, u64* counters) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int ins = set_insert(table, mask, pack_key(kp, c0[i], c1 ? c1[i] : 0u), counters);
+    const u64 m = __ballot(ins);
+    if (m && lane_id() == (__ffsll((long long)m) - 1))
+      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
+  }
+}
+hipError_t set_insert_rows(u64* table, u64 mask, const uint32_t* c0, const uint32_t* c1, int64_t n,
+                           KeyPack kp, unsigned long long* counters, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  set_insert_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(table, mask, c0, c1, n, kp, counters);
+  return hipGetLastError();
+}
+
+__global__ void table16_insert_rows_k(Slot16* t, u64 mask, const uint32_t* c0, const uint32_t* c1,
+                                      const uint32_t* v, int64_t n, KeyPack kp, int type,
+                                      int is_max, u64* counters) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    bool ins;
+    const u64 s = slot_find_or_insert(t, mask, pack_key(kp, c0[i], c1 ? c1[i] : 0u), &ins,
+                                      counters);
+    if (s != ~0ull) atomicMin(&t[s].val, fold_encode(v[i], type, is_max));
+    const u64 m = __ballot(ins);
+    if (m && lane_id() == (__ffsll((long long)m) - 1))
+      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
+  }
+}
+hipError_t table16_insert_rows(Slot16* t, u64 mask, const uint32_t* c0, const uint32_t* c1,
+                               const uint32_t* v, int64_t n, KeyPack kp, int type, int is_max,
+                               unsigned long long* counters, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  table16_insert_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(t, mask, c0, c1, v, n, kp, type,
+                                                               is_max, counters);
+  return hipGetLastError();
+}
+
+__global__ void table16_rehash_k(const Slot16* old, int64_t old_cap, Slot16* nt, u64 mask,
+                                 u64* counters) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < old_cap;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const Slot16 s = old[i];
+    if (s.key == EMPTY_KEY) continue;
+    bool ins;
+    const u64 j = slot_find_or_insert(nt, mask, s.key, &ins, counters);
+    if (j != ~0ull) {
+      nt[j].val = s.val;
+      nt[j].stamp = s.stamp;
+    }
+  }
+}
+hipError_t table16_rehash(const Slot16* old, int64_t old_cap, Slot16* nt, u64 mask,
+                          unsigned long long* counters, hipStream_t s) {
+  table16_rehash_k<<<grid_for(old_cap, 256, 8192), 256, 0, s>>>(old, old_cap, nt, mask, counters);
+  return hipGetLastError();
+}
+
+__global__ void table16_stamped_k(const Slot16* t, int64_t cap, uint32_t round, uint32_t* idx,
+                                  u64* counter) {
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < cap;
+       base += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = base + threadIdx.x;
+    const bool hit = i < cap && t[i].key != EMPTY_KEY && t[i].stamp == round;
+    const u64 m = __ballot(hit);
+    if (!m) continue;
+    const int leader = __ffsll((long long)m) - 1;
+    u64 pos0 = 0;
+    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
+    pos0 = __shfl(pos0, leader, 64);
+    if (hit) idx[pos0 + __popcll(m & lanemask_lt())] = (uint32_t)i;
+  }
+}
+hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_t* delta_idx,
+                           unsigned long long* counter, hipStream_t s) {
+  table16_stamped_k<<<grid_for(cap, 256, 8192), 256, 0, s>>>(t, cap, round, delta_idx, counter);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ uint32_t stored_value(uint32_t e, int type, int fold_kind) {
+  if (fold_kind == FOLD_MIN) return fold_decode(e, type, 0);
+  if (fold_kind == FOLD_MAX) return fold_decode(e, type, 1);
+  return e;
+}
+
+__global__ void table16_rows_from_idx_k(const Slot16* t, const uint32_t* idx, int64_t n,
+                                        KeyPack kp, int type, int fold_kind, uint32_t* k0,
+                                        uint32_t* k1, uint32_t* v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const Slot16 s = t[idx[i]];
+    uint32_t a, b;
+    unpack_key(kp, s.key, &a, &b);
+    k0[i] = a;
+    if (k1) k1[i] = b;
+    v[i] = stored_value(s.val, type, fold_kind);
+  }
+}
+hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n, KeyPack kp,
+                                 int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
+                                 hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  table16_rows_from_idx_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(t, idx, n, kp, type, fold_kind,
+                                                                 k0, k1, v);
+  return hipGetLastError();
+}
+
+__global__ void table16_compact_k(const Slot16* t, int64_t cap, KeyPack kp, int type,
+                                  int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
+                                  int64_t out_cap, u64* counter) {
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < cap;
+       base += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = base + threadIdx.x;
+    Slot16 s;
+    s.key = EMPTY_KEY;
+    if (i < cap) s = t[i];
+    const bool hit = s.key != EMPTY_KEY;
+    const u64 m = __ballot(hit);
+    if (!m) continue;
+    const int leader = __ffsll((long long)m) - 1;
+    u64 pos0 = 0;
+    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
+    pos0 = __shfl(pos0, leader, 64);
+    if (hit) {
+      const u64 p = pos0 + __popcll(m & lanemask_lt());
+      if (p >= (u64)out_cap) continue;  // the host detects the count mismatch
+      uint32_t a, b;
+      unpack_key(kp, s.key, &a, &b);
+      k0[p] = a;
+      if (k1) k1[p] = b;
+      v[p] = stored_value(s.val, type, fold_kind);
+    }
+  }
+}
+hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
+                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap,
+                           unsigned long long* counter, hipStream_t s) {
+  table16_compact_k<<<grid_for(cap, 256, 8192), 256, 0, s>>>(t, cap, kp, type, fold_kind, k0, k1,
+                                                             v, out_cap, counter);
+  return hipGetLastError();
+}
+
+// ============================================================ stage kernel
+// One launch evaluates one join step of a rule plan for a batch of source
+// rows: bind the source row's columns, expand it through an index (all rows
+// of the indexed relation whose key column equals a bound variable), bind
+// the matched row's columns, run comparisons and arithmetic, and emit.
+//
+// Load balance: a wavefront takes 64 consecutive source rows, scans their
+// index degrees across its lanes, and then walks the concatenated match
+// lists 64 entries at a time, each lane finding its owning source row by a
+// six-step binary search over the wave's scan in LDS.  Consecutive lanes
+// therefore read consecutive rows of the indexed relation (coalesced), and a
+// high-degree key occupies one wavefront for as many iterations as it needs
+// instead of one thread.
+
+// The descriptor is read in place from the kernel-argument segment (constant
+// address space 4, scalar loads) rather than copied into private memory.  The
+// address-space qualifier only exists in the device compilation pass.
+#if defined(__HIP_DEVICE_COMPILE__)
+#define XL_KARG __attribute__((address_space(4)))
+#else
+#define XL_KARG
+#endif
+typedef XL_KARG const StageArgs KernArgs;
+
+// Variable slots live in one 8-wide register vector; an access at a uniform
+// runtime slot index lowers to register-indexed moves, never to private
+// (scratch) memory.
+typedef uint32_t Regs __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ uint32_t getv(const Regs& u, int i) { return u[i & 7]; }
+__device__ __forceinline__ void setv(Regs& u, int i, uint32_t x) { u[i & 7] = x; }
+__device__ __forceinline__ bool eqv(uint32_t x, uint32_t y, int type) {
+  if (type == T_F32) return __uint_as_float(x) == __uint_as_float(y);
+  return x == y;
+}
+
+template <typename SRC>
+__device__ __forceinline__ bool bind_cols(SRC& src, int64_t row, Regs& u) {
+  const int ncols = src.ncols;
+  constexpr int NC = sizeof(src.col) / sizeof(src.col[0]);
+  bool ok = true;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if (c < ncols && src.act[c].kind != CA_NONE) {
+      const uint32_t x = src.col[c][row];
+      const int kind = src.act[c].kind;
+      if (kind == CA_BIND) setv(u, src.act[c].slot, x);
+      else if (kind == CA_CHECK_SLOT) ok = ok && eqv(x, getv(u, src.act[c].slot), src.act[c].type);
+      else ok = ok && eqv(x, src.act[c].cval, src.act[c].type);
+    }
+  }
+  return ok;
+}
+
+__device__ __forceinline__ uint32_t operand(KernArgs& a, const Regs& u, int o) {
+  if (o >= 0) return getv(u, o);
+  uint32_t r = a.consts[0];
+#pragma unroll
+  for (int k = 1; k < MAXK; ++k)
+    if (-1 - o == k) r = a.consts[k];
+  return r;
+}
+
+__device__ __forceinline__ bool compare(int cmp, int type, uint32_t x, uint32_t y) {
+  if (type == T_F32) {
+    const float fx = __uint_as_float(x), fy = __uint_as_float(y);
+    switch (cmp) {
+      case CMP_NE: return fx != fy;
+      case CMP_EQ: return fx == fy;
+      case CMP_LT: return fx < fy;
+      case CMP_LE: return fx <= fy;
+      case CMP_GT: return fx > fy;
+      default: return fx >= fy;
+    }
+  }
+  const int32_t ix = (int32_t)x, iy = (int32_t)y;
+  switch (cmp) {
+    case CMP_NE: return ix != iy;
+    case CMP_EQ: return ix == iy;
+    case CMP_LT: return ix < iy;
+    case CMP_LE: return ix <= iy;
+    case CMP_GT: return ix > iy;
+    default: return ix >= iy;
+  }
+}
+
+__device__ __forceinline__ bool run_ops(KernArgs& a, Regs& u) {
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < MAXOPS; ++i) {
+    if (i >= a.nops) continue;
+    const MicroOp op = a.ops[i];
+    const uint32_t x = operand(a, u, op.a);
+    if (op.kind == OP_CMP) {
+      ok = ok && compare(op.cmp, op.type, x, operand(a, u, op.b));
+    } else if (op.kind == OP_MOV) {
+      setv(u, op.dst, x);
+    } else {
+      const uint32_t y = operand(a, u, op.b);
+      uint32_t r;
+      if (op.type == T_F32) {
+        const float fx = __uint_as_float(x), fy = __uint_as_float(y);
+        // one correctly rounded binary32 operation, never contracted
+        r = __float_as_uint(op.kind == OP_ADD ? __fadd_rn(fx, fy) : __fsub_rn(fx, fy));
+      } else {
+        r = op.kind == OP_ADD ? x + y : x - y;
+      }
+      setv(u, op.dst, r);
+    }
+  }
+  return ok;
+}
+
+struct EmitState {
+  u64 out_base;     // EM_MAT: first output position of this chunk
+  uint32_t running; // rows emitted so far in this chunk
+  uint32_t cands;   // candidates seen in this chunk (EM_SET / EM_MINMAX)
+  bool stop;        // overflow observed: skip the rest of this launch
+};
+
+template <int MODE>
+__device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
+                                     EmitState& st) {
+  typedef XL_KARG const EmitSpec KEmit;
+  KEmit& e = a.emit;
+  const u64 lt = lanemask_lt();
+  if (MODE == EM_COUNT) {
+    st.running += (uint32_t)__popcll(__ballot(act));
+    return;
+  }
+  if (MODE == EM_MAT) {
+    const u64 m = __ballot(act);
+    if (act) {
+      const u64 pos = st.out_base + st.running + __popcll(m & lt);
+      if (e.mat_packed) {
+        e.out_key[pos] = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
+        if (e.val_slot >= 0) e.out_val[pos] = getv(u, e.val_slot);
+      } else {
+#pragma unroll
+        for (int i = 0; i < MAXV; ++i)
+          if (i < e.nout) e.out_col[i][pos] = getv(u, e.out_slot[i]);
+      }
+    }
+    st.running += (uint32_t)__popcll(m);
+    return;
+  }
+  // EM_SET / EM_MINMAX: stop early once the table passed its load limit.
+  st.cands += (uint32_t)__popcll(__ballot(act));
+  if (st.stop) return;
+  if (MODE == EM_SET) {
+    int ins = 0;
+    if (act) ins = set_insert(e.table, e.mask, pack_key(e.key, getv(u, e.key.slot[0]),
+                                                       getv(u, e.key.slot[1])), e.counters);
+    const u64 m = __ballot(ins);
+    if (m) {
+      const int leader = __ffsll((long long)m) - 1;
+      u64 base = 0;
+      if (lane_id() == leader) {
+        base = atomicAdd(&e.counters[CNT_APPENDED], (u64)__popcll(m));
+        if (base + __popcll(m) > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
+      }
+      base = __shfl(base, leader, 64);
+      if (base + __popcll(m) > e.limit) st.stop = true;
+      if (ins) {
+        const u64 p = (u64)e.row_base + base + __popcll(m & lt);
+        if (p < (u64)e.row_cap) {
+          e.row_col[0][p] = getv(u, e.key.slot[0]);
+          if (e.key.nkey == 2) e.row_col[1][p] = getv(u, e.key.slot[1]);
+        } else {
+          atomicOr(&e.counters[CNT_FATAL], 2ull);
+        }
+      }
+    }
+    return;
+  }
+  if (MODE == EM_MINMAX) {
+    bool ins = false, app = false;
+    u64 slot = ~0ull;
+    if (act) {
+      slot = slot_find_or_insert(e.table16, e.mask, pack_key(e.key, getv(u, e.key.slot[0]),
+                                                             getv(u, e.key.slot[1])),
+                                 &ins, e.counters);
+      if (slot != ~0ull) {
+        const uint32_t enc = fold_encode(getv(u, e.val_slot), e.val_type, e.is_max);
+        const uint32_t old = atomicMin(&e.table16[slot].val, enc);
+        if (ins || enc < old) app = atomicExch(&e.table16[slot].stamp, e.round) != e.round;
+      }
+    }
+    const u64 mi = __ballot(ins);
+    if (mi) {
+      const int leader = __ffsll((long long)mi) - 1;
+      u64 base = 0;
+      if (lane_id() == leader) {
+        base = atomicAdd(&e.counters[CNT_INSERTED], (u64)__popcll(mi));
+        if (base + __popcll(mi) > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
+      }
+      base = __shfl(base, leader, 64);
+      if (base + __popcll(mi) > e.limit) st.stop = true;
+    }
+    const u64 ma = __ballot(app);
+    if (ma) {
+      const int leader = __ffsll((long long)ma) - 1;
+      u64 base = 0;
+      if (lane_id() == leader) base = atomicAdd(&e.counters[CNT_APPENDED], (u64)__popcll(ma));
+      base = __shfl(base, leader, 64);
+      if (app) e.delta_idx[base + __popcll(ma & lt)] = (uint32_t)slot;
+    }
+  }
+}
+
+constexpr int ST_THREADS = 256;
+constexpr int ST_WAVES = ST_THREADS / 64;
+
+template <int MODE, bool HAS_INDEX>
+__global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
+  (void)by_value;
+  KernArgs& a = *(KernArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  __shared__ uint32_t s_excl[ST_WAVES][64];
+  __shared__ uint32_t s_beg[ST_WAVES][64];
+  __shared__ uint32_t s_v[ST_WAVES][MAXV][64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const int64_t nchunks = (a.src.n + 63) / 64;
+  const int64_t nwaves = (int64_t)gridDim.x * ST_WAVES;
+  EmitState st;
+  st.stop = false;
+  for (int64_t chunk = (int64_t)blockIdx.x * ST_WAVES + w; chunk < nchunks; chunk += nwaves) {
+    st.running = 0;
+    st.cands = 0;
+    st.out_base = (MODE == EM_MAT) ? a.emit.chunk_off[chunk] + (u64)a.emit.mat_base : 0;
+    if (MODE == EM_SET || MODE == EM_MINMAX) {
+      if (!st.stop) st.stop = atomic_load_agent(&a.emit.counters[CNT_OVERFLOW]) != 0;
+    }
+    const int64_t row = chunk * 64 + lane;
+    Regs v = (Regs)(0u);
+    bool ok = row < a.src.n;
+    if (ok) ok = bind_cols(a.src, row, v);
+    if (HAS_INDEX) {
+      uint32_t beg = 0, deg = 0;
+      if (ok) {
+        const uint32_t kk = getv(v, a.idx.key_slot) - (uint32_t)a.idx.key_lo;
+        if (kk < a.idx.key_range) {
+          beg = a.idx.off[kk];
+          deg = a.idx.off[kk + 1] - beg;
+        }
+      }
+      const uint32_t incl = wave_incl_scan(deg);
+      const uint32_t total = __shfl(incl, 63, 64);
+      s_excl[w][lane] = incl - deg;
+      s_beg[w][lane] = beg;
+#pragma unroll
+      for (int s = 0; s < MAXV; ++s) s_v[w][s][lane] = v[s];
+      wave_lds_sync();
+      for (uint32_t base = 0; base < total; base += 64) {
+        const uint32_t j = base + lane;
+        bool act = j < total;
+        int r = 0;
+#pragma unroll
+        for (int step = 32; step > 0; step >>= 1)
+          if (s_excl[w][r + step] <= j) r += step;
+        Regs u;
+#pragma unroll
+        for (int s = 0; s < MAXV; ++s) u[s] = s_v[w][s][r];
+        if (act) {
+          const uint32_t erow = s_beg[w][r] + (j - s_excl[w][r]);
+          act = bind_cols(a.idx, erow, u);
+        }
+        if (act) act = run_ops(a, u);
+        emit<MODE>(a, u, act, st);
+      }
+      wave_lds_sync();
+    } else {
+      bool act = ok;
+      if (act) act = run_ops(a, v);
+      emit<MODE>(a, v, act, st);
+    }
+    if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
+    if ((MODE == EM_SET || MODE == EM_MINMAX) && lane == 0 && st.cands)
+      atomicAdd(&a.emit.counters[CNT_CANDIDATES], (u64)st.cands);
+  }
+}
+
+template <int MODE>
+static void launch_mode(const StageArgs& a, unsigned grid, hipStream_t s) {
+  if (a.has_index) stage_k<MODE, true><<<grid, ST_THREADS, 0, s>>>(a);
+  else stage_k<MODE, false><<<grid, ST_THREADS, 0, s>>>(a);
+}
+
+hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
+  if (a.src.n <= 0) return hipSuccess;
+  const int64_t nchunks = (a.src.n + 63) / 64;
+  const unsigned grid = grid_for(nchunks, ST_WAVES, grid_cap);
+  switch (a.emit.mode) {
+    case EM_COUNT: launch_mode<EM_COUNT>(a, grid, s); break;
+    case EM_MAT: launch_mode<EM_MAT>(a, grid, s); break;
+    case EM_SET: launch_mode<EM_SET>(a, grid, s); break;
+    default: launch_mode<EM_MINMAX>(a, grid, s); break;
+  }
+  return hipGetLastError();
+}
+
+// ============================================================ segmented aggregation
+__global__ void seg_heads_k(const u64* keys, int64_t n, uint32_t* flag) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    flag[i] = (i == 0) || keys[i] != keys[i - 1];
+}
+hipError_t seg_heads(const u64* keys, int64_t n, uint32_t* flag, hipStream_t s) {
+  seg_heads_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(keys, n, flag);
+  return hipGetLastError();
+}
+
+__global__ void seg_starts_k(const uint32_t* flag, const uint32_t* pos, int64_t n,
+                             uint32_t* start) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    if (flag[i]) start[pos[i]] = (uint32_t)i;
+}
+hipError_t seg_starts(const uint32_t* flag, const uint32_t* pos, int64_t n, uint32_t* start,
+                      hipStream_t s) {
+  seg_starts_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(flag, pos, n, start);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ float lse2(float a, float b) {
+  if (a == -INFINITY) return b;
+  if (b == -INFINITY) return a;
+  const float m = fmaxf(a, b);
+  return m + log1pf(expf(-fabsf(a - b)));
+}
+
+// One thread folds one key group of the sorted candidates, in sorted order.
+// logsumexp is the two-pass max-shifted form: m = max, then m + log(sum exp(x - m)).
+__global__ void seg_reduce_k(const u64* keys, const uint32_t* vals, const uint32_t* start,
+                             int64_t nseg, int64_t n, KeyPack kp, int type, int fold_kind,
+                             uint32_t* k0, uint32_t* k1, uint32_t* v) {
+  for (int64_t sg = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; sg < nseg;
+       sg += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t b = start[sg];
+    const uint32_t e = sg + 1 < nseg ? start[sg + 1] : (uint32_t)n;
+    uint32_t out;
+    if (fold_kind == FOLD_COUNT) {
+      out = e - b;
+    } else if (fold_kind == FOLD_LSE) {
+      float m = -INFINITY;
+      for (uint32_t i = b; i < e; ++i) m = fmaxf(m, __uint_as_float(vals[i]));
+      if (m == -INFINITY) {
+        out = __float_as_uint(-INFINITY);
+      } else {
+        float acc = 0.0f;
+        for (uint32_t i = b; i < e; ++i) acc += expf(__uint_as_float(vals[i]) - m);
+        out = __float_as_uint(m + logf(acc));
+      }
+    } else if (fold_kind == FOLD_SUM) {
+      if (type == T_F32) {
+        float acc = 0.0f;
+        for (uint32_t i = b; i < e; ++i) acc += __uint_as_float(vals[i]);
+        out = __float_as_uint(acc);
+      } else {
+        uint32_t acc = 0;
+        for (uint32_t i = b; i < e; ++i) acc += vals[i];
+        out = acc;
+      }
+    } else {  // FOLD_MIN / FOLD_MAX
+      const int is_max = fold_kind == FOLD_MAX;
+      uint32_t best = fold_encode(vals[b], type, is_max);
+      for (uint32_t i = b + 1; i < e; ++i) best = min(best, fold_encode(vals[i], type, is_max));
+      out = fold_decode(best, type, is_max);
+    }
+    uint32_t a0, a1;
+    unpack_key(kp, keys[b], &a0, &a1);
+    k0[sg] = a0;
+    if (k1) k1[sg] = a1;
+    v[sg] = out;
+  }
+}
+hipError_t seg_reduce(const u64* keys, const uint32_t* vals, const uint32_t* start, int64_t nseg,
+                      int64_t n, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      uint32_t* v, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  seg_reduce_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(keys, vals, start, nseg, n, kp, type,
+                                                          fold_kind, k0, k1, v);
+  return hipGetLastError();
+}
+
+__global__ void agg_merge_k(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1,
+                            const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
+                            u64* counters) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    bool ins;
+    const u64 s = slot_find_or_insert(t, mask, pack_key(kp, k0[i], k1 ? k1[i] : 0u), &ins,
+                                      counters);
+    if (s != ~0ull) {
+      const uint32_t d = v[i];
+      uint32_t r = d;
+      if (!ins) {
+        const uint32_t cur = t[s].val;
+        if (fold_kind == FOLD_LSE) {
+          r = __float_as_uint(lse2(__uint_as_float(cur), __uint_as_float(d)));
+        } else if (fold_kind == FOLD_SUM) {
+          r = type == T_F32 ? __float_as_uint(__fadd_rn(__uint_as_float(cur), __uint_as_float(d)))
+                            : cur + d;
+        } else if (fold_kind == FOLD_COUNT) {
+          r = cur + d;
+        }
+      }
+      t[s].val = r;
+    }
+    const u64 m = __ballot(ins);
+    if (m && lane_id() == (__ffsll((long long)m) - 1))
+      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
+  }
+}
+hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1,
+                     const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
+                     unsigned long long* counters, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  agg_merge_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(t, mask, k0, k1, v, n, kp, type, fold_kind,
+                                                     counters);
+  return hipGetLastError();
+}
+
+}  // namespace k
+}  // namespace xlh

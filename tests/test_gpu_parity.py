@@ -1,0 +1,268 @@
+"""GPU parity: the HIP engine (through the C ABI) against the CPU oracle.
+
+Sets and counts must match bit for bit; min within 1e-6 relative (the f32
+fixpoint is expected to be bit-exact); logsumexp within 1e-5 * max(1, |ref|).
+"""
+import os
+
+import numpy as np
+import pytest
+
+from helpers import assert_same_relation, engine_run, select_rows, value_tolerance
+from oracle import evaluate
+from paper_2609_27203_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _compare(wl, rels, ref, where=""):
+    for name, types in wl.idb.items():
+        assert_same_relation(name, types, rels[name], ref.relations[name][1], where,
+                             tol=value_tolerance(wl.rules, name))
+
+
+def _golden(name):
+    rows = [tuple(int(x) for x in ln.split()) for ln in open(os.path.join(GOLDEN, name))
+            if ln.strip() and not ln.startswith("#")]
+    return [np.array(c, np.int32) for c in zip(*sorted(rows))]
+
+
+def _edges(src, dst):
+    return {"edge": (("i32", "i32"), [np.asarray(src, np.int32), np.asarray(dst, np.int32)])}
+
+
+# ------------------------------------------------------------- worked examples
+def test_listing_minimal_reach():
+    wl = W.Workload("listing", "reach(X, Y) :- edge(X, Y).\nreach(X, Z) :- reach(X, Y), edge(Y, Z).",
+                    _edges([1, 2, 3], [2, 3, 4]), {"reach": ("i32", "i32")})
+    print("case: listing minimal reach", flush=True)
+    rels, stats, _ = engine_run(wl, workspace_bytes=256 << 20)
+    exp = _golden("listing_minimal_reach.txt")
+    assert all(np.array_equal(a, b) for a, b in zip(rels["reach"], exp))
+    assert stats["delta_rows"] == [3, 2, 1, 0] and stats["iterations"] == 3
+
+
+def test_listing_agg_degree():
+    wl = W.Workload("agg", "degree(X, count(Y)) :- edge(X, Y).", _edges([1, 1, 1, 2], [2, 3, 4, 3]),
+                    {"degree": ("i32", "i32")})
+    print("case: listing degree count", flush=True)
+    rels, _, _ = engine_run(wl, workspace_bytes=256 << 20)
+    exp = _golden("listing_agg_degree.txt")
+    assert all(np.array_equal(a, b) for a, b in zip(rels["degree"], exp))
+
+
+# ------------------------------------------------------------- small workloads, every row
+@pytest.mark.parametrize("name", list(W.small_workloads()))
+def test_small_workload_matches_oracle(name):
+    wl = W.small_workloads()[name]()
+    print(f"case: small {name} {wl.digest()[:12]}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl)
+    _compare(wl, rels, ref)
+    assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
+
+
+@pytest.mark.parametrize("name", ["tc_uniform", "sssp", "same_generation"])
+def test_small_workload_with_forced_table_growth(name):
+    """A tiny initial table forces overflow, growth and re-run of rounds."""
+    wl = W.small_workloads()[name]()
+    print(f"case: growth {name}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"hash_min_log2": 10})
+    _compare(wl, rels, ref)
+    assert stats["table_grows"] > 0
+
+
+def test_tc_delta_sizes_are_walk_levels():
+    """Per-round |delta| of linear TC equals the number of pairs first joined at that walk length."""
+    wl = W.small_workloads()["tc_uniform"]()
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    _, stats, _ = engine_run(wl)
+    sizes = ref.sizes["path"]
+    levels = [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
+    assert stats["delta_rows"] == levels
+    assert stats["iterations"] == len(levels) - 1
+
+
+# ------------------------------------------------------------- full-size workloads
+def test_full_tc_uniform_every_row():
+    wl = W.tc_uniform()
+    print("case: full tc_uniform", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, _, _ = engine_run(wl, workspace_bytes=4 << 30)
+    _compare(wl, rels, ref)
+
+
+def test_full_sssp_sampled_sources():
+    wl = W.sssp()
+    print("case: full sssp", flush=True)
+    rels, stats, _ = engine_run(wl, workspace_bytes=8 << 30)
+    sources = wl.edb["source"][1][0]
+    pick = sources[[0, 31, 63]]
+    sub = dict(wl.edb)
+    sub["source"] = (("i32",), [pick])
+    ref = evaluate(wl.rules, sub, wl.idb)
+    got = select_rows(rels["dist"], 0, pick)
+    assert_same_relation("dist", wl.idb["dist"], got, ref.relations["dist"][1], " (sampled sources)")
+    # every source reaches every node it can reach; total rows bounded by 64 * n
+    assert len(rels["dist"][0]) <= 64 * wl.params["n_nodes"]
+    assert set(np.unique(rels["dist"][0]).tolist()) == set(sources.tolist())
+
+
+def test_full_lse_sampled_sources():
+    wl = W.layered_dag()
+    print("case: full lse_dag", flush=True)
+    rels, _, _ = engine_run(wl, workspace_bytes=8 << 30)
+    pick = wl.edb["source"][1][0][[0, 200]]
+    sub = dict(wl.edb)
+    sub["source"] = (("i32",), [pick])
+    ref = evaluate(wl.rules, sub, wl.idb)
+    got = select_rows(rels["score"], 0, pick)
+    assert_same_relation("score", wl.idb["score"], got, ref.relations["score"][1], " (sampled sources)",
+                         tol=value_tolerance(wl.rules, "score"))
+
+
+def test_full_same_generation_sampled_and_closed_form():
+    wl = W.same_generation()
+    print("case: full same_generation", flush=True)
+    rels, _, _ = engine_run(wl, workspace_bytes=8 << 30)
+    child, par = wl.edb["parent"][1]
+    depth, root = wl.params["depth"], wl.params["root"]
+    # closed form: |sg| = sum over (tree, depth) groups of n (n - 1) among non-roots
+    has_parent = np.zeros(len(depth), bool)
+    has_parent[child] = True
+    key = root[has_parent].astype(np.int64) * 64 + depth[has_parent]
+    _, cnt = np.unique(key, return_counts=True)
+    assert len(rels["sg"][0]) == int((cnt.astype(np.int64) * (cnt - 1)).sum())
+    # sampled rows: the restriction set must be closed under parent
+    parent_of = dict(zip(child.tolist(), par.tolist()))
+    rng = np.random.default_rng(0)
+    sample = set()
+    for x in rng.choice(child, 6, replace=False).tolist():
+        while x in parent_of:
+            sample.add(x)
+            x = parent_of[x]
+    allowed = np.array(sorted(sample), np.int32)
+    ref = evaluate(wl.rules, wl.edb, wl.idb, restrict={"sg": (0, allowed)})
+    got = select_rows(rels["sg"], 0, allowed)
+    assert_same_relation("sg", wl.idb["sg"], got, ref.relations["sg"][1], " (sampled nodes)")
+
+
+def test_full_tc_rmat_count_sampled_sources():
+    wl = W.tc_rmat()
+    print("case: full tc_rmat_count", flush=True)
+    rels, stats, _ = engine_run(wl, workspace_bytes=32 << 30)
+    path, rc = rels["path"], rels["reach_count"]
+    # count stratum agrees with the closure it was computed from
+    xs, cnt = np.unique(path[0], return_counts=True)
+    assert np.array_equal(rc[0], xs) and np.array_equal(rc[1], cnt.astype(np.int32))
+    src = wl.edb["edge"][1][0]
+    rng = np.random.default_rng(1)
+    pick = np.sort(rng.choice(np.unique(src), 6, replace=False)).astype(np.int32)
+    ref = evaluate(W.TC_RULES, wl.edb, {"path": ("i32", "i32")}, restrict={"path": (0, pick)})
+    assert_same_relation("path", ("i32", "i32"), select_rows(path, 0, pick), ref.relations["path"][1],
+                         " (sampled sources)")
+    assert stats["derived_tuples"] == len(path[0]) + len(rc[0])
+
+
+# ------------------------------------------------------------- edge cases and errors
+def test_empty_edb():
+    wl = W.Workload("empty", W.TC_COUNT_RULES, _edges([], []),
+                    {"path": ("i32", "i32"), "reach_count": ("i32", "i32")})
+    rels, stats, _ = engine_run(wl, workspace_bytes=256 << 20)
+    assert len(rels["path"][0]) == 0 and len(rels["reach_count"][0]) == 0
+    assert stats["iterations"] == 0
+
+
+def test_self_loop_and_duplicates():
+    wl = W.Workload("loops", W.TC_RULES, _edges([0, 0, 1, 1, 2], [0, 1, 2, 2, 0]), {"path": ("i32", "i32")})
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, _, _ = engine_run(wl, workspace_bytes=256 << 20)
+    _compare(wl, rels, ref)
+
+
+def test_negative_ids_and_wide_key_range():
+    src = np.array([-2_000_000_000, -5, 7, 1_900_000_000], np.int32)
+    dst = np.array([-5, 7, 1_900_000_000, -2_000_000_000], np.int32)
+    wl = W.Workload("wide", W.TC_RULES, _edges(src, dst), {"path": ("i32", "i32")})
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    from paper_2609_27203_amd import xlh
+    try:
+        rels, _, _ = engine_run(wl, workspace_bytes=256 << 20)
+    except xlh.XlError as e:   # the CSR index covers at most 2^30 key values
+        assert e.status_name == "XL_UNSUPPORTED"
+        return
+    _compare(wl, rels, ref)
+
+
+def test_iteration_cap_is_convergence_failure():
+    from paper_2609_27203_amd import xlh
+    n = 6
+    wl = W.Workload("chain", W.TC_RULES, _edges(np.arange(n - 1), np.arange(1, n)), {"path": ("i32", "i32")})
+    with pytest.raises(xlh.XlError) as ei:
+        engine_run(wl, workspace_bytes=256 << 20, max_iterations=1)
+    assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+
+
+def test_capacity_and_workspace_errors():
+    from paper_2609_27203_amd import xlh
+    wl = W.small_workloads()["tc_uniform"]()
+    ctx = xlh.Context(device=0, workspace_bytes=256 << 20)
+    ctx.relation("edge", ("i32", "i32"))
+    ctx.relation("path", ("i32", "i32"), max_rows=1000)
+    with pytest.raises(xlh.XlError) as ei:
+        engine_run(wl, ctx=ctx)
+    assert ei.value.status_name == "XL_CAPACITY_EXCEEDED"
+    small = xlh.Context(device=0, workspace_bytes=2 << 20)
+    small.relation("edge", ("i32", "i32"))
+    small.relation("path", ("i32", "i32"))
+    with pytest.raises(xlh.XlError) as ei:
+        engine_run(wl, ctx=small)
+    assert ei.value.status_name == "XL_RESOURCE_EXHAUSTED"
+
+
+def test_resume_from_fixpoint_is_idempotent():
+    wl = W.small_workloads()["same_generation"]()
+    rels, _, ctx = engine_run(wl)
+    ctx.relations["sg"].load(rels["sg"])
+    prog = ctx.compile(wl.rules)
+    stats = prog.run()
+    assert stats["delta_rows"][0] == 0 and stats["iterations"] == 0
+    again = ctx.relations["sg"].read()
+    assert all(np.array_equal(a, b) for a, b in zip(again, rels["sg"]))
+
+
+def test_min_resume_from_fixpoint_is_idempotent():
+    wl = W.small_workloads()["sssp"]()
+    rels, _, ctx = engine_run(wl)
+    ctx.relations["dist"].load(rels["dist"])
+    stats = ctx.compile(wl.rules).run()
+    assert stats["delta_rows"][0] == 0
+    again = ctx.relations["dist"].read()
+    assert all(np.array_equal(a.view(np.int32), b.view(np.int32)) for a, b in zip(again, rels["dist"]))
+
+
+def test_repeat_runs_are_identical():
+    for name in ("tc_rmat_count", "sssp", "lse_dag"):
+        wl = W.small_workloads()[name]()
+        a, _, ctx = engine_run(wl)
+        b, _, _ = engine_run(wl, ctx=ctx)
+        for rel in wl.idb:
+            for x, y in zip(a[rel], b[rel]):
+                assert np.array_equal(x.view(np.int32), y.view(np.int32)), (name, rel)
+
+
+def test_device_columns_round_trip():
+    import torch
+    from paper_2609_27203_amd import xlh
+    wl = W.small_workloads()["tc_uniform"]()
+    ctx = xlh.Context(device=0, workspace_bytes=512 << 20)
+    ctx.relation("edge", ("i32", "i32"))
+    ctx.relation("path", ("i32", "i32"))
+    src, dst = wl.edb["edge"][1]
+    ctx.relations["edge"].load([torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda()])
+    ctx.compile(wl.rules).run()
+    dev = ctx.relations["path"].read_device()
+    host = ctx.relations["path"].read()
+    assert all(np.array_equal(d.cpu().numpy(), h) for d, h in zip(dev, host))

@@ -1,0 +1,100 @@
+"""Host-only checks (no GPU): the C-ABI library loads and exports what the
+header declares, and the planner accepts, plans and rejects rule forms."""
+import os
+import re
+
+import pytest
+
+from paper_2609_27203_amd import workloads as W
+from paper_2609_27203_amd import xlh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "xlh.h")).read()
+    declared = set(re.findall(r"\b(xl_[a-z_]+)\s*\(", header))
+    lib = xlh.lib()
+    missing = [name for name in sorted(declared) if not hasattr(lib, name)]
+    assert not missing, missing
+    assert declared == set(xlh.EXPORTS)
+
+
+def test_status_strings():
+    lib = xlh.lib()
+    for i, name in enumerate(xlh.STATUS):
+        assert lib.xl_status_string(i).decode() == name
+
+
+def _ctx(rels):
+    c = xlh.Context(device=-1)
+    for name, types in rels.items():
+        c.relation(name, types)
+    return c
+
+
+@pytest.mark.parametrize("name", list(W.full_workloads()))
+def test_workload_programs_compile(name):
+    wl = W.small_workloads()[name]()
+    c = _ctx({**{k: t for k, (t, _) in wl.edb.items()}, **wl.idb})
+    plan = c.compile(wl.rules).explain()
+    assert "recursive" in plan
+    if name == "tc_rmat_count":
+        assert plan.index("stratum 0 recursive heads: path") < plan.index("stratum 1 non-recursive heads: reach_count[count]")
+    if name == "same_generation":   # delta variant joins parent twice, both by the parent column
+        assert "delta sg(v0,v1) -> join parent on col 1=v0 (v2,_) -> join parent on col 1=v1 (v3,_)" in plan
+
+
+def test_delta_variant_per_recursive_atom():
+    c = _ctx({"e": ("i32", "i32"), "p": ("i32", "i32"), "q": ("i32", "i32")})
+    plan = c.compile("p(X,Y) :- e(X,Y).\np(X,Y) :- q(X,Z), e(Z,Y).\nq(X,Y) :- p(X,Y).").explain()
+    assert "stratum 0 recursive heads: p[set] q[set]" in plan or "stratum 0 recursive heads: q[set] p[set]" in plan
+    assert plan.count("  delta rule") == 2
+
+
+I2 = ("i32", "i32")
+W3 = ("i32", "i32", "f32")
+
+
+@pytest.mark.parametrize("rels,text,status", [
+    ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y", "XL_PARSE_ERROR"),
+    ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y) e(Y,Z).", "XL_PARSE_ERROR"),
+    ({"e": I2, "p": I2}, "p(1,2).", "XL_PARSE_ERROR"),
+    ({"e": I2, "p": I2}, "p(X,Y) :- nope(X,Y).", "XL_INVALID_ARGUMENT"),
+    ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y,Z).", "XL_INVALID_ARGUMENT"),
+    ({"e": I2, "p": I2}, "p(X,Y,count(Z)) :- e(X,Y), e(Y,Z).", "XL_INVALID_ARGUMENT"),
+    ({"e": I2, "c": I2}, "c(X,count(Y)) :- c(X,Z), e(Z,Y).", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": I2}, "p(X,Y) :- p(X,Z), p(Z,Y).", "XL_UNSUPPORTED"),
+    ({"e": I2, "f": I2, "p": I2}, "p(X,Y) :- e(X,A), f(B,Y).", "XL_UNSUPPORTED"),
+    ({"w": W3, "p": ("f32", "i32")}, "p(W,Y) :- w(X,Y,W).", "XL_UNSUPPORTED"),
+    ({"w": W3, "p": I2}, "p(X,W) :- w(X,Y,W).", "XL_TYPE_MISMATCH"),
+    ({"w": W3, "e": I2, "p": I2}, "p(X,Y) :- w(X,Y,W), e(W,Y).", "XL_TYPE_MISMATCH"),
+    ({"w": W3, "p": W3}, "p(X,Y,logsumexp(D)) :- w(X,Y,W), D is W + 1.", "XL_TYPE_MISMATCH"),
+    ({"w": W3, "p": ("i32", "i32", "i32")}, "p(X,Y,logsumexp(Y)) :- w(X,Y,_).", "XL_TYPE_MISMATCH"),
+    ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y), Y is X + 1.", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": I2}, "p(X,Z) :- e(X,Y).", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": I2, "m": ("i32", "i32", "i32")},
+     "m(X,Y,min(Y)) :- e(X,Y).\nm(X,Y,max(Y)) :- e(Y,X).", "XL_UNSUPPORTED"),
+])
+def test_rejected_programs(rels, text, status):
+    c = _ctx(rels)
+    with pytest.raises(xlh.XlError) as ei:
+        c.compile(text)
+    assert ei.value.status_name == status, str(ei.value)
+
+
+def test_planning_context_refuses_data():
+    c = _ctx({"e": I2})
+    import numpy as np
+    with pytest.raises(xlh.XlError) as ei:
+        c.relations["e"].load([np.zeros(3, np.int32), np.ones(3, np.int32)])
+    assert ei.value.status_name == "XL_INVALID_ARGUMENT"
+
+
+def test_options():
+    c = xlh.Context(device=-1)
+    c.set_option("hash_min_log2", 12)
+    c.set_option("profile", 1)
+    for k, v in [("hash_min_log2", 3), ("nope", 1), ("profile", 7)]:
+        with pytest.raises(xlh.XlError):
+            c.set_option(k, v)
