@@ -25,6 +25,15 @@ import numpy as np
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
+DESCRIPTIONS = {
+    "tc_uniform": "transitive closure, uniform random graph (1,000 nodes, 4,000 edges, seed 1)",
+    "sssp": "multi-source shortest paths, min aggregate (100,000 nodes, 1,000,000 edges, 64 sources, seed 2)",
+    "lse_dag": "probabilistic reachability, logsumexp aggregate (20 x 5,000 layered DAG, 8 out-edges, "
+               "256 sources, seed 3)",
+    "same_generation": "same generation over a 20,000-node forest (seed 4)",
+    "tc_rmat_count": "R-MAT transitive closure + reach_count (2^14 nodes, 2^18 edges, seed 5)",
+}
+
 
 def _algorithmic_bytes(st: dict) -> float:
     """Bytes the fused join/insert kernel must move, by its definition.
@@ -61,6 +70,9 @@ def main():
     ap.add_argument("--workspace-gb", type=float, default=24.0)
     ap.add_argument("--cpu-sources", type=int, default=48)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default="tc_rmat_count",
+                    help="one of the engine's five workloads (the headline line uses tc_rmat_count)")
+    ap.add_argument("--index-mode", type=int, default=0, help="0 auto, 1 hash tables only, 2 prefer dense")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this engine "
@@ -71,9 +83,10 @@ def main():
     from paper_2609_27203_amd import workloads as W
     from paper_2609_27203_amd import xlh
 
-    wl = W.tc_rmat()
+    wl = W.full_workloads()[args.workload]()
     ctx = xlh.Context(device=0, workspace_bytes=int(args.workspace_gb * (1 << 30)))
     ctx.set_option("profile", 1)
+    ctx.set_option("index_mode", args.index_mode)
     for name, (types, cols) in wl.edb.items():
         ctx.relation(name, types).load(cols)
     for name, types in wl.idb.items():
@@ -117,12 +130,12 @@ def main():
         "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int32", "data": "synthetic",
-        "config": {"workload": "R-MAT transitive closure + reach_count (2^14 nodes, 2^18 edges, seed 5)",
+        "config": {"workload": DESCRIPTIONS[args.workload], "index_mode": args.index_mode,
                    "derived_tuples": derived, "iterations": stats[-1]["iterations"],
                    "candidates": stats[-1]["candidates_total"], "parallelism": "none (1 GPU)"},
         "roofline": roofline,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "tc_rmat_count":
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sources)
     print(json.dumps(line), flush=True)
 

@@ -77,6 +77,7 @@ enum EmitMode : int32_t {
   EM_MAT = 1,     // write bindings or (packed key, value) at scanned offsets
   EM_SET = 2,     // insert-if-absent into a key set; winners append head rows
   EM_MINMAX = 3,  // atomic improvement in a keyed table; improved keys to delta
+  EM_BITSET = 4,  // test-and-set in a dense key-domain bitmap; winners append head rows
 };
 
 // Device-side counters of one emission (cleared per round).
@@ -86,6 +87,7 @@ enum Counter : int32_t {
   CNT_OVERFLOW = 2,   // set when inserted keys pass the table's load limit
   CNT_CANDIDATES = 3, // head tuples produced by the join/project step
   CNT_FATAL = 4,      // probe sequence exhausted (must never happen)
+  CNT_SEGS = 5,       // delta segments written by the grouped expansion
   CNT_N = 8
 };
 
@@ -110,6 +112,9 @@ struct EmitSpec {
   uint32_t* row_col[2];      // head row list (key columns), written at row_base + k
   int64_t row_base;
   int64_t row_cap;
+  // EM_BITSET: bit (k0 - lo0) * row_bits + (k1 - lo1) of a dense key domain
+  uint32_t* bits;
+  unsigned long long row_bits;
   // EM_MINMAX
   Slot16* table16;
   uint32_t round;
@@ -127,6 +132,31 @@ struct StageArgs {
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];
   EmitSpec emit;
+};
+
+// Grouped delta: rows [start, start + count) of the head's row list all have
+// first key column x.  One entry per distinct x of the round's delta.
+struct SegList {
+  uint32_t* x;
+  uint32_t* start;
+  uint32_t* count;
+};
+
+// Transitive-closure-shaped recursive rule head(X, Y) :- delta(X, Z), e(Z, Y)
+// over a dense set head: the delta arrives grouped by X, each workgroup owns
+// one X, stages that X's bitmap row in LDS and merges all of its expansions.
+struct GroupedArgs {
+  SegList seg;            // this round's delta segments
+  int64_t nseg;
+  const uint32_t* dz;     // delta column holding Z (head row list, column 1)
+  IndexProbe idx;         // e indexed by the join column
+  int32_t ybind_col;      // column of e bound to Y
+  uint32_t* bits;         // dense membership bitmap of the head
+  int32_t lo0, lo1;
+  uint32_t row_words;     // bitmap row length in 32-bit words
+  uint32_t* diff;         // [nseg][row_words] new bits of this round (scratch)
+  uint32_t* seg_new;      // [nseg] number of new tuples per segment
+  unsigned long long* counters;  // CNT_CANDIDATES accumulates here
 };
 
 }  // namespace xlh

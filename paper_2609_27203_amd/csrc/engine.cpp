@@ -345,6 +345,19 @@ struct HeadRun {
   int64_t ccap = 0, cn = 0;
   uint32_t round = 0;
   int64_t preloaded = 0;
+  // dense set heads: one bit per key of the (range0 x range1) key domain,
+  // rows of row_bits bits indexed by the first key component
+  bool dense = false;
+  Buf bits;
+  u64 row_bits = 0;
+  uint32_t row_words = 0;
+  int64_t range0 = 0;
+  // grouped delta of a dense two-column head: segments per first key value
+  Buf segb[2][3];
+  int seg_cur = 0;
+  int64_t nseg = 0, nseg_next = 0;
+  bool grouped = false;
+  int round_grouped = 0, round_other = 0;
 };
 
 struct Runner {
@@ -518,6 +531,26 @@ struct Runner {
       hr->kp = kp;
       hr->bits0 = bits0;
       hr->domain = dsize;
+      if (hr->is_set && c->index_mode != 1) {
+        const Interval i0 = d[0].empty() ? Interval{0, 0} : d[0];
+        const int64_t range0 = i0.hi - i0.lo + 1;
+        int64_t range1 = 1;
+        if (hr->nkey == 2) {
+          const Interval i1 = d[1].empty() ? Interval{0, 0} : d[1];
+          range1 = i1.hi - i1.lo + 1;
+        }
+        const u64 row_bits = hr->nkey == 2 ? (u64)((range1 + 31) / 32) * 32 : 1;
+        const double total_bits = hr->nkey == 2 ? (double)range0 * (double)row_bits
+                                                : (double)((range0 + 31) / 32) * 32.0;
+        const double budget = c->index_mode == 2 ? (double)c->arena.capacity() / 2
+                                                 : std::min(4294967296.0, (double)c->arena.capacity() / 4);
+        if (total_bits / 8 <= budget) {
+          hr->dense = true;
+          hr->range0 = range0;
+          hr->row_bits = row_bits;
+          hr->row_words = (uint32_t)std::min<u64>(row_bits / 32, 0xffffffffull);
+        }
+      }
       hr->preloaded = (hr->is_set || hr->is_minmax) ? h->nrows : 0;
       XL_TRY(init_head(hr.get()));
       heads.push_back(std::move(hr));
@@ -538,8 +571,49 @@ struct Runner {
     return (int64_t)std::max<uint64_t>(cap, next_pow2((uint64_t)std::max<int64_t>(expect, 1) * 4));
   }
 
+  xl_status init_dense(HeadRun* h) {
+    Relation* r = h->rel;
+    const double total_bits = h->nkey == 2 ? (double)h->range0 * (double)h->row_bits
+                                           : (double)((h->range0 + 31) / 32) * 32.0;
+    const size_t bytes = (size_t)(total_bits / 8);
+    XL_TRY(dalloc(c, bytes, &h->bits, "dense key bitmap"));
+    HIP_TRY(c, hipMemsetAsync(h->bits.p, 0, bytes, c->stream));
+    h->rows_cap = std::max<int64_t>(((int64_t)1 << c->hash_min_log2) / 4, std::max<int64_t>(2 * h->preloaded, 1024));
+    for (int j = 0; j < h->nkey; ++j) {
+      XL_TRY(dalloc(c, (size_t)h->rows_cap * 4, &h->rows[j], "relation rows"));
+      if (h->preloaded)
+        HIP_TRY(c, hipMemcpyAsync(h->rows[j].p, r->col[j], (size_t)h->preloaded * 4,
+                                  hipMemcpyDeviceToDevice, c->stream));
+    }
+    HIP_TRY(c, k::bits_set_rows(h->bits.as<uint32_t>(), h->row_bits, h->rows[0].as<uint32_t>(),
+                                h->nkey == 2 ? h->rows[1].as<uint32_t>() : nullptr, h->preloaded, h->kp,
+                                c->stream));
+    h->nrows = h->keys = h->preloaded;
+    h->dbeg = h->dend = 0;
+    if (h->nkey == 2)
+      for (int b = 0; b < 2; ++b)
+        for (int j = 0; j < 3; ++j)
+          XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->segb[b][j], "delta segments"));
+    return XL_OK;
+  }
+
+  xl_status grow_rows(HeadRun* h, int64_t need) {
+    int64_t ncap = std::max<int64_t>(h->rows_cap * 2, need);
+    Buf nr[2];
+    for (int j = 0; j < h->nkey; ++j) {
+      XL_TRY(dalloc(c, (size_t)ncap * 4, &nr[j], "relation rows"));
+      HIP_TRY(c, hipMemcpyAsync(nr[j].p, h->rows[j].p, (size_t)h->nrows * 4, hipMemcpyDeviceToDevice,
+                                c->stream));
+    }
+    for (int j = 0; j < h->nkey; ++j) std::swap(h->rows[j].p, nr[j].p);
+    h->rows_cap = ncap;
+    st->table_grows++;
+    return XL_OK;
+  }
+
   xl_status init_head(HeadRun* h) {
     Relation* r = h->rel;
+    if (h->dense) return init_dense(h);
     h->cap = initial_cap(h->preloaded);
     XL_TRY(alloc_table(h, h->cap, &h->table));
     if (h->is_set) {
@@ -578,6 +652,7 @@ struct Runner {
 
   // Grow the head's table (and row list) so it holds at least `need` keys.
   xl_status grow(HeadRun* h, int64_t need) {
+    if (h->dense) return grow_rows(h, need);
     int64_t ncap = h->cap * 4;
     while (ncap / 2 < need || ncap - need < 64 * 4 * EMIT_GRID + 1024) ncap *= 2;
     Buf nt;
@@ -665,8 +740,125 @@ struct Runner {
     return XL_OK;
   }
 
+  // Transitive-closure-shaped variant over a dense head: grouped expansion.
+  xl_status eval_grouped(const RulePlan& p, HeadRun* h) {
+    if (!h->grouped) XL_TRY(regroup(h));
+    h->round_grouped++;
+    const int64_t nseg = h->nseg;
+    h->nseg_next = 0;
+    if (nseg == 0) return XL_OK;
+    GroupedArgs g{};
+    for (int j = 0; j < 3; ++j) (&g.seg.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
+    g.nseg = nseg;
+    g.dz = h->rows[1].as<uint32_t>();
+    XL_TRY(get_index(p.steps[0].rel, p.steps[0].key_col, &g.idx));
+    g.ybind_col = p.carried_ycol;
+    g.bits = h->bits.as<uint32_t>();
+    g.lo0 = h->kp.lo[0];
+    g.lo1 = h->kp.lo[1];
+    g.row_words = h->row_words;
+    Buf diff, segnew, segoff, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)nseg * h->row_words * 4, &diff, "grouped new-bit rows"));
+    XL_TRY(dalloc(c, (size_t)nseg * 4, &segnew, "segment counts"));
+    XL_TRY(dalloc(c, (size_t)nseg * 4, &segoff, "segment offsets"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(nseg), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    g.diff = diff.as<uint32_t>();
+    g.seg_new = segnew.as<uint32_t>();
+    g.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+    HIP_TRY(c, k::grouped_expand(g, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(segnew.as<uint32_t>(), segoff.as<uint32_t>(), nseg, tot.as<uint32_t>(),
+                                     tmp.p, c->stream));
+    uint32_t total = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &total));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    int64_t src_rows = 0;
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->emit_ms += ms;
+      st->emit_launches++;
+      st->emit_source_rows += h->dend - h->dbeg;
+      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->emit_new += total;
+    }
+    (void)src_rows;
+    if (h->nrows + (int64_t)total > h->rows_cap) XL_TRY(grow_rows(h, h->nrows + total));
+    SegList cur, next;
+    for (int j = 0; j < 3; ++j) {
+      (&cur.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
+      (&next.x)[j] = h->segb[h->seg_cur ^ 1][j].as<uint32_t>();
+    }
+    HIP_TRY(c, k::grouped_emit(cur, nseg, diff.as<uint32_t>(), h->row_words, segnew.as<uint32_t>(),
+                               segoff.as<uint32_t>(), h->kp.lo[1], h->rows[0].as<uint32_t>(),
+                               h->rows[1].as<uint32_t>(), h->nrows, next, c->dcounters + CNT_SEGS,
+                               c->stream));
+    u64 nnext = 0;
+    XL_TRY(ctl_read(c, c->dcounters + CNT_SEGS, 8, &nnext));
+    h->nseg_next = (int64_t)nnext;
+    h->nrows += total;
+    h->keys += total;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
+  // Sort the current delta of a dense two-column head by its first key and
+  // build its segment list.
+  xl_status regroup(HeadRun* h) {
+    const int64_t n = h->dend - h->dbeg;
+    h->nseg = 0;
+    h->grouped = true;
+    if (n == 0) return XL_OK;
+    uint32_t* r0 = h->rows[0].as<uint32_t>() + h->dbeg;
+    uint32_t* r1 = h->rows[1].as<uint32_t>() + h->dbeg;
+    Buf ka, kb, va, vb, tmp;
+    XL_TRY(dalloc(c, (size_t)n * 4, &ka, "regroup keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &kb, "regroup keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &vb, "regroup values"));
+    XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
+    HIP_TRY(c, k::sub_lo(r0, h->kp.lo[0], ka.as<uint32_t>(), n, c->stream));
+    int alt = 0;
+    HIP_TRY(c, k::radix_sort_u32(ka.as<uint32_t>(), r1, kb.as<uint32_t>(), vb.as<uint32_t>(), n, h->bits0,
+                                 tmp.p, c->stream, &alt));
+    if (alt) {
+      HIP_TRY(c, k::add_u32(kb.as<uint32_t>(), (uint32_t)h->kp.lo[0], r0, n, c->stream));
+      HIP_TRY(c, hipMemcpyAsync(r1, vb.p, (size_t)n * 4, hipMemcpyDeviceToDevice, c->stream));
+    } else {
+      HIP_TRY(c, k::add_u32(ka.as<uint32_t>(), (uint32_t)h->kp.lo[0], r0, n, c->stream));
+    }
+    Buf flag, pos, tot, starts;
+    XL_TRY(dalloc(c, (size_t)n * 4, &flag, "segment flags"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &pos, "segment ids"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    tmp.reset();
+    XL_TRY(dalloc(c, k::scan_temp_bytes(n), &tmp, "scan scratch"));
+    const uint32_t* cols[1] = {r0};
+    HIP_TRY(c, k::row_change_flags(cols, 1, n, flag.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), n, tot.as<uint32_t>(), tmp.p,
+                                     c->stream));
+    uint32_t nseg = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &nseg));
+    XL_TRY(dalloc(c, (size_t)nseg * 4, &starts, "segment starts"));
+    HIP_TRY(c, k::seg_starts(flag.as<uint32_t>(), pos.as<uint32_t>(), n, starts.as<uint32_t>(), c->stream));
+    SegList out;
+    for (int j = 0; j < 3; ++j) (&out.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
+    HIP_TRY(c, k::seg_fill(starts.as<uint32_t>(), nseg, n, r0, h->dbeg, out, c->stream));
+    h->nseg = nseg;
+    return XL_OK;
+  }
+
   xl_status eval_plan(const RulePlan& p) {
     HeadRun* h = head_of(p.head);
+    if (h->dense && p.carried && h->nkey == 2 && p.driver_delta && h->row_words <= 4096)
+      return eval_grouped(p, h);
+    if (h->dense) h->round_other++;
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
@@ -769,6 +961,22 @@ struct Runner {
         // limit is crossed, so the limit leaves room for all of them: the
         // table can never fill and the row list never overflows.
         const int64_t waves = std::min<int64_t>((a.src.n + 63) / 64, (int64_t)EMIT_GRID * 4);
+        if (h->dense) {
+          const int64_t max_rows = h->rows_cap - 64 * waves - 1024;
+          if (h->nrows >= max_rows) {
+            XL_TRY(grow_rows(h, h->nrows + 2 * (64 * waves + 1024)));
+            continue;
+          }
+          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+          a.emit.limit = (u64)(max_rows - h->nrows);
+          a.emit.mode = EM_BITSET;
+          a.emit.bits = h->bits.as<uint32_t>();
+          a.emit.row_bits = h->row_bits;
+          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
+          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
+          a.emit.row_base = h->nrows;
+          a.emit.row_cap = h->rows_cap;
+        } else {
         const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - 64 * waves - 1024);
         if (h->keys >= max_keys) {
           XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + 64 * waves + 1024)));
@@ -777,7 +985,10 @@ struct Runner {
         HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
         a.emit.limit = (u64)(max_keys - h->keys);
         a.emit.mask = (u64)h->cap - 1;
-        if (h->is_set) {
+        }
+        if (h->dense) {
+          // EM_BITSET configured above
+        } else if (h->is_set) {
           a.emit.mode = EM_SET;
           a.emit.table = h->table.as<u64>();
           a.emit.row_col[0] = h->rows[0].as<uint32_t>();
@@ -819,7 +1030,7 @@ struct Runner {
           return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                    std::to_string(h->rel->max_rows));
         if (!cnt[CNT_OVERFLOW]) break;
-        XL_TRY(grow(h, h->keys * 2 + 1));
+        XL_TRY(grow(h, h->dense ? h->nrows + 2 * (64 * waves + 1024) : h->keys * 2 + 1));
         if (h->is_minmax) {  // slot indices moved: rebuild this round's delta list
           HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
           HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(),
@@ -842,6 +1053,7 @@ struct Runner {
   }
 
   void begin_round(HeadRun* h) {
+    h->round_grouped = h->round_other = 0;
     h->round++;
     h->round_begin = h->nrows;
     h->didx_n = 0;
@@ -853,6 +1065,18 @@ struct Runner {
       h->dbeg = h->round_begin;
       h->dend = h->nrows;
       *delta = h->dend - h->dbeg;
+      if (h->dense && h->nkey == 2) {
+        if (*delta == 0) {
+          h->grouped = true;
+          h->nseg = 0;
+        } else if (h->round_grouped == 1 && h->round_other == 0) {
+          h->seg_cur ^= 1;  // the grouped expansion wrote this delta's segments
+          h->nseg = h->nseg_next;
+          h->grouped = true;
+        } else {
+          h->grouped = false;
+        }
+      }
       return XL_OK;
     }
     if (h->is_minmax) {

@@ -133,6 +133,10 @@ struct RulePlan {
   // column -> (var slot or -1 for an is-result) binding source, for domains
   std::vector<std::pair<Relation*, int>> var_sources[MAXV];
   bool var_is_arith[MAXV] = {};
+  // head(X, Y) :- delta head(X, Z), e(Z, Y) with nothing else: the first key
+  // passes through from the delta, so the delta can be processed grouped by X.
+  bool carried = false;
+  int carried_ycol = -1;  // column of e bound to Y
 };
 
 struct HeadInfo {

@@ -469,6 +469,23 @@ struct Planner {
         if (kv.second <= k && used.count(slot[kv.first])) p.live_after[k].push_back(slot[kv.first]);
       std::sort(p.live_after[k].begin(), p.live_after[k].end());
     }
+    // transitive-closure shape (see RulePlan::carried)
+    if (delta && p.driver == p.head && p.head->arity == 2 && r.agg == Agg::NONE && nst == 1 &&
+        p.stage_ops[0].empty() && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
+        p.driver_act[0].slot != p.driver_act[1].slot && p.steps[0].key_slot == p.driver_act[1].slot &&
+        p.key_slot[0] == p.driver_act[0].slot) {
+      int ycol = -1, nbind = 0, nother = 0;
+      for (int j = 0; j < p.steps[0].rel->arity; ++j) {
+        if (j == p.steps[0].key_col) continue;
+        if (p.steps[0].act[j].kind == CA_BIND) { ++nbind; ycol = j; }
+        else if (p.steps[0].act[j].kind != CA_NONE) ++nother;
+      }
+      if (nbind == 1 && nother == 0 && p.steps[0].act[ycol].slot == p.key_slot[1] &&
+          p.steps[0].rel->types[ycol] == T_I32) {
+        p.carried = true;
+        p.carried_ycol = ycol;
+      }
+    }
     *out = p;
     return true;
   }
@@ -646,6 +663,7 @@ std::string explain_program(const Program* p) {
         if (rp.nkey == 2) os << ",v" << rp.key_slot[1];
         os << ")";
         if (rp.val_slot >= 0) os << " val v" << rp.val_slot;
+        if (rp.carried) os << " [grouped by v" << rp.key_slot[0] << "]";
         os << "\n";
       }
     }

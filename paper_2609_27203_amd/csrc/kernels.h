@@ -84,6 +84,19 @@ hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1
                      const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
                      unsigned long long* counters, hipStream_t s);
 
+// ---- dense set heads ----
+hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const uint32_t* c1,
+                         int64_t n, KeyPack kp, hipStream_t s);
+hipError_t grouped_expand(const GroupedArgs& a, hipStream_t s);
+hipError_t grouped_emit(SegList cur, int64_t nseg, const uint32_t* diff, uint32_t row_words,
+                        const uint32_t* seg_new, const uint32_t* seg_off, int32_t lo1,
+                        uint32_t* rows0, uint32_t* rows1, int64_t row_base, SegList next,
+                        unsigned long long* seg_counter, hipStream_t s);
+hipError_t seg_fill(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
+                    int64_t row_base, SegList out, hipStream_t s);
+// out[i] = in[i] + add
+hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s);
+
 enum FoldKind { FOLD_NONE = 0, FOLD_COUNT, FOLD_SUM, FOLD_MIN, FOLD_MAX, FOLD_LSE };
 
 }  // namespace k

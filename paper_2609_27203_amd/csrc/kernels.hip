@@ -764,13 +764,25 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     st.running += (uint32_t)__popcll(m);
     return;
   }
-  // EM_SET / EM_MINMAX: stop early once the table passed its load limit.
+  // EM_SET / EM_BITSET / EM_MINMAX: stop early once the load limit is passed.
   st.cands += (uint32_t)__popcll(__ballot(act));
   if (st.stop) return;
-  if (MODE == EM_SET) {
+  if (MODE == EM_SET || MODE == EM_BITSET) {
     int ins = 0;
-    if (act) ins = set_insert(e.table, e.mask, pack_key(e.key, getv(u, e.key.slot[0]),
-                                                       getv(u, e.key.slot[1])), e.counters);
+    if (act) {
+      const u64 key = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
+      if (MODE == EM_SET) {
+        ins = set_insert(e.table, e.mask, key, e.counters);
+      } else {
+        // dense domain: the packed key's two components index row and column
+        const u64 b = e.key.nkey == 2
+                          ? (key >> e.key.shift) * e.row_bits + (key & ((1ull << e.key.shift) - 1ull))
+                          : key;
+        uint32_t* wp = e.bits + (b >> 5);
+        const uint32_t bit = 1u << (b & 31);
+        if (!(*wp & bit)) ins = (atomicOr(wp, bit) & bit) == 0;
+      }
+    }
     const u64 m = __ballot(ins);
     if (m) {
       const int leader = __ffsll((long long)m) - 1;
@@ -847,7 +859,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     st.running = 0;
     st.cands = 0;
     st.out_base = (MODE == EM_MAT) ? a.emit.chunk_off[chunk] + (u64)a.emit.mat_base : 0;
-    if (MODE == EM_SET || MODE == EM_MINMAX) {
+    if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX) {
       if (!st.stop) st.stop = atomic_load_agent(&a.emit.counters[CNT_OVERFLOW]) != 0;
     }
     const int64_t row = chunk * 64 + lane;
@@ -894,7 +906,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
       emit<MODE>(a, v, act, st);
     }
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
-    if ((MODE == EM_SET || MODE == EM_MINMAX) && lane == 0 && st.cands)
+    if ((MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX) && lane == 0 && st.cands)
       atomicAdd(&a.emit.counters[CNT_CANDIDATES], (u64)st.cands);
   }
 }
@@ -913,6 +925,7 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
     case EM_COUNT: launch_mode<EM_COUNT>(a, grid, s); break;
     case EM_MAT: launch_mode<EM_MAT>(a, grid, s); break;
     case EM_SET: launch_mode<EM_SET>(a, grid, s); break;
+    case EM_BITSET: launch_mode<EM_BITSET>(a, grid, s); break;
     default: launch_mode<EM_MINMAX>(a, grid, s); break;
   }
   return hipGetLastError();
@@ -1037,6 +1050,217 @@ hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1
   if (n <= 0) return hipSuccess;
   agg_merge_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(t, mask, k0, k1, v, n, kp, type, fold_kind,
                                                      counters);
+  return hipGetLastError();
+}
+
+// ============================================================ dense set heads
+__global__ void bits_set_rows_k(uint32_t* bits, u64 row_bits, const uint32_t* c0,
+                                const uint32_t* c1, int64_t n, KeyPack kp) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const u64 key = pack_key(kp, c0[i], c1 ? c1[i] : 0u);
+    const u64 b = kp.nkey == 2 ? (key >> kp.shift) * row_bits + (key & ((1ull << kp.shift) - 1ull))
+                               : key;
+    atomicOr(&bits[b >> 5], 1u << (b & 31));
+  }
+}
+hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const uint32_t* c1,
+                         int64_t n, KeyPack kp, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  bits_set_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(bits, row_bits, c0, c1, n, kp);
+  return hipGetLastError();
+}
+
+// Grouped expansion, phase 1.  One workgroup per delta segment (one first-key
+// value x).  The workgroup copies bitmap row x into LDS twice (before / after),
+// expands every delta row (x, z) of the segment through the index of e --
+// wave-balanced exactly like the generic stage kernel -- and sets the bit of
+// each produced y in the LDS row with an LDS atomic (after a plain test, since
+// most candidates are already known).  It then writes back the changed words
+// of row x, the per-word difference to a scratch row, and the segment's count
+// of new tuples.  A row is owned by exactly one workgroup per round, so the
+// global bitmap needs no atomics here.
+constexpr int GR_THREADS = 256;
+constexpr int GR_WAVES = GR_THREADS / 64;
+
+__global__ __launch_bounds__(GR_THREADS) void grouped_expand_k(GroupedArgs a) {
+  extern __shared__ uint32_t lds[];
+  uint32_t* old_row = lds;
+  uint32_t* new_row = lds + a.row_words;
+  __shared__ uint32_t s_excl[GR_WAVES][64];
+  __shared__ uint32_t s_beg[GR_WAVES][64];
+  __shared__ uint32_t s_red[GR_WAVES];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t W = a.row_words;
+  for (int64_t sg = blockIdx.x; sg < a.nseg; sg += gridDim.x) {
+    const uint32_t x = a.seg.x[sg];
+    const uint32_t start = a.seg.start[sg];
+    const uint32_t cnt = a.seg.count[sg];
+    uint32_t* grow = a.bits + (u64)(x - (uint32_t)a.lo0) * W;
+    for (uint32_t i = threadIdx.x; i < W; i += GR_THREADS) {
+      const uint32_t v = grow[i];
+      old_row[i] = v;
+      new_row[i] = v;
+    }
+    __syncthreads();
+    uint32_t cands = 0;
+    for (uint32_t base_row = (uint32_t)w * 64; base_row < cnt; base_row += GR_WAVES * 64) {
+      const uint32_t r = base_row + lane;
+      uint32_t beg = 0, deg = 0;
+      if (r < cnt) {
+        const uint32_t kk = a.dz[start + r] - (uint32_t)a.idx.key_lo;
+        if (kk < a.idx.key_range) {
+          beg = a.idx.off[kk];
+          deg = a.idx.off[kk + 1] - beg;
+        }
+      }
+      const uint32_t incl = wave_incl_scan(deg);
+      const uint32_t total = __shfl(incl, 63, 64);
+      s_excl[w][lane] = incl - deg;
+      s_beg[w][lane] = beg;
+      wave_lds_sync();
+      cands += total;
+      const uint32_t* ycol = a.idx.col[a.ybind_col];
+      for (uint32_t b0 = 0; b0 < total; b0 += 64) {
+        const uint32_t j = b0 + lane;
+        if (j < total) {
+          int q = 0;
+#pragma unroll
+          for (int step = 32; step > 0; step >>= 1)
+            if (s_excl[w][q + step] <= j) q += step;
+          const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
+          const uint32_t bit = 1u << (y & 31);
+          if (!(new_row[y >> 5] & bit)) atomicOr(&new_row[y >> 5], bit);
+        }
+      }
+      wave_lds_sync();
+    }
+    __syncthreads();
+    uint32_t nnew = 0;
+    uint32_t* drow = a.diff + (u64)sg * W;
+    for (uint32_t i = threadIdx.x; i < W; i += GR_THREADS) {
+      const uint32_t nv = new_row[i];
+      const uint32_t d = nv & ~old_row[i];
+      drow[i] = d;
+      if (d) {
+        grow[i] = nv;
+        nnew += __popc(d);
+      }
+    }
+    for (int d = 32; d > 0; d >>= 1) nnew += __shfl_xor(nnew, d, 64);
+    for (int d = 32; d > 0; d >>= 1) cands += __shfl_xor(cands, d, 64);
+    if (lane == 0) {
+      s_red[w] = nnew;
+      if (cands) atomicAdd(&a.counters[CNT_CANDIDATES], (u64)(cands / 64));
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t t = 0;
+      for (int i = 0; i < GR_WAVES; ++i) t += s_red[i];
+      a.seg_new[sg] = t;
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t grouped_expand(const GroupedArgs& a, hipStream_t s) {
+  if (a.nseg <= 0) return hipSuccess;
+  const size_t lds = (size_t)a.row_words * 2 * sizeof(uint32_t);
+  const unsigned grid = (unsigned)std::min<int64_t>(a.nseg, 1 << 20);
+  grouped_expand_k<<<grid, GR_THREADS, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+// Grouped expansion, phase 2: write each segment's new tuples (x, y) in
+// ascending y at its scanned offset and record the segment for the next round.
+__global__ __launch_bounds__(GR_THREADS) void grouped_emit_k(SegList cur, int64_t nseg,
+                                                             const uint32_t* diff, uint32_t row_words,
+                                                             const uint32_t* seg_new,
+                                                             const uint32_t* seg_off, int32_t lo1,
+                                                             uint32_t* rows0, uint32_t* rows1,
+                                                             int64_t row_base, SegList next,
+                                                             u64* seg_counter) {
+  __shared__ uint32_t s_w[GR_WAVES];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  for (int64_t sg = blockIdx.x; sg < nseg; sg += gridDim.x) {
+    const uint32_t t = seg_new[sg];
+    if (t == 0) continue;
+    const uint32_t x = cur.x[sg];
+    const u64 out0 = (u64)row_base + seg_off[sg];
+    const uint32_t* drow = diff + (u64)sg * row_words;
+    uint32_t running = 0;
+    for (uint32_t base = 0; base < row_words; base += GR_THREADS) {
+      const uint32_t i = base + threadIdx.x;
+      const uint32_t d = i < row_words ? drow[i] : 0u;
+      const uint32_t c = __popc(d);
+      const uint32_t incl = wave_incl_scan(c);
+      if (lane == 63) s_w[w] = incl;
+      __syncthreads();
+      uint32_t pre = 0, tot = 0;
+      for (int k = 0; k < GR_WAVES; ++k) {
+        if (k < w) pre += s_w[k];
+        tot += s_w[k];
+      }
+      uint32_t pos = running + pre + incl - c;
+      uint32_t bits = d;
+      while (bits) {
+        const int b = __ffs(bits) - 1;
+        bits &= bits - 1;
+        rows0[out0 + pos] = x;
+        rows1[out0 + pos] = (uint32_t)lo1 + i * 32u + (uint32_t)b;
+        ++pos;
+      }
+      running += tot;
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      const u64 k = atomicAdd(seg_counter, 1ull);
+      next.x[k] = x;
+      next.start[k] = (uint32_t)out0;
+      next.count[k] = t;
+    }
+  }
+}
+
+hipError_t grouped_emit(SegList cur, int64_t nseg, const uint32_t* diff, uint32_t row_words,
+                        const uint32_t* seg_new, const uint32_t* seg_off, int32_t lo1,
+                        uint32_t* rows0, uint32_t* rows1, int64_t row_base, SegList next,
+                        unsigned long long* seg_counter, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>(nseg, 1 << 20);
+  grouped_emit_k<<<grid, GR_THREADS, 0, s>>>(cur, nseg, diff, row_words, seg_new, seg_off, lo1, rows0,
+                                             rows1, row_base, next, seg_counter);
+  return hipGetLastError();
+}
+
+// Segments of a delta sorted by its first key column: starts come from the
+// change flags; x and count are filled here.
+__global__ void seg_fill_k(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
+                           int64_t row_base, SegList out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nseg;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t b = starts[i];
+    const uint32_t e = i + 1 < nseg ? starts[i + 1] : (uint32_t)n;
+    out.x[i] = xcol[b];
+    out.start[i] = (uint32_t)(row_base + b);
+    out.count[i] = e - b;
+  }
+}
+hipError_t seg_fill(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
+                    int64_t row_base, SegList out, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  seg_fill_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(starts, nseg, n, xcol, row_base, out);
+  return hipGetLastError();
+}
+
+__global__ void add_u32_k(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = in[i] + add;
+}
+hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  add_u32_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(in, add, out, n);
   return hipGetLastError();
 }
 

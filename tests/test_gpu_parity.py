@@ -53,23 +53,26 @@ def test_listing_agg_degree():
 
 
 # ------------------------------------------------------------- small workloads, every row
+@pytest.mark.parametrize("index_mode", [0, 1])
 @pytest.mark.parametrize("name", list(W.small_workloads()))
-def test_small_workload_matches_oracle(name):
+def test_small_workload_matches_oracle(name, index_mode):
+    """index_mode 0 picks dense bitmaps for small set domains, 1 forces hash tables."""
     wl = W.small_workloads()[name]()
-    print(f"case: small {name} {wl.digest()[:12]}", flush=True)
+    print(f"case: small {name} index_mode={index_mode} {wl.digest()[:12]}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, stats, _ = engine_run(wl)
+    rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
     _compare(wl, rels, ref)
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
-@pytest.mark.parametrize("name", ["tc_uniform", "sssp", "same_generation"])
-def test_small_workload_with_forced_table_growth(name):
-    """A tiny initial table forces overflow, growth and re-run of rounds."""
+@pytest.mark.parametrize("index_mode", [0, 1])
+@pytest.mark.parametrize("name", ["tc_uniform", "sssp", "same_generation", "tc_rmat_count"])
+def test_small_workload_with_forced_table_growth(name, index_mode):
+    """A tiny initial table / row list forces overflow, growth and re-run of rounds."""
     wl = W.small_workloads()[name]()
-    print(f"case: growth {name}", flush=True)
+    print(f"case: growth {name} index_mode={index_mode}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, stats, _ = engine_run(wl, options={"hash_min_log2": 10})
+    rels, stats, _ = engine_run(wl, options={"hash_min_log2": 10, "index_mode": index_mode})
     _compare(wl, rels, ref)
     assert stats["table_grows"] > 0
 
