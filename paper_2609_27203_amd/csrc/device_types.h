@@ -78,6 +78,7 @@ enum EmitMode : int32_t {
   EM_SET = 2,     // insert-if-absent into a key set; winners append head rows
   EM_MINMAX = 3,  // atomic improvement in a keyed table; improved keys to delta
   EM_BITSET = 4,  // test-and-set in a dense key-domain bitmap; winners append head rows
+  EM_DCOUNT = 5,  // count per key in a dense counter array (runs of equal keys combined)
 };
 
 // Device-side counters of one emission (cleared per round).
@@ -113,6 +114,7 @@ struct EmitSpec {
   int64_t row_base;
   int64_t row_cap;
   // EM_BITSET: bit (k0 - lo0) * row_bits + (k1 - lo1) of a dense key domain
+  // EM_DCOUNT: counter of the same index, with row_bits = the second key's range
   uint32_t* bits;
   unsigned long long row_bits;
   // EM_MINMAX
@@ -134,29 +136,25 @@ struct StageArgs {
   EmitSpec emit;
 };
 
-// Grouped delta: rows [start, start + count) of the head's row list all have
-// first key column x.  One entry per distinct x of the round's delta.
-struct SegList {
-  uint32_t* x;
-  uint32_t* start;
-  uint32_t* count;
-};
-
-// Transitive-closure-shaped recursive rule head(X, Y) :- delta(X, Z), e(Z, Y)
-// over a dense set head: the delta arrives grouped by X, each workgroup owns
-// one X, stages that X's bitmap row in LDS and merges all of its expansions.
-struct GroupedArgs {
-  SegList seg;            // this round's delta segments
+// Closure-shaped recursive rule head(X, Y) :- delta head(X, Z), e(Z, Y) over a
+// dense set head, run in frontier form: the delta of every first-key value x
+// is a bitmap row holding the Z values that became true in the previous
+// round.  One workgroup owns one x per round: it stages bitmap row x in LDS,
+// expands every Z of x's delta row through the index of e, merges the
+// produced Y values with LDS atomics and writes the next delta row.
+struct FrontierArgs {
+  const uint32_t* x;        // [nseg] first-key value of delta row sg (fixed after the seed)
+  const uint32_t* in_cnt;   // [nseg] bits in delta row sg (0: skip)
+  const uint32_t* in_diff;  // [nseg][row_words] delta bits
   int64_t nseg;
-  const uint32_t* dz;     // delta column holding Z (head row list, column 1)
-  IndexProbe idx;         // e indexed by the join column
-  int32_t ybind_col;      // column of e bound to Y
-  uint32_t* bits;         // dense membership bitmap of the head
+  IndexProbe idx;           // e indexed by its join column
+  int32_t ybind_col;        // column of e bound to Y
+  uint32_t* bits;           // dense membership bitmap of the head
   int32_t lo0, lo1;
-  uint32_t row_words;     // bitmap row length in 32-bit words
-  uint32_t* diff;         // [nseg][row_words] new bits of this round (scratch)
-  uint32_t* seg_new;      // [nseg] number of new tuples per segment
-  unsigned long long* counters;  // CNT_CANDIDATES accumulates here
+  uint32_t row_words;
+  uint32_t* out_cnt;        // next delta: counts and bitmap rows, same slots
+  uint32_t* out_diff;
+  unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED (= new tuples)
 };
 
 }  // namespace xlh

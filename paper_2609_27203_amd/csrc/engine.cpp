@@ -352,12 +352,19 @@ struct HeadRun {
   u64 row_bits = 0;
   uint32_t row_words = 0;
   int64_t range0 = 0;
-  // grouped delta of a dense two-column head: segments per first key value
-  Buf segb[2][3];
-  int seg_cur = 0;
-  int64_t nseg = 0, nseg_next = 0;
-  bool grouped = false;
-  int round_grouped = 0, round_other = 0;
+  // frontier form (closure-shaped stratum over a dense two-column head): the
+  // delta is one bitmap row per first-key value that gained tuples
+  bool frontier = false;
+  bool frontier_ready = false;  // the current delta is in fcnt/fdiff[fcur]
+  Buf fx, fcnt[2], fdiff[2];    // delta row slot sg belongs to first-key value fx[sg]
+  int fcur = 0;
+  int64_t fn = 0, fnew = 0;
+  // dense count heads: one counter per key of the domain
+  bool dcount = false;
+  Buf counts;
+  int64_t range1 = 1;
+  // key-column domains (bounds recorded on the materialized relation)
+  int64_t dom_lo[2] = {0, 0}, dom_hi[2] = {0, 0};
 };
 
 struct Runner {
@@ -531,6 +538,20 @@ struct Runner {
       hr->kp = kp;
       hr->bits0 = bits0;
       hr->domain = dsize;
+      for (int j = 0; j < hr->nkey; ++j) {
+        const Interval iv = d[j].empty() ? Interval{0, 0} : d[j];
+        hr->dom_lo[j] = iv.lo;
+        hr->dom_hi[j] = iv.hi;
+      }
+      if (hr->agg == Agg::COUNT && c->index_mode != 1) {
+        const int64_t r0 = hr->dom_hi[0] - hr->dom_lo[0] + 1;
+        const int64_t r1 = hr->nkey == 2 ? hr->dom_hi[1] - hr->dom_lo[1] + 1 : 1;
+        if ((double)r0 * (double)r1 * 4 <= std::min(4294967296.0, (double)c->arena.capacity() / 8)) {
+          hr->dcount = true;
+          hr->range0 = r0;
+          hr->range1 = r1;
+        }
+      }
       if (hr->is_set && c->index_mode != 1) {
         const Interval i0 = d[0].empty() ? Interval{0, 0} : d[0];
         const int64_t range0 = i0.hi - i0.lo + 1;
@@ -549,6 +570,10 @@ struct Runner {
           hr->range0 = range0;
           hr->row_bits = row_bits;
           hr->row_words = (uint32_t)std::min<u64>(row_bits / 32, 0xffffffffull);
+          // frontier form: the stratum is this head alone with one closure-shaped variant
+          hr->frontier = s.recursive && s.heads.size() == 1 && s.variants.size() == 1 &&
+                         s.variants[0].carried && hr->nkey == 2 && hr->row_words <= 4096 &&
+                         total_bits / 8 * 3 <= budget;
         }
       }
       hr->preloaded = (hr->is_set || hr->is_minmax) ? h->nrows : 0;
@@ -590,10 +615,21 @@ struct Runner {
                                 c->stream));
     h->nrows = h->keys = h->preloaded;
     h->dbeg = h->dend = 0;
-    if (h->nkey == 2)
-      for (int b = 0; b < 2; ++b)
-        for (int j = 0; j < 3; ++j)
-          XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->segb[b][j], "delta segments"));
+    if (h->frontier) {
+      XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->fx, "delta row keys"));
+      for (int b = 0; b < 2; ++b) {
+        XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->fcnt[b], "delta row counts"));
+        XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * h->row_words * 4, &h->fdiff[b],
+                      "delta bitmap rows"));
+      }
+    }
+    return XL_OK;
+  }
+
+  xl_status init_dcount(HeadRun* h) {
+    const size_t bytes = (size_t)h->range0 * (size_t)h->range1 * 4;
+    XL_TRY(dalloc(c, bytes, &h->counts, "dense counters"));
+    HIP_TRY(c, hipMemsetAsync(h->counts.p, 0, bytes, c->stream));
     return XL_OK;
   }
 
@@ -614,6 +650,7 @@ struct Runner {
   xl_status init_head(HeadRun* h) {
     Relation* r = h->rel;
     if (h->dense) return init_dense(h);
+    if (h->dcount) return init_dcount(h);
     h->cap = initial_cap(h->preloaded);
     XL_TRY(alloc_table(h, h->cap, &h->table));
     if (h->is_set) {
@@ -740,85 +777,58 @@ struct Runner {
     return XL_OK;
   }
 
-  // Transitive-closure-shaped variant over a dense head: grouped expansion.
-  xl_status eval_grouped(const RulePlan& p, HeadRun* h) {
-    if (!h->grouped) XL_TRY(regroup(h));
-    h->round_grouped++;
-    const int64_t nseg = h->nseg;
-    h->nseg_next = 0;
-    if (nseg == 0) return XL_OK;
-    GroupedArgs g{};
-    for (int j = 0; j < 3; ++j) (&g.seg.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
-    g.nseg = nseg;
-    g.dz = h->rows[1].as<uint32_t>();
-    XL_TRY(get_index(p.steps[0].rel, p.steps[0].key_col, &g.idx));
-    g.ybind_col = p.carried_ycol;
-    g.bits = h->bits.as<uint32_t>();
-    g.lo0 = h->kp.lo[0];
-    g.lo1 = h->kp.lo[1];
-    g.row_words = h->row_words;
-    Buf diff, segnew, segoff, tmp, tot;
-    XL_TRY(dalloc(c, (size_t)nseg * h->row_words * 4, &diff, "grouped new-bit rows"));
-    XL_TRY(dalloc(c, (size_t)nseg * 4, &segnew, "segment counts"));
-    XL_TRY(dalloc(c, (size_t)nseg * 4, &segoff, "segment offsets"));
-    XL_TRY(dalloc(c, k::scan_temp_bytes(nseg), &tmp, "scan scratch"));
-    XL_TRY(dalloc(c, 8, &tot, "count"));
-    g.diff = diff.as<uint32_t>();
-    g.seg_new = segnew.as<uint32_t>();
-    g.counters = c->dcounters;
+  // One round of the closure-shaped variant in frontier form.
+  xl_status eval_frontier(const RulePlan& p, HeadRun* h) {
+    h->fnew = 0;
+    if (h->fn == 0) return XL_OK;
+    FrontierArgs f{};
+    f.x = h->fx.as<uint32_t>();
+    f.in_cnt = h->fcnt[h->fcur].as<uint32_t>();
+    f.in_diff = h->fdiff[h->fcur].as<uint32_t>();
+    f.nseg = h->fn;
+    XL_TRY(get_index(p.steps[0].rel, p.steps[0].key_col, &f.idx));
+    f.ybind_col = p.carried_ycol;
+    f.bits = h->bits.as<uint32_t>();
+    f.lo0 = h->kp.lo[0];
+    f.lo1 = h->kp.lo[1];
+    f.row_words = h->row_words;
+    f.out_cnt = h->fcnt[h->fcur ^ 1].as<uint32_t>();
+    f.out_diff = h->fdiff[h->fcur ^ 1].as<uint32_t>();
+    f.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
-    HIP_TRY(c, k::grouped_expand(g, c->stream));
+    HIP_TRY(c, k::frontier_round(f, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
-    HIP_TRY(c, k::scan_exclusive_u32(segnew.as<uint32_t>(), segoff.as<uint32_t>(), nseg, tot.as<uint32_t>(),
-                                     tmp.p, c->stream));
-    uint32_t total = 0;
-    XL_TRY(ctl_read(c, tot.p, 4, &total));
     u64 cnt[CNT_N];
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
-    int64_t src_rows = 0;
     cands += (int64_t)cnt[CNT_CANDIDATES];
     if (c->profile) {
       float ms = 0;
       HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
       st->emit_ms += ms;
       st->emit_launches++;
-      st->emit_source_rows += h->dend - h->dbeg;
+      st->emit_source_rows += h->fn;
       st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
-      st->emit_new += total;
+      st->emit_new += (int64_t)cnt[CNT_APPENDED];
     }
-    (void)src_rows;
-    if (h->nrows + (int64_t)total > h->rows_cap) XL_TRY(grow_rows(h, h->nrows + total));
-    SegList cur, next;
-    for (int j = 0; j < 3; ++j) {
-      (&cur.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
-      (&next.x)[j] = h->segb[h->seg_cur ^ 1][j].as<uint32_t>();
-    }
-    HIP_TRY(c, k::grouped_emit(cur, nseg, diff.as<uint32_t>(), h->row_words, segnew.as<uint32_t>(),
-                               segoff.as<uint32_t>(), h->kp.lo[1], h->rows[0].as<uint32_t>(),
-                               h->rows[1].as<uint32_t>(), h->nrows, next, c->dcounters + CNT_SEGS,
-                               c->stream));
-    u64 nnext = 0;
-    XL_TRY(ctl_read(c, c->dcounters + CNT_SEGS, 8, &nnext));
-    h->nseg_next = (int64_t)nnext;
-    h->nrows += total;
-    h->keys += total;
+    h->fnew = (int64_t)cnt[CNT_APPENDED];
+    h->keys += h->fnew;
     if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
       return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                std::to_string(h->rel->max_rows));
     return XL_OK;
   }
 
-  // Sort the current delta of a dense two-column head by its first key and
-  // build its segment list.
-  xl_status regroup(HeadRun* h) {
+  // Turn the row-list delta [dbeg, dend) of a frontier head into delta bitmap
+  // rows: sort by the first key, one delta row per distinct value.
+  xl_status frontier_from_rows(HeadRun* h) {
     const int64_t n = h->dend - h->dbeg;
-    h->nseg = 0;
-    h->grouped = true;
+    h->fn = 0;
+    h->frontier_ready = true;
     if (n == 0) return XL_OK;
     uint32_t* r0 = h->rows[0].as<uint32_t>() + h->dbeg;
     uint32_t* r1 = h->rows[1].as<uint32_t>() + h->dbeg;
-    Buf ka, kb, va, vb, tmp;
+    Buf ka, kb, vb, tmp;
     XL_TRY(dalloc(c, (size_t)n * 4, &ka, "regroup keys"));
     XL_TRY(dalloc(c, (size_t)n * 4, &kb, "regroup keys"));
     XL_TRY(dalloc(c, (size_t)n * 4, &vb, "regroup values"));
@@ -827,12 +837,9 @@ struct Runner {
     int alt = 0;
     HIP_TRY(c, k::radix_sort_u32(ka.as<uint32_t>(), r1, kb.as<uint32_t>(), vb.as<uint32_t>(), n, h->bits0,
                                  tmp.p, c->stream, &alt));
-    if (alt) {
-      HIP_TRY(c, k::add_u32(kb.as<uint32_t>(), (uint32_t)h->kp.lo[0], r0, n, c->stream));
-      HIP_TRY(c, hipMemcpyAsync(r1, vb.p, (size_t)n * 4, hipMemcpyDeviceToDevice, c->stream));
-    } else {
-      HIP_TRY(c, k::add_u32(ka.as<uint32_t>(), (uint32_t)h->kp.lo[0], r0, n, c->stream));
-    }
+    uint32_t* sk = alt ? kb.as<uint32_t>() : ka.as<uint32_t>();
+    uint32_t* sy = alt ? vb.as<uint32_t>() : r1;
+    HIP_TRY(c, k::add_u32(sk, (uint32_t)h->kp.lo[0], r0, n, c->stream));
     Buf flag, pos, tot, starts;
     XL_TRY(dalloc(c, (size_t)n * 4, &flag, "segment flags"));
     XL_TRY(dalloc(c, (size_t)n * 4, &pos, "segment ids"));
@@ -847,18 +854,18 @@ struct Runner {
     XL_TRY(ctl_read(c, tot.p, 4, &nseg));
     XL_TRY(dalloc(c, (size_t)nseg * 4, &starts, "segment starts"));
     HIP_TRY(c, k::seg_starts(flag.as<uint32_t>(), pos.as<uint32_t>(), n, starts.as<uint32_t>(), c->stream));
-    SegList out;
-    for (int j = 0; j < 3; ++j) (&out.x)[j] = h->segb[h->seg_cur][j].as<uint32_t>();
-    HIP_TRY(c, k::seg_fill(starts.as<uint32_t>(), nseg, n, r0, h->dbeg, out, c->stream));
-    h->nseg = nseg;
+    HIP_TRY(c, k::seg_first_x(starts.as<uint32_t>(), nseg, r0, h->fx.as<uint32_t>(), c->stream));
+    HIP_TRY(c, hipMemsetAsync(h->fcnt[h->fcur].p, 0xff, (size_t)nseg * 4, c->stream));  // every row non-empty
+    HIP_TRY(c, hipMemsetAsync(h->fdiff[h->fcur].p, 0, (size_t)nseg * h->row_words * 4, c->stream));
+    HIP_TRY(c, k::rows_to_frontier(sy, flag.as<uint32_t>(), pos.as<uint32_t>(), n, h->kp.lo[1], h->row_words,
+                                   h->fdiff[h->fcur].as<uint32_t>(), c->stream));
+    h->fn = nseg;
     return XL_OK;
   }
 
   xl_status eval_plan(const RulePlan& p) {
     HeadRun* h = head_of(p.head);
-    if (h->dense && p.carried && h->nkey == 2 && p.driver_delta && h->row_words <= 4096)
-      return eval_grouped(p, h);
-    if (h->dense) h->round_other++;
+    if (h->frontier && p.driver_delta) return eval_frontier(p, h);
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
@@ -920,6 +927,17 @@ struct Runner {
       a.emit.key.shift = h->kp.shift;
       a.emit.val_slot = (int8_t)p.val_slot;
       a.emit.val_type = p.val_type;
+      if (h->dcount) {
+        a.emit.mode = EM_DCOUNT;
+        a.emit.bits = h->counts.as<uint32_t>();
+        a.emit.row_bits = (u64)h->range1;
+        HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+        HIP_TRY(c, k::stage_launch(a, c->stream, 1 << 16));
+        u64 cnt[CNT_N];
+        XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+        cands += (int64_t)cnt[CNT_CANDIDATES];
+        return XL_OK;
+      }
       if (h->is_sortagg) {
         a.emit.mode = EM_MAT;
         a.emit.mat_packed = 1;
@@ -1053,7 +1071,6 @@ struct Runner {
   }
 
   void begin_round(HeadRun* h) {
-    h->round_grouped = h->round_other = 0;
     h->round++;
     h->round_begin = h->nrows;
     h->didx_n = 0;
@@ -1061,23 +1078,21 @@ struct Runner {
   }
 
   xl_status finish_round(HeadRun* h, int64_t* delta) {
+    if (h->frontier && h->frontier_ready) {  // a frontier round produced the new delta rows
+      h->fcur ^= 1;
+      *delta = h->fnew;
+      return XL_OK;
+    }
     if (h->is_set) {
       h->dbeg = h->round_begin;
       h->dend = h->nrows;
       *delta = h->dend - h->dbeg;
-      if (h->dense && h->nkey == 2) {
-        if (*delta == 0) {
-          h->grouped = true;
-          h->nseg = 0;
-        } else if (h->round_grouped == 1 && h->round_other == 0) {
-          h->seg_cur ^= 1;  // the grouped expansion wrote this delta's segments
-          h->nseg = h->nseg_next;
-          h->grouped = true;
-        } else {
-          h->grouped = false;
-        }
-      }
+      if (h->frontier) XL_TRY(frontier_from_rows(h));  // seed round -> first frontier
       return XL_OK;
+    }
+    if (h->dcount) {
+      *delta = 0;
+      return XL_OK;  // counted in place; rows are produced at materialization
     }
     if (h->is_minmax) {
       XL_TRY(ensure_drow(h, h->didx_n));
@@ -1140,8 +1155,80 @@ struct Runner {
     return XL_OK;
   }
 
-  xl_status materialize(HeadRun* h) {
+  // Key-column bounds come from the planner's domains (a superset is enough
+  // for packing and index ranges); i32 value columns are scanned.
+  xl_status set_bounds(HeadRun* h) {
     Relation* r = h->rel;
+    if (r->nrows == 0) return XL_OK;
+    for (int j = 0; j < h->nkey; ++j) {
+      r->lo[j] = (int32_t)h->dom_lo[j];
+      r->hi[j] = (int32_t)h->dom_hi[j];
+    }
+    if (h->nkey < r->arity && r->types[h->nkey] == T_I32) {
+      Buf mm;
+      XL_TRY(dalloc(c, 8, &mm, "bounds"));
+      const int32_t init[2] = {INT32_MAX, INT32_MIN};
+      HIP_TRY(c, hipMemcpyAsync(mm.p, init, 8, hipMemcpyHostToDevice, c->stream));
+      HIP_TRY(c, k::minmax_i32((const int32_t*)r->col[h->nkey], r->nrows, mm.as<int32_t>(), c->stream));
+      int32_t out[2];
+      XL_TRY(ctl_read(c, mm.p, 8, out));
+      r->lo[h->nkey] = out[0];
+      r->hi[h->nkey] = out[1];
+    }
+    return XL_OK;
+  }
+
+  xl_status materialize(HeadRun* h) {
+    XL_TRY(materialize_rows(h));
+    return set_bounds(h);
+  }
+
+  xl_status materialize_rows(HeadRun* h) {
+    Relation* r = h->rel;
+    if (h->frontier) {  // every tuple is a set bit: rows in ascending (x, y)
+      Buf cnt, off, tmp, tot;
+      XL_TRY(dalloc(c, (size_t)h->range0 * 4, &cnt, "row counts"));
+      XL_TRY(dalloc(c, (size_t)h->range0 * 4, &off, "row offsets"));
+      XL_TRY(dalloc(c, k::scan_temp_bytes(h->range0), &tmp, "scan scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
+      HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0, tot.as<uint32_t>(),
+                                       tmp.p, c->stream));
+      uint32_t n = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &n));
+      if ((int64_t)n != h->keys) return c->fail(XL_DEVICE_ERROR, "bitmap row count mismatch (internal)");
+      h->rows[0].reset();
+      h->rows[1].reset();
+      Buf out[2];
+      for (int j = 0; j < 2; ++j) XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(n, 1) * 4, &out[j], "relation column"));
+      HIP_TRY(c, k::bits_to_rows(h->bits.as<uint32_t>(), h->range0, h->row_words, off.as<uint32_t>(), h->kp.lo[0],
+                                 h->kp.lo[1], out[0].as<uint32_t>(), out[1].as<uint32_t>(), c->stream));
+      relation_free_storage(r);
+      for (int j = 0; j < 2; ++j) r->col[j] = (uint32_t*)out[j].keep();
+      r->nrows = n;
+      return XL_OK;
+    }
+    if (h->dcount) {
+      const int64_t n = h->range0 * h->range1;
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->nkey, h->kp.lo[0], h->kp.lo[1], nullptr,
+                                nullptr, nullptr, 0, c->dcounters, 1, c->stream));
+      u64 m = 0;
+      XL_TRY(ctl_read(c, c->dcounters, 8, &m));
+      Buf out[3];
+      for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<u64>(m, 1) * 4, &out[j], "relation column"));
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->nkey, h->kp.lo[0], h->kp.lo[1],
+                                out[0].as<uint32_t>(), h->nkey == 2 ? out[1].as<uint32_t>() : nullptr,
+                                out[h->nkey].as<uint32_t>(), (int64_t)m, c->dcounters, 0, c->stream));
+      relation_free_storage(r);
+      for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
+      r->nrows = (int64_t)m;
+      h->keys = (int64_t)m;
+      if (r->max_rows > 0 && r->nrows > r->max_rows)
+        return c->fail(XL_CAPACITY_EXCEEDED, "relation " + r->name + " exceeds its max_rows");
+      return XL_OK;
+    }
     if (h->is_set) {
       relation_free_storage(r);
       for (int j = 0; j < h->nkey; ++j) r->col[j] = (uint32_t*)h->rows[j].keep();
@@ -1162,7 +1249,7 @@ struct Runner {
       for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
       r->nrows = n;
     }
-    return compute_bounds(c, r);
+    return XL_OK;
   }
 
   // ------------------------------------------------------------ strata

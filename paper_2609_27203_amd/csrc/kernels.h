@@ -87,15 +87,24 @@ hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1
 // ---- dense set heads ----
 hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const uint32_t* c1,
                          int64_t n, KeyPack kp, hipStream_t s);
-hipError_t grouped_expand(const GroupedArgs& a, hipStream_t s);
-hipError_t grouped_emit(SegList cur, int64_t nseg, const uint32_t* diff, uint32_t row_words,
-                        const uint32_t* seg_new, const uint32_t* seg_off, int32_t lo1,
-                        uint32_t* rows0, uint32_t* rows1, int64_t row_base, SegList next,
-                        unsigned long long* seg_counter, hipStream_t s);
-hipError_t seg_fill(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
-                    int64_t row_base, SegList out, hipStream_t s);
+hipError_t frontier_round(const FrontierArgs& a, hipStream_t s);
+// Delta bitmap rows of a row range sorted by its first key (head = first-row
+// flags, pos = their exclusive scan).
+hipError_t rows_to_frontier(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
+                            int32_t lo1, uint32_t row_words, uint32_t* diff, hipStream_t s);
+hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
+                        hipStream_t s);
+hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
+                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s);
+hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
+                       hipStream_t s);
 // out[i] = in[i] + add
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s);
+
+// Rows (k0[, k1], count) of the nonzero counters (count_only: just count them).
+hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0, int32_t lo1,
+                       uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap, unsigned long long* counter,
+                       int count_only, hipStream_t s);
 
 enum FoldKind { FOLD_NONE = 0, FOLD_COUNT, FOLD_SUM, FOLD_MIN, FOLD_MAX, FOLD_LSE };
 

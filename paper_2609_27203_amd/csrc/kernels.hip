@@ -734,8 +734,9 @@ __device__ __forceinline__ bool run_ops(KernArgs& a, Regs& u) {
 struct EmitState {
   u64 out_base;     // EM_MAT: first output position of this chunk
   uint32_t running; // rows emitted so far in this chunk
-  uint32_t cands;   // candidates seen in this chunk (EM_SET / EM_MINMAX)
+  u64 cands;        // candidates seen by this wave (flushed once at the end)
   bool stop;        // overflow observed: skip the rest of this launch
+  uint32_t pend_idx, pend_cnt;  // EM_DCOUNT: open run carried to the next batch
 };
 
 template <int MODE>
@@ -765,8 +766,8 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     return;
   }
   // EM_SET / EM_BITSET / EM_MINMAX: stop early once the load limit is passed.
-  st.cands += (uint32_t)__popcll(__ballot(act));
-  if (st.stop) return;
+  st.cands += (u64)__popcll(__ballot(act));
+  if (MODE != EM_DCOUNT && st.stop) return;
   if (MODE == EM_SET || MODE == EM_BITSET) {
     int ins = 0;
     if (act) {
@@ -802,6 +803,46 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
           atomicOr(&e.counters[CNT_FATAL], 2ull);
         }
       }
+    }
+    return;
+  }
+  if (MODE == EM_DCOUNT) {
+    // lanes holding the same key consecutively form a run; one atomic per run
+    uint32_t idx = 0;
+    if (act) {
+      const u64 key = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
+      idx = (uint32_t)(e.key.nkey == 2
+                           ? (key >> e.key.shift) * e.row_bits + (key & ((1ull << e.key.shift) - 1ull))
+                           : key);
+    }
+    const int lane = lane_id();
+    const uint32_t prev = __shfl_up(idx, 1, 64);
+    const u64 am = __ballot(act);
+    const bool prev_act = lane > 0 && ((am >> (lane - 1)) & 1ull);
+    const bool start = act && !(prev_act && prev == idx);
+    const u64 sm = __ballot(start);
+    if (!sm) return;
+    const u64 bnd = sm | ~am;
+    uint32_t len = 0;
+    if (start) {
+      const u64 above = bnd & ~((2ull << lane) - 1ull);
+      const int nxt = above ? __ffsll((long long)above) - 1 : 64;
+      len = (uint32_t)(nxt - lane);
+    }
+    // The wave walks its rows in order: the batch's last run stays open and
+    // absorbs the next batch's first run when the key repeats (sums commute,
+    // so merging equal keys is always exact).
+    const int f = __ffsll((long long)sm) - 1;
+    const int l = 63 - __clzll((long long)sm);
+    const uint32_t idx_f = __shfl(idx, f, 64), len_f = __shfl(len, f, 64);
+    const uint32_t idx_l = __shfl(idx, l, 64), len_l = __shfl(len, l, 64);
+    const bool merged = st.pend_cnt && st.pend_idx == idx_f;
+    if (start && lane != l && !(lane == f && merged)) atomicAdd(&e.bits[idx], len);
+    if (merged) st.pend_cnt += len_f;
+    if (!(merged && f == l)) {
+      if (st.pend_cnt && lane == 0) atomicAdd(&e.bits[st.pend_idx], st.pend_cnt);
+      st.pend_idx = idx_l;
+      st.pend_cnt = len_l;
     }
     return;
   }
@@ -855,9 +896,17 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   const int64_t nwaves = (int64_t)gridDim.x * ST_WAVES;
   EmitState st;
   st.stop = false;
-  for (int64_t chunk = (int64_t)blockIdx.x * ST_WAVES + w; chunk < nchunks; chunk += nwaves) {
+  st.cands = 0;
+  st.pend_idx = st.pend_cnt = 0;
+  // EM_DCOUNT walks one contiguous range of chunks per wave (runs of equal
+  // keys stay in one wave); every other mode interleaves chunks.
+  const int64_t wave_id = (int64_t)blockIdx.x * ST_WAVES + w;
+  const int64_t per = (nchunks + nwaves - 1) / nwaves;
+  const int64_t c_first = MODE == EM_DCOUNT ? wave_id * per : wave_id;
+  const int64_t c_end = MODE == EM_DCOUNT ? min(nchunks, c_first + per) : nchunks;
+  const int64_t c_step = MODE == EM_DCOUNT ? 1 : nwaves;
+  for (int64_t chunk = c_first; chunk < c_end; chunk += c_step) {
     st.running = 0;
-    st.cands = 0;
     st.out_base = (MODE == EM_MAT) ? a.emit.chunk_off[chunk] + (u64)a.emit.mat_base : 0;
     if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX) {
       if (!st.stop) st.stop = atomic_load_agent(&a.emit.counters[CNT_OVERFLOW]) != 0;
@@ -906,9 +955,19 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
       emit<MODE>(a, v, act, st);
     }
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
-    if ((MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX) && lane == 0 && st.cands)
-      atomicAdd(&a.emit.counters[CNT_CANDIDATES], (u64)st.cands);
   }
+  if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT) {
+    // one atomic per workgroup: a shared counter hit by every wave serializes
+    __shared__ u64 s_cands[ST_WAVES];
+    if (lane == 0) s_cands[w] = st.cands;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      u64 t = 0;
+      for (int i = 0; i < ST_WAVES; ++i) t += s_cands[i];
+      if (t) atomicAdd(&a.emit.counters[CNT_CANDIDATES], t);
+    }
+  }
+  if (MODE == EM_DCOUNT && st.pend_cnt && lane == 0) atomicAdd(&a.emit.bits[st.pend_idx], st.pend_cnt);
 }
 
 template <int MODE>
@@ -922,6 +981,7 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
   const int64_t nchunks = (a.src.n + 63) / 64;
   const unsigned grid = grid_for(nchunks, ST_WAVES, grid_cap);
   switch (a.emit.mode) {
+    case EM_DCOUNT: launch_mode<EM_DCOUNT>(a, std::min(grid, 4096u), s); return hipGetLastError();
     case EM_COUNT: launch_mode<EM_COUNT>(a, grid, s); break;
     case EM_MAT: launch_mode<EM_MAT>(a, grid, s); break;
     case EM_SET: launch_mode<EM_SET>(a, grid, s); break;
@@ -1071,185 +1131,249 @@ hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const
   return hipGetLastError();
 }
 
-// Grouped expansion, phase 1.  One workgroup per delta segment (one first-key
-// value x).  The workgroup copies bitmap row x into LDS twice (before / after),
-// expands every delta row (x, z) of the segment through the index of e --
-// wave-balanced exactly like the generic stage kernel -- and sets the bit of
-// each produced y in the LDS row with an LDS atomic (after a plain test, since
-// most candidates are already known).  It then writes back the changed words
-// of row x, the per-word difference to a scratch row, and the segment's count
-// of new tuples.  A row is owned by exactly one workgroup per round, so the
-// global bitmap needs no atomics here.
-constexpr int GR_THREADS = 256;
-constexpr int GR_WAVES = GR_THREADS / 64;
+// Frontier round (see FrontierArgs).  LDS holds bitmap row x before and after
+// the round plus a chunk of the delta row decoded into a list of Z values;
+// the delta row is consumed in chunks of FR_CHUNK words so the Z list stays
+// small.  The wave-balanced expansion of the Z list is the same as in the
+// generic stage kernel.  A plain LDS test precedes each LDS atomic because
+// most produced tuples are already known.
+constexpr int FR_THREADS = 256;
+constexpr int FR_WAVES = FR_THREADS / 64;
+constexpr int FR_CHUNK = 128;  // delta words decoded per step (<= 4096 Z values)
 
-__global__ __launch_bounds__(GR_THREADS) void grouped_expand_k(GroupedArgs a) {
+__device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t* total, uint32_t* s_w) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t incl = wave_incl_scan(x);
+  if (lane == 63) s_w[w] = incl;
+  __syncthreads();
+  uint32_t pre = 0, tot = 0;
+  for (int k = 0; k < (int)(blockDim.x >> 6); ++k) {
+    const uint32_t y = s_w[k];
+    if (k < w) pre += y;
+    tot += y;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + incl - x;
+}
+
+__global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
   extern __shared__ uint32_t lds[];
   uint32_t* old_row = lds;
   uint32_t* new_row = lds + a.row_words;
-  __shared__ uint32_t s_excl[GR_WAVES][64];
-  __shared__ uint32_t s_beg[GR_WAVES][64];
-  __shared__ uint32_t s_red[GR_WAVES];
+  __shared__ uint32_t zlist[FR_CHUNK * 32];
+  __shared__ uint32_t s_excl[FR_WAVES][64];
+  __shared__ uint32_t s_beg[FR_WAVES][64];
+  __shared__ uint32_t s_w[FR_WAVES];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const uint32_t W = a.row_words;
+  const uint32_t* ycol = a.idx.col[a.ybind_col];
+  u64 cands = 0, news = 0;  // wave-uniform totals of this workgroup's segments
   for (int64_t sg = blockIdx.x; sg < a.nseg; sg += gridDim.x) {
-    const uint32_t x = a.seg.x[sg];
-    const uint32_t start = a.seg.start[sg];
-    const uint32_t cnt = a.seg.count[sg];
+    if (a.in_cnt[sg] == 0) {  // x gained nothing last round: its delta row is empty
+      if (threadIdx.x == 0) a.out_cnt[sg] = 0;
+      continue;
+    }
+    const uint32_t x = a.x[sg];
     uint32_t* grow = a.bits + (u64)(x - (uint32_t)a.lo0) * W;
-    for (uint32_t i = threadIdx.x; i < W; i += GR_THREADS) {
+    const uint32_t* drow = a.in_diff + (u64)sg * W;
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
       const uint32_t v = grow[i];
       old_row[i] = v;
       new_row[i] = v;
     }
-    __syncthreads();
-    uint32_t cands = 0;
-    for (uint32_t base_row = (uint32_t)w * 64; base_row < cnt; base_row += GR_WAVES * 64) {
-      const uint32_t r = base_row + lane;
-      uint32_t beg = 0, deg = 0;
-      if (r < cnt) {
-        const uint32_t kk = a.dz[start + r] - (uint32_t)a.idx.key_lo;
-        if (kk < a.idx.key_range) {
-          beg = a.idx.off[kk];
-          deg = a.idx.off[kk + 1] - beg;
+    for (uint32_t cb = 0; cb < W; cb += FR_CHUNK) {
+      // decode delta words [cb, cb + FR_CHUNK) into the Z list
+      const uint32_t wi = cb + threadIdx.x;
+      const uint32_t d = (threadIdx.x < FR_CHUNK && wi < W) ? drow[wi] : 0u;
+      uint32_t nz;
+      uint32_t pos = block_excl_scan_u32(__popc(d), &nz, s_w);
+      for (uint32_t bits = d; bits; bits &= bits - 1)
+        zlist[pos++] = (uint32_t)a.lo1 + wi * 32u + (uint32_t)(__ffs(bits) - 1);
+      __syncthreads();
+      for (uint32_t r0 = (uint32_t)w * 64; r0 < nz; r0 += FR_WAVES * 64) {
+        const uint32_t r = r0 + lane;
+        uint32_t beg = 0, deg = 0;
+        if (r < nz) {
+          const uint32_t kk = zlist[r] - (uint32_t)a.idx.key_lo;
+          if (kk < a.idx.key_range) {
+            beg = a.idx.off[kk];
+            deg = a.idx.off[kk + 1] - beg;
+          }
         }
-      }
-      const uint32_t incl = wave_incl_scan(deg);
-      const uint32_t total = __shfl(incl, 63, 64);
-      s_excl[w][lane] = incl - deg;
-      s_beg[w][lane] = beg;
-      wave_lds_sync();
-      cands += total;
-      const uint32_t* ycol = a.idx.col[a.ybind_col];
-      for (uint32_t b0 = 0; b0 < total; b0 += 64) {
-        const uint32_t j = b0 + lane;
-        if (j < total) {
-          int q = 0;
+        // Rows with at least 64 matches are walked by the whole wavefront, one
+        // row at a time, lane = item: no owner search at all.  The remaining
+        // small rows share 64-item steps through a scan and a six-step search.
+        const bool big = deg >= 64;
+        u64 bigm = __ballot(big);
+        const uint32_t sdeg = big ? 0u : deg;
+        const uint32_t incl = wave_incl_scan(sdeg);
+        const uint32_t total = __shfl(incl, 63, 64);
+        s_excl[w][lane] = incl - sdeg;
+        s_beg[w][lane] = beg;
+        wave_lds_sync();
+        cands += total;
+        while (bigm) {
+          const int rb = __ffsll((long long)bigm) - 1;
+          bigm &= bigm - 1;
+          const uint32_t bb = __shfl(beg, rb, 64), bd = __shfl(deg, rb, 64);
+          cands += bd;
+          for (uint32_t k0 = 0; k0 < bd; k0 += 256) {
+            uint32_t y[4];
 #pragma unroll
-          for (int step = 32; step > 0; step >>= 1)
-            if (s_excl[w][q + step] <= j) q += step;
-          const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
-          const uint32_t bit = 1u << (y & 31);
-          if (!(new_row[y >> 5] & bit)) atomicOr(&new_row[y >> 5], bit);
+            for (int u = 0; u < 4; ++u) {
+              const uint32_t k = k0 + 64 * u + lane;
+              y[u] = k < bd ? ycol[bb + k] - (uint32_t)a.lo1 : 0xffffffffu;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              if (y[u] != 0xffffffffu) {
+                const uint32_t bit = 1u << (y[u] & 31);
+                if (!(new_row[y[u] >> 5] & bit)) atomicOr(&new_row[y[u] >> 5], bit);
+              }
+            }
+          }
         }
+        for (uint32_t b0 = 0; b0 < total; b0 += 64) {
+          const uint32_t j = b0 + lane;
+          if (j < total) {
+            int q = 0;
+#pragma unroll
+            for (int step = 32; step > 0; step >>= 1)
+              if (s_excl[w][q + step] <= j) q += step;
+            const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
+            const uint32_t bit = 1u << (y & 31);
+            if (!(new_row[y >> 5] & bit)) atomicOr(&new_row[y >> 5], bit);
+          }
+        }
+        wave_lds_sync();
       }
-      wave_lds_sync();
+      __syncthreads();
     }
-    __syncthreads();
+    // next delta row = new bits; write back the changed words of row x
     uint32_t nnew = 0;
-    uint32_t* drow = a.diff + (u64)sg * W;
-    for (uint32_t i = threadIdx.x; i < W; i += GR_THREADS) {
+    uint32_t* orow = a.out_diff + (u64)sg * W;
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
       const uint32_t nv = new_row[i];
-      const uint32_t d = nv & ~old_row[i];
-      drow[i] = d;
-      if (d) {
+      const uint32_t dd = nv & ~old_row[i];
+      orow[i] = dd;
+      if (dd) {
         grow[i] = nv;
-        nnew += __popc(d);
+        nnew += __popc(dd);
       }
     }
-    for (int d = 32; d > 0; d >>= 1) nnew += __shfl_xor(nnew, d, 64);
-    for (int d = 32; d > 0; d >>= 1) cands += __shfl_xor(cands, d, 64);
-    if (lane == 0) {
-      s_red[w] = nnew;
-      if (cands) atomicAdd(&a.counters[CNT_CANDIDATES], (u64)(cands / 64));
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t t = 0;
-      for (int i = 0; i < GR_WAVES; ++i) t += s_red[i];
-      a.seg_new[sg] = t;
-    }
-    __syncthreads();
+    uint32_t tnew;
+    block_excl_scan_u32(nnew, &tnew, s_w);
+    if (threadIdx.x == 0) a.out_cnt[sg] = tnew;
+    news += tnew;
+  }
+  // one atomic per workgroup for each total
+  __shared__ u64 s_c[FR_WAVES];
+  if (lane == 0) s_c[w] = cands;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 t = 0;
+    for (int i = 0; i < FR_WAVES; ++i) t += s_c[i];
+    if (t) atomicAdd(&a.counters[CNT_CANDIDATES], t);
+    if (news) atomicAdd(&a.counters[CNT_APPENDED], news);
   }
 }
 
-hipError_t grouped_expand(const GroupedArgs& a, hipStream_t s) {
+hipError_t frontier_round(const FrontierArgs& a, hipStream_t s) {
   if (a.nseg <= 0) return hipSuccess;
   const size_t lds = (size_t)a.row_words * 2 * sizeof(uint32_t);
-  const unsigned grid = (unsigned)std::min<int64_t>(a.nseg, 1 << 20);
-  grouped_expand_k<<<grid, GR_THREADS, lds, s>>>(a);
+  const unsigned grid = (unsigned)std::min<int64_t>(a.nseg, 4096);
+  frontier_round_k<<<grid, FR_THREADS, lds, s>>>(a);
   return hipGetLastError();
 }
 
-// Grouped expansion, phase 2: write each segment's new tuples (x, y) in
-// ascending y at its scanned offset and record the segment for the next round.
-__global__ __launch_bounds__(GR_THREADS) void grouped_emit_k(SegList cur, int64_t nseg,
-                                                             const uint32_t* diff, uint32_t row_words,
-                                                             const uint32_t* seg_new,
-                                                             const uint32_t* seg_off, int32_t lo1,
-                                                             uint32_t* rows0, uint32_t* rows1,
-                                                             int64_t row_base, SegList next,
-                                                             u64* seg_counter) {
-  __shared__ uint32_t s_w[GR_WAVES];
-  const int lane = lane_id(), w = threadIdx.x >> 6;
-  for (int64_t sg = blockIdx.x; sg < nseg; sg += gridDim.x) {
-    const uint32_t t = seg_new[sg];
-    if (t == 0) continue;
-    const uint32_t x = cur.x[sg];
-    const u64 out0 = (u64)row_base + seg_off[sg];
-    const uint32_t* drow = diff + (u64)sg * row_words;
-    uint32_t running = 0;
-    for (uint32_t base = 0; base < row_words; base += GR_THREADS) {
-      const uint32_t i = base + threadIdx.x;
-      const uint32_t d = i < row_words ? drow[i] : 0u;
-      const uint32_t c = __popc(d);
-      const uint32_t incl = wave_incl_scan(c);
-      if (lane == 63) s_w[w] = incl;
-      __syncthreads();
-      uint32_t pre = 0, tot = 0;
-      for (int k = 0; k < GR_WAVES; ++k) {
-        if (k < w) pre += s_w[k];
-        tot += s_w[k];
-      }
-      uint32_t pos = running + pre + incl - c;
-      uint32_t bits = d;
-      while (bits) {
-        const int b = __ffs(bits) - 1;
-        bits &= bits - 1;
-        rows0[out0 + pos] = x;
-        rows1[out0 + pos] = (uint32_t)lo1 + i * 32u + (uint32_t)b;
-        ++pos;
-      }
-      running += tot;
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-      const u64 k = atomicAdd(seg_counter, 1ull);
-      next.x[k] = x;
-      next.start[k] = (uint32_t)out0;
-      next.count[k] = t;
-    }
-  }
-}
-
-hipError_t grouped_emit(SegList cur, int64_t nseg, const uint32_t* diff, uint32_t row_words,
-                        const uint32_t* seg_new, const uint32_t* seg_off, int32_t lo1,
-                        uint32_t* rows0, uint32_t* rows1, int64_t row_base, SegList next,
-                        unsigned long long* seg_counter, hipStream_t s) {
-  if (nseg <= 0) return hipSuccess;
-  const unsigned grid = (unsigned)std::min<int64_t>(nseg, 1 << 20);
-  grouped_emit_k<<<grid, GR_THREADS, 0, s>>>(cur, nseg, diff, row_words, seg_new, seg_off, lo1, rows0,
-                                             rows1, row_base, next, seg_counter);
-  return hipGetLastError();
-}
-
-// Segments of a delta sorted by its first key column: starts come from the
-// change flags; x and count are filled here.
-__global__ void seg_fill_k(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
-                           int64_t row_base, SegList out) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nseg;
+// Delta rows of a row range sorted by its first key.  head[i] flags the first
+// row of each key and pos is the exclusive scan of head, so row i belongs to
+// delta row pos[i] + head[i] - 1.
+__global__ void rows_to_frontier_k(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
+                                   int32_t lo1, uint32_t row_words, uint32_t* diff) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t b = starts[i];
-    const uint32_t e = i + 1 < nseg ? starts[i + 1] : (uint32_t)n;
-    out.x[i] = xcol[b];
-    out.start[i] = (uint32_t)(row_base + b);
-    out.count[i] = e - b;
+    const uint32_t seg = pos[i] + head[i] - 1u;
+    const uint32_t y = ycol[i] - (uint32_t)lo1;
+    atomicOr(&diff[(u64)seg * row_words + (y >> 5)], 1u << (y & 31));
   }
 }
-hipError_t seg_fill(const uint32_t* starts, int64_t nseg, int64_t n, const uint32_t* xcol,
-                    int64_t row_base, SegList out, hipStream_t s) {
+hipError_t rows_to_frontier(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
+                            int32_t lo1, uint32_t row_words, uint32_t* diff, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  rows_to_frontier_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(ycol, head, pos, n, lo1, row_words, diff);
+  return hipGetLastError();
+}
+
+// Number of set bits in each bitmap row.
+__global__ __launch_bounds__(256) void row_popcount_k(const uint32_t* bits, int64_t nrows,
+                                                      uint32_t row_words, uint32_t* cnt) {
+  __shared__ uint32_t s_w[4];
+  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    const uint32_t* row = bits + (u64)r * row_words;
+    uint32_t c = 0;
+    for (uint32_t i = threadIdx.x; i < row_words; i += 256) c += __popc(row[i]);
+    uint32_t tot;
+    block_excl_scan_u32(c, &tot, s_w);
+    if (threadIdx.x == 0) cnt[r] = tot;
+  }
+}
+hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
+                        hipStream_t s) {
+  if (nrows <= 0) return hipSuccess;
+  row_popcount_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, cnt);
+  return hipGetLastError();
+}
+
+// Relation rows (x, y) of every set bit, in ascending (x, y) order: bitmap row
+// r holds x = lo0 + r and starts at off[r].  Each chunk of 256 words is
+// decoded into LDS first so the column writes are coalesced.
+__global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int64_t nrows,
+                                                      uint32_t row_words, const uint32_t* off,
+                                                      int32_t lo0, int32_t lo1, uint32_t* c0,
+                                                      uint32_t* c1) {
+  __shared__ uint32_t stage[256 * 32];
+  __shared__ uint32_t s_w[4];
+  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    const uint32_t* row = bits + (u64)r * row_words;
+    u64 out = off[r];
+    const uint32_t x = (uint32_t)lo0 + (uint32_t)r;
+    for (uint32_t cb = 0; cb < row_words; cb += 256) {
+      const uint32_t wi = cb + threadIdx.x;
+      const uint32_t d = wi < row_words ? row[wi] : 0u;
+      uint32_t n;
+      uint32_t pos = block_excl_scan_u32(__popc(d), &n, s_w);
+      for (uint32_t b = d; b; b &= b - 1) stage[pos++] = (uint32_t)lo1 + wi * 32u + (uint32_t)(__ffs(b) - 1);
+      __syncthreads();
+      for (uint32_t i = threadIdx.x; i < n; i += 256) {
+        c0[out + i] = x;
+        c1[out + i] = stage[i];
+      }
+      out += n;
+      __syncthreads();
+    }
+  }
+}
+hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
+                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s) {
+  if (nrows <= 0) return hipSuccess;
+  bits_to_rows_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, off,
+                                                                            lo0, lo1, c0, c1);
+  return hipGetLastError();
+}
+
+// First-key value of every segment of a row range sorted by that key.
+__global__ void seg_first_x_k(const uint32_t* starts, int64_t nseg, const uint32_t* xcol,
+                              uint32_t* out_x) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nseg;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out_x[i] = xcol[starts[i]];
+}
+hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
+                       hipStream_t s) {
   if (nseg <= 0) return hipSuccess;
-  seg_fill_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(starts, nseg, n, xcol, row_base, out);
+  seg_first_x_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(starts, nseg, xcol, out_x);
   return hipGetLastError();
 }
 
@@ -1261,6 +1385,43 @@ __global__ void add_u32_k(const uint32_t* in, uint32_t add, uint32_t* out, int64
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   add_u32_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(in, add, out, n);
+  return hipGetLastError();
+}
+
+// ============================================================ dense count heads
+__global__ void dcount_rows_k(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0,
+                              int32_t lo1, uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap,
+                              u64* counter, int count_only) {
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < n;
+       base += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = base + threadIdx.x;
+    const uint32_t c = i < n ? counts[i] : 0u;
+    const u64 m = __ballot(c != 0);
+    if (!m) continue;
+    const int leader = __ffsll((long long)m) - 1;
+    u64 pos0 = 0;
+    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
+    if (count_only) continue;
+    pos0 = __shfl(pos0, leader, 64);
+    if (c) {
+      const u64 p = pos0 + __popcll(m & lanemask_lt());
+      if (p >= (u64)cap) continue;
+      if (nkey == 2) {
+        k0[p] = (uint32_t)(i / range1) + (uint32_t)lo0;
+        k1[p] = (uint32_t)(i % range1) + (uint32_t)lo1;
+      } else {
+        k0[p] = (uint32_t)i + (uint32_t)lo0;
+      }
+      v[p] = c;
+    }
+  }
+}
+hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0, int32_t lo1,
+                       uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap, unsigned long long* counter,
+                       int count_only, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dcount_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(counts, n, range1, nkey, lo0, lo1, k0, k1, v, cap,
+                                                       counter, count_only);
   return hipGetLastError();
 }
 
