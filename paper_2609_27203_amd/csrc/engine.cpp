@@ -14,6 +14,9 @@ typedef unsigned long long u64;
 
 // Grid cap (blocks of four wavefronts) of the insert-or-improve emission kernels.
 constexpr int EMIT_GRID = 2048;
+// Rows a wavefront may insert after the load limit is crossed before it
+// learns so: its LDS staging buffer (512) plus one 64-item step.
+constexpr int64_t WAVE_SLACK = 512 + 64;
 
 // ================================================================== arena
 void Arena::init(char* base, size_t size) {
@@ -691,7 +694,7 @@ struct Runner {
   xl_status grow(HeadRun* h, int64_t need) {
     if (h->dense) return grow_rows(h, need);
     int64_t ncap = h->cap * 4;
-    while (ncap / 2 < need || ncap - need < 64 * 4 * EMIT_GRID + 1024) ncap *= 2;
+    while (ncap / 2 < need || ncap - need < WAVE_SLACK * 4 * EMIT_GRID + 1024) ncap *= 2;
     Buf nt;
     XL_TRY(alloc_table(h, ncap, &nt));
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
@@ -980,9 +983,9 @@ struct Runner {
         // table can never fill and the row list never overflows.
         const int64_t waves = std::min<int64_t>((a.src.n + 63) / 64, (int64_t)EMIT_GRID * 4);
         if (h->dense) {
-          const int64_t max_rows = h->rows_cap - 64 * waves - 1024;
+          const int64_t max_rows = h->rows_cap - WAVE_SLACK * waves - 1024;
           if (h->nrows >= max_rows) {
-            XL_TRY(grow_rows(h, h->nrows + 2 * (64 * waves + 1024)));
+            XL_TRY(grow_rows(h, h->nrows + 2 * (WAVE_SLACK * waves + 1024)));
             continue;
           }
           HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
@@ -995,9 +998,9 @@ struct Runner {
           a.emit.row_base = h->nrows;
           a.emit.row_cap = h->rows_cap;
         } else {
-        const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - 64 * waves - 1024);
+        const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
         if (h->keys >= max_keys) {
-          XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + 64 * waves + 1024)));
+          XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + WAVE_SLACK * waves + 1024)));
           continue;
         }
         HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
@@ -1048,13 +1051,15 @@ struct Runner {
           return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                    std::to_string(h->rel->max_rows));
         if (!cnt[CNT_OVERFLOW]) break;
-        XL_TRY(grow(h, h->dense ? h->nrows + 2 * (64 * waves + 1024) : h->keys * 2 + 1));
+        XL_TRY(grow(h, h->dense ? h->nrows + 2 * (WAVE_SLACK * waves + 1024) : h->keys * 2 + 1));
         if (h->is_minmax) {  // slot indices moved: rebuild this round's delta list
-          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-          HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(),
-                                        c->dcounters, c->stream));
-          u64 n2 = 0;
-          XL_TRY(ctl_read(c, c->dcounters, 8, &n2));
+          Buf tmp, tot;
+          XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
+          XL_TRY(dalloc(c, 8, &tot, "count"));
+          HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(), h->cap,
+                                        tot.as<uint32_t>(), tmp.p, c->stream));
+          uint32_t n2 = 0;
+          XL_TRY(ctl_read(c, tot.p, 4, &n2));
           h->didx_n = (int64_t)n2;
         }
       }
@@ -1210,17 +1215,18 @@ struct Runner {
     }
     if (h->dcount) {
       const int64_t n = h->range0 * h->range1;
-      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->nkey, h->kp.lo[0], h->kp.lo[1], nullptr,
-                                nullptr, nullptr, 0, c->dcounters, 1, c->stream));
-      u64 m = 0;
-      XL_TRY(ctl_read(c, c->dcounters, 8, &m));
+      Buf tmp, tot;
+      XL_TRY(dalloc(c, k::compact_temp_bytes(n), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->kp, nullptr, nullptr, nullptr, 0,
+                                tot.as<uint32_t>(), tmp.p, c->stream));
+      uint32_t m = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &m));
       Buf out[3];
-      for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<u64>(m, 1) * 4, &out[j], "relation column"));
-      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->nkey, h->kp.lo[0], h->kp.lo[1],
-                                out[0].as<uint32_t>(), h->nkey == 2 ? out[1].as<uint32_t>() : nullptr,
-                                out[h->nkey].as<uint32_t>(), (int64_t)m, c->dcounters, 0, c->stream));
+      for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(m, 1) * 4, &out[j], "relation column"));
+      HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->kp, out[0].as<uint32_t>(),
+                                h->nkey == 2 ? out[1].as<uint32_t>() : nullptr, out[h->nkey].as<uint32_t>(),
+                                (int64_t)m, tot.as<uint32_t>(), tmp.p, c->stream));
       relation_free_storage(r);
       for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
       r->nrows = (int64_t)m;
@@ -1237,13 +1243,15 @@ struct Runner {
       Buf out[3];
       const int64_t n = h->keys;
       for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
-      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      Buf tmp, tot;
+      XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
       HIP_TRY(c, k::table16_compact(h->table.as<Slot16>(), h->cap, h->kp, r->types[h->nkey], h->fold,
                                     out[0].as<uint32_t>(), h->nkey == 2 ? out[1].as<uint32_t>() : nullptr,
-                                    out[h->nkey].as<uint32_t>(), std::max<int64_t>(n, 1), c->dcounters,
+                                    out[h->nkey].as<uint32_t>(), std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p,
                                     c->stream));
-      u64 m = 0;
-      XL_TRY(ctl_read(c, c->dcounters, 8, &m));
+      uint32_t m = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &m));
       if ((int64_t)m != n) return c->fail(XL_DEVICE_ERROR, "table compaction count mismatch (internal)");
       relation_free_storage(r);
       for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();

@@ -61,15 +61,21 @@ hipError_t table16_insert_rows(Slot16* table, u64 mask, const uint32_t* c0, cons
                                unsigned long long* counters, hipStream_t s);
 hipError_t table16_rehash(const Slot16* old, int64_t old_cap, Slot16* nt, u64 mask,
                           unsigned long long* counters, hipStream_t s);
+// Ordered compactions (count -> scan -> write; *total = items kept; pass null
+// outputs to count only).  temp: compact_temp_bytes(n).
+size_t compact_temp_bytes(int64_t n);
 hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_t* delta_idx,
-                           unsigned long long* counter, hipStream_t s);
+                           int64_t out_cap, uint32_t* total, void* temp, hipStream_t s);
 // Rows (k0[, k1], v) of the given slots; folds are decoded (min/max transform).
 hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n, KeyPack kp,
                                  int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                                  uint32_t* v, hipStream_t s);
 hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
-                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap,
-                           unsigned long long* counter, hipStream_t s);
+                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap, uint32_t* total,
+                           void* temp, hipStream_t s);
+hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, KeyPack kp, uint32_t* k0,
+                       uint32_t* k1, uint32_t* v, int64_t out_cap, uint32_t* total, void* temp,
+                       hipStream_t s);
 
 // ---- sorted-candidate aggregation (sum / logsumexp / count) ----
 hipError_t seg_heads(const u64* keys, int64_t n, uint32_t* flag, hipStream_t s);
@@ -100,11 +106,6 @@ hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xco
                        hipStream_t s);
 // out[i] = in[i] + add
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s);
-
-// Rows (k0[, k1], count) of the nonzero counters (count_only: just count them).
-hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0, int32_t lo1,
-                       uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap, unsigned long long* counter,
-                       int count_only, hipStream_t s);
 
 enum FoldKind { FOLD_NONE = 0, FOLD_COUNT, FOLD_SUM, FOLD_MIN, FOLD_MAX, FOLD_LSE };
 

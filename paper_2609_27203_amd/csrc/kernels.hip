@@ -475,15 +475,27 @@ __device__ __forceinline__ uint32_t fold_decode(uint32_t e, int type, int is_max
   return o ^ 0x80000000u;
 }
 
+// One atomic per workgroup for a per-thread count (every thread must call).
+__device__ __forceinline__ void block_count_add(u64* counter, uint32_t mine) {
+  __shared__ uint32_t s_bc[4];
+  uint32_t v = mine;
+  for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+  if (lane_id() == 0) s_bc[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += s_bc[i];
+    if (t) atomicAdd(counter, (u64)t);
+  }
+}
+
 __global__ void set_insert_rows_k(u64* table, u64 mask, const uint32_t* c0, const uint32_t* c1,
                                   int64_t n, KeyPack kp, u64* counters) {
+  uint32_t mine = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int ins = set_insert(table, mask, pack_key(kp, c0[i], c1 ? c1[i] : 0u), counters);
-    const u64 m = __ballot(ins);
-    if (m && lane_id() == (__ffsll((long long)m) - 1))
-      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
-  }
+       i += (int64_t)gridDim.x * blockDim.x)
+    mine += set_insert(table, mask, pack_key(kp, c0[i], c1 ? c1[i] : 0u), counters);
+  block_count_add(&counters[CNT_INSERTED], mine);
 }
 hipError_t set_insert_rows(u64* table, u64 mask, const uint32_t* c0, const uint32_t* c1, int64_t n,
                            KeyPack kp, unsigned long long* counters, hipStream_t s) {
@@ -495,16 +507,16 @@ hipError_t set_insert_rows(u64* table, u64 mask, const uint32_t* c0, const uint3
 __global__ void table16_insert_rows_k(Slot16* t, u64 mask, const uint32_t* c0, const uint32_t* c1,
                                       const uint32_t* v, int64_t n, KeyPack kp, int type,
                                       int is_max, u64* counters) {
+  uint32_t mine = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     bool ins;
     const u64 s = slot_find_or_insert(t, mask, pack_key(kp, c0[i], c1 ? c1[i] : 0u), &ins,
                                       counters);
     if (s != ~0ull) atomicMin(&t[s].val, fold_encode(v[i], type, is_max));
-    const u64 m = __ballot(ins);
-    if (m && lane_id() == (__ffsll((long long)m) - 1))
-      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
+    mine += ins;
   }
+  block_count_add(&counters[CNT_INSERTED], mine);
 }
 hipError_t table16_insert_rows(Slot16* t, u64 mask, const uint32_t* c0, const uint32_t* c1,
                                const uint32_t* v, int64_t n, KeyPack kp, int type, int is_max,
@@ -532,27 +544,6 @@ __global__ void table16_rehash_k(const Slot16* old, int64_t old_cap, Slot16* nt,
 hipError_t table16_rehash(const Slot16* old, int64_t old_cap, Slot16* nt, u64 mask,
                           unsigned long long* counters, hipStream_t s) {
   table16_rehash_k<<<grid_for(old_cap, 256, 8192), 256, 0, s>>>(old, old_cap, nt, mask, counters);
-  return hipGetLastError();
-}
-
-__global__ void table16_stamped_k(const Slot16* t, int64_t cap, uint32_t round, uint32_t* idx,
-                                  u64* counter) {
-  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < cap;
-       base += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t i = base + threadIdx.x;
-    const bool hit = i < cap && t[i].key != EMPTY_KEY && t[i].stamp == round;
-    const u64 m = __ballot(hit);
-    if (!m) continue;
-    const int leader = __ffsll((long long)m) - 1;
-    u64 pos0 = 0;
-    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
-    pos0 = __shfl(pos0, leader, 64);
-    if (hit) idx[pos0 + __popcll(m & lanemask_lt())] = (uint32_t)i;
-  }
-}
-hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_t* delta_idx,
-                           unsigned long long* counter, hipStream_t s) {
-  table16_stamped_k<<<grid_for(cap, 256, 8192), 256, 0, s>>>(t, cap, round, delta_idx, counter);
   return hipGetLastError();
 }
 
@@ -584,39 +575,146 @@ hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n
   return hipGetLastError();
 }
 
-__global__ void table16_compact_k(const Slot16* t, int64_t cap, KeyPack kp, int type,
-                                  int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
-                                  int64_t out_cap, u64* counter) {
-  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < cap;
-       base += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t i = base + threadIdx.x;
-    Slot16 s;
-    s.key = EMPTY_KEY;
-    if (i < cap) s = t[i];
-    const bool hit = s.key != EMPTY_KEY;
-    const u64 m = __ballot(hit);
-    if (!m) continue;
-    const int leader = __ffsll((long long)m) - 1;
-    u64 pos0 = 0;
-    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
-    pos0 = __shfl(pos0, leader, 64);
-    if (hit) {
-      const u64 p = pos0 + __popcll(m & lanemask_lt());
-      if (p >= (u64)out_cap) continue;  // the host detects the count mismatch
-      uint32_t a, b;
-      unpack_key(kp, s.key, &a, &b);
-      k0[p] = a;
-      if (k1) k1[p] = b;
-      v[p] = stored_value(s.val, type, fold_kind);
+// ---- ordered compaction of table slots / counters ----------------------------
+// Two passes over the same contiguous ranges (CP_RANGE items per workgroup):
+// count the kept items, scan the per-range counts, then write each kept item
+// at its range offset plus its rank inside the range.  No shared counter, and
+// the output order is the slot order.
+constexpr int CP_THREADS = 256;
+constexpr int CP_RANGE = CP_THREADS * 32;
+
+enum CompactKind { CK_NONEMPTY = 0, CK_STAMP = 1, CK_COUNTER = 2 };
+
+struct CompactArgs {
+  int kind;
+  const Slot16* t;        // CK_NONEMPTY / CK_STAMP
+  const uint32_t* counts; // CK_COUNTER
+  int64_t n;
+  uint32_t round;         // CK_STAMP
+  KeyPack kp;
+  int type, fold_kind;
+  int64_t range1;         // CK_COUNTER: second-key range
+  uint32_t* k0;           // CK_NONEMPTY / CK_COUNTER rows; CK_STAMP: slot indices
+  uint32_t* k1;
+  uint32_t* v;
+  uint32_t* range_cnt;    // [nranges]
+  const uint32_t* range_off;
+  int64_t out_cap;
+};
+
+__device__ __forceinline__ bool cp_keep(const CompactArgs& a, int64_t i) {
+  if (i >= a.n) return false;
+  if (a.kind == CK_COUNTER) return a.counts[i] != 0;
+  const Slot16 s = a.t[i];
+  if (s.key == EMPTY_KEY) return false;
+  return a.kind == CK_NONEMPTY || s.stamp == a.round;
+}
+
+__global__ __launch_bounds__(CP_THREADS) void compact_count_k(CompactArgs a) {
+  const int64_t base = (int64_t)blockIdx.x * CP_RANGE;
+  uint32_t c = 0;
+  for (int k = 0; k < CP_RANGE / CP_THREADS; ++k) c += cp_keep(a, base + (int64_t)k * CP_THREADS + threadIdx.x);
+  uint32_t tot;
+  block_excl_scan<uint32_t>(c, &tot);
+  if (threadIdx.x == 0) a.range_cnt[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
+  const int64_t base = (int64_t)blockIdx.x * CP_RANGE;
+  uint32_t out = a.range_off[blockIdx.x];
+  for (int k = 0; k < CP_RANGE / CP_THREADS; ++k) {
+    const int64_t i = base + (int64_t)k * CP_THREADS + threadIdx.x;
+    const bool keep = cp_keep(a, i);
+    uint32_t tot;
+    const uint32_t p = out + block_excl_scan<uint32_t>(keep ? 1u : 0u, &tot);
+    if (keep && p < (u64)a.out_cap) {
+      if (a.kind == CK_STAMP) {
+        a.k0[p] = (uint32_t)i;
+      } else if (a.kind == CK_COUNTER) {
+        if (a.kp.nkey == 2) {
+          a.k0[p] = (uint32_t)(i / a.range1) + (uint32_t)a.kp.lo[0];
+          a.k1[p] = (uint32_t)(i % a.range1) + (uint32_t)a.kp.lo[1];
+        } else {
+          a.k0[p] = (uint32_t)i + (uint32_t)a.kp.lo[0];
+        }
+        a.v[p] = a.counts[i];
+      } else {
+        const Slot16 s = a.t[i];
+        uint32_t x0, x1;
+        unpack_key(a.kp, s.key, &x0, &x1);
+        a.k0[p] = x0;
+        if (a.k1) a.k1[p] = x1;
+        a.v[p] = stored_value(s.val, a.type, a.fold_kind);
+      }
     }
+    out += tot;
   }
 }
-hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
-                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap,
-                           unsigned long long* counter, hipStream_t s) {
-  table16_compact_k<<<grid_for(cap, 256, 8192), 256, 0, s>>>(t, cap, kp, type, fold_kind, k0, k1,
-                                                             v, out_cap, counter);
+
+static hipError_t compact_run(CompactArgs a, uint32_t* total, void* temp, hipStream_t s) {
+  const int64_t nr = (a.n + CP_RANGE - 1) / CP_RANGE;
+  if (nr == 0) return hipMemsetAsync(total, 0, 4, s);
+  uint32_t* cnt = (uint32_t*)temp;
+  uint32_t* off = cnt + ((nr + 63) & ~63ll);
+  char* stemp = (char*)(off + ((nr + 63) & ~63ll));
+  a.range_cnt = cnt;
+  compact_count_k<<<(unsigned)nr, CP_THREADS, 0, s>>>(a);
+  hipError_t e = scan_exclusive_u32(cnt, off, nr, total, stemp, s);
+  if (e != hipSuccess) return e;
+  if (!a.k0) return hipSuccess;  // count only
+  a.range_off = off;
+  compact_write_k<<<(unsigned)nr, CP_THREADS, 0, s>>>(a);
   return hipGetLastError();
+}
+
+size_t compact_temp_bytes(int64_t n) {
+  const int64_t nr = (n + CP_RANGE - 1) / CP_RANGE;
+  return (size_t)((nr + 63) & ~63ll) * 8 + scan_temp_bytes(nr) + 256;
+}
+
+hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_t* delta_idx,
+                           int64_t out_cap, uint32_t* total, void* temp, hipStream_t s) {
+  CompactArgs a{};
+  a.kind = CK_STAMP;
+  a.t = t;
+  a.n = cap;
+  a.round = round;
+  a.k0 = delta_idx;
+  a.out_cap = out_cap;
+  return compact_run(a, total, temp, s);
+}
+
+hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
+                           uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap, uint32_t* total,
+                           void* temp, hipStream_t s) {
+  CompactArgs a{};
+  a.kind = CK_NONEMPTY;
+  a.t = t;
+  a.n = cap;
+  a.kp = kp;
+  a.type = type;
+  a.fold_kind = fold_kind;
+  a.k0 = k0;
+  a.k1 = k1;
+  a.v = v;
+  a.out_cap = out_cap;
+  return compact_run(a, total, temp, s);
+}
+
+hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, KeyPack kp, uint32_t* k0,
+                       uint32_t* k1, uint32_t* v, int64_t out_cap, uint32_t* total, void* temp,
+                       hipStream_t s) {
+  CompactArgs a{};
+  a.kind = CK_COUNTER;
+  a.counts = counts;
+  a.n = n;
+  a.kp = kp;
+  a.range1 = range1;
+  a.k0 = k0;
+  a.k1 = k1;
+  a.v = v;
+  a.out_cap = out_cap;
+  return compact_run(a, total, temp, s);
 }
 
 // ============================================================ stage kernel
@@ -731,13 +829,70 @@ __device__ __forceinline__ bool run_ops(KernArgs& a, Regs& u) {
   return ok;
 }
 
+// Rows produced by EM_SET / EM_BITSET / EM_MINMAX are staged in a per-wave
+// LDS buffer and written out with one counter reservation per flush, so a
+// launch issues one global atomic per OUTB rows instead of one per 64.
+constexpr int OUTB = 512;
+
 struct EmitState {
   u64 out_base;     // EM_MAT: first output position of this chunk
   uint32_t running; // rows emitted so far in this chunk
   u64 cands;        // candidates seen by this wave (flushed once at the end)
-  bool stop;        // overflow observed: skip the rest of this launch
+  bool stop;        // overflow observed: no further inserts in this launch
   uint32_t pend_idx, pend_cnt;  // EM_DCOUNT: open run carried to the next batch
+  uint32_t buf_n;   // staged rows in this wave's buffer
+  uint32_t ins_pend;  // EM_MINMAX: keys inserted since the last flush
+  uint32_t* buf0;   // this wave's LDS staging columns
+  uint32_t* buf1;
 };
+
+__device__ __forceinline__ u64 shfl_u64(u64 v, int src) {
+  const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)(v >> 32), src, 64);
+  return ((u64)hi << 32) | lo;
+}
+
+// Write the wave's staged rows with one reservation; the reservation also
+// tells the wave whether the launch has passed its load limit.
+template <int MODE>
+__device__ __forceinline__ void flush_rows(KernArgs& a, EmitState& st) {
+  typedef XL_KARG const EmitSpec KEmit;
+  KEmit& e = a.emit;
+  const int lane = lane_id();
+  if (MODE == EM_MINMAX && st.ins_pend) {
+    u64 b = 0;
+    if (lane == 0) {
+      b = atomicAdd(&e.counters[CNT_INSERTED], (u64)st.ins_pend);
+      if (b + st.ins_pend > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
+    }
+    b = shfl_u64(b, 0);
+    if (b + st.ins_pend > e.limit) st.stop = true;
+    st.ins_pend = 0;
+  }
+  if (st.buf_n == 0) return;
+  wave_lds_sync();
+  u64 base = 0;
+  if (lane == 0) {
+    base = atomicAdd(&e.counters[CNT_APPENDED], (u64)st.buf_n);
+    if (MODE != EM_MINMAX && base + st.buf_n > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
+  }
+  base = shfl_u64(base, 0);
+  if (MODE != EM_MINMAX && base + st.buf_n > e.limit) st.stop = true;
+  for (uint32_t i = lane; i < st.buf_n; i += 64) {
+    if (MODE == EM_MINMAX) {
+      e.delta_idx[base + i] = st.buf0[i];
+    } else {
+      const u64 p = (u64)e.row_base + base + i;
+      if (p < (u64)e.row_cap) {
+        e.row_col[0][p] = st.buf0[i];
+        if (e.key.nkey == 2) e.row_col[1][p] = st.buf1[i];
+      } else {
+        atomicOr(&e.counters[CNT_FATAL], 2ull);
+      }
+    }
+  }
+  wave_lds_sync();
+  st.buf_n = 0;
+}
 
 template <int MODE>
 __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
@@ -786,23 +941,13 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     }
     const u64 m = __ballot(ins);
     if (m) {
-      const int leader = __ffsll((long long)m) - 1;
-      u64 base = 0;
-      if (lane_id() == leader) {
-        base = atomicAdd(&e.counters[CNT_APPENDED], (u64)__popcll(m));
-        if (base + __popcll(m) > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
-      }
-      base = __shfl(base, leader, 64);
-      if (base + __popcll(m) > e.limit) st.stop = true;
+      if (st.buf_n + 64 > OUTB) flush_rows<MODE>(a, st);
       if (ins) {
-        const u64 p = (u64)e.row_base + base + __popcll(m & lt);
-        if (p < (u64)e.row_cap) {
-          e.row_col[0][p] = getv(u, e.key.slot[0]);
-          if (e.key.nkey == 2) e.row_col[1][p] = getv(u, e.key.slot[1]);
-        } else {
-          atomicOr(&e.counters[CNT_FATAL], 2ull);
-        }
+        const uint32_t pos = st.buf_n + (uint32_t)__popcll(m & lt);
+        st.buf0[pos] = getv(u, e.key.slot[0]);
+        st.buf1[pos] = getv(u, e.key.slot[1]);
       }
+      st.buf_n += (uint32_t)__popcll(m);
     }
     return;
   }
@@ -859,24 +1004,12 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
         if (ins || enc < old) app = atomicExch(&e.table16[slot].stamp, e.round) != e.round;
       }
     }
-    const u64 mi = __ballot(ins);
-    if (mi) {
-      const int leader = __ffsll((long long)mi) - 1;
-      u64 base = 0;
-      if (lane_id() == leader) {
-        base = atomicAdd(&e.counters[CNT_INSERTED], (u64)__popcll(mi));
-        if (base + __popcll(mi) > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
-      }
-      base = __shfl(base, leader, 64);
-      if (base + __popcll(mi) > e.limit) st.stop = true;
-    }
+    st.ins_pend += (uint32_t)__popcll(__ballot(ins));
     const u64 ma = __ballot(app);
-    if (ma) {
-      const int leader = __ffsll((long long)ma) - 1;
-      u64 base = 0;
-      if (lane_id() == leader) base = atomicAdd(&e.counters[CNT_APPENDED], (u64)__popcll(ma));
-      base = __shfl(base, leader, 64);
-      if (app) e.delta_idx[base + __popcll(ma & lt)] = (uint32_t)slot;
+    if (ma || st.ins_pend + 64 > OUTB) {
+      if (st.buf_n + 64 > OUTB || st.ins_pend + 64 > OUTB) flush_rows<MODE>(a, st);
+      if (app) st.buf0[st.buf_n + (uint32_t)__popcll(ma & lt)] = (uint32_t)slot;
+      st.buf_n += (uint32_t)__popcll(ma);
     }
   }
 }
@@ -891,6 +1024,8 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   __shared__ uint32_t s_excl[ST_WAVES][64];
   __shared__ uint32_t s_beg[ST_WAVES][64];
   __shared__ uint32_t s_v[ST_WAVES][MAXV][64];
+  constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX;
+  __shared__ uint32_t s_out[STAGED ? ST_WAVES : 1][2][STAGED ? OUTB : 1];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int64_t nchunks = (a.src.n + 63) / 64;
   const int64_t nwaves = (int64_t)gridDim.x * ST_WAVES;
@@ -898,6 +1033,9 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   st.stop = false;
   st.cands = 0;
   st.pend_idx = st.pend_cnt = 0;
+  st.buf_n = st.ins_pend = 0;
+  st.buf0 = s_out[STAGED ? w : 0][0];
+  st.buf1 = s_out[STAGED ? w : 0][1];
   // EM_DCOUNT walks one contiguous range of chunks per wave (runs of equal
   // keys stay in one wave); every other mode interleaves chunks.
   const int64_t wave_id = (int64_t)blockIdx.x * ST_WAVES + w;
@@ -908,9 +1046,6 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   for (int64_t chunk = c_first; chunk < c_end; chunk += c_step) {
     st.running = 0;
     st.out_base = (MODE == EM_MAT) ? a.emit.chunk_off[chunk] + (u64)a.emit.mat_base : 0;
-    if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX) {
-      if (!st.stop) st.stop = atomic_load_agent(&a.emit.counters[CNT_OVERFLOW]) != 0;
-    }
     const int64_t row = chunk * 64 + lane;
     Regs v = (Regs)(0u);
     bool ok = row < a.src.n;
@@ -968,6 +1103,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     }
   }
   if (MODE == EM_DCOUNT && st.pend_cnt && lane == 0) atomicAdd(&a.emit.bits[st.pend_idx], st.pend_cnt);
+  if (STAGED) flush_rows<MODE>(a, st);  // rows already inserted are always written
 }
 
 template <int MODE>
@@ -1078,6 +1214,7 @@ hipError_t seg_reduce(const u64* keys, const uint32_t* vals, const uint32_t* sta
 __global__ void agg_merge_k(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1,
                             const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
                             u64* counters) {
+  uint32_t mine = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     bool ins;
@@ -1099,10 +1236,9 @@ __global__ void agg_merge_k(Slot16* t, u64 mask, const uint32_t* k0, const uint3
       }
       t[s].val = r;
     }
-    const u64 m = __ballot(ins);
-    if (m && lane_id() == (__ffsll((long long)m) - 1))
-      atomicAdd(&counters[CNT_INSERTED], (u64)__popcll(m));
+    mine += ins;
   }
+  block_count_add(&counters[CNT_INSERTED], mine);
 }
 hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1,
                      const uint32_t* v, int64_t n, KeyPack kp, int type, int fold_kind,
@@ -1385,43 +1521,6 @@ __global__ void add_u32_k(const uint32_t* in, uint32_t add, uint32_t* out, int64
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   add_u32_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(in, add, out, n);
-  return hipGetLastError();
-}
-
-// ============================================================ dense count heads
-__global__ void dcount_rows_k(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0,
-                              int32_t lo1, uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap,
-                              u64* counter, int count_only) {
-  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < n;
-       base += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t i = base + threadIdx.x;
-    const uint32_t c = i < n ? counts[i] : 0u;
-    const u64 m = __ballot(c != 0);
-    if (!m) continue;
-    const int leader = __ffsll((long long)m) - 1;
-    u64 pos0 = 0;
-    if (lane_id() == leader) pos0 = atomicAdd(counter, (u64)__popcll(m));
-    if (count_only) continue;
-    pos0 = __shfl(pos0, leader, 64);
-    if (c) {
-      const u64 p = pos0 + __popcll(m & lanemask_lt());
-      if (p >= (u64)cap) continue;
-      if (nkey == 2) {
-        k0[p] = (uint32_t)(i / range1) + (uint32_t)lo0;
-        k1[p] = (uint32_t)(i % range1) + (uint32_t)lo1;
-      } else {
-        k0[p] = (uint32_t)i + (uint32_t)lo0;
-      }
-      v[p] = c;
-    }
-  }
-}
-hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, int nkey, int32_t lo0, int32_t lo1,
-                       uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t cap, unsigned long long* counter,
-                       int count_only, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  dcount_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(counts, n, range1, nkey, lo0, lo1, k0, k1, v, cap,
-                                                       counter, count_only);
   return hipGetLastError();
 }
 
