@@ -108,6 +108,8 @@ def main():
     ap.add_argument("--workload", default="tc_rmat_count",
                     help="one of the engine's five workloads (the headline line uses tc_rmat_count)")
     ap.add_argument("--index-mode", type=int, default=0, help="0 auto, 1 hash tables only, 2 prefer dense")
+    ap.add_argument("--option", action="append", default=[], metavar="KEY=VALUE",
+                    help="extra engine option (xl_context_set_option), repeatable")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
@@ -125,6 +127,9 @@ def main():
     ctx = xlh.Context(device=0, workspace_bytes=int(args.workspace_gb * (1 << 30)))
     ctx.set_option("profile", 1)
     ctx.set_option("index_mode", args.index_mode)
+    for kv in args.option:
+        k, v = kv.split("=")
+        ctx.set_option(k, int(v))
     for name, (types, cols) in wl.edb.items():
         ctx.relation(name, types).load(cols)
     for name, types in wl.idb.items():

@@ -128,6 +128,11 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *   "index_mode"      0 = automatic, 1 = always open-addressing hash tables,
  *                     2 = prefer dense key-domain tables where they fit
  *   "profile"         1 = time the fused join/insert kernels (receipt emit_*)
+ *   "pull_ratio"      closure-shaped strata over dense heads: a source whose
+ *                     delta row has d bits and u unreached targets with an
+ *                     in-edge is expanded by pulling (scanning in-edges of the
+ *                     unreached targets) when pull_ratio * d >= u; 0 = always
+ *                     push (default 64)
  * XL_INVALID_ARGUMENT for an unknown key or value.
  */
 xl_status xl_context_set_option(xl_context* ctx, const char* key, int64_t value);

@@ -69,6 +69,11 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     c->index_mode = (int)value;
     return XL_OK;
   }
+  if (!strcmp(key, "pull_ratio")) {
+    if (value < 0 || value > 1024) return c->fail(XL_INVALID_ARGUMENT, "pull_ratio must be in [0, 1024]");
+    c->pull_ratio = (int)value;
+    return XL_OK;
+  }
   if (!strcmp(key, "profile")) {
     if (value < 0 || value > 1) return c->fail(XL_INVALID_ARGUMENT, "profile must be 0 or 1");
     c->profile = (int)value;

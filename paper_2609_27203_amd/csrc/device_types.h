@@ -102,7 +102,8 @@ struct EmitSpec {
   int32_t nout;
   int8_t out_slot[MAXV];
   uint32_t* out_col[MAXV];
-  unsigned long long* out_key;
+  unsigned long long* out_key;  // EM_MAT packed: 64-bit keys, or 32-bit when key32
+  uint8_t key32;
   uint32_t* out_val;
   const unsigned long long* chunk_off;  // EM_MAT: exclusive offsets per chunk
   int64_t mat_base;                     // EM_MAT: added to every output position
@@ -155,6 +156,13 @@ struct FrontierArgs {
   uint32_t* out_cnt;        // next delta: counts and bitmap rows, same slots
   uint32_t* out_diff;
   unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED (= new tuples)
+  // Pull direction: e indexed by the Y column; Z is rev.col[rev_zcol].  A
+  // workgroup pulls when pull_ratio * |delta(x)| >= |unreached Y with an
+  // in-edge| (pull_ratio 0: always push).
+  IndexProbe rev;
+  int32_t rev_zcol;
+  const uint32_t* hasin;    // bit (y - lo1): y has at least one in-edge
+  uint32_t pull_ratio;
 };
 
 }  // namespace xlh

@@ -360,6 +360,7 @@ struct HeadRun {
   bool frontier = false;
   bool frontier_ready = false;  // the current delta is in fcnt/fdiff[fcur]
   Buf fx, fcnt[2], fdiff[2];    // delta row slot sg belongs to first-key value fx[sg]
+  Buf hasin;                    // Y values with an in-edge (pull direction)
   int fcur = 0;
   int64_t fn = 0, fnew = 0;
   // dense count heads: one counter per key of the domain
@@ -797,6 +798,16 @@ struct Runner {
     f.row_words = h->row_words;
     f.out_cnt = h->fcnt[h->fcur ^ 1].as<uint32_t>();
     f.out_diff = h->fdiff[h->fcur ^ 1].as<uint32_t>();
+    f.pull_ratio = (uint32_t)c->pull_ratio;
+    if (c->pull_ratio) {
+      XL_TRY(get_index(p.steps[0].rel, p.carried_ycol, &f.rev));
+      f.rev_zcol = p.steps[0].key_col;
+      if (!h->hasin.p) {
+        XL_TRY(dalloc(c, (size_t)h->row_words * 4, &h->hasin, "in-edge bitmap"));
+        HIP_TRY(c, k::hasin_bits(f.rev, h->kp.lo[1], h->row_words, h->hasin.as<uint32_t>(), c->stream));
+      }
+      f.hasin = h->hasin.as<uint32_t>();
+    }
     f.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
@@ -949,13 +960,14 @@ struct Runner {
         XL_TRY(counted_pass(a, &total, &offs));
         cands += total;
         if (total == 0) return XL_OK;
+        const size_t kb = key_bytes(h);
         if (h->cn + total > h->ccap) {
           const int64_t ncap = std::max<int64_t>(h->cn + total, h->ccap * 2);
           Buf nk, nv;
-          XL_TRY(dalloc(c, (size_t)ncap * 8, &nk, "aggregate candidates"));
+          XL_TRY(dalloc(c, (size_t)ncap * kb, &nk, "aggregate candidates"));
           XL_TRY(dalloc(c, (size_t)ncap * 4, &nv, "aggregate candidates"));
           if (h->cn) {
-            HIP_TRY(c, hipMemcpyAsync(nk.p, h->ckey.p, (size_t)h->cn * 8, hipMemcpyDeviceToDevice, c->stream));
+            HIP_TRY(c, hipMemcpyAsync(nk.p, h->ckey.p, (size_t)h->cn * kb, hipMemcpyDeviceToDevice, c->stream));
             HIP_TRY(c, hipMemcpyAsync(nv.p, h->cval.p, (size_t)h->cn * 4, hipMemcpyDeviceToDevice, c->stream));
           }
           std::swap(h->ckey.p, nk.p);
@@ -964,6 +976,7 @@ struct Runner {
           h->ccap = ncap;
         }
         a.emit.out_key = h->ckey.as<u64>();
+        a.emit.key32 = kb == 4;
         a.emit.out_val = h->cval.as<uint32_t>();
         a.emit.chunk_off = offs.as<u64>();
         a.emit.mat_base = h->cn;
@@ -1067,6 +1080,12 @@ struct Runner {
     return XL_OK;
   }
 
+  // Candidate keys of sorted aggregation are 32-bit when the packed key fits.
+  size_t key_bytes(const HeadRun* h) const {
+    const int kbits = h->nkey == 2 ? h->bits0 + h->kp.shift : h->bits0;
+    return kbits <= 32 ? 4 : 8;
+  }
+
   xl_status ensure_drow(HeadRun* h, int64_t n) {
     if (n <= h->dcap) return XL_OK;
     const int64_t ncap = std::max<int64_t>(n, h->dcap * 2);
@@ -1117,21 +1136,26 @@ struct Runner {
       return XL_OK;
     }
     const int kbits = h->nkey == 2 ? h->bits0 + h->kp.shift : h->bits0;
+    const int kb = (int)key_bytes(h);
     Buf k2, v2, tmp, flag, pos, tot;
-    XL_TRY(dalloc(c, (size_t)n * 8, &k2, "sort keys"));
+    XL_TRY(dalloc(c, (size_t)n * kb, &k2, "sort keys"));
     XL_TRY(dalloc(c, (size_t)n * 4, &v2, "sort values"));
     XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
     int alt = 0;
-    HIP_TRY(c, k::radix_sort_u64(h->ckey.as<u64>(), h->cval.as<uint32_t>(), k2.as<u64>(), v2.as<uint32_t>(),
-                                 n, kbits, tmp.p, c->stream, &alt));
-    u64* sk = alt ? k2.as<u64>() : h->ckey.as<u64>();
+    if (kb == 4)
+      HIP_TRY(c, k::radix_sort_u32(h->ckey.as<uint32_t>(), h->cval.as<uint32_t>(), k2.as<uint32_t>(),
+                                   v2.as<uint32_t>(), n, kbits, tmp.p, c->stream, &alt));
+    else
+      HIP_TRY(c, k::radix_sort_u64(h->ckey.as<u64>(), h->cval.as<uint32_t>(), k2.as<u64>(), v2.as<uint32_t>(),
+                                   n, kbits, tmp.p, c->stream, &alt));
+    void* sk = alt ? k2.p : h->ckey.p;
     uint32_t* sv = alt ? v2.as<uint32_t>() : h->cval.as<uint32_t>();
     XL_TRY(dalloc(c, (size_t)n * 4, &flag, "segment flags"));
     XL_TRY(dalloc(c, (size_t)n * 4, &pos, "segment ids"));
     XL_TRY(dalloc(c, 8, &tot, "count"));
     tmp.reset();
     XL_TRY(dalloc(c, k::scan_temp_bytes(n), &tmp, "scan scratch"));
-    HIP_TRY(c, k::seg_heads(sk, n, flag.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::seg_heads(sk, kb, n, flag.as<uint32_t>(), c->stream));
     HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), n, tot.as<uint32_t>(), tmp.p,
                                      c->stream));
     uint32_t nseg = 0;
@@ -1140,7 +1164,7 @@ struct Runner {
     XL_TRY(dalloc(c, (size_t)nseg * 4, &starts, "segment starts"));
     HIP_TRY(c, k::seg_starts(flag.as<uint32_t>(), pos.as<uint32_t>(), n, starts.as<uint32_t>(), c->stream));
     XL_TRY(ensure_drow(h, nseg));
-    HIP_TRY(c, k::seg_reduce(sk, sv, starts.as<uint32_t>(), nseg, n, h->kp, h->rel->types[h->nkey], h->fold,
+    HIP_TRY(c, k::seg_reduce(sk, kb, sv, starts.as<uint32_t>(), nseg, n, h->kp, h->rel->types[h->nkey], h->fold,
                              h->drow[0].as<uint32_t>(), h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
                              h->drow[h->nkey].as<uint32_t>(), c->stream));
     if (h->keys + (int64_t)nseg > h->cap / 2) XL_TRY(grow(h, h->keys + nseg));

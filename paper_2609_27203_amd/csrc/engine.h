@@ -60,6 +60,7 @@ struct Context {
   int hash_min_log2 = 22;
   int index_mode = 0;
   int profile = 0;
+  int pull_ratio = 64;
   int64_t control_bytes = 0;
 
   xl_status fail(xl_status st, const std::string& msg) {

@@ -78,11 +78,11 @@ hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, KeyPac
                        hipStream_t s);
 
 // ---- sorted-candidate aggregation (sum / logsumexp / count) ----
-hipError_t seg_heads(const u64* keys, int64_t n, uint32_t* flag, hipStream_t s);
+hipError_t seg_heads(const void* keys, int key_bytes, int64_t n, uint32_t* flag, hipStream_t s);
 hipError_t seg_starts(const uint32_t* flag, const uint32_t* pos, int64_t n, uint32_t* start,
                       hipStream_t s);
 // fold_kind: FOLD_SUM / FOLD_LSE / FOLD_COUNT / FOLD_MIN / FOLD_MAX
-hipError_t seg_reduce(const u64* keys, const uint32_t* vals, const uint32_t* start, int64_t nseg,
+hipError_t seg_reduce(const void* keys, int key_bytes, const uint32_t* vals, const uint32_t* start, int64_t nseg,
                       int64_t n, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                       uint32_t* v, hipStream_t s);
 // S(key) = S(key) (+) delta for every delta row (keys unique within the call).
@@ -94,6 +94,7 @@ hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1
 hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const uint32_t* c1,
                          int64_t n, KeyPack kp, hipStream_t s);
 hipError_t frontier_round(const FrontierArgs& a, hipStream_t s);
+hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s);
 // Delta bitmap rows of a row range sorted by its first key (head = first-row
 // flags, pos = their exclusive scan).
 hipError_t rows_to_frontier(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,

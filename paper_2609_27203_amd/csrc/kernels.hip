@@ -909,7 +909,9 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     if (act) {
       const u64 pos = st.out_base + st.running + __popcll(m & lt);
       if (e.mat_packed) {
-        e.out_key[pos] = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
+        const u64 key = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
+        if (e.key32) ((uint32_t*)e.out_key)[pos] = (uint32_t)key;
+        else e.out_key[pos] = key;
         if (e.val_slot >= 0) e.out_val[pos] = getv(u, e.val_slot);
       } else {
 #pragma unroll
@@ -1128,13 +1130,15 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
 }
 
 // ============================================================ segmented aggregation
-__global__ void seg_heads_k(const u64* keys, int64_t n, uint32_t* flag) {
+template <typename K>
+__global__ void seg_heads_k(const K* keys, int64_t n, uint32_t* flag) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     flag[i] = (i == 0) || keys[i] != keys[i - 1];
 }
-hipError_t seg_heads(const u64* keys, int64_t n, uint32_t* flag, hipStream_t s) {
-  seg_heads_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(keys, n, flag);
+hipError_t seg_heads(const void* keys, int key_bytes, int64_t n, uint32_t* flag, hipStream_t s) {
+  if (key_bytes == 4) seg_heads_k<uint32_t><<<grid_for(n, 256, 65536), 256, 0, s>>>((const uint32_t*)keys, n, flag);
+  else seg_heads_k<u64><<<grid_for(n, 256, 65536), 256, 0, s>>>((const u64*)keys, n, flag);
   return hipGetLastError();
 }
 
@@ -1159,7 +1163,8 @@ __device__ __forceinline__ float lse2(float a, float b) {
 
 // One thread folds one key group of the sorted candidates, in sorted order.
 // logsumexp is the two-pass max-shifted form: m = max, then m + log(sum exp(x - m)).
-__global__ void seg_reduce_k(const u64* keys, const uint32_t* vals, const uint32_t* start,
+template <typename K>
+__global__ void seg_reduce_k(const K* keys, const uint32_t* vals, const uint32_t* start,
                              int64_t nseg, int64_t n, KeyPack kp, int type, int fold_kind,
                              uint32_t* k0, uint32_t* k1, uint32_t* v) {
   for (int64_t sg = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; sg < nseg;
@@ -1202,12 +1207,16 @@ __global__ void seg_reduce_k(const u64* keys, const uint32_t* vals, const uint32
     v[sg] = out;
   }
 }
-hipError_t seg_reduce(const u64* keys, const uint32_t* vals, const uint32_t* start, int64_t nseg,
+hipError_t seg_reduce(const void* keys, int key_bytes, const uint32_t* vals, const uint32_t* start, int64_t nseg,
                       int64_t n, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                       uint32_t* v, hipStream_t s) {
   if (nseg <= 0) return hipSuccess;
-  seg_reduce_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(keys, vals, start, nseg, n, kp, type,
-                                                          fold_kind, k0, k1, v);
+  if (key_bytes == 4)
+    seg_reduce_k<uint32_t><<<grid_for(nseg, 256, 65536), 256, 0, s>>>((const uint32_t*)keys, vals, start, nseg, n,
+                                                                      kp, type, fold_kind, k0, k1, v);
+  else
+    seg_reduce_k<u64><<<grid_for(nseg, 256, 65536), 256, 0, s>>>((const u64*)keys, vals, start, nseg, n, kp, type,
+                                                                 fold_kind, k0, k1, v);
   return hipGetLastError();
 }
 
@@ -1297,6 +1306,7 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
   extern __shared__ uint32_t lds[];
   uint32_t* old_row = lds;
   uint32_t* new_row = lds + a.row_words;
+  uint32_t* f_row = lds + 2 * a.row_words;  // this round's delta row of x
   __shared__ uint32_t zlist[FR_CHUNK * 32];
   __shared__ uint32_t s_excl[FR_WAVES][64];
   __shared__ uint32_t s_beg[FR_WAVES][64];
@@ -1304,7 +1314,8 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const uint32_t W = a.row_words;
   const uint32_t* ycol = a.idx.col[a.ybind_col];
-  u64 cands = 0, news = 0;  // wave-uniform totals of this workgroup's segments
+  const uint32_t* zcol = a.rev.col[a.rev_zcol];
+  u64 cands = 0, news = 0;  // cands: this lane's share; news: workgroup total
   for (int64_t sg = blockIdx.x; sg < a.nseg; sg += gridDim.x) {
     if (a.in_cnt[sg] == 0) {  // x gained nothing last round: its delta row is empty
       if (threadIdx.x == 0) a.out_cnt[sg] = 0;
@@ -1313,20 +1324,50 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
     const uint32_t x = a.x[sg];
     uint32_t* grow = a.bits + (u64)(x - (uint32_t)a.lo0) * W;
     const uint32_t* drow = a.in_diff + (u64)sg * W;
+    uint32_t nd = 0, nu = 0;
     for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
-      const uint32_t v = grow[i];
+      const uint32_t v = grow[i], f = drow[i];
       old_row[i] = v;
       new_row[i] = v;
+      f_row[i] = f;
+      nd += __popc(f);
+      if (a.pull_ratio) nu += __popc(~v & a.hasin[i]);
     }
+    uint32_t tnd, tnu;
+    block_excl_scan_u32(nd, &tnd, s_w);
+    block_excl_scan_u32(nu, &tnu, s_w);
+    const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
     for (uint32_t cb = 0; cb < W; cb += FR_CHUNK) {
-      // decode delta words [cb, cb + FR_CHUNK) into the Z list
+      // decode words [cb, cb + FR_CHUNK): push takes the delta's Z values,
+      // pull the unreached Y values that have an in-edge
       const uint32_t wi = cb + threadIdx.x;
-      const uint32_t d = (threadIdx.x < FR_CHUNK && wi < W) ? drow[wi] : 0u;
+      uint32_t d = 0;
+      if (threadIdx.x < FR_CHUNK && wi < W) d = pull ? (~old_row[wi] & a.hasin[wi]) : f_row[wi];
       uint32_t nz;
       uint32_t pos = block_excl_scan_u32(__popc(d), &nz, s_w);
       for (uint32_t bits = d; bits; bits &= bits - 1)
         zlist[pos++] = (uint32_t)a.lo1 + wi * 32u + (uint32_t)(__ffs(bits) - 1);
       __syncthreads();
+      if (pull) {
+        // one lane per unreached Y: scan its in-edges until one comes from the delta
+        for (uint32_t r = threadIdx.x; r < nz; r += FR_THREADS) {
+          const uint32_t y = zlist[r];
+          const uint32_t kk = y - (uint32_t)a.rev.key_lo;
+          if (kk >= a.rev.key_range) continue;
+          const uint32_t e1 = a.rev.off[kk + 1];
+          for (uint32_t e = a.rev.off[kk]; e < e1; ++e) {
+            const uint32_t z = zcol[e] - (uint32_t)a.lo1;
+            ++cands;
+            if (z < W * 32u && ((f_row[z >> 5] >> (z & 31)) & 1u)) {
+              const uint32_t yb = y - (uint32_t)a.lo1;
+              atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
+              break;
+            }
+          }
+        }
+        __syncthreads();
+        continue;
+      }
       for (uint32_t r0 = (uint32_t)w * 64; r0 < nz; r0 += FR_WAVES * 64) {
         const uint32_t r = r0 + lane;
         uint32_t beg = 0, deg = 0;
@@ -1348,12 +1389,12 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
         s_excl[w][lane] = incl - sdeg;
         s_beg[w][lane] = beg;
         wave_lds_sync();
-        cands += total;
+        if (lane == 0) cands += total;
         while (bigm) {
           const int rb = __ffsll((long long)bigm) - 1;
           bigm &= bigm - 1;
           const uint32_t bb = __shfl(beg, rb, 64), bd = __shfl(deg, rb, 64);
-          cands += bd;
+          if (lane == 0) cands += bd;
           for (uint32_t k0 = 0; k0 < bd; k0 += 256) {
             uint32_t y[4];
 #pragma unroll
@@ -1404,6 +1445,7 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
     news += tnew;
   }
   // one atomic per workgroup for each total
+  for (int k = 32; k > 0; k >>= 1) cands += __shfl_xor(cands, k, 64);
   __shared__ u64 s_c[FR_WAVES];
   if (lane == 0) s_c[w] = cands;
   __syncthreads();
@@ -1417,7 +1459,7 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
 
 hipError_t frontier_round(const FrontierArgs& a, hipStream_t s) {
   if (a.nseg <= 0) return hipSuccess;
-  const size_t lds = (size_t)a.row_words * 2 * sizeof(uint32_t);
+  const size_t lds = (size_t)a.row_words * 3 * sizeof(uint32_t);
   const unsigned grid = (unsigned)std::min<int64_t>(a.nseg, 4096);
   frontier_round_k<<<grid, FR_THREADS, lds, s>>>(a);
   return hipGetLastError();
@@ -1521,6 +1563,23 @@ __global__ void add_u32_k(const uint32_t* in, uint32_t add, uint32_t* out, int64
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   add_u32_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(in, add, out, n);
+  return hipGetLastError();
+}
+
+// hasin bit (y - lo1) for y in [lo1, lo1 + 32 * words): y has an in-edge in
+// the index of e by its Y column.
+__global__ void hasin_bits_k(IndexProbe rev, int32_t lo1, uint32_t words, uint32_t* out) {
+  for (uint32_t wi = blockIdx.x * blockDim.x + threadIdx.x; wi < words; wi += gridDim.x * blockDim.x) {
+    uint32_t m = 0;
+    for (int b = 0; b < 32; ++b) {
+      const uint32_t kk = (uint32_t)lo1 + wi * 32u + (uint32_t)b - (uint32_t)rev.key_lo;
+      if (kk < rev.key_range && rev.off[kk + 1] > rev.off[kk]) m |= 1u << b;
+    }
+    out[wi] = m;
+  }
+}
+hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s) {
+  hasin_bits_k<<<grid_for(words, 256, 4096), 256, 0, s>>>(rev, lo1, words, out);
   return hipGetLastError();
 }
 

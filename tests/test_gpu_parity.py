@@ -77,6 +77,23 @@ def test_small_workload_with_forced_table_growth(name, index_mode):
     assert stats["table_grows"] > 0
 
 
+@pytest.mark.parametrize("pull_ratio", [0, 1, 64, 1024])
+@pytest.mark.parametrize("name", ["tc_uniform", "tc_rmat_count"])
+def test_closure_push_and_pull_directions(name, pull_ratio):
+    """Frontier rounds give the same closure whether sources push, pull or mix."""
+    wl = W.small_workloads()[name]()
+    print(f"case: direction {name} pull_ratio={pull_ratio}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"pull_ratio": pull_ratio})
+    _compare(wl, rels, ref)
+    assert stats["delta_rows"] == _delta_levels(ref, "path") + ([0] * (len(stats["delta_rows"]) - len(ref.sizes["path"])))
+
+
+def _delta_levels(ref, name):
+    sizes = ref.sizes[name]
+    return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
+
+
 def test_tc_delta_sizes_are_walk_levels():
     """Per-round |delta| of linear TC equals the number of pairs first joined at that walk length."""
     wl = W.small_workloads()["tc_uniform"]()
