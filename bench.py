@@ -36,20 +36,31 @@ DESCRIPTIONS = {
 
 
 KERNELS = {
-    "tc_rmat_count": "frontier_round_k (delta expand + membership test + merge, one first key per workgroup)",
-    "tc_uniform": "frontier_round_k (delta expand + membership test + merge, one first key per workgroup)",
+    "front": "frontier_round_k (delta expand or in-edge pull + membership test + merge, one first key per workgroup)",
+    "emit": "stage_k (fused delta expand + probe + insert)",
 }
 
 
-def _algorithmic_bytes(st: dict) -> float:
-    """Bytes the fused join/insert kernel must move, by its definition.
+def _algorithmic_bytes(candidates: float, new: float) -> float:
+    """Bytes the join/dedup/merge work must move, by its definition.
 
-    Per source (delta) row: the row (8 B) and its index range (8 B).  Per
-    candidate: the matched edge's target (4 B) and one probe of the packed key
-    (8 B).  Per new tuple: the key written to the table (8 B) and the row
-    appended to the relation (8 B).
+    Per candidate (a head tuple produced, or an edge examined): the matched
+    edge's endpoint (4 B) and one membership probe of the packed key (8 B).
+    Per new tuple: the key written to the full relation (8 B), the delta row
+    written (8 B) and read again by the next round (8 B).
     """
-    return 16.0 * st["emit_source_rows"] + 12.0 * st["emit_candidates"] + 16.0 * st["emit_new"]
+    return 12.0 * candidates + 24.0 * new
+
+
+def dominant_kernel(stats: list) -> dict:
+    """The join kernel family with the larger event-timed share: frontier
+    rounds (closure-shaped strata) or the generic fused stage kernel."""
+    front = sum(s["front_ms"] for s in stats)
+    emit = sum(s["emit_ms"] for s in stats)
+    k = "front" if front >= emit else "emit"
+    return {"family": k, "ms": front if k == "front" else emit,
+            "launches": sum(s[k + "_launches"] for s in stats),
+            "bytes": sum(_algorithmic_bytes(s[k + "_candidates"], s[k + "_new"]) for s in stats)}
 
 
 def recorded_traffic(workload: str):
@@ -153,19 +164,17 @@ def main():
     ms_per_step = 1e3 * dt / args.steps
     derived = stats[-1]["derived_tuples"]
 
-    emit_ms = sum(s["emit_ms"] for s in stats)
-    emit_launches = sum(s["emit_launches"] for s in stats)
-    ab = sum(_algorithmic_bytes(s) for s in stats)
-    achieved = ab / (emit_ms * 1e-3) / 1e9 if emit_ms > 0 else 0.0
-    traffic = recorded_traffic(args.workload)
+    dk = dominant_kernel(stats)
+    achieved = dk["bytes"] / (dk["ms"] * 1e-3) / 1e9 if dk["ms"] > 0 else 0.0
+    traffic = recorded_traffic(args.workload) if dk["family"] == "front" else None
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4),
         "traffic": round(traffic) if traffic is not None else None,
-        "kernel": KERNELS.get(args.workload, "stage_k (fused delta expand + probe + insert)"),
-        "launches_per_step": emit_launches / args.steps,
-        "avg_launch_ms": emit_ms / max(emit_launches, 1),
-        "algorithmic_bytes_per_step": ab / args.steps,
+        "kernel": KERNELS[dk["family"]],
+        "launches_per_step": dk["launches"] / args.steps,
+        "avg_launch_ms": dk["ms"] / max(dk["launches"], 1),
+        "algorithmic_bytes_per_launch": dk["bytes"] / max(dk["launches"], 1),
     }
     line = {
         "metric": "derived tuples/sec to fixpoint (1 MI355X)",

@@ -108,6 +108,13 @@ typedef struct {
     int64_t emit_source_rows;   /* delta or driver rows those launches read */
     int64_t emit_candidates;    /* head tuples they produced */
     int64_t emit_new;           /* keys they inserted (new or improved rows) */
+    /* Frontier rounds of closure-shaped strata (one bitmap row per first key),
+     * timed the same way. */
+    double front_ms;
+    int64_t front_launches;
+    int64_t front_candidates;   /* edges examined: produced tuples when pushing,
+                                   in-edges scanned when pulling */
+    int64_t front_new;          /* tuples added */
 } xl_fixpoint_stats;
 
 /*

@@ -376,6 +376,7 @@ struct Runner {
   Program* prog;
   xl_fixpoint_stats* st;
   std::vector<std::unique_ptr<DevIndex>> indexes;
+  std::vector<std::unique_ptr<DevIndex>> kept;  // ready indexes made while materializing
   std::vector<std::unique_ptr<HeadRun>> heads;
   int64_t cands = 0;
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -819,11 +820,10 @@ struct Runner {
     if (c->profile) {
       float ms = 0;
       HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
-      st->emit_ms += ms;
-      st->emit_launches++;
-      st->emit_source_rows += h->fn;
-      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
-      st->emit_new += (int64_t)cnt[CNT_APPENDED];
+      st->front_ms += ms;
+      st->front_launches++;
+      st->front_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->front_new += (int64_t)cnt[CNT_APPENDED];
     }
     h->fnew = (int64_t)cnt[CNT_APPENDED];
     h->keys += h->fnew;
@@ -875,6 +875,30 @@ struct Runner {
                                    h->fdiff[h->fcur].as<uint32_t>(), c->stream));
     h->fn = nseg;
     return XL_OK;
+  }
+
+  // h(X, count(V)) :- r(..., X, ..., V, ...) with distinct variables, nothing
+  // else in the body, over a finished relation that already has an index by
+  // X's column: returns that index (the count per X is its degree), else null.
+  const DevIndex* degree_index(const RulePlan& p) const {
+    if (p.nkey != 1 || !p.steps.empty() || p.driver_delta) return nullptr;
+    for (const auto& h : heads)
+      if (h->rel == p.driver) return nullptr;
+    for (const auto& ops : p.stage_ops)
+      if (!ops.empty()) return nullptr;
+    int kcol = -1;
+    for (int j = 0; j < p.driver->arity; ++j) {
+      const ColAct& a = p.driver_act[j];
+      if (a.kind != CA_BIND && a.kind != CA_NONE) return nullptr;
+      if (a.kind == CA_BIND && a.slot == p.key_slot[0]) {
+        if (kcol >= 0) return nullptr;
+        kcol = j;
+      }
+    }
+    if (kcol < 0) return nullptr;
+    for (const auto& ix : indexes)
+      if (ix->rel == p.driver && ix->col == kcol) return ix.get();
+    return nullptr;
   }
 
   xl_status eval_plan(const RulePlan& p) {
@@ -942,6 +966,17 @@ struct Runner {
       a.emit.val_slot = (int8_t)p.val_slot;
       a.emit.val_type = p.val_type;
       if (h->dcount) {
+        const DevIndex* dx = degree_index(p);
+        if (dx) {  // the group's count is the index degree of its key
+          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+          HIP_TRY(c, k::index_degree_add(dx->probe.off, dx->probe.key_range, dx->probe.key_lo, h->kp.lo[0],
+                                         (uint32_t)h->range0, h->counts.as<uint32_t>(), c->dcounters, c->stream));
+          u64 cnt[CNT_N];
+          XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+          if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "count key outside the head domain (internal)");
+          cands += src.n;
+          return XL_OK;
+        }
         a.emit.mode = EM_DCOUNT;
         a.emit.bits = h->counts.as<uint32_t>();
         a.emit.row_bits = (u64)h->range1;
@@ -1215,16 +1250,17 @@ struct Runner {
   xl_status materialize_rows(HeadRun* h) {
     Relation* r = h->rel;
     if (h->frontier) {  // every tuple is a set bit: rows in ascending (x, y)
-      Buf cnt, off, tmp, tot;
+      // off (range0 + 1 words) doubles as the CSR offsets of the finished
+      // relation by its first column, kept as a ready index for later strata
+      Buf cnt, off, tmp;
       XL_TRY(dalloc(c, (size_t)h->range0 * 4, &cnt, "row counts"));
-      XL_TRY(dalloc(c, (size_t)h->range0 * 4, &off, "row offsets"));
+      XL_TRY(dalloc(c, (size_t)(h->range0 + 1) * 4, &off, "row offsets"));
       XL_TRY(dalloc(c, k::scan_temp_bytes(h->range0), &tmp, "scan scratch"));
-      XL_TRY(dalloc(c, 8, &tot, "count"));
       HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
-      HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0, tot.as<uint32_t>(),
-                                       tmp.p, c->stream));
+      HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0,
+                                       off.as<uint32_t>() + h->range0, tmp.p, c->stream));
       uint32_t n = 0;
-      XL_TRY(ctl_read(c, tot.p, 4, &n));
+      XL_TRY(ctl_read(c, off.as<uint32_t>() + h->range0, 4, &n));
       if ((int64_t)n != h->keys) return c->fail(XL_DEVICE_ERROR, "bitmap row count mismatch (internal)");
       h->rows[0].reset();
       h->rows[1].reset();
@@ -1235,6 +1271,17 @@ struct Runner {
       relation_free_storage(r);
       for (int j = 0; j < 2; ++j) r->col[j] = (uint32_t*)out[j].keep();
       r->nrows = n;
+      auto ix = std::make_unique<DevIndex>();
+      ix->rel = r;
+      ix->col = 0;
+      ix->probe.off = off.as<uint32_t>();
+      ix->probe.ncols = 2;
+      for (int j = 0; j < 2; ++j) ix->probe.col[j] = r->col[j];
+      ix->probe.key_lo = h->kp.lo[0];
+      ix->probe.key_range = (uint32_t)h->range0;
+      ix->owned.push_back(std::make_unique<Buf>(c));
+      ix->owned.back()->p = off.keep();
+      kept.push_back(std::move(ix));
       return XL_OK;
     }
     if (h->dcount) {
@@ -1318,9 +1365,17 @@ struct Runner {
         record(total);
       }
     }
+    // indexes over this stratum's heads saw unfinished relations; the rest
+    // stay valid (a relation is final once its stratum ends)
+    for (auto& h : heads)
+      indexes.erase(std::remove_if(indexes.begin(), indexes.end(),
+                                   [&](const std::unique_ptr<DevIndex>& ix) { return ix->rel == h->rel; }),
+                    indexes.end());
+    kept.clear();
     for (auto& h : heads) XL_TRY(materialize(h.get()));
+    for (auto& ix : kept) indexes.push_back(std::move(ix));
+    kept.clear();
     heads.clear();
-    indexes.clear();
     return XL_OK;
   }
 };

@@ -105,6 +105,11 @@ hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words,
                         int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s);
 hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
                        hipStream_t s);
+// counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
+// with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
+hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
+                            uint32_t head_range, uint32_t* counts, u64* counters,
+                            hipStream_t s);
 // out[i] = in[i] + add
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s);
 

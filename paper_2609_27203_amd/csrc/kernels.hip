@@ -1566,6 +1566,30 @@ hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, h
   return hipGetLastError();
 }
 
+// Count fold of a one-atom body grouped by an indexed column: key x = key_lo + i
+// has off[i + 1] - off[i] rows, added to counts[x - head_lo].  One thread per
+// key, so no two threads touch one counter; a key with rows outside the head's
+// domain raises the fatal counter.
+__global__ void index_degree_add_k(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
+                                   uint32_t head_range, uint32_t* counts, u64* counters) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < key_range; i += gridDim.x * blockDim.x) {
+    const uint32_t d = off[i + 1] - off[i];
+    if (!d) continue;
+    const uint32_t hk = (uint32_t)key_lo + i - (uint32_t)head_lo;
+    if (hk < head_range)
+      counts[hk] += d;
+    else
+      atomicAdd(&counters[CNT_FATAL], 1ull);
+  }
+}
+hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
+                            uint32_t head_range, uint32_t* counts, u64* counters, hipStream_t s) {
+  if (key_range == 0) return hipSuccess;
+  index_degree_add_k<<<grid_for(key_range, 256, 65536), 256, 0, s>>>(off, key_range, key_lo, head_lo,
+                                                                      head_range, counts, counters);
+  return hipGetLastError();
+}
+
 // hasin bit (y - lo1) for y in [lo1, lo1 + 32 * words): y has an in-edge in
 // the index of e by its Y column.
 __global__ void hasin_bits_k(IndexProbe rev, int32_t lo1, uint32_t words, uint32_t* out) {

@@ -42,6 +42,8 @@ class xl_fixpoint_stats(C.Structure):
         ("ms_total", C.c_double),
         ("emit_ms", C.c_double), ("emit_launches", C.c_int64), ("emit_source_rows", C.c_int64),
         ("emit_candidates", C.c_int64), ("emit_new", C.c_int64),
+        ("front_ms", C.c_double), ("front_launches", C.c_int64), ("front_candidates", C.c_int64),
+        ("front_new", C.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -54,7 +56,8 @@ class xl_fixpoint_stats(C.Structure):
             "control_bytes_read": self.control_bytes_read, "table_grows": self.table_grows,
             "ms_total": self.ms_total, "emit_ms": self.emit_ms, "emit_launches": self.emit_launches,
             "emit_source_rows": self.emit_source_rows, "emit_candidates": self.emit_candidates,
-            "emit_new": self.emit_new,
+            "emit_new": self.emit_new, "front_ms": self.front_ms, "front_launches": self.front_launches,
+            "front_candidates": self.front_candidates, "front_new": self.front_new,
         }
 
 

@@ -89,6 +89,31 @@ def test_closure_push_and_pull_directions(name, pull_ratio):
     assert stats["delta_rows"] == _delta_levels(ref, "path") + ([0] * (len(stats["delta_rows"]) - len(ref.sizes["path"])))
 
 
+COUNT_SHAPES_RULES = W.TC_RULES + """
+out_count(X,count(Y)) :- path(X,Y).
+in_count(Y,count(X)) :- path(X,Y).
+far_count(X,count(Y)) :- path(X,Y), Y > X.
+back(X,Z) :- edge(X,Y), path(Y,Z).
+back_count(X,count(Z)) :- back(X,Z).
+"""
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_counts_and_joins_over_a_finished_closure(index_mode):
+    """Counts grouped by the closure's first column (read from its row offsets
+    when the closure ran in frontier form), by its second column, with a
+    filter, and a later join probing the closure by its first column."""
+    base = W.small_workloads()["tc_rmat_count"]()
+    idb = {"path": ("i32", "i32"), "out_count": ("i32", "i32"), "in_count": ("i32", "i32"),
+           "far_count": ("i32", "i32"), "back": ("i32", "i32"), "back_count": ("i32", "i32")}
+    wl = W.Workload("count_shapes", COUNT_SHAPES_RULES, base.edb, idb)
+    print(f"case: count shapes index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
+    _compare(wl, rels, ref)
+    assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
+
+
 def _delta_levels(ref, name):
     sizes = ref.sizes[name]
     return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
