@@ -1277,14 +1277,15 @@ hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const
 }
 
 // Frontier round (see FrontierArgs).  LDS holds bitmap row x before and after
-// the round plus a chunk of the delta row decoded into a list of Z values;
-// the delta row is consumed in chunks of FR_CHUNK words so the Z list stays
-// small.  The wave-balanced expansion of the Z list is the same as in the
-// generic stage kernel.  A plain LDS test precedes each LDS atomic because
-// most produced tuples are already known.
+// the round plus a piece of the delta row decoded into a list of Z values;
+// each step decodes up to 512 words, cut so the list holds at most FR_ZCAP
+// values (a sparse row takes one step).  The wave-balanced expansion of the
+// Z list is the same as in the generic stage kernel.  A plain LDS test
+// precedes each LDS atomic because most produced tuples are already known.
 constexpr int FR_THREADS = 256;
 constexpr int FR_WAVES = FR_THREADS / 64;
-constexpr int FR_CHUNK = 128;  // delta words decoded per step (<= 4096 Z values)
+constexpr uint32_t FR_ZCAP = 4096;  // Z (or Y) values decoded per step
+constexpr int FR_PROBE = 4;         // in-edges a pulling lane loads at once
 
 __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t* total, uint32_t* s_w) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
@@ -1302,15 +1303,38 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t* to
   return pre + incl - x;
 }
 
+// Workgroup totals of two per-thread counts (one barrier pair).
+__device__ __forceinline__ void block_sum2(uint32_t x, uint32_t y, uint32_t* tx, uint32_t* ty, uint32_t* s_w,
+                                           uint32_t* s_w2) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  for (int k = 32; k > 0; k >>= 1) {
+    x += __shfl_xor(x, k, 64);
+    y += __shfl_xor(y, k, 64);
+  }
+  if (lane == 0) {
+    s_w[w] = x;
+    s_w2[w] = y;
+  }
+  __syncthreads();
+  uint32_t a = 0, b = 0;
+  for (int k = 0; k < (int)(blockDim.x >> 6); ++k) {
+    a += s_w[k];
+    b += s_w2[k];
+  }
+  __syncthreads();
+  *tx = a;
+  *ty = b;
+}
+
 __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
   extern __shared__ uint32_t lds[];
   uint32_t* old_row = lds;
   uint32_t* new_row = lds + a.row_words;
   uint32_t* f_row = lds + 2 * a.row_words;  // this round's delta row of x
-  __shared__ uint32_t zlist[FR_CHUNK * 32];
+  __shared__ uint32_t zlist[FR_ZCAP];
   __shared__ uint32_t s_excl[FR_WAVES][64];
   __shared__ uint32_t s_beg[FR_WAVES][64];
-  __shared__ uint32_t s_w[FR_WAVES];
+  __shared__ uint32_t s_w[FR_WAVES], s_w2[FR_WAVES], s_cut[2];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const uint32_t W = a.row_words;
   const uint32_t* ycol = a.idx.col[a.ybind_col];
@@ -1334,35 +1358,52 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
       if (a.pull_ratio) nu += __popc(~v & a.hasin[i]);
     }
     uint32_t tnd, tnu;
-    block_excl_scan_u32(nd, &tnd, s_w);
-    block_excl_scan_u32(nu, &tnu, s_w);
+    block_sum2(nd, nu, &tnd, &tnu, s_w, s_w2);
     const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
-    for (uint32_t cb = 0; cb < W; cb += FR_CHUNK) {
-      // decode words [cb, cb + FR_CHUNK): push takes the delta's Z values,
-      // pull the unreached Y values that have an in-edge
-      const uint32_t wi = cb + threadIdx.x;
-      uint32_t d = 0;
-      if (threadIdx.x < FR_CHUNK && wi < W) d = pull ? (~old_row[wi] & a.hasin[wi]) : f_row[wi];
-      uint32_t nz;
-      uint32_t pos = block_excl_scan_u32(__popc(d), &nz, s_w);
-      for (uint32_t bits = d; bits; bits &= bits - 1)
-        zlist[pos++] = (uint32_t)a.lo1 + wi * 32u + (uint32_t)(__ffs(bits) - 1);
+    for (uint32_t cb = 0; cb < W;) {
+      // Decode words [cb, cb + 512), two per thread, cut after the last
+      // thread whose values still fit the list: push takes the delta's Z
+      // values, pull the unreached Y values that have an in-edge.
+      const uint32_t w0 = cb + 2u * threadIdx.x;
+      uint32_t d0 = 0, d1 = 0;
+      if (w0 < W) d0 = pull ? (~old_row[w0] & a.hasin[w0]) : f_row[w0];
+      if (w0 + 1 < W) d1 = pull ? (~old_row[w0 + 1] & a.hasin[w0 + 1]) : f_row[w0 + 1];
+      const uint32_t c = __popc(d0) + __popc(d1);
+      uint32_t tot;
+      uint32_t pos = block_excl_scan_u32(c, &tot, s_w);
+      if (pos + c <= FR_ZCAP) {
+        for (uint32_t bits = d0; bits; bits &= bits - 1)
+          zlist[pos++] = (uint32_t)a.lo1 + w0 * 32u + (uint32_t)(__ffs(bits) - 1);
+        for (uint32_t bits = d1; bits; bits &= bits - 1)
+          zlist[pos++] = (uint32_t)a.lo1 + (w0 + 1) * 32u + (uint32_t)(__ffs(bits) - 1);
+      } else if (pos <= FR_ZCAP) {  // the first thread that does not fit
+        s_cut[0] = pos;
+        s_cut[1] = 2u * threadIdx.x;
+      }
       __syncthreads();
+      const uint32_t nz = tot <= FR_ZCAP ? tot : s_cut[0];
+      cb += tot <= FR_ZCAP ? 2u * FR_THREADS : s_cut[1];
       if (pull) {
-        // one lane per unreached Y: scan its in-edges until one comes from the delta
+        // One lane per unreached Y: test its in-edges FR_PROBE at a time
+        // (independent loads) until one comes from the delta.
         for (uint32_t r = threadIdx.x; r < nz; r += FR_THREADS) {
           const uint32_t y = zlist[r];
           const uint32_t kk = y - (uint32_t)a.rev.key_lo;
           if (kk >= a.rev.key_range) continue;
           const uint32_t e1 = a.rev.off[kk + 1];
-          for (uint32_t e = a.rev.off[kk]; e < e1; ++e) {
-            const uint32_t z = zcol[e] - (uint32_t)a.lo1;
-            ++cands;
-            if (z < W * 32u && ((f_row[z >> 5] >> (z & 31)) & 1u)) {
-              const uint32_t yb = y - (uint32_t)a.lo1;
-              atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
-              break;
-            }
+          bool hit = false;
+          for (uint32_t e = a.rev.off[kk]; e < e1 && !hit; e += FR_PROBE) {
+            uint32_t zz[FR_PROBE];
+#pragma unroll
+            for (int u = 0; u < FR_PROBE; ++u) zz[u] = e + u < e1 ? zcol[e + u] - (uint32_t)a.lo1 : 0xffffffffu;
+#pragma unroll
+            for (int u = 0; u < FR_PROBE; ++u)
+              hit = hit || (zz[u] < W * 32u && ((f_row[zz[u] >> 5] >> (zz[u] & 31)) & 1u));
+            cands += e1 - e < (uint32_t)FR_PROBE ? e1 - e : (uint32_t)FR_PROBE;
+          }
+          if (hit) {
+            const uint32_t yb = y - (uint32_t)a.lo1;
+            atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
           }
         }
         __syncthreads();
