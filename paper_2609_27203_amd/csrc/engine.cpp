@@ -575,9 +575,11 @@ struct Runner {
           hr->range0 = range0;
           hr->row_bits = row_bits;
           hr->row_words = (uint32_t)std::min<u64>(row_bits / 32, 0xffffffffull);
-          // frontier form: the stratum is this head alone with one closure-shaped variant
+          // frontier form: the stratum is this head alone with one closure-shaped
+          // variant; its kernel stages three rows of row_words words plus about
+          // 19 KB in LDS, which must stay within a workgroup's 64 KB
           hr->frontier = s.recursive && s.heads.size() == 1 && s.variants.size() == 1 &&
-                         s.variants[0].carried && hr->nkey == 2 && hr->row_words <= 4096 &&
+                         s.variants[0].carried && hr->nkey == 2 && hr->row_words <= 3072 &&
                          total_bits / 8 * 3 <= budget;
         }
       }

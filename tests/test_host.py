@@ -95,6 +95,8 @@ def test_options():
     c = xlh.Context(device=-1)
     c.set_option("hash_min_log2", 12)
     c.set_option("profile", 1)
-    for k, v in [("hash_min_log2", 3), ("nope", 1), ("profile", 7)]:
+    c.set_option("pull_ratio", 0)
+    for k, v in [("hash_min_log2", 3), ("nope", 1), ("profile", 7), ("pull_ratio", 2000),
+                 ("index_mode", -1)]:
         with pytest.raises(xlh.XlError):
             c.set_option(k, v)
