@@ -79,6 +79,8 @@ enum EmitMode : int32_t {
   EM_MINMAX = 3,  // atomic improvement in a keyed table; improved keys to delta
   EM_BITSET = 4,  // test-and-set in a dense key-domain bitmap; winners append head rows
   EM_DCOUNT = 5,  // count per key in a dense counter array (runs of equal keys combined)
+  EM_DMIN = 6,    // atomic improvement in a dense value array over (dictionary rank of
+                  // the first key) x (second key); improved slots to delta
 };
 
 // Device-side counters of one emission (cleared per round).
@@ -121,7 +123,14 @@ struct EmitSpec {
   // EM_MINMAX
   Slot16* table16;
   uint32_t round;
-  uint32_t* delta_idx;
+  uint32_t* delta_idx;       // EM_MINMAX / EM_DMIN: improved slots of this round
+  // EM_DMIN: slot = dmap[k0 - lo0] * row_bits + (k1 - lo1) of the value array
+  // `bits`; dpres marks slots holding a value, dchg slots already listed in
+  // this round's delta.
+  const uint32_t* dmap;
+  uint32_t dmap_n;
+  uint32_t* dpres;
+  uint32_t* dchg;
   // shared
   unsigned long long* counters;
   unsigned long long limit;  // overflow threshold on CNT_INSERTED

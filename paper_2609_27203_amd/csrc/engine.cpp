@@ -367,6 +367,13 @@ struct HeadRun {
   bool dcount = false;
   Buf counts;
   int64_t range1 = 1;
+  // dense value heads (min/max): value array over (rank of the first key in
+  // a dictionary of its possible values) x (second key - lo1), presence and
+  // listed-this-round bits, and the dictionary (dmap: value - lo0 -> rank)
+  bool dv = false;
+  Buf dmap, dict, dvals, dpres, dchg;
+  int64_t n0 = 0, dmap_n = 0;
+  std::vector<std::pair<Relation*, int>> dict_src;
   // key-column domains (bounds recorded on the materialized relation)
   int64_t dom_lo[2] = {0, 0}, dom_hi[2] = {0, 0};
 };
@@ -474,6 +481,41 @@ struct Runner {
     return Interval{rel->lo[col], rel->hi[col]};
   }
 
+  // A min/max head can use a dense value array when every rule binds its
+  // first key from a finished relation's column (a superset of the values it
+  // can take) or carries it over from the head's own first column.  The
+  // dictionary is the union of those columns (and of rows already loaded
+  // into the head).
+  void plan_dense_values(const Stratum& s, HeadRun* hr) {
+    Relation* h = hr->rel;
+    const int64_t r0 = hr->dom_hi[0] - hr->dom_lo[0] + 1;
+    const int64_t r1 = hr->nkey == 2 ? hr->dom_hi[1] - hr->dom_lo[1] + 1 : 1;
+    if (r0 <= 0 || r0 > ((int64_t)1 << 28) || r1 <= 0 || r1 > ((int64_t)1 << 30)) return;
+    std::vector<std::pair<Relation*, int>> src;
+    for (const RulePlan& p : s.full) {
+      if (p.head != h) continue;
+      const int sl = p.key_slot[0];
+      if (p.var_is_arith[sl]) return;
+      bool carried = false;
+      std::pair<Relation*, int> best{nullptr, 0};
+      for (const auto& vs : p.var_sources[sl]) {
+        if (vs.first == h && vs.second == 0) carried = true;
+        bool in_stratum = false;
+        for (Relation* o : s.heads) in_stratum = in_stratum || o == vs.first;
+        if (in_stratum || vs.first->types[vs.second] != T_I32) continue;
+        if (!best.first || vs.first->nrows < best.first->nrows) best = vs;
+      }
+      if (carried) continue;
+      if (!best.first) return;
+      src.push_back(best);
+    }
+    if (h->nrows > 0) src.push_back({h, 0});  // loaded rows
+    hr->dv = true;
+    hr->dmap_n = r0;
+    hr->range1 = r1;
+    hr->dict_src = src;
+  }
+
   xl_status setup_heads(Stratum& s) {
     std::map<Relation*, std::vector<Interval>> dom;
     for (Relation* h : s.heads) {
@@ -557,6 +599,7 @@ struct Runner {
           hr->range1 = r1;
         }
       }
+      if (hr->is_minmax && c->index_mode != 1) plan_dense_values(s, hr.get());
       if (hr->is_set && c->index_mode != 1) {
         const Interval i0 = d[0].empty() ? Interval{0, 0} : d[0];
         const int64_t range0 = i0.hi - i0.lo + 1;
@@ -654,8 +697,66 @@ struct Runner {
     return XL_OK;
   }
 
+  // Build the first-key dictionary, then the dense arrays if they fit; a
+  // head that does not fit falls back to the hash table (h->dv cleared).
+  xl_status init_dv(HeadRun* h) {
+    Relation* r = h->rel;
+    const uint32_t range = (uint32_t)h->dmap_n;
+    Buf pos, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)range * 4, &h->dmap, "key dictionary map"));
+    HIP_TRY(c, hipMemsetAsync(h->dmap.p, 0, (size_t)range * 4, c->stream));
+    for (const auto& sc : h->dict_src) {
+      const int64_t n = sc.first == r ? h->preloaded : sc.first->nrows;
+      HIP_TRY(c, k::dict_mark(sc.first->col[sc.second], n, h->kp.lo[0], range, h->dmap.as<uint32_t>(),
+                              c->stream));
+    }
+    XL_TRY(dalloc(c, (size_t)range * 4, &pos, "key dictionary ranks"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(range), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    HIP_TRY(c, k::scan_exclusive_u32(h->dmap.as<uint32_t>(), pos.as<uint32_t>(), range, tot.as<uint32_t>(),
+                                     tmp.p, c->stream));
+    uint32_t n0 = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &n0));
+    h->n0 = n0;
+    const double slots = (double)std::max<uint32_t>(n0, 1) * (double)h->range1;
+    const double budget = std::min(8589934592.0, (double)c->arena.capacity() / 4);
+    if (slots >= 4294967296.0 || slots * 8.25 > budget) {
+      h->dv = false;
+      h->dmap.reset();
+      return XL_OK;
+    }
+    XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(n0, 1) * 4, &h->dict, "key dictionary"));
+    HIP_TRY(c, k::dict_finish(h->dmap.as<uint32_t>(), pos.as<uint32_t>(), range, h->kp.lo[0],
+                              h->dict.as<uint32_t>(), c->stream));
+    const size_t ns = (size_t)slots, nw = (ns + 31) / 32;
+    XL_TRY(dalloc(c, ns * 4, &h->dvals, "dense values"));
+    XL_TRY(dalloc(c, nw * 4, &h->dpres, "dense presence bits"));
+    XL_TRY(dalloc(c, nw * 4, &h->dchg, "dense delta bits"));
+    XL_TRY(dalloc(c, ns * 4, &h->didx, "delta slot list"));
+    HIP_TRY(c, hipMemsetAsync(h->dvals.p, 0xff, ns * 4, c->stream));
+    HIP_TRY(c, hipMemsetAsync(h->dpres.p, 0, nw * 4, c->stream));
+    HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nw * 4, c->stream));
+    h->keys = 0;
+    if (h->preloaded) {
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      HIP_TRY(c, k::dense_insert_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dmap.as<uint32_t>(),
+                                      range, (uint32_t)h->range1, r->col[0], h->nkey == 2 ? r->col[1] : nullptr,
+                                      r->col[h->nkey], h->preloaded, h->kp, r->types[h->nkey],
+                                      h->agg == Agg::MAX, c->dcounters, c->stream));
+      u64 cnt[CNT_N];
+      XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+      if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "loaded row outside the dense domain (internal)");
+      h->keys = (int64_t)cnt[CNT_INSERTED];
+    }
+    return XL_OK;
+  }
+
   xl_status init_head(HeadRun* h) {
     Relation* r = h->rel;
+    if (h->dv) {
+      XL_TRY(init_dv(h));
+      if (h->dv) return XL_OK;
+    }
     if (h->dense) return init_dense(h);
     if (h->dcount) return init_dcount(h);
     h->cap = initial_cap(h->preloaded);
@@ -1032,7 +1133,19 @@ struct Runner {
         // limit is crossed, so the limit leaves room for all of them: the
         // table can never fill and the row list never overflows.
         const int64_t waves = std::min<int64_t>((a.src.n + 63) / 64, (int64_t)EMIT_GRID * 4);
-        if (h->dense) {
+        if (h->dv) {  // every slot exists up front: nothing can overflow
+          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+          a.emit.limit = ~0ull;
+          a.emit.mode = EM_DMIN;
+          a.emit.bits = h->dvals.as<uint32_t>();
+          a.emit.row_bits = (u64)h->range1;
+          a.emit.dmap = h->dmap.as<uint32_t>();
+          a.emit.dmap_n = (uint32_t)h->dmap_n;
+          a.emit.dpres = h->dpres.as<uint32_t>();
+          a.emit.dchg = h->dchg.as<uint32_t>();
+          a.emit.is_max = h->agg == Agg::MAX;
+          a.emit.delta_idx = h->didx.as<uint32_t>() + h->didx_n;
+        } else if (h->dense) {
           const int64_t max_rows = h->rows_cap - WAVE_SLACK * waves - 1024;
           if (h->nrows >= max_rows) {
             XL_TRY(grow_rows(h, h->nrows + 2 * (WAVE_SLACK * waves + 1024)));
@@ -1057,8 +1170,8 @@ struct Runner {
         a.emit.limit = (u64)(max_keys - h->keys);
         a.emit.mask = (u64)h->cap - 1;
         }
-        if (h->dense) {
-          // EM_BITSET configured above
+        if (h->dense || h->dv) {
+          // EM_BITSET / EM_DMIN configured above
         } else if (h->is_set) {
           a.emit.mode = EM_SET;
           a.emit.table = h->table.as<u64>();
@@ -1088,7 +1201,8 @@ struct Runner {
           st->emit_new += (int64_t)(h->is_set ? cnt[CNT_APPENDED] : cnt[CNT_INSERTED] + cnt[CNT_APPENDED]);
         }
         if (cnt[CNT_FATAL])
-          return c->fail(XL_DEVICE_ERROR, "hash table probe exhausted or row list overflow (internal)");
+          return c->fail(XL_DEVICE_ERROR, h->dv ? "key outside the dense domain (internal)"
+                                                : "hash table probe exhausted or row list overflow (internal)");
         cands += (int64_t)cnt[CNT_CANDIDATES];
         if (h->is_set) {
           h->nrows += (int64_t)cnt[CNT_APPENDED];
@@ -1154,6 +1268,17 @@ struct Runner {
     if (h->dcount) {
       *delta = 0;
       return XL_OK;  // counted in place; rows are produced at materialization
+    }
+    if (h->dv) {
+      XL_TRY(ensure_drow(h, h->didx_n));
+      HIP_TRY(c, k::dense_delta_rows(h->didx.as<uint32_t>(), h->didx_n, h->dvals.as<uint32_t>(),
+                                     h->dchg.as<uint32_t>(), h->dict.as<uint32_t>(), (uint32_t)h->range1,
+                                     h->kp.lo[1], h->rel->types[h->nkey], h->fold, h->drow[0].as<uint32_t>(),
+                                     h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
+                                     h->drow[h->nkey].as<uint32_t>(), c->stream));
+      h->dn = h->didx_n;
+      *delta = h->dn;
+      return XL_OK;
     }
     if (h->is_minmax) {
       XL_TRY(ensure_drow(h, h->didx_n));
@@ -1308,7 +1433,24 @@ struct Runner {
         return c->fail(XL_CAPACITY_EXCEEDED, "relation " + r->name + " exceeds its max_rows");
       return XL_OK;
     }
-    if (h->is_set) {
+    if (h->dv) {
+      const int64_t n = h->keys;
+      const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+      Buf out[3], tmp, tot;
+      for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
+      XL_TRY(dalloc(c, k::compact_temp_bytes(ns), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
+                               h->range1, h->kp, r->types[h->nkey], h->fold, out[0].as<uint32_t>(),
+                               h->nkey == 2 ? out[1].as<uint32_t>() : nullptr, out[h->nkey].as<uint32_t>(),
+                               std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p, c->stream));
+      uint32_t m = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &m));
+      if ((int64_t)m != n) return c->fail(XL_DEVICE_ERROR, "dense value count mismatch (internal)");
+      relation_free_storage(r);
+      for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
+      r->nrows = n;
+    } else if (h->is_set) {
       relation_free_storage(r);
       for (int j = 0; j < h->nkey; ++j) r->col[j] = (uint32_t*)h->rows[j].keep();
       r->nrows = h->nrows;

@@ -105,6 +105,20 @@ hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words,
                         int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s);
 hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
                        hipStream_t s);
+// Dense value heads (first key through a dictionary, second key direct).
+// Rows of every present slot in slot order (= ascending keys).
+hipError_t dense_rows(const uint32_t* vals, const uint32_t* pres, const uint32_t* dict, int64_t n,
+                      int64_t range1, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      uint32_t* v, int64_t out_cap, uint32_t* total, void* temp, hipStream_t s);
+hipError_t dict_mark(const uint32_t* col, int64_t n, int32_t lo, uint32_t range, uint32_t* mark, hipStream_t s);
+hipError_t dict_finish(uint32_t* map, const uint32_t* pos, uint32_t range, int32_t lo, uint32_t* dict,
+                       hipStream_t s);
+hipError_t dense_insert_rows(uint32_t* vals, uint32_t* pres, const uint32_t* map, uint32_t map_n, uint32_t range1,
+                             const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, KeyPack kp,
+                             int type, int is_max, u64* counters, hipStream_t s);
+hipError_t dense_delta_rows(const uint32_t* idx, int64_t n, const uint32_t* vals, uint32_t* chg, const uint32_t* dict,
+                            uint32_t range1, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                            uint32_t* v, hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,

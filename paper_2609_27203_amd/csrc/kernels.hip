@@ -583,12 +583,14 @@ hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n
 constexpr int CP_THREADS = 256;
 constexpr int CP_RANGE = CP_THREADS * 32;
 
-enum CompactKind { CK_NONEMPTY = 0, CK_STAMP = 1, CK_COUNTER = 2 };
+enum CompactKind { CK_NONEMPTY = 0, CK_STAMP = 1, CK_COUNTER = 2, CK_DENSE = 3 };
 
 struct CompactArgs {
   int kind;
   const Slot16* t;        // CK_NONEMPTY / CK_STAMP
-  const uint32_t* counts; // CK_COUNTER
+  const uint32_t* counts; // CK_COUNTER; CK_DENSE: value array
+  const uint32_t* pres;   // CK_DENSE: presence bits
+  const uint32_t* dict;   // CK_DENSE: first-key dictionary
   int64_t n;
   uint32_t round;         // CK_STAMP
   KeyPack kp;
@@ -605,6 +607,7 @@ struct CompactArgs {
 __device__ __forceinline__ bool cp_keep(const CompactArgs& a, int64_t i) {
   if (i >= a.n) return false;
   if (a.kind == CK_COUNTER) return a.counts[i] != 0;
+  if (a.kind == CK_DENSE) return (a.pres[i >> 5] >> (i & 31)) & 1u;
   const Slot16 s = a.t[i];
   if (s.key == EMPTY_KEY) return false;
   return a.kind == CK_NONEMPTY || s.stamp == a.round;
@@ -630,6 +633,10 @@ __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
     if (keep && p < (u64)a.out_cap) {
       if (a.kind == CK_STAMP) {
         a.k0[p] = (uint32_t)i;
+      } else if (a.kind == CK_DENSE) {
+        a.k0[p] = a.dict[i / a.range1];
+        if (a.k1) a.k1[p] = (uint32_t)(i % a.range1) + (uint32_t)a.kp.lo[1];
+        a.v[p] = stored_value(a.counts[i], a.type, a.fold_kind);
       } else if (a.kind == CK_COUNTER) {
         if (a.kp.nkey == 2) {
           a.k0[p] = (uint32_t)(i / a.range1) + (uint32_t)a.kp.lo[0];
@@ -715,6 +722,108 @@ hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, KeyPac
   a.v = v;
   a.out_cap = out_cap;
   return compact_run(a, total, temp, s);
+}
+
+hipError_t dense_rows(const uint32_t* vals, const uint32_t* pres, const uint32_t* dict, int64_t n,
+                      int64_t range1, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      uint32_t* v, int64_t out_cap, uint32_t* total, void* temp, hipStream_t s) {
+  CompactArgs a{};
+  a.kind = CK_DENSE;
+  a.counts = vals;
+  a.pres = pres;
+  a.dict = dict;
+  a.n = n;
+  a.kp = kp;
+  a.type = type;
+  a.fold_kind = fold_kind;
+  a.range1 = range1;
+  a.k0 = k0;
+  a.k1 = k1;
+  a.v = v;
+  a.out_cap = out_cap;
+  return compact_run(a, total, temp, s);
+}
+
+// ---- first-key dictionaries ---------------------------------------------------
+// mark[v - lo] = 1 for every value of a column that falls in [lo, lo + range).
+__global__ void dict_mark_k(const uint32_t* col, int64_t n, int32_t lo, uint32_t range, uint32_t* mark) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t k = col[i] - (uint32_t)lo;
+    if (k < range) mark[k] = 1u;
+  }
+}
+hipError_t dict_mark(const uint32_t* col, int64_t n, int32_t lo, uint32_t range, uint32_t* mark, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dict_mark_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(col, n, lo, range, mark);
+  return hipGetLastError();
+}
+
+// Marked values get consecutive ranks in value order: map[k] = rank (or
+// ~0 when unmarked; map may be the mark array itself), dict[rank] = lo + k.
+__global__ void dict_finish_k(uint32_t* map, const uint32_t* pos, uint32_t range, int32_t lo, uint32_t* dict) {
+  for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < range; k += gridDim.x * blockDim.x) {
+    const bool m = map[k] != 0;
+    if (m) dict[pos[k]] = (uint32_t)lo + k;
+    map[k] = m ? pos[k] : 0xffffffffu;
+  }
+}
+hipError_t dict_finish(uint32_t* map, const uint32_t* pos, uint32_t range, int32_t lo, uint32_t* dict,
+                       hipStream_t s) {
+  if (range == 0) return hipSuccess;
+  dict_finish_k<<<grid_for(range, 256, 65536), 256, 0, s>>>(map, pos, range, lo, dict);
+  return hipGetLastError();
+}
+
+// Preloaded rows into a dense value head: improve the value, set presence,
+// count keys that were absent.
+__global__ void dense_insert_rows_k(uint32_t* vals, uint32_t* pres, const uint32_t* map, uint32_t map_n,
+                                    uint32_t range1, const uint32_t* c0, const uint32_t* c1, const uint32_t* v,
+                                    int64_t n, KeyPack kp, int type, int is_max, u64* counters) {
+  uint32_t mine = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t k0 = c0[i] - (uint32_t)kp.lo[0];
+    const uint32_t k1 = c1 ? c1[i] - (uint32_t)kp.lo[1] : 0u;
+    const uint32_t r0 = k0 < map_n ? map[k0] : 0xffffffffu;
+    if (r0 == 0xffffffffu || k1 >= range1) {
+      atomicOr(&counters[CNT_FATAL], 4ull);
+      continue;
+    }
+    const uint32_t slot = r0 * range1 + k1;
+    atomicMin(&vals[slot], fold_encode(v[i], type, is_max));
+    const uint32_t bit = 1u << (slot & 31);
+    mine += (atomicOr(&pres[slot >> 5], bit) & bit) == 0;
+  }
+  block_count_add(&counters[CNT_INSERTED], mine);
+}
+hipError_t dense_insert_rows(uint32_t* vals, uint32_t* pres, const uint32_t* map, uint32_t map_n, uint32_t range1,
+                             const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, KeyPack kp,
+                             int type, int is_max, u64* counters, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dense_insert_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(vals, pres, map, map_n, range1, c0, c1, v, n, kp,
+                                                             type, is_max, counters);
+  return hipGetLastError();
+}
+
+// Delta rows of the listed slots (values read after the round, i.e. the
+// round's best), clearing each slot's listed bit for the next round.
+__global__ void dense_delta_rows_k(const uint32_t* idx, int64_t n, const uint32_t* vals, uint32_t* chg,
+                                   const uint32_t* dict, uint32_t range1, int32_t lo1, int type, int fold_kind,
+                                   uint32_t* k0, uint32_t* k1, uint32_t* v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t slot = idx[i];
+    k0[i] = dict[slot / range1];
+    if (k1) k1[i] = slot % range1 + (uint32_t)lo1;
+    v[i] = stored_value(vals[slot], type, fold_kind);
+    atomicAnd(&chg[slot >> 5], ~(1u << (slot & 31)));
+  }
+}
+hipError_t dense_delta_rows(const uint32_t* idx, int64_t n, const uint32_t* vals, uint32_t* chg, const uint32_t* dict,
+                            uint32_t range1, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                            uint32_t* v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dense_delta_rows_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(idx, n, vals, chg, dict, range1, lo1, type, fold_kind,
+                                                             k0, k1, v);
+  return hipGetLastError();
 }
 
 // ============================================================ stage kernel
@@ -858,7 +967,7 @@ __device__ __forceinline__ void flush_rows(KernArgs& a, EmitState& st) {
   typedef XL_KARG const EmitSpec KEmit;
   KEmit& e = a.emit;
   const int lane = lane_id();
-  if (MODE == EM_MINMAX && st.ins_pend) {
+  if ((MODE == EM_MINMAX || MODE == EM_DMIN) && st.ins_pend) {
     u64 b = 0;
     if (lane == 0) {
       b = atomicAdd(&e.counters[CNT_INSERTED], (u64)st.ins_pend);
@@ -873,12 +982,13 @@ __device__ __forceinline__ void flush_rows(KernArgs& a, EmitState& st) {
   u64 base = 0;
   if (lane == 0) {
     base = atomicAdd(&e.counters[CNT_APPENDED], (u64)st.buf_n);
-    if (MODE != EM_MINMAX && base + st.buf_n > e.limit) atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
+    if (MODE != EM_MINMAX && MODE != EM_DMIN && base + st.buf_n > e.limit)
+      atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
   }
   base = shfl_u64(base, 0);
-  if (MODE != EM_MINMAX && base + st.buf_n > e.limit) st.stop = true;
+  if (MODE != EM_MINMAX && MODE != EM_DMIN && base + st.buf_n > e.limit) st.stop = true;
   for (uint32_t i = lane; i < st.buf_n; i += 64) {
-    if (MODE == EM_MINMAX) {
+    if (MODE == EM_MINMAX || MODE == EM_DMIN) {
       e.delta_idx[base + i] = st.buf0[i];
     } else {
       const u64 p = (u64)e.row_base + base + i;
@@ -993,6 +1103,44 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     }
     return;
   }
+  if (MODE == EM_DMIN) {
+    // Dense slots: a plain read first (most candidates do not improve), then
+    // one atomicMin.  A slot holds a key once its presence bit is set; the
+    // lane that sets it counts the key.  The first lane to improve a slot in
+    // this round lists it in the delta.
+    bool ins = false, app = false;
+    uint32_t slot = 0;
+    if (act) {
+      const uint32_t k0 = getv(u, e.key.slot[0]) - (uint32_t)e.key.lo[0];
+      const uint32_t k1 = e.key.nkey == 2 ? getv(u, e.key.slot[1]) - (uint32_t)e.key.lo[1] : 0u;
+      const uint32_t r0 = k0 < e.dmap_n ? e.dmap[k0] : 0xffffffffu;
+      if (r0 == 0xffffffffu || (u64)k1 >= e.row_bits) {
+        atomicOr(&e.counters[CNT_FATAL], 4ull);  // key outside the planned domain
+      } else {
+        slot = r0 * (uint32_t)e.row_bits + k1;
+        const uint32_t enc = fold_encode(getv(u, e.val_slot), e.val_type, e.is_max);
+        const uint32_t cur = e.bits[slot];
+        bool better = false;
+        uint32_t old = cur;
+        if (enc < cur) {
+          old = atomicMin(&e.bits[slot], enc);
+          better = enc < old;
+        }
+        const uint32_t bit = 1u << (slot & 31);
+        if ((better && old == 0xffffffffu) || (enc == 0xffffffffu && cur == 0xffffffffu))
+          ins = (atomicOr(&e.dpres[slot >> 5], bit) & bit) == 0;
+        if (better || ins) app = (atomicOr(&e.dchg[slot >> 5], bit) & bit) == 0;
+      }
+    }
+    st.ins_pend += (uint32_t)__popcll(__ballot(ins));
+    const u64 ma = __ballot(app);
+    if (ma || st.ins_pend + 64 > OUTB) {
+      if (st.buf_n + 64 > OUTB || st.ins_pend + 64 > OUTB) flush_rows<MODE>(a, st);
+      if (app) st.buf0[st.buf_n + (uint32_t)__popcll(ma & lt)] = slot;
+      st.buf_n += (uint32_t)__popcll(ma);
+    }
+    return;
+  }
   if (MODE == EM_MINMAX) {
     bool ins = false, app = false;
     u64 slot = ~0ull;
@@ -1026,7 +1174,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   __shared__ uint32_t s_excl[ST_WAVES][64];
   __shared__ uint32_t s_beg[ST_WAVES][64];
   __shared__ uint32_t s_v[ST_WAVES][MAXV][64];
-  constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX;
+  constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DMIN;
   __shared__ uint32_t s_out[STAGED ? ST_WAVES : 1][2][STAGED ? OUTB : 1];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int64_t nchunks = (a.src.n + 63) / 64;
@@ -1093,7 +1241,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     }
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
   }
-  if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT) {
+  if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT || MODE == EM_DMIN) {
     // one atomic per workgroup: a shared counter hit by every wave serializes
     __shared__ u64 s_cands[ST_WAVES];
     if (lane == 0) s_cands[w] = st.cands;
@@ -1124,6 +1272,7 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
     case EM_MAT: launch_mode<EM_MAT>(a, grid, s); break;
     case EM_SET: launch_mode<EM_SET>(a, grid, s); break;
     case EM_BITSET: launch_mode<EM_BITSET>(a, grid, s); break;
+    case EM_DMIN: launch_mode<EM_DMIN>(a, grid, s); break;
     default: launch_mode<EM_MINMAX>(a, grid, s); break;
   }
   return hipGetLastError();
