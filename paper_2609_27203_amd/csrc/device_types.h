@@ -81,6 +81,7 @@ enum EmitMode : int32_t {
   EM_DCOUNT = 5,  // count per key in a dense counter array (runs of equal keys combined)
   EM_DMIN = 6,    // atomic improvement in a dense value array over (dictionary rank of
                   // the first key) x (second key); improved slots to delta
+  EM_MARK = 7,    // set the bit of the same dense slot (keys that receive a contribution)
 };
 
 // Device-side counters of one emission (cleared per round).
@@ -144,6 +145,38 @@ struct StageArgs {
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];
   EmitSpec emit;
+};
+
+// One round of a carried-value rule over a dense sum/logsumexp head, for the
+// keys marked in the round: key (s, y) folds the contributions of every row
+// of e whose Y column is y (rev) and whose Z value z has (s, z) in the
+// current delta, evaluating the rule's comparisons and arithmetic per row.
+// Slot of (s, y) = rank(s) * range1 + (y - lo1); a thread owns one listed
+// slot, so the fold order is the index order and the result deterministic.
+struct DensePullArgs {
+  const uint32_t* list;   // marked slots, ascending
+  int64_t n;
+  const uint32_t* dict;   // rank -> first key value
+  uint32_t range1;
+  int32_t lo1;
+  IndexProbe rev;         // e indexed by its Y column; act[] = the rule's actions on e
+  int32_t zcol;
+  int8_t slot_s, slot_z, slot_y, slot_p, val_slot;
+  uint8_t val_type;
+  int32_t fold_kind;
+  int32_t nops;
+  MicroOp ops[MAXOPS];
+  uint32_t consts[MAXK];
+  const uint32_t* cval;   // current delta: values and presence bits
+  const uint32_t* cpres;
+  uint32_t* nval;         // next delta: values and presence bits
+  uint32_t* npres;
+  uint32_t* fval;         // full relation: values and presence bits
+  uint32_t* fpres;
+  uint32_t* k0;           // next delta rows, row i for list[i]
+  uint32_t* k1;
+  uint32_t* v;
+  unsigned long long* counters;  // CNT_INSERTED: keys new to the full relation; CNT_FATAL
 };
 
 // Closure-shaped recursive rule head(X, Y) :- delta head(X, Z), e(Z, Y) over a

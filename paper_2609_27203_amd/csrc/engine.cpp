@@ -374,6 +374,14 @@ struct HeadRun {
   Buf dmap, dict, dvals, dpres, dchg;
   int64_t n0 = 0, dmap_n = 0;
   std::vector<std::pair<Relation*, int>> dict_src;
+  // dense sum/logsumexp heads (one carried-value variant): the same slots;
+  // dvals/dpres hold the full relation, dcur/dcur_pres this round's delta,
+  // dnext/dnext_pres the next one, dchg the keys marked for the pull
+  bool ds = false;
+  Buf dcur, dcur_pres, dnext, dnext_pres;
+  Buf ndrow[3];
+  bool pulled = false;
+  int64_t pull_n = 0;
   // key-column domains (bounds recorded on the materialized relation)
   int64_t dom_lo[2] = {0, 0}, dom_hi[2] = {0, 0};
 };
@@ -509,7 +517,7 @@ struct Runner {
       if (!best.first) return;
       src.push_back(best);
     }
-    if (h->nrows > 0) src.push_back({h, 0});  // loaded rows
+    if (hr->is_minmax && h->nrows > 0) src.push_back({h, 0});  // loaded rows
     hr->dv = true;
     hr->dmap_n = r0;
     hr->range1 = r1;
@@ -600,6 +608,11 @@ struct Runner {
         }
       }
       if (hr->is_minmax && c->index_mode != 1) plan_dense_values(s, hr.get());
+      if ((hr->agg == Agg::SUM || hr->agg == Agg::LSE) && hr->nkey == 2 && c->index_mode != 1 && s.recursive &&
+          s.heads.size() == 1 && s.variants.size() == 1 && s.variants[0].carried_val) {
+        plan_dense_values(s, hr.get());
+        hr->ds = hr->dv;
+      }
       if (hr->is_set && c->index_mode != 1) {
         const Interval i0 = d[0].empty() ? Interval{0, 0} : d[0];
         const int64_t range0 = i0.hi - i0.lo + 1;
@@ -720,8 +733,8 @@ struct Runner {
     h->n0 = n0;
     const double slots = (double)std::max<uint32_t>(n0, 1) * (double)h->range1;
     const double budget = std::min(8589934592.0, (double)c->arena.capacity() / 4);
-    if (slots >= 4294967296.0 || slots * 8.25 > budget) {
-      h->dv = false;
+    if (slots >= 4294967296.0 || slots * (h->ds ? 16.5 : 8.25) > budget) {
+      h->dv = h->ds = false;
       h->dmap.reset();
       return XL_OK;
     }
@@ -732,10 +745,19 @@ struct Runner {
     XL_TRY(dalloc(c, ns * 4, &h->dvals, "dense values"));
     XL_TRY(dalloc(c, nw * 4, &h->dpres, "dense presence bits"));
     XL_TRY(dalloc(c, nw * 4, &h->dchg, "dense delta bits"));
-    XL_TRY(dalloc(c, ns * 4, &h->didx, "delta slot list"));
     HIP_TRY(c, hipMemsetAsync(h->dvals.p, 0xff, ns * 4, c->stream));
     HIP_TRY(c, hipMemsetAsync(h->dpres.p, 0, nw * 4, c->stream));
     HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nw * 4, c->stream));
+    if (h->ds) {
+      XL_TRY(dalloc(c, ns * 4, &h->dcur, "dense delta values"));
+      XL_TRY(dalloc(c, ns * 4, &h->dnext, "dense delta values"));
+      XL_TRY(dalloc(c, nw * 4, &h->dcur_pres, "dense delta bits"));
+      XL_TRY(dalloc(c, nw * 4, &h->dnext_pres, "dense delta bits"));
+      HIP_TRY(c, hipMemsetAsync(h->dcur_pres.p, 0, nw * 4, c->stream));
+      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, nw * 4, c->stream));
+    } else {
+      XL_TRY(dalloc(c, ns * 4, &h->didx, "delta slot list"));
+    }
     h->keys = 0;
     if (h->preloaded) {
       HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
@@ -1004,9 +1026,104 @@ struct Runner {
     return nullptr;
   }
 
+  // One round of the carried-value variant over a dense sum/logsumexp head:
+  // mark every key that receives a contribution (the stage kernel over the
+  // delta rows), list the marked slots in order, then fold each key's
+  // contributions by scanning e's rows for its Y value against the delta.
+  xl_status eval_dense_pull(const RulePlan& p, HeadRun* h) {
+    h->pulled = true;
+    h->pull_n = 0;
+    Source src = resolve_driver(p);
+    if (src.n == 0) return XL_OK;
+    const StepPlan& sp = p.steps[0];
+    StageArgs a{};
+    a.src.n = src.n;
+    a.src.ncols = p.driver->arity;
+    for (int j = 0; j < a.src.ncols; ++j) {
+      a.src.col[j] = src.col[j];
+      a.src.act[j] = p.driver_act[j];
+    }
+    a.has_index = 1;
+    XL_TRY(get_index(sp.rel, sp.key_col, &a.idx));
+    a.idx.key_slot = (int8_t)sp.key_slot;
+    for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
+    fill_ops(a, p, 0);
+    a.emit.mode = EM_MARK;
+    a.emit.key.nkey = 2;
+    a.emit.key.slot[0] = (int8_t)p.key_slot[0];
+    a.emit.key.slot[1] = (int8_t)p.key_slot[1];
+    a.emit.key.lo[0] = h->kp.lo[0];
+    a.emit.key.lo[1] = h->kp.lo[1];
+    a.emit.val_slot = (int8_t)p.val_slot;
+    a.emit.dmap = h->dmap.as<uint32_t>();
+    a.emit.dmap_n = (uint32_t)h->dmap_n;
+    a.emit.row_bits = (u64)h->range1;
+    a.emit.dchg = h->dchg.as<uint32_t>();
+    a.emit.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+    Buf tmp, tot, list;
+    XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &tmp, "compaction scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), ns, nullptr, tot.as<uint32_t>(), tmp.p, false, c->stream));
+    uint32_t n = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &n));
+    if (n == 0) return XL_OK;
+    XL_TRY(dalloc(c, (size_t)n * 4, &list, "marked keys"));
+    HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), ns, list.as<uint32_t>(), tot.as<uint32_t>(), tmp.p, true,
+                            c->stream));
+    for (int j = 0; j < 3; ++j) XL_TRY(dalloc(c, (size_t)n * 4, &h->ndrow[j], "delta rows"));
+    DensePullArgs q{};
+    q.list = list.as<uint32_t>();
+    q.n = n;
+    q.dict = h->dict.as<uint32_t>();
+    q.range1 = (uint32_t)h->range1;
+    q.lo1 = h->kp.lo[1];
+    XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
+    for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
+    q.rev.act[p.carried_ycol].kind = CA_NONE;  // Y is bound from the key
+    q.zcol = sp.key_col;
+    q.slot_s = (int8_t)p.cv_slot_s;
+    q.slot_z = (int8_t)p.cv_slot_z;
+    q.slot_y = (int8_t)p.key_slot[1];
+    q.slot_p = (int8_t)p.cv_slot_p;
+    q.val_slot = (int8_t)p.val_slot;
+    q.val_type = p.val_type;
+    q.fold_kind = h->fold;
+    q.nops = (int32_t)p.stage_ops[0].size();
+    for (int i = 0; i < q.nops; ++i) q.ops[i] = p.stage_ops[0][i];
+    for (size_t i = 0; i < p.stage_consts[0].size(); ++i) q.consts[i] = p.stage_consts[0][i];
+    q.cval = h->dcur.as<uint32_t>();
+    q.cpres = h->dcur_pres.as<uint32_t>();
+    q.nval = h->dnext.as<uint32_t>();
+    q.npres = h->dnext_pres.as<uint32_t>();
+    q.fval = h->dvals.as<uint32_t>();
+    q.fpres = h->dpres.as<uint32_t>();
+    q.k0 = h->ndrow[0].as<uint32_t>();
+    q.k1 = h->ndrow[1].as<uint32_t>();
+    q.v = h->ndrow[2].as<uint32_t>();
+    q.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    HIP_TRY(c, k::dense_pull(q, c->stream));
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "marked key without a contribution (internal)");
+    h->keys += (int64_t)cnt[CNT_INSERTED];
+    h->pull_n = n;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
   xl_status eval_plan(const RulePlan& p) {
     HeadRun* h = head_of(p.head);
     if (h->frontier && p.driver_delta) return eval_frontier(p, h);
+    if (h->ds && p.driver_delta) return eval_dense_pull(p, h);
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
@@ -1269,7 +1386,23 @@ struct Runner {
       *delta = 0;
       return XL_OK;  // counted in place; rows are produced at materialization
     }
-    if (h->dv) {
+    if (h->ds && h->pulled) {  // the pull wrote the next delta rows and values
+      h->pulled = false;
+      for (int j = 0; j < 3; ++j) {
+        std::swap(h->drow[j].p, h->ndrow[j].p);
+        h->drow[j].c = c;
+        h->ndrow[j].reset();
+      }
+      h->dcap = h->pull_n;
+      h->dn = h->pull_n;
+      std::swap(h->dcur.p, h->dnext.p);
+      std::swap(h->dcur_pres.p, h->dnext_pres.p);
+      const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)((ns + 31) / 32) * 4, c->stream));
+      *delta = h->dn;
+      return XL_OK;
+    }
+    if (h->dv && !h->ds) {
       XL_TRY(ensure_drow(h, h->didx_n));
       HIP_TRY(c, k::dense_delta_rows(h->didx.as<uint32_t>(), h->didx_n, h->dvals.as<uint32_t>(),
                                      h->dchg.as<uint32_t>(), h->dict.as<uint32_t>(), (uint32_t)h->range1,
@@ -1329,6 +1462,24 @@ struct Runner {
     HIP_TRY(c, k::seg_reduce(sk, kb, sv, starts.as<uint32_t>(), nseg, n, h->kp, h->rel->types[h->nkey], h->fold,
                              h->drow[0].as<uint32_t>(), h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
                              h->drow[h->nkey].as<uint32_t>(), c->stream));
+    if (h->ds) {  // seed round of a dense head: the folded rows become the first delta
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      HIP_TRY(c, k::dense_apply_rows(h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
+                                     nseg, h->dmap.as<uint32_t>(), (uint32_t)h->dmap_n, (uint32_t)h->range1, h->kp,
+                                     h->fold, h->rel->types[h->nkey], h->dcur.as<uint32_t>(),
+                                     h->dcur_pres.as<uint32_t>(), h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(),
+                                     c->dcounters, c->stream));
+      u64 cnt[CNT_N];
+      XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+      if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
+      h->keys += (int64_t)cnt[CNT_INSERTED];
+      if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+        return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows");
+      h->dn = nseg;
+      h->cn = 0;
+      *delta = nseg;
+      return XL_OK;
+    }
     if (h->keys + (int64_t)nseg > h->cap / 2) XL_TRY(grow(h, h->keys + nseg));
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     HIP_TRY(c, k::agg_merge(h->table.as<Slot16>(), (u64)h->cap - 1, h->drow[0].as<uint32_t>(),

@@ -138,6 +138,12 @@ struct RulePlan {
   // passes through from the delta, so the delta can be processed grouped by X.
   bool carried = false;
   int carried_ycol = -1;  // column of e bound to Y
+  // head(S, Y, agg(P)) :- delta head(S, Z, P1), e(..Z..Y..), arithmetic and
+  // comparisons: the first key passes through and Y comes from one column of
+  // e, so a head key (s, y) can collect its contributions by scanning the
+  // rows of e whose Y column is y (carried_ycol) against the delta.
+  bool carried_val = false;
+  int cv_slot_s = -1, cv_slot_z = -1, cv_slot_p = -1;  // P1's slot, -1 when unused
 };
 
 struct HeadInfo {

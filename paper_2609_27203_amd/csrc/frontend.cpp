@@ -486,6 +486,24 @@ struct Planner {
         p.carried_ycol = ycol;
       }
     }
+    // carried value shape (see RulePlan::carried_val)
+    if (delta && p.driver == p.head && p.head->arity == 3 && (r.agg == Agg::SUM || r.agg == Agg::LSE) &&
+        nst == 1 && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
+        (p.driver_act[2].kind == CA_BIND || p.driver_act[2].kind == CA_NONE) &&
+        p.driver_act[0].slot != p.driver_act[1].slot && p.steps[0].key_slot == p.driver_act[1].slot &&
+        p.key_slot[0] == p.driver_act[0].slot && p.val_slot >= 0) {
+      int ycol = -1;
+      for (int j = 0; j < p.steps[0].rel->arity; ++j)
+        if (j != p.steps[0].key_col && p.steps[0].act[j].kind == CA_BIND && p.steps[0].act[j].slot == p.key_slot[1])
+          ycol = j;
+      if (ycol >= 0 && p.steps[0].rel->types[ycol] == T_I32) {
+        p.carried_val = true;
+        p.carried_ycol = ycol;
+        p.cv_slot_s = p.driver_act[0].slot;
+        p.cv_slot_z = p.driver_act[1].slot;
+        p.cv_slot_p = p.driver_act[2].kind == CA_BIND ? p.driver_act[2].slot : -1;
+      }
+    }
     *out = p;
     return true;
   }
@@ -664,6 +682,7 @@ std::string explain_program(const Program* p) {
         os << ")";
         if (rp.val_slot >= 0) os << " val v" << rp.val_slot;
         if (rp.carried) os << " [grouped by v" << rp.key_slot[0] << "]";
+        if (rp.carried_val) os << " [keyed by v" << rp.key_slot[0] << ", v" << rp.key_slot[1] << " pulled]";
         os << "\n";
       }
     }

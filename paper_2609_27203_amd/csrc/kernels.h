@@ -119,6 +119,16 @@ hipError_t dense_insert_rows(uint32_t* vals, uint32_t* pres, const uint32_t* map
 hipError_t dense_delta_rows(const uint32_t* idx, int64_t n, const uint32_t* vals, uint32_t* chg, const uint32_t* dict,
                             uint32_t range1, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                             uint32_t* v, hipStream_t s);
+// Dense sum/logsumexp heads.  bits_list: ascending list of the set bits,
+// in two calls on the same temp (write=false counts into *total; write=true
+// writes the list and clears the bits).
+size_t bits_list_temp_bytes(int64_t nbits);
+hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, void* temp, bool write,
+                     hipStream_t s);
+hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);
+hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
+                            uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
+                            uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,

@@ -879,7 +879,8 @@ __device__ __forceinline__ bool bind_cols(SRC& src, int64_t row, Regs& u) {
   return ok;
 }
 
-__device__ __forceinline__ uint32_t operand(KernArgs& a, const Regs& u, int o) {
+template <class A>
+__device__ __forceinline__ uint32_t operand(A& a, const Regs& u, int o) {
   if (o >= 0) return getv(u, o);
   uint32_t r = a.consts[0];
 #pragma unroll
@@ -911,7 +912,8 @@ __device__ __forceinline__ bool compare(int cmp, int type, uint32_t x, uint32_t 
   }
 }
 
-__device__ __forceinline__ bool run_ops(KernArgs& a, Regs& u) {
+template <class A>
+__device__ __forceinline__ bool run_ops(A& a, Regs& u) {
   bool ok = true;
 #pragma unroll
   for (int i = 0; i < MAXOPS; ++i) {
@@ -1141,6 +1143,20 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     }
     return;
   }
+  if (MODE == EM_MARK) {
+    if (act) {
+      const uint32_t k0 = getv(u, e.key.slot[0]) - (uint32_t)e.key.lo[0];
+      const uint32_t k1 = getv(u, e.key.slot[1]) - (uint32_t)e.key.lo[1];
+      const uint32_t r0 = k0 < e.dmap_n ? e.dmap[k0] : 0xffffffffu;
+      if (r0 == 0xffffffffu || (u64)k1 >= e.row_bits) {
+        atomicOr(&e.counters[CNT_FATAL], 4ull);
+      } else {
+        const uint32_t slot = r0 * (uint32_t)e.row_bits + k1, bit = 1u << (slot & 31);
+        if (!(e.dchg[slot >> 5] & bit)) atomicOr(&e.dchg[slot >> 5], bit);
+      }
+    }
+    return;
+  }
   if (MODE == EM_MINMAX) {
     bool ins = false, app = false;
     u64 slot = ~0ull;
@@ -1241,7 +1257,8 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     }
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
   }
-  if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT || MODE == EM_DMIN) {
+  if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT || MODE == EM_DMIN ||
+      MODE == EM_MARK) {
     // one atomic per workgroup: a shared counter hit by every wave serializes
     __shared__ u64 s_cands[ST_WAVES];
     if (lane == 0) s_cands[w] = st.cands;
@@ -1273,8 +1290,284 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
     case EM_SET: launch_mode<EM_SET>(a, grid, s); break;
     case EM_BITSET: launch_mode<EM_BITSET>(a, grid, s); break;
     case EM_DMIN: launch_mode<EM_DMIN>(a, grid, s); break;
+    case EM_MARK: launch_mode<EM_MARK>(a, grid, s); break;
     default: launch_mode<EM_MINMAX>(a, grid, s); break;
   }
+  return hipGetLastError();
+}
+
+// ============================================================ dense sum / logsumexp heads
+// Marked slots -> ascending slot list, clearing the marks.  Each workgroup
+// owns MK_WORDS consecutive bitmap words: count pass, scan of the per-group
+// counts, write pass.
+constexpr int MK_THREADS = 256, MK_WPT = 4, MK_WORDS = MK_THREADS * MK_WPT;
+
+__global__ __launch_bounds__(MK_THREADS) void bits_count_k(const uint32_t* bits, int64_t nw, uint32_t* cnt) {
+  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < MK_WPT; ++k)
+    if (w0 + k < nw) c += __popc(bits[w0 + k]);
+  uint32_t tot;
+  block_excl_scan<uint32_t>(c, &tot);
+  if (threadIdx.x == 0) cnt[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_t nw, const uint32_t* off,
+                                                          uint32_t* list) {
+  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
+  uint32_t d[MK_WPT], c = 0;
+#pragma unroll
+  for (int k = 0; k < MK_WPT; ++k) {
+    d[k] = w0 + k < nw ? bits[w0 + k] : 0u;
+    c += __popc(d[k]);
+  }
+  uint32_t tot;
+  uint32_t p = off[blockIdx.x] + block_excl_scan<uint32_t>(c, &tot);
+#pragma unroll
+  for (int k = 0; k < MK_WPT; ++k) {
+    if (!d[k]) continue;
+    bits[w0 + k] = 0u;
+    for (uint32_t b = d[k]; b; b &= b - 1) list[p++] = (uint32_t)(w0 + k) * 32u + (uint32_t)(__ffs(b) - 1);
+  }
+}
+
+size_t bits_list_temp_bytes(int64_t nbits) {
+  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  return (size_t)((nb + 63) & ~63ll) * 8 + scan_temp_bytes(nb) + 256;
+}
+
+hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, void* temp, bool write,
+                     hipStream_t s) {
+  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
+  uint32_t* cnt = (uint32_t*)temp;
+  uint32_t* off = cnt + ((nb + 63) & ~63ll);
+  char* stemp = (char*)(off + ((nb + 63) & ~63ll));
+  if (!write) {
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, cnt);
+    return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
+  }
+  bits_list_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, off, list);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ float lse2(float a, float b) {
+  if (a == -INFINITY) return b;
+  if (b == -INFINITY) return a;
+  const float m = fmaxf(a, b);
+  return m + log1pf(expf(-fabsf(a - b)));
+}
+
+// Fold a contribution into a full-relation slot this thread owns; returns
+// whether the key is new to the relation.
+__device__ __forceinline__ bool dense_merge(uint32_t* fval, uint32_t* fpres, uint32_t t, uint32_t x,
+                                            int fold_kind, int type) {
+  const uint32_t bit = 1u << (t & 31);
+  const bool had = atomicOr(&fpres[t >> 5], bit) & bit;
+  uint32_t r = x;
+  if (had) {
+    const uint32_t cur = fval[t];
+    if (fold_kind == FOLD_LSE) r = __float_as_uint(lse2(__uint_as_float(cur), __uint_as_float(x)));
+    else if (type == T_F32) r = __float_as_uint(__fadd_rn(__uint_as_float(cur), __uint_as_float(x)));
+    else r = cur + x;
+  }
+  fval[t] = r;
+  return !had;
+}
+
+typedef XL_KARG const DensePullArgs PullArgs;
+
+// Binds S, Z, Y and P1, then e's row e_row; false when the row does not
+// derive anything for this key.
+__device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, uint32_t y, uint32_t e_row,
+                                          Regs& u) {
+  const uint32_t z = a.rev.col[a.zcol][e_row];
+  const uint32_t zb = z - (uint32_t)a.lo1;
+  if (zb >= a.range1) return false;
+  const uint32_t zs = r * a.range1 + zb;
+  if (!((a.cpres[zs >> 5] >> (zs & 31)) & 1u)) return false;
+  u = (Regs)(0u);
+  setv(u, a.slot_s, s);
+  setv(u, a.slot_z, z);
+  setv(u, a.slot_y, y);
+  if (a.slot_p >= 0) setv(u, a.slot_p, a.cval[zs]);
+  if (!bind_cols(a.rev, e_row, u)) return false;
+  return run_ops(a, u);
+}
+
+// Wave-balanced pull: a wavefront takes 64 listed keys, scans their row
+// counts in rev and walks the concatenated row lists 64 rows per step (owner
+// found by a six-step search), so consecutive lanes read consecutive rows
+// of e.  Per step, the lanes of one key form a run; its contributions are
+// folded across the run (segmented shuffles) and merged by the run's last
+// lane into the key's running state in LDS: (max m, sum of exp(x - m)) for
+// logsumexp, the sum otherwise.  The order is fixed, so the result is
+// deterministic.
+constexpr int DP_WAVES = 4;
+
+__device__ __forceinline__ float seg_max_scan(float v, int lane, int head) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const float t = __shfl_up(v, d, 64);
+    if (lane - d >= head) v = fmaxf(v, t);
+  }
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T seg_sum_scan(T v, int lane, int head) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const T t = __shfl_up(v, d, 64);
+    if (lane - d >= head) v = v + t;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_value) {
+  (void)by_value;
+  PullArgs& a = *(PullArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  __shared__ uint32_t s_excl[DP_WAVES][64], s_beg[DP_WAVES][64], s_key[DP_WAVES][64];
+  __shared__ uint32_t s_m[DP_WAVES][64], s_acc[DP_WAVES][64], s_any[DP_WAVES][64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const bool lse = a.fold_kind == FOLD_LSE, f32 = a.val_type == T_F32;
+  const int64_t nchunks = (a.n + 63) / 64;
+  uint32_t mine = 0;
+  for (int64_t chunk = (int64_t)blockIdx.x * DP_WAVES + w; chunk < nchunks; chunk += (int64_t)gridDim.x * DP_WAVES) {
+    const int64_t i = chunk * 64 + lane;
+    uint32_t t = 0, e0 = 0, deg = 0;
+    if (i < a.n) {
+      t = a.list[i];
+      const uint32_t kk = t % a.range1 + (uint32_t)a.lo1 - (uint32_t)a.rev.key_lo;
+      if (kk < a.rev.key_range) {
+        e0 = a.rev.off[kk];
+        deg = a.rev.off[kk + 1] - e0;
+      }
+    }
+    const uint32_t incl = wave_incl_scan(deg);
+    const uint32_t total = __shfl(incl, 63, 64);
+    s_excl[w][lane] = incl - deg;
+    s_beg[w][lane] = e0;
+    s_key[w][lane] = t;
+    s_m[w][lane] = __float_as_uint(-INFINITY);
+    s_acc[w][lane] = 0u;
+    s_any[w][lane] = 0u;
+    wave_lds_sync();
+    for (uint32_t base = 0; base < total; base += 64) {
+      const uint32_t j = base + (uint32_t)lane;
+      const bool act = j < total;
+      int q = 0;
+#pragma unroll
+      for (int step = 32; step > 0; step >>= 1)
+        if (s_excl[w][q + step] <= j) q += step;
+      bool ok = false;
+      uint32_t x = 0;
+      if (act) {
+        const uint32_t tq = s_key[w][q], r = tq / a.range1;
+        Regs u;
+        ok = pull_bind(a, r, a.dict[r], tq % a.range1 + (uint32_t)a.lo1, s_beg[w][q] + (j - s_excl[w][q]), u);
+        if (ok) x = getv(u, a.val_slot);
+      }
+      // runs of equal owners among the active lanes
+      const int qp = __shfl_up(q, 1, 64);
+      const u64 am = __ballot(act);
+      const u64 heads = __ballot(act && (lane == 0 || qp != q)) | ~am;
+      const int head = 63 - __clzll((long long)(heads & ((2ull << lane) - 1ull)));
+      const u64 above = heads & ~((2ull << lane) - 1ull);
+      const int tail = above ? __ffsll((long long)above) - 2 : 63;
+      const bool is_tail = act && tail == lane;
+      const int oks = seg_sum_scan<int>(ok ? 1 : 0, lane, head);
+      if (lse) {
+        const float xv = ok ? __uint_as_float(x) : -INFINITY;
+        const float mrun = __shfl(seg_max_scan(xv, lane, head), tail, 64);
+        const float ev = (ok && mrun != -INFINITY) ? expf(xv - mrun) : 0.0f;
+        const float srun = seg_sum_scan<float>(ev, lane, head);
+        if (is_tail && oks > 0) {
+          const float m = __uint_as_float(s_m[w][q]), acc = __uint_as_float(s_acc[w][q]);
+          float nm = m, nacc = acc;
+          if (mrun != -INFINITY) {
+            if (mrun > m) {
+              nacc = (m == -INFINITY ? 0.0f : acc * expf(m - mrun)) + srun;
+              nm = mrun;
+            } else {
+              nacc = acc + srun * expf(mrun - m);
+            }
+          }
+          s_m[w][q] = __float_as_uint(nm);
+          s_acc[w][q] = __float_as_uint(nacc);
+          s_any[w][q] = 1u;
+        }
+      } else if (f32) {
+        const float srun = seg_sum_scan<float>(ok ? __uint_as_float(x) : 0.0f, lane, head);
+        if (is_tail && oks > 0) {
+          s_acc[w][q] = __float_as_uint(__fadd_rn(__uint_as_float(s_acc[w][q]), srun));
+          s_any[w][q] = 1u;
+        }
+      } else {
+        const uint32_t srun = seg_sum_scan<uint32_t>(ok ? x : 0u, lane, head);
+        if (is_tail && oks > 0) {
+          s_acc[w][q] += srun;
+          s_any[w][q] = 1u;
+        }
+      }
+      wave_lds_sync();
+    }
+    if (i < a.n) {
+      uint32_t out;
+      if (lse) {
+        const float m = __uint_as_float(s_m[w][lane]);
+        out = __float_as_uint(m == -INFINITY ? -INFINITY : m + logf(__uint_as_float(s_acc[w][lane])));
+      } else {
+        out = s_acc[w][lane];
+      }
+      if (!s_any[w][lane]) atomicOr(&a.counters[CNT_FATAL], 8ull);  // a marked key always has a contribution
+      const uint32_t r = t / a.range1;
+      a.k0[i] = a.dict[r];
+      a.k1[i] = t % a.range1 + (uint32_t)a.lo1;
+      a.v[i] = out;
+      a.nval[t] = out;
+      atomicOr(&a.npres[t >> 5], 1u << (t & 31));
+      mine += dense_merge(a.fval, a.fpres, t, out, a.fold_kind, a.val_type);
+    }
+    wave_lds_sync();
+  }
+  block_count_add(&a.counters[CNT_INSERTED], mine);
+}
+
+hipError_t dense_pull(const DensePullArgs& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  dense_pull_k<<<grid_for((a.n + 63) / 64, DP_WAVES, 16384), DP_WAVES * 64, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// Rows with distinct keys (a folded seed round) into a dense sum/logsumexp
+// head: each becomes the current delta value of its slot and is folded into
+// the full relation.
+__global__ void dense_apply_rows_k(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n,
+                                   const uint32_t* map, uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind,
+                                   int type, uint32_t* cval, uint32_t* cpres, uint32_t* fval, uint32_t* fpres,
+                                   u64* counters) {
+  uint32_t mine = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t k0 = c0[i] - (uint32_t)kp.lo[0], k1 = c1[i] - (uint32_t)kp.lo[1];
+    const uint32_t r0 = k0 < map_n ? map[k0] : 0xffffffffu;
+    if (r0 == 0xffffffffu || k1 >= range1) {
+      atomicOr(&counters[CNT_FATAL], 4ull);
+      continue;
+    }
+    const uint32_t t = r0 * range1 + k1;
+    cval[t] = v[i];
+    atomicOr(&cpres[t >> 5], 1u << (t & 31));
+    mine += dense_merge(fval, fpres, t, v[i], fold_kind, type);
+  }
+  block_count_add(&counters[CNT_INSERTED], mine);
+}
+hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
+                            uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
+                            uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dense_apply_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(c0, c1, v, n, map, map_n, range1, kp, fold_kind, type,
+                                                            cval, cpres, fval, fpres, counters);
   return hipGetLastError();
 }
 
@@ -1301,13 +1594,6 @@ hipError_t seg_starts(const uint32_t* flag, const uint32_t* pos, int64_t n, uint
                       hipStream_t s) {
   seg_starts_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(flag, pos, n, start);
   return hipGetLastError();
-}
-
-__device__ __forceinline__ float lse2(float a, float b) {
-  if (a == -INFINITY) return b;
-  if (b == -INFINITY) return a;
-  const float m = fmaxf(a, b);
-  return m + log1pf(expf(-fabsf(a - b)));
 }
 
 // One thread folds one key group of the sorted candidates, in sorted order.

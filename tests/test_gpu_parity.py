@@ -118,6 +118,35 @@ def test_counts_and_joins_over_a_finished_closure(index_mode):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+PULL_RULES = {
+    # integer sum over derivations: the number of paths from each source
+    "npaths": ("""
+npaths(S,Y,sum(C)) :- source(S), C is 1, edge(S,Y,_).
+npaths(S,Y,sum(C)) :- npaths(S,Z,C1), edge(Z,Y,_), C is C1.
+""", {"npaths": ("i32", "i32", "i32")}),
+    # logsumexp with a comparison on the joined edge
+    "score_filtered": ("""
+score(S,Y,logsumexp(P)) :- source(S), edge(S,Y,P).
+score(S,Y,logsumexp(P)) :- score(S,Z,P1), edge(Z,Y,W), W > -2.0, P is P1 + W.
+""", {"score": ("i32", "i32", "f32")}),
+}
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+@pytest.mark.parametrize("name", list(PULL_RULES))
+def test_sum_and_logsumexp_heads_dense_and_hashed(name, index_mode):
+    """Carried-value sum/logsumexp rules: index mode 0 keeps the head in dense
+    slots and folds each key's contributions by scanning its in-edges, mode 1
+    sorts and folds candidates into a hash table; both match the oracle."""
+    rules, idb = PULL_RULES[name]
+    wl = W.Workload(name, rules, W.small_workloads()["lse_dag"]().edb, idb)
+    print(f"case: pull heads {name} index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
+    _compare(wl, rels, ref)
+    assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
+
+
 def _delta_levels(ref, name):
     sizes = ref.sizes[name]
     return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
