@@ -63,18 +63,28 @@ def dominant_kernel(stats: list) -> dict:
             "bytes": sum(_algorithmic_bytes(s[k + "_candidates"], s[k + "_new"]) for s in stats)}
 
 
+FRONTIER_SOURCES = ("frontier.hip", "device_util.h", "device_types.h")
+
+
+def frontier_sources_sha256() -> str:
+    """Hash of the sources the frontier kernel is compiled from."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_27203_amd", "csrc")
+    for f in FRONTIER_SOURCES:
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
 def recorded_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from the committed counter
-    record, or None when the kernel source changed since it was measured."""
-    import hashlib
+    record, or None when the kernel's sources changed since it was measured."""
     root = os.path.dirname(os.path.abspath(__file__))
     rec = os.path.join(root, "profiles", "frontier_round_rmat_traffic.json")
-    src = os.path.join(root, "paper_2609_27203_amd", "csrc", "kernels.hip")
     if workload != "tc_rmat_count" or not os.path.exists(rec):
         return None
     r = json.load(open(rec))
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    return r["hbm_bytes_per_launch"] if r["kernels_hip_sha256"] == sha else None
+    return r["hbm_bytes_per_launch"] if r.get("frontier_sources_sha256") == frontier_sources_sha256() else None
 
 
 def copy_calibration():
