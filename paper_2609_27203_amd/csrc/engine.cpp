@@ -422,7 +422,6 @@ struct Runner {
     ix->rel = rel;
     ix->col = col;
     IndexProbe& p = ix->probe;
-    const int64_t n = rel->nrows;
     p.ncols = rel->arity;
     auto own = [&](size_t bytes, const char* what, void** ptr) -> xl_status {
       ix->owned.push_back(std::make_unique<Buf>());
@@ -430,6 +429,41 @@ struct Runner {
       *ptr = ix->owned.back()->p;
       return XL_OK;
     };
+    // rows as this round sees them: a head of the running stratum (a
+    // self-join) contributes its current full relation
+    const uint32_t* rcol[MAXC] = {};
+    int64_t n = rel->nrows;
+    int32_t klo = rel->lo[col], khi = rel->hi[col];
+    for (int j = 0; j < rel->arity; ++j) rcol[j] = rel->col[j];
+    if (HeadRun* h = head_of(rel)) {
+      if (h->frontier || h->dcount || h->is_sortagg || col >= h->nkey)
+        return c->fail(XL_UNSUPPORTED, "relation " + rel->name + " cannot be joined inside its own stratum");
+      klo = (int32_t)h->dom_lo[col];
+      khi = (int32_t)h->dom_hi[col];
+      if (h->is_set) {
+        n = h->nrows;
+        for (int j = 0; j < h->nkey; ++j) rcol[j] = h->rows[j].as<uint32_t>();
+      } else {  // min/max: compact a snapshot of the current keys and values
+        n = h->keys;
+        void* snap[3];
+        for (int j = 0; j <= h->nkey; ++j) XL_TRY(own((size_t)std::max<int64_t>(n, 1) * 4, "head snapshot", &snap[j]));
+        Buf tmp, tot;
+        const int64_t ns = h->dv ? std::max<int64_t>(h->n0, 1) * h->range1 : h->cap;
+        XL_TRY(dalloc(c, k::compact_temp_bytes(ns), &tmp, "compaction scratch"));
+        XL_TRY(dalloc(c, 8, &tot, "count"));
+        uint32_t* k1 = h->nkey == 2 ? (uint32_t*)snap[1] : nullptr;
+        if (h->dv)
+          HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
+                                   h->range1, h->kp, rel->types[h->nkey], h->fold, (uint32_t*)snap[0], k1,
+                                   (uint32_t*)snap[h->nkey], std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p,
+                                   c->stream));
+        else
+          HIP_TRY(c, k::table16_compact(h->table.as<Slot16>(), h->cap, h->kp, rel->types[h->nkey], h->fold,
+                                        (uint32_t*)snap[0], k1, (uint32_t*)snap[h->nkey], std::max<int64_t>(n, 1),
+                                        tot.as<uint32_t>(), tmp.p, c->stream));
+        for (int j = 0; j <= h->nkey; ++j) rcol[j] = (const uint32_t*)snap[j];
+      }
+    }
     if (n == 0) {
       void* off;
       XL_TRY(own(8, "index offsets", &off));
@@ -441,7 +475,7 @@ struct Runner {
       if (rel->types[col] != T_I32) return c->fail(XL_UNSUPPORTED, "index key columns must be int32");
       if (n > ((int64_t)1 << 25))
         return c->fail(XL_UNSUPPORTED, "indexed relation " + rel->name + " exceeds 2^25 rows");
-      const int64_t range = (int64_t)rel->hi[col] - rel->lo[col] + 1;
+      const int64_t range = (int64_t)khi - klo + 1;
       if (range > ((int64_t)1 << 30))
         return c->fail(XL_UNSUPPORTED, "key range of " + rel->name + " column " + std::to_string(col) +
                                            " exceeds 2^30 values");
@@ -451,7 +485,7 @@ struct Runner {
       XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));
       XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
       XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
-      HIP_TRY(c, k::sub_lo(rel->col[col], rel->lo[col], keys.as<uint32_t>(), n, c->stream));
+      HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
       HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
       int alt = 0;
       HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(),
@@ -462,14 +496,14 @@ struct Runner {
       for (int j = 0; j < rel->arity; ++j) {
         void* cj;
         XL_TRY(own((size_t)n * 4, "index column", &cj));
-        HIP_TRY(c, k::gather_u32(rel->col[j], sp, (uint32_t*)cj, n, c->stream));
+        HIP_TRY(c, k::gather_u32(rcol[j], sp, (uint32_t*)cj, n, c->stream));
         p.col[j] = (uint32_t*)cj;
       }
       void* off;
       XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
       HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
       p.off = (uint32_t*)off;
-      p.key_lo = rel->lo[col];
+      p.key_lo = klo;
       p.key_range = (uint32_t)range;
     }
     *out = p;
@@ -1626,11 +1660,30 @@ struct Runner {
     return XL_OK;
   }
 
+  // Indexes over heads of the running stratum describe the relation as it
+  // was when they were built; each pass rebuilds them from the current rows.
+  // All of a pass's joins with a head of the stratum read the relation as it
+  // was when the pass began (Alg. 1: every variant of round k sees S_k), so
+  // those indexes are built up front, before any variant adds tuples.
+  xl_status snapshot_head_indexes(const std::vector<RulePlan>& plans) {
+    indexes.erase(std::remove_if(indexes.begin(), indexes.end(),
+                                 [&](const std::unique_ptr<DevIndex>& ix) { return head_of(ix->rel) != nullptr; }),
+                  indexes.end());
+    for (const RulePlan& p : plans)
+      for (const StepPlan& sp : p.steps)
+        if (head_of(sp.rel)) {
+          IndexProbe probe;
+          XL_TRY(get_index(sp.rel, sp.key_col, &probe));
+        }
+    return XL_OK;
+  }
+
   // ------------------------------------------------------------ strata
   xl_status run_stratum(Stratum& s, int64_t max_iterations) {
     heads.clear();
     XL_TRY(setup_heads(s));
     for (auto& h : heads) begin_round(h.get());
+    XL_TRY(snapshot_head_indexes(s.full));
     for (RulePlan& p : s.full) XL_TRY(eval_plan(p));
     int64_t total = 0;
     for (auto& h : heads) {
@@ -1649,6 +1702,7 @@ struct Runner {
         ++pass;
         st->iterations++;
         for (auto& h : heads) begin_round(h.get());
+        XL_TRY(snapshot_head_indexes(s.variants));
         for (RulePlan& p : s.variants) XL_TRY(eval_plan(p));
         total = 0;
         for (auto& h : heads) {

@@ -471,6 +471,7 @@ struct Planner {
     }
     // transitive-closure shape (see RulePlan::carried)
     if (delta && p.driver == p.head && p.head->arity == 2 && r.agg == Agg::NONE && nst == 1 &&
+        p.steps[0].rel != p.head &&
         p.stage_ops[0].empty() && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
         p.driver_act[0].slot != p.driver_act[1].slot && p.steps[0].key_slot == p.driver_act[1].slot &&
         p.key_slot[0] == p.driver_act[0].slot) {
@@ -488,7 +489,7 @@ struct Planner {
     }
     // carried value shape (see RulePlan::carried_val)
     if (delta && p.driver == p.head && p.head->arity == 3 && (r.agg == Agg::SUM || r.agg == Agg::LSE) &&
-        nst == 1 && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
+        nst == 1 && p.steps[0].rel != p.head && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
         (p.driver_act[2].kind == CA_BIND || p.driver_act[2].kind == CA_NONE) &&
         p.driver_act[0].slot != p.driver_act[1].slot && p.steps[0].key_slot == p.driver_act[1].slot &&
         p.key_slot[0] == p.driver_act[0].slot && p.val_slot >= 0) {
@@ -622,23 +623,24 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
       std::vector<int> rec;
       for (int k = 0; k < (int)r.atoms.size(); ++k)
         if (in.count(ctx->find(r.atoms[k].pred))) rec.push_back(k);
-      if (rec.size() > 1)
-        return bad(XL_UNSUPPORTED, "rule '" + r.text + "': non-linear recursion (more than one recursive atom) is not supported yet");
+      // Several recursive atoms (a self-join): one delta variant per
+      // recursive atom, the other atoms reading the full relations
+      // (Alg. 1).  Folds that are not idempotent would count a derivation
+      // once per variant, so sum/logsumexp stay linear.
+      if (rec.size() > 1) {
+        const Agg ha = prog->head_agg(ctx->find(r.head));
+        if (ha == Agg::SUM || ha == Agg::LSE)
+          return bad(XL_UNSUPPORTED, "rule '" + r.text + "': sum and logsumexp need linear recursion (one recursive atom)");
+      }
       RulePlan full;
       if (!pl.plan(r, ri, rec.empty() ? 0 : rec[0], false, &full)) return bad(pl.status, pl.err);
       st.full.push_back(full);
-      if (!rec.empty()) {
+      for (int k : rec) {
         RulePlan var;
-        if (!pl.plan(r, ri, rec[0], true, &var)) return bad(pl.status, pl.err);
+        if (!pl.plan(r, ri, k, true, &var)) return bad(pl.status, pl.err);
         st.variants.push_back(var);
       }
     }
-    // every index join must target a relation outside the stratum
-    for (auto* plans : {&st.full, &st.variants})
-      for (auto& p : *plans)
-        for (auto& s : p.steps)
-          if (in.count(s.rel))
-            return bad(XL_UNSUPPORTED, "rule '" + prog->rules[p.rule].text + "': non-linear recursion is not supported yet");
     prog->strata.push_back(st);
   }
   *out = prog;

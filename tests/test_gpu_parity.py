@@ -147,6 +147,52 @@ def test_sum_and_logsumexp_heads_dense_and_hashed(name, index_mode):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+SELF_JOIN_TC = """
+path(X,Y) :- edge(X,Y).
+path(X,Y) :- path(X,Z), path(Z,Y).
+"""
+
+SELF_JOIN_MIN = """
+dist(X,Y,min(D)) :- edge(X,Y,D).
+dist(X,Y,min(D)) :- dist(X,Z,D1), dist(Z,Y,D2), D is D1 + D2.
+"""
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_self_join_closure_matches_oracle_and_doubles_path_length(index_mode):
+    """Non-linear closure: two delta variants per round; after round k the
+    relation holds every pair joined by a walk of length <= 2^k, so the
+    per-round delta sizes equal the oracle's naive iterations."""
+    base = W.tc_uniform(150, 600, 11)
+    wl = W.Workload("tc_self_join", SELF_JOIN_TC, base.edb, {"path": ("i32", "i32")})
+    print(f"case: self-join closure index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
+    _compare(wl, rels, ref)
+    assert stats["delta_rows"] == _delta_levels(ref, "path")
+    linear = evaluate(W.TC_RULES, base.edb, {"path": ("i32", "i32")})
+    assert len(ref.sizes["path"]) < len(linear.sizes["path"])
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_self_join_min_matches_oracle(index_mode):
+    """Non-linear shortest paths (dist joined with dist): integer-valued f32
+    weights keep every sum exact, so the min fixpoint is compared bit for bit."""
+    rng = np.random.default_rng(21)
+    n, m = 120, 480
+    src = rng.integers(0, n, 3 * m)
+    dst = rng.integers(0, n, 3 * m)
+    keep = src != dst
+    pairs = np.unique(np.stack([src[keep], dst[keep]], 1), axis=0)[:m]
+    wgt = rng.integers(1, 9, len(pairs)).astype(np.float32)
+    edb = {"edge": (("i32", "i32", "f32"), [pairs[:, 0].astype(np.int32), pairs[:, 1].astype(np.int32), wgt])}
+    wl = W.Workload("min_self_join", SELF_JOIN_MIN, edb, {"dist": ("i32", "i32", "f32")})
+    print(f"case: self-join min index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, _, _ = engine_run(wl, options={"index_mode": index_mode})
+    assert_same_relation("dist", wl.idb["dist"], rels["dist"], ref.relations["dist"][1], tol=(0.0, 0.0))
+
+
 def _delta_levels(ref, name):
     sizes = ref.sizes[name]
     return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]

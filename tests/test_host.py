@@ -56,6 +56,17 @@ I2 = ("i32", "i32")
 W3 = ("i32", "i32", "f32")
 
 
+def test_self_join_gets_one_delta_variant_per_recursive_atom():
+    """Alg. 1: a rule with two recursive atoms has two delta variants, each
+    scanning the delta at one atom and joining the full relation at the other."""
+    c = _ctx({"e": I2, "p": I2})
+    plan = c.compile("p(X,Y) :- e(X,Y).\np(X,Y) :- p(X,Z), p(Z,Y).").explain()
+    variants = [ln for ln in plan.splitlines() if ln.startswith("  delta rule")]
+    assert len(variants) == 2
+    assert "delta p(v0,v1) -> join p on col 0=v1" in variants[0]
+    assert "delta p(v0,v1) -> join p on col 1=v0" in variants[1]
+
+
 @pytest.mark.parametrize("rels,text,status", [
     ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y", "XL_PARSE_ERROR"),
     ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y) e(Y,Z).", "XL_PARSE_ERROR"),
@@ -64,7 +75,8 @@ W3 = ("i32", "i32", "f32")
     ({"e": I2, "p": I2}, "p(X,Y) :- e(X,Y,Z).", "XL_INVALID_ARGUMENT"),
     ({"e": I2, "p": I2}, "p(X,Y,count(Z)) :- e(X,Y), e(Y,Z).", "XL_INVALID_ARGUMENT"),
     ({"e": I2, "c": I2}, "c(X,count(Y)) :- c(X,Z), e(Z,Y).", "XL_UNSUPPORTED"),
-    ({"e": I2, "p": I2}, "p(X,Y) :- p(X,Z), p(Z,Y).", "XL_UNSUPPORTED"),
+    ({"w": W3, "s": W3}, "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), s(Z,Y,P2), P is P1 + P2.",
+     "XL_UNSUPPORTED"),
     ({"e": I2, "f": I2, "p": I2}, "p(X,Y) :- e(X,A), f(B,Y).", "XL_UNSUPPORTED"),
     ({"w": W3, "p": ("f32", "i32")}, "p(W,Y) :- w(X,Y,W).", "XL_UNSUPPORTED"),
     ({"w": W3, "p": I2}, "p(X,W) :- w(X,Y,W).", "XL_TYPE_MISMATCH"),
