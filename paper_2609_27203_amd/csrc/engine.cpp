@@ -994,6 +994,30 @@ struct Runner {
 
   // Turn the row-list delta [dbeg, dend) of a frontier head into delta bitmap
   // rows: sort by the first key, one delta row per distinct value.
+  // First frontier when the head started empty: every set bit is new, so the
+  // delta rows are the nonempty bitmap rows themselves (no regrouping sort).
+  xl_status frontier_from_bits(HeadRun* h) {
+    h->fn = 0;
+    h->frontier_ready = true;
+    if (h->dend == h->dbeg) return XL_OK;
+    Buf cnt, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)h->range0 * 4, &cnt, "row counts"));
+    XL_TRY(dalloc(c, k::compact_temp_bytes(h->range0), &tmp, "compaction scratch"));
+    XL_TRY(dalloc(c, 8, &tot, "count"));
+    HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
+    KeyPack kx{};
+    kx.nkey = 1;
+    kx.lo[0] = h->kp.lo[0];
+    HIP_TRY(c, k::dcount_rows(cnt.as<uint32_t>(), h->range0, 1, kx, h->fx.as<uint32_t>(), nullptr,
+                              h->fcnt[h->fcur].as<uint32_t>(), h->range0, tot.as<uint32_t>(), tmp.p, c->stream));
+    uint32_t nseg = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &nseg));
+    HIP_TRY(c, k::gather_rows(h->bits.as<uint32_t>(), h->row_words, h->fx.as<uint32_t>(), h->kp.lo[0], nseg,
+                              h->fdiff[h->fcur].as<uint32_t>(), c->stream));
+    h->fn = nseg;
+    return XL_OK;
+  }
+
   xl_status frontier_from_rows(HeadRun* h) {
     const int64_t n = h->dend - h->dbeg;
     h->fn = 0;
@@ -1413,7 +1437,8 @@ struct Runner {
       h->dbeg = h->round_begin;
       h->dend = h->nrows;
       *delta = h->dend - h->dbeg;
-      if (h->frontier) XL_TRY(frontier_from_rows(h));  // seed round -> first frontier
+      if (h->frontier)  // seed round -> first frontier
+        XL_TRY(h->preloaded == 0 ? frontier_from_bits(h) : frontier_from_rows(h));
       return XL_OK;
     }
     if (h->dcount) {

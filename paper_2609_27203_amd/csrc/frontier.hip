@@ -306,6 +306,22 @@ hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words,
   return hipGetLastError();
 }
 
+// out row sg = bitmap row (x[sg] - lo0), row_words words each.
+__global__ void gather_rows_k(const uint32_t* bits, uint32_t row_words, const uint32_t* x, int32_t lo0,
+                              int64_t nseg, uint32_t* out) {
+  for (int64_t sg = blockIdx.x; sg < nseg; sg += gridDim.x) {
+    const uint32_t* src = bits + (u64)(x[sg] - (uint32_t)lo0) * row_words;
+    uint32_t* dst = out + (u64)sg * row_words;
+    for (uint32_t i = threadIdx.x; i < row_words; i += blockDim.x) dst[i] = src[i];
+  }
+}
+hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t* x, int32_t lo0, int64_t nseg,
+                       uint32_t* out, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  gather_rows_k<<<(unsigned)std::min<int64_t>(nseg, 1 << 16), 256, 0, s>>>(bits, row_words, x, lo0, nseg, out);
+  return hipGetLastError();
+}
+
 // hasin bit (y - lo1) for y in [lo1, lo1 + 32 * words): y has an in-edge in
 // the index of e by its Y column.
 __global__ void hasin_bits_k(IndexProbe rev, int32_t lo1, uint32_t words, uint32_t* out) {

@@ -103,6 +103,9 @@ hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words,
                         hipStream_t s);
 hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
                         int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s);
+// out row sg = bitmap row (x[sg] - lo0)
+hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t* x, int32_t lo0, int64_t nseg,
+                       uint32_t* out, hipStream_t s);
 hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
                        hipStream_t s);
 // Dense value heads (first key through a dictionary, second key direct).

@@ -119,15 +119,19 @@ hipError_t scan_exclusive_u64(const u64* in, u64* out, int64_t n, u64* total, vo
 // stable scatter.  In the scatter each wavefront ranks its keys with a
 // ballot-based match of equal digits and running per-wave digit counters in
 // LDS, so the pass is stable without a block-wide sort.
+// Tiles of RS_THREADS * ITEMS keys: 16 items per thread for large inputs,
+// 4 for small ones so that a few hundred thousand keys still spread over
+// every CU.
 constexpr int RS_THREADS = 256;
 constexpr int RS_WAVES = RS_THREADS / 64;
-constexpr int RS_ITEMS = 16;
-constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
+constexpr int RS_SMALL_ITEMS = 4;
+constexpr int64_t RS_SMALL_N = (int64_t)1 << 22;  // below this, small tiles
 
-template <typename K>
+template <typename K, int RS_ITEMS>
 __global__ __launch_bounds__(RS_THREADS) void rs_hist_k(const K* keys, int64_t n, int shift,
                                                          uint32_t dmask, uint32_t* hist,
                                                          uint32_t nblocks) {
+  constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -141,12 +145,13 @@ __global__ __launch_bounds__(RS_THREADS) void rs_hist_k(const K* keys, int64_t n
   hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-template <typename K>
+template <typename K, int RS_ITEMS>
 __global__ __launch_bounds__(RS_THREADS) void rs_scatter_k(const K* kin, const uint32_t* vin,
                                                             K* kout, uint32_t* vout, int64_t n,
                                                             int shift, int nbits,
                                                             const uint32_t* off,
                                                             uint32_t nblocks) {
+  constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
   __shared__ uint32_t cnt[RS_WAVES][256];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < RS_WAVES * 256; i += RS_THREADS) (&cnt[0][0])[i] = 0;
@@ -190,8 +195,10 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter_k(const K* kin, const u
   }
 }
 
+static int64_t rs_tile(int64_t n) { return (int64_t)RS_THREADS * (n < RS_SMALL_N ? RS_SMALL_ITEMS : 16); }
+
 size_t radix_temp_bytes(int64_t n) {
-  int64_t nb = (n + RS_TILE - 1) / RS_TILE;
+  int64_t nb = (n + rs_tile(n) - 1) / rs_tile(n);
   if (nb < 1) nb = 1;
   size_t hist = (((size_t)nb * 256 * 4) + 255) & ~(size_t)255;
   return hist + scan_temp_bytes(nb * 256);
@@ -202,7 +209,8 @@ static hipError_t radix_sort_t(K* keys, uint32_t* vals, K* keys_alt, uint32_t* v
                                int64_t n, int bits, void* temp, hipStream_t s, int* in_alt) {
   *in_alt = 0;
   if (n <= 1 || bits <= 0) return hipSuccess;
-  const uint32_t nb = (uint32_t)((n + RS_TILE - 1) / RS_TILE);
+  const bool small = n < RS_SMALL_N;
+  const uint32_t nb = (uint32_t)((n + rs_tile(n) - 1) / rs_tile(n));
   uint32_t* hist = (uint32_t*)temp;
   char* stemp = (char*)temp + ((((size_t)nb * 256 * 4) + 255) & ~(size_t)255);
   K* ka = keys;
@@ -211,10 +219,16 @@ static hipError_t radix_sort_t(K* keys, uint32_t* vals, K* keys_alt, uint32_t* v
   uint32_t* vb = vals ? vals_alt : nullptr;
   for (int shift = 0; shift < bits; shift += 8) {
     const int nbits = bits - shift < 8 ? bits - shift : 8;
-    rs_hist_k<K><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
+    if (small)
+      rs_hist_k<K, RS_SMALL_ITEMS><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
+    else
+      rs_hist_k<K, 16><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
     hipError_t e = scan_exclusive_u32(hist, hist, (int64_t)nb * 256, nullptr, stemp, s);
     if (e != hipSuccess) return e;
-    rs_scatter_k<K><<<nb, RS_THREADS, 0, s>>>(ka, va, kb, vb, n, shift, nbits, hist, nb);
+    if (small)
+      rs_scatter_k<K, RS_SMALL_ITEMS><<<nb, RS_THREADS, 0, s>>>(ka, va, kb, vb, n, shift, nbits, hist, nb);
+    else
+      rs_scatter_k<K, 16><<<nb, RS_THREADS, 0, s>>>(ka, va, kb, vb, n, shift, nbits, hist, nb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     K* tk = ka; ka = kb; kb = tk;
