@@ -1000,19 +1000,52 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
   if (MODE != EM_DCOUNT && st.stop) return;
   if (MODE == EM_SET || MODE == EM_BITSET) {
     int ins = 0;
-    if (act) {
-      const u64 key = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
-      if (MODE == EM_SET) {
-        ins = set_insert(e.table, e.mask, key, e.counters);
-      } else {
-        // dense domain: the packed key's two components index row and column
+    if (MODE == EM_SET) {
+      if (act) ins = set_insert(e.table, e.mask, pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1])),
+                                e.counters);
+    } else {
+      // Dense domain: the packed key's two components index row and column.
+      // Consecutive lanes that hit the same bitmap word (neighbouring second
+      // keys of one first key) form a run; the run's bits are OR-combined
+      // and its first lane does a single test-and-set for all of them.
+      u64 wi = ~0ull;
+      uint32_t bit = 0;
+      if (act) {
+        const u64 key = pack_key(e.key, getv(u, e.key.slot[0]), getv(u, e.key.slot[1]));
         const u64 b = e.key.nkey == 2
                           ? (key >> e.key.shift) * e.row_bits + (key & ((1ull << e.key.shift) - 1ull))
                           : key;
-        uint32_t* wp = e.bits + (b >> 5);
-        const uint32_t bit = 1u << (b & 31);
-        if (!(*wp & bit)) ins = (atomicOr(wp, bit) & bit) == 0;
+        wi = b >> 5;
+        bit = 1u << (b & 31);
       }
+      const int lane = lane_id();
+      const u64 prev = shfl_u64(wi, lane > 0 ? lane - 1 : 0);
+      const u64 am = __ballot(act);
+      const bool head = act && (lane == 0 || !((am >> (lane - 1)) & 1ull) || prev != wi);
+      const u64 heads = __ballot(head) | ~am;
+      const int h0 = 63 - __clzll((long long)(heads & ((2ull << lane) - 1ull)));
+      const u64 ahead = heads & ~((2ull << lane) - 1ull);
+      const int tail = (ahead ? __ffsll((long long)ahead) - 1 : 64) - 1;
+      // inclusive OR of the run's bits from its first lane
+      uint32_t incl = bit;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t t = __shfl_up(incl, d, 64);
+        if (lane - d >= h0) incl |= t;
+      }
+      const uint32_t before = __shfl_up(incl, 1, 64);
+      const uint32_t excl = lane > h0 ? before : 0u;  // bits of earlier lanes of the run
+      const uint32_t total = __shfl(incl, tail, 64);
+      uint32_t old = 0;
+      if (head) {
+        uint32_t* wp = e.bits + wi;
+        old = *wp;
+        if ((old & total) != total) old = atomicOr(wp, total);
+      }
+      old = __shfl(old, h0, 64);
+      // a bit is inserted once: by the first lane of the run that holds it,
+      // and only if the word did not have it before
+      if (act) ins = !(old & bit) && !(excl & bit);
     }
     const u64 m = __ballot(ins);
     if (m) {
