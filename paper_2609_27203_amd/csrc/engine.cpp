@@ -339,6 +339,7 @@ struct HeadRun {
   // set heads: append-only row list of every tuple; the delta is a range
   Buf rows[2];
   int64_t rows_cap = 0, nrows = 0, dbeg = 0, dend = 0, round_begin = 0;
+  int64_t round_new = 0;  // dense heads: tuples added this round
   // aggregate heads: delta rows (k0[, k1], value)
   Buf drow[3];
   int64_t dcap = 0, dn = 0;
@@ -352,6 +353,7 @@ struct HeadRun {
   // rows of row_bits bits indexed by the first key component
   bool dense = false;
   Buf bits;
+  Buf dbits;  // tuples new in this round (same layout as bits)
   u64 row_bits = 0;
   uint32_t row_words = 0;
   int64_t range0 = 0;
@@ -440,7 +442,31 @@ struct Runner {
         return c->fail(XL_UNSUPPORTED, "relation " + rel->name + " cannot be joined inside its own stratum");
       klo = (int32_t)h->dom_lo[col];
       khi = (int32_t)h->dom_hi[col];
-      if (h->is_set) {
+      if (h->dense) {  // rows of the current bitmap, in key order
+        n = h->keys;
+        void* snap[2] = {nullptr, nullptr};
+        for (int j = 0; j < h->nkey; ++j) XL_TRY(own((size_t)std::max<int64_t>(n, 1) * 4, "head snapshot", &snap[j]));
+        Buf tmp, tot;
+        if (h->nkey == 2) {
+          Buf cnt, off;
+          XL_TRY(dalloc(c, (size_t)h->range0 * 4, &cnt, "row counts"));
+          XL_TRY(dalloc(c, (size_t)(h->range0 + 1) * 4, &off, "row offsets"));
+          XL_TRY(dalloc(c, k::scan_temp_bytes(h->range0), &tmp, "scan scratch"));
+          HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
+          HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0,
+                                           off.as<uint32_t>() + h->range0, tmp.p, c->stream));
+          HIP_TRY(c, k::bits_to_rows(h->bits.as<uint32_t>(), h->range0, h->row_words, off.as<uint32_t>(),
+                                     h->kp.lo[0], h->kp.lo[1], (uint32_t*)snap[0], (uint32_t*)snap[1], c->stream));
+        } else {
+          const int64_t nbits = (h->range0 + 31) / 32 * 32;
+          XL_TRY(dalloc(c, k::bits_list_temp_bytes(nbits), &tmp, "compaction scratch"));
+          XL_TRY(dalloc(c, 8, &tot, "count"));
+          for (int pass = 0; pass < 2; ++pass)
+            HIP_TRY(c, k::bits_keys(h->bits.as<uint32_t>(), nbits, 1, h->kp.lo[0], 0, 1, false, (uint32_t*)snap[0],
+                                    nullptr, tot.as<uint32_t>(), tmp.p, pass == 1, c->stream));
+        }
+        for (int j = 0; j < h->nkey; ++j) rcol[j] = (const uint32_t*)snap[j];
+      } else if (h->is_set) {
         n = h->nrows;
         for (int j = 0; j < h->nkey; ++j) rcol[j] = h->rows[j].as<uint32_t>();
       } else {  // min/max: compact a snapshot of the current keys and values
@@ -700,7 +726,11 @@ struct Runner {
     const size_t bytes = (size_t)(total_bits / 8);
     XL_TRY(dalloc(c, bytes, &h->bits, "dense key bitmap"));
     HIP_TRY(c, hipMemsetAsync(h->bits.p, 0, bytes, c->stream));
-    h->rows_cap = std::max<int64_t>(((int64_t)1 << c->hash_min_log2) / 4, std::max<int64_t>(2 * h->preloaded, 1024));
+    XL_TRY(dalloc(c, bytes, &h->dbits, "dense delta bitmap"));
+    HIP_TRY(c, hipMemsetAsync(h->dbits.p, 0, bytes, c->stream));
+    // the row list only holds loaded rows (the seed scans them); derived
+    // tuples live in the bitmap and each round's delta in dbits
+    h->rows_cap = std::max<int64_t>(h->preloaded, 1);
     for (int j = 0; j < h->nkey; ++j) {
       XL_TRY(dalloc(c, (size_t)h->rows_cap * 4, &h->rows[j], "relation rows"));
       if (h->preloaded)
@@ -730,19 +760,7 @@ struct Runner {
     return XL_OK;
   }
 
-  xl_status grow_rows(HeadRun* h, int64_t need) {
-    int64_t ncap = std::max<int64_t>(h->rows_cap * 2, need);
-    Buf nr[2];
-    for (int j = 0; j < h->nkey; ++j) {
-      XL_TRY(dalloc(c, (size_t)ncap * 4, &nr[j], "relation rows"));
-      HIP_TRY(c, hipMemcpyAsync(nr[j].p, h->rows[j].p, (size_t)h->nrows * 4, hipMemcpyDeviceToDevice,
-                                c->stream));
-    }
-    for (int j = 0; j < h->nkey; ++j) std::swap(h->rows[j].p, nr[j].p);
-    h->rows_cap = ncap;
-    st->table_grows++;
-    return XL_OK;
-  }
+
 
   // Build the first-key dictionary, then the dense arrays if they fit; a
   // head that does not fit falls back to the hash table (h->dv cleared).
@@ -853,7 +871,6 @@ struct Runner {
 
   // Grow the head's table (and row list) so it holds at least `need` keys.
   xl_status grow(HeadRun* h, int64_t need) {
-    if (h->dense) return grow_rows(h, need);
     int64_t ncap = h->cap * 4;
     while (ncap / 2 < need || ncap - need < WAVE_SLACK * 4 * EMIT_GRID + 1024) ncap *= 2;
     Buf nt;
@@ -899,7 +916,7 @@ struct Runner {
     Source s{};
     HeadRun* h = head_of(p.driver);
     if (h && p.driver_delta) {
-      if (h->is_set) {
+      if (h->is_set && !h->dense) {
         for (int j = 0; j < h->nkey; ++j) s.col[j] = h->rows[j].as<uint32_t>() + h->dbeg;
         s.n = h->dend - h->dbeg;
       } else {
@@ -994,17 +1011,17 @@ struct Runner {
 
   // Turn the row-list delta [dbeg, dend) of a frontier head into delta bitmap
   // rows: sort by the first key, one delta row per distinct value.
-  // First frontier when the head started empty: every set bit is new, so the
-  // delta rows are the nonempty bitmap rows themselves (no regrouping sort).
+  // First frontier: the seed round's new tuples are the delta bitmap; its
+  // nonempty rows become the delta rows (no regrouping), then it is cleared.
   xl_status frontier_from_bits(HeadRun* h) {
     h->fn = 0;
     h->frontier_ready = true;
-    if (h->dend == h->dbeg) return XL_OK;
+    if (h->round_new == 0) return XL_OK;
     Buf cnt, tmp, tot;
     XL_TRY(dalloc(c, (size_t)h->range0 * 4, &cnt, "row counts"));
     XL_TRY(dalloc(c, k::compact_temp_bytes(h->range0), &tmp, "compaction scratch"));
     XL_TRY(dalloc(c, 8, &tot, "count"));
-    HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::row_popcount(h->dbits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
     KeyPack kx{};
     kx.nkey = 1;
     kx.lo[0] = h->kp.lo[0];
@@ -1012,53 +1029,14 @@ struct Runner {
                               h->fcnt[h->fcur].as<uint32_t>(), h->range0, tot.as<uint32_t>(), tmp.p, c->stream));
     uint32_t nseg = 0;
     XL_TRY(ctl_read(c, tot.p, 4, &nseg));
-    HIP_TRY(c, k::gather_rows(h->bits.as<uint32_t>(), h->row_words, h->fx.as<uint32_t>(), h->kp.lo[0], nseg,
+    HIP_TRY(c, k::gather_rows(h->dbits.as<uint32_t>(), h->row_words, h->fx.as<uint32_t>(), h->kp.lo[0], nseg,
                               h->fdiff[h->fcur].as<uint32_t>(), c->stream));
+    HIP_TRY(c, hipMemsetAsync(h->dbits.p, 0, (size_t)h->range0 * h->row_words * 4, c->stream));
     h->fn = nseg;
     return XL_OK;
   }
 
-  xl_status frontier_from_rows(HeadRun* h) {
-    const int64_t n = h->dend - h->dbeg;
-    h->fn = 0;
-    h->frontier_ready = true;
-    if (n == 0) return XL_OK;
-    uint32_t* r0 = h->rows[0].as<uint32_t>() + h->dbeg;
-    uint32_t* r1 = h->rows[1].as<uint32_t>() + h->dbeg;
-    Buf ka, kb, vb, tmp;
-    XL_TRY(dalloc(c, (size_t)n * 4, &ka, "regroup keys"));
-    XL_TRY(dalloc(c, (size_t)n * 4, &kb, "regroup keys"));
-    XL_TRY(dalloc(c, (size_t)n * 4, &vb, "regroup values"));
-    XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
-    HIP_TRY(c, k::sub_lo(r0, h->kp.lo[0], ka.as<uint32_t>(), n, c->stream));
-    int alt = 0;
-    HIP_TRY(c, k::radix_sort_u32(ka.as<uint32_t>(), r1, kb.as<uint32_t>(), vb.as<uint32_t>(), n, h->bits0,
-                                 tmp.p, c->stream, &alt));
-    uint32_t* sk = alt ? kb.as<uint32_t>() : ka.as<uint32_t>();
-    uint32_t* sy = alt ? vb.as<uint32_t>() : r1;
-    HIP_TRY(c, k::add_u32(sk, (uint32_t)h->kp.lo[0], r0, n, c->stream));
-    Buf flag, pos, tot, starts;
-    XL_TRY(dalloc(c, (size_t)n * 4, &flag, "segment flags"));
-    XL_TRY(dalloc(c, (size_t)n * 4, &pos, "segment ids"));
-    XL_TRY(dalloc(c, 8, &tot, "count"));
-    tmp.reset();
-    XL_TRY(dalloc(c, k::scan_temp_bytes(n), &tmp, "scan scratch"));
-    const uint32_t* cols[1] = {r0};
-    HIP_TRY(c, k::row_change_flags(cols, 1, n, flag.as<uint32_t>(), c->stream));
-    HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), n, tot.as<uint32_t>(), tmp.p,
-                                     c->stream));
-    uint32_t nseg = 0;
-    XL_TRY(ctl_read(c, tot.p, 4, &nseg));
-    XL_TRY(dalloc(c, (size_t)nseg * 4, &starts, "segment starts"));
-    HIP_TRY(c, k::seg_starts(flag.as<uint32_t>(), pos.as<uint32_t>(), n, starts.as<uint32_t>(), c->stream));
-    HIP_TRY(c, k::seg_first_x(starts.as<uint32_t>(), nseg, r0, h->fx.as<uint32_t>(), c->stream));
-    HIP_TRY(c, hipMemsetAsync(h->fcnt[h->fcur].p, 0xff, (size_t)nseg * 4, c->stream));  // every row non-empty
-    HIP_TRY(c, hipMemsetAsync(h->fdiff[h->fcur].p, 0, (size_t)nseg * h->row_words * 4, c->stream));
-    HIP_TRY(c, k::rows_to_frontier(sy, flag.as<uint32_t>(), pos.as<uint32_t>(), n, h->kp.lo[1], h->row_words,
-                                   h->fdiff[h->fcur].as<uint32_t>(), c->stream));
-    h->fn = nseg;
-    return XL_OK;
-  }
+
 
   // h(X, count(V)) :- r(..., X, ..., V, ...) with distinct variables, nothing
   // else in the body, over a finished relation that already has an index by
@@ -1320,21 +1298,13 @@ struct Runner {
           a.emit.dchg = h->dchg.as<uint32_t>();
           a.emit.is_max = h->agg == Agg::MAX;
           a.emit.delta_idx = h->didx.as<uint32_t>() + h->didx_n;
-        } else if (h->dense) {
-          const int64_t max_rows = h->rows_cap - WAVE_SLACK * waves - 1024;
-          if (h->nrows >= max_rows) {
-            XL_TRY(grow_rows(h, h->nrows + 2 * (WAVE_SLACK * waves + 1024)));
-            continue;
-          }
+        } else if (h->dense) {  // bitmap and delta bitmap cover the whole domain
           HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-          a.emit.limit = (u64)(max_rows - h->nrows);
+          a.emit.limit = ~0ull;
           a.emit.mode = EM_BITSET;
           a.emit.bits = h->bits.as<uint32_t>();
           a.emit.row_bits = h->row_bits;
-          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
-          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
-          a.emit.row_base = h->nrows;
-          a.emit.row_cap = h->rows_cap;
+          a.emit.dchg = h->dbits.as<uint32_t>();
         } else {
         const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
         if (h->keys >= max_keys) {
@@ -1379,7 +1349,10 @@ struct Runner {
           return c->fail(XL_DEVICE_ERROR, h->dv ? "key outside the dense domain (internal)"
                                                 : "hash table probe exhausted or row list overflow (internal)");
         cands += (int64_t)cnt[CNT_CANDIDATES];
-        if (h->is_set) {
+        if (h->dense) {
+          h->keys += (int64_t)cnt[CNT_APPENDED];
+          h->round_new += (int64_t)cnt[CNT_APPENDED];
+        } else if (h->is_set) {
           h->nrows += (int64_t)cnt[CNT_APPENDED];
           h->keys += (int64_t)cnt[CNT_APPENDED];
         } else {
@@ -1390,7 +1363,7 @@ struct Runner {
           return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                    std::to_string(h->rel->max_rows));
         if (!cnt[CNT_OVERFLOW]) break;
-        XL_TRY(grow(h, h->dense ? h->nrows + 2 * (WAVE_SLACK * waves + 1024) : h->keys * 2 + 1));
+        XL_TRY(grow(h, h->keys * 2 + 1));
         if (h->is_minmax) {  // slot indices moved: rebuild this round's delta list
           Buf tmp, tot;
           XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
@@ -1422,6 +1395,7 @@ struct Runner {
 
   void begin_round(HeadRun* h) {
     h->round++;
+    h->round_new = 0;
     h->round_begin = h->nrows;
     h->didx_n = 0;
     h->cn = 0;
@@ -1433,12 +1407,32 @@ struct Runner {
       *delta = h->fnew;
       return XL_OK;
     }
+    if (h->dense) {
+      *delta = h->round_new;
+      if (h->frontier) return frontier_from_bits(h);  // seed round -> first frontier
+      // this round's new tuples, in key order, become the delta rows
+      const int64_t nbits = (int64_t)(h->nkey == 2 ? (u64)h->range0 * h->row_bits : (u64)((h->range0 + 31) / 32) * 32);
+      Buf tmp, tot;
+      XL_TRY(dalloc(c, k::bits_list_temp_bytes(nbits), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      auto keys = [&](bool write) {
+        return k::bits_keys(h->dbits.as<uint32_t>(), nbits, h->row_bits, h->kp.lo[0], h->kp.lo[1], h->nkey, true,
+                            h->drow[0].as<uint32_t>(), h->nkey == 2 ? h->drow[1].as<uint32_t>() : nullptr,
+                            tot.as<uint32_t>(), tmp.p, write, c->stream);
+      };
+      HIP_TRY(c, keys(false));
+      uint32_t n = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &n));
+      if ((int64_t)n != h->round_new) return c->fail(XL_DEVICE_ERROR, "delta bitmap count mismatch (internal)");
+      XL_TRY(ensure_drow(h, n));
+      if (n) HIP_TRY(c, keys(true));
+      h->dn = n;
+      return XL_OK;
+    }
     if (h->is_set) {
       h->dbeg = h->round_begin;
       h->dend = h->nrows;
       *delta = h->dend - h->dbeg;
-      if (h->frontier)  // seed round -> first frontier
-        XL_TRY(h->preloaded == 0 ? frontier_from_bits(h) : frontier_from_rows(h));
       return XL_OK;
     }
     if (h->dcount) {
@@ -1586,7 +1580,26 @@ struct Runner {
 
   xl_status materialize_rows(HeadRun* h) {
     Relation* r = h->rel;
-    if (h->frontier) {  // every tuple is a set bit: rows in ascending (x, y)
+    if (h->dense && h->nkey == 1) {  // one bitmap row: the set bits in order
+      const int64_t nbits = (h->range0 + 31) / 32 * 32;
+      Buf tmp, tot, out;
+      XL_TRY(dalloc(c, k::bits_list_temp_bytes(nbits), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->keys, 1) * 4, &out, "relation column"));
+      HIP_TRY(c, k::bits_keys(h->bits.as<uint32_t>(), nbits, 1, h->kp.lo[0], 0, 1, false, out.as<uint32_t>(), nullptr,
+                              tot.as<uint32_t>(), tmp.p, false, c->stream));
+      uint32_t n = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &n));
+      if ((int64_t)n != h->keys) return c->fail(XL_DEVICE_ERROR, "bitmap key count mismatch (internal)");
+      HIP_TRY(c, k::bits_keys(h->bits.as<uint32_t>(), nbits, 1, h->kp.lo[0], 0, 1, false, out.as<uint32_t>(), nullptr,
+                              tot.as<uint32_t>(), tmp.p, true, c->stream));
+      h->rows[0].reset();
+      relation_free_storage(r);
+      r->col[0] = (uint32_t*)out.keep();
+      r->nrows = n;
+      return XL_OK;
+    }
+    if (h->dense) {  // every tuple is a set bit: rows in ascending (x, y)
       // off (range0 + 1 words) doubles as the CSR offsets of the finished
       // relation by its first column, kept as a ready index for later strata
       Buf cnt, off, tmp;

@@ -230,24 +230,6 @@ hipError_t frontier_round(const FrontierArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Delta rows of a row range sorted by its first key.  head[i] flags the first
-// row of each key and pos is the exclusive scan of head, so row i belongs to
-// delta row pos[i] + head[i] - 1.
-__global__ void rows_to_frontier_k(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
-                                   int32_t lo1, uint32_t row_words, uint32_t* diff) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t seg = pos[i] + head[i] - 1u;
-    const uint32_t y = ycol[i] - (uint32_t)lo1;
-    atomicOr(&diff[(u64)seg * row_words + (y >> 5)], 1u << (y & 31));
-  }
-}
-hipError_t rows_to_frontier(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
-                            int32_t lo1, uint32_t row_words, uint32_t* diff, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  rows_to_frontier_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(ycol, head, pos, n, lo1, row_words, diff);
-  return hipGetLastError();
-}
 
 // Number of set bits in each bitmap row.
 __global__ __launch_bounds__(256) void row_popcount_k(const uint32_t* bits, int64_t nrows,

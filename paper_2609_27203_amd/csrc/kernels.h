@@ -95,10 +95,6 @@ hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const
                          int64_t n, KeyPack kp, hipStream_t s);
 hipError_t frontier_round(const FrontierArgs& a, hipStream_t s);
 hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s);
-// Delta bitmap rows of a row range sorted by its first key (head = first-row
-// flags, pos = their exclusive scan).
-hipError_t rows_to_frontier(const uint32_t* ycol, const uint32_t* head, const uint32_t* pos, int64_t n,
-                            int32_t lo1, uint32_t row_words, uint32_t* diff, hipStream_t s);
 hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
                         hipStream_t s);
 hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
@@ -106,8 +102,6 @@ hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words,
 // out row sg = bitmap row (x[sg] - lo0)
 hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t* x, int32_t lo0, int64_t nseg,
                        uint32_t* out, hipStream_t s);
-hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
-                       hipStream_t s);
 // Dense value heads (first key through a dictionary, second key direct).
 // Rows of every present slot in slot order (= ascending keys).
 hipError_t dense_rows(const uint32_t* vals, const uint32_t* pres, const uint32_t* dict, int64_t n,
@@ -129,6 +123,11 @@ size_t bits_list_temp_bytes(int64_t nbits);
 hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, void* temp, bool write,
                      hipStream_t s);
 hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);
+// Rows of the set bits of a dense key bitmap in bit order (two calls on the
+// same temp as bits_list; temp sized by bits_list_temp_bytes); clear = zero
+// the words read.
+hipError_t bits_keys(uint32_t* bits, int64_t nbits, u64 row_bits, int32_t lo0, int32_t lo1, int nkey, bool clear,
+                     uint32_t* c0, uint32_t* c1, uint32_t* total, void* temp, bool write, hipStream_t s);
 hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
                             uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
                             uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s);

@@ -1007,7 +1007,9 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
       // Dense domain: the packed key's two components index row and column.
       // Consecutive lanes that hit the same bitmap word (neighbouring second
       // keys of one first key) form a run; the run's bits are OR-combined
-      // and its first lane does a single test-and-set for all of them.
+      // and its first lane does a single test-and-set for all of them.  The
+      // bits that were off are this round's new tuples: they are set in the
+      // delta bitmap (dchg), which is turned into rows after the round.
       u64 wi = ~0ull;
       uint32_t bit = 0;
       if (act) {
@@ -1033,19 +1035,20 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
         const uint32_t t = __shfl_up(incl, d, 64);
         if (lane - d >= h0) incl |= t;
       }
-      const uint32_t before = __shfl_up(incl, 1, 64);
-      const uint32_t excl = lane > h0 ? before : 0u;  // bits of earlier lanes of the run
       const uint32_t total = __shfl(incl, tail, 64);
-      uint32_t old = 0;
       if (head) {
         uint32_t* wp = e.bits + wi;
-        old = *wp;
-        if ((old & total) != total) old = atomicOr(wp, total);
+        const uint32_t cur = *wp;
+        if ((cur & total) != total) {
+          // the bits this run turned on are new tuples: they go to the delta bitmap
+          const uint32_t fresh = total & ~atomicOr(wp, total);
+          if (fresh) {
+            atomicOr(&e.dchg[wi], fresh);
+            st.ins_pend += (uint32_t)__popc(fresh);
+          }
+        }
       }
-      old = __shfl(old, h0, 64);
-      // a bit is inserted once: by the first lane of the run that holds it,
-      // and only if the word did not have it before
-      if (act) ins = !(old & bit) && !(excl & bit);
+      return;
     }
     const u64 m = __ballot(ins);
     if (m) {
@@ -1254,13 +1257,25 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT || MODE == EM_DMIN ||
       MODE == EM_MARK) {
     // one atomic per workgroup: a shared counter hit by every wave serializes
-    __shared__ u64 s_cands[ST_WAVES];
-    if (lane == 0) s_cands[w] = st.cands;
+    __shared__ u64 s_cands[ST_WAVES], s_new[ST_WAVES];
+    u64 nw = 0;
+    if (MODE == EM_BITSET) {  // new tuples: per-lane counts summed over the wave
+      nw = st.ins_pend;
+      for (int k = 32; k > 0; k >>= 1) nw += __shfl_xor(nw, k, 64);
+    }
+    if (lane == 0) {
+      s_cands[w] = st.cands;
+      s_new[w] = nw;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
-      u64 t = 0;
-      for (int i = 0; i < ST_WAVES; ++i) t += s_cands[i];
+      u64 t = 0, tn = 0;
+      for (int i = 0; i < ST_WAVES; ++i) {
+        t += s_cands[i];
+        tn += s_new[i];
+      }
       if (t) atomicAdd(&a.emit.counters[CNT_CANDIDATES], t);
+      if (tn) atomicAdd(&a.emit.counters[CNT_APPENDED], tn);
     }
   }
   if (MODE == EM_DCOUNT && st.pend_cnt && lane == 0) atomicAdd(&a.emit.bits[st.pend_idx], st.pend_cnt);
@@ -1324,6 +1339,53 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
     bits[w0 + k] = 0u;
     for (uint32_t b = d[k]; b; b &= b - 1) list[p++] = (uint32_t)(w0 + k) * 32u + (uint32_t)(__ffs(b) - 1);
   }
+}
+
+// Rows (k0, k1) of the set bits of a dense key bitmap, in bit order: bit b
+// is k0 = lo0 + b / row_bits, k1 = lo1 + b % row_bits (one key: k0 = lo0 + b).
+// Optionally clears the words it read (a delta bitmap).
+__global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_t nw, const uint32_t* off,
+                                                          u64 row_bits, int32_t lo0, int32_t lo1, int nkey,
+                                                          bool clear, uint32_t* c0, uint32_t* c1) {
+  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
+  uint32_t d[MK_WPT], c = 0;
+#pragma unroll
+  for (int k = 0; k < MK_WPT; ++k) {
+    d[k] = w0 + k < nw ? bits[w0 + k] : 0u;
+    c += __popc(d[k]);
+  }
+  uint32_t tot;
+  uint32_t p = off[blockIdx.x] + block_excl_scan<uint32_t>(c, &tot);
+#pragma unroll
+  for (int k = 0; k < MK_WPT; ++k) {
+    if (!d[k]) continue;
+    if (clear) bits[w0 + k] = 0u;
+    for (uint32_t b = d[k]; b; b &= b - 1) {
+      const u64 bi = (u64)(w0 + k) * 32u + (u64)(__ffs(b) - 1);
+      if (nkey == 2) {
+        c0[p] = (uint32_t)lo0 + (uint32_t)(bi / row_bits);
+        c1[p] = (uint32_t)lo1 + (uint32_t)(bi % row_bits);
+      } else {
+        c0[p] = (uint32_t)lo0 + (uint32_t)bi;
+      }
+      ++p;
+    }
+  }
+}
+
+hipError_t bits_keys(uint32_t* bits, int64_t nbits, u64 row_bits, int32_t lo0, int32_t lo1, int nkey, bool clear,
+                     uint32_t* c0, uint32_t* c1, uint32_t* total, void* temp, bool write, hipStream_t s) {
+  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
+  uint32_t* cnt = (uint32_t*)temp;
+  uint32_t* off = cnt + ((nb + 63) & ~63ll);
+  char* stemp = (char*)(off + ((nb + 63) & ~63ll));
+  if (!write) {
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, cnt);
+    return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
+  }
+  bits_keys_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, off, row_bits, lo0, lo1, nkey, clear, c0, c1);
+  return hipGetLastError();
 }
 
 size_t bits_list_temp_bytes(int64_t nbits) {
@@ -1705,19 +1767,6 @@ hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const
   return hipGetLastError();
 }
 
-// First-key value of every segment of a row range sorted by that key.
-__global__ void seg_first_x_k(const uint32_t* starts, int64_t nseg, const uint32_t* xcol,
-                              uint32_t* out_x) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nseg;
-       i += (int64_t)gridDim.x * blockDim.x)
-    out_x[i] = xcol[starts[i]];
-}
-hipError_t seg_first_x(const uint32_t* starts, int64_t nseg, const uint32_t* xcol, uint32_t* out_x,
-                       hipStream_t s) {
-  if (nseg <= 0) return hipSuccess;
-  seg_first_x_k<<<grid_for(nseg, 256, 65536), 256, 0, s>>>(starts, nseg, xcol, out_x);
-  return hipGetLastError();
-}
 
 __global__ void add_u32_k(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
