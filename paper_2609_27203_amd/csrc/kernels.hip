@@ -1343,33 +1343,38 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
 
 // Rows (k0, k1) of the set bits of a dense key bitmap, in bit order: bit b
 // is k0 = lo0 + b / row_bits, k1 = lo1 + b % row_bits (one key: k0 = lo0 + b).
-// Optionally clears the words it read (a delta bitmap).
+// Optionally clears the words it read (a delta bitmap).  A workgroup owns
+// MK_WORDS consecutive words (the same ranges as bits_count_k) and walks them
+// in steps of one word per thread: the step's set bits are ranked by a block
+// scan and staged in LDS, then written out with consecutive threads on
+// consecutive rows.
 __global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_t nw, const uint32_t* off,
                                                           u64 row_bits, int32_t lo0, int32_t lo1, int nkey,
                                                           bool clear, uint32_t* c0, uint32_t* c1) {
-  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
-  uint32_t d[MK_WPT], c = 0;
-#pragma unroll
+  __shared__ uint32_t stage[MK_THREADS * 32];
+  uint32_t p = off[blockIdx.x];
   for (int k = 0; k < MK_WPT; ++k) {
-    d[k] = w0 + k < nw ? bits[w0 + k] : 0u;
-    c += __popc(d[k]);
-  }
-  uint32_t tot;
-  uint32_t p = off[blockIdx.x] + block_excl_scan<uint32_t>(c, &tot);
-#pragma unroll
-  for (int k = 0; k < MK_WPT; ++k) {
-    if (!d[k]) continue;
-    if (clear) bits[w0 + k] = 0u;
-    for (uint32_t b = d[k]; b; b &= b - 1) {
-      const u64 bi = (u64)(w0 + k) * 32u + (u64)(__ffs(b) - 1);
-      if (nkey == 2) {
-        c0[p] = (uint32_t)lo0 + (uint32_t)(bi / row_bits);
-        c1[p] = (uint32_t)lo1 + (uint32_t)(bi % row_bits);
-      } else {
-        c0[p] = (uint32_t)lo0 + (uint32_t)bi;
-      }
-      ++p;
+    const int64_t wi = (int64_t)blockIdx.x * MK_WORDS + (int64_t)k * MK_THREADS + threadIdx.x;
+    const uint32_t d = wi < nw ? bits[wi] : 0u;
+    uint32_t tot;
+    uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
+    if (d) {
+      if (clear) bits[wi] = 0u;
+      for (uint32_t b = d; b; b &= b - 1) stage[q++] = (uint32_t)(k * MK_THREADS + threadIdx.x) * 32u + (uint32_t)(__ffs(b) - 1);
     }
+    __syncthreads();
+    const u64 base = (u64)blockIdx.x * MK_WORDS * 32u;
+    for (uint32_t r = threadIdx.x; r < tot; r += MK_THREADS) {
+      const u64 bi = base + stage[r];
+      if (nkey == 2) {
+        c0[p + r] = (uint32_t)lo0 + (uint32_t)(bi / row_bits);
+        c1[p + r] = (uint32_t)lo1 + (uint32_t)(bi % row_bits);
+      } else {
+        c0[p + r] = (uint32_t)lo0 + (uint32_t)bi;
+      }
+    }
+    p += tot;
+    __syncthreads();
   }
 }
 
