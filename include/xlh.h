@@ -140,6 +140,10 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     in-edge is expanded by pulling (scanning in-edges of the
  *                     unreached targets) when pull_ratio * d >= u; 0 = always
  *                     push (default 64)
+ *   "dense_tiles"     rounds of a carried min/max rule over a dense head run
+ *                     one workgroup per (first key, tile of second keys) with
+ *                     the tile in LDS: 0 = choose the tile count (default),
+ *                     k = k tiles per first key, -1 = untiled emission
  * XL_INVALID_ARGUMENT for an unknown key or value.
  */
 xl_status xl_context_set_option(xl_context* ctx, const char* key, int64_t value);

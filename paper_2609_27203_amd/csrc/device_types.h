@@ -179,6 +179,35 @@ struct DensePullArgs {
   unsigned long long* counters;  // CNT_INSERTED: keys new to the full relation; CNT_FATAL
 };
 
+// One round of a carried-value rule over a dense min/max head, tiled: the
+// workgroup for (rank r, tile t) keeps value slots [t * tile, t * tile + tile)
+// of rank r's row in LDS, walks all delta rows of rank r (grouped by rank,
+// roff), expands each through e's index by Z and folds the candidates whose Y
+// falls in its tile with LDS atomicMin.  It owns those slots, so the write-back
+// of values, presence and delta bits needs no global atomics.
+struct DenseTileArgs {
+  const uint32_t* dk1;    // delta rows of this round: Z and value, grouped by rank
+  const uint32_t* dval;
+  const uint32_t* roff;   // [n0 + 1] first delta row of each rank
+  const uint32_t* dict;   // rank -> first key value
+  uint32_t n0;
+  uint32_t range1;        // slots per rank (a multiple of 32)
+  int32_t lo1;
+  uint32_t tile, ntiles;  // tile width (a multiple of 32) and tiles per rank
+  IndexProbe idx;         // e's columns grouped by (Z, tile of Y); act[] = the rule's actions on e
+  const uint32_t* toff;   // [(z - idx.key_lo) * (ntiles + 1) + t]: first row of Z value z in tile t
+  int32_t ycol;           // column of e bound to Y
+  int8_t slot_s, slot_z, slot_p, slot_y, val_slot;
+  uint8_t val_type, is_max;
+  int32_t nops;
+  MicroOp ops[MAXOPS];
+  uint32_t consts[MAXK];
+  uint32_t* vals;         // encoded values (fold_encode), presence bits, delta bits
+  uint32_t* pres;
+  uint32_t* chg;
+  unsigned long long* counters;  // CNT_CANDIDATES, CNT_INSERTED (new keys), CNT_APPENDED (improved keys)
+};
+
 // Closure-shaped recursive rule head(X, Y) :- delta head(X, Z), e(Z, Y) over a
 // dense set head, run in frontier form: the delta of every first-key value x
 // is a bitmap row holding the Z values that became true in the previous

@@ -384,6 +384,15 @@ struct HeadRun {
   Buf ndrow[3];
   bool pulled = false;
   int64_t pull_n = 0;
+  // dense min/max heads with one carried-value variant: tiled rounds, the
+  // delta rows grouped by rank (roff: first row of each rank)
+  bool tiled = false;
+  Buf roff;
+  // e's rows grouped by (Z, tile of Y), built at the first tiled round
+  std::vector<std::unique_ptr<Buf>> tcols;
+  Buf toff;
+  IndexProbe tidx{};
+  uint32_t tile = 0, ntiles = 0;
   // key-column domains (bounds recorded on the materialized relation)
   int64_t dom_lo[2] = {0, 0}, dom_hi[2] = {0, 0};
 };
@@ -580,7 +589,7 @@ struct Runner {
     if (hr->is_minmax && h->nrows > 0) src.push_back({h, 0});  // loaded rows
     hr->dv = true;
     hr->dmap_n = r0;
-    hr->range1 = r1;
+    hr->range1 = (r1 + 31) / 32 * 32;  // rank rows start on word boundaries
     hr->dict_src = src;
   }
 
@@ -667,7 +676,11 @@ struct Runner {
           hr->range1 = r1;
         }
       }
-      if (hr->is_minmax && c->index_mode != 1) plan_dense_values(s, hr.get());
+      if (hr->is_minmax && c->index_mode != 1) {
+        plan_dense_values(s, hr.get());
+        hr->tiled = hr->dv && hr->nkey == 2 && c->dense_tiles >= 0 && s.recursive && s.heads.size() == 1 &&
+                    s.variants.size() == 1 && s.variants[0].carried_val;
+      }
       if ((hr->agg == Agg::SUM || hr->agg == Agg::LSE) && hr->nkey == 2 && c->index_mode != 1 && s.recursive &&
           s.heads.size() == 1 && s.variants.size() == 1 && s.variants[0].carried_val) {
         plan_dense_values(s, hr.get());
@@ -786,7 +799,7 @@ struct Runner {
     const double slots = (double)std::max<uint32_t>(n0, 1) * (double)h->range1;
     const double budget = std::min(8589934592.0, (double)c->arena.capacity() / 4);
     if (slots >= 4294967296.0 || slots * (h->ds ? 16.5 : 8.25) > budget) {
-      h->dv = h->ds = false;
+      h->dv = h->ds = h->tiled = false;
       h->dmap.reset();
       return XL_OK;
     }
@@ -800,6 +813,7 @@ struct Runner {
     HIP_TRY(c, hipMemsetAsync(h->dvals.p, 0xff, ns * 4, c->stream));
     HIP_TRY(c, hipMemsetAsync(h->dpres.p, 0, nw * 4, c->stream));
     HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nw * 4, c->stream));
+    if (h->tiled) XL_TRY(dalloc(c, (size_t)(n0 + 1) * 4, &h->roff, "delta rows per rank"));
     if (h->ds) {
       XL_TRY(dalloc(c, ns * 4, &h->dcur, "dense delta values"));
       XL_TRY(dalloc(c, ns * 4, &h->dnext, "dense delta values"));
@@ -1156,10 +1170,123 @@ struct Runner {
     return XL_OK;
   }
 
+  // Tile layout (as many slots as fit 128 KB of LDS, or fewer so that every
+  // CU gets a workgroup; a multiple of 32 slots) and e's rows
+  // sorted by (Z, tile of Y) with offsets per (Z, tile), so a tile's
+  // workgroup reads only the rows that land in it.
+  xl_status build_tile_index(const RulePlan& p, HeadRun* h) {
+    const StepPlan& sp = p.steps[0];
+    Relation* e = sp.rel;
+    const uint32_t max_tile = 32768;
+    uint32_t nt = (uint32_t)((h->range1 + max_tile - 1) / max_tile);
+    if (c->dense_tiles > 0) nt = (uint32_t)c->dense_tiles;
+    else nt = std::max<uint32_t>(nt, (uint32_t)((256 + h->n0 - 1) / std::max<int64_t>(h->n0, 1)));
+    uint32_t tile = (uint32_t)(((h->range1 + nt - 1) / nt + 31) / 32 * 32);
+    tile = std::min<uint32_t>(std::max<uint32_t>(tile, 32), max_tile);
+    h->tile = tile;
+    h->ntiles = (uint32_t)((h->range1 + tile - 1) / tile);
+    const int64_t n = e->nrows;
+    IndexProbe& q = h->tidx;
+    q = IndexProbe{};
+    q.ncols = e->arity;
+    const int zc = sp.key_col;
+    const int64_t zr = n ? (int64_t)e->hi[zc] - e->lo[zc] + 1 : 0;
+    const int64_t nkeys = zr * (h->ntiles + 1);
+    if (nkeys >= ((int64_t)1 << 31)) return c->fail(XL_UNSUPPORTED, "tiled index key range too large");
+    q.key_lo = n ? e->lo[zc] : 0;
+    q.key_range = (uint32_t)zr;
+    XL_TRY(dalloc(c, (size_t)(nkeys + 1) * 4, &h->toff, "tiled index offsets"));
+    if (n == 0) {
+      HIP_TRY(c, hipMemsetAsync(h->toff.p, 0, 4, c->stream));
+      return XL_OK;
+    }
+    if (n > ((int64_t)1 << 30)) return c->fail(XL_UNSUPPORTED, "relation " + e->name + " too large to tile");
+    Buf keys, keys2, perm, perm2, tmp;
+    XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
+    XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
+    HIP_TRY(c, k::tile_keys(e->col[zc], e->col[p.carried_ycol], n, e->lo[zc], h->kp.lo[1], h->tile, h->ntiles,
+                            keys.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
+    int alt = 0;
+    HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(), perm2.as<uint32_t>(),
+                                 n, std::max(1, bitlen((uint64_t)nkeys - 1)), tmp.p, c->stream, &alt));
+    uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
+    uint32_t* spm = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+    for (int j = 0; j < e->arity; ++j) {
+      h->tcols.push_back(std::make_unique<Buf>());
+      XL_TRY(dalloc(c, (size_t)n * 4, h->tcols.back().get(), "tiled index column"));
+      HIP_TRY(c, k::gather_u32(e->col[j], spm, h->tcols.back()->as<uint32_t>(), n, c->stream));
+      q.col[j] = h->tcols.back()->as<uint32_t>();
+    }
+    HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)nkeys, h->toff.as<uint32_t>(), c->stream));
+    return XL_OK;
+  }
+
+  // One round of the carried-value variant over a dense min/max head: one
+  // workgroup per (rank, tile of second-key slots) with the tile in LDS.
+  xl_status eval_dense_tiles(const RulePlan& p, HeadRun* h) {
+    if (h->dn == 0) return XL_OK;
+    const StepPlan& sp = p.steps[0];
+    DenseTileArgs a{};
+    a.dk1 = h->drow[1].as<uint32_t>();
+    a.dval = h->drow[2].as<uint32_t>();
+    a.roff = h->roff.as<uint32_t>();
+    a.dict = h->dict.as<uint32_t>();
+    a.n0 = (uint32_t)h->n0;
+    a.range1 = (uint32_t)h->range1;
+    a.lo1 = h->kp.lo[1];
+    if (!h->toff.p) XL_TRY(build_tile_index(p, h));
+    a.tile = h->tile;
+    a.ntiles = h->ntiles;
+    a.idx = h->tidx;
+    a.toff = h->toff.as<uint32_t>();
+    for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
+    a.ycol = p.carried_ycol;
+    a.slot_s = (int8_t)p.cv_slot_s;
+    a.slot_z = (int8_t)p.cv_slot_z;
+    a.slot_p = (int8_t)p.cv_slot_p;
+    a.slot_y = (int8_t)p.key_slot[1];
+    a.val_slot = (int8_t)p.val_slot;
+    a.val_type = p.val_type;
+    a.is_max = h->agg == Agg::MAX;
+    a.nops = (int32_t)p.stage_ops[0].size();
+    for (int i = 0; i < a.nops; ++i) a.ops[i] = p.stage_ops[0][i];
+    for (size_t i = 0; i < p.stage_consts[0].size(); ++i) a.consts[i] = p.stage_consts[0][i];
+    a.vals = h->dvals.as<uint32_t>();
+    a.pres = h->dpres.as<uint32_t>();
+    a.chg = h->dchg.as<uint32_t>();
+    a.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+    HIP_TRY(c, k::dense_min_tiles(a, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->emit_ms += ms;
+      st->emit_launches++;
+      st->emit_source_rows += h->dn;
+      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->emit_new += (int64_t)cnt[CNT_APPENDED];
+    }
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    h->keys += (int64_t)cnt[CNT_INSERTED];
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
   xl_status eval_plan(const RulePlan& p) {
     HeadRun* h = head_of(p.head);
     if (h->frontier && p.driver_delta) return eval_frontier(p, h);
     if (h->ds && p.driver_delta) return eval_dense_pull(p, h);
+    if (h->tiled && p.driver_delta) return eval_dense_tiles(p, h);
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
@@ -1453,6 +1580,26 @@ struct Runner {
       const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
       HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)((ns + 31) / 32) * 4, c->stream));
       *delta = h->dn;
+      return XL_OK;
+    }
+    if (h->tiled) {  // delta rows from the delta bits, grouped by rank
+      const uint32_t wpr = (uint32_t)(h->range1 / 32);
+      Buf cnt, tmp;
+      XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->n0, 1) * 4, &cnt, "delta rows per rank"));
+      XL_TRY(dalloc(c, k::scan_temp_bytes(h->n0), &tmp, "scan scratch"));
+      HIP_TRY(c, k::row_popcount(h->dchg.as<uint32_t>(), h->n0, wpr, cnt.as<uint32_t>(), c->stream));
+      HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), h->roff.as<uint32_t>(), h->n0,
+                                       h->roff.as<uint32_t>() + h->n0, tmp.p, c->stream));
+      uint32_t n = 0;
+      XL_TRY(ctl_read(c, h->roff.as<uint32_t>() + h->n0, 4, &n));
+      XL_TRY(ensure_drow(h, n));
+      if (n)
+        HIP_TRY(c, k::dense_delta_by_rank(h->dchg.as<uint32_t>(), (uint32_t)h->n0, wpr, h->roff.as<uint32_t>(),
+                                          h->dvals.as<uint32_t>(), h->dict.as<uint32_t>(), h->kp.lo[1],
+                                          h->rel->types[h->nkey], h->fold, h->drow[0].as<uint32_t>(),
+                                          h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(), c->stream));
+      h->dn = n;
+      *delta = n;
       return XL_OK;
     }
     if (h->dv && !h->ds) {

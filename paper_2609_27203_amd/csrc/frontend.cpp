@@ -488,7 +488,8 @@ struct Planner {
       }
     }
     // carried value shape (see RulePlan::carried_val)
-    if (delta && p.driver == p.head && p.head->arity == 3 && (r.agg == Agg::SUM || r.agg == Agg::LSE) &&
+    if (delta && p.driver == p.head && p.head->arity == 3 &&
+        (r.agg == Agg::SUM || r.agg == Agg::LSE || r.agg == Agg::MIN || r.agg == Agg::MAX) &&
         nst == 1 && p.steps[0].rel != p.head && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
         (p.driver_act[2].kind == CA_BIND || p.driver_act[2].kind == CA_NONE) &&
         p.driver_act[0].slot != p.driver_act[1].slot && p.steps[0].key_slot == p.driver_act[1].slot &&
@@ -684,7 +685,7 @@ std::string explain_program(const Program* p) {
         os << ")";
         if (rp.val_slot >= 0) os << " val v" << rp.val_slot;
         if (rp.carried) os << " [grouped by v" << rp.key_slot[0] << "]";
-        if (rp.carried_val) os << " [keyed by v" << rp.key_slot[0] << ", v" << rp.key_slot[1] << " pulled]";
+        if (rp.carried_val) os << " [keyed by v" << rp.key_slot[0] << ", v" << rp.key_slot[1] << "]";
         os << "\n";
       }
     }

@@ -131,6 +131,14 @@ hipError_t bits_keys(uint32_t* bits, int64_t nbits, u64 row_bits, int32_t lo0, i
 hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
                             uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
                             uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s);
+// Dense min/max heads, tiled rounds (see DenseTileArgs).
+hipError_t dense_delta_by_rank(uint32_t* chg, uint32_t n0, uint32_t wpr, const uint32_t* off, const uint32_t* vals,
+                               const uint32_t* dict, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                               uint32_t* v, hipStream_t s);
+size_t dense_tile_lds_bytes(uint32_t tile);
+hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
+                     uint32_t ntiles, uint32_t* key, hipStream_t s);
+hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,

@@ -1632,6 +1632,197 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
   return hipGetLastError();
 }
 
+// ============================================================ dense min/max heads, tiled rounds
+// Delta rows of a dense min/max head from its delta bits, one workgroup per
+// rank row (rank-major slot order, so rows come out grouped by rank and
+// ascending in the second key), clearing the bits.  off[r] is the first row
+// of rank r (scan of the per-rank bit counts).
+__global__ __launch_bounds__(256) void dense_delta_by_rank_k(uint32_t* chg, uint32_t n0, uint32_t wpr,
+                                                             const uint32_t* off, const uint32_t* vals,
+                                                             const uint32_t* dict, int32_t lo1, int type,
+                                                             int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v) {
+  __shared__ uint32_t stage[256 * 32];
+  for (uint32_t r = blockIdx.x; r < n0; r += gridDim.x) {
+    uint32_t p = off[r];
+    const uint32_t s = dict[r];
+    uint32_t* row = chg + (u64)r * wpr;
+    for (uint32_t cb = 0; cb < wpr; cb += 256) {
+      const uint32_t wi = cb + threadIdx.x;
+      const uint32_t d = wi < wpr ? row[wi] : 0u;
+      uint32_t tot;
+      uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
+      if (d) {
+        row[wi] = 0u;
+        for (uint32_t b = d; b; b &= b - 1) stage[q++] = wi * 32u + (uint32_t)(__ffs(b) - 1);
+      }
+      __syncthreads();
+      for (uint32_t i = threadIdx.x; i < tot; i += 256) {
+        const uint32_t yb = stage[i];
+        k0[p + i] = s;
+        k1[p + i] = (uint32_t)lo1 + yb;
+        v[p + i] = stored_value(vals[(u64)r * wpr * 32u + yb], type, fold_kind);
+      }
+      p += tot;
+      __syncthreads();
+    }
+  }
+}
+hipError_t dense_delta_by_rank(uint32_t* chg, uint32_t n0, uint32_t wpr, const uint32_t* off, const uint32_t* vals,
+                               const uint32_t* dict, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                               uint32_t* v, hipStream_t s) {
+  if (n0 == 0) return hipSuccess;
+  dense_delta_by_rank_k<<<std::min<uint32_t>(n0, 65536), 256, 0, s>>>(chg, n0, wpr, off, vals, dict, lo1, type,
+                                                                      fold_kind, k0, k1, v);
+  return hipGetLastError();
+}
+
+typedef XL_KARG const DenseTileArgs TileArgs;
+constexpr int DT_THREADS = 1024, DT_WAVES = DT_THREADS / 64;
+
+__global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_value) {
+  (void)by_value;
+  TileArgs& a = *(TileArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  extern __shared__ uint32_t lds[];
+  uint32_t* tv = lds;                    // tile values
+  uint32_t* tchg = lds + a.tile;         // improved in this round
+  uint32_t* tpres = tchg + a.tile / 32;  // presence before the round
+  __shared__ uint32_t s_excl[DT_WAVES][64], s_beg[DT_WAVES][64], s_z[DT_WAVES][64], s_d[DT_WAVES][64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t* ycol = a.idx.col[a.ycol];
+  u64 cands = 0;
+  uint32_t ins = 0, imp = 0;
+  const uint32_t nwork = a.n0 * a.ntiles;
+  for (uint32_t b = blockIdx.x; b < nwork; b += gridDim.x) {
+    const uint32_t r = b / a.ntiles, t = b % a.ntiles;
+    const uint32_t y0 = t * a.tile;
+    const uint32_t tw = min(a.tile, a.range1 - y0);
+    const u64 base = (u64)r * a.range1 + y0;  // first slot (a multiple of 32)
+    for (uint32_t i = threadIdx.x; i < tw; i += DT_THREADS) tv[i] = a.vals[base + i];
+    for (uint32_t i = threadIdx.x; i < tw / 32; i += DT_THREADS) {
+      tchg[i] = 0u;
+      tpres[i] = a.pres[base / 32 + i];
+    }
+    __syncthreads();
+    const uint32_t s = a.dict[r];
+    const uint32_t rb = a.roff[r], re = a.roff[r + 1];
+    for (uint32_t r0 = rb + (uint32_t)w * 64; r0 < re; r0 += DT_WAVES * 64) {
+      const uint32_t j = r0 + (uint32_t)lane;
+      uint32_t beg = 0, deg = 0, z = 0, d1 = 0;
+      if (j < re) {
+        z = a.dk1[j];
+        d1 = a.dval[j];
+        const uint32_t kk = z - (uint32_t)a.idx.key_lo;
+        if (kk < a.idx.key_range) {  // only the rows of z whose Y is in this tile
+          const u64 o = (u64)kk * (a.ntiles + 1) + t;
+          beg = a.toff[o];
+          deg = a.toff[o + 1] - beg;
+        }
+      }
+      const uint32_t incl = wave_incl_scan(deg);
+      const uint32_t total = __shfl(incl, 63, 64);
+      s_excl[w][lane] = incl - deg;
+      s_beg[w][lane] = beg;
+      s_z[w][lane] = z;
+      s_d[w][lane] = d1;
+      wave_lds_sync();
+      for (uint32_t k0 = 0; k0 < total; k0 += 64) {
+        const uint32_t jj = k0 + (uint32_t)lane;
+        if (jj < total) {
+          int q = 0;
+#pragma unroll
+          for (int step = 32; step > 0; step >>= 1)
+            if (s_excl[w][q + step] <= jj) q += step;
+          const uint32_t erow = s_beg[w][q] + (jj - s_excl[w][q]);
+          const uint32_t y = ycol[erow];
+          const uint32_t yl = y - (uint32_t)a.lo1 - y0;
+          if (yl < tw) {  // the tiled index only lists rows of this tile
+            ++cands;
+            Regs u = (Regs)(0u);
+            setv(u, a.slot_s, s);
+            setv(u, a.slot_z, s_z[w][q]);
+            if (a.slot_p >= 0) setv(u, a.slot_p, s_d[w][q]);
+            setv(u, a.slot_y, y);
+            if (bind_cols(a.idx, erow, u) && run_ops(a, u)) {
+              const uint32_t enc = fold_encode(getv(u, a.val_slot), a.val_type, a.is_max);
+              const uint32_t bit = 1u << (yl & 31);
+              if (enc < tv[yl]) {
+                if (enc < atomicMin(&tv[yl], enc) && !(tchg[yl >> 5] & bit)) atomicOr(&tchg[yl >> 5], bit);
+              } else if (enc == 0xffffffffu && !(tpres[yl >> 5] & bit) && !(tchg[yl >> 5] & bit)) {
+                atomicOr(&tchg[yl >> 5], bit);  // a first value equal to the empty encoding
+              }
+            }
+          }
+        }
+      }
+      wave_lds_sync();
+    }
+    __syncthreads();
+    // write back the improved slots; new keys get their presence bit
+    for (uint32_t i = threadIdx.x; i < tw; i += DT_THREADS)
+      if ((tchg[i >> 5] >> (i & 31)) & 1u) a.vals[base + i] = tv[i];
+    for (uint32_t i = threadIdx.x; i < tw / 32; i += DT_THREADS) {
+      const uint32_t c = tchg[i];
+      if (!c) continue;
+      a.chg[base / 32 + i] = c;  // the delta bits were cleared when this round's rows were made
+      const uint32_t fresh = c & ~tpres[i];
+      if (fresh) a.pres[base / 32 + i] = tpres[i] | fresh;
+      ins += (uint32_t)__popc(fresh);
+      imp += (uint32_t)__popc(c);
+    }
+    __syncthreads();
+  }
+  // one atomic per workgroup for each count
+  __shared__ u64 s_c[DT_WAVES], s_i[DT_WAVES], s_m[DT_WAVES];
+  u64 ci = ins, cm = imp;
+  for (int k = 32; k > 0; k >>= 1) {
+    cands += __shfl_xor(cands, k, 64);
+    ci += __shfl_xor(ci, k, 64);
+    cm += __shfl_xor(cm, k, 64);
+  }
+  if (lane == 0) {
+    s_c[w] = cands;
+    s_i[w] = ci;
+    s_m[w] = cm;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 tc = 0, ti = 0, tm = 0;
+    for (int i = 0; i < DT_WAVES; ++i) {
+      tc += s_c[i];
+      ti += s_i[i];
+      tm += s_m[i];
+    }
+    if (tc) atomicAdd(&a.counters[CNT_CANDIDATES], tc);
+    if (ti) atomicAdd(&a.counters[CNT_INSERTED], ti);
+    if (tm) atomicAdd(&a.counters[CNT_APPENDED], tm);
+  }
+}
+
+// Composite sort key of e's rows for the tiled index: (z - zlo) * (ntiles + 1)
+// + the tile of y (ntiles for a y outside the head's second-key slots).
+__global__ void tile_keys_k(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1,
+                            uint32_t tile, uint32_t ntiles, uint32_t* key) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t tt = min((yc[i] - (uint32_t)lo1) / tile, ntiles);
+    key[i] = (zc[i] - (uint32_t)zlo) * (ntiles + 1) + tt;
+  }
+}
+hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
+                     uint32_t ntiles, uint32_t* key, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  tile_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(zc, yc, n, zlo, lo1, tile, ntiles, key);
+  return hipGetLastError();
+}
+
+size_t dense_tile_lds_bytes(uint32_t tile) { return ((size_t)tile + 2 * (size_t)(tile / 32)) * 4; }
+
+hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s) {
+  const uint32_t nwork = a.n0 * a.ntiles;
+  if (nwork == 0) return hipSuccess;
+  dense_min_tile_k<<<std::min<uint32_t>(nwork, 65536), DT_THREADS, dense_tile_lds_bytes(a.tile), s>>>(a);
+  return hipGetLastError();
+}
+
 // ============================================================ segmented aggregation
 template <typename K>
 __global__ void seg_heads_k(const K* keys, int64_t n, uint32_t* flag) {

@@ -148,6 +148,22 @@ def test_sum_and_logsumexp_heads_dense_and_hashed(name, index_mode):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+@pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
+def test_min_rounds_tiled_and_untiled(tiles):
+    """Carried min rule over a dense head: one workgroup per (source, tile of
+    targets) with the tile in LDS (1 tile, 7 uneven tiles, the automatic
+    choice) or the untiled emission (-1); all match the oracle bit for bit
+    and give the same per-round delta sizes."""
+    wl = W.small_workloads()["sssp"]()
+    print(f"case: min tiles={tiles}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"dense_tiles": tiles})
+    assert_same_relation("dist", wl.idb["dist"], rels["dist"], ref.relations["dist"][1], tol=(0.0, 0.0))
+    base, _, _ = engine_run(wl, options={"dense_tiles": -1})
+    if tiles != -1:
+        assert stats["delta_rows"] == engine_run(wl, options={"dense_tiles": -1})[1]["delta_rows"]
+
+
 SELF_JOIN_TC = """
 path(X,Y) :- edge(X,Y).
 path(X,Y) :- path(X,Z), path(Z,Y).
