@@ -163,6 +163,7 @@ struct DensePullArgs {
   int32_t zcol;
   int8_t slot_s, slot_z, slot_y, slot_p, val_slot;
   uint8_t val_type;
+  int8_t fast, fcol;      // as in DenseTileArgs
   int32_t fold_kind;
   int32_t nops;
   MicroOp ops[MAXOPS];
@@ -199,6 +200,9 @@ struct DenseTileArgs {
   int32_t ycol;           // column of e bound to Y
   int8_t slot_s, slot_z, slot_p, slot_y, val_slot;
   uint8_t val_type, is_max;
+  // 1 / 2: the rule is "value is P1 + / - e.col[fcol]" with nothing else to
+  // check, evaluated directly instead of through the micro-op list
+  int8_t fast, fcol;
   int32_t nops;
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];

@@ -1076,6 +1076,29 @@ struct Runner {
     return nullptr;
   }
 
+  // "value is P1 + W" / "P1 - W" with W bound by one column of e and nothing
+  // else to check: returns 1 / 2 and the column, else 0.
+  int affine_value(const RulePlan& p, int* col) const {
+    const StepPlan& sp = p.steps[0];
+    const auto& ops = p.stage_ops[0];
+    if (p.cv_slot_p < 0 || ops.size() != 2) return 0;
+    const MicroOp& m = ops[0];
+    const MicroOp& o = ops[1];
+    if (m.kind != OP_MOV || m.dst != p.val_slot || m.a != p.cv_slot_p || m.type != p.val_type) return 0;
+    if ((o.kind != OP_ADD && o.kind != OP_SUB) || o.dst != p.val_slot || o.a != p.val_slot || o.b < 0 ||
+        o.type != p.val_type)
+      return 0;
+    int wc = -1;
+    for (int j = 0; j < sp.rel->arity; ++j) {
+      const ColAct& ac = sp.act[j];
+      if (ac.kind == CA_CHECK_SLOT || ac.kind == CA_CHECK_CONST) return 0;
+      if (ac.kind == CA_BIND && ac.slot == o.b) wc = j;
+    }
+    if (wc < 0 || wc == sp.key_col || sp.rel->types[wc] != p.val_type) return 0;
+    *col = wc;
+    return o.kind == OP_ADD ? 1 : 2;
+  }
+
   // One round of the carried-value variant over a dense sum/logsumexp head:
   // mark every key that receives a contribution (the stage kernel over the
   // delta rows), list the marked slots in order, then fold each key's
@@ -1145,6 +1168,9 @@ struct Runner {
     q.val_slot = (int8_t)p.val_slot;
     q.val_type = p.val_type;
     q.fold_kind = h->fold;
+    int fcol = 0;
+    q.fast = (int8_t)affine_value(p, &fcol);
+    q.fcol = (int8_t)fcol;
     q.nops = (int32_t)p.stage_ops[0].size();
     for (int i = 0; i < q.nops; ++i) q.ops[i] = p.stage_ops[0][i];
     for (size_t i = 0; i < p.stage_consts[0].size(); ++i) q.consts[i] = p.stage_consts[0][i];
@@ -1252,6 +1278,9 @@ struct Runner {
     a.val_slot = (int8_t)p.val_slot;
     a.val_type = p.val_type;
     a.is_max = h->agg == Agg::MAX;
+    int fcol = 0;
+    a.fast = (int8_t)affine_value(p, &fcol);
+    a.fcol = (int8_t)fcol;
     a.nops = (int32_t)p.stage_ops[0].size();
     for (int i = 0; i < a.nops; ++i) a.ops[i] = p.stage_ops[0][i];
     for (size_t i = 0; i < p.stage_consts[0].size(); ++i) a.consts[i] = p.stage_consts[0][i];

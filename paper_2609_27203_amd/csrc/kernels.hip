@@ -1305,6 +1305,16 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
   return hipGetLastError();
 }
 
+// "value is P1 + / - W" of a carried-value rule: one correctly rounded
+// binary32 operation (or int32 wrap-around), as the micro-op list would do.
+__device__ __forceinline__ uint32_t fast_value(int fast, int type, uint32_t p1, uint32_t w) {
+  if (type == T_F32) {
+    const float x = __uint_as_float(p1), y = __uint_as_float(w);
+    return __float_as_uint(fast == 1 ? __fadd_rn(x, y) : __fsub_rn(x, y));
+  }
+  return fast == 1 ? p1 + w : p1 - w;
+}
+
 // ============================================================ dense sum / logsumexp heads
 // Marked slots -> ascending slot list, clearing the marks.  Each workgroup
 // owns MK_WORDS consecutive bitmap words: count pass, scan of the per-group
@@ -1448,6 +1458,10 @@ __device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, u
   if (zb >= a.range1) return false;
   const uint32_t zs = r * a.range1 + zb;
   if (!((a.cpres[zs >> 5] >> (zs & 31)) & 1u)) return false;
+  if (a.fast) {
+    setv(u, a.val_slot, fast_value(a.fast, a.val_type, a.cval[zs], a.rev.col[a.fcol][e_row]));
+    return true;
+  }
   u = (Regs)(0u);
   setv(u, a.slot_s, s);
   setv(u, a.slot_z, z);
@@ -1737,13 +1751,22 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
           const uint32_t yl = y - (uint32_t)a.lo1 - y0;
           if (yl < tw) {  // the tiled index only lists rows of this tile
             ++cands;
-            Regs u = (Regs)(0u);
-            setv(u, a.slot_s, s);
-            setv(u, a.slot_z, s_z[w][q]);
-            if (a.slot_p >= 0) setv(u, a.slot_p, s_d[w][q]);
-            setv(u, a.slot_y, y);
-            if (bind_cols(a.idx, erow, u) && run_ops(a, u)) {
-              const uint32_t enc = fold_encode(getv(u, a.val_slot), a.val_type, a.is_max);
+            bool ok;
+            uint32_t val;
+            if (a.fast) {
+              val = fast_value(a.fast, a.val_type, s_d[w][q], a.idx.col[a.fcol][erow]);
+              ok = true;
+            } else {
+              Regs u = (Regs)(0u);
+              setv(u, a.slot_s, s);
+              setv(u, a.slot_z, s_z[w][q]);
+              if (a.slot_p >= 0) setv(u, a.slot_p, s_d[w][q]);
+              setv(u, a.slot_y, y);
+              ok = bind_cols(a.idx, erow, u) && run_ops(a, u);
+              val = getv(u, a.val_slot);
+            }
+            if (ok) {
+              const uint32_t enc = fold_encode(val, a.val_type, a.is_max);
               const uint32_t bit = 1u << (yl & 31);
               if (enc < tv[yl]) {
                 if (enc < atomicMin(&tv[yl], enc) && !(tchg[yl >> 5] & bit)) atomicOr(&tchg[yl >> 5], bit);
