@@ -787,6 +787,16 @@ hipError_t dense_delta_rows(const uint32_t* idx, int64_t n, const uint32_t* vals
   return hipGetLastError();
 }
 
+// "value is P1 + / - W" of a carried-value rule: one correctly rounded
+// binary32 operation (or int32 wrap-around), as the micro-op list would do.
+__device__ __forceinline__ uint32_t fast_value(int fast, int type, uint32_t p1, uint32_t w) {
+  if (type == T_F32) {
+    const float x = __uint_as_float(p1), y = __uint_as_float(w);
+    return __float_as_uint(fast == 1 ? __fadd_rn(x, y) : __fsub_rn(x, y));
+  }
+  return fast == 1 ? p1 + w : p1 - w;
+}
+
 // ============================================================ stage kernel
 // One launch evaluates one join step of a rule plan for a batch of source
 // rows: bind the source row's columns, expand it through an index (all rows
@@ -899,6 +909,20 @@ __device__ __forceinline__ bool run_ops(A& a, Regs& u) {
     }
   }
   return ok;
+}
+
+// Micro-op evaluation, specialized at launch: OPS 0 = no ops, 2 = the
+// affine pattern "v is x + / - y" (a move then an add or subtract of two
+// slots), 1 = the general interpreter.
+template <int OPS>
+__device__ __forceinline__ bool eval_ops(KernArgs& a, Regs& u) {
+  if (OPS == 0) return true;
+  if (OPS == 2) {
+    setv(u, a.ops[0].dst, fast_value(a.ops[1].kind == OP_ADD ? 1 : 2, a.ops[1].type, getv(u, a.ops[0].a),
+                                     getv(u, a.ops[1].b)));
+    return true;
+  }
+  return run_ops(a, u);
 }
 
 // Rows produced by EM_SET / EM_BITSET / EM_MINMAX are staged in a per-wave
@@ -1180,7 +1204,7 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
 constexpr int ST_THREADS = 256;
 constexpr int ST_WAVES = ST_THREADS / 64;
 
-template <int MODE, bool HAS_INDEX>
+template <int MODE, bool HAS_INDEX, int OPS>
 __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   (void)by_value;
   KernArgs& a = *(KernArgs*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -1243,13 +1267,13 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
           const uint32_t erow = s_beg[w][r] + (j - s_excl[w][r]);
           act = bind_cols(a.idx, erow, u);
         }
-        if (act) act = run_ops(a, u);
+        if (act) act = eval_ops<OPS>(a, u);
         emit<MODE>(a, u, act, st);
       }
       wave_lds_sync();
     } else {
       bool act = ok;
-      if (act) act = run_ops(a, v);
+      if (act) act = eval_ops<OPS>(a, v);
       emit<MODE>(a, v, act, st);
     }
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
@@ -1282,10 +1306,29 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   if (STAGED) flush_rows<MODE>(a, st);  // rows already inserted are always written
 }
 
+static int ops_kind(const StageArgs& a) {
+  if (a.nops == 0) return 0;
+  const MicroOp& m = a.ops[0];
+  const MicroOp& o = a.ops[1];
+  if (a.nops == 2 && m.kind == OP_MOV && m.a >= 0 && (o.kind == OP_ADD || o.kind == OP_SUB) && o.dst == m.dst &&
+      o.a == m.dst && o.b >= 0 && o.type == m.type)
+    return 2;
+  return 1;
+}
+
+template <int MODE, int OPS>
+static void launch_ops(const StageArgs& a, unsigned grid, hipStream_t s) {
+  if (a.has_index) stage_k<MODE, true, OPS><<<grid, ST_THREADS, 0, s>>>(a);
+  else stage_k<MODE, false, OPS><<<grid, ST_THREADS, 0, s>>>(a);
+}
+
 template <int MODE>
 static void launch_mode(const StageArgs& a, unsigned grid, hipStream_t s) {
-  if (a.has_index) stage_k<MODE, true><<<grid, ST_THREADS, 0, s>>>(a);
-  else stage_k<MODE, false><<<grid, ST_THREADS, 0, s>>>(a);
+  switch (ops_kind(a)) {
+    case 0: launch_ops<MODE, 0>(a, grid, s); break;
+    case 2: launch_ops<MODE, 2>(a, grid, s); break;
+    default: launch_ops<MODE, 1>(a, grid, s); break;
+  }
 }
 
 hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
@@ -1303,16 +1346,6 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
     default: launch_mode<EM_MINMAX>(a, grid, s); break;
   }
   return hipGetLastError();
-}
-
-// "value is P1 + / - W" of a carried-value rule: one correctly rounded
-// binary32 operation (or int32 wrap-around), as the micro-op list would do.
-__device__ __forceinline__ uint32_t fast_value(int fast, int type, uint32_t p1, uint32_t w) {
-  if (type == T_F32) {
-    const float x = __uint_as_float(p1), y = __uint_as_float(w);
-    return __float_as_uint(fast == 1 ? __fadd_rn(x, y) : __fsub_rn(x, y));
-  }
-  return fast == 1 ? p1 + w : p1 - w;
 }
 
 // ============================================================ dense sum / logsumexp heads
