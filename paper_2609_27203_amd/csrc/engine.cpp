@@ -1619,14 +1619,21 @@ struct Runner {
       HIP_TRY(c, k::row_popcount(h->dchg.as<uint32_t>(), h->n0, wpr, cnt.as<uint32_t>(), c->stream));
       HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), h->roff.as<uint32_t>(), h->n0,
                                        h->roff.as<uint32_t>() + h->n0, tmp.p, c->stream));
+      const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+      Buf ltmp, tot;
+      XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &ltmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      auto rows = [&](bool write) {
+        return k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
+                                   h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
+                                   h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
+                                   tot.as<uint32_t>(), ltmp.p, write, c->stream);
+      };
+      HIP_TRY(c, rows(false));
       uint32_t n = 0;
-      XL_TRY(ctl_read(c, h->roff.as<uint32_t>() + h->n0, 4, &n));
+      XL_TRY(ctl_read(c, tot.p, 4, &n));
       XL_TRY(ensure_drow(h, n));
-      if (n)
-        HIP_TRY(c, k::dense_delta_by_rank(h->dchg.as<uint32_t>(), (uint32_t)h->n0, wpr, h->roff.as<uint32_t>(),
-                                          h->dvals.as<uint32_t>(), h->dict.as<uint32_t>(), h->kp.lo[1],
-                                          h->rel->types[h->nkey], h->fold, h->drow[0].as<uint32_t>(),
-                                          h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(), c->stream));
+      if (n) HIP_TRY(c, rows(true));
       h->dn = n;
       *delta = n;
       return XL_OK;

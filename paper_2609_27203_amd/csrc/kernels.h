@@ -132,9 +132,12 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
                             uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
                             uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s);
 // Dense min/max heads, tiled rounds (see DenseTileArgs).
-hipError_t dense_delta_by_rank(uint32_t* chg, uint32_t n0, uint32_t wpr, const uint32_t* off, const uint32_t* vals,
-                               const uint32_t* dict, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
-                               uint32_t* v, hipStream_t s);
+// Delta rows from the delta bits in slot order (two calls on the same temp,
+// sized by bits_list_temp_bytes: write=false counts, write=true writes the
+// rows and clears the bits).
+hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1, const uint32_t* vals, const uint32_t* dict,
+                            int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
+                            uint32_t* total, void* temp, bool write, hipStream_t s);
 size_t dense_tile_lds_bytes(uint32_t tile);
 hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
                      uint32_t ntiles, uint32_t* key, hipStream_t s);

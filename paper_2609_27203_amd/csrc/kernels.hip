@@ -1680,46 +1680,53 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
 }
 
 // ============================================================ dense min/max heads, tiled rounds
-// Delta rows of a dense min/max head from its delta bits, one workgroup per
-// rank row (rank-major slot order, so rows come out grouped by rank and
-// ascending in the second key), clearing the bits.  off[r] is the first row
-// of rank r (scan of the per-rank bit counts).
-__global__ __launch_bounds__(256) void dense_delta_by_rank_k(uint32_t* chg, uint32_t n0, uint32_t wpr,
-                                                             const uint32_t* off, const uint32_t* vals,
-                                                             const uint32_t* dict, int32_t lo1, int type,
-                                                             int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v) {
-  __shared__ uint32_t stage[256 * 32];
-  for (uint32_t r = blockIdx.x; r < n0; r += gridDim.x) {
-    uint32_t p = off[r];
-    const uint32_t s = dict[r];
-    uint32_t* row = chg + (u64)r * wpr;
-    for (uint32_t cb = 0; cb < wpr; cb += 256) {
-      const uint32_t wi = cb + threadIdx.x;
-      const uint32_t d = wi < wpr ? row[wi] : 0u;
-      uint32_t tot;
-      uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
-      if (d) {
-        row[wi] = 0u;
-        for (uint32_t b = d; b; b &= b - 1) stage[q++] = wi * 32u + (uint32_t)(__ffs(b) - 1);
-      }
-      __syncthreads();
-      for (uint32_t i = threadIdx.x; i < tot; i += 256) {
-        const uint32_t yb = stage[i];
-        k0[p + i] = s;
-        k1[p + i] = (uint32_t)lo1 + yb;
-        v[p + i] = stored_value(vals[(u64)r * wpr * 32u + yb], type, fold_kind);
-      }
-      p += tot;
-      __syncthreads();
+// Delta rows of a dense min/max head from its delta bits, in slot order
+// (rank-major, so grouped by rank and ascending in the second key), clearing
+// the bits.  Same word ranges and count pass as bits_keys; the write pass
+// stages each step's set bits in LDS so the row writes are coalesced.
+__global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, int64_t nw, const uint32_t* off,
+                                                                 uint32_t range1, const uint32_t* vals,
+                                                                 const uint32_t* dict, int32_t lo1, int type,
+                                                                 int fold_kind, uint32_t* k0, uint32_t* k1,
+                                                                 uint32_t* v) {
+  __shared__ uint32_t stage[MK_THREADS * 32];
+  uint32_t p = off[blockIdx.x];
+  const u64 base = (u64)blockIdx.x * MK_WORDS * 32u;
+  for (int k = 0; k < MK_WPT; ++k) {
+    const int64_t wi = (int64_t)blockIdx.x * MK_WORDS + (int64_t)k * MK_THREADS + threadIdx.x;
+    const uint32_t d = wi < nw ? chg[wi] : 0u;
+    uint32_t tot;
+    uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
+    if (d) {
+      chg[wi] = 0u;
+      for (uint32_t b = d; b; b &= b - 1)
+        stage[q++] = (uint32_t)(k * MK_THREADS + threadIdx.x) * 32u + (uint32_t)(__ffs(b) - 1);
     }
+    __syncthreads();
+    for (uint32_t r = threadIdx.x; r < tot; r += MK_THREADS) {
+      const u64 slot = base + stage[r];
+      k0[p + r] = dict[slot / range1];
+      k1[p + r] = (uint32_t)lo1 + (uint32_t)(slot % range1);
+      v[p + r] = stored_value(vals[slot], type, fold_kind);
+    }
+    p += tot;
+    __syncthreads();
   }
 }
-hipError_t dense_delta_by_rank(uint32_t* chg, uint32_t n0, uint32_t wpr, const uint32_t* off, const uint32_t* vals,
-                               const uint32_t* dict, int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
-                               uint32_t* v, hipStream_t s) {
-  if (n0 == 0) return hipSuccess;
-  dense_delta_by_rank_k<<<std::min<uint32_t>(n0, 65536), 256, 0, s>>>(chg, n0, wpr, off, vals, dict, lo1, type,
-                                                                      fold_kind, k0, k1, v);
+hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1, const uint32_t* vals, const uint32_t* dict,
+                            int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
+                            uint32_t* total, void* temp, bool write, hipStream_t s) {
+  const int64_t nw = (nslots + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
+  uint32_t* cnt = (uint32_t*)temp;
+  uint32_t* off = cnt + ((nb + 63) & ~63ll);
+  char* stemp = (char*)(off + ((nb + 63) & ~63ll));
+  if (!write) {
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, cnt);
+    return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
+  }
+  dense_delta_bits_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, off, range1, vals, dict, lo1, type, fold_kind, k0,
+                                                         k1, v);
   return hipGetLastError();
 }
 
