@@ -37,7 +37,7 @@ DESCRIPTIONS = {
 
 KERNELS = {
     "front": "frontier_round_k (delta expand or in-edge pull + membership test + merge, one first key per workgroup)",
-    "emit": "stage_k (fused delta expand + probe + insert)",
+    "emit": "stage_k / dense_min_tile_k (fused delta expand + probe + fold into the head)",
 }
 
 
