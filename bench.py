@@ -36,31 +36,44 @@ DESCRIPTIONS = {
 
 
 KERNELS = {
-    "front": "frontier_round_k (delta expand or in-edge pull + membership test + merge, one first key per workgroup)",
+    "front": "frontier_resident_k (every round of a first key in one workgroup, its row in LDS: delta "
+             "expand or in-edge pull + membership test + merge)",
     "emit": "stage_k / dense_min_tile_k (fused delta expand + probe + fold into the head)",
+    "pull": "dense_pull_k (segmented fold of each marked key's in-edges against the delta)",
+}
+
+# Algorithmic bytes per unit of work (candidates, new tuples), counting only
+# what the join/dedup/merge must move:
+#   set heads: per candidate (a head tuple produced, or an edge examined) the
+#     matched edge's endpoint (4 B) and one membership probe of the packed key
+#     (8 B); per new tuple the key written to the full relation (8 B), the
+#     delta row written (8 B) and read again by the next round (8 B);
+#   value heads (min / logsumexp): per candidate the edge's endpoint and
+#     weight (8 B) and a key + value probe (12 B); per new or improved key
+#     24 B as above.
+BYTES_PER_UNIT = {
+    "tc_uniform": (12.0, 24.0),
+    "tc_rmat_count": (12.0, 24.0),
+    "same_generation": (12.0, 24.0),
+    "sssp": (20.0, 24.0),
+    "lse_dag": (20.0, 24.0),
 }
 
 
-def _algorithmic_bytes(candidates: float, new: float) -> float:
-    """Bytes the join/dedup/merge work must move, by its definition.
-
-    Per candidate (a head tuple produced, or an edge examined): the matched
-    edge's endpoint (4 B) and one membership probe of the packed key (8 B).
-    Per new tuple: the key written to the full relation (8 B), the delta row
-    written (8 B) and read again by the next round (8 B).
-    """
-    return 12.0 * candidates + 24.0 * new
+def _algorithmic_bytes(workload: str, candidates: float, new: float) -> float:
+    per_cand, per_new = BYTES_PER_UNIT[workload]
+    return per_cand * candidates + per_new * new
 
 
-def dominant_kernel(stats: list) -> dict:
-    """The join kernel family with the larger event-timed share: frontier
-    rounds (closure-shaped strata) or the generic fused stage kernel."""
-    front = sum(s["front_ms"] for s in stats)
-    emit = sum(s["emit_ms"] for s in stats)
-    k = "front" if front >= emit else "emit"
-    return {"family": k, "ms": front if k == "front" else emit,
+def dominant_kernel(stats: list, workload: str) -> dict:
+    """The join kernel family with the largest event-timed share: frontier
+    rounds (closure-shaped strata), the generic fused stage kernel, or the
+    segmented pull fold (sum / logsumexp over dense heads)."""
+    ms = {k: sum(s[k + "_ms"] for s in stats) for k in KERNELS}
+    k = max(ms, key=lambda f: ms[f])
+    return {"family": k, "ms": ms[k],
             "launches": sum(s[k + "_launches"] for s in stats),
-            "bytes": sum(_algorithmic_bytes(s[k + "_candidates"], s[k + "_new"]) for s in stats)}
+            "bytes": sum(_algorithmic_bytes(workload, s[k + "_candidates"], s[k + "_new"]) for s in stats)}
 
 
 FRONTIER_SOURCES = ("frontier.hip", "device_util.h", "device_types.h")
@@ -80,7 +93,7 @@ def recorded_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from the committed counter
     record, or None when the kernel's sources changed since it was measured."""
     root = os.path.dirname(os.path.abspath(__file__))
-    rec = os.path.join(root, "profiles", "frontier_round_rmat_traffic.json")
+    rec = os.path.join(root, "profiles", "frontier_resident_rmat_traffic.json")
     if workload != "tc_rmat_count" or not os.path.exists(rec):
         return None
     r = json.load(open(rec))
@@ -174,7 +187,7 @@ def main():
     ms_per_step = 1e3 * dt / args.steps
     derived = stats[-1]["derived_tuples"]
 
-    dk = dominant_kernel(stats)
+    dk = dominant_kernel(stats, args.workload)
     achieved = dk["bytes"] / (dk["ms"] * 1e-3) / 1e9 if dk["ms"] > 0 else 0.0
     traffic = recorded_traffic(args.workload) if dk["family"] == "front" else None
     roofline = {

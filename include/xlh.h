@@ -115,13 +115,22 @@ typedef struct {
     int64_t front_candidates;   /* edges examined: produced tuples when pushing,
                                    in-edges scanned when pulling */
     int64_t front_new;          /* tuples added */
+    /* Segmented folds of carried sum / logsumexp rules over dense heads (each
+     * marked key scans all its in-edges against the delta), timed the same
+     * way. */
+    double pull_ms;
+    int64_t pull_launches;
+    int64_t pull_candidates;    /* in-edges scanned */
+    int64_t pull_new;           /* keys whose value was added or changed */
 } xl_fixpoint_stats;
 
 /*
  * Create a context on HIP device `device` that enqueues all work on
  * `hip_stream` (a hipStream_t, may be NULL for the null stream) and
  * sub-allocates from `workspace` (device memory of `workspace_bytes` bytes,
- * owned by the caller; it and the stream must outlive the context).
+ * owned by the caller; it and the stream must outlive the context; the
+ * library uses it from the first 256-byte boundary on, in blocks of whole
+ * 256-byte units; at least 1 MiB, else XL_INVALID_ARGUMENT).
  * device = -1 creates a planning-only context: relations can be declared and
  * rules compiled (no device work), but loads and runs fail with
  * XL_INVALID_ARGUMENT.
@@ -140,6 +149,11 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     in-edge is expanded by pulling (scanning in-edges of the
  *                     unreached targets) when pull_ratio * d >= u; 0 = always
  *                     push (default 64)
+ *   "frontier_resident"  closure-shaped strata over dense heads: 1 = every
+ *                     pass in one launch, each source iterating its own rounds
+ *                     with its row in LDS until its delta is empty, the pass
+ *                     count and per-pass delta sizes read back once at the end
+ *                     (default); 0 = one launch and one host read per pass
  *   "dense_tiles"     rounds of a carried min/max rule over a dense head run
  *                     one workgroup per (first key, tile of second keys) with
  *                     the tile in LDS: 0 = choose the tile count (default),

@@ -74,6 +74,11 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     c->pull_ratio = (int)value;
     return XL_OK;
   }
+  if (!strcmp(key, "frontier_resident")) {
+    if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "frontier_resident must be 0 or 1");
+    c->frontier_resident = (int)value;
+    return XL_OK;
+  }
   if (!strcmp(key, "dense_tiles")) {
     if (value < -1 || value > 4096) return c->fail(XL_INVALID_ARGUMENT, "dense_tiles must be in [-1, 4096]");
     c->dense_tiles = (int)value;

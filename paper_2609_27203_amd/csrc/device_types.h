@@ -231,11 +231,26 @@ struct FrontierArgs {
   uint32_t* out_cnt;        // next delta: counts and bitmap rows, same slots
   uint32_t* out_diff;
   unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED (= new tuples)
-  // Pull direction: e indexed by the Y column; Z is rev.col[rev_zcol].  A
-  // workgroup pulls when pull_ratio * |delta(x)| >= |unreached Y with an
-  // in-edge| (pull_ratio 0: always push).
+  // Pull direction: e indexed by the Y column; Z is rev.col[rev_zcol], the
+  // rows of one Y ordered by the number of in-edges of their Z, most first;
+  // rev_first[y - rev.key_lo] is the Z of Y's first row.  A workgroup pulls
+  // when pull_ratio * |delta(x)| >= |unreached Y with an in-edge| (pull_ratio
+  // 0: always push).
   IndexProbe rev;
   int32_t rev_zcol;
+  const uint32_t* rev_first;
+  // Resident form: each workgroup takes first keys from *queue (zero at
+  // launch) and runs all of a key's rounds with its row held in LDS, writing
+  // the row back once; per round r (from 0) it adds the tuples found to
+  // round_new[min(r, round_slots - 1)], raises *max_round to the rounds it
+  // ran (the last one found nothing), and sets *overflow when a key still has
+  // a delta after max_rounds rounds.
+  uint32_t* queue;
+  uint32_t* max_round;
+  uint32_t* overflow;
+  unsigned long long* round_new;
+  uint32_t round_slots;
+  uint32_t max_rounds;
   const uint32_t* hasin;    // bit (y - lo1): y has at least one in-edge
   uint32_t pull_ratio;
 };

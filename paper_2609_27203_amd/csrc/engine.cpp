@@ -20,8 +20,11 @@ constexpr int64_t WAVE_SLACK = 512 + 64;
 
 // ================================================================== arena
 void Arena::init(char* base, size_t size) {
-  base_ = base;
-  size_ = size & ~(size_t)255;
+  // every block starts on a 256-B boundary and spans a multiple of 256 B, so
+  // kernels may read whole aligned vectors that hold a valid element
+  const size_t skip = (256 - (uintptr_t)base % 256) % 256;
+  base_ = base + skip;
+  size_ = size > skip ? (size - skip) & ~(size_t)255 : 0;
   free_.clear();
   used_.clear();
   if (size_) free_[0] = size_;
@@ -321,6 +324,8 @@ struct Interval {
 struct DevIndex {
   Relation* rel = nullptr;
   int col = 0;
+  int order_col = -1;  // >= 0: rows of one key ordered by the degree of this column's value
+  uint32_t* first = nullptr;  // with order_col: order_col value of each key's first row
   IndexProbe probe{};
   std::vector<std::unique_ptr<Buf>> owned;
 };
@@ -423,15 +428,24 @@ struct Runner {
   }
 
   // ------------------------------------------------------------ indexes
-  xl_status get_index(Relation* rel, int col, IndexProbe* out) {
+  // Index of rel by column col.  With order_col >= 0 the rows of each key are
+  // further ordered by how many rows have the order_col value as their key,
+  // most first; the frontier pull scans in-edges in that order, so that edges
+  // from well-connected sources, the likeliest to be in a delta, come first.
+  // first (when given, with order_col >= 0) receives an array holding, per
+  // key, the order_col value of the key's first row.
+  xl_status get_index(Relation* rel, int col, IndexProbe* out, int order_col = -1,
+                      const uint32_t** first = nullptr) {
     for (auto& ix : indexes)
-      if (ix->rel == rel && ix->col == col) {
+      if (ix->rel == rel && ix->col == col && ix->order_col == order_col) {
         *out = ix->probe;
+        if (first) *first = ix->first;
         return XL_OK;
       }
     auto ix = std::make_unique<DevIndex>();
     ix->rel = rel;
     ix->col = col;
+    ix->order_col = order_col;
     IndexProbe& p = ix->probe;
     p.ncols = rel->arity;
     auto own = [&](size_t bytes, const char* what, void** ptr) -> xl_status {
@@ -528,20 +542,40 @@ struct Runner {
                                    tmp.p, c->stream, &alt));
       uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
       uint32_t* sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+      void* off;
+      XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
+      HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
+      if (order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32) {
+        Buf k64, k64b;
+        XL_TRY(dalloc(c, (size_t)n * 8, &k64, "index order keys"));
+        XL_TRY(dalloc(c, (size_t)n * 8, &k64b, "index order keys"));
+        uint32_t* sp_alt = alt ? perm.as<uint32_t>() : perm2.as<uint32_t>();
+        HIP_TRY(c, k::degree_order_keys(sk, sp, rcol[order_col], klo, (uint32_t)range, (const uint32_t*)off, n,
+                                        k64.as<u64>(), c->stream));
+        int alt2 = 0;
+        HIP_TRY(c, k::radix_sort_u64(k64.as<u64>(), sp, k64b.as<u64>(), sp_alt, n,
+                                     16 + std::max(1, bitlen((uint64_t)range - 1)), tmp.p, c->stream, &alt2));
+        if (alt2) sp = sp_alt;
+      }
       for (int j = 0; j < rel->arity; ++j) {
         void* cj;
         XL_TRY(own((size_t)n * 4, "index column", &cj));
         HIP_TRY(c, k::gather_u32(rcol[j], sp, (uint32_t*)cj, n, c->stream));
         p.col[j] = (uint32_t*)cj;
       }
-      void* off;
-      XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
-      HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
+      if (order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32) {
+        void* fp;
+        XL_TRY(own((size_t)range * 4, "index first rows", &fp));
+        HIP_TRY(c, k::segment_first((const uint32_t*)off, p.col[order_col], (uint32_t)range, (uint32_t*)fp,
+                                    c->stream));
+        ix->first = (uint32_t*)fp;
+      }
       p.off = (uint32_t*)off;
       p.key_lo = klo;
       p.key_range = (uint32_t)range;
     }
     *out = p;
+    if (first) *first = ix->first;
     indexes.push_back(std::move(ix));
     return XL_OK;
   }
@@ -972,11 +1006,9 @@ struct Runner {
     return XL_OK;
   }
 
-  // One round of the closure-shaped variant in frontier form.
-  xl_status eval_frontier(const RulePlan& p, HeadRun* h) {
-    h->fnew = 0;
-    if (h->fn == 0) return XL_OK;
-    FrontierArgs f{};
+  // Kernel arguments of the closure-shaped variant in frontier form, reading
+  // the current delta rows.
+  xl_status frontier_args(const RulePlan& p, HeadRun* h, FrontierArgs& f) {
     f.x = h->fx.as<uint32_t>();
     f.in_cnt = h->fcnt[h->fcur].as<uint32_t>();
     f.in_diff = h->fdiff[h->fcur].as<uint32_t>();
@@ -991,7 +1023,8 @@ struct Runner {
     f.out_diff = h->fdiff[h->fcur ^ 1].as<uint32_t>();
     f.pull_ratio = (uint32_t)c->pull_ratio;
     if (c->pull_ratio) {
-      XL_TRY(get_index(p.steps[0].rel, p.carried_ycol, &f.rev));
+      XL_TRY(get_index(p.steps[0].rel, p.carried_ycol, &f.rev, p.steps[0].key_col, &f.rev_first));
+      if (!f.rev_first) return c->fail(XL_DEVICE_ERROR, "pull index without first rows (internal)");
       f.rev_zcol = p.steps[0].key_col;
       if (!h->hasin.p) {
         XL_TRY(dalloc(c, (size_t)h->row_words * 4, &h->hasin, "in-edge bitmap"));
@@ -1000,6 +1033,15 @@ struct Runner {
       f.hasin = h->hasin.as<uint32_t>();
     }
     f.counters = c->dcounters;
+    return XL_OK;
+  }
+
+  // One round of the closure-shaped variant in frontier form.
+  xl_status eval_frontier(const RulePlan& p, HeadRun* h) {
+    h->fnew = 0;
+    if (h->fn == 0) return XL_OK;
+    FrontierArgs f{};
+    XL_TRY(frontier_args(p, h, f));
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
     HIP_TRY(c, k::frontier_round(f, c->stream));
@@ -1017,6 +1059,68 @@ struct Runner {
     }
     h->fnew = (int64_t)cnt[CNT_APPENDED];
     h->keys += h->fnew;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
+  // Every pass of a frontier stratum in one launch (resident form): each
+  // first key runs its own rounds until its delta is empty.  The pass count
+  // and per-pass delta sizes match the round-by-round loop, since a key's
+  // rounds never read another key's rows: the i-th pass's delta is the union
+  // of every key's i-th round.
+  bool resident_frontier(const Stratum& s) {
+    return c->frontier_resident && heads.size() == 1 && heads[0]->frontier && heads[0]->frontier_ready &&
+           s.variants.size() == 1 && s.variants[0].driver_delta && head_of(s.variants[0].head) == heads[0].get();
+  }
+
+  xl_status run_frontier_resident(const RulePlan& p, HeadRun* h, int64_t max_iterations) {
+    if (h->fn == 0) return XL_OK;
+    FrontierArgs f{};
+    XL_TRY(frontier_args(p, h, f));
+    constexpr size_t HDR = 16;
+    Buf rs;
+    XL_TRY(dalloc(c, HDR + 8 * XL_STATS_ROUNDS, &rs, "round counters"));
+    HIP_TRY(c, hipMemsetAsync(rs.p, 0, HDR + 8 * XL_STATS_ROUNDS, c->stream));
+    f.queue = rs.as<uint32_t>();
+    f.max_round = rs.as<uint32_t>() + 1;
+    f.overflow = rs.as<uint32_t>() + 2;
+    f.round_new = (unsigned long long*)((char*)rs.p + HDR);
+    f.round_slots = XL_STATS_ROUNDS;
+    f.max_rounds = (uint32_t)std::min<int64_t>(max_iterations, 0xffffffffll);
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+    HIP_TRY(c, k::frontier_resident(f, 0, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    uint32_t hdr[4];
+    XL_TRY(ctl_read(c, rs.p, HDR, hdr));
+    const uint32_t rounds = hdr[1];
+    std::vector<u64> per((size_t)XL_STATS_ROUNDS, 0);
+    if (rounds) XL_TRY(ctl_read(c, f.round_new, 8 * std::min<size_t>(rounds, XL_STATS_ROUNDS), per.data()));
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->front_ms += ms;
+      st->front_launches++;
+      st->front_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->front_new += (int64_t)cnt[CNT_APPENDED];
+    }
+    // one recorded round per pass (the last counter slot sums the passes from
+    // there on, which the receipt does not list anyway)
+    for (uint32_t r = 0; r < rounds; ++r) {
+      st->iterations++;
+      record(r < (uint32_t)XL_STATS_ROUNDS ? (int64_t)per[r] : 0);
+    }
+    st->new_tuples_total += (int64_t)cnt[CNT_APPENDED];
+    h->keys += (int64_t)cnt[CNT_APPENDED];
+    h->fn = 0;
+    if (hdr[2])
+      return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                 " reached before the fixpoint");
     if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
       return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                std::to_string(h->rel->max_rows));
@@ -1134,10 +1238,20 @@ struct Runner {
     a.emit.dchg = h->dchg.as<uint32_t>();
     a.emit.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
     HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
     u64 cnt[CNT_N];
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
     if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->emit_ms += ms;
+      st->emit_launches++;
+      st->emit_source_rows += src.n;
+      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+    }
     cands += (int64_t)cnt[CNT_CANDIDATES];
     const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
     Buf tmp, tot, list;
@@ -1185,9 +1299,19 @@ struct Runner {
     q.v = h->ndrow[2].as<uint32_t>();
     q.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
     HIP_TRY(c, k::dense_pull(q, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
     if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "marked key without a contribution (internal)");
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->pull_ms += ms;
+      st->pull_launches++;
+      st->pull_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->pull_new += (int64_t)n;
+    }
     h->keys += (int64_t)cnt[CNT_INSERTED];
     h->pull_n = n;
     if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
@@ -1914,6 +2038,12 @@ struct Runner {
       st->new_tuples_total += d;
     }
     record(total);
+    if (s.recursive && total > 0 && resident_frontier(s)) {
+      if (max_iterations == 0)
+        return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap 0 reached before the fixpoint");
+      XL_TRY(run_frontier_resident(s.variants[0], heads[0].get(), max_iterations));
+      total = 0;
+    }
     if (s.recursive) {
       int64_t pass = 0;
       while (total > 0) {

@@ -61,6 +61,7 @@ struct Context {
   int index_mode = 0;
   int profile = 0;
   int pull_ratio = 64;
+  int frontier_resident = 1;  // closure strata: 1 all rounds in one launch, 0 one launch per round
   int dense_tiles = 0;  // tiled min/max rounds: 0 auto, k tiles per rank, -1 off
   int64_t control_bytes = 0;
 

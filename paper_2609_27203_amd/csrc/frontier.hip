@@ -19,7 +19,9 @@ namespace k {
 constexpr int FR_THREADS = 256;
 constexpr int FR_WAVES = FR_THREADS / 64;
 constexpr uint32_t FR_ZCAP = 4096;  // Z (or Y) values decoded per step
-constexpr int FR_PROBE = 4;         // in-edges a pulling lane loads at once
+constexpr int FR_PROBE = 4;         // in-edges a pulling lane loads at once: one aligned 16-B block
+constexpr int FR_UNROLL = 8;        // first in-edges a pulling lane tests together
+constexpr uint32_t FR_LONG = 64;    // longer remaining in-edge lists are scanned by the whole wave
 
 
 // Workgroup totals of two per-thread counts (one barrier pair).
@@ -45,20 +47,236 @@ __device__ __forceinline__ void block_sum2(uint32_t x, uint32_t y, uint32_t* tx,
   *ty = b;
 }
 
+// LDS of one frontier workgroup besides the three bitmap rows.
+struct FrontierShared {
+  uint32_t zlist[FR_ZCAP];
+  uint32_t s_excl[FR_WAVES][64];
+  uint32_t s_beg[FR_WAVES][64];
+  uint32_t s_w[FR_WAVES], s_w2[FR_WAVES], s_cut[2];
+  uint32_t s_sg;
+};
+
+// One round of row x in LDS: every Y reachable in one step from the delta
+// row f_row (push: expand each delta Z through the index; pull: test each
+// unreached Y's in-edges against f_row) is set in new_row, which starts as a
+// copy of old_row.  Ends with a workgroup barrier.
+__device__ __forceinline__ void frontier_expand(const FrontierArgs& a, const uint32_t* old_row, uint32_t* new_row,
+                                                const uint32_t* f_row, bool pull, FrontierShared& L, u64& cands) {
+  uint32_t* zlist = L.zlist;
+  auto& s_excl = L.s_excl;
+  auto& s_beg = L.s_beg;
+  uint32_t* s_w = L.s_w;
+  uint32_t* s_cut = L.s_cut;
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t W = a.row_words;
+  const uint32_t* ycol = a.idx.col[a.ybind_col];
+  const uint32_t* zcol = a.rev.col[a.rev_zcol];
+  for (uint32_t cb = 0; cb < W;) {
+    // Decode words [cb, cb + 512), two per thread, cut after the last
+    // thread whose values still fit the list: push takes the delta's Z
+    // values, pull the unreached Y values that have an in-edge.
+    const uint32_t w0 = cb + 2u * threadIdx.x;
+    uint32_t d0 = 0, d1 = 0;
+    if (w0 < W) d0 = pull ? (~old_row[w0] & a.hasin[w0]) : f_row[w0];
+    if (w0 + 1 < W) d1 = pull ? (~old_row[w0 + 1] & a.hasin[w0 + 1]) : f_row[w0 + 1];
+    const uint32_t c = __popc(d0) + __popc(d1);
+    uint32_t tot;
+    uint32_t pos = block_excl_scan_u32(c, &tot, s_w);
+    if (pos + c <= FR_ZCAP) {
+      for (uint32_t bits = d0; bits; bits &= bits - 1)
+        zlist[pos++] = (uint32_t)a.lo1 + w0 * 32u + (uint32_t)(__ffs(bits) - 1);
+      for (uint32_t bits = d1; bits; bits &= bits - 1)
+        zlist[pos++] = (uint32_t)a.lo1 + (w0 + 1) * 32u + (uint32_t)(__ffs(bits) - 1);
+    } else if (pos <= FR_ZCAP) {  // the first thread that does not fit
+      s_cut[0] = pos;
+      s_cut[1] = 2u * threadIdx.x;
+    }
+    __syncthreads();
+    const uint32_t nz = tot <= FR_ZCAP ? tot : s_cut[0];
+    cb += tot <= FR_ZCAP ? 2u * FR_THREADS : s_cut[1];
+    if (pull) {
+      // Phase A: every lane tests the first in-edge of FR_UNROLL unreached
+      // Y values, read from the dense first-row array with the loads issued
+      // together.  The Y values whose first in-edge misses the delta are
+      // compacted into the list slots this wavefront owns (slot m of wave w
+      // is 256 * (m / 64) + 64 * w + m % 64; a miss is never written past
+      // the slot its own Y was read from, so no unread value is lost).
+      uint32_t nmiss = 0;
+      for (uint32_t b = 0; b < nz; b += FR_THREADS * FR_UNROLL) {
+        uint32_t yv[FR_UNROLL], zv[FR_UNROLL];
+#pragma unroll
+        for (int j = 0; j < FR_UNROLL; ++j) {
+          const uint32_t pos = b + (uint32_t)j * FR_THREADS + threadIdx.x;
+          yv[j] = pos < nz ? zlist[pos] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < FR_UNROLL; ++j) {
+          const uint32_t pos = b + (uint32_t)j * FR_THREADS + threadIdx.x;
+          const uint32_t kk = yv[j] - (uint32_t)a.rev.key_lo;
+          zv[j] = pos < nz && kk < a.rev.key_range ? a.rev_first[kk] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < FR_UNROLL; ++j) {
+          const uint32_t pos = b + (uint32_t)j * FR_THREADS + threadIdx.x;
+          const uint32_t kk = yv[j] - (uint32_t)a.rev.key_lo;
+          bool miss = false;
+          if (pos < nz && kk < a.rev.key_range) {  // every listed Y has an in-edge
+            ++cands;
+            const uint32_t z0 = zv[j] - (uint32_t)a.lo1;
+            if (z0 < W * 32u && ((f_row[z0 >> 5] >> (z0 & 31)) & 1u)) {
+              const uint32_t yb = yv[j] - (uint32_t)a.lo1;
+              atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
+            } else {
+              miss = true;
+            }
+          }
+          const u64 bm = __ballot(miss);
+          if (miss) {
+            const uint32_t m = nmiss + (uint32_t)__popcll(bm & lanemask_lt());
+            zlist[(m >> 6) * FR_THREADS + (uint32_t)w * 64 + (m & 63)] = yv[j];
+          }
+          nmiss += (uint32_t)__popcll(bm);
+        }
+      }
+      wave_lds_sync();
+      // Phase B, per wavefront over its misses: one lane per Y tests the
+      // remaining in-edges one aligned 16-B block at a time (index columns
+      // are 256-B aligned arena blocks rounded up to 256 B, so a block never
+      // leaves the column's allocation) until one comes from the delta;
+      // lists with more than FR_LONG left are scanned by the whole
+      // wavefront, 64 in-edges per step, stopping at the first hit.  The
+      // candidates counted are the in-edges a scan in order examines, up to
+      // the first hit (the rest of a block or step is wasted load).
+      for (uint32_t m0 = 0; m0 < nmiss; m0 += 64) {
+        const uint32_t m = m0 + lane;
+        uint32_t y = 0, e = 0, e1 = 0;
+        if (m < nmiss) {
+          y = zlist[(m >> 6) * FR_THREADS + (uint32_t)w * 64 + (m & 63)];
+          const uint32_t kk = y - (uint32_t)a.rev.key_lo;
+          e = a.rev.off[kk] + 1;
+          e1 = a.rev.off[kk + 1];
+        }
+        const bool longl = e1 > e + FR_LONG;
+        u64 lm = __ballot(longl);
+        bool hit = false;
+        if (!longl) {
+          while (e < e1 && !hit) {
+            const uint32_t base = e & ~(uint32_t)(FR_PROBE - 1);
+            const uint4 q = *reinterpret_cast<const uint4*>(zcol + base);
+            const uint32_t zz[FR_PROBE] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+            for (int u = 0; u < FR_PROBE; ++u) {
+              const uint32_t i = base + (uint32_t)u;
+              if (hit || i < e || i >= e1) continue;
+              ++cands;
+              const uint32_t zb = zz[u] - (uint32_t)a.lo1;
+              hit = zb < W * 32u && ((f_row[zb >> 5] >> (zb & 31)) & 1u);
+            }
+            e = base + FR_PROBE;
+          }
+        }
+        if (hit) {
+          const uint32_t yb = y - (uint32_t)a.lo1;
+          atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
+        }
+        while (lm) {
+          const int rb = __ffsll((long long)lm) - 1;
+          lm &= lm - 1;
+          const uint32_t by = __shfl(y, rb, 64), bb = __shfl(e, rb, 64), be = __shfl(e1, rb, 64);
+          for (uint32_t k0 = bb; k0 < be; k0 += 64) {
+            const uint32_t i = k0 + lane;
+            bool h = false;
+            if (i < be) {
+              const uint32_t zb = zcol[i] - (uint32_t)a.lo1;
+              h = zb < W * 32u && ((f_row[zb >> 5] >> (zb & 31)) & 1u);
+            }
+            const u64 hm = __ballot(h);
+            if (hm) {
+              if (lane == 0) {
+                cands += (u64)__ffsll((long long)hm);
+                const uint32_t yb = by - (uint32_t)a.lo1;
+                atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
+              }
+              break;
+            }
+            if (lane == 0) cands += be - k0 < 64u ? be - k0 : 64u;
+          }
+        }
+      }
+      __syncthreads();
+      continue;
+    }
+    for (uint32_t r0 = (uint32_t)w * 64; r0 < nz; r0 += FR_WAVES * 64) {
+      const uint32_t r = r0 + lane;
+      uint32_t beg = 0, deg = 0;
+      if (r < nz) {
+        const uint32_t kk = zlist[r] - (uint32_t)a.idx.key_lo;
+        if (kk < a.idx.key_range) {
+          beg = a.idx.off[kk];
+          deg = a.idx.off[kk + 1] - beg;
+        }
+      }
+      // Rows with at least 64 matches are walked by the whole wavefront, one
+      // row at a time, lane = item: no owner search at all.  The remaining
+      // small rows share 64-item steps through a scan and a six-step search.
+      const bool big = deg >= 64;
+      u64 bigm = __ballot(big);
+      const uint32_t sdeg = big ? 0u : deg;
+      const uint32_t incl = wave_incl_scan(sdeg);
+      const uint32_t total = __shfl(incl, 63, 64);
+      s_excl[w][lane] = incl - sdeg;
+      s_beg[w][lane] = beg;
+      wave_lds_sync();
+      if (lane == 0) cands += total;
+      while (bigm) {
+        const int rb = __ffsll((long long)bigm) - 1;
+        bigm &= bigm - 1;
+        const uint32_t bb = __shfl(beg, rb, 64), bd = __shfl(deg, rb, 64);
+        if (lane == 0) cands += bd;
+        for (uint32_t k0 = 0; k0 < bd; k0 += 256) {
+          uint32_t y[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const uint32_t k = k0 + 64 * u + lane;
+            y[u] = k < bd ? ycol[bb + k] - (uint32_t)a.lo1 : 0xffffffffu;
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (y[u] != 0xffffffffu) {
+              const uint32_t bit = 1u << (y[u] & 31);
+              if (!(new_row[y[u] >> 5] & bit)) atomicOr(&new_row[y[u] >> 5], bit);
+            }
+          }
+        }
+      }
+      for (uint32_t b0 = 0; b0 < total; b0 += 64) {
+        const uint32_t j = b0 + lane;
+        if (j < total) {
+          int q = 0;
+#pragma unroll
+          for (int step = 32; step > 0; step >>= 1)
+            if (s_excl[w][q + step] <= j) q += step;
+          const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
+          const uint32_t bit = 1u << (y & 31);
+          if (!(new_row[y >> 5] & bit)) atomicOr(&new_row[y >> 5], bit);
+        }
+      }
+      wave_lds_sync();
+    }
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
   extern __shared__ uint32_t lds[];
   uint32_t* old_row = lds;
   uint32_t* new_row = lds + a.row_words;
   uint32_t* f_row = lds + 2 * a.row_words;  // this round's delta row of x
-  __shared__ uint32_t zlist[FR_ZCAP];
-  __shared__ uint32_t s_excl[FR_WAVES][64];
-  __shared__ uint32_t s_beg[FR_WAVES][64];
-  __shared__ uint32_t s_w[FR_WAVES], s_w2[FR_WAVES], s_cut[2];
+  __shared__ FrontierShared L;
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const uint32_t W = a.row_words;
-  const uint32_t* ycol = a.idx.col[a.ybind_col];
-  const uint32_t* zcol = a.rev.col[a.rev_zcol];
   u64 cands = 0, news = 0;  // cands: this lane's share; news: workgroup total
+  uint32_t* s_w = L.s_w;
   for (int64_t sg = blockIdx.x; sg < a.nseg; sg += gridDim.x) {
     if (a.in_cnt[sg] == 0) {  // x gained nothing last round: its delta row is empty
       if (threadIdx.x == 0) a.out_cnt[sg] = 0;
@@ -77,121 +295,9 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
       if (a.pull_ratio) nu += __popc(~v & a.hasin[i]);
     }
     uint32_t tnd, tnu;
-    block_sum2(nd, nu, &tnd, &tnu, s_w, s_w2);
+    block_sum2(nd, nu, &tnd, &tnu, L.s_w, L.s_w2);
     const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
-    for (uint32_t cb = 0; cb < W;) {
-      // Decode words [cb, cb + 512), two per thread, cut after the last
-      // thread whose values still fit the list: push takes the delta's Z
-      // values, pull the unreached Y values that have an in-edge.
-      const uint32_t w0 = cb + 2u * threadIdx.x;
-      uint32_t d0 = 0, d1 = 0;
-      if (w0 < W) d0 = pull ? (~old_row[w0] & a.hasin[w0]) : f_row[w0];
-      if (w0 + 1 < W) d1 = pull ? (~old_row[w0 + 1] & a.hasin[w0 + 1]) : f_row[w0 + 1];
-      const uint32_t c = __popc(d0) + __popc(d1);
-      uint32_t tot;
-      uint32_t pos = block_excl_scan_u32(c, &tot, s_w);
-      if (pos + c <= FR_ZCAP) {
-        for (uint32_t bits = d0; bits; bits &= bits - 1)
-          zlist[pos++] = (uint32_t)a.lo1 + w0 * 32u + (uint32_t)(__ffs(bits) - 1);
-        for (uint32_t bits = d1; bits; bits &= bits - 1)
-          zlist[pos++] = (uint32_t)a.lo1 + (w0 + 1) * 32u + (uint32_t)(__ffs(bits) - 1);
-      } else if (pos <= FR_ZCAP) {  // the first thread that does not fit
-        s_cut[0] = pos;
-        s_cut[1] = 2u * threadIdx.x;
-      }
-      __syncthreads();
-      const uint32_t nz = tot <= FR_ZCAP ? tot : s_cut[0];
-      cb += tot <= FR_ZCAP ? 2u * FR_THREADS : s_cut[1];
-      if (pull) {
-        // One lane per unreached Y: test its in-edges FR_PROBE at a time
-        // (independent loads) until one comes from the delta.
-        for (uint32_t r = threadIdx.x; r < nz; r += FR_THREADS) {
-          const uint32_t y = zlist[r];
-          const uint32_t kk = y - (uint32_t)a.rev.key_lo;
-          if (kk >= a.rev.key_range) continue;
-          const uint32_t e1 = a.rev.off[kk + 1];
-          bool hit = false;
-          for (uint32_t e = a.rev.off[kk]; e < e1 && !hit; e += FR_PROBE) {
-            uint32_t zz[FR_PROBE];
-#pragma unroll
-            for (int u = 0; u < FR_PROBE; ++u) zz[u] = e + u < e1 ? zcol[e + u] - (uint32_t)a.lo1 : 0xffffffffu;
-            // count the in-edges a scan in order would examine: up to the
-            // first one from the delta (the rest of the batch is wasted load)
-            const uint32_t nb = e1 - e < (uint32_t)FR_PROBE ? e1 - e : (uint32_t)FR_PROBE;
-#pragma unroll
-            for (int u = 0; u < FR_PROBE; ++u) {
-              if (hit || (uint32_t)u >= nb) continue;
-              ++cands;
-              hit = zz[u] < W * 32u && ((f_row[zz[u] >> 5] >> (zz[u] & 31)) & 1u);
-            }
-          }
-          if (hit) {
-            const uint32_t yb = y - (uint32_t)a.lo1;
-            atomicOr(&new_row[yb >> 5], 1u << (yb & 31));
-          }
-        }
-        __syncthreads();
-        continue;
-      }
-      for (uint32_t r0 = (uint32_t)w * 64; r0 < nz; r0 += FR_WAVES * 64) {
-        const uint32_t r = r0 + lane;
-        uint32_t beg = 0, deg = 0;
-        if (r < nz) {
-          const uint32_t kk = zlist[r] - (uint32_t)a.idx.key_lo;
-          if (kk < a.idx.key_range) {
-            beg = a.idx.off[kk];
-            deg = a.idx.off[kk + 1] - beg;
-          }
-        }
-        // Rows with at least 64 matches are walked by the whole wavefront, one
-        // row at a time, lane = item: no owner search at all.  The remaining
-        // small rows share 64-item steps through a scan and a six-step search.
-        const bool big = deg >= 64;
-        u64 bigm = __ballot(big);
-        const uint32_t sdeg = big ? 0u : deg;
-        const uint32_t incl = wave_incl_scan(sdeg);
-        const uint32_t total = __shfl(incl, 63, 64);
-        s_excl[w][lane] = incl - sdeg;
-        s_beg[w][lane] = beg;
-        wave_lds_sync();
-        if (lane == 0) cands += total;
-        while (bigm) {
-          const int rb = __ffsll((long long)bigm) - 1;
-          bigm &= bigm - 1;
-          const uint32_t bb = __shfl(beg, rb, 64), bd = __shfl(deg, rb, 64);
-          if (lane == 0) cands += bd;
-          for (uint32_t k0 = 0; k0 < bd; k0 += 256) {
-            uint32_t y[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const uint32_t k = k0 + 64 * u + lane;
-              y[u] = k < bd ? ycol[bb + k] - (uint32_t)a.lo1 : 0xffffffffu;
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              if (y[u] != 0xffffffffu) {
-                const uint32_t bit = 1u << (y[u] & 31);
-                if (!(new_row[y[u] >> 5] & bit)) atomicOr(&new_row[y[u] >> 5], bit);
-              }
-            }
-          }
-        }
-        for (uint32_t b0 = 0; b0 < total; b0 += 64) {
-          const uint32_t j = b0 + lane;
-          if (j < total) {
-            int q = 0;
-#pragma unroll
-            for (int step = 32; step > 0; step >>= 1)
-              if (s_excl[w][q + step] <= j) q += step;
-            const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
-            const uint32_t bit = 1u << (y & 31);
-            if (!(new_row[y >> 5] & bit)) atomicOr(&new_row[y >> 5], bit);
-          }
-        }
-        wave_lds_sync();
-      }
-      __syncthreads();
-    }
+    frontier_expand(a, old_row, new_row, f_row, pull, L, cands);
     // next delta row = new bits; write back the changed words of row x
     uint32_t nnew = 0;
     uint32_t* orow = a.out_diff + (u64)sg * W;
@@ -230,6 +336,99 @@ hipError_t frontier_round(const FrontierArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Resident form (see FrontierArgs): the rounds of one first key x depend only
+// on x's own row and the fixed index, so a workgroup runs them back to back
+// with the row, the delta and the next row in LDS and no launch, host read or
+// HBM round trip in between.
+__global__ __launch_bounds__(FR_THREADS) void frontier_resident_k(FrontierArgs a) {
+  extern __shared__ uint32_t lds[];
+  uint32_t* old_row = lds;
+  uint32_t* new_row = lds + a.row_words;
+  uint32_t* f_row = lds + 2 * a.row_words;
+  __shared__ FrontierShared L;
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const uint32_t W = a.row_words;
+  u64 cands = 0, news = 0;
+  for (;;) {
+    if (threadIdx.x == 0) L.s_sg = atomicAdd(a.queue, 1u);
+    __syncthreads();
+    const uint32_t sg = L.s_sg;
+    if ((int64_t)sg >= a.nseg) break;
+    if (a.in_cnt[sg] == 0) {  // keeps the barrier above between two reads of s_sg
+      __syncthreads();
+      continue;
+    }
+    const uint32_t x = a.x[sg];
+    uint32_t* grow = a.bits + (u64)(x - (uint32_t)a.lo0) * W;
+    const uint32_t* drow = a.in_diff + (u64)sg * W;
+    uint32_t nd = 0, nu = 0;
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
+      const uint32_t v = grow[i], f = drow[i];
+      old_row[i] = v;
+      new_row[i] = v;
+      f_row[i] = f;
+      nd += __popc(f);
+      if (a.pull_ratio) nu += __popc(~v & a.hasin[i]);
+    }
+    uint32_t tnd, tnu;
+    block_sum2(nd, nu, &tnd, &tnu, L.s_w, L.s_w2);
+    uint32_t round = 0;
+    while (tnd > 0) {
+      if (round >= a.max_rounds) {
+        if (threadIdx.x == 0) atomicOr(a.overflow, 1u);
+        break;
+      }
+      const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
+      frontier_expand(a, old_row, new_row, f_row, pull, L, cands);
+      // the new bits become the next delta; the row takes them
+      nd = 0;
+      nu = 0;
+      for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
+        const uint32_t nv = new_row[i];
+        const uint32_t dd = nv & ~old_row[i];
+        f_row[i] = dd;
+        old_row[i] = nv;
+        nd += __popc(dd);
+        if (a.pull_ratio) nu += __popc(~nv & a.hasin[i]);
+      }
+      block_sum2(nd, nu, &tnd, &tnu, L.s_w, L.s_w2);
+      if (threadIdx.x == 0 && tnd) atomicAdd(&a.round_new[round < a.round_slots ? round : a.round_slots - 1], (u64)tnd);
+      news += tnd;
+      ++round;
+    }
+    if (threadIdx.x == 0) atomicMax(a.max_round, round);
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) grow[i] = old_row[i];
+    __syncthreads();  // the row is written before LDS takes the next key
+  }
+  for (int k = 32; k > 0; k >>= 1) cands += __shfl_xor(cands, k, 64);
+  __shared__ u64 s_c[FR_WAVES];
+  if (lane == 0) s_c[w] = cands;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 t = 0;
+    for (int i = 0; i < FR_WAVES; ++i) t += s_c[i];
+    if (t) atomicAdd(&a.counters[CNT_CANDIDATES], t);
+    if (news) atomicAdd(&a.counters[CNT_APPENDED], news);
+  }
+}
+
+hipError_t frontier_resident(const FrontierArgs& a, unsigned grid, hipStream_t s) {
+  if (a.nseg <= 0) return hipSuccess;
+  if (!a.queue || !a.max_round || !a.overflow || !a.round_new || a.round_slots == 0) return hipErrorInvalidValue;
+  const size_t lds = (size_t)a.row_words * 3 * sizeof(uint32_t);
+  if (grid == 0) {
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, frontier_resident_k, FR_THREADS, lds);
+    if (e != hipSuccess) return e;
+    grid = (unsigned)std::max(1, cus * std::max(1, per_cu));
+  }
+  grid = (unsigned)std::min<int64_t>(grid, a.nseg);
+  frontier_resident_k<<<grid, FR_THREADS, lds, s>>>(a);
+  return hipGetLastError();
+}
 
 // Number of set bits in each bitmap row.
 __global__ __launch_bounds__(256) void row_popcount_k(const uint32_t* bits, int64_t nrows,

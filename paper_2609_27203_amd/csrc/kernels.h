@@ -43,6 +43,12 @@ hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hip
 // off[k] = first i with sorted[i] >= k, for k in [0, range].
 hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
                        hipStream_t s);
+// key[i] = (sorted[i] << 16) | (0xffff - min(deg(zcol[perm[i]]), 0xffff)), deg
+// read from the CSR offsets off over keys [klo, klo + range).
+hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol, int32_t klo,
+                             uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s);
+// out[k] = col[off[k]] for keys k in [0, range) with rows, 0xffffffff otherwise.
+hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s);
 // flag[i] = 1 if row i differs (bitwise) from row i-1 in any column (or i == 0).
 hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
                             hipStream_t s);
@@ -94,6 +100,9 @@ hipError_t agg_merge(Slot16* t, u64 mask, const uint32_t* k0, const uint32_t* k1
 hipError_t bits_set_rows(uint32_t* bits, u64 row_bits, const uint32_t* c0, const uint32_t* c1,
                          int64_t n, KeyPack kp, hipStream_t s);
 hipError_t frontier_round(const FrontierArgs& a, hipStream_t s);
+// All rounds of every first key in one launch; grid 0 = as many workgroups
+// as the device keeps resident.
+hipError_t frontier_resident(const FrontierArgs& a, unsigned grid, hipStream_t s);
 hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s);
 hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
                         hipStream_t s);

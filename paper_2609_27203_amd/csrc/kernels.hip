@@ -334,6 +334,41 @@ hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32
   return hipGetLastError();
 }
 
+// key[i] = (sorted[i] << 16) | (0xffff - min(deg(z), 0xffff)) with z =
+// zcol[perm[i]] and deg(z) = off[z - klo + 1] - off[z - klo] (0 outside the
+// key range): sorting by it keeps the key order and puts, inside each key's
+// segment, the rows whose z has the most rows first.
+__global__ void degree_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol,
+                                    int32_t klo, uint32_t range, const uint32_t* off, int64_t n, u64* key) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t kz = zcol[perm[i]] - (uint32_t)klo;
+    const uint32_t deg = kz < range ? off[kz + 1] - off[kz] : 0u;
+    key[i] = ((u64)sorted[i] << 16) | (0xffffu - (deg < 0xffffu ? deg : 0xffffu));
+  }
+}
+hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol, int32_t klo,
+                             uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  degree_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, zcol, klo, range, off, n, key);
+  return hipGetLastError();
+}
+
+// out[k] = col[off[k]] (the first row of key k's segment), or 0xffffffff
+// for an empty segment.
+__global__ void segment_first_k(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < (int64_t)range;
+       k += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t b = off[k];
+    out[k] = b < off[k + 1] ? col[b] : 0xffffffffu;
+  }
+}
+hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s) {
+  if (range == 0) return hipSuccess;
+  segment_first_k<<<grid_for(range, 256, 65536), 256, 0, s>>>(off, col, range, out);
+  return hipGetLastError();
+}
+
 struct ColPtrs { const uint32_t* c[MAXC]; };
 
 __global__ void row_change_k(ColPtrs cols, int ncols, int64_t n, uint32_t* flag) {
@@ -1540,7 +1575,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const bool lse = a.fold_kind == FOLD_LSE, f32 = a.val_type == T_F32;
   const int64_t nchunks = (a.n + 63) / 64;
-  uint32_t mine = 0;
+  uint32_t mine = 0, examined = 0;
   for (int64_t chunk = (int64_t)blockIdx.x * DP_WAVES + w; chunk < nchunks; chunk += (int64_t)gridDim.x * DP_WAVES) {
     const int64_t i = chunk * 64 + lane;
     uint32_t t = 0, e0 = 0, deg = 0;
@@ -1554,6 +1589,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
     }
     const uint32_t incl = wave_incl_scan(deg);
     const uint32_t total = __shfl(incl, 63, 64);
+    if (lane == 0) examined += total;
     s_excl[w][lane] = incl - deg;
     s_beg[w][lane] = e0;
     s_key[w][lane] = t;
@@ -1640,6 +1676,8 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
     wave_lds_sync();
   }
   block_count_add(&a.counters[CNT_INSERTED], mine);
+  __syncthreads();  // the helper's LDS words are reused by the second call
+  block_count_add(&a.counters[CNT_CANDIDATES], examined);
 }
 
 hipError_t dense_pull(const DensePullArgs& a, hipStream_t s) {

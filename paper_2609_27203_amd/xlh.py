@@ -44,6 +44,8 @@ class xl_fixpoint_stats(C.Structure):
         ("emit_candidates", C.c_int64), ("emit_new", C.c_int64),
         ("front_ms", C.c_double), ("front_launches", C.c_int64), ("front_candidates", C.c_int64),
         ("front_new", C.c_int64),
+        ("pull_ms", C.c_double), ("pull_launches", C.c_int64), ("pull_candidates", C.c_int64),
+        ("pull_new", C.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -58,6 +60,8 @@ class xl_fixpoint_stats(C.Structure):
             "emit_source_rows": self.emit_source_rows, "emit_candidates": self.emit_candidates,
             "emit_new": self.emit_new, "front_ms": self.front_ms, "front_launches": self.front_launches,
             "front_candidates": self.front_candidates, "front_new": self.front_new,
+            "pull_ms": self.pull_ms, "pull_launches": self.pull_launches,
+            "pull_candidates": self.pull_candidates, "pull_new": self.pull_new,
         }
 
 

@@ -82,16 +82,24 @@ def test_small_workload_with_forced_table_growth(name, index_mode):
         assert stats["table_grows"] > 0
 
 
+@pytest.mark.parametrize("resident", [0, 1])
 @pytest.mark.parametrize("pull_ratio", [0, 1, 64, 1024])
 @pytest.mark.parametrize("name", ["tc_uniform", "tc_rmat_count"])
-def test_closure_push_and_pull_directions(name, pull_ratio):
-    """Frontier rounds give the same closure whether sources push, pull or mix."""
+def test_closure_push_and_pull_directions(name, pull_ratio, resident):
+    """Frontier rounds give the same closure whether sources push, pull or mix,
+    launched one round at a time or all rounds of a source in one launch; the
+    per-pass delta sizes are the oracle's in both."""
     wl = W.small_workloads()[name]()
-    print(f"case: direction {name} pull_ratio={pull_ratio}", flush=True)
+    print(f"case: direction {name} pull_ratio={pull_ratio} resident={resident}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, stats, _ = engine_run(wl, options={"pull_ratio": pull_ratio})
+    rels, stats, _ = engine_run(wl, options={"pull_ratio": pull_ratio, "frontier_resident": resident,
+                                             "profile": 1})
     _compare(wl, rels, ref)
     assert stats["delta_rows"] == _delta_levels(ref, "path") + ([0] * (len(stats["delta_rows"]) - len(ref.sizes["path"])))
+    passes = len(ref.sizes["path"]) - 1
+    assert stats["iterations"] == passes
+    assert stats["front_launches"] == (1 if resident else passes)
+    assert stats["front_new"] == len(ref.relations["path"][1][0]) - stats["delta_rows"][0]
 
 
 COUNT_SHAPES_RULES = W.TC_RULES + """
@@ -337,13 +345,22 @@ def test_negative_ids_and_wide_key_range():
     _compare(wl, rels, ref)
 
 
-def test_iteration_cap_is_convergence_failure():
+@pytest.mark.parametrize("resident", [0, 1])
+def test_iteration_cap_is_convergence_failure(resident):
+    """A chain of 6 nodes needs 5 passes (deltas 4, 3, 2, 1, 0 after the
+    seed): a cap of 5 converges, 4 and 0 do not."""
     from paper_2609_27203_amd import xlh
     n = 6
     wl = W.Workload("chain", W.TC_RULES, _edges(np.arange(n - 1), np.arange(1, n)), {"path": ("i32", "i32")})
-    with pytest.raises(xlh.XlError) as ei:
-        engine_run(wl, workspace_bytes=256 << 20, max_iterations=1)
-    assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+    print(f"case: iteration cap resident={resident}", flush=True)
+    opts = {"frontier_resident": resident}
+    for cap in (0, 1, 4):
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, workspace_bytes=256 << 20, max_iterations=cap, options=opts)
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+    rels, stats, _ = engine_run(wl, workspace_bytes=256 << 20, max_iterations=5, options=opts)
+    assert stats["iterations"] == 5 and stats["delta_rows"] == [5, 4, 3, 2, 1, 0]
+    assert len(rels["path"][0]) == n * (n - 1) // 2
 
 
 def test_capacity_and_workspace_errors():
