@@ -239,7 +239,9 @@ struct FrontierArgs {
   IndexProbe rev;
   int32_t rev_zcol;
   const uint32_t* rev_first;
-  // Resident form: each workgroup takes first keys from *queue (zero at
+  // Resident form (x and in_cnt may be null: delta row sg then belongs to
+  // first key lo0 + sg, and an empty row is found by counting its bits): each
+  // workgroup takes first keys from *queue (zero at
   // launch) and runs all of a key's rounds with its row held in LDS, writing
   // the row back once; per round r (from 0) it adds the tuples found to
   // round_new[min(r, round_slots - 1)], raises *max_round to the rounds it

@@ -365,7 +365,9 @@ struct HeadRun {
   // frontier form (closure-shaped stratum over a dense two-column head): the
   // delta is one bitmap row per first-key value that gained tuples
   bool frontier = false;
-  bool frontier_ready = false;  // the current delta is in fcnt/fdiff[fcur]
+  bool resident = false;        // frontier form run by one resident launch, which reads
+                                // the seed's delta straight from dbits
+  bool frontier_ready = false;  // the current delta is in fcnt/fdiff[fcur] (or dbits)
   Buf fx, fcnt[2], fdiff[2];    // delta row slot sg belongs to first-key value fx[sg]
   Buf hasin;                    // Y values with an in-edge (pull direction)
   int fcur = 0;
@@ -744,6 +746,7 @@ struct Runner {
           hr->frontier = s.recursive && s.heads.size() == 1 && s.variants.size() == 1 &&
                          s.variants[0].carried && hr->nkey == 2 && hr->row_words <= 3072 &&
                          total_bits / 8 * 3 <= budget;
+          hr->resident = hr->frontier && c->frontier_resident;
         }
       }
       hr->preloaded = (hr->is_set || hr->is_minmax) ? h->nrows : 0;
@@ -789,7 +792,7 @@ struct Runner {
                                 c->stream));
     h->nrows = h->keys = h->preloaded;
     h->dbeg = h->dend = 0;
-    if (h->frontier) {
+    if (h->frontier && !h->resident) {
       XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->fx, "delta row keys"));
       for (int b = 0; b < 2; ++b) {
         XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->fcnt[b], "delta row counts"));
@@ -1071,7 +1074,7 @@ struct Runner {
   // rounds never read another key's rows: the i-th pass's delta is the union
   // of every key's i-th round.
   bool resident_frontier(const Stratum& s) {
-    return c->frontier_resident && heads.size() == 1 && heads[0]->frontier && heads[0]->frontier_ready &&
+    return heads.size() == 1 && heads[0]->resident && heads[0]->frontier_ready &&
            s.variants.size() == 1 && s.variants[0].driver_delta && head_of(s.variants[0].head) == heads[0].get();
   }
 
@@ -1079,6 +1082,11 @@ struct Runner {
     if (h->fn == 0) return XL_OK;
     FrontierArgs f{};
     XL_TRY(frontier_args(p, h, f));
+    f.x = nullptr;  // delta row sg of first key lo0 + sg is dbits row sg
+    f.in_cnt = nullptr;
+    f.in_diff = h->dbits.as<uint32_t>();
+    f.nseg = h->range0;
+    f.out_cnt = f.out_diff = nullptr;
     constexpr size_t HDR = 16;
     Buf rs;
     XL_TRY(dalloc(c, HDR + 8 * XL_STATS_ROUNDS, &rs, "round counters"));
@@ -1689,6 +1697,11 @@ struct Runner {
     }
     if (h->dense) {
       *delta = h->round_new;
+      if (h->resident) {  // the resident launch reads the seed's delta rows from dbits
+        h->frontier_ready = true;
+        h->fn = h->round_new ? h->range0 : 0;
+        return XL_OK;
+      }
       if (h->frontier) return frontier_from_bits(h);  // seed round -> first frontier
       // this round's new tuples, in key order, become the delta rows
       const int64_t nbits = (int64_t)(h->nkey == 2 ? (u64)h->range0 * h->row_bits : (u64)((h->range0 + 31) / 32) * 32);

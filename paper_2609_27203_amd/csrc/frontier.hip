@@ -354,24 +354,28 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_resident_k(FrontierArgs a
     __syncthreads();
     const uint32_t sg = L.s_sg;
     if ((int64_t)sg >= a.nseg) break;
-    if (a.in_cnt[sg] == 0) {  // keeps the barrier above between two reads of s_sg
+    if (a.in_cnt && a.in_cnt[sg] == 0) {  // keeps the barrier above between two reads of s_sg
       __syncthreads();
       continue;
     }
-    const uint32_t x = a.x[sg];
+    const uint32_t x = a.x ? a.x[sg] : (uint32_t)a.lo0 + sg;
     uint32_t* grow = a.bits + (u64)(x - (uint32_t)a.lo0) * W;
     const uint32_t* drow = a.in_diff + (u64)sg * W;
-    uint32_t nd = 0, nu = 0;
+    uint32_t nd = 0, nu = 0, tnd, tnu;
     for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
-      const uint32_t v = grow[i], f = drow[i];
-      old_row[i] = v;
-      new_row[i] = v;
+      const uint32_t f = drow[i];
       f_row[i] = f;
       nd += __popc(f);
+    }
+    block_sum2(nd, 0u, &tnd, &tnu, L.s_w, L.s_w2);
+    if (tnd == 0) continue;  // no delta: the row stays as it is (block_sum2 ended with a barrier)
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
+      const uint32_t v = grow[i];
+      old_row[i] = v;
+      new_row[i] = v;
       if (a.pull_ratio) nu += __popc(~v & a.hasin[i]);
     }
-    uint32_t tnd, tnu;
-    block_sum2(nd, nu, &tnd, &tnu, L.s_w, L.s_w2);
+    block_sum2(nu, 0u, &tnu, &nd, L.s_w, L.s_w2);
     uint32_t round = 0;
     while (tnd > 0) {
       if (round >= a.max_rounds) {
@@ -396,8 +400,9 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_resident_k(FrontierArgs a
       news += tnd;
       ++round;
     }
-    if (threadIdx.x == 0) atomicMax(a.max_round, round);
-    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) grow[i] = old_row[i];
+    if (threadIdx.x == 0 && round) atomicMax(a.max_round, round);
+    if (round)
+      for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) grow[i] = old_row[i];
     __syncthreads();  // the row is written before LDS takes the next key
   }
   for (int k = 32; k > 0; k >>= 1) cands += __shfl_xor(cands, k, 64);
