@@ -28,6 +28,15 @@ What it computes (the plain definition the semi-naive method reaches):
   logsumexp uses the max-shifted form m + log(sum(exp(x - m))) in float64;
   a group whose values are all -inf folds to -inf.
 
+* Stratified negation (Sec. 3, completeness over finite domains: explicit
+  stratified negation-as-failure; Sec. 2, program to GPU plan: negative
+  dependency edges in the SCC analysis).  A body literal ``not q(t1, .., tk)``
+  holds for a derivation when no row of q agrees with it on every column
+  given by a variable or a constant (``_`` columns are unconstrained).  Every
+  variable of a negated literal must occur in a positive atom or an ``is``
+  of the same rule, and q must be complete before the rule runs: a negative
+  dependency inside one strongly connected component is rejected.
+
 Readings where the paper is silent are listed with the engine's design notes;
 the ones that change results here are: aggregates fold over derivations (so
 count(Y) with body path(X,Y) counts distinct Y per X), groups without
@@ -75,6 +84,7 @@ class Rule:
     atoms: list = field(default_factory=list)    # (pred, [terms])
     assigns: list = field(default_factory=list)  # (var, [(sign, term)])
     filters: list = field(default_factory=list)  # (op, term, term)
+    negs: list = field(default_factory=list)     # (pred, [terms]) of 'not' literals
 
 
 def _tokens(text):
@@ -154,7 +164,11 @@ def parse(text: str) -> list:
         expect(":-")
         while True:
             t0 = toks[i]
-            if t0[0] == "name" and not (t0[1][0].isupper() or t0[1][0] == "_") \
+            if t0 == ("name", "not") and toks[i + 1][0] == "name" and toks[i + 2][1] == "(":
+                pred = toks[i + 1][1]
+                i += 2
+                rule.negs.append((pred, atom_args()))
+            elif t0[0] == "name" and not (t0[1][0].isupper() or t0[1][0] == "_") \
                     and toks[i + 1][1] == "(":
                 i += 1
                 rule.atoms.append((t0[1], atom_args()))
@@ -301,12 +315,44 @@ def _eval_body(rule, rels, var_types):
             raise TypeError(f"variable {var} used at two types")
         binding[var] = acc.astype(np.float32) if ty == "f32" else acc.astype(np.int64).astype(np.int32)
     mask = np.ones(n, bool)
+    for pred, terms in rule.negs:
+        mask &= ~_negated_match(pred, terms, rels, binding, var_types, n)
     for op, a, b in rule.filters:
         av = binding[a[1]] if a[0] == "var" else a[1]
         bv = binding[b[1]] if b[0] == "var" else b[1]
         mask &= {"!=": np.not_equal, "==": np.equal, "<": np.less, "<=": np.less_equal,
                  ">": np.greater, ">=": np.greater_equal}[op](av, bv)
     return {v: c[mask] for v, c in binding.items()}, int(mask.sum())
+
+
+def _negated_match(pred, terms, rels, binding, var_types, n):
+    """For each of the n derivations: does some row of pred agree with it on
+    every variable and constant column of the negated literal?"""
+    types, cols = rels[pred]
+    if len(terms) != len(types):
+        raise TypeError(f"{pred}/{len(types)} used with {len(terms)} arguments")
+    mask = np.ones(len(cols[0]), bool)
+    first = {}
+    for j, t in enumerate(terms):
+        if t[0] in ("int", "float"):
+            mask &= cols[j] == np.asarray(t[1], _NP[types[j]])
+        elif t[0] == "var":
+            if t[1] not in binding:
+                raise ValueError(f"{t[1]} occurs only in a negated literal")
+            if var_types[t[1]] != types[j]:
+                raise TypeError(f"variable {t[1]} used at two types")
+            if t[1] in first:
+                mask &= cols[j] == cols[first[t[1]]]
+            else:
+                first[t[1]] = j
+    rows = [c[mask] for c in cols]
+    if not first:  # only constants and '_': the literal fails iff such a row exists
+        return np.full(n, len(rows[0]) > 0)
+    if len(rows[0]) == 0 or n == 0:
+        return np.zeros(n, bool)
+    vs = list(first)
+    lcode, rcode = _join_codes([binding[v] for v in vs], [rows[first[v]] for v in vs])
+    return np.isin(lcode, rcode)
 
 
 def _fold(op, keys, vals, ty):
@@ -380,10 +426,15 @@ def _apply_rules(head, htypes, rules, rels):
 def _strata(rules, idb):
     """Strongly connected components of the IDB dependency graph, dependencies first."""
     deps = {h: set() for h in idb}
+    negdeps = []
     for r in rules:
         for pred, _ in r.atoms:
             if pred in idb:
                 deps[r.head].add(pred)
+        for pred, _ in r.negs:
+            if pred in idb:
+                deps[r.head].add(pred)
+                negdeps.append((r.head, pred))
     index, low, stack, on, out = {}, {}, [], set(), []
 
     def visit(v):
@@ -409,6 +460,11 @@ def _strata(rules, idb):
     for v in sorted(idb):
         if v not in index:
             visit(v)
+    comp_of = {h: k for k, comp in enumerate(out) for h in comp}
+    for head, pred in negdeps:
+        if comp_of[head] == comp_of[pred]:
+            raise ValueError(f"{head} depends negatively on {pred} inside one recursive component "
+                             "(negation is stratified)")
     return out  # Tarjan emits components in reverse topological order of deps
 
 

@@ -325,6 +325,86 @@ def test_sg_closed_form_small_forest():
     assert len(got) == sum(len(g) * (len(g) - 1) for g in groups.values())
 
 
+# ---------------------------------------------------------------- stratified negation
+NEG_LISTING = """
+degree(X, count(Y)) :- edge(X, Y).
+violation(X) :- edge(X, _), not degree(X, _).
+sink(Y) :- edge(_, Y), not degree(Y, _).
+"""
+
+
+def test_listing_negation_constraint_and_sinks():
+    res = evaluate(NEG_LISTING, _edges([1, 1, 1, 2], [2, 3, 4, 3]),
+                   {"degree": I2, "violation": ("i32",), "sink": ("i32",)})
+    assert _rows(res, "violation") == []
+    assert _rows(res, "sink") == _golden("listing_negation_degree.txt")
+    assert _rows(res, "degree") == _golden("listing_agg_degree.txt")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_negation_set_difference_brute_force(seed):
+    """oneway = E minus the reversed E, and a constant in the negated literal,
+    against Python set algebra over the edge tuples."""
+    rng = np.random.default_rng(seed)
+    n, m = 12, 40
+    src, dst = rng.integers(0, n, m), rng.integers(0, n, m)
+    rules = """
+    oneway(X, Y) :- edge(X, Y), not edge(Y, X).
+    notfrom0(X, Y) :- edge(X, Y), not edge(0, Y).
+    noloop(X) :- edge(X, _), not edge(X, X).
+    """
+    res = evaluate(rules, _edges(src, dst), {"oneway": I2, "notfrom0": I2, "noloop": ("i32",)})
+    E = set(zip(src.tolist(), dst.tolist()))
+    assert _rows(res, "oneway") == sorted((x, y) for x, y in E if (y, x) not in E)
+    assert _rows(res, "notfrom0") == sorted((x, y) for x, y in E if (0, y) not in E)
+    assert _rows(res, "noloop") == sorted({(x,) for x, _ in E if (x, x) not in E})
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_negation_of_a_recursive_relation_vs_bfs(seed):
+    """Pairs (listed as an input relation) that the closure does not contain,
+    against breadth-first search from every node."""
+    rng = np.random.default_rng(seed)
+    n, m = 15, 22
+    src, dst = rng.integers(0, n, m), rng.integers(0, n, m)
+    px, py = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    edb = _edges(src, dst)
+    edb["pair"] = (I2, [px.ravel().astype(np.int32), py.ravel().astype(np.int32)])
+    rules = TC + "unreached(X, Y) :- pair(X, Y), not path(X, Y).\n"
+    res = evaluate(rules, edb, {"path": I2, "unreached": I2})
+    adj = {u: set() for u in range(n)}
+    for u, v in zip(src.tolist(), dst.tolist()):
+        adj[u].add(v)
+    expect = []
+    for x in range(n):
+        seen, todo = set(), list(adj[x])
+        while todo:
+            v = todo.pop()
+            if v not in seen:
+                seen.add(v)
+                todo.extend(adj[v])
+        expect += [(x, y) for y in range(n) if y not in seen]
+    assert _rows(res, "unreached") == sorted(expect)
+    assert len(_rows(res, "unreached")) + len(_rows(res, "path")) == n * n
+
+
+def test_negation_repeated_variable_and_unbound_rejection():
+    res = evaluate("nosym(X) :- node(X), not edge(X, X).",
+                   {**_edges([1, 2, 3], [1, 3, 3]), "node": (("i32",), [np.array([1, 2, 3, 4], np.int32)])},
+                   {"nosym": ("i32",)})
+    assert _rows(res, "nosym") == [(2,), (4,)]
+    with pytest.raises(ValueError):   # Z occurs only under 'not'
+        evaluate("bad(X) :- edge(X, _), not edge(X, Z).", _edges([1], [2]), {"bad": ("i32",)})
+
+
+def test_negation_inside_recursion_is_rejected():
+    with pytest.raises(ValueError):
+        evaluate("p(X) :- edge(X, _), not q(X).\nq(X) :- edge(_, X), not p(X).",
+                 _edges([1, 2], [2, 3]), {"p": ("i32",), "q": ("i32",)})
+    with pytest.raises(ValueError):
+        evaluate("p(X) :- edge(X, _), not p(X).", _edges([1], [2]), {"p": ("i32",)})
+
+
 # ---------------------------------------------------------------- restriction helper
 def test_restriction_matches_full_rows():
     wl = W.small_workloads()["tc_uniform"]()
@@ -374,3 +454,15 @@ def test_planted_mistakes_are_caught(monkeypatch):
     monkeypatch.setattr(D, "_eval_body", transposed_edges)
     with pytest.raises(AssertionError):
         test_tc_chain_closed_form(5)
+    monkeypatch.setattr(D, "_eval_body", real_body)
+
+    real_neg = D._negated_match
+
+    def negation_ignores_second_column(pred, terms, rels, binding, var_types, n):
+        terms = [t if j == 0 else ("anon",) for j, t in enumerate(terms)]
+        return real_neg(pred, terms, rels, binding, var_types, n)
+
+    monkeypatch.setattr(D, "_negated_match", negation_ignores_second_column)
+    with pytest.raises(AssertionError):
+        test_negation_set_difference_brute_force(0)
+    monkeypatch.setattr(D, "_negated_match", real_neg)
