@@ -25,12 +25,25 @@ struct ColAct {
 };
 
 // Micro-ops run after all columns of a stage are bound.
-enum OpKind : uint8_t { OP_CMP = 1, OP_ADD = 2, OP_SUB = 3, OP_MOV = 4 };
+// OP_NOTIN: stratified negation; cmp = the rule's negation table, type = the
+// number of constrained columns (0, 1 or 2), a and b their operands.
+enum OpKind : uint8_t { OP_CMP = 1, OP_ADD = 2, OP_SUB = 3, OP_MOV = 4, OP_NOTIN = 5 };
 enum CmpKind : uint8_t { CMP_NE = 0, CMP_EQ, CMP_LT, CMP_LE, CMP_GT, CMP_GE };
 // Operand encoding: >= 0 is a slot, < 0 is constant index (-1 - k).
 struct MicroOp {
   uint8_t kind, cmp, type, pad;
   int8_t dst, a, b, pad2;
+};
+
+// A negated literal not q(...) over a complete relation q: the sorted keys
+// of q's rows projected onto the literal's constrained columns (variables and
+// constants; none, one, or two int32 columns packed (v0 << 32) | v1 as
+// unsigned), searched per candidate.  With no constrained column the literal
+// only asks whether q has a row (n > 0).
+constexpr int MAXNEG = 2;
+struct NegTable {
+  const unsigned long long* keys;
+  int64_t n;
 };
 
 // Rows that drive a stage: a relation, a delta, or materialized bindings
@@ -144,6 +157,7 @@ struct StageArgs {
   int32_t nops;
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];
+  NegTable neg[MAXNEG];
   EmitSpec emit;
 };
 
@@ -168,6 +182,7 @@ struct DensePullArgs {
   int32_t nops;
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];
+  NegTable neg[MAXNEG];     // unused: rules with negation do not take this form
   const uint32_t* cval;   // current delta: values and presence bits
   const uint32_t* cpres;
   uint32_t* nval;         // next delta: values and presence bits
@@ -206,6 +221,7 @@ struct DenseTileArgs {
   int32_t nops;
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];
+  NegTable neg[MAXNEG];   // unused: rules with negation do not take this form
   uint32_t* vals;         // encoded values (fold_encode), presence bits, delta bits
   uint32_t* pres;
   uint32_t* chg;

@@ -330,6 +330,16 @@ struct DevIndex {
   std::vector<std::unique_ptr<Buf>> owned;
 };
 
+// Sorted keys of a complete relation projected onto the columns a negated
+// literal constrains.
+struct DevNeg {
+  Relation* rel = nullptr;
+  int ncols = 0;
+  int col[2] = {0, 0};
+  Buf keys;
+  int64_t n = 0;
+};
+
 struct HeadRun {
   Relation* rel = nullptr;
   Agg agg = Agg::NONE;
@@ -410,6 +420,7 @@ struct Runner {
   xl_fixpoint_stats* st;
   std::vector<std::unique_ptr<DevIndex>> indexes;
   std::vector<std::unique_ptr<DevIndex>> kept;  // ready indexes made while materializing
+  std::vector<std::unique_ptr<DevNeg>> negtabs;  // negation tables over complete relations
   std::vector<std::unique_ptr<HeadRun>> heads;
   int64_t cands = 0;
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -984,10 +995,46 @@ struct Runner {
     return s;
   }
 
-  void fill_ops(StageArgs& a, const RulePlan& p, int ks) {
+  xl_status fill_ops(StageArgs& a, const RulePlan& p, int ks) {
     a.nops = (int)p.stage_ops[ks].size();
     for (int i = 0; i < a.nops; ++i) a.ops[i] = p.stage_ops[ks][i];
     for (size_t i = 0; i < p.stage_consts[ks].size(); ++i) a.consts[i] = p.stage_consts[ks][i];
+    for (size_t q = 0; q < p.negs.size(); ++q) XL_TRY(get_neg(p.negs[q], &a.neg[q]));
+    return XL_OK;
+  }
+
+  // The negation table of a negated literal over a complete relation (its
+  // stratum ran before; stratification guarantees it): q's rows projected
+  // onto the constrained columns, packed and radix sorted.
+  xl_status get_neg(const NegPlan& np, NegTable* out) {
+    for (auto& t : negtabs)
+      if (t->rel == np.rel && t->ncols == np.ncols && (np.ncols < 1 || t->col[0] == np.col[0]) &&
+          (np.ncols < 2 || t->col[1] == np.col[1])) {
+        *out = NegTable{t->keys.as<unsigned long long>(), t->n};
+        return XL_OK;
+      }
+    if (head_of(np.rel)) return c->fail(XL_DEVICE_ERROR, "negated relation is not complete (internal)");
+    auto t = std::make_unique<DevNeg>();
+    t->rel = np.rel;
+    t->ncols = np.ncols;
+    t->col[0] = np.col[0];
+    t->col[1] = np.col[1];
+    t->n = np.rel->nrows;
+    if (np.ncols > 0 && t->n > 0) {
+      Buf alt, tmp;
+      XL_TRY(dalloc(c, (size_t)t->n * 8, &t->keys, "negation keys"));
+      XL_TRY(dalloc(c, (size_t)t->n * 8, &alt, "negation keys"));
+      XL_TRY(dalloc(c, k::radix_temp_bytes(t->n), &tmp, "sort scratch"));
+      HIP_TRY(c, k::neg_keys(np.rel->col[np.col[0]], np.ncols > 1 ? np.rel->col[np.col[1]] : nullptr, t->n,
+                             t->keys.as<u64>(), c->stream));
+      int alt_used = 0;
+      HIP_TRY(c, k::radix_sort_u64(t->keys.as<u64>(), nullptr, alt.as<u64>(), nullptr, t->n,
+                                   np.ncols > 1 ? 64 : 32, tmp.p, c->stream, &alt_used));
+      if (alt_used) std::swap(t->keys.p, alt.p);
+    }
+    *out = NegTable{t->keys.as<unsigned long long>(), t->n};
+    negtabs.push_back(std::move(t));
+    return XL_OK;
   }
 
   xl_status counted_pass(StageArgs& a, int64_t* total, Buf* offs) {
@@ -1232,7 +1279,7 @@ struct Runner {
     XL_TRY(get_index(sp.rel, sp.key_col, &a.idx));
     a.idx.key_slot = (int8_t)sp.key_slot;
     for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
-    fill_ops(a, p, 0);
+    XL_TRY(fill_ops(a, p, 0));
     a.emit.mode = EM_MARK;
     a.emit.key.nkey = 2;
     a.emit.key.slot[0] = (int8_t)p.key_slot[0];
@@ -1471,7 +1518,7 @@ struct Runner {
         a.idx.key_slot = (int8_t)sp.key_slot;
         for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
       }
-      fill_ops(a, p, ks);
+      XL_TRY(fill_ops(a, p, ks));
       a.emit.counters = c->dcounters;
       if (ks + 1 < nkst) {
         // intermediate: count -> scan -> materialize the live slots

@@ -97,6 +97,7 @@ struct RuleAst {
   Agg agg = Agg::NONE;
   std::string agg_var;
   std::vector<AtomAst> atoms;
+  std::vector<AtomAst> negs;  // literals "not q(...)" (stratified negation)
   struct Assign {
     std::string var;
     std::vector<std::pair<int, Term>> parts;  // (+1 / -1, term)
@@ -111,6 +112,12 @@ struct RuleAst {
 };
 
 // ------------------------------------------------------------------ plans
+struct NegPlan {         // a negated literal: the columns it constrains
+  Relation* rel = nullptr;
+  int ncols = 0;
+  int col[2] = {0, 0};
+};
+
 struct StepPlan {        // index join against a full relation
   Relation* rel = nullptr;
   int key_col = 0;
@@ -125,6 +132,7 @@ struct RulePlan {
   bool driver_delta = false;    // scan the driver's delta instead of all rows
   ColAct driver_act[MAXC] = {};
   std::vector<StepPlan> steps;
+  std::vector<NegPlan> negs;    // negated literals, referenced by OP_NOTIN ops
   // micro-ops executed by kernel stage k (k = max(0, #steps - 1) when no steps)
   std::vector<std::vector<MicroOp>> stage_ops;
   std::vector<std::vector<uint32_t>> stage_consts;

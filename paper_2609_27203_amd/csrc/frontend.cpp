@@ -171,6 +171,9 @@ struct Parser {
     if (t[i].s == ".") return fail("facts are not accepted in rule text; load them as relation rows");
     if (!expect(":-")) return false;
     while (true) {
+      const bool negated = t[i].kind == Tok::NAME && t[i].s == "not" && t[i + 1].kind == Tok::NAME &&
+                           !is_var_name(t[i + 1].s) && t[i + 2].s == "(";
+      if (negated) ++i;
       if (t[i].kind == Tok::NAME && !is_var_name(t[i].s) && t[i + 1].s == "(") {
         AtomAst a;
         a.pred = t[i].s;
@@ -182,7 +185,7 @@ struct Parser {
           if (t[i].s == ")") { ++i; break; }
           if (!expect(",")) return false;
         }
-        r->atoms.push_back(a);
+        (negated ? r->negs : r->atoms).push_back(a);
       } else if (t[i].kind == Tok::NAME && t[i + 1].kind == Tok::NAME && t[i + 1].s == "is") {
         if (!is_var_name(t[i].s) || t[i].s == "_") return fail("the left side of 'is' must be a variable");
         RuleAst::Assign as;
@@ -419,6 +422,52 @@ struct Planner {
       op.type = t1;
       p.stage_ops[ks].push_back(op);
     }
+    // negated literals: a membership test at the first stage where all their
+    // variables are bound
+    if (r.negs.size() > (size_t)MAXNEG)
+      return fail(XL_UNSUPPORTED, "rule '" + r.text + "': at most " + std::to_string(MAXNEG) + " negated literals");
+    for (const AtomAst& a : r.negs) {
+      Relation* rel = ctx->find(a.pred);
+      NegPlan np;
+      np.rel = rel;
+      std::vector<const Term*> used;
+      std::vector<int> cols;
+      for (int j = 0; j < rel->arity; ++j) {
+        const Term& t = a.args[j];
+        if (t.kind == Term::ANON) continue;
+        if (t.kind == Term::VAR) {
+          if (!avail.count(t.name))
+            return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " occurs in 'not " + a.pred +
+                                            "' but in no positive atom or 'is' before it");
+          if (vtype[t.name] != rel->types[j])
+            return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': variable " + t.name + " is used at two column types");
+        } else if (term_type(t) != rel->types[j]) {
+          return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': constant does not match column " + std::to_string(j) + " of " + rel->name);
+        }
+        if (rel->types[j] != T_I32)
+          return fail(XL_UNSUPPORTED, "rule '" + r.text + "': negated literals may constrain int32 columns only");
+        used.push_back(&t);
+        cols.push_back(j);
+      }
+      // (a variable may occur twice: the packed key then asks for a row with
+      // both columns equal to it)
+      if (used.size() > 2)
+        return fail(XL_UNSUPPORTED, "rule '" + r.text + "': 'not " + a.pred + "' constrains more than two columns");
+      np.ncols = (int)used.size();
+      for (int q = 0; q < np.ncols; ++q) np.col[q] = cols[q];
+      const int ks = stage_needed(used);
+      MicroOp op{};
+      op.kind = OP_NOTIN;
+      op.cmp = (uint8_t)p.negs.size();
+      op.type = (uint8_t)np.ncols;
+      op.a = 0;
+      op.b = 0;
+      uint8_t ty;
+      if (np.ncols > 0 && !operand(ks, *used[0], &ty, &op.a)) return false;
+      if (np.ncols > 1 && !operand(ks, *used[1], &ty, &op.b)) return false;
+      p.stage_ops[ks].push_back(op);
+      p.negs.push_back(np);
+    }
     if ((int)slot.size() > MAXV) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': more than 8 variables");
     for (int k = 0; k < nkst; ++k)
       if (p.stage_ops[k].size() > (size_t)MAXOPS) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': too many comparisons/arithmetic terms");
@@ -488,7 +537,7 @@ struct Planner {
       }
     }
     // carried value shape (see RulePlan::carried_val)
-    if (delta && p.driver == p.head && p.head->arity == 3 &&
+    if (delta && p.negs.empty() && p.driver == p.head && p.head->arity == 3 &&
         (r.agg == Agg::SUM || r.agg == Agg::LSE || r.agg == Agg::MIN || r.agg == Agg::MAX) &&
         nst == 1 && p.steps[0].rel != p.head && p.driver_act[0].kind == CA_BIND && p.driver_act[1].kind == CA_BIND &&
         (p.driver_act[2].kind == CA_BIND || p.driver_act[2].kind == CA_NONE) &&
@@ -542,12 +591,13 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
       return bad(XL_UNSUPPORTED, "rule '" + r.text + "': derived relations need one or two key columns");
     for (size_t j = 0; j < r.head_args.size(); ++j)
       if (h->types[j] != T_I32) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': key columns of derived relations must be int32");
-    for (auto& a : r.atoms) {
-      Relation* rel = ctx->find(a.pred);
-      if (!rel) return bad(XL_INVALID_ARGUMENT, "relation '" + a.pred + "' is not declared");
-      if ((int)a.args.size() != rel->arity)
-        return bad(XL_INVALID_ARGUMENT, "rule '" + r.text + "': " + a.pred + " used with " + std::to_string(a.args.size()) + " arguments but has arity " + std::to_string(rel->arity));
-    }
+    for (const auto* list : {&r.atoms, &r.negs})
+      for (auto& a : *list) {
+        Relation* rel = ctx->find(a.pred);
+        if (!rel) return bad(XL_INVALID_ARGUMENT, "relation '" + a.pred + "' is not declared");
+        if ((int)a.args.size() != rel->arity)
+          return bad(XL_INVALID_ARGUMENT, "rule '" + r.text + "': " + a.pred + " used with " + std::to_string(a.args.size()) + " arguments but has arity " + std::to_string(rel->arity));
+      }
     if (r.atoms.empty()) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': a rule needs at least one body atom");
     bool found = false;
     for (auto& hi : prog->heads)
@@ -565,11 +615,20 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
     return -1;
   };
   std::vector<std::set<int>> deps(nh);
-  for (auto& r : prog->rules)
+  std::vector<std::pair<int, int>> negdeps;  // (head, relation under 'not')
+  for (auto& r : prog->rules) {
     for (auto& a : r.atoms) {
       int d = hid(ctx->find(a.pred));
       if (d >= 0) deps[hid(ctx->find(r.head))].insert(d);
     }
+    for (auto& a : r.negs) {
+      int d = hid(ctx->find(a.pred));
+      if (d >= 0) {
+        deps[hid(ctx->find(r.head))].insert(d);
+        negdeps.push_back({hid(ctx->find(r.head)), d});
+      }
+    }
+  }
   std::vector<int> index(nh, -1), low(nh, 0), stack;
   std::vector<bool> on(nh, false);
   std::vector<std::vector<int>> comps;
@@ -600,6 +659,18 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
   };
   for (int v = 0; v < nh; ++v)
     if (index[v] < 0) visit(v);
+  // negation is stratified: the negated relation must be complete, i.e. in an
+  // earlier component than the rule's head (Sec. 2: negative dependency edges)
+  {
+    std::vector<int> comp_of(nh, -1);
+    for (size_t k = 0; k < comps.size(); ++k)
+      for (int v : comps[k]) comp_of[v] = (int)k;
+    for (auto& nd : negdeps)
+      if (comp_of[nd.first] == comp_of[nd.second])
+        return bad(XL_UNSUPPORTED, "relation " + prog->heads[nd.first].rel->name + " depends negatively on " +
+                                       prog->heads[nd.second].rel->name + " inside one recursive component "
+                                       "(negation must be stratified)");
+  }
   // Tarjan emits components after everything they depend on.
   Planner pl{ctx};
   for (auto& c : comps) {
@@ -677,6 +748,11 @@ std::string explain_program(const Program* p) {
           const StepPlan& sp = rp.steps[k];
           os << " -> join " << sp.rel->name << " on col " << sp.key_col << "=v" << sp.key_slot << " ("
              << acts(sp.act, sp.rel->arity) << ")";
+        }
+        for (const NegPlan& np : rp.negs) {
+          os << " -> not " << np.rel->name << "(cols";
+          for (int q = 0; q < np.ncols; ++q) os << " " << np.col[q];
+          os << ")";
         }
         int nops = 0;
         for (auto& v : rp.stage_ops) nops += (int)v.size();

@@ -49,6 +49,8 @@ hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const
                              uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s);
 // out[k] = col[off[k]] for keys k in [0, range) with rows, 0xffffffff otherwise.
 hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s);
+// Packed keys of a negation table: c0[i], or (c0[i] << 32) | c1[i].
+hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s);
 // flag[i] = 1 if row i differs (bitwise) from row i-1 in any column (or i == 0).
 hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
                             hipStream_t s);

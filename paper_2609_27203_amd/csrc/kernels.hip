@@ -369,6 +369,18 @@ hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t rang
   return hipGetLastError();
 }
 
+// key[i] = c0[i] (c1 null) or (c0[i] << 32) | c1[i], as unsigned.
+__global__ void neg_keys_k(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    key[i] = c1 ? ((u64)c0[i] << 32) | c1[i] : (u64)c0[i];
+}
+hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  neg_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(c0, c1, n, key);
+  return hipGetLastError();
+}
+
 struct ColPtrs { const uint32_t* c[MAXC]; };
 
 __global__ void row_change_k(ColPtrs cols, int ncols, int64_t n, uint32_t* flag) {
@@ -918,6 +930,20 @@ __device__ __forceinline__ bool compare(int cmp, int type, uint32_t x, uint32_t 
   }
 }
 
+// Stratified negation: does the negated relation have a row whose
+// constrained columns equal (x[, y])?  Binary search of the sorted keys.
+__device__ __forceinline__ bool neg_member(const NegTable t, int ncols, uint32_t x, uint32_t y) {
+  if (ncols == 0) return t.n > 0;
+  const u64 k = ncols == 1 ? (u64)x : ((u64)x << 32) | y;
+  int64_t lo = 0, hi = t.n;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (t.keys[mid] < k) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo < t.n && t.keys[lo] == k;
+}
+
 template <class A>
 __device__ __forceinline__ bool run_ops(A& a, Regs& u) {
   bool ok = true;
@@ -928,6 +954,9 @@ __device__ __forceinline__ bool run_ops(A& a, Regs& u) {
     const uint32_t x = operand(a, u, op.a);
     if (op.kind == OP_CMP) {
       ok = ok && compare(op.cmp, op.type, x, operand(a, u, op.b));
+    } else if (op.kind == OP_NOTIN) {
+      const NegTable t = {a.neg[op.cmp].keys, a.neg[op.cmp].n};
+      ok = ok && !neg_member(t, op.type, x, op.type > 1 ? operand(a, u, op.b) : 0u);
     } else if (op.kind == OP_MOV) {
       setv(u, op.dst, x);
     } else {

@@ -102,6 +102,71 @@ def test_closure_push_and_pull_directions(name, pull_ratio, resident):
     assert stats["front_new"] == len(ref.relations["path"][1][0]) - stats["delta_rows"][0]
 
 
+# ------------------------------------------------------------- stratified negation
+NEG_RULES = W.TC_RULES + """
+blocked(X) :- edge(X, X).
+oneway(X, Y) :- edge(X, Y), not edge(Y, X).
+notfrom0(X, Y) :- edge(X, Y), not edge(0, Y).
+noloop(X) :- edge(X, _), not edge(X, X).
+unreached(X, Y) :- pair(X, Y), not path(X, Y).
+safe(X, Y) :- edge(X, Y), not blocked(Y).
+safe(X, Y) :- safe(X, Z), edge(Z, Y), not blocked(Y), not blocked(Z).
+sink(Y) :- edge(_, Y), not edge(Y, _).
+"""
+NEG_IDB = {"path": ("i32", "i32"), "blocked": ("i32",), "oneway": ("i32", "i32"),
+           "notfrom0": ("i32", "i32"), "noloop": ("i32",), "unreached": ("i32", "i32"),
+           "safe": ("i32", "i32"), "sink": ("i32",)}
+
+
+def test_listing_negation_degree():
+    """The paper's aggregation listing with its integrity constraint written as
+    a rule (no violations) and the sinks it implies (golden file)."""
+    wl = W.Workload("neg_listing", """
+degree(X, count(Y)) :- edge(X, Y).
+violation(X) :- edge(X, _), not degree(X, _).
+sink(Y) :- edge(_, Y), not degree(Y, _).
+""", _edges([1, 1, 1, 2], [2, 3, 4, 3]), {"degree": ("i32", "i32"), "violation": ("i32",), "sink": ("i32",)})
+    print("case: negation listing", flush=True)
+    rels, _, _ = engine_run(wl, workspace_bytes=256 << 20)
+    assert len(rels["violation"][0]) == 0
+    assert np.array_equal(rels["sink"][0], _golden("listing_negation_degree.txt")[0])
+
+
+_NEG_REF = {}
+
+
+def _negation_case(n, m, seed):
+    """Random edges plus three self-loops (so 'blocked' is never empty) and
+    all pairs over the first min(n, 60) nodes; the oracle's result is kept
+    for the second index mode."""
+    if (n, m, seed) not in _NEG_REF:
+        rng = np.random.default_rng(seed)
+        src = np.concatenate([rng.integers(0, n, m), [5, 17, 33]])
+        dst = np.concatenate([rng.integers(0, n, m), [5, 17, 33]])
+        keep = np.unique(src * n + dst)
+        src, dst = (keep // n).astype(np.int32), (keep % n).astype(np.int32)
+        edb = _edges(src, dst)
+        k = min(n, 60)
+        px, py = np.meshgrid(np.arange(k), np.arange(k), indexing="ij")
+        edb["pair"] = (("i32", "i32"), [px.ravel().astype(np.int32), py.ravel().astype(np.int32)])
+        wl = W.Workload("negation", NEG_RULES, edb, NEG_IDB)
+        _NEG_REF[(n, m, seed)] = (wl, evaluate(wl.rules, wl.edb, wl.idb))
+    return _NEG_REF[(n, m, seed)]
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+@pytest.mark.parametrize("n,m,seed", [(40, 90, 0), (300, 1500, 1), (700, 1000, 2)])
+def test_negation_matches_oracle(n, m, seed, index_mode):
+    """Set difference against an EDB relation (with a constant, a repeated
+    variable, '_' columns), against a closure from an earlier stratum, and
+    inside a recursive rule, in both head representations."""
+    print(f"case: negation n={n} m={m} seed={seed} index_mode={index_mode}", flush=True)
+    wl, ref = _negation_case(n, m, seed)
+    rels, _, _ = engine_run(wl, options={"index_mode": index_mode})
+    _compare(wl, rels, ref)
+    assert sum(len(r[1][0]) for r in ref.relations.values()) > 0
+
+
 COUNT_SHAPES_RULES = W.TC_RULES + """
 out_count(X,count(Y)) :- path(X,Y).
 in_count(Y,count(X)) :- path(X,Y).

@@ -56,6 +56,21 @@ I2 = ("i32", "i32")
 W3 = ("i32", "i32", "f32")
 
 
+def test_negated_literals_are_planned_as_membership_tests():
+    """A negated literal over a relation of an earlier stratum is a membership
+    test on the constrained columns, after the atoms that bind them; a rule
+    with one is not run in the grouped closure form."""
+    c = _ctx({"e": I2, "b": ("i32",), "p": I2})
+    plan = c.compile("b(X) :- e(X,X).\np(X,Y) :- e(X,Y), not b(Y).\n"
+                     "p(X,Y) :- p(X,Z), e(Z,Y), not b(Y), not e(Y, 0).").explain()
+    lines = plan.splitlines()
+    assert lines[0].startswith("stratum 0") and "b[set]" in lines[0]
+    assert any("-> not b(cols 0)" in ln and "seed" in ln for ln in lines)
+    delta = [ln for ln in lines if ln.startswith("  delta rule")]
+    assert len(delta) == 1 and "-> not b(cols 0) -> not e(cols 0 1)" in delta[0]
+    assert "grouped" not in delta[0]
+
+
 def test_self_join_gets_one_delta_variant_per_recursive_atom():
     """Alg. 1: a rule with two recursive atoms has two delta variants, each
     scanning the delta at one atom and joining the full relation at the other."""
@@ -87,6 +102,19 @@ def test_self_join_gets_one_delta_variant_per_recursive_atom():
     ({"e": I2, "p": I2}, "p(X,Z) :- e(X,Y).", "XL_UNSUPPORTED"),
     ({"e": I2, "p": I2, "m": ("i32", "i32", "i32")},
      "m(X,Y,min(Y)) :- e(X,Y).\nm(X,Y,max(Y)) :- e(Y,X).", "XL_UNSUPPORTED"),
+    # stratified negation: no negative edge inside a recursive component, every
+    # variable of a negated literal bound positively, int32 columns, at most
+    # two constrained columns and two negated literals per rule
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not p(X).", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": ("i32",), "q": ("i32",)}, "p(X) :- e(X,_), not q(X).\nq(X) :- e(_,X), not p(X).",
+     "XL_UNSUPPORTED"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not e(X,Z).", "XL_UNSUPPORTED"),
+    ({"w": W3, "p": ("i32",)}, "p(X) :- w(X,_,W), not w(X,_,W).", "XL_UNSUPPORTED"),
+    ({"t": ("i32", "i32", "i32"), "p": ("i32",)}, "p(X) :- t(X,Y,Z), not t(Z,Y,X).", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,Y), not e(Y,X), not e(X,X), not e(Y,Y).", "XL_UNSUPPORTED"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not nope(X).", "XL_INVALID_ARGUMENT"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not e(X).", "XL_INVALID_ARGUMENT"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not e(X, 1.5).", "XL_TYPE_MISMATCH"),
 ])
 def test_rejected_programs(rels, text, status):
     c = _ctx(rels)
