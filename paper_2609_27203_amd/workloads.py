@@ -43,6 +43,10 @@ score(S,Y,logsumexp(P)) :- source(S), edge(S,Y,P).
 score(S,Y,logsumexp(P)) :- score(S,Z,P1), edge(Z,Y,W), P is P1 + W.
 """
 
+TRIANGLE_RULES = """
+tri(X,Y,Z) :- r(X,Y), s(Y,Z), t(X,Z).
+"""
+
 SG_RULES = """
 sg(X,Y) :- parent(X,P), parent(Y,P), X != Y.
 sg(X,Y) :- parent(X,A), sg(A,B), parent(Y,B).
@@ -269,6 +273,75 @@ def tc_rmat(scale: int = 14, n_edges: int = 1 << 18, seed: int = 5,
 
 
 # The five full-size workloads, in the order they are listed for this engine.
+def _distinct_pairs(fixed, parts, rng):
+    """Distinct (a, b) pairs: the fixed pairs first, then for each (count,
+    draw) of parts, drawn pairs not seen before until count of them are
+    added (draw(rng, k) returns k candidate pairs)."""
+    seen = set(zip(fixed[0].tolist(), fixed[1].tolist()))
+    out_a, out_b = [fixed[0].tolist()], [fixed[1].tolist()]
+    for count, draw in parts:
+        added = 0
+        while added < count:
+            a, b = draw(rng, 2 * (count - added) + 16)
+            for u, v in zip(a.tolist(), b.tolist()):
+                if (u, v) not in seen:
+                    seen.add((u, v))
+                    out_a[0].append(u)
+                    out_b[0].append(v)
+                    added += 1
+                    if added == count:
+                        break
+    return np.array(out_a[0], np.int32), np.array(out_b[0], np.int32)
+
+
+def triangle(rows: int = 1 << 16, core: int = 161, hubs: int = 8, seed: int = 6,
+             core_frac: float = 0.4, hub_frac: float = 0.3) -> Workload:
+    """Three-way triangle join tri(X,Y,Z) :- r(X,Y), s(Y,Z), t(X,Z) over three
+    relations of `rows` distinct pairs each, shaped so that every join
+    variable has a small hot domain.
+
+    The paper's fixture (three relations of 65,536 rows, about 4.19 M output
+    triples, hot domains that make a binary-join plan's intermediate far
+    larger than the result; Sec. 10, WCOJ ablation) is not available; this
+    stands in for it.  Values 0..core-1 form a hot core: each relation holds
+    min(core_frac * rows, core^2) distinct core x core pairs drawn without
+    replacement (all of them at the defaults, which alone close
+    161^3 = 4,173,281 triangles).  Values core..core+hubs-1 are hubs:
+    hub_frac of r's rows pair a cold X with a hub Y and hub_frac of s's rows
+    pair a hub Y with a cold Z, so r joined with s on Y is large while t,
+    which holds no hub rows, closes few of those pairs.  The remaining rows
+    are uniform over the cold values [core + hubs, rows).
+    """
+    rng = _rng(seed)
+    lo_cold = core + hubs
+    n_core = min(int(round(core_frac * rows)), core * core)
+    n_hub = int(round(hub_frac * rows))
+    if n_core + n_hub > rows or lo_cold >= rows:
+        raise ValueError("triangle: core and hub rows exceed the relation size")
+
+    def core_pairs():
+        k = rng.choice(core * core, n_core, replace=False)
+        return k // core, k % core
+
+    def cold_pairs(g, k):
+        return g.integers(lo_cold, rows, k), g.integers(lo_cold, rows, k)
+
+    def cold_hub(g, k):
+        return g.integers(lo_cold, rows, k), g.integers(core, lo_cold, k)
+
+    def hub_cold(g, k):
+        return g.integers(core, lo_cold, k), g.integers(lo_cold, rows, k)
+
+    r = _distinct_pairs(core_pairs(), [(n_hub, cold_hub), (rows - n_core - n_hub, cold_pairs)], rng)
+    s_ = _distinct_pairs(core_pairs(), [(n_hub, hub_cold), (rows - n_core - n_hub, cold_pairs)], rng)
+    t = _distinct_pairs(core_pairs(), [(rows - n_core, cold_pairs)], rng)
+    i2 = ("i32", "i32")
+    return Workload("triangle", TRIANGLE_RULES,
+                    {"r": (i2, list(r)), "s": (i2, list(s_)), "t": (i2, list(t))},
+                    {"tri": ("i32", "i32", "i32")},
+                    {"rows": rows, "core": core, "hubs": hubs, "seed": seed})
+
+
 def full_workloads():
     return {
         "tc_uniform": tc_uniform,

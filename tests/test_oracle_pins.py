@@ -405,6 +405,55 @@ def test_negation_inside_recursion_is_rejected():
         evaluate("p(X) :- edge(X, _), not p(X).", _edges([1], [2]), {"p": ("i32",)})
 
 
+# ---------------------------------------------------------------- triangle join
+TRI3 = ("i32", "i32", "i32")
+
+
+def _tri_edb(r, s, t):
+    def rel(p):
+        p = np.asarray(p, np.int64).reshape(-1, 2)
+        return (I2, [p[:, 0].astype(np.int32), p[:, 1].astype(np.int32)])
+    return {"r": rel(r), "s": rel(s), "t": rel(t)}
+
+
+@pytest.mark.parametrize("a,b,c", [(1, 1, 1), (2, 3, 4), (5, 1, 7), (6, 6, 6)])
+def test_triangle_complete_tripartite_closed_form(a, b, c):
+    """r = A x B, s = B x C, t = A x C with disjoint value ranges: every
+    (x, y, z) in A x B x C is a triangle, a*b*c of them."""
+    A, B, C = range(0, a), range(100, 100 + b), range(200, 200 + c)
+    res = evaluate(W.TRIANGLE_RULES, _tri_edb([(x, y) for x in A for y in B], [(y, z) for y in B for z in C],
+                                              [(x, z) for x in A for z in C]), {"tri": TRI3})
+    assert _rows(res, "tri") == [(x, y, z) for x in A for y in B for z in C]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_triangle_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    r, s_, t = (rng.integers(0, 7, (25, 2)) for _ in range(3))
+    res = evaluate(W.TRIANGLE_RULES, _tri_edb(r, s_, t), {"tri": TRI3})
+    R, S, T = (set(map(tuple, m.tolist())) for m in (r, s_, t))
+    expect = sorted({(x, y, z) for (x, y) in R for (y2, z) in S if y2 == y for (x2, z2) in T
+                     if x2 == x and z2 == z})
+    assert _rows(res, "tri") == expect
+    assert len(expect) > 0
+
+
+def test_triangle_small_workload_vs_set_intersection():
+    """Per r row (x, y): the z values in s[y] intersected with t[x]."""
+    wl = W.triangle(rows=4096, core=40, hubs=4, seed=16)
+    res = evaluate(wl.rules, wl.edb, wl.idb)
+    (r0, r1), (s0, s1), (t0, t1) = [wl.edb[k][1] for k in "rst"]
+    S, T = {}, {}
+    for y, z in zip(s0.tolist(), s1.tolist()):
+        S.setdefault(y, set()).add(z)
+    for x, z in zip(t0.tolist(), t1.tolist()):
+        T.setdefault(x, set()).add(z)
+    expect = sorted((x, y, z) for x, y in zip(r0.tolist(), r1.tolist())
+                    for z in S.get(y, set()) & T.get(x, set()))
+    assert _rows(res, "tri") == expect
+    assert len(expect) == 64057
+
+
 # ---------------------------------------------------------------- restriction helper
 def test_restriction_matches_full_rows():
     wl = W.small_workloads()["tc_uniform"]()
@@ -466,3 +515,15 @@ def test_planted_mistakes_are_caught(monkeypatch):
     with pytest.raises(AssertionError):
         test_negation_set_difference_brute_force(0)
     monkeypatch.setattr(D, "_negated_match", real_neg)
+
+    def transposed_t(rule, rels, var_types):   # joins t on its columns swapped
+        rels = dict(rels)
+        if "t" in rels:
+            ty, c = rels["t"]
+            rels["t"] = (ty, [c[1], c[0]])
+        return real_body(rule, rels, var_types)
+
+    monkeypatch.setattr(D, "_eval_body", transposed_t)
+    with pytest.raises(AssertionError):
+        test_triangle_brute_force(0)
+    monkeypatch.setattr(D, "_eval_body", real_body)
