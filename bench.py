@@ -32,6 +32,8 @@ DESCRIPTIONS = {
                "256 sources, seed 3)",
     "same_generation": "same generation over a 20,000-node forest (seed 4)",
     "tc_rmat_count": "R-MAT transitive closure + reach_count (2^14 nodes, 2^18 edges, seed 5)",
+    "triangle": "three-way triangle join tri(X,Y,Z) :- r(X,Y), s(Y,Z), t(X,Z), three relations of 65,536 rows "
+                "with a 161-value hot core and 8 hubs (seed 6)",
 }
 
 
@@ -40,6 +42,7 @@ KERNELS = {
              "expand or in-edge pull + membership test + merge)",
     "emit": "stage_k / dense_min_tile_k (fused delta expand + probe + fold into the head)",
     "pull": "dense_pull_k (segmented fold of each marked key's in-edges against the delta)",
+    "wcoj": "wcoj_probe_k (count and materialize passes: each driver row's shorter Z list probed into the longer)",
 }
 
 # Algorithmic bytes per unit of work (candidates, new tuples), counting only
@@ -50,13 +53,17 @@ KERNELS = {
 #     delta row written (8 B) and read again by the next round (8 B);
 #   value heads (min / logsumexp): per candidate the edge's endpoint and
 #     weight (8 B) and a key + value probe (12 B); per new or improved key
-#     24 B as above.
+#     24 B as above;
+#   triangle join: per probe the probed Z value (4 B) and one membership
+#     test in the other list (4 B); per output triple its three columns
+#     written (12 B).
 BYTES_PER_UNIT = {
     "tc_uniform": (12.0, 24.0),
     "tc_rmat_count": (12.0, 24.0),
     "same_generation": (12.0, 24.0),
     "sssp": (20.0, 24.0),
     "lse_dag": (20.0, 24.0),
+    "triangle": (8.0, 12.0),
 }
 
 

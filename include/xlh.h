@@ -122,6 +122,12 @@ typedef struct {
     int64_t pull_launches;
     int64_t pull_candidates;    /* in-edges scanned */
     int64_t pull_new;           /* keys whose value was added or changed */
+    /* Worst-case-optimal triangle joins: the probe passes (count and
+     * materialize), timed the same way. */
+    double wcoj_ms;
+    int64_t wcoj_launches;
+    int64_t wcoj_candidates;    /* probes: per driver row, the shorter list's length */
+    int64_t wcoj_new;           /* triples produced */
 } xl_fixpoint_stats;
 
 /*

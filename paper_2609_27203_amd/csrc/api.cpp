@@ -74,6 +74,11 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     c->pull_ratio = (int)value;
     return XL_OK;
   }
+  if (!strcmp(key, "wcoj_shorter")) {
+    if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "wcoj_shorter must be 0 or 1");
+    c->wcoj_shorter = (int)value;
+    return XL_OK;
+  }
   if (!strcmp(key, "frontier_resident")) {
     if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "frontier_resident must be 0 or 1");
     c->frontier_resident = (int)value;

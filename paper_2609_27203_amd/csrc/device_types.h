@@ -248,7 +248,7 @@ struct FrontierArgs {
   uint32_t* out_diff;
   unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED (= new tuples)
   // Pull direction: e indexed by the Y column; Z is rev.col[rev_zcol], the
-  // rows of one Y ordered by the number of in-edges of their Z, most first;
+  // rows of one Y ordered by the out-degree of their Z, most first;
   // rev_first[y - rev.key_lo] is the Z of Y's first row.  A workgroup pulls
   // when pull_ratio * |delta(x)| >= |unreached Y with an in-edge| (pull_ratio
   // 0: always push).
@@ -271,6 +271,35 @@ struct FrontierArgs {
   uint32_t max_rounds;
   const uint32_t* hasin;    // bit (y - lo1): y has at least one in-edge
   uint32_t pull_ratio;
+};
+
+// Worst-case-optimal triangle join (count -> scan -> materialize).  Driver
+// rows (x, y) come from a's index in (X, Y) order; b is indexed by its Y
+// column and c by its X column, each with the rows of one key sorted by the
+// Z value.  Work item k of driver row i (items of row crow[q] are
+// [cofs[q], cofs[q + 1])) probes the k-th Z value of the shorter of b(y) and
+// c(x) into the longer one by binary search; a hit is the triple (x, y, z).
+// A wavefront handles WC_CHUNK consecutive items; items, and so the output,
+// follow (row, k) order, which is ascending (x, y, z).
+struct WcojArgs {
+  const uint32_t* ax;       // [na] X of driver row i (a's index order)
+  const uint32_t* ay;       // [na] Y of driver row i
+  int64_t na;
+  IndexProbe ib;            // b by its Y column
+  const uint32_t* bz;       // b's Z column in ib's row order
+  IndexProbe ic;            // c by its X column
+  const uint32_t* cz;       // c's Z column in ic's row order
+  int32_t probe_shorter;    // 1: probe the shorter list; 0: always b's (the binary-join order)
+  uint32_t* work;           // [na] items of row i (work pass)
+  const uint32_t* crow;     // [nz] driver rows with items, ascending
+  const unsigned long long* cofs;  // [nz + 1] first item of each such row
+  int64_t nz;
+  unsigned long long items;
+  uint32_t* chunk_cnt;      // count pass: hits per chunk
+  const uint32_t* chunk_off;  // materialize pass: first output row per chunk
+  uint32_t* out0;           // materialize pass: X, Y, Z columns
+  uint32_t* out1;
+  uint32_t* out2;
 };
 
 }  // namespace xlh

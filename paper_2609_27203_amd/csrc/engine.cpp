@@ -324,7 +324,8 @@ struct Interval {
 struct DevIndex {
   Relation* rel = nullptr;
   int col = 0;
-  int order_col = -1;  // >= 0: rows of one key ordered by the degree of this column's value
+  int order_col = -1;  // >= 0: rows of one key ordered by this column (see order_kind)
+  int order_kind = 0;  // 0: by the degree of the value, most first; 1: by the int32 value
   uint32_t* first = nullptr;  // with order_col: order_col value of each key's first row
   IndexProbe probe{};
   std::vector<std::unique_ptr<Buf>> owned;
@@ -442,15 +443,19 @@ struct Runner {
 
   // ------------------------------------------------------------ indexes
   // Index of rel by column col.  With order_col >= 0 the rows of each key are
-  // further ordered by how many rows have the order_col value as their key,
-  // most first; the frontier pull scans in-edges in that order, so that edges
-  // from well-connected sources, the likeliest to be in a delta, come first.
+  // further ordered: order_kind 0 by how many rows of rel have the order_col
+  // value in column order_col (its out-degree when rel is an edge relation
+  // indexed by its target), most first -- the frontier pull scans in-edges
+  // in that order, so that edges from well-connected sources, the likeliest
+  // to be in a delta, come first; order_kind 1 by the int32 value itself
+  // (the triangle join intersects sorted lists).
   // first (when given, with order_col >= 0) receives an array holding, per
   // key, the order_col value of the key's first row.
   xl_status get_index(Relation* rel, int col, IndexProbe* out, int order_col = -1,
-                      const uint32_t** first = nullptr) {
+                      const uint32_t** first = nullptr, int order_kind = 0) {
     for (auto& ix : indexes)
-      if (ix->rel == rel && ix->col == col && ix->order_col == order_col) {
+      if (ix->rel == rel && ix->col == col && ix->order_col == order_col &&
+          (order_col < 0 || ix->order_kind == order_kind)) {
         *out = ix->probe;
         if (first) *first = ix->first;
         return XL_OK;
@@ -459,6 +464,7 @@ struct Runner {
     ix->rel = rel;
     ix->col = col;
     ix->order_col = order_col;
+    ix->order_kind = order_kind;
     IndexProbe& p = ix->probe;
     p.ncols = rel->arity;
     auto own = [&](size_t bytes, const char* what, void** ptr) -> xl_status {
@@ -541,34 +547,48 @@ struct Runner {
       if (range > ((int64_t)1 << 30))
         return c->fail(XL_UNSUPPORTED, "key range of " + rel->name + " column " + std::to_string(col) +
                                            " exceeds 2^30 values");
-      Buf keys, keys2, perm, perm2, tmp;
+      const bool ordered = order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32;
+      const int kbits = std::max(1, bitlen((uint64_t)range - 1));
+      Buf keys, perm, perm2, tmp;
       XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
-      XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
       XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));
       XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
       XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
       HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
       HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
-      int alt = 0;
-      HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(),
-                                   perm2.as<uint32_t>(), n, std::max(1, bitlen((uint64_t)range - 1)),
-                                   tmp.p, c->stream, &alt));
-      uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
-      uint32_t* sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
       void* off;
       XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
-      HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
-      if (order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32) {
+      uint32_t* sp = nullptr;
+      if (ordered) {
+        // one sort by (key, order value); the offsets come from the sorted
+        // keys.  Degree order reads each order value's degree from the plain
+        // index of rel by the order column (its row count as a key there).
+        IndexProbe dz{};
+        if (order_kind == 0) XL_TRY(get_index(rel, order_col, &dz));
         Buf k64, k64b;
         XL_TRY(dalloc(c, (size_t)n * 8, &k64, "index order keys"));
         XL_TRY(dalloc(c, (size_t)n * 8, &k64b, "index order keys"));
-        uint32_t* sp_alt = alt ? perm.as<uint32_t>() : perm2.as<uint32_t>();
-        HIP_TRY(c, k::degree_order_keys(sk, sp, rcol[order_col], klo, (uint32_t)range, (const uint32_t*)off, n,
-                                        k64.as<u64>(), c->stream));
-        int alt2 = 0;
-        HIP_TRY(c, k::radix_sort_u64(k64.as<u64>(), sp, k64b.as<u64>(), sp_alt, n,
-                                     16 + std::max(1, bitlen((uint64_t)range - 1)), tmp.p, c->stream, &alt2));
-        if (alt2) sp = sp_alt;
+        if (order_kind == 1)
+          HIP_TRY(c, k::value_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], n, k64.as<u64>(), c->stream));
+        else
+          HIP_TRY(c, k::degree_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], dz.key_lo, dz.key_range,
+                                          dz.off, n, k64.as<u64>(), c->stream));
+        const int obits = order_kind == 1 ? 32 : 16;
+        int alt = 0;
+        HIP_TRY(c, k::radix_sort_u64(k64.as<u64>(), perm.as<uint32_t>(), k64b.as<u64>(), perm2.as<uint32_t>(), n,
+                                     obits + kbits, tmp.p, c->stream, &alt));
+        sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+        HIP_TRY(c, k::high_bits(alt ? k64b.as<u64>() : k64.as<u64>(), obits, n, keys.as<uint32_t>(), c->stream));
+        HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)range, (uint32_t*)off, c->stream));
+      } else {
+        Buf keys2;
+        XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
+        int alt = 0;
+        HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(),
+                                     perm2.as<uint32_t>(), n, kbits, tmp.p, c->stream, &alt));
+        const uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
+        sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+        HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
       }
       for (int j = 0; j < rel->arity; ++j) {
         void* cj;
@@ -576,7 +596,7 @@ struct Runner {
         HIP_TRY(c, k::gather_u32(rcol[j], sp, (uint32_t*)cj, n, c->stream));
         p.col[j] = (uint32_t*)cj;
       }
-      if (order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32) {
+      if (ordered && order_kind == 0) {
         void* fp;
         XL_TRY(own((size_t)range * 4, "index first rows", &fp));
         HIP_TRY(c, k::segment_first((const uint32_t*)off, p.col[order_col], (uint32_t)range, (uint32_t*)fp,
@@ -2084,7 +2104,114 @@ struct Runner {
   }
 
   // ------------------------------------------------------------ strata
+  // A triangle-join stratum (see RulePlan::wcoj): count -> scan ->
+  // materialize straight into the head's columns, in ascending (X, Y, Z)
+  // order; no hash table or bitmap is needed because every (driver row, Z)
+  // pair is produced once.
+  xl_status run_wcoj(const RulePlan& p) {
+    Relation* h = p.head;
+    relation_free_storage(h);
+    WcojArgs a{};
+    IndexProbe ia{};
+    XL_TRY(get_index(p.driver, p.tri_a[0], &ia, p.tri_a[1], nullptr, 1));
+    XL_TRY(get_index(p.tri_brel, p.tri_b[0], &a.ib, p.tri_b[1], nullptr, 1));
+    XL_TRY(get_index(p.tri_crel, p.tri_c[0], &a.ic, p.tri_c[1], nullptr, 1));
+    a.ax = ia.col[p.tri_a[0]];
+    a.ay = ia.col[p.tri_a[1]];
+    a.na = p.driver->nrows;
+    a.bz = a.ib.col[p.tri_b[1]];
+    a.cz = a.ic.col[p.tri_c[1]];
+    a.probe_shorter = c->wcoj_shorter;
+    auto finish = [&](int64_t n) -> xl_status {
+      h->nrows = n;
+      h->lo[0] = p.driver->lo[p.tri_a[0]];
+      h->hi[0] = p.driver->hi[p.tri_a[0]];
+      h->lo[1] = p.driver->lo[p.tri_a[1]];
+      h->hi[1] = p.driver->hi[p.tri_a[1]];
+      h->lo[2] = p.tri_brel->lo[p.tri_b[1]];
+      h->hi[2] = p.tri_brel->hi[p.tri_b[1]];
+      record(n);
+      st->new_tuples_total += n;
+      return XL_OK;
+    };
+    if (a.na == 0 || p.tri_brel->nrows == 0 || p.tri_crel->nrows == 0) return finish(0);
+    Buf work, flag_pos, crow, cw, cofs, tmp, tot;
+    XL_TRY(dalloc(c, (size_t)a.na * 4, &work, "triangle work"));
+    XL_TRY(dalloc(c, (size_t)a.na * 4, &flag_pos, "triangle row positions"));
+    XL_TRY(dalloc(c, std::max(k::scan_temp_bytes(a.na), k::scan_temp_bytes(a.na + 1)), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, 16, &tot, "count"));
+    a.work = work.as<uint32_t>();
+    HIP_TRY(c, k::wcoj_work(a, c->stream));
+    HIP_TRY(c, k::nonzero_flags(work.as<uint32_t>(), a.na, flag_pos.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(flag_pos.as<uint32_t>(), flag_pos.as<uint32_t>(), a.na, tot.as<uint32_t>(), tmp.p,
+                                     c->stream));
+    uint32_t nz = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &nz));
+    if (nz == 0) return finish(0);
+    XL_TRY(dalloc(c, (size_t)nz * 4, &crow, "triangle rows"));
+    XL_TRY(dalloc(c, (size_t)(nz + 1) * 8, &cw, "triangle row work"));
+    XL_TRY(dalloc(c, (size_t)(nz + 1) * 8, &cofs, "triangle row offsets"));
+    HIP_TRY(c, k::wcoj_compact(work.as<uint32_t>(), flag_pos.as<uint32_t>(), a.na, crow.as<uint32_t>(),
+                               cw.as<unsigned long long>(), c->stream));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(nz), &tmp, "scan scratch"));
+    HIP_TRY(c, k::scan_exclusive_u64(cw.as<u64>(), cofs.as<u64>(), nz, cofs.as<u64>() + nz, tmp.p, c->stream));
+    u64 items = 0;
+    XL_TRY(ctl_read(c, cofs.as<u64>() + nz, 8, &items));
+    if (items >= ((u64)1 << 40)) return c->fail(XL_UNSUPPORTED, "triangle join with more than 2^40 probes");
+    a.crow = crow.as<uint32_t>();
+    a.cofs = cofs.as<unsigned long long>();
+    a.nz = nz;
+    a.items = items;
+    const u64 nchunks = (items + k::WC_CHUNK - 1) / k::WC_CHUNK;
+    Buf ccnt, coff, tmp2;
+    XL_TRY(dalloc(c, (size_t)nchunks * 4, &ccnt, "chunk counts"));
+    XL_TRY(dalloc(c, (size_t)nchunks * 4, &coff, "chunk offsets"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes((int64_t)nchunks), &tmp2, "scan scratch"));
+    a.chunk_cnt = ccnt.as<uint32_t>();
+    float ms_total = 0;
+    auto timed = [&](bool mat) -> xl_status {
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+      HIP_TRY(c, k::wcoj_probe(a, mat, c->stream));
+      if (c->profile) {
+        HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+        HIP_TRY(c, hipEventSynchronize(ev[1]));
+        float ms = 0;
+        HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+        ms_total += ms;
+      }
+      return XL_OK;
+    };
+    XL_TRY(timed(false));
+    HIP_TRY(c, k::scan_exclusive_u32(ccnt.as<uint32_t>(), coff.as<uint32_t>(), (int64_t)nchunks, tot.as<uint32_t>(),
+                                     tmp2.p, c->stream));
+    uint32_t n = 0;
+    XL_TRY(ctl_read(c, tot.p, 4, &n));
+    if (h->max_rows > 0 && (int64_t)n > h->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->name + " exceeds its max_rows " +
+                                               std::to_string(h->max_rows));
+    Buf out[3];
+    for (int j = 0; j < 3; ++j) XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(n, 1) * 4, &out[j], "relation column"));
+    a.chunk_off = coff.as<uint32_t>();
+    a.out0 = out[0].as<uint32_t>();
+    a.out1 = out[1].as<uint32_t>();
+    a.out2 = out[2].as<uint32_t>();
+    if (n) XL_TRY(timed(true));
+    cands += (int64_t)items;
+    if (c->profile) {
+      st->wcoj_ms += ms_total;
+      st->wcoj_launches += n ? 2 : 1;
+      st->wcoj_candidates += (int64_t)items;
+      st->wcoj_new += n;
+    }
+    for (int j = 0; j < 3; ++j) h->col[j] = (uint32_t*)out[j].keep();
+    return finish(n);
+  }
+
   xl_status run_stratum(Stratum& s, int64_t max_iterations) {
+    if (s.full.size() == 1 && s.full[0].wcoj) {
+      heads.clear();
+      return run_wcoj(s.full[0]);
+    }
     heads.clear();
     XL_TRY(setup_heads(s));
     for (auto& h : heads) begin_round(h.get());

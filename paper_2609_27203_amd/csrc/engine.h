@@ -62,6 +62,7 @@ struct Context {
   int profile = 0;
   int pull_ratio = 64;
   int frontier_resident = 1;  // closure strata: 1 all rounds in one launch, 0 one launch per round
+  int wcoj_shorter = 1;       // triangle joins: 1 probe the shorter list, 0 always b's (binary-join order)
   int dense_tiles = 0;  // tiled min/max rounds: 0 auto, k tiles per rank, -1 off
   int64_t control_bytes = 0;
 
@@ -154,6 +155,16 @@ struct RulePlan {
   // rows of e whose Y column is y (carried_ycol) against the delta.
   bool carried_val = false;
   int cv_slot_s = -1, cv_slot_z = -1, cv_slot_p = -1;  // P1's slot, -1 when unused
+  // h(X, Y, Z) :- a(..X..Y..), b(..Y..Z..), c(..X..Z..) with three distinct
+  // variables over binary int32 relations and nothing else (a triangle): a
+  // worst-case-optimal join.  For each row (x, y) of a, the Z values of b's
+  // rows with Y = y are intersected with those of c's rows with X = x.
+  // driver = a; tri_a[0], tri_a[1] = a's X and Y columns; tri_b = b's Y and
+  // Z columns; tri_c = c's X and Z columns (head order X, Y, Z).
+  bool wcoj = false;
+  Relation* tri_brel = nullptr;
+  Relation* tri_crel = nullptr;
+  int tri_a[2] = {0, 1}, tri_b[2] = {0, 1}, tri_c[2] = {0, 1};
 };
 
 struct HeadInfo {

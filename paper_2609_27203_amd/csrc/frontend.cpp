@@ -225,6 +225,58 @@ struct Parser {
 };
 
 // ------------------------------------------------------------------ planning
+// The triangle shape (see RulePlan::wcoj): a set head over three distinct
+// variables h0, h1, h2 and exactly three body atoms, each over a binary int32
+// relation with two of the variables, one atom per pair.
+static bool triangle_plan(Context* ctx, const RuleAst& r, RulePlan* p) {
+  if (r.head_args.size() != 3 || r.agg != Agg::NONE || r.atoms.size() != 3 || !r.negs.empty() ||
+      !r.assigns.empty() || !r.cmps.empty())
+    return false;
+  std::string hv[3];
+  for (int j = 0; j < 3; ++j) {
+    if (r.head_args[j].kind != Term::VAR) return false;
+    hv[j] = r.head_args[j].name;
+  }
+  if (hv[0] == hv[1] || hv[1] == hv[2] || hv[0] == hv[2]) return false;
+  auto var_index = [&](const Term& t) {
+    if (t.kind != Term::VAR) return -1;
+    for (int j = 0; j < 3; ++j)
+      if (t.name == hv[j]) return j;
+    return -1;
+  };
+  // atom covering head variables {u, v}: its relation and the columns of u, v
+  Relation* rel[3] = {nullptr, nullptr, nullptr};
+  int col[3][2] = {};
+  const int pu[3] = {0, 1, 0}, pv[3] = {1, 2, 2};  // pairs (h0,h1), (h1,h2), (h0,h2)
+  for (const AtomAst& a : r.atoms) {
+    Relation* q = ctx->find(a.pred);
+    if (!q || q->arity != 2 || q->types[0] != T_I32 || q->types[1] != T_I32) return false;
+    const int i0 = var_index(a.args[0]), i1 = var_index(a.args[1]);
+    if (i0 < 0 || i1 < 0 || i0 == i1) return false;
+    const int lo = std::min(i0, i1), hi = std::max(i0, i1);
+    int k = -1;
+    for (int m = 0; m < 3; ++m)
+      if (pu[m] == lo && pv[m] == hi) k = m;
+    if (k < 0 || rel[k]) return false;
+    rel[k] = q;
+    col[k][0] = i0 == lo ? 0 : 1;  // column of the pair's first variable
+    col[k][1] = 1 - col[k][0];
+  }
+  p->wcoj = true;
+  p->head = ctx->find(r.head);
+  p->driver = rel[0];
+  p->tri_a[0] = col[0][0];  // X
+  p->tri_a[1] = col[0][1];  // Y
+  p->tri_brel = rel[1];
+  p->tri_b[0] = col[1][0];  // Y
+  p->tri_b[1] = col[1][1];  // Z
+  p->tri_crel = rel[2];
+  p->tri_c[0] = col[2][0];  // X
+  p->tri_c[1] = col[2][1];  // Z
+  p->nkey = 3;
+  return true;
+}
+
 struct Planner {
   Context* ctx;
   std::string err;
@@ -587,8 +639,10 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
     if (!h) return bad(XL_INVALID_ARGUMENT, "relation '" + r.head + "' is not declared");
     const int want = (int)r.head_args.size() + (r.agg != Agg::NONE ? 1 : 0);
     if (want != h->arity) return bad(XL_INVALID_ARGUMENT, "rule '" + r.text + "': head has " + std::to_string(want) + " arguments but " + h->name + " has arity " + std::to_string(h->arity));
-    if (r.head_args.empty() || r.head_args.size() > 2)
-      return bad(XL_UNSUPPORTED, "rule '" + r.text + "': derived relations need one or two key columns");
+    RulePlan tri;
+    if (r.head_args.empty() || (r.head_args.size() > 2 && !triangle_plan(ctx, r, &tri)))
+      return bad(XL_UNSUPPORTED, "rule '" + r.text + "': derived relations need one or two key columns "
+                                 "(three only for a triangle join h(X,Y,Z) :- a(X,Y), b(Y,Z), c(X,Z))");
     for (size_t j = 0; j < r.head_args.size(); ++j)
       if (h->types[j] != T_I32) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': key columns of derived relations must be int32");
     for (const auto* list : {&r.atoms, &r.negs})
@@ -681,6 +735,31 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
       in.insert(prog->heads[v].rel);
     }
     st.recursive = c.size() > 1 || deps[c[0]].count(c[0]);
+    // a three-column head: derived by exactly one triangle rule, outside recursion
+    {
+      int n3 = 0, nrules = 0, ntri = 0;
+      for (int v : c) n3 += prog->heads[v].rel->arity == 3 && prog->heads[v].agg == Agg::NONE;
+      for (const RuleAst& r : prog->rules)
+        if (in.count(ctx->find(r.head))) {
+          ++nrules;
+          RulePlan tp;
+          if (triangle_plan(ctx, r, &tp)) ++ntri;
+        }
+      if (ntri > 0 || n3 > 0) {
+        if (st.recursive || c.size() != 1 || nrules != 1 || ntri != 1)
+          return bad(XL_UNSUPPORTED, "a three-column relation (" + prog->heads[c[0]].rel->name +
+                                         ") must be derived by one non-recursive triangle join rule alone");
+        for (int ri = 0; ri < (int)prog->rules.size(); ++ri)
+          if (in.count(ctx->find(prog->rules[ri].head))) {
+            RulePlan tp;
+            triangle_plan(ctx, prog->rules[ri], &tp);
+            tp.rule = ri;
+            st.full.push_back(tp);
+          }
+        prog->strata.push_back(st);
+        continue;
+      }
+    }
     bool has_agg = false;
     for (int v : c) has_agg = has_agg || prog->heads[v].agg != Agg::NONE;
     if (st.recursive && has_agg) {
@@ -743,6 +822,13 @@ std::string explain_program(const Program* p) {
       const auto& plans = pass == 0 ? st.full : st.variants;
       for (const RulePlan& rp : plans) {
         os << "  " << (pass == 0 ? (st.recursive ? "seed " : "eval ") : "delta ") << "rule " << rp.rule << ": ";
+        if (rp.wcoj) {
+          os << "triangle join " << rp.driver->name << "(X=col " << rp.tri_a[0] << ", Y=col " << rp.tri_a[1] << ") x "
+             << rp.tri_brel->name << "(Y=col " << rp.tri_b[0] << ", Z=col " << rp.tri_b[1] << ") x "
+             << rp.tri_crel->name << "(X=col " << rp.tri_c[0] << ", Z=col " << rp.tri_c[1] << ") -> "
+             << rp.head->name << "(X,Y,Z)\n";
+          continue;
+        }
         os << (rp.driver_delta ? "delta " : "scan ") << rp.driver->name << "(" << acts(rp.driver_act, rp.driver->arity) << ")";
         for (size_t k = 0; k < rp.steps.size(); ++k) {
           const StepPlan& sp = rp.steps[k];

@@ -44,13 +44,29 @@ hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hip
 hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
                        hipStream_t s);
 // key[i] = (sorted[i] << 16) | (0xffff - min(deg(zcol[perm[i]]), 0xffff)), deg
-// read from the CSR offsets off over keys [klo, klo + range).
+// read from the CSR offsets off over keys [klo, klo + range); perm may be
+// null (identity), also in value_order_keys.
 hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol, int32_t klo,
                              uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s);
 // out[k] = col[off[k]] for keys k in [0, range) with rows, 0xffffffff otherwise.
 hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s);
 // Packed keys of a negation table: c0[i], or (c0[i] << 32) | c1[i].
 hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s);
+// key[i] = (sorted[i] << 32) | (vcol[perm[i]] ^ 0x80000000): sorting by it
+// keeps the key order and orders each key's rows by the int32 value.
+hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
+                            u64* key, hipStream_t s);
+// ---- worst-case-optimal triangle join (see WcojArgs) ----
+constexpr int WC_CHUNK = 256;  // items per wavefront chunk
+hipError_t wcoj_work(const WcojArgs& a, hipStream_t s);
+// flag[i] = v[i] != 0
+hipError_t nonzero_flags(const uint32_t* v, int64_t n, uint32_t* flag, hipStream_t s);
+// crow[pos[i]] = i and cw[pos[i]] = work[i] for rows with work
+hipError_t wcoj_compact(const uint32_t* work, const uint32_t* pos, int64_t n, uint32_t* crow,
+                        unsigned long long* cw, hipStream_t s);
+hipError_t wcoj_probe(const WcojArgs& a, bool materialize, hipStream_t s);
+// out[i] = key[i] >> shift
+hipError_t high_bits(const u64* key, int shift, int64_t n, uint32_t* out, hipStream_t s);
 // flag[i] = 1 if row i differs (bitwise) from row i-1 in any column (or i == 0).
 hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
                             hipStream_t s);

@@ -342,7 +342,7 @@ __global__ void degree_order_keys_k(const uint32_t* sorted, const uint32_t* perm
                                     int32_t klo, uint32_t range, const uint32_t* off, int64_t n, u64* key) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t kz = zcol[perm[i]] - (uint32_t)klo;
+    const uint32_t kz = zcol[perm ? perm[i] : i] - (uint32_t)klo;
     const uint32_t deg = kz < range ? off[kz + 1] - off[kz] : 0u;
     key[i] = ((u64)sorted[i] << 16) | (0xffffu - (deg < 0xffffu ? deg : 0xffffu));
   }
@@ -378,6 +378,31 @@ __global__ void neg_keys_k(const uint32_t* c0, const uint32_t* c1, int64_t n, u6
 hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   neg_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(c0, c1, n, key);
+  return hipGetLastError();
+}
+
+__global__ void value_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
+                                   u64* key) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    key[i] = ((u64)sorted[i] << 32) | (vcol[perm ? perm[i] : i] ^ 0x80000000u);
+}
+hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
+                            u64* key, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  value_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, vcol, n, key);
+  return hipGetLastError();
+}
+
+// out[i] = key[i] >> shift
+__global__ void high_bits_k(const u64* key, int shift, int64_t n, uint32_t* out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = (uint32_t)(key[i] >> shift);
+}
+hipError_t high_bits(const u64* key, int shift, int64_t n, uint32_t* out, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  high_bits_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(key, shift, n, out);
   return hipGetLastError();
 }
 

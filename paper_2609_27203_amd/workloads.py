@@ -349,6 +349,7 @@ def full_workloads():
         "lse_dag": layered_dag,
         "same_generation": same_generation,
         "tc_rmat_count": tc_rmat,
+        "triangle": triangle,
     }
 
 
@@ -361,4 +362,5 @@ def small_workloads():
         "lse_dag": lambda: layered_dag(8, 300, 8, 32, seed=13),
         "same_generation": lambda: same_generation(1500, seed=14),
         "tc_rmat_count": lambda: tc_rmat(10, 1 << 13, seed=15),
+        "triangle": lambda: triangle(rows=4096, core=40, hubs=4, seed=16),
     }

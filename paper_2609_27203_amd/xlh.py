@@ -46,6 +46,8 @@ class xl_fixpoint_stats(C.Structure):
         ("front_new", C.c_int64),
         ("pull_ms", C.c_double), ("pull_launches", C.c_int64), ("pull_candidates", C.c_int64),
         ("pull_new", C.c_int64),
+        ("wcoj_ms", C.c_double), ("wcoj_launches", C.c_int64), ("wcoj_candidates", C.c_int64),
+        ("wcoj_new", C.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -62,6 +64,8 @@ class xl_fixpoint_stats(C.Structure):
             "front_candidates": self.front_candidates, "front_new": self.front_new,
             "pull_ms": self.pull_ms, "pull_launches": self.pull_launches,
             "pull_candidates": self.pull_candidates, "pull_new": self.pull_new,
+            "wcoj_ms": self.wcoj_ms, "wcoj_launches": self.wcoj_launches,
+            "wcoj_candidates": self.wcoj_candidates, "wcoj_new": self.wcoj_new,
         }
 
 

@@ -71,6 +71,17 @@ def test_negated_literals_are_planned_as_membership_tests():
     assert "grouped" not in delta[0]
 
 
+def test_triangle_rules_become_one_worst_case_optimal_join():
+    """Any column order of the three atoms and any head order: the driver is
+    the atom over the first two head variables."""
+    c = _ctx({"r": I2, "s": I2, "t": I2, "tri": ("i32", "i32", "i32")})
+    plan = c.compile("tri(Z,X,Y) :- s(Y,Z), r(X,Y), t(Z,X).").explain()
+    line = [ln for ln in plan.splitlines() if "triangle join" in ln][0]
+    # head columns (Z, X, Y) play the roles X, Y, Z: a = t over (Z, X), b = r
+    # over (X, Y), c = s over (Z, Y)
+    assert "t(X=col 0, Y=col 1) x r(Y=col 0, Z=col 1) x s(X=col 1, Z=col 0) -> tri(X,Y,Z)" in line
+
+
 def test_self_join_gets_one_delta_variant_per_recursive_atom():
     """Alg. 1: a rule with two recursive atoms has two delta variants, each
     scanning the delta at one atom and joining the full relation at the other."""
@@ -115,6 +126,13 @@ def test_self_join_gets_one_delta_variant_per_recursive_atom():
     ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not nope(X).", "XL_INVALID_ARGUMENT"),
     ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not e(X).", "XL_INVALID_ARGUMENT"),
     ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,_), not e(X, 1.5).", "XL_TYPE_MISMATCH"),
+    # three-column heads: only one non-recursive triangle join rule
+    ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Z) :- e(X,Y), e(Y,Z).", "XL_UNSUPPORTED"),
+    ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Z) :- e(X,Y), e(Y,Z), e(X,Z), X != Z.", "XL_UNSUPPORTED"),
+    ({"e": I2, "h": ("i32", "i32", "i32")},
+     "h(X,Y,Z) :- e(X,Y), e(Y,Z), e(X,Z).\nh(X,Y,Z) :- e(Y,X), e(Y,Z), e(X,Z).", "XL_UNSUPPORTED"),
+    ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Z) :- e(X,Y), e(Y,Z), h(X,Z,Y).", "XL_UNSUPPORTED"),
+    ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Y) :- e(X,Y), e(Y,Y), e(X,Y).", "XL_UNSUPPORTED"),
 ])
 def test_rejected_programs(rels, text, status):
     c = _ctx(rels)
