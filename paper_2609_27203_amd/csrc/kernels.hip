@@ -297,7 +297,18 @@ __global__ void minmax_k(const int32_t* col, int64_t n, int32_t* out) {
     lo = min(lo, __shfl_xor(lo, d, 64));
     hi = max(hi, __shfl_xor(hi, d, 64));
   }
+  // one atomic pair per workgroup: same-address atomics serialize
+  __shared__ int32_t s_lo[4], s_hi[4];
   if (lane_id() == 0) {
+    s_lo[threadIdx.x >> 6] = lo;
+    s_hi[threadIdx.x >> 6] = hi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+      lo = min(lo, s_lo[w]);
+      hi = max(hi, s_hi[w]);
+    }
     atomicMin(&out[0], lo);
     atomicMax(&out[1], hi);
   }
