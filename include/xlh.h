@@ -100,6 +100,8 @@ typedef struct {
     int64_t peak_workspace_bytes;
     int64_t control_bytes_read;
     int64_t table_grows;
+    int64_t index_builds;       /* join indexes built in this run */
+    int64_t index_reuses;       /* join indexes taken from the cross-run cache */
     double ms_total;
     /* Fused join/insert kernels (set, min and max heads), timed with HIP
      * events on the context's stream when the "profile" option is 1. */
@@ -155,6 +157,14 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     in-edge is expanded by pulling (scanning in-edges of the
  *                     unreached targets) when pull_ratio * d >= u; 0 = always
  *                     push (default 64)
+ *   "index_cache_mb"  budget of a cache that keeps the join indexes of
+ *                     relations that are not derived in the running stratum
+ *                     (inputs, finished strata) across xl_fixpoint_run calls,
+ *                     each valid until its relation's rows change (load,
+ *                     clear, re-derivation), least recently used entries
+ *                     evicted first (Sec. 4, runtime optimization: persistent
+ *                     index manager); its blocks come from the workspace.
+ *                     0 = off: every run builds its indexes (default)
  *   "frontier_resident"  closure-shaped strata over dense heads: 1 = every
  *                     pass in one launch, each source iterating its own rounds
  *                     with its row in LDS until its delta is empty, the pass

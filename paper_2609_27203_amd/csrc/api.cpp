@@ -74,6 +74,13 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     c->pull_ratio = (int)value;
     return XL_OK;
   }
+  if (!strcmp(key, "index_cache_mb")) {
+    if (value < 0 || value > ((int64_t)1 << 20)) return c->fail(XL_INVALID_ARGUMENT, "index_cache_mb must be in [0, 2^20]");
+    c->index_cache_bytes = (size_t)value << 20;
+    if (value == 0)
+      while (!c->icache.empty()) c->icache_drop(c->icache.front().rel, false);
+    return XL_OK;
+  }
   if (!strcmp(key, "wcoj_shorter")) {
     if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "wcoj_shorter must be 0 or 1");
     c->wcoj_shorter = (int)value;
@@ -188,7 +195,10 @@ void xl_program_destroy(xl_program* p) {
 void xl_relation_destroy(xl_relation* r) {
   if (!r) return;
   Context* c = r->ctx;
-  if (c->device >= 0) relation_free_storage(r);
+  if (c->device >= 0) {
+    relation_free_storage(r);
+    c->icache_drop(r, false);
+  }
   c->rels.erase(std::remove(c->rels.begin(), c->rels.end(), static_cast<Relation*>(r)), c->rels.end());
   delete r;
 }

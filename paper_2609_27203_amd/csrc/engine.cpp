@@ -70,6 +70,12 @@ void Arena::release(void* p) {
   free_[off] = sz;
 }
 
+size_t Arena::block_size(const void* p) const {
+  if (!p) return 0;
+  auto it = used_.find((size_t)((const char*)p - base_));
+  return it == used_.end() ? 0 : it->second;
+}
+
 size_t Arena::largest_free() const {
   size_t m = 0;
   for (auto& kv : free_) m = std::max(m, kv.second);
@@ -205,6 +211,8 @@ void relation_free_storage(Relation* r) {
     r->col[j] = nullptr;
   }
   r->nrows = 0;
+  r->generation = ++r->ctx->generations;  // cached indexes of the old rows no longer match
+  r->ctx->icache_drop(r, true);
 }
 
 xl_status relation_clear(Relation* r) {
@@ -460,6 +468,26 @@ struct Runner {
         if (first) *first = ix->first;
         return XL_OK;
       }
+    const bool cacheable = c->index_cache_bytes > 0 && !head_of(rel);
+    if (cacheable)
+      for (CachedIndex& ce : c->icache)
+        if (ce.rel == rel && ce.generation == rel->generation && ce.col == col && ce.order_col == order_col &&
+            (order_col < 0 || ce.order_kind == order_kind)) {
+          ce.last_run = c->runs;
+          auto ix = std::make_unique<DevIndex>();
+          ix->rel = rel;
+          ix->col = col;
+          ix->order_col = order_col;
+          ix->order_kind = order_kind;
+          ix->probe = ce.probe;
+          ix->first = ce.first;
+          *out = ix->probe;
+          if (first) *first = ix->first;
+          indexes.push_back(std::move(ix));
+          st->index_reuses++;
+          return XL_OK;
+        }
+    st->index_builds++;
     auto ix = std::make_unique<DevIndex>();
     ix->rel = rel;
     ix->col = col;
@@ -609,8 +637,44 @@ struct Runner {
     }
     *out = p;
     if (first) *first = ix->first;
+    if (cacheable) cache_index(*ix);
     indexes.push_back(std::move(ix));
     return XL_OK;
+  }
+
+  // Hand a freshly built index of a relation that is not a head to the
+  // context's cache (its blocks then outlive the run), and evict the least
+  // recently used entries not used by this run while the cache is over its
+  // budget.
+  void cache_index(DevIndex& ix) {
+    CachedIndex ce;
+    ce.rel = ix.rel;
+    ce.generation = ix.rel->generation;
+    ce.col = ix.col;
+    ce.order_col = ix.order_col;
+    ce.order_kind = ix.order_kind;
+    ce.probe = ix.probe;
+    ce.first = ix.first;
+    ce.last_run = c->runs;
+    for (auto& b : ix.owned) {
+      ce.bytes += c->arena.block_size(b->p);
+      ce.blocks.push_back(b->keep());
+    }
+    ix.owned.clear();
+    c->icache.push_back(std::move(ce));
+    size_t total = 0;
+    for (const CachedIndex& e : c->icache) total += e.bytes;
+    while (total > c->index_cache_bytes) {
+      int victim = -1;
+      for (int i = 0; i < (int)c->icache.size(); ++i)
+        if (c->icache[i].last_run != c->runs &&
+            (victim < 0 || c->icache[i].last_run < c->icache[victim].last_run))
+          victim = i;
+      if (victim < 0) break;  // every entry serves the running program
+      total -= c->icache[victim].bytes;
+      for (void* b : c->icache[victim].blocks) c->arena.release(b);
+      c->icache.erase(c->icache.begin() + victim);
+    }
   }
 
   // ------------------------------------------------------------ domains / heads
@@ -2275,6 +2339,7 @@ xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st)
   if (c->device < 0) return c->fail(XL_INVALID_ARGUMENT, "planning-only context cannot run programs");
   if (max_iterations < 0) return c->fail(XL_INVALID_ARGUMENT, "negative iteration cap");
   c->arena.reset_peak();
+  c->runs++;
   const int64_t ctl0 = c->control_bytes;
   hipEvent_t e0, e1;
   HIP_TRY(c, hipEventCreate(&e0));

@@ -26,6 +26,7 @@ class Arena {
   void reset_peak() { peak_ = in_use_; }
   size_t capacity() const { return size_; }
   size_t largest_free() const;
+  size_t block_size(const void* p) const;  // 0 for a pointer that is not a live block
 
  private:
   char* base_ = nullptr;
@@ -46,6 +47,21 @@ struct Relation {
   uint32_t* col[MAXC] = {};  // device columns (arena), nrows valid rows
   int64_t nrows = 0;
   int32_t lo[MAXC] = {}, hi[MAXC] = {};  // bounds of i32 columns when nrows > 0
+  uint64_t generation = 0;  // new value (unique in the context) whenever the rows change
+};
+
+// An index of a relation kept across runs (option "index_cache_mb"): valid
+// while the relation's generation is unchanged.  The blocks are arena memory
+// owned by the cache.
+struct CachedIndex {
+  Relation* rel = nullptr;
+  uint64_t generation = 0;
+  int col = 0, order_col = -1, order_kind = 0;
+  IndexProbe probe{};
+  uint32_t* first = nullptr;
+  std::vector<void*> blocks;
+  size_t bytes = 0;
+  uint64_t last_run = 0;
 };
 
 struct Context {
@@ -65,6 +81,21 @@ struct Context {
   int wcoj_shorter = 1;       // triangle joins: 1 probe the shorter list, 0 always b's (binary-join order)
   int dense_tiles = 0;  // tiled min/max rounds: 0 auto, k tiles per rank, -1 off
   int64_t control_bytes = 0;
+  uint64_t generations = 0;      // source of Relation::generation values
+  size_t index_cache_bytes = 0;  // budget of the cross-run index cache (0: off)
+  uint64_t runs = 0;             // xl_fixpoint_run calls so far
+  std::vector<CachedIndex> icache;
+  // drop cached indexes of rel (all of them, or those of older generations)
+  void icache_drop(const Relation* rel, bool stale_only) {
+    for (size_t i = 0; i < icache.size();) {
+      if (icache[i].rel == rel && (!stale_only || icache[i].generation != rel->generation)) {
+        for (void* b : icache[i].blocks) arena.release(b);
+        icache.erase(icache.begin() + (long)i);
+      } else {
+        ++i;
+      }
+    }
+  }
 
   xl_status fail(xl_status st, const std::string& msg) {
     err = msg;

@@ -38,7 +38,7 @@ class xl_fixpoint_stats(C.Structure):
         ("rounds_recorded", C.c_int32), ("delta_rows", C.c_int64 * STATS_ROUNDS),
         ("candidates_total", C.c_int64), ("new_tuples_total", C.c_int64),
         ("derived_tuples", C.c_int64), ("peak_workspace_bytes", C.c_int64),
-        ("control_bytes_read", C.c_int64), ("table_grows", C.c_int64),
+        ("control_bytes_read", C.c_int64), ("table_grows", C.c_int64), ("index_builds", C.c_int64), ("index_reuses", C.c_int64),
         ("ms_total", C.c_double),
         ("emit_ms", C.c_double), ("emit_launches", C.c_int64), ("emit_source_rows", C.c_int64),
         ("emit_candidates", C.c_int64), ("emit_new", C.c_int64),
@@ -58,6 +58,7 @@ class xl_fixpoint_stats(C.Structure):
             "candidates_total": self.candidates_total, "new_tuples_total": self.new_tuples_total,
             "derived_tuples": self.derived_tuples, "peak_workspace_bytes": self.peak_workspace_bytes,
             "control_bytes_read": self.control_bytes_read, "table_grows": self.table_grows,
+            "index_builds": self.index_builds, "index_reuses": self.index_reuses,
             "ms_total": self.ms_total, "emit_ms": self.emit_ms, "emit_launches": self.emit_launches,
             "emit_source_rows": self.emit_source_rows, "emit_candidates": self.emit_candidates,
             "emit_new": self.emit_new, "front_ms": self.front_ms, "front_launches": self.front_launches,

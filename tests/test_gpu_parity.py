@@ -247,6 +247,44 @@ def test_triangle_full_size_sampled_and_sound():
     assert stats["wcoj_candidates"] < 5_000_000  # the probes stay near the output size
 
 
+# ------------------------------------------------------------- index reuse across runs
+@pytest.mark.parametrize("name", ["tc_rmat_count", "triangle", "sssp", "same_generation"])
+def test_index_cache_across_runs(name):
+    """With "index_cache_mb" the second run of a program over unchanged inputs
+    builds no input index again and gives the same rows; reloading an input
+    invalidates its cached indexes, and a tiny budget (LRU eviction between
+    runs) changes nothing in the results."""
+    from paper_2609_27203_amd import xlh
+    wl = W.small_workloads()[name]()
+    print(f"case: index cache {name}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    for budget in (256, 1):
+        ctx = xlh.Context(device=0, workspace_bytes=1 << 30)
+        ctx.set_option("index_cache_mb", budget)
+        for n, (t, cols) in wl.edb.items():
+            ctx.relation(n, t).load(cols)
+        for n, t in wl.idb.items():
+            ctx.relation(n, t)
+        prog = ctx.compile(wl.rules)
+        seen = []
+        for run in range(3):
+            for n in wl.idb:
+                ctx.relations[n].clear()
+            if run == 2:  # new rows for one input: its cached indexes are stale
+                first = sorted(wl.edb)[0]
+                ctx.relations[first].load(wl.edb[first][1])
+            st = prog.run()
+            rels = {n: ctx.relations[n].read() for n in wl.idb}
+            _compare(wl, rels, ref, f" run {run} budget {budget}")
+            seen.append((st["index_builds"], st["index_reuses"]))
+        if name == "sssp":  # tiled min rounds read their own (Z, tile) layout, built per run
+            continue
+        assert seen[0][0] > 0 and seen[0][1] == 0
+        if budget == 256:
+            assert seen[1][1] > 0 and seen[1][0] < seen[0][0]
+            assert seen[2][0] > 0
+
+
 COUNT_SHAPES_RULES = W.TC_RULES + """
 out_count(X,count(Y)) :- path(X,Y).
 in_count(Y,count(X)) :- path(X,Y).
