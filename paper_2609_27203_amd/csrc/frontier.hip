@@ -206,8 +206,10 @@ __device__ __forceinline__ void frontier_expand(const FrontierArgs& a, const uin
       __syncthreads();
       continue;
     }
-    for (uint32_t r0 = (uint32_t)w * 64; r0 < nz; r0 += FR_WAVES * 64) {
-      const uint32_t r = r0 + lane;
+    // list positions interleaved over the wavefronts (lane l of wavefront w
+    // takes j0 + 4 l + w), so a short list still reaches all of them
+    for (uint32_t j0 = 0; j0 < nz; j0 += FR_WAVES * 64) {
+      const uint32_t r = j0 + (uint32_t)lane * FR_WAVES + (uint32_t)w;
       uint32_t beg = 0, deg = 0;
       if (r < nz) {
         const uint32_t kk = zlist[r] - (uint32_t)a.idx.key_lo;
