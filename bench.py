@@ -41,7 +41,7 @@ KERNELS = {
     "front": "frontier_resident_k (every round of a first key in one workgroup, its row in LDS: delta "
              "expand or in-edge pull + membership test + merge)",
     "emit": "stage_k / dense_min_tile_k (fused delta expand + probe + fold into the head)",
-    "pull": "dense_pull_k (segmented fold of each marked key's in-edges against the delta)",
+    "pull": "dense_pull_k (fold of each marked key's in-edges against the delta, keys ordered by target)",
     "wcoj": "wcoj_probe_k (count and materialize passes: each driver row's shorter Z list probed into the longer)",
 }
 

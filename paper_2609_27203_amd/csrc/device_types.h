@@ -145,6 +145,9 @@ struct EmitSpec {
   uint32_t dmap_n;
   uint32_t* dpres;
   uint32_t* dchg;
+  // EM_MARK: bit (k1 - lo1) * nrank + dmap[k0 - lo0] of dchg (second key
+  // major: the keys of one second key lie together)
+  uint32_t nrank;
   // shared
   unsigned long long* counters;
   unsigned long long limit;  // overflow threshold on CNT_INSERTED
@@ -165,13 +168,19 @@ struct StageArgs {
 // keys marked in the round: key (s, y) folds the contributions of every row
 // of e whose Y column is y (rev) and whose Z value z has (s, z) in the
 // current delta, evaluating the rule's comparisons and arithmetic per row.
-// Slot of (s, y) = rank(s) * range1 + (y - lo1); a thread owns one listed
-// slot, so the fold order is the index order and the result deterministic.
+// The delta arrays (cval/cpres, nval/npres) and the marked list use the
+// second-key-major slot (y - lo1) * nrank + rank(s): listed keys of one y lie
+// together, and the delta values of (s, z) for a fixed z and consecutive s
+// are consecutive words, so the wavefront's reads of one in-edge coalesce.
+// The full relation (fval/fpres) keeps the first-key-major slot
+// rank(s) * range1 + (y - lo1), which yields the rows in key order.  A key's
+// contributions are folded in index order: the result is deterministic.
 struct DensePullArgs {
-  const uint32_t* list;   // marked slots, ascending
+  const uint32_t* list;   // marked delta slots, ascending
   int64_t n;
   const uint32_t* dict;   // rank -> first key value
   uint32_t range1;
+  uint32_t nrank;         // ranks (first key values in the dictionary)
   int32_t lo1;
   IndexProbe rev;         // e indexed by its Y column; act[] = the rule's actions on e
   int32_t zcol;

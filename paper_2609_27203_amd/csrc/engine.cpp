@@ -550,7 +550,7 @@ struct Runner {
         uint32_t* k1 = h->nkey == 2 ? (uint32_t*)snap[1] : nullptr;
         if (h->dv)
           HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
-                                   h->range1, h->kp, rel->types[h->nkey], h->fold, (uint32_t*)snap[0], k1,
+                                   h->range1, 0, h->kp, rel->types[h->nkey], h->fold, (uint32_t*)snap[0], k1,
                                    (uint32_t*)snap[h->nkey], std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p,
                                    c->stream));
         else
@@ -1374,6 +1374,7 @@ struct Runner {
     a.emit.dmap = h->dmap.as<uint32_t>();
     a.emit.dmap_n = (uint32_t)h->dmap_n;
     a.emit.row_bits = (u64)h->range1;
+    a.emit.nrank = (uint32_t)std::max<int64_t>(h->n0, 1);
     a.emit.dchg = h->dchg.as<uint32_t>();
     a.emit.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
@@ -1409,6 +1410,7 @@ struct Runner {
     q.n = n;
     q.dict = h->dict.as<uint32_t>();
     q.range1 = (uint32_t)h->range1;
+    q.nrank = (uint32_t)std::max<int64_t>(h->n0, 1);
     q.lo1 = h->kp.lo[1];
     XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
     for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
@@ -1969,7 +1971,8 @@ struct Runner {
     if (h->ds) {  // seed round of a dense head: the folded rows become the first delta
       HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
       HIP_TRY(c, k::dense_apply_rows(h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
-                                     nseg, h->dmap.as<uint32_t>(), (uint32_t)h->dmap_n, (uint32_t)h->range1, h->kp,
+                                     nseg, h->dmap.as<uint32_t>(), (uint32_t)h->dmap_n, (uint32_t)h->range1,
+                                     (uint32_t)std::max<int64_t>(h->n0, 1), h->kp,
                                      h->fold, h->rel->types[h->nkey], h->dcur.as<uint32_t>(),
                                      h->dcur_pres.as<uint32_t>(), h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(),
                                      c->dcounters, c->stream));
@@ -2115,7 +2118,7 @@ struct Runner {
       XL_TRY(dalloc(c, k::compact_temp_bytes(ns), &tmp, "compaction scratch"));
       XL_TRY(dalloc(c, 8, &tot, "count"));
       HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
-                               h->range1, h->kp, r->types[h->nkey], h->fold, out[0].as<uint32_t>(),
+                               h->range1, 0, h->kp, r->types[h->nkey], h->fold, out[0].as<uint32_t>(),
                                h->nkey == 2 ? out[1].as<uint32_t>() : nullptr, out[h->nkey].as<uint32_t>(),
                                std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p, c->stream));
       uint32_t m = 0;

@@ -131,8 +131,9 @@ hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t*
                        uint32_t* out, hipStream_t s);
 // Dense value heads (first key through a dictionary, second key direct).
 // Rows of every present slot in slot order (= ascending keys).
+// nrank = 0: slot rank * range1 + (y - lo1); nrank > 0: slot (y - lo1) * nrank + rank.
 hipError_t dense_rows(const uint32_t* vals, const uint32_t* pres, const uint32_t* dict, int64_t n,
-                      int64_t range1, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      int64_t range1, int64_t nrank, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                       uint32_t* v, int64_t out_cap, uint32_t* total, void* temp, hipStream_t s);
 hipError_t dict_mark(const uint32_t* col, int64_t n, int32_t lo, uint32_t range, uint32_t* mark, hipStream_t s);
 hipError_t dict_finish(uint32_t* map, const uint32_t* pos, uint32_t range, int32_t lo, uint32_t* dict,
@@ -156,7 +157,8 @@ hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);
 hipError_t bits_keys(uint32_t* bits, int64_t nbits, u64 row_bits, int32_t lo0, int32_t lo1, int nkey, bool clear,
                      uint32_t* c0, uint32_t* c1, uint32_t* total, void* temp, bool write, hipStream_t s);
 hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
-                            uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
+                            uint32_t map_n, uint32_t range1, uint32_t nrank, KeyPack kp, int fold_kind, int type,
+                            uint32_t* cval,
                             uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s);
 // Dense min/max heads, tiled rounds (see DenseTileArgs).
 // Delta rows from the delta bits in slot order (two calls on the same temp,

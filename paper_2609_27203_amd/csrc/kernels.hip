@@ -640,6 +640,7 @@ struct CompactArgs {
   KeyPack kp;
   int type, fold_kind;
   int64_t range1;         // CK_COUNTER: second-key range
+  int64_t nrank;          // CK_DENSE: 0 = slot rank * range1 + y, else slot y * nrank + rank
   uint32_t* k0;           // CK_NONEMPTY / CK_COUNTER rows; CK_STAMP: slot indices
   uint32_t* k1;
   uint32_t* v;
@@ -678,8 +679,9 @@ __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
       if (a.kind == CK_STAMP) {
         a.k0[p] = (uint32_t)i;
       } else if (a.kind == CK_DENSE) {
-        a.k0[p] = a.dict[i / a.range1];
-        if (a.k1) a.k1[p] = (uint32_t)(i % a.range1) + (uint32_t)a.kp.lo[1];
+        const int64_t rk = a.nrank ? i % a.nrank : i / a.range1, yb = a.nrank ? i / a.nrank : i % a.range1;
+        a.k0[p] = a.dict[rk];
+        if (a.k1) a.k1[p] = (uint32_t)yb + (uint32_t)a.kp.lo[1];
         a.v[p] = stored_value(a.counts[i], a.type, a.fold_kind);
       } else if (a.kind == CK_COUNTER) {
         if (a.kp.nkey == 2) {
@@ -769,10 +771,11 @@ hipError_t dcount_rows(const uint32_t* counts, int64_t n, int64_t range1, KeyPac
 }
 
 hipError_t dense_rows(const uint32_t* vals, const uint32_t* pres, const uint32_t* dict, int64_t n,
-                      int64_t range1, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                      int64_t range1, int64_t nrank, KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                       uint32_t* v, int64_t out_cap, uint32_t* total, void* temp, hipStream_t s) {
   CompactArgs a{};
   a.kind = CK_DENSE;
+  a.nrank = nrank;
   a.counts = vals;
   a.pres = pres;
   a.dict = dict;
@@ -1272,7 +1275,7 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
       if (r0 == 0xffffffffu || (u64)k1 >= e.row_bits) {
         atomicOr(&e.counters[CNT_FATAL], 4ull);
       } else {
-        const uint32_t slot = r0 * (uint32_t)e.row_bits + k1, bit = 1u << (slot & 31);
+        const uint32_t slot = k1 * e.nrank + r0, bit = 1u << (slot & 31);
         if (!(e.dchg[slot >> 5] & bit)) atomicOr(&e.dchg[slot >> 5], bit);
       }
     }
@@ -1589,7 +1592,7 @@ __device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, u
   const uint32_t z = a.rev.col[a.zcol][e_row];
   const uint32_t zb = z - (uint32_t)a.lo1;
   if (zb >= a.range1) return false;
-  const uint32_t zs = r * a.range1 + zb;
+  const uint32_t zs = zb * a.nrank + r;
   if (!((a.cpres[zs >> 5] >> (zs & 31)) & 1u)) return false;
   if (a.fast) {
     setv(u, a.val_slot, fast_value(a.fast, a.val_type, a.cval[zs], a.rev.col[a.fcol][e_row]));
@@ -1613,6 +1616,7 @@ __device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, u
 // logsumexp, the sum otherwise.  The order is fixed, so the result is
 // deterministic.
 constexpr int DP_WAVES = 4;
+constexpr uint32_t DP_LANE_MAX = 32;  // wavefronts whose keys have at most this many rows: one lane per key
 
 __device__ __forceinline__ float seg_max_scan(float v, int lane, int head) {
 #pragma unroll
@@ -1646,7 +1650,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
     uint32_t t = 0, e0 = 0, deg = 0;
     if (i < a.n) {
       t = a.list[i];
-      const uint32_t kk = t % a.range1 + (uint32_t)a.lo1 - (uint32_t)a.rev.key_lo;
+      const uint32_t kk = t / a.nrank + (uint32_t)a.lo1 - (uint32_t)a.rev.key_lo;
       if (kk < a.rev.key_range) {
         e0 = a.rev.off[kk];
         deg = a.rev.off[kk + 1] - e0;
@@ -1662,7 +1666,85 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
     s_acc[w][lane] = 0u;
     s_any[w][lane] = 0u;
     wave_lds_sync();
-    for (uint32_t base = 0; base < total; base += 64) {
+    uint32_t maxdeg = deg;
+    for (int k = 32; k > 0; k >>= 1) maxdeg = max(maxdeg, (uint32_t)__shfl_xor(maxdeg, k, 64));
+    if (maxdeg <= DP_LANE_MAX) {
+      // Short lists: one lane per key, every key's j-th in-edge in step j.
+      // Listed keys are ordered by y, so the keys of one y read the delta
+      // values of one z at consecutive slots.  Sequential fold per key in
+      // index order (online max shift for logsumexp).
+      const uint32_t r = t % a.nrank, y = t / a.nrank + (uint32_t)a.lo1;
+      float m = -INFINITY, facc = 0.0f;
+      uint32_t uacc = 0;
+      bool any = false;
+      auto fold = [&](uint32_t x) {
+        any = true;
+        if (lse) {
+          const float xv = __uint_as_float(x);
+          if (xv > m) {
+            facc = (m == -INFINITY ? 0.0f : facc * expf(m - xv)) + 1.0f;
+            m = xv;
+          } else if (xv != -INFINITY) {
+            facc += expf(xv - m);
+          }
+        } else if (f32) {
+          facc = __fadd_rn(facc, __uint_as_float(x));
+        } else {
+          uacc += x;
+        }
+      };
+      if (a.fast) {
+        // the value is one add/subtract of the delta value and a column of
+        // e: eight in-edges at a time, each level of loads issued together
+        const uint32_t* zc = a.rev.col[a.zcol];
+        const uint32_t* wc = a.rev.col[a.fcol];
+        for (uint32_t jb = 0; jb < maxdeg; jb += 8) {
+          uint32_t zs[8], wv[8], pw[8], cv[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t jj = jb + (uint32_t)q;
+            const uint32_t zb = jj < deg ? zc[e0 + jj] - (uint32_t)a.lo1 : 0xffffffffu;
+            zs[q] = zb < a.range1 ? zb * a.nrank + r : 0xffffffffu;
+            wv[q] = jj < deg ? wc[e0 + jj] : 0u;
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) pw[q] = zs[q] != 0xffffffffu ? a.cpres[zs[q] >> 5] : 0u;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const bool pres = zs[q] != 0xffffffffu && ((pw[q] >> (zs[q] & 31)) & 1u);
+            cv[q] = pres ? a.cval[zs[q]] : 0u;
+            pw[q] = pres;
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (pw[q]) fold(fast_value(a.fast, a.val_type, cv[q], wv[q]));
+        }
+      }
+      for (uint32_t jj = 0; !a.fast && jj < maxdeg; ++jj) {
+        if (jj >= deg) continue;
+        Regs u;
+        if (!pull_bind(a, r, a.dict[r], y, e0 + jj, u)) continue;
+        const uint32_t x = getv(u, a.val_slot);
+        any = true;
+        if (lse) {
+          const float xv = __uint_as_float(x);
+          if (xv > m) {
+            facc = (m == -INFINITY ? 0.0f : facc * expf(m - xv)) + 1.0f;
+            m = xv;
+          } else if (xv != -INFINITY) {
+            facc += expf(xv - m);
+          }
+        } else if (f32) {
+          facc = __fadd_rn(facc, __uint_as_float(x));
+        } else {
+          uacc += x;
+        }
+      }
+      s_m[w][lane] = __float_as_uint(m);
+      s_acc[w][lane] = (lse || f32) ? __float_as_uint(facc) : uacc;
+      s_any[w][lane] = any ? 1u : 0u;
+    }
+    for (uint32_t base = 0; maxdeg > DP_LANE_MAX && base < total; base += 64) {
       const uint32_t j = base + (uint32_t)lane;
       const bool act = j < total;
       int q = 0;
@@ -1672,9 +1754,9 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
       bool ok = false;
       uint32_t x = 0;
       if (act) {
-        const uint32_t tq = s_key[w][q], r = tq / a.range1;
+        const uint32_t tq = s_key[w][q], r = tq % a.nrank;
         Regs u;
-        ok = pull_bind(a, r, a.dict[r], tq % a.range1 + (uint32_t)a.lo1, s_beg[w][q] + (j - s_excl[w][q]), u);
+        ok = pull_bind(a, r, a.dict[r], tq / a.nrank + (uint32_t)a.lo1, s_beg[w][q] + (j - s_excl[w][q]), u);
         if (ok) x = getv(u, a.val_slot);
       }
       // runs of equal owners among the active lanes
@@ -1730,13 +1812,13 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
         out = s_acc[w][lane];
       }
       if (!s_any[w][lane]) atomicOr(&a.counters[CNT_FATAL], 8ull);  // a marked key always has a contribution
-      const uint32_t r = t / a.range1;
+      const uint32_t r = t % a.nrank, yb = t / a.nrank;
       a.k0[i] = a.dict[r];
-      a.k1[i] = t % a.range1 + (uint32_t)a.lo1;
+      a.k1[i] = yb + (uint32_t)a.lo1;
       a.v[i] = out;
       a.nval[t] = out;
       atomicOr(&a.npres[t >> 5], 1u << (t & 31));
-      mine += dense_merge(a.fval, a.fpres, t, out, a.fold_kind, a.val_type);
+      mine += dense_merge(a.fval, a.fpres, r * a.range1 + yb, out, a.fold_kind, a.val_type);
     }
     wave_lds_sync();
   }
@@ -1755,9 +1837,9 @@ hipError_t dense_pull(const DensePullArgs& a, hipStream_t s) {
 // head: each becomes the current delta value of its slot and is folded into
 // the full relation.
 __global__ void dense_apply_rows_k(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n,
-                                   const uint32_t* map, uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind,
-                                   int type, uint32_t* cval, uint32_t* cpres, uint32_t* fval, uint32_t* fpres,
-                                   u64* counters) {
+                                   const uint32_t* map, uint32_t map_n, uint32_t range1, uint32_t nrank, KeyPack kp,
+                                   int fold_kind, int type, uint32_t* cval, uint32_t* cpres, uint32_t* fval,
+                                   uint32_t* fpres, u64* counters) {
   uint32_t mine = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t k0 = c0[i] - (uint32_t)kp.lo[0], k1 = c1[i] - (uint32_t)kp.lo[1];
@@ -1766,19 +1848,20 @@ __global__ void dense_apply_rows_k(const uint32_t* c0, const uint32_t* c1, const
       atomicOr(&counters[CNT_FATAL], 4ull);
       continue;
     }
-    const uint32_t t = r0 * range1 + k1;
+    const uint32_t t = k1 * nrank + r0;  // delta: second-key-major; full relation: first-key-major
     cval[t] = v[i];
     atomicOr(&cpres[t >> 5], 1u << (t & 31));
-    mine += dense_merge(fval, fpres, t, v[i], fold_kind, type);
+    mine += dense_merge(fval, fpres, r0 * range1 + k1, v[i], fold_kind, type);
   }
   block_count_add(&counters[CNT_INSERTED], mine);
 }
 hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32_t* v, int64_t n, const uint32_t* map,
-                            uint32_t map_n, uint32_t range1, KeyPack kp, int fold_kind, int type, uint32_t* cval,
-                            uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters, hipStream_t s) {
+                            uint32_t map_n, uint32_t range1, uint32_t nrank, KeyPack kp, int fold_kind, int type,
+                            uint32_t* cval, uint32_t* cpres, uint32_t* fval, uint32_t* fpres, u64* counters,
+                            hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  dense_apply_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(c0, c1, v, n, map, map_n, range1, kp, fold_kind, type,
-                                                            cval, cpres, fval, fpres, counters);
+  dense_apply_rows_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(c0, c1, v, n, map, map_n, range1, nrank, kp, fold_kind,
+                                                            type, cval, cpres, fval, fpres, counters);
   return hipGetLastError();
 }
 
