@@ -401,6 +401,7 @@ struct HeadRun {
   bool dv = false;
   Buf dmap, dict, dvals, dpres, dchg;
   int64_t n0 = 0, dmap_n = 0;
+  int64_t nrank_d = 0;  // sum/logsumexp heads: rank stride of the target-major delta slots (n0 rounded up to 32)
   std::vector<std::pair<Relation*, int>> dict_src;
   // dense sum/logsumexp heads (one carried-value variant): the same slots;
   // dvals/dpres hold the full relation, dcur/dcur_pres this round's delta,
@@ -947,12 +948,17 @@ struct Runner {
     HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nw * 4, c->stream));
     if (h->tiled) XL_TRY(dalloc(c, (size_t)(n0 + 1) * 4, &h->roff, "delta rows per rank"));
     if (h->ds) {
-      XL_TRY(dalloc(c, ns * 4, &h->dcur, "dense delta values"));
-      XL_TRY(dalloc(c, ns * 4, &h->dnext, "dense delta values"));
-      XL_TRY(dalloc(c, nw * 4, &h->dcur_pres, "dense delta bits"));
-      XL_TRY(dalloc(c, nw * 4, &h->dnext_pres, "dense delta bits"));
-      HIP_TRY(c, hipMemsetAsync(h->dcur_pres.p, 0, nw * 4, c->stream));
-      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, nw * 4, c->stream));
+      // target-major delta slots with whole words per target: y * nrank_d + rank
+      h->nrank_d = (std::max<int64_t>(n0, 1) + 31) / 32 * 32;
+      const size_t nsd = (size_t)h->nrank_d * (size_t)h->range1, nwd = nsd / 32;
+      XL_TRY(dalloc(c, nsd * 4, &h->dcur, "dense delta values"));
+      XL_TRY(dalloc(c, nsd * 4, &h->dnext, "dense delta values"));
+      XL_TRY(dalloc(c, nwd * 4, &h->dcur_pres, "dense delta bits"));
+      XL_TRY(dalloc(c, nwd * 4, &h->dnext_pres, "dense delta bits"));
+      XL_TRY(dalloc(c, nwd * 4, &h->dchg, "dense delta marks"));
+      HIP_TRY(c, hipMemsetAsync(h->dcur_pres.p, 0, nwd * 4, c->stream));
+      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, nwd * 4, c->stream));
+      HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nwd * 4, c->stream));
     } else {
       XL_TRY(dalloc(c, ns * 4, &h->didx, "delta slot list"));
     }
@@ -1364,6 +1370,27 @@ struct Runner {
     a.idx.key_slot = (int8_t)sp.key_slot;
     for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
     XL_TRY(fill_ops(a, p, 0));
+    int fcol = 0;
+    const int fast = affine_value(p, &fcol);
+    const int64_t nsd = h->nrank_d * h->range1;
+    if (fast) {
+      // every key with an in-edge from a delta key receives a value, so the
+      // marks are the OR of the in-neighbours' delta presence rows
+      IndexProbe rev{};
+      XL_TRY(get_index(sp.rel, p.carried_ycol, &rev));
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+      HIP_TRY(c, k::dense_mark_in(rev, sp.key_col, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
+                                  h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+      if (c->profile) {
+        HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+        HIP_TRY(c, hipEventSynchronize(ev[1]));
+        float ms = 0;
+        HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+        st->emit_ms += ms;
+        st->emit_launches++;
+        st->emit_source_rows += src.n;
+      }
+    }
     a.emit.mode = EM_MARK;
     a.emit.key.nkey = 2;
     a.emit.key.slot[0] = (int8_t)p.key_slot[0];
@@ -1374,26 +1401,28 @@ struct Runner {
     a.emit.dmap = h->dmap.as<uint32_t>();
     a.emit.dmap_n = (uint32_t)h->dmap_n;
     a.emit.row_bits = (u64)h->range1;
-    a.emit.nrank = (uint32_t)std::max<int64_t>(h->n0, 1);
+    a.emit.nrank = (uint32_t)h->nrank_d;
     a.emit.dchg = h->dchg.as<uint32_t>();
     a.emit.counters = c->dcounters;
-    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
-    HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
-    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
     u64 cnt[CNT_N];
-    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
-    if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
-    if (c->profile) {
-      float ms = 0;
-      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
-      st->emit_ms += ms;
-      st->emit_launches++;
-      st->emit_source_rows += src.n;
-      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+    if (!fast) {
+      HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+      HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+      XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+      if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
+      if (c->profile) {
+        float ms = 0;
+        HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+        st->emit_ms += ms;
+        st->emit_launches++;
+        st->emit_source_rows += src.n;
+        st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      }
+      cands += (int64_t)cnt[CNT_CANDIDATES];
     }
-    cands += (int64_t)cnt[CNT_CANDIDATES];
-    const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+    const int64_t ns = nsd;
     Buf tmp, tot, list;
     XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &tmp, "compaction scratch"));
     XL_TRY(dalloc(c, 8, &tot, "count"));
@@ -1410,7 +1439,7 @@ struct Runner {
     q.n = n;
     q.dict = h->dict.as<uint32_t>();
     q.range1 = (uint32_t)h->range1;
-    q.nrank = (uint32_t)std::max<int64_t>(h->n0, 1);
+    q.nrank = (uint32_t)h->nrank_d;
     q.lo1 = h->kp.lo[1];
     XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
     for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
@@ -1423,8 +1452,7 @@ struct Runner {
     q.val_slot = (int8_t)p.val_slot;
     q.val_type = p.val_type;
     q.fold_kind = h->fold;
-    int fcol = 0;
-    q.fast = (int8_t)affine_value(p, &fcol);
+    q.fast = (int8_t)fast;
     q.fcol = (int8_t)fcol;
     q.nops = (int32_t)p.stage_ops[0].size();
     for (int i = 0; i < q.nops; ++i) q.ops[i] = p.stage_ops[0][i];
@@ -1453,6 +1481,7 @@ struct Runner {
       st->pull_candidates += (int64_t)cnt[CNT_CANDIDATES];
       st->pull_new += (int64_t)n;
     }
+    if (fast) cands += (int64_t)cnt[CNT_CANDIDATES];  // no mark pass: count the in-edges the fold examined
     h->keys += (int64_t)cnt[CNT_INSERTED];
     h->pull_n = n;
     if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
@@ -1876,8 +1905,7 @@ struct Runner {
       h->dn = h->pull_n;
       std::swap(h->dcur.p, h->dnext.p);
       std::swap(h->dcur_pres.p, h->dnext_pres.p);
-      const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
-      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)((ns + 31) / 32) * 4, c->stream));
+      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)(h->nrank_d * h->range1 / 32) * 4, c->stream));
       *delta = h->dn;
       return XL_OK;
     }
@@ -1972,7 +2000,7 @@ struct Runner {
       HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
       HIP_TRY(c, k::dense_apply_rows(h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
                                      nseg, h->dmap.as<uint32_t>(), (uint32_t)h->dmap_n, (uint32_t)h->range1,
-                                     (uint32_t)std::max<int64_t>(h->n0, 1), h->kp,
+                                     (uint32_t)h->nrank_d, h->kp,
                                      h->fold, h->rel->types[h->nkey], h->dcur.as<uint32_t>(),
                                      h->dcur_pres.as<uint32_t>(), h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(),
                                      c->dcounters, c->stream));

@@ -1865,6 +1865,37 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
   return hipGetLastError();
 }
 
+// Marks of a carried-value round whose value is one add or subtract (every
+// candidate then yields a value): word w of target y's mark row = OR over
+// y's in-edges (z, y) of word w of z's delta presence row, both rows
+// target-major with wpr words.  Plain stores, no atomics; the threads of one
+// target read one presence row segment each.
+__global__ void dense_mark_in_k(IndexProbe rev, int zcol, int32_t lo1, uint32_t range1, uint32_t wpr,
+                                const uint32_t* pres, uint32_t* mark) {
+  const int64_t n = (int64_t)range1 * wpr;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t yb = (uint32_t)(i / wpr), wd = (uint32_t)(i % wpr);
+    const uint32_t kk = yb + (uint32_t)lo1 - (uint32_t)rev.key_lo;
+    uint32_t acc = 0;
+    if (kk < rev.key_range) {
+      const uint32_t e1 = rev.off[kk + 1];
+      for (uint32_t e = rev.off[kk]; e < e1; ++e) {
+        const uint32_t zb = rev.col[zcol][e] - (uint32_t)lo1;
+        if (zb < range1) acc |= pres[(u64)zb * wpr + wd];
+      }
+    }
+    mark[i] = acc;
+  }
+}
+hipError_t dense_mark_in(const IndexProbe& rev, int zcol, int32_t lo1, uint32_t range1, uint32_t nrank,
+                         const uint32_t* pres, uint32_t* mark, hipStream_t s) {
+  const uint32_t wpr = nrank / 32;
+  if (range1 == 0 || wpr == 0 || nrank % 32 != 0) return hipErrorInvalidValue;
+  dense_mark_in_k<<<grid_for((int64_t)range1 * wpr, 256, 65536), 256, 0, s>>>(rev, zcol, lo1, range1, wpr, pres,
+                                                                             mark);
+  return hipGetLastError();
+}
+
 // ============================================================ dense min/max heads, tiled rounds
 // Delta rows of a dense min/max head from its delta bits, in slot order
 // (rank-major, so grouped by rank and ascending in the second key), clearing
