@@ -3,15 +3,16 @@
 
 Workload: transitive closure plus per-source reach count over an R-MAT graph
 (2^14 nodes, 2^18 distinct edges, a=0.57 b=0.19 c=0.19 d=0.05, seed 5) -- the
-largest of the engine's five workloads.  One step is one complete
+largest of the engine's workloads.  One step is one complete
 xl_fixpoint_run of the program (index build, seed, every semi-naive round,
 the count stratum) with the input edges already resident in device memory;
 derived relations are cleared before each step.
 
-Prints one JSON line.  `roofline` covers the dominant kernel (the fused
-delta-expand / probe / insert kernel), timed live with HIP events on the
-engine's stream; `cpu_baseline` times the CPU oracle on a bounded sample of
-the same workload (the closure rows of a few sources).
+Prints one JSON line.  `roofline` covers the dominant kernel (for the
+headline the resident frontier kernel: every round of the closure, delta
+expand or in-edge pull + membership test + merge), timed live with HIP
+events on the engine's stream; `cpu_baseline` times the CPU oracle on a
+bounded sample of the same workload (the closure rows of a few sources).
 """
 from __future__ import annotations
 

@@ -151,7 +151,8 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *   "hash_min_log2"   log2 of the smallest hash table (default 22)
  *   "index_mode"      0 = automatic, 1 = always open-addressing hash tables,
  *                     2 = prefer dense key-domain tables where they fit
- *   "profile"         1 = time the fused join/insert kernels (receipt emit_*)
+ *   "profile"         1 = time the join kernels with HIP events (receipt
+ *                     emit_*, front_*, pull_*, wcoj_*)
  *   "pull_ratio"      closure-shaped strata over dense heads: a source whose
  *                     delta row has d bits and u unreached targets with an
  *                     in-edge is expanded by pulling (scanning in-edges of the
@@ -170,6 +171,9 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     with its row in LDS until its delta is empty, the pass
  *                     count and per-pass delta sizes read back once at the end
  *                     (default); 0 = one launch and one host read per pass
+ *   "wcoj_shorter"    triangle joins: 1 = probe each driver row's shorter Z
+ *                     list into the longer (default); 0 = always probe b's
+ *                     list (the candidate count of a binary join a x b)
  *   "dense_tiles"     rounds of a carried min/max rule over a dense head run
  *                     one workgroup per (first key, tile of second keys) with
  *                     the tile in LDS: 0 = choose the tile count (default),
