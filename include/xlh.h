@@ -171,6 +171,10 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     with its row in LDS until its delta is empty, the pass
  *                     count and per-pass delta sizes read back once at the end
  *                     (default); 0 = one launch and one host read per pass
+ *   "product_joins"   1 = a rule whose two join steps are both keyed by
+ *                     variables of the driver row (into a set head) runs as
+ *                     one launch over the product of the two match lists
+ *                     (default); 0 = materialize the first step's bindings
  *   "wcoj_shorter"    triangle joins: 1 = probe each driver row's shorter Z
  *                     list into the longer (default); 0 = always probe b's
  *                     list (the candidate count of a binary join a x b)

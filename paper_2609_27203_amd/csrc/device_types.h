@@ -157,6 +157,11 @@ struct StageArgs {
   RowSource src;
   int32_t has_index;
   IndexProbe idx;
+  // has_idx2: a second index whose key the driver row binds too; a driver
+  // row then yields the product of its two match lists (row k of the
+  // product: idx row k / deg2, idx2 row k % deg2)
+  int32_t has_idx2;
+  IndexProbe idx2;
   int32_t nops;
   MicroOp ops[MAXOPS];
   uint32_t consts[MAXK];

@@ -1605,7 +1605,32 @@ struct Runner {
     return XL_OK;
   }
 
-  xl_status eval_plan(const RulePlan& p) {
+  // Two index steps whose keys the driver row binds both (e.g. the children
+  // of both members of a same-generation pair): one launch walks the product
+  // of the two match lists, with both stages' micro-ops, instead of
+  // materializing the first step's bindings.  Set heads only: a row whose
+  // product is too long is refused by the kernel and the rule then runs
+  // again with the two steps apart, which insert-if-absent makes harmless.
+  bool product_plan(const RulePlan& p, const HeadRun* h, std::vector<MicroOp>* ops, std::vector<uint32_t>* consts) {
+    if (p.steps.size() != 2 || !h->is_set || h->frontier) return false;
+    const int k2 = p.steps[1].key_slot;
+    bool by_driver = false;
+    for (int j = 0; j < p.driver->arity; ++j)
+      by_driver = by_driver || (p.driver_act[j].kind == CA_BIND && p.driver_act[j].slot == k2);
+    if (!by_driver) return false;
+    *ops = p.stage_ops[0];
+    *consts = p.stage_consts[0];
+    const int shift = (int)p.stage_consts[0].size();
+    for (MicroOp op : p.stage_ops[1]) {
+      if (op.a < 0) op.a = (int8_t)(op.a - shift);
+      if (op.b < 0) op.b = (int8_t)(op.b - shift);
+      ops->push_back(op);
+    }
+    for (uint32_t v : p.stage_consts[1]) consts->push_back(v);
+    return ops->size() <= (size_t)MAXOPS && consts->size() <= (size_t)MAXK;
+  }
+
+  xl_status eval_plan(const RulePlan& p, bool allow_product = true) {
     HeadRun* h = head_of(p.head);
     if (h->frontier && p.driver_delta) return eval_frontier(p, h);
     if (h->ds && p.driver_delta) return eval_dense_pull(p, h);
@@ -1614,6 +1639,10 @@ struct Runner {
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
     if (src.n == 0) return XL_OK;
+    std::vector<MicroOp> pops;
+    std::vector<uint32_t> pconsts;
+    const bool product = allow_product && c->product_joins && product_plan(p, h, &pops, &pconsts);
+    bool refused = false;
     // materialized bindings between stages
     std::vector<std::unique_ptr<Buf>> live_bufs;
     RowSource rs{};
@@ -1634,8 +1663,18 @@ struct Runner {
         for (int j = 0; j < sp.rel->arity; ++j) a.idx.act[j] = sp.act[j];
       }
       XL_TRY(fill_ops(a, p, ks));
+      if (product) {
+        const StepPlan& s2 = p.steps[1];
+        a.has_idx2 = 1;
+        XL_TRY(get_index(s2.rel, s2.key_col, &a.idx2));
+        a.idx2.key_slot = (int8_t)s2.key_slot;
+        for (int j = 0; j < s2.rel->arity; ++j) a.idx2.act[j] = s2.act[j];
+        a.nops = (int)pops.size();
+        for (int i = 0; i < a.nops; ++i) a.ops[i] = pops[i];
+        for (size_t i = 0; i < pconsts.size(); ++i) a.consts[i] = pconsts[i];
+      }
       a.emit.counters = c->dcounters;
-      if (ks + 1 < nkst) {
+      if (!product && ks + 1 < nkst) {
         // intermediate: count -> scan -> materialize the live slots
         const std::vector<int>& live = p.live_after[ks];
         a.emit.mode = EM_MAT;
@@ -1795,9 +1834,12 @@ struct Runner {
           st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
           st->emit_new += (int64_t)(h->is_set ? cnt[CNT_APPENDED] : cnt[CNT_INSERTED] + cnt[CNT_APPENDED]);
         }
-        if (cnt[CNT_FATAL])
+        if (product && cnt[CNT_FATAL] == 16) {
+          refused = true;  // some product rows were skipped: the rule runs again unfused below
+        } else if (cnt[CNT_FATAL]) {
           return c->fail(XL_DEVICE_ERROR, h->dv ? "key outside the dense domain (internal)"
                                                 : "hash table probe exhausted or row list overflow (internal)");
+        }
         cands += (int64_t)cnt[CNT_CANDIDATES];
         if (h->dense) {
           h->keys += (int64_t)cnt[CNT_APPENDED];
@@ -1825,7 +1867,9 @@ struct Runner {
           h->didx_n = (int64_t)n2;
         }
       }
+      if (product) break;  // the one launch covered both steps
     }
+    if (refused) return eval_plan(p, false);
     return XL_OK;
   }
 

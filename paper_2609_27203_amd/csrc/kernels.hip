@@ -1313,6 +1313,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   KernArgs& a = *(KernArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   __shared__ uint32_t s_excl[ST_WAVES][64];
   __shared__ uint32_t s_beg[ST_WAVES][64];
+  __shared__ uint32_t s_beg2[ST_WAVES][64], s_deg2[ST_WAVES][64];
   __shared__ uint32_t s_v[ST_WAVES][MAXV][64];
   constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DMIN;
   __shared__ uint32_t s_out[STAGED ? ST_WAVES : 1][2][STAGED ? OUTB : 1];
@@ -1341,18 +1342,36 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     bool ok = row < a.src.n;
     if (ok) ok = bind_cols(a.src, row, v);
     if (HAS_INDEX) {
-      uint32_t beg = 0, deg = 0;
+      uint32_t beg = 0, deg = 0, beg2 = 0, deg2 = 1;
       if (ok) {
         const uint32_t kk = getv(v, a.idx.key_slot) - (uint32_t)a.idx.key_lo;
         if (kk < a.idx.key_range) {
           beg = a.idx.off[kk];
           deg = a.idx.off[kk + 1] - beg;
         }
+        if (a.has_idx2) {
+          const uint32_t k2 = getv(v, a.idx2.key_slot) - (uint32_t)a.idx2.key_lo;
+          deg2 = 0;
+          if (k2 < a.idx2.key_range) {
+            beg2 = a.idx2.off[k2];
+            deg2 = a.idx2.off[k2 + 1] - beg2;
+          }
+          // the wave's product count must stay below 2^32: a row beyond
+          // 2^24 products is refused (the host then runs the two steps apart)
+          if ((u64)deg * deg2 >= (1u << 24)) {
+            atomicOr(&a.emit.counters[CNT_FATAL], 16ull);
+            deg = 0;
+          } else {
+            deg *= deg2;
+          }
+        }
       }
       const uint32_t incl = wave_incl_scan(deg);
       const uint32_t total = __shfl(incl, 63, 64);
       s_excl[w][lane] = incl - deg;
       s_beg[w][lane] = beg;
+      s_beg2[w][lane] = beg2;
+      s_deg2[w][lane] = deg2;
 #pragma unroll
       for (int s = 0; s < MAXV; ++s) s_v[w][s][lane] = v[s];
       wave_lds_sync();
@@ -1367,8 +1386,13 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
 #pragma unroll
         for (int s = 0; s < MAXV; ++s) u[s] = s_v[w][s][r];
         if (act) {
-          const uint32_t erow = s_beg[w][r] + (j - s_excl[w][r]);
-          act = bind_cols(a.idx, erow, u);
+          const uint32_t k = j - s_excl[w][r];
+          if (a.has_idx2) {
+            const uint32_t d2 = s_deg2[w][r];
+            act = bind_cols(a.idx, s_beg[w][r] + k / d2, u) && bind_cols(a.idx2, s_beg2[w][r] + k % d2, u);
+          } else {
+            act = bind_cols(a.idx, s_beg[w][r] + k, u);
+          }
         }
         if (act) act = eval_ops<OPS>(a, u);
         emit<MODE>(a, u, act, st);

@@ -285,6 +285,45 @@ def test_index_cache_across_runs(name):
             assert seen[2][0] > 0
 
 
+# ------------------------------------------------------------- product joins
+@pytest.mark.parametrize("index_mode", [0, 1])
+@pytest.mark.parametrize("product", [0, 1])
+def test_product_joins_match_oracle(product, index_mode):
+    """Rules whose two join steps are both keyed by the driver row (same
+    generation's recursive rule, a filtered variant, a non-recursive pair
+    rule) give the oracle's rows with and without the one-launch product."""
+    base = W.small_workloads()["same_generation"]()
+    rules = W.SG_RULES + """
+cousins(X,Y) :- parent(X,A), sg(A,B), parent(Y,B), X < Y.
+pairs(X,Y) :- parent(A,X), parent(B,Y), parent(A,B).
+"""
+    wl = W.Workload("sg_product", rules, base.edb,
+                    {"sg": ("i32", "i32"), "cousins": ("i32", "i32"), "pairs": ("i32", "i32")})
+    print(f"case: product joins product={product} index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, _, _ = engine_run(wl, options={"product_joins": product, "index_mode": index_mode})
+    _compare(wl, rels, ref)
+
+
+def test_product_join_row_over_the_limit_runs_unfused():
+    """A driver row whose product of match lists reaches 2^24 is refused by
+    the one-launch kernel; the rule then runs again with the steps apart and
+    the result is still complete."""
+    n = 4096
+    edb = {"d": (("i32", "i32"), [np.array([0, 1], np.int32), np.array([0, 1], np.int32)]),
+           "p": (("i32", "i32"), [np.arange(n, dtype=np.int32), np.zeros(n, np.int32)]),
+           "q": (("i32", "i32"), [np.arange(n + 1, dtype=np.int32),
+                                   np.concatenate([np.zeros(n), [1]]).astype(np.int32)])}
+    wl = W.Workload("big_product", "h(X,Y) :- d(A,B), p(X,A), q(Y,B).", edb, {"h": ("i32", "i32")})
+    print("case: product over the limit", flush=True)
+    rels, _, _ = engine_run(wl, options={"product_joins": 1})
+    x, y = rels["h"]
+    # (a, b) = (0, 0): 4096 X times 4096 Y = 2^24 products in one row; (1, 1): no X
+    assert len(x) == n * n
+    key = x.astype(np.int64) * n + y
+    assert np.array_equal(key, np.arange(n * n, dtype=np.int64))
+
+
 COUNT_SHAPES_RULES = W.TC_RULES + """
 out_count(X,count(Y)) :- path(X,Y).
 in_count(Y,count(X)) :- path(X,Y).
