@@ -171,6 +171,12 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     with its row in LDS until its delta is empty, the pass
  *                     count and per-pass delta sizes read back once at the end
  *                     (default); 0 = one launch and one host read per pass
+ *   "batched_rounds"  rounds of a tiled min/max stratum (see "dense_tiles")
+ *                     enqueued per host read: every round takes its sizes
+ *                     from device memory and reports its delta size to a
+ *                     device array read once per batch; rounds past the
+ *                     fixpoint change nothing (default 4; 0 = one round and
+ *                     two host reads per pass; at most 64)
  *   "product_joins"   1 = a rule whose two join steps are both keyed by
  *                     variables of the driver row (into a set head) runs as
  *                     one launch over the product of the two match lists

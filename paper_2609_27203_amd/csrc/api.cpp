@@ -81,6 +81,11 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
       while (!c->icache.empty()) c->icache_drop(c->icache.front().rel, false);
     return XL_OK;
   }
+  if (!strcmp(key, "batched_rounds")) {
+    if (value < 0 || value > 64) return c->fail(XL_INVALID_ARGUMENT, "batched_rounds must be in [0, 64]");
+    c->batched_rounds = (int)value;
+    return XL_OK;
+  }
   if (!strcmp(key, "product_joins")) {
     if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "product_joins must be 0 or 1");
     c->product_joins = (int)value;

@@ -1549,8 +1549,161 @@ struct Runner {
   // workgroup per (rank, tile of second-key slots) with the tile in LDS.
   xl_status eval_dense_tiles(const RulePlan& p, HeadRun* h) {
     if (h->dn == 0) return XL_OK;
-    const StepPlan& sp = p.steps[0];
     DenseTileArgs a{};
+    XL_TRY(tile_args(p, h, a));
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+    HIP_TRY(c, k::dense_min_tiles(a, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->emit_ms += ms;
+      st->emit_launches++;
+      st->emit_source_rows += h->dn;
+      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->emit_new += (int64_t)cnt[CNT_APPENDED];
+    }
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    h->keys += (int64_t)cnt[CNT_INSERTED];
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
+  // Delta rows of a tiled head from its delta bits, grouped by rank (row
+  // counts per rank, their scan into roff, count and write passes); the row
+  // total goes to *total on the device.
+  xl_status tile_delta_rows(HeadRun* h, uint32_t* total, Buf* cnt, Buf* tmp, Buf* ltmp) {
+    const uint32_t wpr = (uint32_t)(h->range1 / 32);
+    const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+    HIP_TRY(c, k::row_popcount(h->dchg.as<uint32_t>(), h->n0, wpr, cnt->as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(cnt->as<uint32_t>(), h->roff.as<uint32_t>(), h->n0,
+                                     h->roff.as<uint32_t>() + h->n0, tmp->p, c->stream));
+    HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
+                                        h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
+                                        h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
+                                        total, ltmp->p, false, c->stream));
+    HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
+                                        h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
+                                        h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
+                                        total, ltmp->p, true, c->stream));
+    return XL_OK;
+  }
+
+  // Tiled min/max stratum, rounds enqueued in batches (option
+  // "batched_rounds"): every kernel of a round takes its sizes from device
+  // memory (the rank offsets of the delta rows, the delta bits), the delta
+  // row buffers hold any delta (one row per slot), and each round's delta
+  // size goes to a device array that the host reads once per batch.  Rounds
+  // enqueued past the fixpoint find an empty delta and change nothing, so
+  // the pass count and per-pass sizes are the round-by-round ones.
+  bool batched_tiles(const Stratum& s) {
+    if (c->batched_rounds <= 0 || heads.size() != 1 || !heads[0]->tiled || s.variants.size() != 1 ||
+        !s.variants[0].driver_delta || head_of(s.variants[0].head) != heads[0].get())
+      return false;
+    HeadRun* h = heads[0].get();
+    const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+    return (double)ns * 12 <= (double)c->arena.largest_free() / 2;  // delta rows for every slot
+  }
+
+  xl_status run_tiles_batched(const RulePlan& p, HeadRun* h, int64_t max_iterations) {
+    const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+    if (h->dcap < ns) {  // room for a delta row per slot, keeping the seed's rows
+      Buf nd[3];
+      for (int j = 0; j < 3; ++j) {
+        XL_TRY(dalloc(c, (size_t)ns * 4, &nd[j], "delta rows"));
+        if (h->dn)
+          HIP_TRY(c, hipMemcpyAsync(nd[j].p, h->drow[j].p, (size_t)h->dn * 4, hipMemcpyDeviceToDevice, c->stream));
+      }
+      for (int j = 0; j < 3; ++j) {
+        std::swap(h->drow[j].p, nd[j].p);
+        h->drow[j].c = c;
+      }
+      h->dcap = ns;
+    }
+    DenseTileArgs a{};
+    XL_TRY(tile_args(p, h, a));
+    const int B = c->batched_rounds;
+    Buf acc, rounds, cnt, tmp, ltmp;
+    XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
+    XL_TRY(dalloc(c, (size_t)B * 4, &rounds, "round delta sizes"));
+    XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->n0, 1) * 4, &cnt, "delta rows per rank"));
+    XL_TRY(dalloc(c, k::scan_temp_bytes(h->n0), &tmp, "scan scratch"));
+    XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &ltmp, "compaction scratch"));
+    HIP_TRY(c, hipMemsetAsync(acc.p, 0, 8 * CNT_N, c->stream));
+    a.counters = acc.as<unsigned long long>();
+    std::vector<hipEvent_t> evs;
+    if (c->profile) {
+      evs.resize(2 * (size_t)B, nullptr);
+      for (auto& e : evs) HIP_TRY(c, hipEventCreate(&e));
+    }
+    auto destroy_events = [&]() {
+      for (auto& e : evs)
+        if (e) (void)hipEventDestroy(e);
+      evs.clear();
+    };
+    int64_t pass = 0, delta = h->dn;
+    xl_status status = XL_OK;
+    while (delta > 0 && status == XL_OK) {
+      if (pass >= max_iterations) {
+        status = c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                     " reached before the fixpoint");
+        break;
+      }
+      const int nb = (int)std::min<int64_t>(B, max_iterations - pass);
+      for (int r = 0; r < nb; ++r) {
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
+        HIP_TRY(c, k::dense_min_tiles(a, c->stream));
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
+        XL_TRY(tile_delta_rows(h, rounds.as<uint32_t>() + r, &cnt, &tmp, &ltmp));
+      }
+      std::vector<uint32_t> n(nb);
+      XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));
+      int done = nb;
+      for (int r = 0; r < nb; ++r)
+        if (n[r] == 0) {
+          done = r + 1;
+          break;
+        }
+      for (int r = 0; r < done; ++r) {
+        st->iterations++;
+        record(n[r]);
+        st->new_tuples_total += n[r];
+        if (c->profile) {
+          float ms = 0;
+          HIP_TRY(c, hipEventElapsedTime(&ms, evs[2 * r], evs[2 * r + 1]));
+          st->emit_ms += ms;
+          st->emit_launches++;
+          st->emit_source_rows += r == 0 ? delta : n[r - 1];
+        }
+      }
+      pass += done;
+      delta = n[done - 1];
+    }
+    destroy_events();
+    u64 tot[CNT_N];
+    XL_TRY(ctl_read(c, acc.p, sizeof(tot), tot));
+    cands += (int64_t)tot[CNT_CANDIDATES];
+    if (c->profile) {
+      st->emit_candidates += (int64_t)tot[CNT_CANDIDATES];
+      st->emit_new += (int64_t)tot[CNT_APPENDED];
+    }
+    h->keys += (int64_t)tot[CNT_INSERTED];
+    h->dn = 0;
+    if (status != XL_OK) return status;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
+  // Arguments of the tiled min/max round kernel for the current delta rows.
+  xl_status tile_args(const RulePlan& p, HeadRun* h, DenseTileArgs& a) {
+    const StepPlan& sp = p.steps[0];
     a.dk1 = h->drow[1].as<uint32_t>();
     a.dval = h->drow[2].as<uint32_t>();
     a.roff = h->roff.as<uint32_t>();
@@ -1582,26 +1735,6 @@ struct Runner {
     a.pres = h->dpres.as<uint32_t>();
     a.chg = h->dchg.as<uint32_t>();
     a.counters = c->dcounters;
-    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
-    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
-    HIP_TRY(c, k::dense_min_tiles(a, c->stream));
-    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
-    u64 cnt[CNT_N];
-    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
-    if (c->profile) {
-      float ms = 0;
-      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
-      st->emit_ms += ms;
-      st->emit_launches++;
-      st->emit_source_rows += h->dn;
-      st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
-      st->emit_new += (int64_t)cnt[CNT_APPENDED];
-    }
-    cands += (int64_t)cnt[CNT_CANDIDATES];
-    h->keys += (int64_t)cnt[CNT_INSERTED];
-    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
-      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
-                                               std::to_string(h->rel->max_rows));
     return XL_OK;
   }
 
@@ -2364,6 +2497,10 @@ struct Runner {
       st->new_tuples_total += d;
     }
     record(total);
+    if (s.recursive && total > 0 && batched_tiles(s)) {
+      XL_TRY(run_tiles_batched(s.variants[0], heads[0].get(), max_iterations));
+      total = 0;
+    }
     if (s.recursive && total > 0 && resident_frontier(s)) {
       if (max_iterations == 0)
         return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap 0 reached before the fixpoint");

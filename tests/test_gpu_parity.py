@@ -378,20 +378,38 @@ def test_sum_and_logsumexp_heads_dense_and_hashed(name, index_mode):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+@pytest.mark.parametrize("batch", [0, 1, 4, 64])
 @pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
-def test_min_rounds_tiled_and_untiled(tiles):
+def test_min_rounds_tiled_and_untiled(tiles, batch):
     """Carried min rule over a dense head: one workgroup per (source, tile of
     targets) with the tile in LDS (1 tile, 7 uneven tiles, the automatic
-    choice) or the untiled emission (-1); all match the oracle bit for bit
-    and give the same per-round delta sizes."""
+    choice) or the untiled emission (-1), tiled rounds enqueued one at a
+    time or in batches of 1, 4 or 64 per host read; all match the oracle bit
+    for bit and give the same per-round delta sizes and pass count."""
     wl = W.small_workloads()["sssp"]()
-    print(f"case: min tiles={tiles}", flush=True)
+    print(f"case: min tiles={tiles} batch={batch}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, stats, _ = engine_run(wl, options={"dense_tiles": tiles})
+    rels, stats, _ = engine_run(wl, options={"dense_tiles": tiles, "batched_rounds": batch})
     assert_same_relation("dist", wl.idb["dist"], rels["dist"], ref.relations["dist"][1], tol=(0.0, 0.0))
-    base, _, _ = engine_run(wl, options={"dense_tiles": -1})
-    if tiles != -1:
-        assert stats["delta_rows"] == engine_run(wl, options={"dense_tiles": -1})[1]["delta_rows"]
+    if tiles != -1 or batch:
+        base = engine_run(wl, options={"dense_tiles": -1, "batched_rounds": 0})[1]
+        assert stats["delta_rows"] == base["delta_rows"]
+        assert stats["iterations"] == base["iterations"]
+
+
+@pytest.mark.parametrize("batch", [0, 4])
+def test_min_rounds_iteration_cap(batch):
+    """A cap below the pass count is a convergence failure in both forms; the
+    exact pass count converges."""
+    from paper_2609_27203_amd import xlh
+    wl = W.small_workloads()["sssp"]()
+    print(f"case: min cap batch={batch}", flush=True)
+    passes = engine_run(wl, options={"batched_rounds": 0})[1]["iterations"]
+    for cap in (0, 1, passes - 1):
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, max_iterations=cap, options={"batched_rounds": batch})
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+    assert engine_run(wl, max_iterations=passes, options={"batched_rounds": batch})[1]["iterations"] == passes
 
 
 SELF_JOIN_TC = """

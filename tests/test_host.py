@@ -159,9 +159,10 @@ def test_options():
     c.set_option("index_cache_mb", 64)
     c.set_option("index_cache_mb", 0)
     c.set_option("product_joins", 0)
+    c.set_option("batched_rounds", 8)
     for k, v in [("hash_min_log2", 3), ("nope", 1), ("profile", 7), ("pull_ratio", 2000),
                  ("index_mode", -1), ("dense_tiles", -2),
                  ("frontier_resident", 2), ("index_cache_mb", -1),
-                 ("product_joins", 3)]:
+                 ("product_joins", 3), ("batched_rounds", 65)]:
         with pytest.raises(xlh.XlError):
             c.set_option(k, v)
