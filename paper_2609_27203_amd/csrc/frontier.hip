@@ -384,6 +384,10 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_resident_k(FrontierArgs a
         if (threadIdx.x == 0) atomicOr(a.overflow, 1u);
         break;
       }
+      if (a.pull_ratio && tnu == 0) {  // every target with an in-edge is reached:
+        ++round;                       // this round finds nothing and ends x's passes
+        break;
+      }
       const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
       frontier_expand(a, old_row, new_row, f_row, pull, L, cands);
       // the new bits become the next delta; the row takes them
