@@ -7,8 +7,16 @@ here from the definitions below), and it is deliberately slow and direct.
 
 What it computes (the plain definition the semi-naive method reaches):
 
-* Relations are sets of typed tuples (Sec. 3.1-3.2 of the paper).  Columns are
-  int32 ("i32") or IEEE-754 binary32 ("f32").
+* Relations are sets of typed tuples (Sec. 3.1-3.2 of the paper).  Column
+  types are the paper's scalar types other than symbol (Sec. 3.2, type
+  system): "i32", "u32", "i64", "u64" (integers of those widths), "bool"
+  (false < true), "f32" and "f64" (IEEE-754 binary32 / binary64).  Values of
+  every type but f32 are equal when identical and ordered by the type's
+  order; for f64 that order is IEEE 754 totalOrder, so -0.0 < +0.0 and the two
+  are different values.  f32 keeps IEEE comparison (-0.0 == +0.0).  A
+  constant must be a value of the column type it meets (an integer literal in
+  the column's range, a decimal literal for a float column).  ``is``
+  arithmetic, sum and logsumexp take i32 and f32 values only.
 * The immediate-consequence operator T_P(I) enumerates every derivation of a
   rule -- one fact per body atom, all agreeing on shared variables, all
   comparison filters true -- against the input relations plus I, computes the
@@ -67,7 +75,7 @@ class ConvergenceFailure(RuntimeError):
 # --------------------------------------------------------------------------
 _TOKEN = re.compile(r"""
     (?P<ws>\s+|//[^\n]*)
-  | (?P<num>\d+\.\d*(?:[eE][-+]?\d+)?|\d+[eE][-+]?\d+|\d+)
+  | (?P<num>\d+\.\d+(?:[eE][-+]?\d+)?|\d+[eE][-+]?\d+|\d+)
   | (?P<name>[A-Za-z_][A-Za-z0-9_]*)
   | (?P<op>:-|!=|==|<=|>=|<|>|[(),.+-])
 """, re.VERBOSE)
@@ -199,9 +207,47 @@ def parse(text: str) -> list:
 
 
 # --------------------------------------------------------------------------
-# Relations: (types, [columns]) with numpy int32 / float32 columns.
+# Relations: (types, [columns]) with numpy columns of the types' dtypes.
 # --------------------------------------------------------------------------
-_NP = {"i32": np.int32, "f32": np.float32}
+_NP = {"i32": np.int32, "f32": np.float32, "u32": np.uint32, "i64": np.int64, "u64": np.uint64,
+       "f64": np.float64, "bool": np.bool_}
+_INT_RANGE = {"i32": (-2 ** 31, 2 ** 31 - 1), "u32": (0, 2 ** 32 - 1), "i64": (-2 ** 63, 2 ** 63 - 1),
+              "u64": (0, 2 ** 64 - 1), "bool": (0, 1)}
+_SIGN64 = np.uint64(1 << 63)
+
+
+def _const(t, ty):
+    """Constant term t as a value of column type ty; TypeError if it is not one."""
+    if ty in ("f32", "f64"):
+        if t[0] != "float":
+            raise TypeError(f"constant {t[1]!r} is not a {ty} value")
+        return np.asarray(t[1], _NP[ty])
+    lo, hi = _INT_RANGE[ty]
+    if t[0] != "int" or not lo <= t[1] <= hi:
+        raise TypeError(f"constant {t[1]!r} is not a {ty} value")
+    return np.asarray(t[1], _NP[ty])
+
+
+def _order(c):
+    """Keys whose numeric order is the column type's order: f64 values by IEEE
+    754 totalOrder (negative values: every bit flipped; others: the sign bit
+    set, as unsigned 64-bit integers); other types as they are."""
+    c = np.asarray(c)
+    if c.dtype == np.float64:
+        b = c.view(np.uint64)
+        return np.where((b & _SIGN64) != 0, ~b, b | _SIGN64)
+    return c
+
+
+def _from_order(k):
+    """Inverse of _order for f64 keys."""
+    k = np.asarray(k, np.uint64)
+    return np.where((k & _SIGN64) != 0, k & ~_SIGN64, ~k).view(np.float64)
+
+
+def _eq(col, val):
+    """Equality of values: identity for f64, IEEE equality for f32."""
+    return _bits(col) == _bits(np.asarray(val, col.dtype)) if col.dtype == np.float64 else col == val
 
 
 def _empty(types):
@@ -209,11 +255,12 @@ def _empty(types):
 
 
 def _canonical(types, cols):
-    """Distinct rows in ascending lexicographic order (int32 signed, f32 by value)."""
+    """Distinct rows in ascending lexicographic order (each column in its
+    type's order; f32 by value)."""
     cols = [np.asarray(c, _NP[t]) for t, c in zip(types, cols)]
     if len(cols[0]) == 0:
         return (tuple(types), cols)
-    order = np.lexsort(cols[::-1])
+    order = np.lexsort([_order(c) for c in cols][::-1])
     cols = [c[order] for c in cols]
     keep = np.ones(len(cols[0]), bool)
     same = np.ones(len(cols[0]) - 1, bool)
@@ -224,7 +271,9 @@ def _canonical(types, cols):
 
 
 def _bits(c):
-    return c.view(np.int32) if c.dtype == np.float32 else c
+    if c.dtype == np.float32:
+        return c.view(np.int32)
+    return c.view(np.int64) if c.dtype == np.float64 else c
 
 
 def _identical(a, b):
@@ -236,9 +285,15 @@ def _join_codes(left, right):
     """Dense integer codes such that equal codes <=> equal values in every column."""
     nl = len(left[0]) if left else 0
     code = None
+    def ident(c):  # equal entries <=> equal values (f32 by IEEE value, f64 by identity)
+        if c.dtype == np.float32:
+            return np.asarray(c, np.float64)
+        if c.dtype in (np.float64, np.uint64):
+            return c.view(np.int64)
+        return np.asarray(c, np.int64)
+
     for lc, rc in zip(left, right):
-        vals = np.concatenate([np.asarray(lc, np.float64 if lc.dtype == np.float32 else np.int64),
-                               np.asarray(rc, np.float64 if rc.dtype == np.float32 else np.int64)])
+        vals = np.concatenate([ident(lc), ident(rc)])
         _, inv = np.unique(vals, return_inverse=True)
         inv = inv.astype(np.int64)
         code = inv if code is None else np.unique(code * (inv.max() + 1) + inv,
@@ -259,7 +314,7 @@ def _eval_body(rule, rels, var_types):
         first = {}
         for j, t in enumerate(terms):
             if t[0] in ("int", "float"):
-                mask &= cols[j] == np.asarray(t[1], _NP[types[j]])
+                mask &= _eq(cols[j], _const(t, types[j]))
             elif t[0] == "var":
                 if var_types.setdefault(t[1], types[j]) != types[j]:
                     raise TypeError(f"variable {t[1]} used at two types")
@@ -306,8 +361,10 @@ def _eval_body(rule, rels, var_types):
             else:
                 raise ValueError("'_' cannot appear in arithmetic")
         if len(ptypes) != 1:
-            raise TypeError(f"mixed i32/f32 arithmetic for {var}")
+            raise TypeError(f"mixed-type arithmetic for {var}")
         ty = ptypes.pop()
+        if ty not in ("i32", "f32"):
+            raise TypeError(f"arithmetic on {ty} values is not supported")
         acc = np.zeros(n, np.float64 if ty == "f32" else np.int64)
         for sign, v in vals:
             acc = acc + sign * np.asarray(v, acc.dtype)
@@ -318,10 +375,19 @@ def _eval_body(rule, rels, var_types):
     for pred, terms in rule.negs:
         mask &= ~_negated_match(pred, terms, rels, binding, var_types, n)
     for op, a, b in rule.filters:
-        av = binding[a[1]] if a[0] == "var" else a[1]
-        bv = binding[b[1]] if b[0] == "var" else b[1]
+        ta = var_types[a[1]] if a[0] == "var" else None
+        tb = var_types[b[1]] if b[0] == "var" else None
+        if ta and tb and ta != tb:
+            raise TypeError(f"comparison between {ta} and {tb}")
+        ty = ta or tb
+        if ty is None:  # two constants: their natural types
+            ty = "f32" if a[0] == "float" else "i32"
+            if ("f32" if b[0] == "float" else "i32") != ty:
+                raise TypeError("comparison between i32 and f32")
+        av = binding[a[1]] if a[0] == "var" else _const(a, ty)
+        bv = binding[b[1]] if b[0] == "var" else _const(b, ty)
         mask &= {"!=": np.not_equal, "==": np.equal, "<": np.less, "<=": np.less_equal,
-                 ">": np.greater, ">=": np.greater_equal}[op](av, bv)
+                 ">": np.greater, ">=": np.greater_equal}[op](_order(av), _order(bv))
     return {v: c[mask] for v, c in binding.items()}, int(mask.sum())
 
 
@@ -335,7 +401,7 @@ def _negated_match(pred, terms, rels, binding, var_types, n):
     first = {}
     for j, t in enumerate(terms):
         if t[0] in ("int", "float"):
-            mask &= cols[j] == np.asarray(t[1], _NP[types[j]])
+            mask &= _eq(cols[j], _const(t, types[j]))
         elif t[0] == "var":
             if t[1] not in binding:
                 raise ValueError(f"{t[1]} occurs only in a negated literal")
@@ -359,24 +425,29 @@ def _fold(op, keys, vals, ty):
     """Group rows by the key columns and fold vals over each group's derivations."""
     if len(vals) == 0:
         return keys, vals
-    order = np.lexsort(keys[::-1]) if keys else np.arange(len(vals))
+    order = np.lexsort([_order(k) for k in keys][::-1]) if keys else np.arange(len(vals))
     keys = [k[order] for k in keys]
     vals = vals[order]
     start = np.ones(len(vals), bool)
     if keys:
         start[1:] = False
         for k in keys:
-            start[1:] |= k[1:] != k[:-1]
+            start[1:] |= _bits(k)[1:] != _bits(k)[:-1]
     else:
         start[1:] = False
     idx = np.flatnonzero(start)
     gkeys = [k[idx] for k in keys]
     if op == "count":
         out = np.diff(np.append(idx, len(vals))).astype(np.int32)
+    elif op in ("min", "max") and ty == "f64":  # by totalOrder
+        red = np.minimum if op == "min" else np.maximum
+        out = _from_order(red.reduceat(_order(vals), idx))
     elif op == "min":
         out = np.minimum.reduceat(vals, idx)
     elif op == "max":
         out = np.maximum.reduceat(vals, idx)
+    elif op in ("sum", "logsumexp") and ty not in ("i32", "f32"):
+        raise TypeError(f"{op} over {ty} values is not supported")
     elif op == "sum":
         if ty == "f32":
             out = np.add.reduceat(vals.astype(np.float64), idx).astype(np.float32)

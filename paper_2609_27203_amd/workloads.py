@@ -342,6 +342,43 @@ def triangle(rows: int = 1 << 16, core: int = 161, hubs: int = 8, seed: int = 6,
                     {"rows": rows, "core": core, "hubs": hubs, "seed": seed})
 
 
+# ---------------------------------------------------------------- typed labels
+TYPED_KINDS = ("u32", "i64", "u64", "f64")
+
+
+def typed_labels(kind: str, n: int) -> np.ndarray:
+    """n distinct values of a column type in strictly ascending order of that
+    type (f64: IEEE totalOrder), spread over the type's range: the extremes,
+    values either side of the signed/unsigned boundary, and for f64 both
+    zeros (-0.0 before +0.0), subnormals and negatives.  Node i of a graph
+    drawn over 0..n-1 becomes label i, so any order-based result over the
+    labels is the i32 result relabelled."""
+    assert n >= 8
+    h = n // 2
+    i = np.arange(n, dtype=object)
+    if kind == "u32":
+        vals = [2 ** 31 - 3 * h + 3 * int(k) for k in i]
+        vals[0], vals[-1] = 0, 2 ** 32 - 1
+        return np.array(vals, dtype=np.uint64).astype(np.uint32)
+    if kind == "i64":
+        vals = [(int(k) - h) * 2 ** 34 + 11 for k in i]
+        vals[0], vals[-1] = -2 ** 63, 2 ** 63 - 1
+        return np.array(vals, dtype=np.int64)
+    if kind == "u64":
+        vals = [2 ** 63 - h * 2 ** 20 + int(k) * 2 ** 20 for k in i]
+        vals[0], vals[-1] = 0, 2 ** 64 - 1
+        return np.array(vals, dtype=np.uint64)
+    if kind == "f64":
+        neg = [-(h - 1 - k) * 0.75 - 5e-324 for k in range(h - 1)]   # ascending negatives
+        pos = [5e-324] + [(k + 1) * 1.25 for k in range(n - h - 2)]
+        vals = neg[:-1] + [-5e-324, -0.0, 0.0] + pos
+        assert len(vals) == n, len(vals)
+        vals[0] = -1.7976931348623157e308
+        vals[-1] = 1.7976931348623157e308
+        return np.array(vals, dtype=np.float64)
+    raise KeyError(kind)
+
+
 def full_workloads():
     return {
         "tc_uniform": tc_uniform,
