@@ -65,7 +65,23 @@ typedef enum {
     XL_PARSE_ERROR = 8         /* the rule text does not parse */
 } xl_status;
 
-typedef enum { XL_I32 = 1, XL_F32 = 2 } xl_type;
+/*
+ * Column types: the paper's scalar types (Sec. 3.2 "Type system") except
+ * symbol.  Element sizes at the load/read boundary: XL_BOOL 1 byte (0 or 1),
+ * XL_I32 / XL_U32 / XL_F32 4 bytes, XL_I64 / XL_U64 / XL_F64 8 bytes.
+ * Values are equal when identical; order is signed for i32 and i64,
+ * unsigned for u32 and u64, false < true, IEEE 754 totalOrder for f64
+ * (so -0.0 < +0.0 and the two never join).  f32 keeps IEEE comparison and
+ * equality.  Arithmetic (`is`), sum and logsumexp take i32 and f32 only.
+ * Internally every column is 4 bytes: u32 and bool are stored as an
+ * order-preserving int32 image; i64, u64 and f64 as ranks in a per-context
+ * sorted dictionary of the distinct values loaded so far (8 bytes of
+ * workspace per distinct value, never shrunk while the context lives; a load
+ * that adds values renumbers the columns already stored, an O(rows) pass).
+ */
+typedef enum {
+    XL_I32 = 1, XL_F32 = 2, XL_U32 = 3, XL_I64 = 4, XL_U64 = 5, XL_F64 = 6, XL_BOOL = 7
+} xl_type;
 
 typedef struct xl_context xl_context;
 typedef struct xl_relation xl_relation;
@@ -203,10 +219,12 @@ xl_status xl_relation_create(xl_context* ctx, const char* name, int arity,
 
 /*
  * Replace the relation's contents with `nrows` rows given column-wise:
- * cols[j] points at nrows int32 or float32 values (host memory, or device
- * memory when cols_on_device != 0).  The data is copied into the workspace;
- * the pointers are only borrowed for the call.  Duplicate rows are removed
- * (relations are sets).  Returns after the copy has completed.
+ * cols[j] points at nrows values of column j's type, packed at that type's
+ * element size (host memory, or device memory when cols_on_device != 0).
+ * The data is copied into the workspace; the pointers are only borrowed for
+ * the call.  Duplicate rows are removed (relations are sets).  A bool byte
+ * other than 0 or 1 is XL_INVALID_ARGUMENT (nothing is stored).  Returns
+ * after the copy has completed.
  */
 xl_status xl_relation_load(xl_relation* rel, const void* const* cols, int64_t nrows,
                            int cols_on_device);
@@ -219,9 +237,9 @@ xl_status xl_relation_size(const xl_relation* rel, int64_t* out_rows);
 
 /*
  * Copy the relation out in canonical order: rows ascending lexicographically
- * by column (int32 signed, float32 by IEEE totalOrder).  cols[j] receives
- * the j-th column (host or device memory per cols_on_device) and must hold
- * capacity_rows values.  If the relation has more rows, nothing is copied,
+ * by column, each column in its type's order (float32 by IEEE totalOrder).
+ * cols[j] receives the j-th column at its type's element size (host or
+ * device memory per cols_on_device) and must hold capacity_rows values.  If the relation has more rows, nothing is copied,
  * *out_rows is set to the number needed and XL_CAPACITY_EXCEEDED returned.
  */
 xl_status xl_relation_read(const xl_relation* rel, void* const* cols, int64_t capacity_rows,

@@ -20,7 +20,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libxlh.so")
 ARCH = os.environ.get("XLH_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["kernels.hip", "frontier.hip", "wcoj.hip", "engine.cpp", "frontend.cpp", "api.cpp"]
+SOURCES = ["kernels.hip", "frontier.hip", "wcoj.hip", "coding.hip", "engine.cpp", "frontend.cpp", "api.cpp"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

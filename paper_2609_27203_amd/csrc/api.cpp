@@ -125,12 +125,15 @@ xl_status xl_relation_create(xl_context* c, const char* name, int arity, const x
     if (!isalnum((unsigned char)*p) && *p != '_') return c->fail(XL_INVALID_ARGUMENT, "bad relation name");
   if (c->find(name)) return c->fail(XL_INVALID_ARGUMENT, std::string("relation '") + name + "' already exists");
   for (int j = 0; j < arity; ++j)
-    if (cols[j] != XL_I32 && cols[j] != XL_F32) return c->fail(XL_INVALID_ARGUMENT, "column types are XL_I32 or XL_F32");
+    if (cols[j] < XL_I32 || cols[j] > XL_BOOL) return c->fail(XL_INVALID_ARGUMENT, "unknown column type");
   auto* r = new xl_relation();
   r->ctx = c;
   r->name = name;
   r->arity = arity;
-  for (int j = 0; j < arity; ++j) r->types[j] = cols[j] == XL_I32 ? T_I32 : T_F32;
+  for (int j = 0; j < arity; ++j) {
+    r->ltypes[j] = (uint8_t)cols[j];
+    r->types[j] = phys_type(cols[j]);
+  }
   r->max_rows = max_rows;
   c->rels.push_back(r);
   *out = r;

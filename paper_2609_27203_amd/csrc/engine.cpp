@@ -203,7 +203,146 @@ xl_status compute_bounds(Context* c, Relation* r) {
   return XL_OK;
 }
 
+// Images of n order keys (device) of the 8-byte type lt: their ranks in the
+// context's dictionary after the keys new to it are added.  Adding keys
+// renumbers the dictionary, so every stored column of type lt is remapped
+// (old rank -> new rank, order kept) and its relation gets a new generation.
+xl_status dict_encode(Context* c, int lt, const u64* keys, int64_t n, uint32_t* images) {
+  if (n <= 0) return XL_OK;
+  const int64_t nd = c->dict_n[lt], nt = nd + n;
+  Buf cat, alt, tmp, flag, pos, stmp, tot;
+  XL_TRY(dalloc(c, (size_t)nt * 8, &cat, "dictionary merge"));
+  XL_TRY(dalloc(c, (size_t)nt * 8, &alt, "dictionary merge"));
+  XL_TRY(dalloc(c, k::radix_temp_bytes(nt), &tmp, "sort scratch"));
+  if (nd > 0)
+    HIP_TRY(c, hipMemcpyAsync(cat.p, c->dict[lt], (size_t)nd * 8, hipMemcpyDeviceToDevice, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(cat.as<u64>() + nd, keys, (size_t)n * 8, hipMemcpyDeviceToDevice, c->stream));
+  int a = 0;
+  HIP_TRY(c, k::radix_sort_u64(cat.as<u64>(), nullptr, alt.as<u64>(), nullptr, nt, 64, tmp.p, c->stream, &a));
+  const u64* sorted = a ? alt.as<u64>() : cat.as<u64>();
+  XL_TRY(dalloc(c, (size_t)nt * 4, &flag, "dictionary flags"));
+  XL_TRY(dalloc(c, (size_t)nt * 4, &pos, "dictionary positions"));
+  XL_TRY(dalloc(c, k::scan_temp_bytes(nt), &stmp, "scan scratch"));
+  XL_TRY(dalloc(c, 8, &tot, "count"));
+  HIP_TRY(c, k::unique_flags64(sorted, nt, flag.as<uint32_t>(), c->stream));
+  HIP_TRY(c, k::scan_exclusive_u32(flag.as<uint32_t>(), pos.as<uint32_t>(), nt, tot.as<uint32_t>(), stmp.p,
+                                   c->stream));
+  uint32_t m = 0;
+  XL_TRY(ctl_read(c, tot.p, 4, &m));
+  if (m > (uint32_t)nd) {
+    if (m >= (1u << 31))
+      return c->fail(XL_CAPACITY_EXCEEDED, std::string("more than 2^31 distinct ") + type_name(lt) + " values");
+    Buf nd_keys;
+    XL_TRY(dalloc(c, (size_t)m * 8, &nd_keys, "type dictionary"));
+    HIP_TRY(c, k::compact64(sorted, flag.as<uint32_t>(), pos.as<uint32_t>(), nd_keys.as<u64>(), nt, c->stream));
+    if (nd > 0) {
+      Buf map;
+      XL_TRY(dalloc(c, (size_t)nd * 4, &map, "dictionary renumbering"));
+      HIP_TRY(c, k::rank64(nd_keys.as<u64>(), m, c->dict[lt], nd, map.as<uint32_t>(), c->stream));
+      for (Relation* r : c->rels) {
+        bool touched = false;
+        for (int j = 0; j < r->arity; ++j)
+          if (r->ltypes[j] == lt && r->nrows > 0 && r->col[j]) {
+            HIP_TRY(c, k::remap_codes(r->col[j], r->nrows, map.as<uint32_t>(), c->stream));
+            touched = true;
+          }
+        if (touched) {
+          r->generation = ++c->generations;
+          c->icache_drop(r, true);
+          XL_TRY(compute_bounds(c, r));
+        }
+      }
+    }
+    c->arena.release(c->dict[lt]);
+    c->dict[lt] = (unsigned long long*)nd_keys.keep();
+    c->dict_n[lt] = m;
+  }
+  HIP_TRY(c, k::rank64(c->dict[lt], c->dict_n[lt], keys, n, images, c->stream));
+  return XL_OK;
+}
+
+// Int32 images of the columns of r given to a load (n values each, in host or
+// device memory, packed at each type's element size) written to img[j] for
+// the columns of type u32, bool, i64, u64 or f64.  The columns of one 8-byte
+// type go through one dictionary update together, so no image of this load
+// is renumbered by a later one.
+xl_status encode_columns(Context* c, const Relation* r, const void* const* cols, int64_t n, int on_device,
+                         uint32_t* const* img) {
+  const hipMemcpyKind kind = on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+  for (int lt : {XL_U32, XL_BOOL}) {
+    for (int j = 0; j < r->arity; ++j) {
+      if (r->ltypes[j] != lt) continue;
+      const size_t es = elem_bytes(lt);
+      Buf in, bad;
+      XL_TRY(dalloc(c, (size_t)n * es, &in, "loaded column"));
+      XL_TRY(dalloc(c, 4, &bad, "check flag"));
+      HIP_TRY(c, hipMemcpyAsync(in.p, cols[j], (size_t)n * es, kind, c->stream));
+      HIP_TRY(c, hipMemsetAsync(bad.p, 0, 4, c->stream));
+      HIP_TRY(c, k::encode_narrow(in.p, lt, n, img[j], bad.as<uint32_t>(), c->stream));
+      uint32_t flag = 0;
+      XL_TRY(ctl_read(c, bad.p, 4, &flag));
+      if (flag)
+        return c->fail(XL_INVALID_ARGUMENT,
+                       "bool column " + std::to_string(j) + " of " + r->name + " holds a byte other than 0 or 1");
+    }
+  }
+  for (int lt : {XL_I64, XL_U64, XL_F64}) {
+    std::vector<int> js;
+    for (int j = 0; j < r->arity; ++j)
+      if (r->ltypes[j] == lt) js.push_back(j);
+    if (js.empty()) continue;
+    const int64_t m = n * (int64_t)js.size();
+    Buf in, keys, imgs;
+    XL_TRY(dalloc(c, (size_t)n * 8, &in, "loaded column"));
+    XL_TRY(dalloc(c, (size_t)m * 8, &keys, "order keys"));
+    XL_TRY(dalloc(c, (size_t)m * 4, &imgs, "column images"));
+    for (size_t q = 0; q < js.size(); ++q) {
+      HIP_TRY(c, hipMemcpyAsync(in.p, cols[js[q]], (size_t)n * 8, kind, c->stream));
+      HIP_TRY(c, k::order_keys64(in.as<u64>(), lt, n, keys.as<u64>() + (int64_t)q * n, c->stream));
+    }
+    XL_TRY(dict_encode(c, lt, keys.as<u64>(), m, imgs.as<uint32_t>()));
+    for (size_t q = 0; q < js.size(); ++q)
+      HIP_TRY(c, hipMemcpyAsync(img[js[q]], imgs.as<uint32_t>() + (int64_t)q * n, (size_t)n * 4,
+                                hipMemcpyDeviceToDevice, c->stream));
+  }
+  return XL_OK;
+}
+
 }  // namespace
+
+// Give every constant of an 8-byte type in p's plans its current image,
+// adding the values the dictionaries lack.
+xl_status resolve_wide_constants(Program* p) {
+  Context* c = p->ctx;
+  for (int lt : {XL_I64, XL_U64, XL_F64}) {
+    std::vector<u64> keys;
+    std::vector<uint32_t*> dst;
+    for (Stratum& st : p->strata)
+      for (std::vector<RulePlan>* v : {&st.full, &st.variants})
+        for (RulePlan& rp : *v)
+          for (const WideConst& w : rp.wconsts) {
+            if (w.ltype != lt) continue;
+            keys.push_back(w.key);
+            dst.push_back(w.where == 0   ? &rp.driver_act[w.a].cval
+                          : w.where == 1 ? &rp.steps[w.a].act[w.b].cval
+                                         : &rp.stage_consts[w.a][w.b]);
+          }
+    if (keys.empty()) continue;
+    const int64_t n = (int64_t)keys.size();
+    Buf dk, di;
+    XL_TRY(dalloc(c, (size_t)n * 8, &dk, "constant keys"));
+    XL_TRY(dalloc(c, (size_t)n * 4, &di, "constant images"));
+    HIP_TRY(c, hipMemcpyAsync(dk.p, keys.data(), (size_t)n * 8, hipMemcpyHostToDevice, c->stream));
+    XL_TRY(dict_encode(c, lt, dk.as<u64>(), n, di.as<uint32_t>()));
+    std::vector<uint32_t> img((size_t)n);
+    for (int64_t i0 = 0; i0 < n; i0 += 1024) {
+      const int64_t m = std::min<int64_t>(1024, n - i0);
+      XL_TRY(ctl_read(c, di.as<uint32_t>() + i0, (size_t)m * 4, img.data() + i0));
+    }
+    for (int64_t i = 0; i < n; ++i) *dst[(size_t)i] = img[(size_t)i];
+  }
+  return XL_OK;
+}
 
 void relation_free_storage(Relation* r) {
   for (int j = 0; j < MAXC; ++j) {
@@ -233,11 +372,15 @@ xl_status relation_load(Relation* r, const void* const* cols, int64_t n, int on_
     return XL_OK;
   }
   Buf raw[MAXC];
+  uint32_t* img[MAXC] = {};
   for (int j = 0; j < r->arity; ++j) {
     XL_TRY(dalloc(c, (size_t)n * 4, &raw[j], "loaded column"));
-    HIP_TRY(c, hipMemcpyAsync(raw[j].p, cols[j], (size_t)n * 4,
-                              on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+    img[j] = raw[j].as<uint32_t>();
+    if (r->ltypes[j] == XL_I32 || r->ltypes[j] == XL_F32)
+      HIP_TRY(c, hipMemcpyAsync(raw[j].p, cols[j], (size_t)n * 4,
+                                on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
   }
+  XL_TRY(encode_columns(c, r, cols, n, on_device, img));
   int64_t m = n;
   Buf fin[MAXC];
   if (n == 1) {
@@ -300,13 +443,26 @@ xl_status relation_read(const Relation* r, void* const* cols, int64_t cap, int64
       if (!cols[j]) return c->fail(XL_INVALID_ARGUMENT, "null column pointer");
     Buf perm;
     XL_TRY(lex_perm(c, r->col, r->types, r->arity, n, &perm));
-    Buf stage;
-    if (!on_device) XL_TRY(dalloc(c, (size_t)n * 4, &stage, "readout staging"));
+    Buf stage, img;
     for (int j = 0; j < r->arity; ++j) {
-      uint32_t* dst = on_device ? (uint32_t*)cols[j] : stage.as<uint32_t>();
-      HIP_TRY(c, k::gather_u32(r->col[j], perm.as<uint32_t>(), dst, n, c->stream));
-      if (!on_device) {
-        HIP_TRY(c, hipMemcpyAsync(cols[j], dst, (size_t)n * 4, hipMemcpyDeviceToHost, c->stream));
+      const int lt = r->ltypes[j];
+      const size_t es = elem_bytes(lt);
+      const bool plain = lt == XL_I32 || lt == XL_F32;
+      // decode straight into the caller's device buffer when it is aligned
+      // for the element size, else through device staging
+      const bool direct = on_device && (uintptr_t)cols[j] % es == 0;
+      if (!direct && !stage.p) XL_TRY(dalloc(c, (size_t)n * 8, &stage, "readout staging"));
+      void* dst = direct ? cols[j] : stage.p;
+      if (plain) {
+        HIP_TRY(c, k::gather_u32(r->col[j], perm.as<uint32_t>(), (uint32_t*)dst, n, c->stream));
+      } else {
+        if (!img.p) XL_TRY(dalloc(c, (size_t)n * 4, &img, "readout images"));
+        HIP_TRY(c, k::gather_u32(r->col[j], perm.as<uint32_t>(), img.as<uint32_t>(), n, c->stream));
+        HIP_TRY(c, k::decode_column(img.as<uint32_t>(), n, lt, c->dict[lt], dst, c->stream));
+      }
+      if (!direct) {
+        HIP_TRY(c, hipMemcpyAsync(cols[j], dst, (size_t)n * es, on_device ? hipMemcpyDeviceToDevice
+                                                                           : hipMemcpyDeviceToHost, c->stream));
         HIP_TRY(c, hipStreamSynchronize(c->stream));
       }
     }
@@ -2553,6 +2709,13 @@ xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st)
   c->arena.reset_peak();
   c->runs++;
   const int64_t ctl0 = c->control_bytes;
+  {
+    const xl_status s0 = resolve_wide_constants(p);
+    if (s0 != XL_OK) {
+      st->status = s0;
+      return s0;
+    }
+  }
   hipEvent_t e0, e1;
   HIP_TRY(c, hipEventCreate(&e0));
   HIP_TRY(c, hipEventCreate(&e1));

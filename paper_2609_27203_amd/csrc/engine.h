@@ -38,11 +38,31 @@ class Arena {
 
 struct Program;
 
+// Scalar types (xl_type values) and their stored int32 images: u32 and bool
+// are stored as order-preserving int32 values, i64/u64/f64 as ranks in the
+// context's dictionary of that type; f32 is stored as it is.
+inline uint8_t phys_type(int ltype) { return ltype == XL_F32 ? T_F32 : T_I32; }
+inline bool dict_type(int ltype) { return ltype == XL_I64 || ltype == XL_U64 || ltype == XL_F64; }
+inline size_t elem_bytes(int ltype) { return ltype == XL_BOOL ? 1 : dict_type(ltype) ? 8 : 4; }
+// Total-order key of an 8-byte value (the dictionary's sort key): i64 flips
+// the sign bit, f64 follows IEEE 754 totalOrder, u64 is itself.
+inline unsigned long long order_key64(unsigned long long bits, int ltype) {
+  const unsigned long long sign = 1ull << 63;
+  if (ltype == XL_I64) return bits ^ sign;
+  if (ltype == XL_F64) return (bits & sign) ? ~bits : (bits | sign);
+  return bits;
+}
+inline const char* type_name(int ltype) {
+  static const char* n[] = {"?", "i32", "f32", "u32", "i64", "u64", "f64", "bool"};
+  return ltype >= 1 && ltype <= 7 ? n[ltype] : n[0];
+}
+
 struct Relation {
   struct Context* ctx = nullptr;
   std::string name;
   int arity = 0;
-  uint8_t types[MAXC] = {};
+  uint8_t ltypes[MAXC] = {};  // declared types (xl_type)
+  uint8_t types[MAXC] = {};   // stored types (ValType of the int32 images)
   int64_t max_rows = 0;
   uint32_t* col[MAXC] = {};  // device columns (arena), nrows valid rows
   int64_t nrows = 0;
@@ -87,6 +107,10 @@ struct Context {
   size_t index_cache_bytes = 0;  // budget of the cross-run index cache (0: off)
   uint64_t runs = 0;             // xl_fixpoint_run calls so far
   std::vector<CachedIndex> icache;
+  // Dictionaries of the 8-byte types, indexed by xl_type: ascending distinct
+  // total-order keys (arena blocks); a stored value is its key's rank.
+  unsigned long long* dict[8] = {};
+  int64_t dict_n[8] = {};
   // drop cached indexes of rel (all of them, or those of older generations)
   void icache_drop(const Relation* rel, bool stale_only) {
     for (size_t i = 0; i < icache.size();) {
@@ -116,7 +140,8 @@ enum class Agg { NONE, COUNT, SUM, MIN, MAX, LSE };
 struct Term {
   enum Kind { VAR, ANON, INT, FLOAT } kind = ANON;
   std::string name;
-  int64_t ival = 0;
+  int64_t ival = 0;  // INT: the value (the low 64 bits when big)
+  bool big = false;  // INT above the int64 range (a u64 value)
   double fval = 0.0;
 };
 
@@ -152,6 +177,16 @@ struct NegPlan {         // a negated literal: the columns it constrains
   int col[2] = {0, 0};
 };
 
+// A constant of an 8-byte type in a plan.  Its stored image is the rank of
+// the value in the context's dictionary, looked up when a run starts (a load
+// between runs may renumber the dictionary).
+struct WideConst {
+  int8_t where;  // 0: driver_act[a].cval, 1: steps[a].act[b].cval, 2: stage_consts[a][b]
+  uint8_t ltype;
+  int16_t a, b;
+  unsigned long long key;  // total-order key of the value
+};
+
 struct StepPlan {        // index join against a full relation
   Relation* rel = nullptr;
   int key_col = 0;
@@ -171,6 +206,7 @@ struct RulePlan {
   std::vector<std::vector<MicroOp>> stage_ops;
   std::vector<std::vector<uint32_t>> stage_consts;
   std::vector<std::vector<int>> live_after;  // slots materialized after stage k
+  std::vector<WideConst> wconsts;            // constants resolved per run
   int nkey = 0;
   int key_slot[2] = {0, 0};
   int val_slot = -1;

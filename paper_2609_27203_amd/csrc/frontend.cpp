@@ -122,8 +122,11 @@ struct Parser {
         out->fval = strtod(k.s.c_str(), nullptr) * (neg ? -1.0 : 1.0);
       } else {
         out->kind = Term::INT;
-        out->ival = strtoll(k.s.c_str(), nullptr, 10) * (neg ? -1 : 1);
-        if (out->ival < INT32_MIN || out->ival > INT32_MAX) return fail("integer constant out of int32 range");
+        errno = 0;
+        const unsigned long long u = strtoull(k.s.c_str(), nullptr, 10);
+        if (errno == ERANGE || (neg && u > (1ull << 63))) return fail("integer constant outside the 64-bit range");
+        out->ival = neg ? (int64_t)(0ull - u) : (int64_t)u;
+        out->big = !neg && u > (unsigned long long)INT64_MAX;
       }
       return true;
     }
@@ -287,15 +290,55 @@ struct Planner {
     return false;
   }
 
-  static uint8_t term_type(const Term& t) { return t.kind == Term::FLOAT ? T_F32 : T_I32; }
-  static uint32_t term_bits(const Term& t) {
+  static int natural_type(const Term& t) { return t.kind == Term::FLOAT ? XL_F32 : XL_I32; }
+  // Stored image of constant t in a column of type lt; false when t is not a
+  // value of lt.  The 8-byte types get their image (a dictionary rank) when
+  // a run starts: *wide is set and *key receives the value's order key.
+  static bool const_image(const Term& t, int lt, uint32_t* bits, bool* wide, unsigned long long* key) {
+    *wide = false;
+    *bits = 0;
+    *key = 0;
     if (t.kind == Term::FLOAT) {
-      float f = (float)t.fval;
-      uint32_t b;
-      memcpy(&b, &f, 4);
-      return b;
+      if (lt == XL_F32) {
+        const float f = (float)t.fval;
+        memcpy(bits, &f, 4);
+        return true;
+      }
+      if (lt != XL_F64) return false;
+      unsigned long long b;
+      memcpy(&b, &t.fval, 8);
+      *key = order_key64(b, XL_F64);
+      *wide = true;
+      return true;
     }
-    return (uint32_t)(int32_t)t.ival;
+    if (t.kind != Term::INT) return false;
+    const int64_t v = t.ival;
+    switch (lt) {
+      case XL_I32:
+        if (t.big || v < INT32_MIN || v > INT32_MAX) return false;
+        *bits = (uint32_t)(int32_t)v;
+        return true;
+      case XL_U32:
+        if (t.big || v < 0 || v > (int64_t)UINT32_MAX) return false;
+        *bits = (uint32_t)v ^ 0x80000000u;
+        return true;
+      case XL_BOOL:
+        if (t.big || (v != 0 && v != 1)) return false;
+        *bits = (uint32_t)v;
+        return true;
+      case XL_I64:
+        if (t.big) return false;
+        *key = order_key64((unsigned long long)v, XL_I64);
+        *wide = true;
+        return true;
+      case XL_U64:
+        if (!t.big && v < 0) return false;
+        *key = (unsigned long long)v;
+        *wide = true;
+        return true;
+      default:
+        return false;
+    }
   }
 
   // Plan one rule with atom `drv` scanned first.
@@ -304,7 +347,7 @@ struct Planner {
     p.rule = rule_id;
     p.head = ctx->find(r.head);
     std::map<std::string, int> slot;
-    std::map<std::string, uint8_t> vtype;
+    std::map<std::string, int> vtype;  // declared (xl_type) type of each variable
     std::map<std::string, int> bstage;  // binding stage (0 = driver, k+1 = step k)
     std::set<std::string> assigned;
     for (auto& a : r.assigns) {
@@ -318,7 +361,8 @@ struct Planner {
       slot[v] = s;
       return s;
     };
-    auto bind_atom = [&](const AtomAst& a, Relation* rel, int stage, int key_col, ColAct* act) -> bool {
+    // step: the join step the atom becomes (-1 for the driver)
+    auto bind_atom = [&](const AtomAst& a, Relation* rel, int stage, int key_col, ColAct* act, int step) -> bool {
       for (int j = 0; j < rel->arity; ++j) {
         const Term& t = a.args[j];
         ColAct c{};
@@ -330,15 +374,20 @@ struct Planner {
         if (t.kind == Term::ANON) {
           c.kind = CA_NONE;
         } else if (t.kind == Term::INT || t.kind == Term::FLOAT) {
-          if (term_type(t) != rel->types[j])
-            return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': constant does not match column " + std::to_string(j) + " of " + rel->name);
+          bool wide;
+          unsigned long long key;
+          if (!const_image(t, rel->ltypes[j], &c.cval, &wide, &key))
+            return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': constant is not a " + type_name(rel->ltypes[j]) +
+                                              " value (column " + std::to_string(j) + " of " + rel->name + ")");
           c.kind = CA_CHECK_CONST;
-          c.cval = term_bits(t);
+          if (wide)
+            p.wconsts.push_back(step < 0 ? WideConst{0, rel->ltypes[j], (int16_t)j, 0, key}
+                                         : WideConst{1, rel->ltypes[j], (int16_t)step, (int16_t)j, key});
         } else {
           if (assigned.count(t.name))
             return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " is both an 'is' result and an atom argument");
           auto vt = vtype.find(t.name);
-          if (vt != vtype.end() && vt->second != rel->types[j])
+          if (vt != vtype.end() && vt->second != rel->ltypes[j])
             return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': variable " + t.name + " is used at two column types");
           if (bstage.count(t.name)) {
             c.kind = CA_CHECK_SLOT;
@@ -347,7 +396,7 @@ struct Planner {
             c.kind = CA_BIND;
             c.slot = (int8_t)new_slot(t.name);
             bstage[t.name] = stage;
-            vtype[t.name] = rel->types[j];
+            vtype[t.name] = rel->ltypes[j];
           }
           p.var_sources[slot[t.name]].push_back({rel, j});
         }
@@ -360,7 +409,7 @@ struct Planner {
     const AtomAst& da = r.atoms[drv];
     p.driver = ctx->find(da.pred);
     p.driver_delta = delta;
-    if (!bind_atom(da, p.driver, 0, -1, p.driver_act)) return false;
+    if (!bind_atom(da, p.driver, 0, -1, p.driver_act, -1)) return false;
     // join order: first remaining atom that shares a bound variable
     std::vector<int> rest;
     for (int k = 0; k < (int)r.atoms.size(); ++k)
@@ -386,11 +435,12 @@ struct Planner {
       st.rel = ctx->find(a.pred);
       st.key_col = key_col;
       const std::string& kv = a.args[key_col].name;
-      if (vtype[kv] != T_I32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': join variable " + kv + " has two types");
+      if (vtype[kv] != st.rel->ltypes[key_col])
+        return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': join variable " + kv + " is used at two column types");
       st.key_slot = slot[kv];
       p.var_sources[st.key_slot].push_back({st.rel, key_col});
       int stage = (int)p.steps.size() + 1;
-      if (!bind_atom(a, st.rel, stage, key_col, st.act)) return false;
+      if (!bind_atom(a, st.rel, stage, key_col, st.act, (int)p.steps.size())) return false;
       p.steps.push_back(st);
       rest.erase(rest.begin() + pick);
     }
@@ -402,18 +452,31 @@ struct Planner {
     std::map<std::string, int> avail;  // var -> kernel stage where available
     for (auto& kv : bstage) avail[kv.first] = kstage_of(kv.second);
 
-    auto operand = [&](int ks, const Term& t, uint8_t* ty, int8_t* enc) -> bool {
+    // declared type of a term in an expression: a bound variable's, or 0 for
+    // a constant (typed by the other operand)
+    auto term_type = [&](const Term& t, int* lt) -> bool {
+      *lt = 0;
+      if (t.kind == Term::ANON) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': '_' cannot be used in arithmetic or comparisons");
+      if (t.kind != Term::VAR) return true;
+      if (!avail.count(t.name)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " is not bound before it is used");
+      *lt = vtype[t.name];
+      return true;
+    };
+    // operand encoding of t at type lt (a constant becomes a stage constant)
+    auto operand = [&](int ks, const Term& t, int lt, int8_t* enc) -> bool {
       if (t.kind == Term::VAR) {
-        if (!avail.count(t.name)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " is not bound before it is used");
-        *ty = vtype[t.name];
         *enc = (int8_t)slot[t.name];
         return true;
       }
-      if (t.kind == Term::ANON) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': '_' cannot be used in arithmetic or comparisons");
       auto& cs = p.stage_consts[ks];
       if (cs.size() >= (size_t)MAXK) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': too many constants");
-      cs.push_back(term_bits(t));
-      *ty = term_type(t);
+      uint32_t bits;
+      bool wide;
+      unsigned long long key;
+      if (!const_image(t, lt, &bits, &wide, &key))
+        return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': a constant is not a " + type_name(lt) + " value");
+      if (wide) p.wconsts.push_back(WideConst{2, (uint8_t)lt, (int16_t)ks, (int16_t)cs.size(), key});
+      cs.push_back(bits);
       *enc = (int8_t)(-(int)cs.size());
       return true;
     };
@@ -428,15 +491,25 @@ struct Planner {
       for (auto& pt : as.parts) ts.push_back(&pt.second);
       int ks = stage_needed(ts);
       int s = new_slot(as.var);
-      uint8_t ty = 0;
+      // the type of the first variable operand, else of the first constant
+      int ty = 0;
+      for (auto& pt : as.parts) {
+        int t1;
+        if (!term_type(pt.second, &t1)) return false;
+        if (!ty) ty = t1;
+      }
+      if (!ty) ty = natural_type(as.parts[0].second);
+      if (ty != XL_I32 && ty != XL_F32)
+        return fail(XL_UNSUPPORTED, "rule '" + r.text + "': arithmetic on " + type_name(ty) + " values is not supported");
       for (size_t q = 0; q < as.parts.size(); ++q) {
-        uint8_t t1;
+        int t1;
         int8_t e1;
-        if (!operand(ks, as.parts[q].second, &t1, &e1)) return false;
-        if (q == 0) ty = t1;
-        else if (t1 != ty) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': 'is' mixes int32 and float32 operands");
+        (void)term_type(as.parts[q].second, &t1);
+        if ((t1 && t1 != ty) || (!t1 && natural_type(as.parts[q].second) != ty))
+          return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': 'is' mixes int32 and float32 operands");
+        if (!operand(ks, as.parts[q].second, ty, &e1)) return false;
         MicroOp op{};
-        op.type = t1;
+        op.type = phys_type(ty);
         op.dst = (int8_t)s;
         if (q == 0) {
           if (as.parts[0].first > 0) {
@@ -444,10 +517,9 @@ struct Planner {
             op.a = e1;
           } else {  // 0 - x
             Term zero;
-            zero.kind = t1 == T_F32 ? Term::FLOAT : Term::INT;
-            uint8_t tz;
+            zero.kind = ty == XL_F32 ? Term::FLOAT : Term::INT;
             int8_t ez;
-            if (!operand(ks, zero, &tz, &ez)) return false;
+            if (!operand(ks, zero, ty, &ez)) return false;
             op.kind = OP_SUB;
             op.a = ez;
             op.b = e1;
@@ -468,10 +540,17 @@ struct Planner {
       MicroOp op{};
       op.kind = OP_CMP;
       op.cmp = (uint8_t)c.op;
-      uint8_t t1, t2;
-      if (!operand(ks, c.lhs, &t1, &op.a) || !operand(ks, c.rhs, &t2, &op.b)) return false;
-      if (t1 != t2) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': comparison between int32 and float32");
-      op.type = t1;
+      int t1, t2;
+      if (!term_type(c.lhs, &t1) || !term_type(c.rhs, &t2)) return false;
+      if (!t1 && !t2) {  // two constants: their natural types
+        t1 = natural_type(c.lhs);
+        t2 = natural_type(c.rhs);
+      }
+      if (t1 && t2 && t1 != t2)
+        return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': comparison between " + type_name(t1) + " and " + type_name(t2));
+      const int lt = t1 ? t1 : t2;
+      if (!operand(ks, c.lhs, lt, &op.a) || !operand(ks, c.rhs, lt, &op.b)) return false;
+      op.type = phys_type(lt);
       p.stage_ops[ks].push_back(op);
     }
     // negated literals: a membership test at the first stage where all their
@@ -491,13 +570,11 @@ struct Planner {
           if (!avail.count(t.name))
             return fail(XL_UNSUPPORTED, "rule '" + r.text + "': " + t.name + " occurs in 'not " + a.pred +
                                             "' but in no positive atom or 'is' before it");
-          if (vtype[t.name] != rel->types[j])
+          if (vtype[t.name] != rel->ltypes[j])
             return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': variable " + t.name + " is used at two column types");
-        } else if (term_type(t) != rel->types[j]) {
-          return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': constant does not match column " + std::to_string(j) + " of " + rel->name);
         }
         if (rel->types[j] != T_I32)
-          return fail(XL_UNSUPPORTED, "rule '" + r.text + "': negated literals may constrain int32 columns only");
+          return fail(XL_UNSUPPORTED, "rule '" + r.text + "': negated literals may not constrain float32 columns");
         used.push_back(&t);
         cols.push_back(j);
       }
@@ -514,9 +591,8 @@ struct Planner {
       op.type = (uint8_t)np.ncols;
       op.a = 0;
       op.b = 0;
-      uint8_t ty;
-      if (np.ncols > 0 && !operand(ks, *used[0], &ty, &op.a)) return false;
-      if (np.ncols > 1 && !operand(ks, *used[1], &ty, &op.b)) return false;
+      if (np.ncols > 0 && !operand(ks, *used[0], rel->ltypes[cols[0]], &op.a)) return false;
+      if (np.ncols > 1 && !operand(ks, *used[1], rel->ltypes[cols[1]], &op.b)) return false;
       p.stage_ops[ks].push_back(op);
       p.negs.push_back(np);
     }
@@ -532,21 +608,23 @@ struct Planner {
       const Term& t = r.head_args[j];
       if (t.kind != Term::VAR) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': head arguments must be variables");
       if (!avail.count(t.name)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': head variable " + t.name + " does not occur in the body");
-      if (vtype[t.name] != h->types[j]) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': head argument " + t.name + " does not match column " + std::to_string(j) + " of " + h->name);
+      if (vtype[t.name] != h->ltypes[j]) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': head argument " + t.name + " does not match column " + std::to_string(j) + " of " + h->name);
       p.key_slot[j] = slot[t.name];
     }
     if (r.agg != Agg::NONE) {
       if (!avail.count(r.agg_var)) return fail(XL_UNSUPPORTED, "rule '" + r.text + "': aggregated variable " + r.agg_var + " does not occur in the body");
-      const uint8_t vt = h->types[nkey];
+      const int vt = h->ltypes[nkey];
       if (r.agg == Agg::COUNT) {
-        if (vt != T_I32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': count produces an int32 column");
+        if (vt != XL_I32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': count produces an int32 column");
         p.val_slot = -1;
       } else {
         if (vtype[r.agg_var] != vt) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': aggregated variable does not match the head's value column");
-        if (r.agg == Agg::LSE && vt != T_F32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': logsumexp needs a float32 column");
+        if (r.agg == Agg::LSE && vt != XL_F32) return fail(XL_TYPE_MISMATCH, "rule '" + r.text + "': logsumexp needs a float32 column");
+        if (r.agg == Agg::SUM && vt != XL_I32 && vt != XL_F32)
+          return fail(XL_UNSUPPORTED, "rule '" + r.text + "': sum over " + type_name(vt) + " values is not supported");
         p.val_slot = slot[r.agg_var];
       }
-      p.val_type = vt;
+      p.val_type = phys_type(vt);
     }
     // live slots between kernel stages
     p.live_after.assign(nkst, {});
@@ -644,7 +722,7 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
       return bad(XL_UNSUPPORTED, "rule '" + r.text + "': derived relations need one or two key columns "
                                  "(three only for a triangle join h(X,Y,Z) :- a(X,Y), b(Y,Z), c(X,Z))");
     for (size_t j = 0; j < r.head_args.size(); ++j)
-      if (h->types[j] != T_I32) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': key columns of derived relations must be int32");
+      if (h->types[j] != T_I32) return bad(XL_UNSUPPORTED, "rule '" + r.text + "': key columns of derived relations cannot be float32");
     for (const auto* list : {&r.atoms, &r.negs})
       for (auto& a : *list) {
         Relation* rel = ctx->find(a.pred);

@@ -185,5 +185,23 @@ hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, h
 
 enum FoldKind { FOLD_NONE = 0, FOLD_COUNT, FOLD_SUM, FOLD_MIN, FOLD_MAX, FOLD_LSE };
 
+// ---- column coding of u32, bool, i64, u64 and f64 (coding.hip) ----
+// out[i] = int32 image of in[i] (XL_U32: 4-byte values, XL_BOOL: bytes; a
+// byte other than 0 or 1 sets *bad).
+hipError_t encode_narrow(const void* in, int ltype, int64_t n, uint32_t* out, uint32_t* bad, hipStream_t s);
+// out[i] = total-order key of the 8-byte value in[i] (XL_I64, XL_U64, XL_F64).
+hipError_t order_keys64(const u64* in, int ltype, int64_t n, u64* out, hipStream_t s);
+// flag[i] = sorted[i] differs from sorted[i - 1] (always 1 at i = 0).
+hipError_t unique_flags64(const u64* sorted, int64_t n, uint32_t* flag, hipStream_t s);
+hipError_t compact64(const u64* src, const uint32_t* flag, const uint32_t* pos, u64* dst, int64_t n,
+                     hipStream_t s);
+// out[i] = number of keys of the ascending dict[0..nd) below q[i].
+hipError_t rank64(const u64* dict, int64_t nd, const u64* q, int64_t n, uint32_t* out, hipStream_t s);
+// col[i] = map[col[i]] in place.
+hipError_t remap_codes(uint32_t* col, int64_t n, const uint32_t* map, hipStream_t s);
+// Values of n int32 images into out (1, 4 or 8 bytes each by ltype); dict
+// holds the order keys of the 8-byte types.
+hipError_t decode_column(const uint32_t* img, int64_t n, int ltype, const u64* dict, void* out, hipStream_t s);
+
 }  // namespace k
 }  // namespace xlh

@@ -346,7 +346,7 @@ def triangle(rows: int = 1 << 16, core: int = 161, hubs: int = 8, seed: int = 6,
 TYPED_KINDS = ("u32", "i64", "u64", "f64")
 
 
-def typed_labels(kind: str, n: int) -> np.ndarray:
+def typed_labels(kind: str, n: int, extremes: bool = True) -> np.ndarray:
     """n distinct values of a column type in strictly ascending order of that
     type (f64: IEEE totalOrder), spread over the type's range: the extremes,
     values either side of the signed/unsigned boundary, and for f64 both
@@ -358,7 +358,8 @@ def typed_labels(kind: str, n: int) -> np.ndarray:
     i = np.arange(n, dtype=object)
     if kind == "u32":
         vals = [2 ** 31 - 3 * h + 3 * int(k) for k in i]
-        vals[0], vals[-1] = 0, 2 ** 32 - 1
+        if extremes:
+            vals[0], vals[-1] = 0, 2 ** 32 - 1
         return np.array(vals, dtype=np.uint64).astype(np.uint32)
     if kind == "i64":
         vals = [(int(k) - h) * 2 ** 34 + 11 for k in i]

@@ -19,9 +19,17 @@ XL_OK = 0
 STATUS = ["XL_OK", "XL_INVALID_ARGUMENT", "XL_TYPE_MISMATCH", "XL_UNSUPPORTED",
           "XL_RESOURCE_EXHAUSTED", "XL_CAPACITY_EXCEEDED", "XL_CONVERGENCE_FAILURE",
           "XL_DEVICE_ERROR", "XL_PARSE_ERROR"]
-XL_I32, XL_F32 = 1, 2
-_TYPES = {"i32": XL_I32, "f32": XL_F32}
-_NP = {"i32": np.int32, "f32": np.float32}
+XL_I32, XL_F32, XL_U32, XL_I64, XL_U64, XL_F64, XL_BOOL = 1, 2, 3, 4, 5, 6, 7
+_TYPES = {"i32": XL_I32, "f32": XL_F32, "u32": XL_U32, "i64": XL_I64, "u64": XL_U64, "f64": XL_F64,
+          "bool": XL_BOOL}
+_NP = {"i32": np.int32, "f32": np.float32, "u32": np.uint32, "i64": np.int64, "u64": np.uint64,
+       "f64": np.float64, "bool": np.bool_}
+
+
+def _torch_dtype(t: str):
+    import torch
+    return {"i32": torch.int32, "f32": torch.float32, "u32": torch.uint32, "i64": torch.int64,
+            "u64": torch.uint64, "f64": torch.float64, "bool": torch.bool}[t]
 STATS_ROUNDS = 256
 
 
@@ -185,12 +193,16 @@ class Relation:
         for j, (t, c) in enumerate(zip(self.types, cols)):
             if on_dev:
                 c = c.contiguous()
-                want = torch.int32 if t == "i32" else torch.float32
-                if c.dtype != want:
+                want = _torch_dtype(t)
+                # bool columns also take raw bytes (uint8), checked by the library
+                if c.dtype != want and not (t == "bool" and c.dtype == torch.uint8):
                     raise TypeError(f"column {j} of {self.name} must be {want}")
                 ptrs[j] = c.data_ptr()
             else:
-                c = np.ascontiguousarray(c, dtype=_NP[t])
+                if t == "bool" and getattr(c, "dtype", None) == np.uint8:
+                    c = np.ascontiguousarray(c)
+                else:
+                    c = np.ascontiguousarray(c, dtype=_NP[t])
                 ptrs[j] = c.ctypes.data
             keep.append(c)
         self.ctx._check(lib().xl_relation_load(self._h, ptrs, n, 1 if on_dev else 0))
@@ -217,8 +229,7 @@ class Relation:
         import torch
         n = self.size()
         dev = f"cuda:{self.ctx.device}"
-        out = [torch.empty(max(n, 1), dtype=torch.int32 if t == "i32" else torch.float32, device=dev)
-               for t in self.types]
+        out = [torch.empty(max(n, 1), dtype=_torch_dtype(t), device=dev) for t in self.types]
         ptrs = (C.c_void_p * len(self.types))(*[o.data_ptr() for o in out])
         got = C.c_int64()
         self.ctx._check(lib().xl_relation_read(self._h, ptrs, n, C.byref(got), 1))

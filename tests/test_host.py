@@ -141,6 +141,49 @@ def test_rejected_programs(rels, text, status):
     assert ei.value.status_name == status, str(ei.value)
 
 
+U2 = ("u64", "u64")
+
+
+@pytest.mark.parametrize("rels,text,status", [
+    # a variable keeps one declared type; constants must be values of the
+    # column type they meet
+    ({"e": U2, "f": I2, "p": ("u64",)}, "p(X) :- e(X,Y), f(Y,_).", "XL_TYPE_MISMATCH"),
+    ({"e": U2, "p": ("i64",)}, "p(X) :- e(X,_).", "XL_TYPE_MISMATCH"),
+    ({"e": ("u32", "u32"), "p": ("u32",)}, "p(X) :- e(X,-1).", "XL_TYPE_MISMATCH"),
+    ({"e": I2, "p": ("i32",)}, "p(X) :- e(X,4294967296).", "XL_TYPE_MISMATCH"),
+    ({"e": ("i64", "i64"), "p": ("i64",)}, "p(X) :- e(X,1.5).", "XL_TYPE_MISMATCH"),
+    ({"e": ("i64", "i64"), "p": ("i64",)}, "p(X) :- e(X,9223372036854775808).", "XL_TYPE_MISMATCH"),
+    ({"e": U2, "p": ("u64",)}, "p(X) :- e(X,18446744073709551616).", "XL_PARSE_ERROR"),
+    ({"e": ("i32", "bool"), "p": ("i32",)}, "p(X) :- e(X,2).", "XL_TYPE_MISMATCH"),
+    ({"e": ("f64", "f64"), "p": ("f64",)}, "p(X) :- e(X,1).", "XL_TYPE_MISMATCH"),
+    ({"e": ("u64", "i32"), "p": ("u64",)}, "p(X) :- e(X,Y), X < Y.", "XL_TYPE_MISMATCH"),
+    ({"e": U2, "p": ("u64",)}, "p(X) :- e(X,_), X > -3.", "XL_TYPE_MISMATCH"),
+    # arithmetic, sum and logsumexp take i32 and f32 only; count is int32
+    ({"e": ("i64", "i64"), "p": ("i64", "i64")}, "p(X,Z) :- e(X,Y), Z is Y + 1.", "XL_UNSUPPORTED"),
+    ({"e": ("i32", "u32"), "p": ("i32", "u32")}, "p(X,sum(Y)) :- e(X,Y).", "XL_UNSUPPORTED"),
+    ({"e": ("i32", "f64"), "p": ("i32", "f64")}, "p(X,logsumexp(Y)) :- e(X,Y).", "XL_TYPE_MISMATCH"),
+    ({"e": U2, "p": ("u64", "i64")}, "p(X,count(Y)) :- e(X,Y).", "XL_TYPE_MISMATCH"),
+])
+def test_rejected_typed_programs(rels, text, status):
+    c = _ctx(rels)
+    with pytest.raises(xlh.XlError) as ei:
+        c.compile(text)
+    assert ei.value.status_name == status, str(ei.value)
+
+
+@pytest.mark.parametrize("rels,text", [
+    ({"e": U2, "p": U2}, "p(X,Y) :- e(X,Y).\np(X,Y) :- p(X,Z), e(Z,Y)."),
+    ({"e": ("u32", "u32"), "p": ("u32",)}, "p(X) :- e(X,4294967295), X >= 2147483648."),
+    ({"e": ("i64", "f64"), "m": ("i64", "f64")}, "m(X,min(W)) :- e(X,W), W < -0.0."),
+    ({"e": ("i64", "f64"), "m": ("i64", "f64")}, "m(X,max(W)) :- e(X,W), W != 2.5."),
+    ({"e": U2, "c": ("u64", "i32")}, "c(X,count(Y)) :- e(X,Y), Y != 18446744073709551615."),
+    ({"e": ("i32", "bool"), "p": ("i32",), "q": ("i32",)}, "p(X) :- e(X,1).\nq(X) :- e(X,0), not p(X)."),
+    ({"e": ("i64", "i64"), "p": ("i64",)}, "p(X) :- e(X,-9223372036854775808)."),
+])
+def test_accepted_typed_programs(rels, text):
+    assert "stratum 0" in _ctx(rels).compile(text).explain()
+
+
 def test_planning_context_refuses_data():
     c = _ctx({"e": I2})
     import numpy as np
