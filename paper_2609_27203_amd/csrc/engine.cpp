@@ -753,12 +753,26 @@ struct Runner {
         Buf k64, k64b;
         XL_TRY(dalloc(c, (size_t)n * 8, &k64, "index order keys"));
         XL_TRY(dalloc(c, (size_t)n * 8, &k64b, "index order keys"));
-        if (order_kind == 1)
-          HIP_TRY(c, k::value_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], n, k64.as<u64>(), c->stream));
-        else
+        // value order: the order column's bounds when known (a finished
+        // relation, or a key column of a head), else the whole int32 range
+        int32_t vlo = INT32_MIN;
+        int vbits = 32;
+        if (order_kind == 1) {
+          HeadRun* oh = head_of(rel);
+          if (!oh && rel->nrows > 0) {
+            vlo = rel->lo[order_col];
+            vbits = std::max(1, bitlen((uint64_t)((int64_t)rel->hi[order_col] - rel->lo[order_col])));
+          } else if (oh && order_col < oh->nkey) {
+            vlo = (int32_t)oh->dom_lo[order_col];
+            vbits = std::max(1, bitlen((uint64_t)(oh->dom_hi[order_col] - oh->dom_lo[order_col])));
+          }
+          HIP_TRY(c, k::value_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], vlo, vbits, n,
+                                         k64.as<u64>(), c->stream));
+        } else {
           HIP_TRY(c, k::degree_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], dz.key_lo, dz.key_range,
                                           dz.off, n, k64.as<u64>(), c->stream));
-        const int obits = order_kind == 1 ? 32 : 16;
+        }
+        const int obits = order_kind == 1 ? vbits : 16;
         int alt = 0;
         HIP_TRY(c, k::radix_sort_u64(k64.as<u64>(), perm.as<uint32_t>(), k64b.as<u64>(), perm2.as<uint32_t>(), n,
                                      obits + kbits, tmp.p, c->stream, &alt));

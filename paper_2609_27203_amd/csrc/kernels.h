@@ -52,10 +52,12 @@ hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const
 hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s);
 // Packed keys of a negation table: c0[i], or (c0[i] << 32) | c1[i].
 hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s);
-// key[i] = (sorted[i] << 32) | (vcol[perm[i]] ^ 0x80000000): sorting by it
-// keeps the key order and orders each key's rows by the int32 value.
-hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
-                            u64* key, hipStream_t s);
+// key[i] = (sorted[i] << vbits) | (vcol[perm[i]] - vlo) (unsigned), for int32
+// values in [vlo, vlo + 2^vbits): sorting by it keeps the key order and
+// orders each key's rows by the value.  vlo = INT32_MIN, vbits = 32 covers
+// every int32.
+hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
+                            int vbits, int64_t n, u64* key, hipStream_t s);
 // ---- worst-case-optimal triangle join (see WcojArgs) ----
 constexpr int WC_CHUNK = 256;  // items per wavefront chunk
 hipError_t wcoj_work(const WcojArgs& a, hipStream_t s);

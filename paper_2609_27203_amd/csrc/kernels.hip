@@ -392,16 +392,16 @@ hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key,
   return hipGetLastError();
 }
 
-__global__ void value_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
-                                   u64* key) {
+__global__ void value_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
+                                   int vbits, int64_t n, u64* key) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
-    key[i] = ((u64)sorted[i] << 32) | (vcol[perm ? perm[i] : i] ^ 0x80000000u);
+    key[i] = ((u64)sorted[i] << vbits) | (u64)(vcol[perm ? perm[i] : i] - (uint32_t)vlo);
 }
-hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int64_t n,
-                            u64* key, hipStream_t s) {
+hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
+                            int vbits, int64_t n, u64* key, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  value_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, vcol, n, key);
+  value_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, vcol, vlo, vbits, n, key);
   return hipGetLastError();
 }
 
