@@ -115,7 +115,9 @@ hipError_t scan_exclusive_u64(const u64* in, u64* out, int64_t n, u64* total, vo
 
 // ============================================================ radix sort
 // LSD radix sort with 8-bit digits.  Per pass: a per-tile digit histogram
-// (LDS atomics), a device-wide scan of the digit-major histogram table, and a
+// (LDS atomics; the tile's counts are also added to the pass's 256 digit
+// totals), the digit-major offsets (one workgroup per digit scans that
+// digit's row of tile counts and adds the keys of all smaller digits), and a
 // stable scatter.  In the scatter each wavefront ranks its keys with a
 // ballot-based match of equal digits and running per-wave digit counters in
 // LDS, so the pass is stable without a block-wide sort.
@@ -130,7 +132,7 @@ constexpr int64_t RS_SMALL_N = (int64_t)1 << 22;  // below this, small tiles
 template <typename K, int RS_ITEMS>
 __global__ __launch_bounds__(RS_THREADS) void rs_hist_k(const K* keys, int64_t n, int shift,
                                                          uint32_t dmask, uint32_t* hist,
-                                                         uint32_t nblocks) {
+                                                         uint32_t nblocks, uint32_t* totals) {
   constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
@@ -142,7 +144,34 @@ __global__ __launch_bounds__(RS_THREADS) void rs_hist_k(const K* keys, int64_t n
     if (idx < n) atomicAdd(&h[(uint32_t)(keys[idx] >> shift) & dmask], 1u);
   }
   __syncthreads();
-  hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+  const uint32_t c = h[threadIdx.x];
+  hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = c;
+  if (c) atomicAdd(&totals[threadIdx.x], c);
+}
+
+// Workgroup d: row d of the histogram table (digit d's count in each tile)
+// becomes digit d's output offset in each tile: the number of keys with a
+// smaller digit plus digit d's count in the earlier tiles.  Workgroup 0 also
+// clears the digit totals of the next pass.
+__global__ __launch_bounds__(RS_THREADS) void rs_offsets_k(uint32_t* hist, uint32_t nblocks,
+                                                           const uint32_t* totals, uint32_t* next_totals) {
+  __shared__ uint32_t s_w[RS_THREADS / 64];
+  __shared__ uint32_t s_base;
+  const uint32_t d = blockIdx.x;
+  uint32_t t;
+  const uint32_t below = block_excl_scan_u32(totals[threadIdx.x], &t, s_w);
+  if (threadIdx.x == d) s_base = below;
+  __syncthreads();
+  uint32_t carry = s_base;
+  uint32_t* row = hist + (size_t)d * nblocks;
+  for (uint32_t b0 = 0; b0 < nblocks; b0 += RS_THREADS) {
+    const uint32_t b = b0 + threadIdx.x;
+    const uint32_t v = b < nblocks ? row[b] : 0u;
+    const uint32_t p = block_excl_scan_u32(v, &t, s_w);
+    if (b < nblocks) row[b] = carry + p;
+    carry += t;
+  }
+  if (d == 0) next_totals[threadIdx.x] = 0u;
 }
 
 template <typename K, int RS_ITEMS>
@@ -201,7 +230,7 @@ size_t radix_temp_bytes(int64_t n) {
   int64_t nb = (n + rs_tile(n) - 1) / rs_tile(n);
   if (nb < 1) nb = 1;
   size_t hist = (((size_t)nb * 256 * 4) + 255) & ~(size_t)255;
-  return hist + scan_temp_bytes(nb * 256);
+  return hist + 2 * 256 * 4;  // + the digit totals of two consecutive passes
 }
 
 template <typename K>
@@ -212,19 +241,23 @@ static hipError_t radix_sort_t(K* keys, uint32_t* vals, K* keys_alt, uint32_t* v
   const bool small = n < RS_SMALL_N;
   const uint32_t nb = (uint32_t)((n + rs_tile(n) - 1) / rs_tile(n));
   uint32_t* hist = (uint32_t*)temp;
-  char* stemp = (char*)temp + ((((size_t)nb * 256 * 4) + 255) & ~(size_t)255);
+  uint32_t* totals = (uint32_t*)((char*)temp + ((((size_t)nb * 256 * 4) + 255) & ~(size_t)255));
+  hipError_t e = hipMemsetAsync(totals, 0, 256 * 4, s);
+  if (e != hipSuccess) return e;
+  int pass = 0;
   K* ka = keys;
   K* kb = keys_alt;
   uint32_t* va = vals;
   uint32_t* vb = vals ? vals_alt : nullptr;
-  for (int shift = 0; shift < bits; shift += 8) {
+  for (int shift = 0; shift < bits; shift += 8, ++pass) {
     const int nbits = bits - shift < 8 ? bits - shift : 8;
+    uint32_t* tot = totals + 256 * (pass & 1);
+    uint32_t* tot_next = totals + 256 * ((pass + 1) & 1);
     if (small)
-      rs_hist_k<K, RS_SMALL_ITEMS><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
+      rs_hist_k<K, RS_SMALL_ITEMS><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb, tot);
     else
-      rs_hist_k<K, 16><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb);
-    hipError_t e = scan_exclusive_u32(hist, hist, (int64_t)nb * 256, nullptr, stemp, s);
-    if (e != hipSuccess) return e;
+      rs_hist_k<K, 16><<<nb, RS_THREADS, 0, s>>>(ka, n, shift, (1u << nbits) - 1u, hist, nb, tot);
+    rs_offsets_k<<<256, RS_THREADS, 0, s>>>(hist, nb, tot, tot_next);
     if (small)
       rs_scatter_k<K, RS_SMALL_ITEMS><<<nb, RS_THREADS, 0, s>>>(ka, va, kb, vb, n, shift, nbits, hist, nb);
     else
