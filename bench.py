@@ -44,6 +44,8 @@ KERNELS = {
     "emit": "stage_k / dense_min_tile_k (fused delta expand + probe + fold into the head)",
     "pull": "dense_pull_k (fold of each marked key's in-edges against the delta, keys ordered by target)",
     "wcoj": "wcoj_probe_k (count and materialize passes: each driver row's shorter Z list probed into the longer)",
+    "gather": "gather_round_k (per head row X staged in LDS: the delta rows of X's A values pushed through e2, "
+              "test-and-set in LDS, changed words written back)",
 }
 
 # Algorithmic bytes per unit of work (candidates, new tuples), counting only
@@ -75,8 +77,9 @@ def _algorithmic_bytes(workload: str, candidates: float, new: float) -> float:
 
 def dominant_kernel(stats: list, workload: str) -> dict:
     """The join kernel family with the largest event-timed share: frontier
-    rounds (closure-shaped strata), the generic fused stage kernel, or the
-    segmented pull fold (sum / logsumexp over dense heads)."""
+    rounds (closure-shaped strata), the generic fused stage kernel, the
+    segmented pull fold (sum / logsumexp over dense heads), the triangle
+    join's probes, or gathered rounds (same generation's shape)."""
     ms = {k: sum(s[k + "_ms"] for s in stats) for k in KERNELS}
     k = max(ms, key=lambda f: ms[f])
     return {"family": k, "ms": ms[k],

@@ -146,6 +146,12 @@ typedef struct {
     int64_t wcoj_launches;
     int64_t wcoj_candidates;    /* probes: per driver row, the shorter list's length */
     int64_t wcoj_new;           /* triples produced */
+    /* Gathered rounds of h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) over dense
+     * set heads (same generation's shape), timed the same way. */
+    double gather_ms;
+    int64_t gather_launches;
+    int64_t gather_candidates;  /* head tuples produced (each X of a row times its Y union) */
+    int64_t gather_new;         /* tuples added */
 } xl_fixpoint_stats;
 
 /*
@@ -193,6 +199,13 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     device array read once per batch; rounds past the
  *                     fixpoint change nothing (default 4; 0 = one round and
  *                     two host reads per pass; at most 64)
+ *   "gather_rounds"   1 = a recursive rule h(X,Y) :- e1(X,A), h(A,B), e2(Y,B)
+ *                     with nothing else (same generation's shape) over a dense
+ *                     set head runs gathered rounds: one workgroup per head
+ *                     row X stages it in LDS and sets there the Y values of
+ *                     e2 for the B bits of the delta rows of X's A values,
+ *                     writing back only changed words (default); 0 = the
+ *                     generic join of each delta tuple
  *   "product_joins"   1 = a rule whose two join steps are both keyed by
  *                     variables of the driver row (into a set head) runs as
  *                     one launch over the product of the two match lists

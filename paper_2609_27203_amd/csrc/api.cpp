@@ -86,6 +86,11 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     c->batched_rounds = (int)value;
     return XL_OK;
   }
+  if (!strcmp(key, "gather_rounds")) {
+    if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "gather_rounds must be 0 or 1");
+    c->gather_rounds = (int)value;
+    return XL_OK;
+  }
   if (!strcmp(key, "product_joins")) {
     if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "product_joins must be 0 or 1");
     c->product_joins = (int)value;

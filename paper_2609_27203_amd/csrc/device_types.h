@@ -287,6 +287,34 @@ struct FrontierArgs {
   uint32_t pull_ratio;
 };
 
+// Gathered round of h(X, Y) :- e1(X, A), delta h(A, B), e2(Y, B) over a dense
+// set head (same generation's shape): head row X receives the Y values that
+// e2 pairs with the B bits of the delta rows of X's A values.  A workgroup
+// owns the head rows X it visits: row X is staged in LDS, the
+// candidates are tested and set there, and the words that changed are
+// written back with plain stores, their new bits into X's next delta row.
+// Rows are visited in a grid-stride loop.  Delta rows are bitmap rows of the
+// head's layout with a per-row flag (nonzero: the row has bits); in_bits is
+// only read (rows are shared by all X of one A) and cleared by
+// clear_flagged_rows after the round.
+struct GatherArgs {
+  const uint32_t* in_bits;  // [range0][row_words] this round's delta
+  const uint32_t* in_flag;  // [range0]
+  uint32_t* out_bits;       // [range0][row_words] next delta (zero on entry)
+  uint32_t* out_flag;       // [range0] (zero on entry)
+  uint32_t* bits;           // the head's membership bitmap
+  IndexProbe e1;            // e1 indexed by its X column
+  int32_t e1_acol;          // column of e1 holding A
+  FrontierArgs push;        // the push expansion through e2: idx = e2 indexed by
+                            // its B column, ybind_col = e2's Y column, lo0, lo1,
+                            // row_words as below
+  int32_t lo0, lo1;
+  uint32_t row_words;
+  int64_t range0;
+  unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED
+};
+
+
 // Worst-case-optimal triangle join (count -> scan -> materialize).  Driver
 // rows (x, y) come from a's index in (X, Y) order; b is indexed by its Y
 // column and c by its X column, each with the rows of one key sorted by the

@@ -544,6 +544,12 @@ struct HeadRun {
                                 // the seed's delta straight from dbits
   bool frontier_ready = false;  // the current delta is in fcnt/fdiff[fcur] (or dbits)
   Buf fx, fcnt[2], fdiff[2];    // delta row slot sg belongs to first-key value fx[sg]
+  // gathered form (h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B)): the delta is
+  // bitmap rows in dbits / gbits (by gcur) with one flag per row in gflag
+  bool gathered = false;
+  bool gather_ready = false;
+  Buf gbits, gflag[2];
+  int gcur = 0;
   Buf hasin;                    // Y values with an in-edge (pull direction)
   int fcur = 0;
   int64_t fn = 0, fnew = 0;
@@ -1013,6 +1019,10 @@ struct Runner {
                          s.variants[0].carried && hr->nkey == 2 && hr->row_words <= 3072 &&
                          total_bits / 8 * 3 <= budget;
           hr->resident = hr->frontier && c->frontier_resident;
+          GatherShape gs;
+          hr->gathered = !hr->frontier && c->gather_rounds && s.recursive && s.heads.size() == 1 &&
+                         s.variants.size() == 1 && hr->nkey == 2 && hr->is_set && hr->row_words <= 3072 &&
+                         total_bits / 8 * 2 <= budget && gather_shape(s.variants[0], &gs);
         }
       }
       hr->preloaded = (hr->is_set || hr->is_minmax) ? h->nrows : 0;
@@ -1058,6 +1068,14 @@ struct Runner {
                                 c->stream));
     h->nrows = h->keys = h->preloaded;
     h->dbeg = h->dend = 0;
+    if (h->gathered) {
+      XL_TRY(dalloc(c, bytes, &h->gbits, "dense delta bitmap"));
+      HIP_TRY(c, hipMemsetAsync(h->gbits.p, 0, bytes, c->stream));
+      for (int b = 0; b < 2; ++b) {
+        XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->gflag[b], "delta row flags"));
+        HIP_TRY(c, hipMemsetAsync(h->gflag[b].p, 0, (size_t)std::max<int64_t>(h->range0, 1) * 4, c->stream));
+      }
+    }
     if (h->frontier && !h->resident) {
       XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->fx, "delta row keys"));
       for (int b = 0; b < 2; ++b) {
@@ -1343,6 +1361,90 @@ struct Runner {
       f.hasin = h->hasin.as<uint32_t>();
     }
     f.counters = c->dcounters;
+    return XL_OK;
+  }
+
+  // h(X, Y) :- e1(X, A), delta h(A, B), e2(Y, B) with nothing else, e1 and e2
+  // binary relations outside the stratum: the shape of a gathered round.
+  struct GatherShape {
+    int s1 = 0, s2 = 0;        // steps keyed by A (e1) and by B (e2)
+    int x_col = 0, y_col = 0;  // e1's X column, e2's Y column
+  };
+  static bool gather_shape(const RulePlan& p, GatherShape* g) {
+    if (!p.driver_delta || p.driver != p.head || p.driver->arity != 2 || p.steps.size() != 2 || p.nkey != 2 ||
+        !p.negs.empty())
+      return false;
+    for (const auto& ops : p.stage_ops)
+      if (!ops.empty()) return false;
+    const ColAct &da = p.driver_act[0], &db = p.driver_act[1];
+    if (da.kind != CA_BIND || db.kind != CA_BIND || da.slot == db.slot) return false;
+    int ia = -1, ib = -1;
+    for (int k = 0; k < 2; ++k) {
+      if (p.steps[k].key_slot == da.slot) ia = k;
+      else if (p.steps[k].key_slot == db.slot) ib = k;
+    }
+    if (ia < 0 || ib < 0) return false;
+    auto other = [&](const StepPlan& st, int* col, int* slot) {
+      if (st.rel == p.head || st.rel->arity != 2) return false;
+      const int oc = 1 - st.key_col;
+      if (st.act[oc].kind != CA_BIND) return false;
+      *col = oc;
+      *slot = st.act[oc].slot;
+      return true;
+    };
+    int xs = -1, ys = -1;
+    if (!other(p.steps[ia], &g->x_col, &xs) || !other(p.steps[ib], &g->y_col, &ys)) return false;
+    if (xs != p.key_slot[0] || ys != p.key_slot[1] || xs == ys) return false;
+    g->s1 = ia;
+    g->s2 = ib;
+    return true;
+  }
+
+  // One gathered round: reads the delta rows flagged in gflag[gcur] from
+  // (gcur ? gbits : dbits), writes the next delta into the other pair, then
+  // clears the rows it read.
+  xl_status eval_gathered(const RulePlan& p, HeadRun* h) {
+    h->fnew = 0;
+    GatherShape g;
+    if (!gather_shape(p, &g)) return c->fail(XL_DEVICE_ERROR, "gathered round of another rule shape (internal)");
+    GatherArgs a{};
+    a.in_bits = (h->gcur ? h->gbits : h->dbits).as<uint32_t>();
+    a.out_bits = (h->gcur ? h->dbits : h->gbits).as<uint32_t>();
+    a.in_flag = h->gflag[h->gcur].as<uint32_t>();
+    a.out_flag = h->gflag[h->gcur ^ 1].as<uint32_t>();
+    a.bits = h->bits.as<uint32_t>();
+    XL_TRY(get_index(p.steps[g.s1].rel, g.x_col, &a.e1));
+    a.e1_acol = p.steps[g.s1].key_col;
+    XL_TRY(get_index(p.steps[g.s2].rel, p.steps[g.s2].key_col, &a.push.idx));
+    a.push.ybind_col = g.y_col;
+    a.lo0 = a.push.lo0 = h->kp.lo[0];
+    a.lo1 = a.push.lo1 = h->kp.lo[1];
+    a.row_words = a.push.row_words = h->row_words;
+    a.range0 = h->range0;
+    a.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+    HIP_TRY(c, k::gather_round(a, c->stream));
+    if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+    // the consumed delta becomes the next round's output buffer
+    HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(), h->gflag[h->gcur].as<uint32_t>(),
+                                     h->range0, h->row_words, c->stream));
+    u64 cnt[CNT_N];
+    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    cands += (int64_t)cnt[CNT_CANDIDATES];
+    if (c->profile) {
+      float ms = 0;
+      HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+      st->gather_ms += ms;
+      st->gather_launches++;
+      st->gather_candidates += (int64_t)cnt[CNT_CANDIDATES];
+      st->gather_new += (int64_t)cnt[CNT_APPENDED];
+    }
+    h->fnew = (int64_t)cnt[CNT_APPENDED];
+    h->keys += h->fnew;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
     return XL_OK;
   }
 
@@ -1936,6 +2038,7 @@ struct Runner {
   xl_status eval_plan(const RulePlan& p, bool allow_product = true) {
     HeadRun* h = head_of(p.head);
     if (h->frontier && p.driver_delta) return eval_frontier(p, h);
+    if (h->gathered && p.driver_delta) return eval_gathered(p, h);
     if (h->ds && p.driver_delta) return eval_dense_pull(p, h);
     if (h->tiled && p.driver_delta) return eval_dense_tiles(p, h);
     const int nst = (int)p.steps.size();
@@ -2204,8 +2307,21 @@ struct Runner {
       *delta = h->fnew;
       return XL_OK;
     }
+    if (h->gathered && h->gather_ready) {  // a gathered round wrote the next delta rows
+      h->gcur ^= 1;
+      *delta = h->fnew;
+      return XL_OK;
+    }
     if (h->dense) {
       *delta = h->round_new;
+      if (h->gathered) {  // seed round: its new tuples in dbits are the first delta rows
+        h->gather_ready = true;
+        h->gcur = 0;
+        if (h->round_new)
+          HIP_TRY(c, k::row_popcount(h->dbits.as<uint32_t>(), h->range0, h->row_words, h->gflag[0].as<uint32_t>(),
+                                     c->stream));
+        return XL_OK;
+      }
       if (h->resident) {  // the resident launch reads the seed's delta rows from dbits
         h->frontier_ready = true;
         h->fn = h->round_new ? h->range0 : 0;

@@ -441,6 +441,104 @@ hipError_t frontier_resident(const FrontierArgs& a, unsigned grid, hipStream_t s
   return hipGetLastError();
 }
 
+// Gathered round (see GatherArgs).  Per head row X with a flagged delta row
+// among its A values: X's row is copied into LDS twice (before, after); each
+// such delta row is pushed through e2 into the after row by the frontier
+// expansion (its B bits decoded into a list, their Y lists walked wave-
+// balanced, each Y tested and set in LDS); then the words that differ are
+// written to the head row and their new bits to X's next delta row.
+__global__ __launch_bounds__(FR_THREADS) void gather_round_k(GatherArgs g) {
+  extern __shared__ uint32_t lds[];
+  const uint32_t W = g.row_words;
+  uint32_t* before = lds;
+  uint32_t* after = lds + W;
+  __shared__ FrontierShared L;
+  __shared__ uint32_t s_any, s_new;
+  const int lane = lane_id();
+  u64 cands = 0, fresh = 0;
+  const uint32_t* acol = g.e1.col[g.e1_acol];
+  // rows in a grid-stride loop: most rows have no delta in a given round, and
+  // a shared work counter would serialize those cheap visits on one address
+  for (int64_t xr64 = blockIdx.x; xr64 < g.range0; xr64 += gridDim.x) {
+    const uint32_t xr = (uint32_t)xr64;
+    if (threadIdx.x == 0) {
+      s_any = 0u;
+      s_new = 0u;
+    }
+    __syncthreads();
+    const uint32_t kk = (uint32_t)g.lo0 + xr - (uint32_t)g.e1.key_lo;
+    uint32_t b1 = 0, n1 = 0;
+    if (kk < g.e1.key_range) {
+      b1 = g.e1.off[kk];
+      n1 = g.e1.off[kk + 1] - b1;
+    }
+    // does any A of X have a delta row?
+    for (uint32_t q = threadIdx.x; q < n1; q += FR_THREADS) {
+      const uint32_t ar = acol[b1 + q] - (uint32_t)g.lo0;
+      if ((int64_t)ar < g.range0 && g.in_flag[ar]) s_any = 1u;
+    }
+    __syncthreads();
+    if (!s_any) {
+      __syncthreads();  // the shared words are rewritten at the top
+      continue;
+    }
+    uint32_t* hrow = g.bits + (u64)xr * W;
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) before[i] = after[i] = hrow[i];
+    __syncthreads();
+    for (uint32_t q = 0; q < n1; ++q) {
+      const uint32_t ar = acol[b1 + q] - (uint32_t)g.lo0;
+      if ((int64_t)ar >= g.range0 || !g.in_flag[ar]) continue;  // (uniform)
+      frontier_expand(g.push, before, after, g.in_bits + (u64)ar * W, false, L, cands);
+    }
+    uint32_t* orow = g.out_bits + (u64)xr * W;
+    uint32_t nb = 0;
+    for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) {
+      const uint32_t nw = after[i] & ~before[i];
+      if (nw) {
+        hrow[i] = after[i];
+        orow[i] = nw;
+        nb += (uint32_t)__popc(nw);
+      }
+    }
+    nb = wave_incl_scan(nb);
+    if (lane == 63 && nb) atomicAdd(&s_new, nb);
+    __syncthreads();
+    if (threadIdx.x == 0 && s_new) {
+      g.out_flag[xr] = 1u;
+      fresh += s_new;
+    }
+    __syncthreads();  // the LDS rows and shared words are reused by the next row
+  }
+  const u64 c = wave_incl_scan_t<u64>(cands), fr = wave_incl_scan_t<u64>(fresh);
+  if (lane == 63) {
+    if (c) atomicAdd(&g.counters[CNT_CANDIDATES], c);
+    if (fr) atomicAdd(&g.counters[CNT_APPENDED], fr);
+  }
+}
+
+hipError_t gather_round(const GatherArgs& a, hipStream_t s) {
+  if (a.range0 <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 2048);
+  gather_round_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
+  return hipGetLastError();
+}
+
+__global__ void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words) {
+  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    if (!flag[r]) continue;  // (uniform)
+    uint32_t* row = bits + (u64)r * row_words;
+    for (uint32_t i = threadIdx.x; i < row_words; i += blockDim.x) row[i] = 0u;
+    __syncthreads();  // every thread has read the flag before it is cleared
+    if (threadIdx.x == 0) flag[r] = 0u;
+  }
+}
+
+hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, hipStream_t s) {
+  if (nrows <= 0) return hipSuccess;
+  clear_flagged_rows_k<<<(unsigned)std::min<int64_t>(nrows, 4096), 256, 0, s>>>(bits, flag, nrows, row_words);
+  return hipGetLastError();
+}
+
 // Number of set bits in each bitmap row.
 __global__ __launch_bounds__(256) void row_popcount_k(const uint32_t* bits, int64_t nrows,
                                                       uint32_t row_words, uint32_t* cnt) {

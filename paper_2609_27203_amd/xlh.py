@@ -56,6 +56,8 @@ class xl_fixpoint_stats(C.Structure):
         ("pull_new", C.c_int64),
         ("wcoj_ms", C.c_double), ("wcoj_launches", C.c_int64), ("wcoj_candidates", C.c_int64),
         ("wcoj_new", C.c_int64),
+        ("gather_ms", C.c_double), ("gather_launches", C.c_int64), ("gather_candidates", C.c_int64),
+        ("gather_new", C.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -75,6 +77,8 @@ class xl_fixpoint_stats(C.Structure):
             "pull_candidates": self.pull_candidates, "pull_new": self.pull_new,
             "wcoj_ms": self.wcoj_ms, "wcoj_launches": self.wcoj_launches,
             "wcoj_candidates": self.wcoj_candidates, "wcoj_new": self.wcoj_new,
+            "gather_ms": self.gather_ms, "gather_launches": self.gather_launches,
+            "gather_candidates": self.gather_candidates, "gather_new": self.gather_new,
         }
 
 

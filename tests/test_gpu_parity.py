@@ -620,6 +620,44 @@ def test_capacity_and_workspace_errors():
     assert ei.value.status_name == "XL_RESOURCE_EXHAUSTED"
 
 
+def _gather_workload(variant):
+    if variant.startswith("sg"):
+        base = W.small_workloads()["same_generation"]()
+        rules = base.rules if variant == "sg" else (
+            "sg(X,Y) :- parent(X,P), parent(Y,P), X != Y.\nsg(X,Y) :- sg(A,B), parent(Y,B), parent(X,A).")
+        return W.Workload(variant, rules, base.edb, base.idb), "sg"
+    e_src, e_dst = W.uniform_graph(300, 900, 31)
+    f_src, f_dst = W.uniform_graph(300, 600, 32)
+    edb = {"e": (("i32", "i32"), [np.asarray(e_src, np.int32), np.asarray(e_dst, np.int32)]),
+           "f": (("i32", "i32"), [np.asarray(f_src, np.int32), np.asarray(f_dst, np.int32)])}
+    rules = {"dag": "h(X,Y) :- e(X,Y).\nh(X,Y) :- e(X,A), h(A,B), f(Y,B).",
+             "dag_swapped": "h(X,Y) :- e(Y,X).\nh(X,Y) :- e(A,X), h(A,B), f(B,Y)."}[variant]
+    return W.Workload(variant, rules, edb, {"h": ("i32", "i32")}), "h"
+
+
+@pytest.mark.parametrize("gather", [0, 1])
+@pytest.mark.parametrize("variant", ["sg", "sg_reordered", "dag", "dag_swapped"])
+def test_gathered_rounds(variant, gather):
+    """h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) in gathered rounds (head row
+    X staged in LDS, the Y values of the B bits of its A values' delta rows
+    set there) and in the generic join: the oracle's rows and per-round delta
+    sizes either way, also over random graphs where an X has many A (several
+    delta rows per head row, one delta row read for many X) and with the
+    columns and atoms in other orders."""
+    wl, head = _gather_workload(variant)
+    print(f"case: gathered rounds {variant} gather={gather}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"gather_rounds": gather, "profile": 1})
+    _compare(wl, rels, ref)
+    levels = _delta_levels(ref, head)
+    assert stats["delta_rows"][:len(levels)] == levels
+    assert stats["iterations"] == len(ref.sizes[head]) - 1
+    if gather:
+        assert stats["gather_launches"] == stats["iterations"] and stats["gather_new"] == sum(levels[1:])
+    else:
+        assert stats["gather_launches"] == 0
+
+
 def test_resume_from_fixpoint_is_idempotent():
     wl = W.small_workloads()["same_generation"]()
     rels, _, ctx = engine_run(wl)
