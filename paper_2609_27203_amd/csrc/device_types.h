@@ -177,9 +177,10 @@ struct StageArgs {
 // second-key-major slot (y - lo1) * nrank + rank(s): listed keys of one y lie
 // together, and the delta values of (s, z) for a fixed z and consecutive s
 // are consecutive words, so the wavefront's reads of one in-edge coalesce.
-// The full relation (fval/fpres) keeps the first-key-major slot
-// rank(s) * range1 + (y - lo1), which yields the rows in key order.  A key's
-// contributions are folded in index order: the result is deterministic.
+// The full relation (fval/fpres) uses the same slots, so each lane's merge
+// reads and writes consecutive words and the presence bits of one word are
+// set by one atomic per run of lanes.  A key's contributions are folded in
+// index order: the result is deterministic.
 struct DensePullArgs {
   const uint32_t* list;   // marked delta slots, ascending
   int64_t n;

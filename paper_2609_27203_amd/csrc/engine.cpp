@@ -601,6 +601,13 @@ struct Runner {
       if (e) (void)hipEventDestroy(e);
   }
 
+  // Slots of a dense value head's full relation and their layout (0: rank
+  // major, n: target-major with n ranks per target, as sum/logsumexp heads).
+  static int64_t full_slots(const HeadRun* h) {
+    return h->ds ? h->nrank_d * h->range1 : std::max<int64_t>(h->n0, 1) * h->range1;
+  }
+  static uint32_t full_nrank(const HeadRun* h) { return h->ds ? (uint32_t)h->nrank_d : 0u; }
+
   HeadRun* head_of(const Relation* r) {
     for (auto& h : heads)
       if (h->rel == r) return h.get();
@@ -707,13 +714,13 @@ struct Runner {
         void* snap[3];
         for (int j = 0; j <= h->nkey; ++j) XL_TRY(own((size_t)std::max<int64_t>(n, 1) * 4, "head snapshot", &snap[j]));
         Buf tmp, tot;
-        const int64_t ns = h->dv ? std::max<int64_t>(h->n0, 1) * h->range1 : h->cap;
+        const int64_t ns = h->dv ? full_slots(h) : h->cap;
         XL_TRY(dalloc(c, k::compact_temp_bytes(ns), &tmp, "compaction scratch"));
         XL_TRY(dalloc(c, 8, &tot, "count"));
         uint32_t* k1 = h->nkey == 2 ? (uint32_t*)snap[1] : nullptr;
         if (h->dv)
           HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
-                                   h->range1, 0, h->kp, rel->types[h->nkey], h->fold, (uint32_t*)snap[0], k1,
+                                   h->range1, full_nrank(h), h->kp, rel->types[h->nkey], h->fold, (uint32_t*)snap[0], k1,
                                    (uint32_t*)snap[h->nkey], std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p,
                                    c->stream));
         else
@@ -1127,7 +1134,10 @@ struct Runner {
     XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(n0, 1) * 4, &h->dict, "key dictionary"));
     HIP_TRY(c, k::dict_finish(h->dmap.as<uint32_t>(), pos.as<uint32_t>(), range, h->kp.lo[0],
                               h->dict.as<uint32_t>(), c->stream));
-    const size_t ns = (size_t)slots, nw = (ns + 31) / 32;
+    // sum/logsumexp heads lay the full relation out like their delta slots
+    // (target-major, ranks padded to whole words)
+    if (h->ds) h->nrank_d = (std::max<int64_t>(n0, 1) + 31) / 32 * 32;
+    const size_t ns = h->ds ? (size_t)h->nrank_d * (size_t)h->range1 : (size_t)slots, nw = (ns + 31) / 32;
     XL_TRY(dalloc(c, ns * 4, &h->dvals, "dense values"));
     XL_TRY(dalloc(c, nw * 4, &h->dpres, "dense presence bits"));
     XL_TRY(dalloc(c, nw * 4, &h->dchg, "dense delta bits"));
@@ -1137,7 +1147,6 @@ struct Runner {
     if (h->tiled) XL_TRY(dalloc(c, (size_t)(n0 + 1) * 4, &h->roff, "delta rows per rank"));
     if (h->ds) {
       // target-major delta slots with whole words per target: y * nrank_d + rank
-      h->nrank_d = (std::max<int64_t>(n0, 1) + 31) / 32 * 32;
       const size_t nsd = (size_t)h->nrank_d * (size_t)h->range1, nwd = nsd / 32;
       XL_TRY(dalloc(c, nsd * 4, &h->dcur, "dense delta values"));
       XL_TRY(dalloc(c, nsd * 4, &h->dnext, "dense delta values"));
@@ -2603,13 +2612,13 @@ struct Runner {
     }
     if (h->dv) {
       const int64_t n = h->keys;
-      const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
+      const int64_t ns = full_slots(h);
       Buf out[3], tmp, tot;
       for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
       XL_TRY(dalloc(c, k::compact_temp_bytes(ns), &tmp, "compaction scratch"));
       XL_TRY(dalloc(c, 8, &tot, "count"));
       HIP_TRY(c, k::dense_rows(h->dvals.as<uint32_t>(), h->dpres.as<uint32_t>(), h->dict.as<uint32_t>(), ns,
-                               h->range1, 0, h->kp, r->types[h->nkey], h->fold, out[0].as<uint32_t>(),
+                               h->range1, full_nrank(h), h->kp, r->types[h->nkey], h->fold, out[0].as<uint32_t>(),
                                h->nkey == 2 ? out[1].as<uint32_t>() : nullptr, out[h->nkey].as<uint32_t>(),
                                std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p, c->stream));
       uint32_t m = 0;

@@ -1860,8 +1860,8 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
       }
       wave_lds_sync();
     }
+    uint32_t out = 0;
     if (i < a.n) {
-      uint32_t out;
       if (lse) {
         const float m = __uint_as_float(s_m[w][lane]);
         out = __float_as_uint(m == -INFINITY ? -INFINITY : m + logf(__uint_as_float(s_acc[w][lane])));
@@ -1874,8 +1874,46 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
       a.k1[i] = yb + (uint32_t)a.lo1;
       a.v[i] = out;
       a.nval[t] = out;
-      atomicOr(&a.npres[t >> 5], 1u << (t & 31));
-      mine += dense_merge(a.fval, a.fpres, r * a.range1 + yb, out, a.fold_kind, a.val_type);
+    }
+    // Presence bits of the next delta and of the full relation (both laid out
+    // like the slots): the listed slots ascend, so the lanes of one presence
+    // word are a run; the run ORs its bits together and its last lane sets
+    // them with one atomic, whose old word tells every lane of the run
+    // whether its slot was present.  The full relation's value is then read
+    // and written by its own lane (each slot is listed once).
+    {
+      const bool act = i < a.n;
+      const uint32_t wd = act ? t >> 5 : 0xffffffffu;
+      const uint32_t bit = act ? 1u << (t & 31) : 0u;
+      const uint32_t wprev = __shfl_up(wd, 1, 64);
+      const u64 heads = __ballot(lane == 0 || wprev != wd);
+      const int head = 63 - __clzll((long long)(heads & ((2ull << lane) - 1ull)));
+      const u64 above = heads & ~((2ull << lane) - 1ull);
+      const int tail = above ? __ffsll((long long)above) - 2 : 63;
+      uint32_t run = bit;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_up(run, d, 64);
+        if (lane - d >= head) run |= o;
+      }
+      uint32_t old = 0;
+      if (act && lane == tail) {
+        atomicOr(&a.npres[wd], run);
+        old = atomicOr(&a.fpres[wd], run);
+      }
+      old = __shfl(old, tail, 64);
+      if (act) {
+        const bool had = old & bit;
+        uint32_t nv = out;
+        if (had) {
+          const uint32_t cur = a.fval[t];
+          if (lse) nv = __float_as_uint(lse2(__uint_as_float(cur), __uint_as_float(out)));
+          else if (f32) nv = __float_as_uint(__fadd_rn(__uint_as_float(cur), __uint_as_float(out)));
+          else nv = cur + out;
+        }
+        a.fval[t] = nv;
+        mine += had ? 0u : 1u;
+      }
     }
     wave_lds_sync();
   }
@@ -1905,10 +1943,10 @@ __global__ void dense_apply_rows_k(const uint32_t* c0, const uint32_t* c1, const
       atomicOr(&counters[CNT_FATAL], 4ull);
       continue;
     }
-    const uint32_t t = k1 * nrank + r0;  // delta: second-key-major; full relation: first-key-major
+    const uint32_t t = k1 * nrank + r0;  // delta and full relation: second-key-major
     cval[t] = v[i];
     atomicOr(&cpres[t >> 5], 1u << (t & 31));
-    mine += dense_merge(fval, fpres, r0 * range1 + k1, v[i], fold_kind, type);
+    mine += dense_merge(fval, fpres, t, v[i], fold_kind, type);
   }
   block_count_add(&counters[CNT_INSERTED], mine);
 }
