@@ -1643,7 +1643,8 @@ __device__ __forceinline__ bool dense_merge(uint32_t* fval, uint32_t* fpres, uin
 typedef XL_KARG const DensePullArgs PullArgs;
 
 // Binds S, Z, Y and P1, then e's row e_row; false when the row does not
-// derive anything for this key.
+// derive anything for this key.  FAST: the value is one add/subtract (a.fast).
+template <bool FAST>
 __device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, uint32_t y, uint32_t e_row,
                                           Regs& u) {
   const uint32_t z = a.rev.col[a.zcol][e_row];
@@ -1651,7 +1652,7 @@ __device__ __forceinline__ bool pull_bind(PullArgs& a, uint32_t r, uint32_t s, u
   if (zb >= a.range1) return false;
   const uint32_t zs = zb * a.nrank + r;
   if (!((a.cpres[zs >> 5] >> (zs & 31)) & 1u)) return false;
-  if (a.fast) {
+  if constexpr (FAST) {
     setv(u, a.val_slot, fast_value(a.fast, a.val_type, a.cval[zs], a.rev.col[a.fcol][e_row]));
     return true;
   }
@@ -1693,6 +1694,7 @@ __device__ __forceinline__ T seg_sum_scan(T v, int lane, int head) {
   return v;
 }
 
+template <bool FAST>
 __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_value) {
   (void)by_value;
   PullArgs& a = *(PullArgs*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -1750,7 +1752,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
           uacc += x;
         }
       };
-      if (a.fast) {
+      if constexpr (FAST) {
         // the value is one add/subtract of the delta value and a column of
         // e: eight in-edges at a time, each level of loads issued together
         const uint32_t* zc = a.rev.col[a.zcol];
@@ -1777,10 +1779,10 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
             if (pw[q]) fold(fast_value(a.fast, a.val_type, cv[q], wv[q]));
         }
       }
-      for (uint32_t jj = 0; !a.fast && jj < maxdeg; ++jj) {
+      for (uint32_t jj = 0; !FAST && jj < maxdeg; ++jj) {
         if (jj >= deg) continue;
         Regs u;
-        if (!pull_bind(a, r, a.dict[r], y, e0 + jj, u)) continue;
+        if (!pull_bind<FAST>(a, r, a.dict[r], y, e0 + jj, u)) continue;
         const uint32_t x = getv(u, a.val_slot);
         any = true;
         if (lse) {
@@ -1813,7 +1815,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
       if (act) {
         const uint32_t tq = s_key[w][q], r = tq % a.nrank;
         Regs u;
-        ok = pull_bind(a, r, a.dict[r], tq / a.nrank + (uint32_t)a.lo1, s_beg[w][q] + (j - s_excl[w][q]), u);
+        ok = pull_bind<FAST>(a, r, a.dict[r], tq / a.nrank + (uint32_t)a.lo1, s_beg[w][q] + (j - s_excl[w][q]), u);
         if (ok) x = getv(u, a.val_slot);
       }
       // runs of equal owners among the active lanes
@@ -1922,10 +1924,24 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
   block_count_add(&a.counters[CNT_CANDIDATES], examined);
 }
 
+// At most as many workgroups as the device keeps resident: each wavefront
+// then loops over several chunks of 64 keys, which costs far less than
+// launching a short-lived wavefront per chunk.
+template <bool FAST>
+static hipError_t dense_pull_launch(const DensePullArgs& a, hipStream_t s) {
+  int dev = 0, cus = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, dense_pull_k<FAST>, DP_WAVES * 64, 0);
+  if (e != hipSuccess) return e;
+  const int cap = std::max(1, cus * std::max(1, per_cu));
+  dense_pull_k<FAST><<<grid_for((a.n + 63) / 64, DP_WAVES, cap), DP_WAVES * 64, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t dense_pull(const DensePullArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  dense_pull_k<<<grid_for((a.n + 63) / 64, DP_WAVES, 16384), DP_WAVES * 64, 0, s>>>(a);
-  return hipGetLastError();
+  return a.fast ? dense_pull_launch<true>(a, s) : dense_pull_launch<false>(a, s);
 }
 
 // Rows with distinct keys (a folded seed round) into a dense sum/logsumexp
