@@ -11,6 +11,19 @@
 namespace xlh {
 namespace k {
 
+// Workgroups of `threads` threads and `lds` dynamic LDS bytes of kernel k
+// that the current device keeps resident at once.
+template <typename Kernel>
+static hipError_t resident_blocks(Kernel k, int threads, size_t lds, int* out) {
+  int dev = 0, cus = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, lds);
+  if (e != hipSuccess) return e;
+  *out = std::max(1, cus * std::max(1, per_cu));
+  return hipSuccess;
+}
+
 // ============================================================ scan
 constexpr int SC_THREADS = 256;
 constexpr int SC_ITEMS = 16;
@@ -1929,12 +1942,9 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
 // launching a short-lived wavefront per chunk.
 template <bool FAST>
 static hipError_t dense_pull_launch(const DensePullArgs& a, hipStream_t s) {
-  int dev = 0, cus = 0, per_cu = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, dense_pull_k<FAST>, DP_WAVES * 64, 0);
+  int cap = 0;
+  hipError_t e = resident_blocks(dense_pull_k<FAST>, DP_WAVES * 64, 0, &cap);
   if (e != hipSuccess) return e;
-  const int cap = std::max(1, cus * std::max(1, per_cu));
   dense_pull_k<FAST><<<grid_for((a.n + 63) / 64, DP_WAVES, cap), DP_WAVES * 64, 0, s>>>(a);
   return hipGetLastError();
 }
