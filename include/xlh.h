@@ -193,7 +193,9 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
  *                     with its row in LDS until its delta is empty, the pass
  *                     count and per-pass delta sizes read back once at the end
  *                     (default); 0 = one launch and one host read per pass
- *   "batched_rounds"  rounds of a tiled min/max stratum (see "dense_tiles")
+ *   "batched_rounds"  rounds of a tiled min/max stratum (see "dense_tiles"),
+ *                     or of a sum/logsumexp stratum whose carried rule adds
+ *                     or subtracts one column (segmented pull rounds),
  *                     enqueued per host read: every round takes its sizes
  *                     from device memory and reports its delta size to a
  *                     device array read once per batch; rounds past the

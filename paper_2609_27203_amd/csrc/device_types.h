@@ -183,7 +183,8 @@ struct StageArgs {
 // index order: the result is deterministic.
 struct DensePullArgs {
   const uint32_t* list;   // marked delta slots, ascending
-  int64_t n;
+  int64_t n;              // listed keys, or their upper bound when n_dev is set
+  const uint32_t* n_dev;  // listed keys in device memory (batched rounds), else null
   const uint32_t* dict;   // rank -> first key value
   uint32_t range1;
   uint32_t nrank;         // ranks (first key values in the dictionary)
@@ -204,7 +205,7 @@ struct DensePullArgs {
   uint32_t* npres;
   uint32_t* fval;         // full relation: values and presence bits
   uint32_t* fpres;
-  uint32_t* k0;           // next delta rows, row i for list[i]
+  uint32_t* k0;           // next delta rows, row i for list[i] (all null: not written)
   uint32_t* k1;
   uint32_t* v;
   unsigned long long* counters;  // CNT_INSERTED: keys new to the full relation; CNT_FATAL

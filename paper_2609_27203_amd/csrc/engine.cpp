@@ -1633,6 +1633,146 @@ struct Runner {
   // mark every key that receives a contribution (the stage kernel over the
   // delta rows), list the marked slots in order, then fold each key's
   // contributions by scanning e's rows for its Y value against the delta.
+  // Arguments of the segmented pull of a carried-value rule over the current
+  // delta (list, counts, row outputs and counters are set by the caller).
+  xl_status pull_args(const RulePlan& p, HeadRun* h, int fast, int fcol, DensePullArgs& q) {
+    const StepPlan& sp = p.steps[0];
+    q.dict = h->dict.as<uint32_t>();
+    q.range1 = (uint32_t)h->range1;
+    q.nrank = (uint32_t)h->nrank_d;
+    q.lo1 = h->kp.lo[1];
+    XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
+    for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
+    q.rev.act[p.carried_ycol].kind = CA_NONE;  // Y is bound from the key
+    q.zcol = sp.key_col;
+    q.slot_s = (int8_t)p.cv_slot_s;
+    q.slot_z = (int8_t)p.cv_slot_z;
+    q.slot_y = (int8_t)p.key_slot[1];
+    q.slot_p = (int8_t)p.cv_slot_p;
+    q.val_slot = (int8_t)p.val_slot;
+    q.val_type = p.val_type;
+    q.fold_kind = h->fold;
+    q.fast = (int8_t)fast;
+    q.fcol = (int8_t)fcol;
+    q.nops = (int32_t)p.stage_ops[0].size();
+    for (int i = 0; i < q.nops; ++i) q.ops[i] = p.stage_ops[0][i];
+    for (size_t i = 0; i < p.stage_consts[0].size(); ++i) q.consts[i] = p.stage_consts[0][i];
+    q.cval = h->dcur.as<uint32_t>();
+    q.cpres = h->dcur_pres.as<uint32_t>();
+    q.nval = h->dnext.as<uint32_t>();
+    q.npres = h->dnext_pres.as<uint32_t>();
+    q.fval = h->dvals.as<uint32_t>();
+    q.fpres = h->dpres.as<uint32_t>();
+    return XL_OK;
+  }
+
+  // Batched pull rounds: a sum/logsumexp stratum whose one carried-value rule
+  // adds or subtracts a column of e (every key with an in-edge from a delta
+  // key gets a value, so the marks need no join) enqueues `batched_rounds`
+  // rounds per host read.  Each round marks, lists and pulls with the key
+  // count in device memory (the list holds every slot), writes no delta
+  // rows, and leaves its delta size in a device array; rounds enqueued past
+  // the fixpoint find no marks and change nothing.
+  bool batched_pull(const Stratum& s) {
+    if (c->batched_rounds <= 0 || heads.size() != 1 || !heads[0]->ds || s.variants.size() != 1 ||
+        !s.variants[0].driver_delta || head_of(s.variants[0].head) != heads[0].get())
+      return false;
+    int fcol = 0;
+    if (!affine_value(s.variants[0], &fcol)) return false;
+    const HeadRun* h = heads[0].get();
+    return (double)h->nrank_d * h->range1 * 4 <= (double)c->arena.largest_free() / 2;  // the list
+  }
+
+  xl_status run_pull_batched(const RulePlan& p, HeadRun* h, int64_t max_iterations) {
+    const StepPlan& sp = p.steps[0];
+    int fcol = 0;
+    const int fast = affine_value(p, &fcol);
+    const int64_t nsd = h->nrank_d * h->range1;
+    IndexProbe rev{};
+    XL_TRY(get_index(sp.rel, p.carried_ycol, &rev));
+    const int B = c->batched_rounds;
+    Buf acc, rounds, list, tmp;
+    XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
+    XL_TRY(dalloc(c, (size_t)B * 4, &rounds, "round delta sizes"));
+    XL_TRY(dalloc(c, (size_t)nsd * 4, &list, "marked keys"));
+    XL_TRY(dalloc(c, k::bits_list_temp_bytes(nsd), &tmp, "compaction scratch"));
+    HIP_TRY(c, hipMemsetAsync(acc.p, 0, 8 * CNT_N, c->stream));
+    std::vector<hipEvent_t> evs;
+    if (c->profile) {
+      evs.resize(2 * (size_t)B, nullptr);
+      for (auto& e : evs) HIP_TRY(c, hipEventCreate(&e));
+    }
+    auto destroy_events = [&]() {
+      for (auto& e : evs)
+        if (e) (void)hipEventDestroy(e);
+      evs.clear();
+    };
+    int64_t pass = 0, delta = h->dn;
+    xl_status status = XL_OK;
+    while (delta > 0 && status == XL_OK) {
+      if (pass >= max_iterations) {
+        status = c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                     " reached before the fixpoint");
+        break;
+      }
+      const int nb = (int)std::min<int64_t>(B, max_iterations - pass);
+      for (int r = 0; r < nb; ++r) {
+        uint32_t* nr = rounds.as<uint32_t>() + r;
+        HIP_TRY(c, k::dense_mark_in(rev, sp.key_col, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
+                                    h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+        HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, nullptr, nr, tmp.p, false, c->stream));
+        HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, list.as<uint32_t>(), nr, tmp.p, true, c->stream));
+        DensePullArgs q{};
+        XL_TRY(pull_args(p, h, fast, fcol, q));
+        q.list = list.as<uint32_t>();
+        q.n = nsd;
+        q.n_dev = nr;
+        q.counters = acc.as<unsigned long long>();
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
+        HIP_TRY(c, k::dense_pull(q, c->stream));
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
+        std::swap(h->dcur.p, h->dnext.p);
+        std::swap(h->dcur_pres.p, h->dnext_pres.p);
+        HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)(nsd / 32) * 4, c->stream));
+      }
+      std::vector<uint32_t> n(nb);
+      XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));
+      int done = nb;
+      for (int r = 0; r < nb; ++r)
+        if (n[r] == 0) {
+          done = r + 1;
+          break;
+        }
+      for (int r = 0; r < done; ++r) {
+        st->iterations++;
+        record(n[r]);
+        st->new_tuples_total += n[r];
+        if (c->profile) {
+          float ms = 0;
+          HIP_TRY(c, hipEventElapsedTime(&ms, evs[2 * r], evs[2 * r + 1]));
+          st->pull_ms += ms;
+          st->pull_launches++;
+          st->pull_new += n[r];
+        }
+      }
+      pass += done;
+      delta = n[done - 1];
+    }
+    destroy_events();
+    u64 tot[CNT_N];
+    XL_TRY(ctl_read(c, acc.p, sizeof(tot), tot));
+    if (tot[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "marked key without a contribution (internal)");
+    cands += (int64_t)tot[CNT_CANDIDATES];
+    if (c->profile) st->pull_candidates += (int64_t)tot[CNT_CANDIDATES];
+    h->keys += (int64_t)tot[CNT_INSERTED];
+    h->dn = 0;
+    if (status != XL_OK) return status;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
+    return XL_OK;
+  }
+
   xl_status eval_dense_pull(const RulePlan& p, HeadRun* h) {
     h->pulled = true;
     h->pull_n = 0;
@@ -1716,34 +1856,9 @@ struct Runner {
                             c->stream));
     for (int j = 0; j < 3; ++j) XL_TRY(dalloc(c, (size_t)n * 4, &h->ndrow[j], "delta rows"));
     DensePullArgs q{};
+    XL_TRY(pull_args(p, h, fast, fcol, q));
     q.list = list.as<uint32_t>();
     q.n = n;
-    q.dict = h->dict.as<uint32_t>();
-    q.range1 = (uint32_t)h->range1;
-    q.nrank = (uint32_t)h->nrank_d;
-    q.lo1 = h->kp.lo[1];
-    XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
-    for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
-    q.rev.act[p.carried_ycol].kind = CA_NONE;  // Y is bound from the key
-    q.zcol = sp.key_col;
-    q.slot_s = (int8_t)p.cv_slot_s;
-    q.slot_z = (int8_t)p.cv_slot_z;
-    q.slot_y = (int8_t)p.key_slot[1];
-    q.slot_p = (int8_t)p.cv_slot_p;
-    q.val_slot = (int8_t)p.val_slot;
-    q.val_type = p.val_type;
-    q.fold_kind = h->fold;
-    q.fast = (int8_t)fast;
-    q.fcol = (int8_t)fcol;
-    q.nops = (int32_t)p.stage_ops[0].size();
-    for (int i = 0; i < q.nops; ++i) q.ops[i] = p.stage_ops[0][i];
-    for (size_t i = 0; i < p.stage_consts[0].size(); ++i) q.consts[i] = p.stage_consts[0][i];
-    q.cval = h->dcur.as<uint32_t>();
-    q.cpres = h->dcur_pres.as<uint32_t>();
-    q.nval = h->dnext.as<uint32_t>();
-    q.npres = h->dnext_pres.as<uint32_t>();
-    q.fval = h->dvals.as<uint32_t>();
-    q.fpres = h->dpres.as<uint32_t>();
     q.k0 = h->ndrow[0].as<uint32_t>();
     q.k1 = h->ndrow[1].as<uint32_t>();
     q.v = h->ndrow[2].as<uint32_t>();
@@ -2794,6 +2909,10 @@ struct Runner {
     record(total);
     if (s.recursive && total > 0 && batched_tiles(s)) {
       XL_TRY(run_tiles_batched(s.variants[0], heads[0].get(), max_iterations));
+      total = 0;
+    }
+    if (s.recursive && total > 0 && batched_pull(s)) {
+      XL_TRY(run_pull_batched(s.variants[0], heads[0].get(), max_iterations));
       total = 0;
     }
     if (s.recursive && total > 0 && resident_frontier(s)) {

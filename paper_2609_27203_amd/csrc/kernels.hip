@@ -1715,12 +1715,13 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
   __shared__ uint32_t s_m[DP_WAVES][64], s_acc[DP_WAVES][64], s_any[DP_WAVES][64];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const bool lse = a.fold_kind == FOLD_LSE, f32 = a.val_type == T_F32;
-  const int64_t nchunks = (a.n + 63) / 64;
+  const int64_t nkeys = a.n_dev ? (int64_t)*a.n_dev : a.n;
+  const int64_t nchunks = (nkeys + 63) / 64;
   uint32_t mine = 0, examined = 0;
   for (int64_t chunk = (int64_t)blockIdx.x * DP_WAVES + w; chunk < nchunks; chunk += (int64_t)gridDim.x * DP_WAVES) {
     const int64_t i = chunk * 64 + lane;
     uint32_t t = 0, e0 = 0, deg = 0;
-    if (i < a.n) {
+    if (i < nkeys) {
       t = a.list[i];
       const uint32_t kk = t / a.nrank + (uint32_t)a.lo1 - (uint32_t)a.rev.key_lo;
       if (kk < a.rev.key_range) {
@@ -1876,7 +1877,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
       wave_lds_sync();
     }
     uint32_t out = 0;
-    if (i < a.n) {
+    if (i < nkeys) {
       if (lse) {
         const float m = __uint_as_float(s_m[w][lane]);
         out = __float_as_uint(m == -INFINITY ? -INFINITY : m + logf(__uint_as_float(s_acc[w][lane])));
@@ -1884,10 +1885,12 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
         out = s_acc[w][lane];
       }
       if (!s_any[w][lane]) atomicOr(&a.counters[CNT_FATAL], 8ull);  // a marked key always has a contribution
-      const uint32_t r = t % a.nrank, yb = t / a.nrank;
-      a.k0[i] = a.dict[r];
-      a.k1[i] = yb + (uint32_t)a.lo1;
-      a.v[i] = out;
+      if (a.k0) {
+        const uint32_t r = t % a.nrank, yb = t / a.nrank;
+        a.k0[i] = a.dict[r];
+        a.k1[i] = yb + (uint32_t)a.lo1;
+        a.v[i] = out;
+      }
       a.nval[t] = out;
     }
     // Presence bits of the next delta and of the full relation (both laid out
@@ -1897,7 +1900,7 @@ __global__ __launch_bounds__(DP_WAVES * 64) void dense_pull_k(DensePullArgs by_v
     // whether its slot was present.  The full relation's value is then read
     // and written by its own lane (each slot is listed once).
     {
-      const bool act = i < a.n;
+      const bool act = i < nkeys;
       const uint32_t wd = act ? t >> 5 : 0xffffffffu;
       const uint32_t bit = act ? 1u << (t & 31) : 0u;
       const uint32_t wprev = __shfl_up(wd, 1, 64);

@@ -412,6 +412,40 @@ def test_min_rounds_iteration_cap(batch):
     assert engine_run(wl, max_iterations=passes, options={"batched_rounds": batch})[1]["iterations"] == passes
 
 
+@pytest.mark.parametrize("batch", [0, 1, 4, 64])
+def test_pull_rounds_batched(batch):
+    """Carried logsumexp rule over a dense head (one add, so the marks are the
+    in-neighbours' delta presence): pull rounds one at a time or enqueued in
+    batches of 1, 4 or 64 per host read with the key counts in device
+    memory; the oracle's values within the logsumexp tolerance and the same
+    per-round delta sizes and pass count either way."""
+    wl = W.small_workloads()["lse_dag"]()
+    print(f"case: pull rounds batch={batch}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"batched_rounds": batch, "profile": 1})
+    _compare(wl, rels, ref)
+    base = engine_run(wl, options={"batched_rounds": 0})[1]
+    assert stats["delta_rows"] == base["delta_rows"]
+    assert stats["iterations"] == base["iterations"] > 1
+    # (one at a time, the last pass finds no marked key and launches nothing)
+    assert stats["pull_launches"] == stats["iterations"] - (0 if batch else 1)
+
+
+@pytest.mark.parametrize("batch", [0, 4])
+def test_pull_rounds_iteration_cap(batch):
+    """A cap below the pass count is a convergence failure in both forms; the
+    exact pass count converges."""
+    from paper_2609_27203_amd import xlh
+    wl = W.small_workloads()["lse_dag"]()
+    print(f"case: pull cap batch={batch}", flush=True)
+    passes = engine_run(wl, options={"batched_rounds": 0})[1]["iterations"]
+    for cap in (0, 1, passes - 1):
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, max_iterations=cap, options={"batched_rounds": batch})
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+    assert engine_run(wl, max_iterations=passes, options={"batched_rounds": batch})[1]["iterations"] == passes
+
+
 SELF_JOIN_TC = """
 path(X,Y) :- edge(X,Y).
 path(X,Y) :- path(X,Z), path(Z,Y).
