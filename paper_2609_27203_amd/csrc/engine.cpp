@@ -1412,11 +1412,9 @@ struct Runner {
   // One gathered round: reads the delta rows flagged in gflag[gcur] from
   // (gcur ? gbits : dbits), writes the next delta into the other pair, then
   // clears the rows it read.
-  xl_status eval_gathered(const RulePlan& p, HeadRun* h) {
-    h->fnew = 0;
+  xl_status gather_args(const RulePlan& p, HeadRun* h, GatherArgs& a) {
     GatherShape g;
     if (!gather_shape(p, &g)) return c->fail(XL_DEVICE_ERROR, "gathered round of another rule shape (internal)");
-    GatherArgs a{};
     a.in_bits = (h->gcur ? h->gbits : h->dbits).as<uint32_t>();
     a.out_bits = (h->gcur ? h->dbits : h->gbits).as<uint32_t>();
     a.in_flag = h->gflag[h->gcur].as<uint32_t>();
@@ -1430,6 +1428,13 @@ struct Runner {
     a.lo1 = a.push.lo1 = h->kp.lo[1];
     a.row_words = a.push.row_words = h->row_words;
     a.range0 = h->range0;
+    return XL_OK;
+  }
+
+  xl_status eval_gathered(const RulePlan& p, HeadRun* h) {
+    h->fnew = 0;
+    GatherArgs a{};
+    XL_TRY(gather_args(p, h, a));
     a.counters = c->dcounters;
     HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
@@ -1663,6 +1668,84 @@ struct Runner {
     q.npres = h->dnext_pres.as<uint32_t>();
     q.fval = h->dvals.as<uint32_t>();
     q.fpres = h->dpres.as<uint32_t>();
+    return XL_OK;
+  }
+
+  // Batched gathered rounds: each round gets its own counter block, so
+  // `batched_rounds` rounds run per host read; rounds past the fixpoint find
+  // no flagged delta row and change nothing.
+  bool batched_gather(const Stratum& s) {
+    return c->batched_rounds > 0 && heads.size() == 1 && heads[0]->gathered && heads[0]->gather_ready &&
+           s.variants.size() == 1 && s.variants[0].driver_delta && head_of(s.variants[0].head) == heads[0].get();
+  }
+
+  xl_status run_gather_batched(const RulePlan& p, HeadRun* h, int64_t max_iterations) {
+    const int B = c->batched_rounds;
+    Buf acc;
+    XL_TRY(dalloc(c, (size_t)B * 8 * CNT_N, &acc, "round counters"));
+    std::vector<hipEvent_t> evs;
+    if (c->profile) {
+      evs.resize(2 * (size_t)B, nullptr);
+      for (auto& e : evs) HIP_TRY(c, hipEventCreate(&e));
+    }
+    auto destroy_events = [&]() {
+      for (auto& e : evs)
+        if (e) (void)hipEventDestroy(e);
+      evs.clear();
+    };
+    int64_t pass = 0, delta = 1;
+    xl_status status = XL_OK;
+    while (delta > 0 && status == XL_OK) {
+      if (pass >= max_iterations) {
+        status = c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                     " reached before the fixpoint");
+        break;
+      }
+      const int nb = (int)std::min<int64_t>(B, max_iterations - pass);
+      HIP_TRY(c, hipMemsetAsync(acc.p, 0, (size_t)nb * 8 * CNT_N, c->stream));
+      for (int r = 0; r < nb; ++r) {
+        GatherArgs a{};
+        XL_TRY(gather_args(p, h, a));
+        a.counters = acc.as<unsigned long long>() + (size_t)r * CNT_N;
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
+        HIP_TRY(c, k::gather_round(a, c->stream));
+        if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
+        HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(),
+                                         h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words, c->stream));
+        h->gcur ^= 1;
+      }
+      std::vector<u64> cnt((size_t)nb * CNT_N);  // at most 64 blocks of 64 B: one control read
+      XL_TRY(ctl_read(c, acc.p, (size_t)nb * 8 * CNT_N, cnt.data()));
+      int done = nb;
+      for (int r = 0; r < nb; ++r)
+        if (cnt[(size_t)r * CNT_N + CNT_APPENDED] == 0) {
+          done = r + 1;
+          break;
+        }
+      for (int r = 0; r < done; ++r) {
+        const u64* cr = cnt.data() + (size_t)r * CNT_N;
+        st->iterations++;
+        record((int64_t)cr[CNT_APPENDED]);
+        st->new_tuples_total += (int64_t)cr[CNT_APPENDED];
+        cands += (int64_t)cr[CNT_CANDIDATES];
+        h->keys += (int64_t)cr[CNT_APPENDED];
+        if (c->profile) {
+          float ms = 0;
+          HIP_TRY(c, hipEventElapsedTime(&ms, evs[2 * r], evs[2 * r + 1]));
+          st->gather_ms += ms;
+          st->gather_launches++;
+          st->gather_candidates += (int64_t)cr[CNT_CANDIDATES];
+          st->gather_new += (int64_t)cr[CNT_APPENDED];
+        }
+      }
+      pass += done;
+      delta = (int64_t)cnt[(size_t)(done - 1) * CNT_N + CNT_APPENDED];
+    }
+    destroy_events();
+    if (status != XL_OK) return status;
+    if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+      return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                               std::to_string(h->rel->max_rows));
     return XL_OK;
   }
 
@@ -2913,6 +2996,10 @@ struct Runner {
     }
     if (s.recursive && total > 0 && batched_pull(s)) {
       XL_TRY(run_pull_batched(s.variants[0], heads[0].get(), max_iterations));
+      total = 0;
+    }
+    if (s.recursive && total > 0 && batched_gather(s)) {
+      XL_TRY(run_gather_batched(s.variants[0], heads[0].get(), max_iterations));
       total = 0;
     }
     if (s.recursive && total > 0 && resident_frontier(s)) {

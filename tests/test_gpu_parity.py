@@ -669,19 +669,20 @@ def _gather_workload(variant):
     return W.Workload(variant, rules, edb, {"h": ("i32", "i32")}), "h"
 
 
-@pytest.mark.parametrize("gather", [0, 1])
+@pytest.mark.parametrize("gather,batch", [(0, 4), (1, 0), (1, 1), (1, 4), (1, 64)])
 @pytest.mark.parametrize("variant", ["sg", "sg_reordered", "dag", "dag_swapped"])
-def test_gathered_rounds(variant, gather):
+def test_gathered_rounds(variant, gather, batch):
     """h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) in gathered rounds (head row
     X staged in LDS, the Y values of the B bits of its A values' delta rows
-    set there) and in the generic join: the oracle's rows and per-round delta
-    sizes either way, also over random graphs where an X has many A (several
+    set there; one round or 1, 4 or 64 rounds per host read) and in the
+    generic join: the oracle's rows and per-round delta sizes either way,
+    also over random graphs where an X has many A (several
     delta rows per head row, one delta row read for many X) and with the
     columns and atoms in other orders."""
     wl, head = _gather_workload(variant)
-    print(f"case: gathered rounds {variant} gather={gather}", flush=True)
+    print(f"case: gathered rounds {variant} gather={gather} batch={batch}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, stats, _ = engine_run(wl, options={"gather_rounds": gather, "profile": 1})
+    rels, stats, _ = engine_run(wl, options={"gather_rounds": gather, "batched_rounds": batch, "profile": 1})
     _compare(wl, rels, ref)
     levels = _delta_levels(ref, head)
     assert stats["delta_rows"][:len(levels)] == levels
