@@ -350,6 +350,7 @@ void relation_free_storage(Relation* r) {
     r->col[j] = nullptr;
   }
   r->nrows = 0;
+  r->sorted = false;
   r->generation = ++r->ctx->generations;  // cached indexes of the old rows no longer match
   r->ctx->icache_drop(r, true);
 }
@@ -423,6 +424,7 @@ xl_status relation_load(Relation* r, const void* const* cols, int64_t n, int on_
   relation_free_storage(r);
   for (int j = 0; j < r->arity; ++j) r->col[j] = (uint32_t*)fin[j].keep();
   r->nrows = m;
+  r->sorted = true;  // the deduplication above leaves the rows in lexicographic order
   XL_TRY(compute_bounds(c, r));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return XL_OK;
@@ -747,6 +749,29 @@ struct Runner {
                                            " exceeds 2^30 values");
       const bool ordered = order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32;
       const int kbits = std::max(1, bitlen((uint64_t)range - 1));
+      // A loaded relation keeps its rows in lexicographic order, so its index
+      // by the first column -- plain, or ordered by the second column's
+      // values -- is its rows as they are: only the offsets are built, and
+      // the index reads the relation's own columns.
+      const bool presorted = !head_of(rel) && rel->sorted && col == 0 &&
+                             (order_col < 0 || (ordered && order_col == 1 && order_kind == 1));
+      if (presorted) {
+        Buf keys;
+        XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+        HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
+        void* off;
+        XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
+        HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)range, (uint32_t*)off, c->stream));
+        for (int j = 0; j < rel->arity; ++j) p.col[j] = rcol[j];
+        p.off = (uint32_t*)off;
+        p.key_lo = klo;
+        p.key_range = (uint32_t)range;
+        *out = p;
+        if (first) *first = ix->first;
+        if (cacheable) cache_index(*ix);
+        indexes.push_back(std::move(ix));
+        return XL_OK;
+      }
       Buf keys, perm, perm2, tmp;
       XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
       XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));

@@ -67,6 +67,7 @@ struct Relation {
   uint32_t* col[MAXC] = {};  // device columns (arena), nrows valid rows
   int64_t nrows = 0;
   int32_t lo[MAXC] = {}, hi[MAXC] = {};  // bounds of i32 columns when nrows > 0
+  bool sorted = false;  // rows in ascending lexicographic order (as a load stores them)
   uint64_t generation = 0;  // new value (unique in the context) whenever the rows change
 };
 
