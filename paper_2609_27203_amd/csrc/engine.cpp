@@ -2025,6 +2025,20 @@ struct Runner {
       return XL_OK;
     }
     if (n > ((int64_t)1 << 30)) return c->fail(XL_UNSUPPORTED, "relation " + e->name + " too large to tile");
+    // A loaded relation with Z in its first column and Y in its second is in
+    // (Z, Y) order, hence in (Z, tile) order when every Y lies in the head's
+    // domain (the tiles ascend with Y): only the offsets are built, and the
+    // index reads the relation's own columns.
+    if (!head_of(e) && e->sorted && zc == 0 && p.carried_ycol == 1 && e->types[1] == T_I32 &&
+        (int64_t)e->lo[1] >= h->kp.lo[1] && (int64_t)e->hi[1] - h->kp.lo[1] < h->range1) {
+      Buf keys;
+      XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+      HIP_TRY(c, k::tile_keys(e->col[0], e->col[1], n, e->lo[0], h->kp.lo[1], h->tile, h->ntiles, keys.as<uint32_t>(),
+                              c->stream));
+      HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)nkeys, h->toff.as<uint32_t>(), c->stream));
+      for (int j = 0; j < e->arity; ++j) q.col[j] = e->col[j];
+      return XL_OK;
+    }
     Buf keys, keys2, perm, perm2, tmp;
     XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
     XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
