@@ -1796,8 +1796,8 @@ struct Runner {
     int fcol = 0;
     const int fast = affine_value(p, &fcol);
     const int64_t nsd = h->nrank_d * h->range1;
-    IndexProbe rev{};
-    XL_TRY(get_index(sp.rel, p.carried_ycol, &rev));
+    IndexProbe fwd{};
+    XL_TRY(get_index(sp.rel, sp.key_col, &fwd));
     const int B = c->batched_rounds;
     Buf acc, rounds, list, tmp;
     XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
@@ -1826,8 +1826,8 @@ struct Runner {
       const int nb = (int)std::min<int64_t>(B, max_iterations - pass);
       for (int r = 0; r < nb; ++r) {
         uint32_t* nr = rounds.as<uint32_t>() + r;
-        HIP_TRY(c, k::dense_mark_in(rev, sp.key_col, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
-                                    h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+        HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
+                                     h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
         HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, nullptr, nr, tmp.p, false, c->stream));
         HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, list.as<uint32_t>(), nr, tmp.p, true, c->stream));
         DensePullArgs q{};
@@ -1904,12 +1904,13 @@ struct Runner {
     const int64_t nsd = h->nrank_d * h->range1;
     if (fast) {
       // every key with an in-edge from a delta key receives a value, so the
-      // marks are the OR of the in-neighbours' delta presence rows
-      IndexProbe rev{};
-      XL_TRY(get_index(sp.rel, p.carried_ycol, &rev));
+      // marks are the delta presence rows pushed to the out-neighbours (the
+      // mark bits are clear: the previous list pass cleared what it listed)
+      IndexProbe fwd{};
+      XL_TRY(get_index(sp.rel, sp.key_col, &fwd));
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
-      HIP_TRY(c, k::dense_mark_in(rev, sp.key_col, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
-                                  h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+      HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
+                                   h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
       if (c->profile) {
         HIP_TRY(c, hipEventRecord(ev[1], c->stream));
         HIP_TRY(c, hipEventSynchronize(ev[1]));

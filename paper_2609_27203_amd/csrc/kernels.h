@@ -158,9 +158,10 @@ hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* to
                      hipStream_t s);
 hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);
 // Marks (target-major, nrank a multiple of 32) of the keys that receive a
-// contribution from the delta presence bits pres, through e's index by Y.
-hipError_t dense_mark_in(const IndexProbe& rev, int zcol, int32_t lo1, uint32_t range1, uint32_t nrank,
-                         const uint32_t* pres, uint32_t* mark, hipStream_t s);
+// contribution from the delta presence bits pres, pushed through e's index by
+// its Z column (fwd; ycol = e's Y column); mark must be all zero on entry.
+hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t nrank,
+                          const uint32_t* pres, uint32_t* mark, hipStream_t s);
 // Rows of the set bits of a dense key bitmap in bit order (two calls on the
 // same temp as bits_list; temp sized by bits_list_temp_bytes); clear = zero
 // the words read.

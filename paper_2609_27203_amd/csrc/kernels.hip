@@ -1990,35 +1990,36 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
 }
 
 // Marks of a carried-value round whose value is one add or subtract (every
-// candidate then yields a value): word w of target y's mark row = OR over
-// y's in-edges (z, y) of word w of z's delta presence row, both rows
-// target-major with wpr words.  Plain stores, no atomics; the threads of one
-// target read one presence row segment each.
-__global__ void dense_mark_in_k(IndexProbe rev, int zcol, int32_t lo1, uint32_t range1, uint32_t wpr,
-                                const uint32_t* pres, uint32_t* mark) {
+// candidate then yields a value), both rows target-major with wpr words:
+// every nonzero word w of z's delta presence row is ORed into word w of the
+// mark row of each out-neighbour y of z (mark all zero on entry).  Only the
+// delta's words cost more than one load; reading every target's in-edges
+// instead took three times as long on the layered DAG.
+__global__ void dense_mark_out_k(IndexProbe fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t wpr,
+                                 const uint32_t* pres, uint32_t* mark) {
   const int64_t n = (int64_t)range1 * wpr;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t yb = (uint32_t)(i / wpr), wd = (uint32_t)(i % wpr);
-    const uint32_t kk = yb + (uint32_t)lo1 - (uint32_t)rev.key_lo;
-    uint32_t acc = 0;
-    if (kk < rev.key_range) {
-      const uint32_t e1 = rev.off[kk + 1];
-      for (uint32_t e = rev.off[kk]; e < e1; ++e) {
-        const uint32_t zb = rev.col[zcol][e] - (uint32_t)lo1;
-        if (zb < range1) acc |= pres[(u64)zb * wpr + wd];
-      }
+    const uint32_t p = pres[i];
+    if (!p) continue;
+    const uint32_t zb = (uint32_t)(i / wpr), wd = (uint32_t)(i % wpr);
+    const uint32_t kk = zb + (uint32_t)lo1 - (uint32_t)fwd.key_lo;
+    if (kk >= fwd.key_range) continue;
+    const uint32_t e1 = fwd.off[kk + 1];
+    for (uint32_t e = fwd.off[kk]; e < e1; ++e) {
+      const uint32_t yb = fwd.col[ycol][e] - (uint32_t)lo1;
+      if (yb < range1) atomicOr(&mark[(u64)yb * wpr + wd], p);
     }
-    mark[i] = acc;
   }
 }
-hipError_t dense_mark_in(const IndexProbe& rev, int zcol, int32_t lo1, uint32_t range1, uint32_t nrank,
-                         const uint32_t* pres, uint32_t* mark, hipStream_t s) {
+hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t nrank,
+                          const uint32_t* pres, uint32_t* mark, hipStream_t s) {
   const uint32_t wpr = nrank / 32;
   if (range1 == 0 || wpr == 0 || nrank % 32 != 0) return hipErrorInvalidValue;
-  dense_mark_in_k<<<grid_for((int64_t)range1 * wpr, 256, 65536), 256, 0, s>>>(rev, zcol, lo1, range1, wpr, pres,
-                                                                             mark);
+  dense_mark_out_k<<<grid_for((int64_t)range1 * wpr, 256, 65536), 256, 0, s>>>(fwd, ycol, lo1, range1, wpr, pres,
+                                                                              mark);
   return hipGetLastError();
 }
+
 
 // ============================================================ dense min/max heads, tiled rounds
 // Delta rows of a dense min/max head from its delta bits, in slot order
