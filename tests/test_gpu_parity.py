@@ -693,6 +693,21 @@ def test_gathered_rounds(variant, gather, batch):
         assert stats["gather_launches"] == 0
 
 
+@pytest.mark.parametrize("batch", [0, 4])
+def test_gathered_rounds_iteration_cap(batch):
+    """Gathered rounds one at a time or batched: a cap below the pass count is
+    a convergence failure, the exact pass count converges."""
+    from paper_2609_27203_amd import xlh
+    wl, _ = _gather_workload("sg")
+    print(f"case: gathered cap batch={batch}", flush=True)
+    passes = engine_run(wl, options={"batched_rounds": 0})[1]["iterations"]
+    for cap in (0, 1, passes - 1):
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, max_iterations=cap, options={"batched_rounds": batch})
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+    assert engine_run(wl, max_iterations=passes, options={"batched_rounds": batch})[1]["iterations"] == passes
+
+
 def test_resume_from_fixpoint_is_idempotent():
     wl = W.small_workloads()["same_generation"]()
     rels, _, ctx = engine_run(wl)
