@@ -664,21 +664,26 @@ def _gather_workload(variant):
     f_src, f_dst = W.uniform_graph(300, 600, 32)
     edb = {"e": (("i32", "i32"), [np.asarray(e_src, np.int32), np.asarray(e_dst, np.int32)]),
            "f": (("i32", "i32"), [np.asarray(f_src, np.int32), np.asarray(f_dst, np.int32)])}
+    if variant == "func":  # e1 pairs every X with exactly one A (a random function, with cycles)
+        g = np.random.default_rng(33)
+        edb["p"] = (("i32", "i32"), [np.arange(300, dtype=np.int32), g.integers(0, 300, 300).astype(np.int32)])
     rules = {"dag": "h(X,Y) :- e(X,Y).\nh(X,Y) :- e(X,A), h(A,B), f(Y,B).",
-             "dag_swapped": "h(X,Y) :- e(Y,X).\nh(X,Y) :- e(A,X), h(A,B), f(B,Y)."}[variant]
+             "dag_swapped": "h(X,Y) :- e(Y,X).\nh(X,Y) :- e(A,X), h(A,B), f(B,Y).",
+             "func": "h(X,Y) :- e(X,Y).\nh(X,Y) :- p(X,A), h(A,B), f(Y,B)."}[variant]
     return W.Workload(variant, rules, edb, {"h": ("i32", "i32")}), "h"
 
 
 @pytest.mark.parametrize("gather,batch", [(0, 4), (1, 0), (1, 1), (1, 4), (1, 64)])
-@pytest.mark.parametrize("variant", ["sg", "sg_reordered", "dag", "dag_swapped"])
+@pytest.mark.parametrize("variant", ["sg", "sg_reordered", "dag", "dag_swapped", "func"])
 def test_gathered_rounds(variant, gather, batch):
     """h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) in gathered rounds (head row
     X staged in LDS, the Y values of the B bits of its A values' delta rows
     set there; one round or 1, 4 or 64 rounds per host read) and in the
     generic join: the oracle's rows and per-round delta sizes either way,
     also over random graphs where an X has many A (several
-    delta rows per head row, one delta row read for many X) and with the
-    columns and atoms in other orders."""
+    delta rows per head row, one delta row read for many X), where e1 is a
+    random function (one A per X, cycles), and with the columns and atoms in
+    other orders."""
     wl, head = _gather_workload(variant)
     print(f"case: gathered rounds {variant} gather={gather} batch={batch}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
