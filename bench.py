@@ -151,7 +151,7 @@ def main():
                     help="run only a plain 1 GiB copy (counter calibration for the traffic figure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default="tc_rmat_count",
-                    help="one of the engine's five workloads (the headline line uses tc_rmat_count)")
+                    help="one of the engine's six workloads (the headline line uses tc_rmat_count)")
     ap.add_argument("--index-mode", type=int, default=0, help="0 auto, 1 hash tables only, 2 prefer dense")
     ap.add_argument("--option", action="append", default=[], metavar="KEY=VALUE",
                     help="extra engine option (xl_context_set_option), repeatable")
