@@ -1150,8 +1150,11 @@ struct Runner {
     XL_TRY(ctl_read(c, tot.p, 4, &n0));
     h->n0 = n0;
     const double slots = (double)std::max<uint32_t>(n0, 1) * (double)h->range1;
+    // sum/logsumexp heads pad the ranks to whole words: their slot indices
+    // (32-bit in the kernels) run up to the padded count
+    const double padded = h->ds ? (double)((std::max<uint32_t>(n0, 1) + 31) / 32 * 32) * (double)h->range1 : slots;
     const double budget = std::min(8589934592.0, (double)c->arena.capacity() / 4);
-    if (slots >= 4294967296.0 || slots * (h->ds ? 16.5 : 8.25) > budget) {
+    if (padded >= 4294967296.0 || padded * (h->ds ? 16.5 : 8.25) > budget) {
       h->dv = h->ds = h->tiled = false;
       h->dmap.reset();
       return XL_OK;
