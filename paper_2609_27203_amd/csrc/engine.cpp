@@ -344,6 +344,37 @@ xl_status resolve_wide_constants(Program* p) {
   return XL_OK;
 }
 
+// The gathered-round shape (see GatherShape).
+bool gather_shape(const RulePlan& p, GatherShape* g) {
+  if (!p.driver_delta || p.driver != p.head || p.driver->arity != 2 || p.steps.size() != 2 || p.nkey != 2 ||
+      !p.negs.empty())
+    return false;
+  for (const auto& ops : p.stage_ops)
+    if (!ops.empty()) return false;
+  const ColAct &da = p.driver_act[0], &db = p.driver_act[1];
+  if (da.kind != CA_BIND || db.kind != CA_BIND || da.slot == db.slot) return false;
+  int ia = -1, ib = -1;
+  for (int k = 0; k < 2; ++k) {
+    if (p.steps[k].key_slot == da.slot) ia = k;
+    else if (p.steps[k].key_slot == db.slot) ib = k;
+  }
+  if (ia < 0 || ib < 0) return false;
+  auto other = [&](const StepPlan& st, int* col, int* slot) {
+    if (st.rel == p.head || st.rel->arity != 2) return false;
+    const int oc = 1 - st.key_col;
+    if (st.act[oc].kind != CA_BIND) return false;
+    *col = oc;
+    *slot = st.act[oc].slot;
+    return true;
+  };
+  int xs = -1, ys = -1;
+  if (!other(p.steps[ia], &g->x_col, &xs) || !other(p.steps[ib], &g->y_col, &ys)) return false;
+  if (xs != p.key_slot[0] || ys != p.key_slot[1] || xs == ys) return false;
+  g->s1 = ia;
+  g->s2 = ib;
+  return true;
+}
+
 void relation_free_storage(Relation* r) {
   for (int j = 0; j < MAXC; ++j) {
     if (r->col[j]) r->ctx->arena.release(r->col[j]);
@@ -1399,42 +1430,6 @@ struct Runner {
     }
     f.counters = c->dcounters;
     return XL_OK;
-  }
-
-  // h(X, Y) :- e1(X, A), delta h(A, B), e2(Y, B) with nothing else, e1 and e2
-  // binary relations outside the stratum: the shape of a gathered round.
-  struct GatherShape {
-    int s1 = 0, s2 = 0;        // steps keyed by A (e1) and by B (e2)
-    int x_col = 0, y_col = 0;  // e1's X column, e2's Y column
-  };
-  static bool gather_shape(const RulePlan& p, GatherShape* g) {
-    if (!p.driver_delta || p.driver != p.head || p.driver->arity != 2 || p.steps.size() != 2 || p.nkey != 2 ||
-        !p.negs.empty())
-      return false;
-    for (const auto& ops : p.stage_ops)
-      if (!ops.empty()) return false;
-    const ColAct &da = p.driver_act[0], &db = p.driver_act[1];
-    if (da.kind != CA_BIND || db.kind != CA_BIND || da.slot == db.slot) return false;
-    int ia = -1, ib = -1;
-    for (int k = 0; k < 2; ++k) {
-      if (p.steps[k].key_slot == da.slot) ia = k;
-      else if (p.steps[k].key_slot == db.slot) ib = k;
-    }
-    if (ia < 0 || ib < 0) return false;
-    auto other = [&](const StepPlan& st, int* col, int* slot) {
-      if (st.rel == p.head || st.rel->arity != 2) return false;
-      const int oc = 1 - st.key_col;
-      if (st.act[oc].kind != CA_BIND) return false;
-      *col = oc;
-      *slot = st.act[oc].slot;
-      return true;
-    };
-    int xs = -1, ys = -1;
-    if (!other(p.steps[ia], &g->x_col, &xs) || !other(p.steps[ib], &g->y_col, &ys)) return false;
-    if (xs != p.key_slot[0] || ys != p.key_slot[1] || xs == ys) return false;
-    g->s1 = ia;
-    g->s2 = ib;
-    return true;
   }
 
   // One gathered round: reads the delta rows flagged in gflag[gcur] from

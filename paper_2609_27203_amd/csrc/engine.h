@@ -272,6 +272,13 @@ xl_status compile_program(Context* ctx, const char* text, Program** out);
 std::string explain_program(const Program* p);
 
 // engine.cpp
+// h(X, Y) :- e1(X, A), delta h(A, B), e2(Y, B) with nothing else, e1 and e2
+// binary relations outside the stratum: the shape of a gathered round.
+struct GatherShape {
+  int s1 = 0, s2 = 0;        // steps keyed by A (e1) and by B (e2)
+  int x_col = 0, y_col = 0;  // e1's X column, e2's Y column
+};
+bool gather_shape(const RulePlan& p, GatherShape* g);
 xl_status relation_load(Relation* r, const void* const* cols, int64_t n, int on_device);
 xl_status relation_read(const Relation* r, void* const* cols, int64_t cap, int64_t* out_rows,
                         int on_device);

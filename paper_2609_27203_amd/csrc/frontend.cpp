@@ -926,6 +926,8 @@ std::string explain_program(const Program* p) {
         if (rp.val_slot >= 0) os << " val v" << rp.val_slot;
         if (rp.carried) os << " [grouped by v" << rp.key_slot[0] << "]";
         if (rp.carried_val) os << " [keyed by v" << rp.key_slot[0] << ", v" << rp.key_slot[1] << "]";
+        GatherShape gs;
+        if (gather_shape(rp, &gs)) os << " [gathered by head row v" << rp.key_slot[0] << "]";
         os << "\n";
       }
     }

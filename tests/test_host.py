@@ -43,6 +43,9 @@ def test_workload_programs_compile(name):
         assert plan.index("stratum 0 recursive heads: path") < plan.index("stratum 1 non-recursive heads: reach_count[count]")
     if name == "same_generation":   # delta variant joins parent twice, both by the parent column
         assert "delta sg(v0,v1) -> join parent on col 1=v0 (v2,_) -> join parent on col 1=v1 (v3,_)" in plan
+        assert "[gathered by head row v2]" in plan  # h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B)
+    if name == "tc_rmat_count":
+        assert "[gathered" not in plan
 
 
 def test_delta_variant_per_recursive_atom():
