@@ -672,6 +672,13 @@ hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n
 // the output order is the slot order.
 constexpr int CP_THREADS = 256;
 constexpr int CP_RANGE = CP_THREADS * 32;
+// Items per workgroup: CP_RANGE for large inputs, fewer for small ones so
+// that about 256 workgroups share the passes (a few long ranges would each
+// walk dozens of scan steps one after another).
+static int64_t cp_range(int64_t n) {
+  const int64_t r = (n / 256 + CP_THREADS - 1) / CP_THREADS * CP_THREADS;
+  return std::min<int64_t>(CP_RANGE, std::max<int64_t>(CP_THREADS, r));
+}
 
 enum CompactKind { CK_NONEMPTY = 0, CK_STAMP = 1, CK_COUNTER = 2, CK_DENSE = 3 };
 
@@ -693,6 +700,7 @@ struct CompactArgs {
   uint32_t* range_cnt;    // [nranges]
   const uint32_t* range_off;
   int64_t out_cap;
+  int64_t rlen;           // items per workgroup (cp_range(n), a multiple of CP_THREADS)
 };
 
 __device__ __forceinline__ bool cp_keep(const CompactArgs& a, int64_t i) {
@@ -705,19 +713,19 @@ __device__ __forceinline__ bool cp_keep(const CompactArgs& a, int64_t i) {
 }
 
 __global__ __launch_bounds__(CP_THREADS) void compact_count_k(CompactArgs a) {
-  const int64_t base = (int64_t)blockIdx.x * CP_RANGE;
+  const int64_t base = (int64_t)blockIdx.x * a.rlen;
   uint32_t c = 0;
-  for (int k = 0; k < CP_RANGE / CP_THREADS; ++k) c += cp_keep(a, base + (int64_t)k * CP_THREADS + threadIdx.x);
+  for (int64_t k = 0; k < a.rlen / CP_THREADS; ++k) c += cp_keep(a, base + k * CP_THREADS + threadIdx.x);
   uint32_t tot;
   block_excl_scan<uint32_t>(c, &tot);
   if (threadIdx.x == 0) a.range_cnt[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
-  const int64_t base = (int64_t)blockIdx.x * CP_RANGE;
+  const int64_t base = (int64_t)blockIdx.x * a.rlen;
   uint32_t out = a.range_off[blockIdx.x];
-  for (int k = 0; k < CP_RANGE / CP_THREADS; ++k) {
-    const int64_t i = base + (int64_t)k * CP_THREADS + threadIdx.x;
+  for (int64_t k = 0; k < a.rlen / CP_THREADS; ++k) {
+    const int64_t i = base + k * CP_THREADS + threadIdx.x;
     const bool keep = cp_keep(a, i);
     uint32_t tot;
     const uint32_t p = out + block_excl_scan<uint32_t>(keep ? 1u : 0u, &tot);
@@ -751,7 +759,8 @@ __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
 }
 
 static hipError_t compact_run(CompactArgs a, uint32_t* total, void* temp, hipStream_t s) {
-  const int64_t nr = (a.n + CP_RANGE - 1) / CP_RANGE;
+  a.rlen = cp_range(a.n);
+  const int64_t nr = (a.n + a.rlen - 1) / a.rlen;
   if (nr == 0) return hipMemsetAsync(total, 0, 4, s);
   uint32_t* cnt = (uint32_t*)temp;
   uint32_t* off = cnt + ((nr + 63) & ~63ll);
@@ -767,7 +776,7 @@ static hipError_t compact_run(CompactArgs a, uint32_t* total, void* temp, hipStr
 }
 
 size_t compact_temp_bytes(int64_t n) {
-  const int64_t nr = (n + CP_RANGE - 1) / CP_RANGE;
+  const int64_t nr = (n + cp_range(n) - 1) / cp_range(n);
   return (size_t)((nr + 63) & ~63ll) * 8 + scan_temp_bytes(nr) + 256;
 }
 
