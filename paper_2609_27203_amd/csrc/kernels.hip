@@ -1532,28 +1532,38 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
 
 // ============================================================ dense sum / logsumexp heads
 // Marked slots -> ascending slot list, clearing the marks.  Each workgroup
-// owns MK_WORDS consecutive bitmap words: count pass, scan of the per-group
+// owns MK_THREADS * wpt consecutive bitmap words: count pass, scan of the per-group
 // counts, write pass.
-constexpr int MK_THREADS = 256, MK_WPT = 4, MK_WORDS = MK_THREADS * MK_WPT;
+constexpr int MK_THREADS = 256, MK_WPT = 4;
 
-__global__ __launch_bounds__(MK_THREADS) void bits_count_k(const uint32_t* bits, int64_t nw, uint32_t* cnt) {
-  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
+// Words per thread of a bitmap pass over nw words: the most (at most MK_WPT)
+// that still gives about 512 workgroups, so a small bitmap spreads over the
+// chip.  The count and write passes of one bitmap take the same value.
+static int mk_wpt(int64_t nw) {
+  return nw >= (int64_t)MK_THREADS * 4 * 512 ? 4 : nw >= (int64_t)MK_THREADS * 2 * 512 ? 2 : 1;
+}
+static int64_t mk_blocks(int64_t nw, int wpt) {
+  const int64_t words = (int64_t)MK_THREADS * wpt;
+  return (nw + words - 1) / words;
+}
+
+__global__ __launch_bounds__(MK_THREADS) void bits_count_k(const uint32_t* bits, int64_t nw, int wpt, uint32_t* cnt) {
+  const int64_t w0 = (int64_t)blockIdx.x * MK_THREADS * wpt + (int64_t)threadIdx.x * wpt;
   uint32_t c = 0;
-#pragma unroll
-  for (int k = 0; k < MK_WPT; ++k)
+  for (int k = 0; k < wpt; ++k)
     if (w0 + k < nw) c += __popc(bits[w0 + k]);
   uint32_t tot;
   block_excl_scan<uint32_t>(c, &tot);
   if (threadIdx.x == 0) cnt[blockIdx.x] = tot;
 }
 
-__global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_t nw, const uint32_t* off,
+__global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_t nw, int wpt, const uint32_t* off,
                                                           uint32_t* list) {
-  const int64_t w0 = (int64_t)blockIdx.x * MK_WORDS + (int64_t)threadIdx.x * MK_WPT;
+  const int64_t w0 = (int64_t)blockIdx.x * MK_THREADS * wpt + (int64_t)threadIdx.x * wpt;
   uint32_t d[MK_WPT], c = 0;
 #pragma unroll
   for (int k = 0; k < MK_WPT; ++k) {
-    d[k] = w0 + k < nw ? bits[w0 + k] : 0u;
+    d[k] = k < wpt && w0 + k < nw ? bits[w0 + k] : 0u;
     c += __popc(d[k]);
   }
   uint32_t tot;
@@ -1569,17 +1579,18 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
 // Rows (k0, k1) of the set bits of a dense key bitmap, in bit order: bit b
 // is k0 = lo0 + b / row_bits, k1 = lo1 + b % row_bits (one key: k0 = lo0 + b).
 // Optionally clears the words it read (a delta bitmap).  A workgroup owns
-// MK_WORDS consecutive words (the same ranges as bits_count_k) and walks them
+// MK_THREADS * wpt consecutive words (the same ranges as bits_count_k) and walks them
 // in steps of one word per thread: the step's set bits are ranked by a block
 // scan and staged in LDS, then written out with consecutive threads on
 // consecutive rows.
-__global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_t nw, const uint32_t* off,
+__global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_t nw, int wpt, const uint32_t* off,
                                                           u64 row_bits, int32_t lo0, int32_t lo1, int nkey,
                                                           bool clear, uint32_t* c0, uint32_t* c1) {
   __shared__ uint32_t stage[MK_THREADS * 32];
   uint32_t p = off[blockIdx.x];
-  for (int k = 0; k < MK_WPT; ++k) {
-    const int64_t wi = (int64_t)blockIdx.x * MK_WORDS + (int64_t)k * MK_THREADS + threadIdx.x;
+  const u64 base = (u64)blockIdx.x * MK_THREADS * wpt * 32u;
+  for (int k = 0; k < wpt; ++k) {
+    const int64_t wi = (int64_t)blockIdx.x * MK_THREADS * wpt + (int64_t)k * MK_THREADS + threadIdx.x;
     const uint32_t d = wi < nw ? bits[wi] : 0u;
     uint32_t tot;
     uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
@@ -1588,7 +1599,6 @@ __global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_
       for (uint32_t b = d; b; b &= b - 1) stage[q++] = (uint32_t)(k * MK_THREADS + threadIdx.x) * 32u + (uint32_t)(__ffs(b) - 1);
     }
     __syncthreads();
-    const u64 base = (u64)blockIdx.x * MK_WORDS * 32u;
     for (uint32_t r = threadIdx.x; r < tot; r += MK_THREADS) {
       const u64 bi = base + stage[r];
       if (nkey == 2) {
@@ -1605,36 +1615,40 @@ __global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_
 
 hipError_t bits_keys(uint32_t* bits, int64_t nbits, u64 row_bits, int32_t lo0, int32_t lo1, int nkey, bool clear,
                      uint32_t* c0, uint32_t* c1, uint32_t* total, void* temp, bool write, hipStream_t s) {
-  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  const int64_t nw = (nbits + 31) / 32;
+  const int wpt = mk_wpt(nw);
+  const int64_t nb = mk_blocks(nw, wpt);
   if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
   uint32_t* cnt = (uint32_t*)temp;
   uint32_t* off = cnt + ((nb + 63) & ~63ll);
   char* stemp = (char*)(off + ((nb + 63) & ~63ll));
   if (!write) {
-    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, cnt);
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, wpt, cnt);
     return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
   }
-  bits_keys_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, off, row_bits, lo0, lo1, nkey, clear, c0, c1);
+  bits_keys_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, wpt, off, row_bits, lo0, lo1, nkey, clear, c0, c1);
   return hipGetLastError();
 }
 
 size_t bits_list_temp_bytes(int64_t nbits) {
-  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  const int64_t nw = (nbits + 31) / 32, nb = mk_blocks(nw, mk_wpt(nw));
   return (size_t)((nb + 63) & ~63ll) * 8 + scan_temp_bytes(nb) + 256;
 }
 
 hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, void* temp, bool write,
                      hipStream_t s) {
-  const int64_t nw = (nbits + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  const int64_t nw = (nbits + 31) / 32;
+  const int wpt = mk_wpt(nw);
+  const int64_t nb = mk_blocks(nw, wpt);
   if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
   uint32_t* cnt = (uint32_t*)temp;
   uint32_t* off = cnt + ((nb + 63) & ~63ll);
   char* stemp = (char*)(off + ((nb + 63) & ~63ll));
   if (!write) {
-    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, cnt);
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, wpt, cnt);
     return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
   }
-  bits_list_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, off, list);
+  bits_list_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(bits, nw, wpt, off, list);
   return hipGetLastError();
 }
 
@@ -2035,16 +2049,16 @@ hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t
 // (rank-major, so grouped by rank and ascending in the second key), clearing
 // the bits.  Same word ranges and count pass as bits_keys; the write pass
 // stages each step's set bits in LDS so the row writes are coalesced.
-__global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, int64_t nw, const uint32_t* off,
+__global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, int64_t nw, int wpt, const uint32_t* off,
                                                                  uint32_t range1, const uint32_t* vals,
                                                                  const uint32_t* dict, int32_t lo1, int type,
                                                                  int fold_kind, uint32_t* k0, uint32_t* k1,
                                                                  uint32_t* v) {
   __shared__ uint32_t stage[MK_THREADS * 32];
   uint32_t p = off[blockIdx.x];
-  const u64 base = (u64)blockIdx.x * MK_WORDS * 32u;
-  for (int k = 0; k < MK_WPT; ++k) {
-    const int64_t wi = (int64_t)blockIdx.x * MK_WORDS + (int64_t)k * MK_THREADS + threadIdx.x;
+  const u64 base = (u64)blockIdx.x * MK_THREADS * wpt * 32u;
+  for (int k = 0; k < wpt; ++k) {
+    const int64_t wi = (int64_t)blockIdx.x * MK_THREADS * wpt + (int64_t)k * MK_THREADS + threadIdx.x;
     const uint32_t d = wi < nw ? chg[wi] : 0u;
     uint32_t tot;
     uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
@@ -2067,16 +2081,18 @@ __global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, 
 hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1, const uint32_t* vals, const uint32_t* dict,
                             int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
                             uint32_t* total, void* temp, bool write, hipStream_t s) {
-  const int64_t nw = (nslots + 31) / 32, nb = (nw + MK_WORDS - 1) / MK_WORDS;
+  const int64_t nw = (nslots + 31) / 32;
+  const int wpt = mk_wpt(nw);
+  const int64_t nb = mk_blocks(nw, wpt);
   if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
   uint32_t* cnt = (uint32_t*)temp;
   uint32_t* off = cnt + ((nb + 63) & ~63ll);
   char* stemp = (char*)(off + ((nb + 63) & ~63ll));
   if (!write) {
-    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, cnt);
+    bits_count_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, wpt, cnt);
     return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
   }
-  dense_delta_bits_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, off, range1, vals, dict, lo1, type, fold_kind, k0,
+  dense_delta_bits_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, wpt, off, range1, vals, dict, lo1, type, fold_kind, k0,
                                                          k1, v);
   return hipGetLastError();
 }
