@@ -1994,9 +1994,10 @@ struct Runner {
   }
 
   // Tile layout (as many slots as fit 128 KB of LDS, or fewer so that every
-  // CU gets a workgroup; a multiple of 32 slots) and e's rows
-  // sorted by (Z, tile of Y) with offsets per (Z, tile), so a tile's
-  // workgroup reads only the rows that land in it.
+  // CU gets a workgroup; a multiple of 32 slots) and e's rows sorted by
+  // (tile of Y, Z) with offsets per (tile, Z): a tile's workgroup reads only
+  // the rows that land in it, and one tile's rows of consecutive Z are
+  // consecutive.
   xl_status build_tile_index(const RulePlan& p, HeadRun* h) {
     const StepPlan& sp = p.steps[0];
     Relation* e = sp.rel;
@@ -2025,19 +2026,11 @@ struct Runner {
     }
     if (n > ((int64_t)1 << 30)) return c->fail(XL_UNSUPPORTED, "relation " + e->name + " too large to tile");
     // A loaded relation with Z in its first column and Y in its second is in
-    // (Z, Y) order, hence in (Z, tile) order when every Y lies in the head's
-    // domain (the tiles ascend with Y): only the offsets are built, and the
-    // index reads the relation's own columns.
-    if (!head_of(e) && e->sorted && zc == 0 && p.carried_ycol == 1 && e->types[1] == T_I32 &&
-        (int64_t)e->lo[1] >= h->kp.lo[1] && (int64_t)e->hi[1] - h->kp.lo[1] < h->range1) {
-      Buf keys;
-      XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
-      HIP_TRY(c, k::tile_keys(e->col[0], e->col[1], n, e->lo[0], h->kp.lo[1], h->tile, h->ntiles, keys.as<uint32_t>(),
-                              c->stream));
-      HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)nkeys, h->toff.as<uint32_t>(), c->stream));
-      for (int j = 0; j < e->arity; ++j) q.col[j] = e->col[j];
-      return XL_OK;
-    }
+    // (Z, Y) order, so a stable sort by the tile of Y alone puts it in
+    // (tile, Z) order when every Y lies in the head's domain; otherwise the
+    // rows are sorted by the whole (tile, Z) key.
+    const bool presorted = !head_of(e) && e->sorted && zc == 0 && p.carried_ycol == 1 && e->types[1] == T_I32 &&
+                           (int64_t)e->lo[1] >= h->kp.lo[1] && (int64_t)e->hi[1] - h->kp.lo[1] < h->range1;
     Buf keys, keys2, perm, perm2, tmp;
     XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
     XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
@@ -2045,11 +2038,12 @@ struct Runner {
     XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
     XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
     HIP_TRY(c, k::tile_keys(e->col[zc], e->col[p.carried_ycol], n, e->lo[zc], h->kp.lo[1], h->tile, h->ntiles,
-                            keys.as<uint32_t>(), c->stream));
+                            (uint32_t)zr, presorted, keys.as<uint32_t>(), c->stream));
     HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
     int alt = 0;
+    const int key_bits = presorted ? bitlen((uint64_t)h->ntiles) : bitlen((uint64_t)nkeys - 1);
     HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(), perm2.as<uint32_t>(),
-                                 n, std::max(1, bitlen((uint64_t)nkeys - 1)), tmp.p, c->stream, &alt));
+                                 n, std::max(1, key_bits), tmp.p, c->stream, &alt));
     uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
     uint32_t* spm = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
     for (int j = 0; j < e->arity; ++j) {
@@ -2058,6 +2052,9 @@ struct Runner {
       HIP_TRY(c, k::gather_u32(e->col[j], spm, h->tcols.back()->as<uint32_t>(), n, c->stream));
       q.col[j] = h->tcols.back()->as<uint32_t>();
     }
+    if (presorted)  // the whole keys of the rows in their new order
+      HIP_TRY(c, k::tile_keys(q.col[zc], q.col[p.carried_ycol], n, e->lo[zc], h->kp.lo[1], h->tile, h->ntiles,
+                              (uint32_t)zr, false, sk, c->stream));
     HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)nkeys, h->toff.as<uint32_t>(), c->stream));
     return XL_OK;
   }

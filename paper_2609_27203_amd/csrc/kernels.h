@@ -179,8 +179,10 @@ hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1,
                             int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
                             uint32_t* total, void* temp, bool write, hipStream_t s);
 size_t dense_tile_lds_bytes(uint32_t tile);
+// key[i] = tile * zr + (z - zlo), where tile = (y - lo1) / tile_slots capped
+// at ntiles (a Y outside the head's range); tile_only: key[i] = tile.
 hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
-                     uint32_t ntiles, uint32_t* key, hipStream_t s);
+                     uint32_t ntiles, uint32_t zr, bool tile_only, uint32_t* key, hipStream_t s);
 hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.

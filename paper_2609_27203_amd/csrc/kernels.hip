@@ -2134,7 +2134,7 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
         d1 = a.dval[j];
         const uint32_t kk = z - (uint32_t)a.idx.key_lo;
         if (kk < a.idx.key_range) {  // only the rows of z whose Y is in this tile
-          const u64 o = (u64)kk * (a.ntiles + 1) + t;
+          const u64 o = (u64)t * a.idx.key_range + kk;
           beg = a.toff[o];
           deg = a.toff[o + 1] - beg;
         }
@@ -2230,17 +2230,19 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
 
 // Composite sort key of e's rows for the tiled index: (z - zlo) * (ntiles + 1)
 // + the tile of y (ntiles for a y outside the head's second-key slots).
+// Key of an edge row in the tiled index: tile of Y (ntiles for a Y outside
+// the head's range) major, Z minor; or the tile alone (tile_only).
 __global__ void tile_keys_k(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1,
-                            uint32_t tile, uint32_t ntiles, uint32_t* key) {
+                            uint32_t tile, uint32_t ntiles, uint32_t zr, bool tile_only, uint32_t* key) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t tt = min((yc[i] - (uint32_t)lo1) / tile, ntiles);
-    key[i] = (zc[i] - (uint32_t)zlo) * (ntiles + 1) + tt;
+    key[i] = tile_only ? tt : tt * zr + (zc[i] - (uint32_t)zlo);
   }
 }
 hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
-                     uint32_t ntiles, uint32_t* key, hipStream_t s) {
+                     uint32_t ntiles, uint32_t zr, bool tile_only, uint32_t* key, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  tile_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(zc, yc, n, zlo, lo1, tile, ntiles, key);
+  tile_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(zc, yc, n, zlo, lo1, tile, ntiles, zr, tile_only, key);
   return hipGetLastError();
 }
 
