@@ -226,8 +226,8 @@ struct DenseTileArgs {
   uint32_t range1;        // slots per rank (a multiple of 32)
   int32_t lo1;
   uint32_t tile, ntiles;  // tile width (a multiple of 32) and tiles per rank
-  IndexProbe idx;         // e's columns grouped by (Z, tile of Y); act[] = the rule's actions on e
-  const uint32_t* toff;   // [(z - idx.key_lo) * (ntiles + 1) + t]: first row of Z value z in tile t
+  IndexProbe idx;         // e's columns grouped by (tile of Y, Z); act[] = the rule's actions on e
+  const uint32_t* toff;   // [t * idx.key_range + (z - idx.key_lo)]: first row of Z value z in tile t
   int32_t ycol;           // column of e bound to Y
   int8_t slot_s, slot_z, slot_p, slot_y, val_slot;
   uint8_t val_type, is_max;
