@@ -2088,23 +2088,17 @@ struct Runner {
     return XL_OK;
   }
 
-  // Delta rows of a tiled head from its delta bits, grouped by rank (row
-  // counts per rank, their scan into roff, count and write passes); the row
-  // total goes to *total on the device.
-  xl_status tile_delta_rows(HeadRun* h, uint32_t* total, Buf* cnt, Buf* tmp, Buf* ltmp) {
-    const uint32_t wpr = (uint32_t)(h->range1 / 32);
+  // Delta rows of a tiled head from its delta bits, grouped by rank (count
+  // and write passes; the write pass also fills roff); the row total goes to
+  // *total on the device.
+  xl_status tile_delta_rows(HeadRun* h, uint32_t* total, Buf* ltmp) {
     const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
-    HIP_TRY(c, k::row_popcount(h->dchg.as<uint32_t>(), h->n0, wpr, cnt->as<uint32_t>(), c->stream));
-    HIP_TRY(c, k::scan_exclusive_u32(cnt->as<uint32_t>(), h->roff.as<uint32_t>(), h->n0,
-                                     h->roff.as<uint32_t>() + h->n0, tmp->p, c->stream));
-    HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
-                                        h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
-                                        h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
-                                        total, ltmp->p, false, c->stream));
-    HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
-                                        h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
-                                        h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
-                                        total, ltmp->p, true, c->stream));
+    for (bool write : {false, true})
+      HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
+                                          h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
+                                          h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(),
+                                          h->drow[2].as<uint32_t>(), h->n0 > 0 ? h->roff.as<uint32_t>() : nullptr,
+                                          total, ltmp->p, write, c->stream));
     return XL_OK;
   }
 
@@ -2142,11 +2136,9 @@ struct Runner {
     DenseTileArgs a{};
     XL_TRY(tile_args(p, h, a));
     const int B = c->batched_rounds;
-    Buf acc, rounds, cnt, tmp, ltmp;
+    Buf acc, rounds, ltmp;
     XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
     XL_TRY(dalloc(c, (size_t)B * 4, &rounds, "round delta sizes"));
-    XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->n0, 1) * 4, &cnt, "delta rows per rank"));
-    XL_TRY(dalloc(c, k::scan_temp_bytes(h->n0), &tmp, "scan scratch"));
     XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &ltmp, "compaction scratch"));
     HIP_TRY(c, hipMemsetAsync(acc.p, 0, 8 * CNT_N, c->stream));
     a.counters = acc.as<unsigned long long>();
@@ -2173,7 +2165,7 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
         HIP_TRY(c, k::dense_min_tiles(a, c->stream));
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
-        XL_TRY(tile_delta_rows(h, rounds.as<uint32_t>() + r, &cnt, &tmp, &ltmp));
+        XL_TRY(tile_delta_rows(h, rounds.as<uint32_t>() + r, &ltmp));
       }
       std::vector<uint32_t> n(nb);
       XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));
@@ -2614,14 +2606,7 @@ struct Runner {
       *delta = h->dn;
       return XL_OK;
     }
-    if (h->tiled) {  // delta rows from the delta bits, grouped by rank
-      const uint32_t wpr = (uint32_t)(h->range1 / 32);
-      Buf cnt, tmp;
-      XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->n0, 1) * 4, &cnt, "delta rows per rank"));
-      XL_TRY(dalloc(c, k::scan_temp_bytes(h->n0), &tmp, "scan scratch"));
-      HIP_TRY(c, k::row_popcount(h->dchg.as<uint32_t>(), h->n0, wpr, cnt.as<uint32_t>(), c->stream));
-      HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), h->roff.as<uint32_t>(), h->n0,
-                                       h->roff.as<uint32_t>() + h->n0, tmp.p, c->stream));
+    if (h->tiled) {  // delta rows from the delta bits, grouped by rank (the write pass fills roff)
       const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
       Buf ltmp, tot;
       XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &ltmp, "compaction scratch"));
@@ -2630,7 +2615,8 @@ struct Runner {
         return k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
                                    h->dict.as<uint32_t>(), h->kp.lo[1], h->rel->types[h->nkey], h->fold,
                                    h->drow[0].as<uint32_t>(), h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(),
-                                   tot.as<uint32_t>(), ltmp.p, write, c->stream);
+                                   h->n0 > 0 ? h->roff.as<uint32_t>() : nullptr, tot.as<uint32_t>(), ltmp.p, write,
+                                   c->stream);
       };
       HIP_TRY(c, rows(false));
       uint32_t n = 0;

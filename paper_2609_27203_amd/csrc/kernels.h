@@ -174,10 +174,12 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
 // Dense min/max heads, tiled rounds (see DenseTileArgs).
 // Delta rows from the delta bits in slot order (two calls on the same temp,
 // sized by bits_list_temp_bytes: write=false counts, write=true writes the
-// rows and clears the bits).
+// rows and clears the bits).  roff (optional, [nslots / range1 + 1], range1 a
+// multiple of 32): the write pass also stores each rank's first row and the
+// row total.
 hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1, const uint32_t* vals, const uint32_t* dict,
                             int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
-                            uint32_t* total, void* temp, bool write, hipStream_t s);
+                            uint32_t* roff, uint32_t* total, void* temp, bool write, hipStream_t s);
 size_t dense_tile_lds_bytes(uint32_t tile);
 // key[i] = tile * zr + (z - zlo), where tile = (y - lo1) / tile_slots capped
 // at ntiles (a Y outside the head's range); tile_only: key[i] = tile.

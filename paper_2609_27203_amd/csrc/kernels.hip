@@ -2048,12 +2048,14 @@ hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t
 // Delta rows of a dense min/max head from its delta bits, in slot order
 // (rank-major, so grouped by rank and ascending in the second key), clearing
 // the bits.  Same word ranges and count pass as bits_keys; the write pass
-// stages each step's set bits in LDS so the row writes are coalesced.
+// stages each step's set bits in LDS so the row writes are coalesced.  With
+// roff, it also writes each rank's first row (the rows before the rank's
+// first word of wpr words) and, after the last rank, the row total.
 __global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, int64_t nw, int wpt, const uint32_t* off,
                                                                  uint32_t range1, const uint32_t* vals,
                                                                  const uint32_t* dict, int32_t lo1, int type,
                                                                  int fold_kind, uint32_t* k0, uint32_t* k1,
-                                                                 uint32_t* v) {
+                                                                 uint32_t* v, uint32_t* roff, uint32_t wpr) {
   __shared__ uint32_t stage[MK_THREADS * 32];
   uint32_t p = off[blockIdx.x];
   const u64 base = (u64)blockIdx.x * MK_THREADS * wpt * 32u;
@@ -2062,6 +2064,7 @@ __global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, 
     const uint32_t d = wi < nw ? chg[wi] : 0u;
     uint32_t tot;
     uint32_t q = block_excl_scan<uint32_t>((uint32_t)__popc(d), &tot);
+    if (roff && wi < nw && (uint32_t)wi % wpr == 0u) roff[(uint32_t)wi / wpr] = p + q;
     if (d) {
       chg[wi] = 0u;
       for (uint32_t b = d; b; b &= b - 1)
@@ -2077,11 +2080,14 @@ __global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, 
     p += tot;
     __syncthreads();
   }
+  if (roff && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) roff[(uint32_t)(nw / wpr)] = p;
 }
 hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1, const uint32_t* vals, const uint32_t* dict,
                             int32_t lo1, int type, int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v,
-                            uint32_t* total, void* temp, bool write, hipStream_t s) {
+                            uint32_t* roff, uint32_t* total, void* temp, bool write, hipStream_t s) {
   const int64_t nw = (nslots + 31) / 32;
+  const uint32_t wpr = range1 / 32;
+  if (roff && (range1 % 32 != 0 || wpr == 0)) return hipErrorInvalidValue;
   const int wpt = mk_wpt(nw);
   const int64_t nb = mk_blocks(nw, wpt);
   if (nb == 0) return hipMemsetAsync(total, 0, 4, s);
@@ -2093,7 +2099,7 @@ hipError_t dense_delta_from_bits(uint32_t* chg, int64_t nslots, uint32_t range1,
     return scan_exclusive_u32(cnt, off, nb, total, stemp, s);
   }
   dense_delta_bits_k<<<(unsigned)nb, MK_THREADS, 0, s>>>(chg, nw, wpt, off, range1, vals, dict, lo1, type, fold_kind, k0,
-                                                         k1, v);
+                                                         k1, v, roff, wpr);
   return hipGetLastError();
 }
 
