@@ -397,6 +397,44 @@ def test_min_rounds_tiled_and_untiled(tiles, batch):
         assert stats["iterations"] == base["iterations"]
 
 
+TILED_FORMS = {
+    # Z in the edge relation's second column: the tiled index sorts the rows
+    # by the whole (tile of Y, Z) key
+    "swapped": ("dist(S,S,min(D)) :- source(S), D is 0.0.\n"
+                "dist(S,Y,min(D)) :- dist(S,Z,D1), redge(Y,Z,W), D is D1 + W.", "redge", (1, 0, 2)),
+    # a derived edge relation (a min head, not stored in sorted order)
+    "derived": ("e2(Z,Y,min(W)) :- edge(Z,Y,W).\ndist(S,S,min(D)) :- source(S), D is 0.0.\n"
+                "dist(S,Y,min(D)) :- dist(S,Z,D1), e2(Z,Y,W), D is D1 + W.", "edge", (0, 1, 2)),
+}
+
+
+@pytest.mark.parametrize("tiles", [0, 1, 7])
+@pytest.mark.parametrize("form", list(TILED_FORMS))
+def test_min_rounds_tiled_index_built_by_sort(form, tiles):
+    """The tiled min rounds over an edge relation whose rows are not already
+    in (Z, Y) order (Z in the second column, or a derived relation) build
+    their (tile of Y, Z) index with a full key sort; they match the oracle bit
+    for bit and the untiled emission's per-round delta sizes."""
+    base_wl = W.small_workloads()["sssp"]()
+    rules, name, perm = TILED_FORMS[form]
+    types, cols = base_wl.edb["edge"]
+    edb = {"source": base_wl.edb["source"],
+           name: (tuple(types[k] for k in perm), [cols[k] for k in perm])}
+    idb = {"dist": base_wl.idb["dist"]}
+    if form == "derived":
+        idb["e2"] = types
+    wl = W.Workload(f"tiled_{form}", rules, edb, idb)
+    print(f"case: tiled index by sort form={form} tiles={tiles}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"dense_tiles": tiles})
+    assert_same_relation("dist", idb["dist"], rels["dist"], ref.relations["dist"][1], tol=(0.0, 0.0))
+    base = engine_run(wl, options={"dense_tiles": -1, "batched_rounds": 0})[1]
+    assert stats["iterations"] == base["iterations"]
+    # the tiled rounds read their own (tile, Z) index; the untiled emission
+    # builds an ordinary index of the edge relation
+    assert stats["index_builds"] < base["index_builds"]
+
+
 @pytest.mark.parametrize("batch", [0, 4])
 def test_min_rounds_iteration_cap(batch):
     """A cap below the pass count is a convergence failure in both forms; the
