@@ -29,12 +29,15 @@ What it computes (the plain definition the semi-naive method reaches):
   connected components of the predicate dependency graph) run in dependency
   order (Sec. 2.4 and Sec. 4.1).  For set heads the result is the least
   fixpoint that Algorithm 1 (semi-naive evaluation) also reaches.
-* Precision: every f32-typed result (``is`` arithmetic and aggregate folds) is
-  computed in float64 and rounded once to float32, i.e. the declared IEEE type.
-  For a sum of two binary32 values this equals the binary32 operation exactly,
-  because binary64 has more than twice the precision plus two bits.
-  logsumexp uses the max-shifted form m + log(sum(exp(x - m))) in float64;
-  a group whose values are all -inf folds to -inf.
+* Precision: ``is`` arithmetic keeps the operands' scalar type (Sec. 3.2), so
+  an expression is evaluated left to right and every add or subtract of f32
+  values is one binary32 operation (computed in float64 and rounded once to
+  float32, which equals the binary32 operation exactly because binary64 has
+  more than twice the precision plus two bits); i32 arithmetic wraps modulo
+  2^32.  Aggregate folds over f32 values (sum) are taken in float64 and
+  rounded once to float32: the exact sum, correctly rounded.  logsumexp uses
+  the max-shifted form m + log(sum(exp(x - m))) in float64; a group whose
+  values are all -inf folds to -inf.
 
 * Stratified negation (Sec. 3, completeness over finite domains: explicit
   stratified negation-as-failure; Sec. 2, program to GPU plan: negative
@@ -365,12 +368,26 @@ def _eval_body(rule, rels, var_types):
         ty = ptypes.pop()
         if ty not in ("i32", "f32"):
             raise TypeError(f"arithmetic on {ty} values is not supported")
-        acc = np.zeros(n, np.float64 if ty == "f32" else np.int64)
+        # Left to right, one operation at a time, each result a value of the
+        # operands' type (Sec. 3.2: arithmetic keeps scalar types): an f32
+        # add or subtract is done in float64 and rounded to float32 at once,
+        # which is the binary32 operation itself; i32 wraps modulo 2^32.  A
+        # leading minus is 0 - x.
+        wide = np.float64 if ty == "f32" else np.int64
+        acc = None
         for sign, v in vals:
-            acc = acc + sign * np.asarray(v, acc.dtype)
+            t = np.broadcast_to(np.asarray(v, wide), (n,))
+            if acc is None:
+                acc = t.copy() if sign > 0 else np.zeros(n, wide) - t
+            else:
+                acc = acc + t if sign > 0 else acc - t
+            if ty == "f32":
+                acc = acc.astype(np.float32).astype(np.float64)
+            else:
+                acc = (acc + 2 ** 31) % 2 ** 32 - 2 ** 31
         if var_types.setdefault(var, ty) != ty:
             raise TypeError(f"variable {var} used at two types")
-        binding[var] = acc.astype(np.float32) if ty == "f32" else acc.astype(np.int64).astype(np.int32)
+        binding[var] = acc.astype(np.float32) if ty == "f32" else acc.astype(np.int32)
     mask = np.ones(n, bool)
     for pred, terms in rule.negs:
         mask &= ~_negated_match(pred, terms, rels, binding, var_types, n)

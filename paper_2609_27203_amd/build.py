@@ -12,6 +12,7 @@ import os
 import shutil
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
@@ -61,7 +62,7 @@ def build(force: bool = False, verbose: bool = False) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
     hdr = _newest_header()
-    objs = []
+    objs, cmds = [], []
     for src in SOURCES:
         s = os.path.join(CSRC, src)
         o = os.path.join(BUILD, src + ".o")
@@ -69,10 +70,18 @@ def build(force: bool = False, verbose: bool = False) -> str:
         if not force and os.path.exists(o) and os.path.getmtime(o) >= max(os.path.getmtime(s), hdr):
             continue
         lang = [] if src.endswith(".hip") else ["-x", "hip"]
-        cmd = [hipcc, *COMMON, *lang, "-c", s, "-o", o]
+        cmds.append([hipcc, *COMMON, *lang, "-c", s, "-o", o])
+    # the sources compile independently: one hipcc per source, in parallel
+    jobs = max(1, min(len(cmds), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+
+    def compile_one(cmd):
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)
+
+    if cmds:
+        with ThreadPoolExecutor(jobs) as ex:
+            list(ex.map(compile_one, cmds))
     # Link with the host linker against the exact HIP runtime PyTorch loads, so
     # the process holds one runtime and torch's streams and allocations are
     # valid in the library (hipcc would add /opt/rocm's runtime instead).

@@ -8,7 +8,7 @@ import os
 import numpy as np
 import pytest
 
-from helpers import assert_same_relation, engine_run, select_rows, value_tolerance
+from helpers import LSE_TOL, assert_same_relation, engine_run, select_rows, value_tolerance
 from oracle import evaluate
 from paper_2609_27203_amd import workloads as W
 
@@ -375,6 +375,64 @@ def test_sum_and_logsumexp_heads_dense_and_hashed(name, index_mode):
     ref = evaluate(wl.rules, wl.edb, wl.idb)
     rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
     _compare(wl, rels, ref)
+    assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
+
+
+SUBTRACT_RULES = {
+    # min over D1 - W: f32 weights are log-probabilities (<= 0), so every
+    # step adds -W >= 0; tiled min rounds with the one-subtract form
+    "min_f32": ("""
+low(S,S,min(D)) :- source(S), D is 0.0.
+low(S,Y,min(D)) :- low(S,Z,D1), edge(Z,Y,W), D is D1 - W.
+""", {"low": ("i32", "i32", "f32")}),
+    # max over D1 - K on integer weights: the negated shortest path
+    "max_i32": ("""
+high(S,S,max(D)) :- source(S), D is 0.
+high(S,Y,max(D)) :- high(S,Z,D1), iedge(Z,Y,K), D is D1 - K.
+""", {"high": ("i32", "i32", "i32")}),
+    # sum over derivations of C1 - K (the dense pull's one-subtract form)
+    "sum_i32": ("""
+ws(S,Y,sum(C)) :- source(S), iedge(S,Y,K), C is 0 - K.
+ws(S,Y,sum(C)) :- ws(S,Z,C1), iedge(Z,Y,K), C is C1 - K.
+""", {"ws": ("i32", "i32", "i32")}),
+    # logsumexp of P1 - W
+    "lse_f32": ("""
+score(S,Y,logsumexp(P)) :- source(S), edge(S,Y,P).
+score(S,Y,logsumexp(P)) :- score(S,Z,P1), edge(Z,Y,W), P is P1 - W - 1.0.
+""", {"score": ("i32", "i32", "f32")}),
+    # set heads through subtraction: an id shifted back one layer, its closure,
+    # and three-term arithmetic with a comparison on the result
+    "set_i32": ("""
+hop(X,Y) :- edge(X,Z,_), Y is Z - 300.
+back(X,Y) :- hop(X,Y).
+back(X,Y) :- back(X,Z), hop(Z,Y).
+mix(X,V) :- iedge(X,Y,K), V is Y - X - K + 7, V > 290.
+""", {"hop": ("i32", "i32"), "back": ("i32", "i32"), "mix": ("i32", "i32")}),
+}
+
+
+@pytest.mark.parametrize("index_mode", [0, 1])
+@pytest.mark.parametrize("name", list(SUBTRACT_RULES))
+def test_subtraction_rules_match_oracle(name, index_mode):
+    """Rules whose arithmetic subtracts, through every value-head form (tiled
+    min rounds, the dense pull, hashed folds, the stage kernel's one-op and
+    general forms); integer and min/max results bit for bit, logsumexp
+    within its tolerance."""
+    rules, idb = SUBTRACT_RULES[name]
+    base = W.small_workloads()["lse_dag"]()
+    src, dst, w = base.edb["edge"][1]
+    edb = dict(base.edb)
+    edb["iedge"] = (("i32", "i32", "i32"), [src, dst, ((src * 7 + dst * 3) % 9 + 1).astype(np.int32)])
+    used = {k: v for k, v in edb.items() if k + "(" in rules}
+    wl = W.Workload(f"subtract_{name}", rules, used, idb)
+    print(f"case: subtraction {name} index_mode={index_mode}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"index_mode": index_mode})
+    for rel, types in wl.idb.items():
+        tol = value_tolerance(wl.rules, rel)
+        assert_same_relation(rel, types, rels[rel], ref.relations[rel][1],
+                             tol=tol if tol[0] == LSE_TOL else (0.0, 0.0))
+        assert len(rels[rel][0]) > 0, rel
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
