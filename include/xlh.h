@@ -169,6 +169,32 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace,
                             size_t workspace_bytes, xl_context** out);
 
 /*
+ * Allocation-free variant of xl_context_create, for callers that cannot
+ * allocate memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The context sub-allocates from the
+ * library's static device array of XL_STATIC_WORKSPACE_BYTES (64 MiB) on
+ * `device` instead of a caller workspace, and keeps its control block in host
+ * memory inside the handle instead of a pinned allocation; every GPU the
+ * library runs on holds that array until the process ends.  Neither this
+ * call nor any later call on the context calls hipMalloc, hipHostMalloc,
+ * hipFree or another allocating routine (xl_fixpoint_run still creates two
+ * HIP events per run, and four more with option "profile").  Work that does
+ * not fit the array fails with XL_RESOURCE_EXHAUSTED and a message naming
+ * the bytes asked for and the limit, as a too small workspace does.
+ * The array is shared by every call on the device and keeps the last call's
+ * contents (the library clears what must start at zero before each use), so
+ * one such context may exist per device at a time: another
+ * xl_context_create_static on that device returns XL_RESOURCE_EXHAUSTED until
+ * the first is destroyed.  Calls on the context from several threads race,
+ * as on any context.  XL_INVALID_ARGUMENT for a null `out` or a device
+ * outside [0, 64); XL_DEVICE_ERROR if the device cannot be selected or the
+ * array's device address cannot be taken.  No message is recorded for a
+ * failed create (there is no context to hold it).
+ */
+#define XL_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+xl_status xl_context_create_static(int device, void* hip_stream, xl_context** out);
+
+/*
  * Tunables (key, value):
  *   "hash_min_log2"   log2 of the smallest hash table (default 22)
  *   "index_mode"      0 = automatic, 1 = always open-addressing hash tables,

@@ -1,18 +1,35 @@
 // extern "C" entry points declared in include/xlh.h.
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "engine.h"
 
 using namespace xlh;
 
-struct xl_context : Context {};
+namespace {
+constexpr size_t PINNED_BYTES = 4096;
+constexpr int STATIC_MAX_DEVICES = 64;
+}  // namespace
+
+struct xl_context : Context {
+  bool static_ws = false;  // the arena is the device's static workspace (xl_context_create_static)
+  alignas(64) unsigned char ctl[PINNED_BYTES];  // control block of a static context (no pinned allocation)
+};
 struct xl_relation : Relation {};
 struct xl_program : Program {};
 
+// Workspace of the allocation-free contexts: one copy per device the library
+// runs on, held until the process ends.  In host code `scratch` names a host
+// stand-in, never the device memory: its device address on each device comes
+// from hipGetSymbolAddress (with that device current) and is kept below.
+static __device__ __align__(256) unsigned char scratch[XL_STATIC_WORKSPACE_BYTES];
+
 namespace {
-constexpr size_t PINNED_BYTES = 4096;
-}
+std::mutex g_static_mu;
+void* g_static_ptr[STATIC_MAX_DEVICES] = {};  // device address of `scratch`, per device
+bool g_static_held[STATIC_MAX_DEVICES] = {};  // a live static context uses that device's copy
+}  // namespace
 
 extern "C" {
 
@@ -53,6 +70,28 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace, size_
     }
     c->dcounters = (unsigned long long*)c->arena.alloc(8 * CNT_N);
   }
+  *out = c;
+  return XL_OK;
+}
+
+xl_status xl_context_create_static(int device, void* hip_stream, xl_context** out) {
+  if (!out || device < 0 || device >= STATIC_MAX_DEVICES) return XL_INVALID_ARGUMENT;
+  if (hipSetDevice(device) != hipSuccess) return XL_DEVICE_ERROR;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_held[device]) return XL_RESOURCE_EXHAUSTED;
+  if (!g_static_ptr[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return XL_DEVICE_ERROR;
+    g_static_ptr[device] = p;
+  }
+  auto* c = new xl_context();
+  c->device = device;
+  c->stream = (hipStream_t)hip_stream;
+  c->static_ws = true;
+  c->pinned = c->ctl;
+  c->arena.init((char*)g_static_ptr[device], XL_STATIC_WORKSPACE_BYTES);
+  c->dcounters = (unsigned long long*)c->arena.alloc(8 * CNT_N);
+  g_static_held[device] = true;
   *out = c;
   return XL_OK;
 }
@@ -226,7 +265,12 @@ void xl_context_destroy(xl_context* c) {
   if (c->device >= 0 && c->stream) (void)hipStreamSynchronize(c->stream);
   for (Program* p : c->progs) delete static_cast<xl_program*>(p);
   for (Relation* r : c->rels) delete static_cast<xl_relation*>(r);
-  if (c->pinned) (void)hipHostFree(c->pinned);
+  if (c->static_ws) {
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    g_static_held[c->device] = false;
+  } else if (c->pinned) {
+    (void)hipHostFree(c->pinned);
+  }
   delete c;
 }
 

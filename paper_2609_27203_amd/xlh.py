@@ -83,7 +83,7 @@ class xl_fixpoint_stats(C.Structure):
 
 
 _lib = None
-EXPORTS = ["xl_context_create", "xl_context_set_option", "xl_relation_create", "xl_relation_load",
+EXPORTS = ["xl_context_create", "xl_context_create_static", "xl_context_set_option", "xl_relation_create", "xl_relation_load",
            "xl_relation_clear", "xl_relation_size", "xl_relation_read", "xl_rule_compile",
            "xl_program_explain", "xl_fixpoint_run", "xl_last_error", "xl_status_string",
            "xl_program_destroy", "xl_relation_destroy", "xl_context_destroy"]
@@ -100,6 +100,7 @@ def lib() -> C.CDLL:
     L = C.CDLL(LIB_PATH)
     vp, i64, i32 = C.c_void_p, C.c_int64, C.c_int
     L.xl_context_create.argtypes = [i32, vp, vp, C.c_size_t, C.POINTER(vp)]
+    L.xl_context_create_static.argtypes = [i32, vp, C.POINTER(vp)]
     L.xl_context_set_option.argtypes = [vp, C.c_char_p, i64]
     L.xl_relation_create.argtypes = [vp, C.c_char_p, i32, C.POINTER(C.c_int), i64, C.POINTER(vp)]
     L.xl_relation_load.argtypes = [vp, C.POINTER(vp), i64, i32]
@@ -126,13 +127,24 @@ def lib() -> C.CDLL:
 class Context:
     """xl_context over a torch-allocated workspace on one device (or planning-only)."""
 
-    def __init__(self, device: int = 0, workspace_bytes: int = 1 << 30, stream=None):
+    def __init__(self, device: int = 0, workspace_bytes: int = 1 << 30, stream=None,
+                 static: bool = False):
+        """static=True: xl_context_create_static (the library's static 64 MiB
+        device workspace, no allocation by the library or here)."""
         L = lib()
         self._h = C.c_void_p()
         self.device = device
         self.workspace = None
         self.stream = None
-        if device >= 0:
+        if static:
+            import torch
+            if not torch.cuda.is_available():
+                raise RuntimeError("no GPU visible: the engine runs only on the device")
+            self.stream = stream if stream is not None else torch.cuda.current_stream(device)
+            st = L.xl_context_create_static(device, C.c_void_p(self.stream.cuda_stream), C.byref(self._h))
+            if st != XL_OK:
+                raise XlError(st, "xl_context_create_static failed")
+        elif device >= 0:
             import torch
             if not torch.cuda.is_available():
                 raise RuntimeError("no GPU visible: the engine runs only on the device")
