@@ -1,0 +1,127 @@
+"""Full-size parity: every row of the five full-size workloads, in the
+launch configuration the benchmark times (default options, index mode 0).
+
+Each result is decided twice, by independent routes:
+* a certificate from a textbook routine computed here on the CPU
+  (tests/certificates.py): breadth-first search from every node for the
+  closures (rows, counts and per-pass delta sizes), the binary32 Bellman
+  equations for shortest paths, the float64 forward pass for logsumexp, the
+  closed form for same generation;
+* the CPU oracle's own full-size output, as SHA-256 digests written by
+  tests/golden/make_full_digests.py (which calls only the oracle), compared
+  with the digest of the engine's rows -- bit for bit; logsumexp values are
+  not bit-exact, so there the oracle evaluates 32 sampled sources here.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import certificates as CERT
+from helpers import LSE_TOL, assert_same_relation, engine_run, select_rows
+from oracle import evaluate
+from paper_2609_27203_amd import workloads as W
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
+DIGESTS = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "full_digests.json")))
+
+_RUNS = {}
+
+
+def _full(name, workspace_gb):
+    """The engine's full-size result (one run per workload and session)."""
+    if name not in _RUNS:
+        wl = W.full_workloads()[name]()
+        print(f"case: full {name} {wl.digest()[:12]}", flush=True)
+        rels, stats, ctx = engine_run(wl, workspace_bytes=workspace_gb << 30)
+        ctx.close()
+        _RUNS[name] = (wl, rels, stats)
+    return _RUNS[name]
+
+
+def _check_digest(name, wl, rels):
+    rec = DIGESTS[name]
+    assert rec["inputs_sha256"] == wl.digest(), f"{name}: inputs differ from the ones the digests were made for"
+    for rel, exp in rec["relations"].items():
+        assert len(rels[rel][0]) == exp["rows"], f"{rel}: {len(rels[rel][0])} rows, oracle {exp['rows']}"
+        assert CERT.row_digest(rels[rel]) == exp["sha256"], f"{rel}: rows differ from the oracle's"
+
+
+def _levels(sizes):
+    return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
+
+
+def test_full_tc_uniform_every_row():
+    wl, rels, stats = _full("tc_uniform", 4)
+    src, dst = wl.edb["edge"][1]
+    n = wl.params["n_nodes"]
+    reached, levels = CERT.closure_bits(n, src, dst)
+    CERT.check_closure_rows(CERT.reached_matrix(reached, n), *rels["path"])
+    assert stats["delta_rows"] == levels and stats["iterations"] == len(levels) - 1
+    _check_digest("tc_uniform", wl, rels)
+    assert _levels(DIGESTS["tc_uniform"]["path_sizes"]) == levels
+
+
+def test_full_tc_rmat_count_every_row():
+    """The headline workload: all 128.9 M closure rows, all reach counts,
+    the per-pass delta sizes and the derived-tuple count the benchmark
+    reports."""
+    wl, rels, stats = _full("tc_rmat_count", 32)
+    src, dst = wl.edb["edge"][1]
+    n = 1 << wl.params["scale"]
+    reached, levels = CERT.closure_bits(n, src, dst)
+    m = CERT.reached_matrix(reached, n)
+    CERT.check_closure_rows(m, *rels["path"])
+    cnt = m.sum(axis=1)
+    rc = rels["reach_count"]
+    assert np.array_equal(rc[0], np.flatnonzero(cnt)) and np.array_equal(rc[1], cnt[cnt > 0])
+    assert stats["delta_rows"] == levels and stats["iterations"] == len(levels) - 1
+    assert stats["derived_tuples"] == int(cnt.sum()) + int((cnt > 0).sum())
+    _check_digest("tc_rmat_count", wl, rels)
+    assert _levels(DIGESTS["tc_rmat_count"]["path_sizes"]) == levels
+
+
+def test_full_sssp_every_row():
+    """All 64 sources, bit for bit: the binary32 Bellman equations hold for
+    every node, and the rows' digest is the oracle's."""
+    wl, rels, _ = _full("sssp", 8)
+    src, dst, w = wl.edb["edge"][1]
+    sources = np.sort(wl.edb["source"][1][0])
+    CERT.bellman_check(wl.params["n_nodes"], src, dst, w, sources, *rels["dist"])
+    _check_digest("sssp", wl, rels)
+
+
+def test_full_lse_every_row_forward_pass():
+    """All 256 sources: every row within 1e-5 * max(1, |ref|) of the float64
+    forward pass, and exactly the (source, node) pairs joined by a path."""
+    wl, rels, _ = _full("lse_dag", 8)
+    src, dst, w = wl.edb["edge"][1]
+    L, K = wl.params["n_layers"], wl.params["width"]
+    sources = np.sort(wl.edb["source"][1][0])
+    total = CERT.forward_scores(L * K, src, dst, w, sources, L)
+    worst = CERT.check_scores(total, sources, *rels["score"], tol=LSE_TOL)
+    print(f"lse worst error / max(1, |ref|): {worst:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("part", [0, 1])
+def test_full_lse_oracle_sampled_sources(part):
+    """32 sources (two halves of 16) recomputed by the oracle, row by row."""
+    wl, rels, _ = _full("lse_dag", 8)
+    sources = wl.edb["source"][1][0]
+    pick = np.sort(np.random.default_rng(3).choice(sources, 32, replace=False))[part::2]
+    sub = dict(wl.edb)
+    sub["source"] = (("i32",), [pick.astype(np.int32)])
+    ref = evaluate(wl.rules, sub, wl.idb)
+    assert_same_relation("score", wl.idb["score"], select_rows(rels["score"], 0, pick),
+                         ref.relations["score"][1], " (oracle-sampled sources)", tol=(LSE_TOL, 1.0))
+
+
+def test_full_same_generation_every_row():
+    wl, rels, stats = _full("same_generation", 8)
+    x, y = rels["sg"]
+    n = len(wl.params["depth"])
+    keys = CERT.same_generation_keys(wl.edb["parent"][1][0], wl.params["depth"], wl.params["root"], n)
+    assert np.array_equal(x.astype(np.int64) * n + y, keys)
+    assert stats["derived_tuples"] == len(keys)
+    _check_digest("same_generation", wl, rels)

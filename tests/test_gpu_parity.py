@@ -8,7 +8,7 @@ import os
 import numpy as np
 import pytest
 
-from helpers import LSE_TOL, assert_same_relation, engine_run, select_rows, value_tolerance
+from helpers import LSE_TOL, assert_same_relation, engine_run, value_tolerance
 from oracle import evaluate
 from paper_2609_27203_amd import workloads as W
 
@@ -602,87 +602,6 @@ def test_tc_delta_sizes_are_walk_levels():
     levels = [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
     assert stats["delta_rows"] == levels
     assert stats["iterations"] == len(levels) - 1
-
-
-# ------------------------------------------------------------- full-size workloads
-def test_full_tc_uniform_every_row():
-    wl = W.tc_uniform()
-    print("case: full tc_uniform", flush=True)
-    ref = evaluate(wl.rules, wl.edb, wl.idb)
-    rels, _, _ = engine_run(wl, workspace_bytes=4 << 30)
-    _compare(wl, rels, ref)
-
-
-def test_full_sssp_sampled_sources():
-    wl = W.sssp()
-    print("case: full sssp", flush=True)
-    rels, stats, _ = engine_run(wl, workspace_bytes=8 << 30)
-    sources = wl.edb["source"][1][0]
-    pick = sources[[0, 31, 63]]
-    sub = dict(wl.edb)
-    sub["source"] = (("i32",), [pick])
-    ref = evaluate(wl.rules, sub, wl.idb)
-    got = select_rows(rels["dist"], 0, pick)
-    assert_same_relation("dist", wl.idb["dist"], got, ref.relations["dist"][1], " (sampled sources)")
-    # every source reaches every node it can reach; total rows bounded by 64 * n
-    assert len(rels["dist"][0]) <= 64 * wl.params["n_nodes"]
-    assert set(np.unique(rels["dist"][0]).tolist()) == set(sources.tolist())
-
-
-def test_full_lse_sampled_sources():
-    wl = W.layered_dag()
-    print("case: full lse_dag", flush=True)
-    rels, _, _ = engine_run(wl, workspace_bytes=8 << 30)
-    pick = wl.edb["source"][1][0][[0, 200]]
-    sub = dict(wl.edb)
-    sub["source"] = (("i32",), [pick])
-    ref = evaluate(wl.rules, sub, wl.idb)
-    got = select_rows(rels["score"], 0, pick)
-    assert_same_relation("score", wl.idb["score"], got, ref.relations["score"][1], " (sampled sources)",
-                         tol=value_tolerance(wl.rules, "score"))
-
-
-def test_full_same_generation_sampled_and_closed_form():
-    wl = W.same_generation()
-    print("case: full same_generation", flush=True)
-    rels, _, _ = engine_run(wl, workspace_bytes=8 << 30)
-    child, par = wl.edb["parent"][1]
-    depth, root = wl.params["depth"], wl.params["root"]
-    # closed form: |sg| = sum over (tree, depth) groups of n (n - 1) among non-roots
-    has_parent = np.zeros(len(depth), bool)
-    has_parent[child] = True
-    key = root[has_parent].astype(np.int64) * 64 + depth[has_parent]
-    _, cnt = np.unique(key, return_counts=True)
-    assert len(rels["sg"][0]) == int((cnt.astype(np.int64) * (cnt - 1)).sum())
-    # sampled rows: the restriction set must be closed under parent
-    parent_of = dict(zip(child.tolist(), par.tolist()))
-    rng = np.random.default_rng(0)
-    sample = set()
-    for x in rng.choice(child, 6, replace=False).tolist():
-        while x in parent_of:
-            sample.add(x)
-            x = parent_of[x]
-    allowed = np.array(sorted(sample), np.int32)
-    ref = evaluate(wl.rules, wl.edb, wl.idb, restrict={"sg": (0, allowed)})
-    got = select_rows(rels["sg"], 0, allowed)
-    assert_same_relation("sg", wl.idb["sg"], got, ref.relations["sg"][1], " (sampled nodes)")
-
-
-def test_full_tc_rmat_count_sampled_sources():
-    wl = W.tc_rmat()
-    print("case: full tc_rmat_count", flush=True)
-    rels, stats, _ = engine_run(wl, workspace_bytes=32 << 30)
-    path, rc = rels["path"], rels["reach_count"]
-    # count stratum agrees with the closure it was computed from
-    xs, cnt = np.unique(path[0], return_counts=True)
-    assert np.array_equal(rc[0], xs) and np.array_equal(rc[1], cnt.astype(np.int32))
-    src = wl.edb["edge"][1][0]
-    rng = np.random.default_rng(1)
-    pick = np.sort(rng.choice(np.unique(src), 6, replace=False)).astype(np.int32)
-    ref = evaluate(W.TC_RULES, wl.edb, {"path": ("i32", "i32")}, restrict={"path": (0, pick)})
-    assert_same_relation("path", ("i32", "i32"), select_rows(path, 0, pick), ref.relations["path"][1],
-                         " (sampled sources)")
-    assert stats["derived_tuples"] == len(path[0]) + len(rc[0])
 
 
 # ------------------------------------------------------------- edge cases and errors
