@@ -2999,6 +2999,13 @@ struct Runner {
       return run_wcoj(s.full[0]);
     }
     heads.clear();
+    // rows the heads keep from before the run (set, min and max heads resume;
+    // count, sum and logsumexp heads are recomputed from empty)
+    int64_t rows_before = 0;
+    for (Relation* h : s.heads) {
+      const Agg a = prog->head_agg(h);
+      if (a == Agg::NONE || a == Agg::MIN || a == Agg::MAX) rows_before += h->nrows;
+    }
     XL_TRY(setup_heads(s));
     for (auto& h : heads) begin_round(h.get());
     XL_TRY(snapshot_head_indexes(s.full));
@@ -3010,6 +3017,7 @@ struct Runner {
       total += d;
       st->new_tuples_total += d;
     }
+    const int32_t seed_record = st->rounds_recorded;
     record(total);
     if (s.recursive && total > 0 && batched_tiles(s)) {
       XL_TRY(run_tiles_batched(s.variants[0], heads[0].get(), max_iterations));
@@ -3058,6 +3066,14 @@ struct Runner {
                     indexes.end());
     kept.clear();
     for (auto& h : heads) XL_TRY(materialize(h.get()));
+    if (!s.recursive && seed_record < XL_STATS_ROUNDS) {
+      // a non-recursive stratum records the rows it produced; aggregate heads
+      // built from sorted segments or index degrees only have them now
+      int64_t produced = -rows_before;
+      for (auto& h : heads) produced += h->rel->nrows;
+      st->new_tuples_total += produced - st->delta_rows[seed_record];
+      st->delta_rows[seed_record] = produced;
+    }
     for (auto& ix : kept) indexes.push_back(std::move(ix));
     kept.clear();
     heads.clear();

@@ -76,7 +76,8 @@ def test_full_tc_rmat_count_every_row():
     cnt = m.sum(axis=1)
     rc = rels["reach_count"]
     assert np.array_equal(rc[0], np.flatnonzero(cnt)) and np.array_equal(rc[1], cnt[cnt > 0])
-    assert stats["delta_rows"] == levels and stats["iterations"] == len(levels) - 1
+    # the closure stratum's seed and passes, then the count stratum's rows
+    assert stats["delta_rows"] == levels + [len(rc[0])] and stats["iterations"] == len(levels) - 1
     assert stats["derived_tuples"] == int(cnt.sum()) + int((cnt > 0).sum())
     _check_digest("tc_rmat_count", wl, rels)
     assert _levels(DIGESTS["tc_rmat_count"]["path_sizes"]) == levels
