@@ -390,7 +390,10 @@ def summarize_trace(d):
                "Command (repository root on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`):", "",
                "    " + profile_commands(d, name)[0], "",
                f"The trace covers {runs} fixpoint runs (3 warm-up + 10 timed); 'ms per run' divides the "
-               f"total by {runs}.", "",
+               f"total by {runs}.  The totals also hold one-time work outside the runs (loading the inputs, "
+               "and reading the result once after the timed runs: copies and the canonical sort of the "
+               "read), so a kernel's per-call average is the figure to compare with the bench's "
+               "event-timed launches.", "",
                "| kernel | calls | total ms | ms per run | avg ms | % |", "|---|---|---|---|---|---|"]
         for r in rows[:14]:
             tot = float(r["TotalDurationNs"]) * 1e-6
