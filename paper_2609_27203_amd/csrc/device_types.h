@@ -55,11 +55,17 @@ struct RowSource {
   ColAct act[MAXV];
 };
 
-// Index join: the rows of a relation whose key column equals slot key_slot.
-// off[k] .. off[k+1] delimit rows with key value key_lo + k; col[] are the
-// relation's columns permuted into key order.
+// Index join: the rows of a relation whose key column equals slot key_slot;
+// col[] are the relation's columns permuted into key order.
+//   direct (keys == nullptr): off[k] .. off[k+1] delimit the rows with key
+//     value key_lo + k, for k < key_range (a dense key range);
+//   compacted (keys != nullptr): keys[0 .. key_range) are the distinct key
+//     values minus key_lo (as unsigned, ascending) and off[i] .. off[i+1]
+//     delimit the rows of keys[i] (sparse or wide key ranges, found by
+//     binary search).
 struct IndexProbe {
   const uint32_t* off;
+  const uint32_t* keys;
   const uint32_t* col[MAXC];
   int32_t ncols;
   int32_t key_lo;

@@ -8,6 +8,29 @@
 namespace xlh {
 namespace k {
 
+// ============================================================ index probes
+// Segment of key value v in an index: on success *seg is the s with rows
+// off[s] .. off[s + 1]; false when no row has key v.
+__device__ __forceinline__ bool index_segment(const IndexProbe& ix, uint32_t v, uint32_t* seg) {
+  const uint32_t kk = v - (uint32_t)ix.key_lo;
+  if (!ix.keys) {
+    *seg = kk;
+    return kk < ix.key_range;
+  }
+  uint32_t lo = 0, len = ix.key_range;  // first distinct key >= kk
+  while (len > 0) {
+    const uint32_t half = len >> 1;
+    if (ix.keys[lo + half] < kk) {
+      lo += half + 1;
+      len -= half + 1;
+    } else {
+      len = half;
+    }
+  }
+  *seg = lo;
+  return lo < ix.key_range && ix.keys[lo] == kk;
+}
+
 // ============================================================ wave helpers
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ u64 lanemask_lt() { return (1ull << lane_id()) - 1ull; }

@@ -663,10 +663,10 @@ struct Runner {
   // first (when given, with order_col >= 0) receives an array holding, per
   // key, the order_col value of the key's first row.
   xl_status get_index(Relation* rel, int col, IndexProbe* out, int order_col = -1,
-                      const uint32_t** first = nullptr, int order_kind = 0) {
+                      const uint32_t** first = nullptr, int order_kind = 0, bool dense_only = false) {
     for (auto& ix : indexes)
       if (ix->rel == rel && ix->col == col && ix->order_col == order_col &&
-          (order_col < 0 || ix->order_kind == order_kind)) {
+          (order_col < 0 || ix->order_kind == order_kind) && (!dense_only || !ix->probe.keys)) {
         *out = ix->probe;
         if (first) *first = ix->first;
         return XL_OK;
@@ -675,6 +675,7 @@ struct Runner {
     if (cacheable)
       for (CachedIndex& ce : c->icache)
         if (ce.rel == rel && ce.generation == rel->generation && ce.col == col && ce.order_col == order_col &&
+            (!dense_only || !ce.probe.keys) &&
             (order_col < 0 || ce.order_kind == order_kind)) {
           ce.last_run = c->runs;
           auto ix = std::make_unique<DevIndex>();
@@ -768,18 +769,52 @@ struct Runner {
       XL_TRY(own(8, "index offsets", &off));
       HIP_TRY(c, hipMemsetAsync(off, 0, 8, c->stream));
       p.off = (uint32_t*)off;
+      p.keys = nullptr;
       p.key_lo = 0;
       p.key_range = 0;
     } else {
       if (rel->types[col] != T_I32) return c->fail(XL_UNSUPPORTED, "index key columns must be int32");
-      if (n > ((int64_t)1 << 25))
-        return c->fail(XL_UNSUPPORTED, "indexed relation " + rel->name + " exceeds 2^25 rows");
       const int64_t range = (int64_t)khi - klo + 1;
-      if (range > ((int64_t)1 << 30))
-        return c->fail(XL_UNSUPPORTED, "key range of " + rel->name + " column " + std::to_string(col) +
-                                           " exceeds 2^30 values");
       const bool ordered = order_col >= 0 && order_col < rel->arity && rel->types[order_col] == T_I32;
+      // Direct-address offsets over a dense key range; a compacted index
+      // (distinct keys, found by binary search) over a wide or sparse one.
+      // The kernels that address per-key arrays by key value (frontier,
+      // tiled, pull and gathered rounds, index degrees, degree order) ask for
+      // the direct form; it and ordered indexes keep at most 2^25 rows.
+      const bool compact = !dense_only && (order_col < 0 || order_kind == 1) &&
+                           (range > ((int64_t)1 << 30) || (range > ((int64_t)1 << 22) && range > 16 * n));
+      if ((dense_only || ordered) && n > ((int64_t)1 << 25))
+        return c->fail(XL_UNSUPPORTED, "indexed relation " + rel->name + " exceeds 2^25 rows for this join form");
+      if (!compact && range > ((int64_t)1 << 30))
+        return c->fail(XL_UNSUPPORTED, "key range of " + rel->name + " column " + std::to_string(col) +
+                                           " exceeds 2^30 values for this join form");
       const int kbits = std::max(1, bitlen((uint64_t)range - 1));
+      // offsets from ascending key images: direct over the range, or compacted
+      auto offsets = [&](const uint32_t* sorted_keys) -> xl_status {
+        void* off;
+        if (!compact) {
+          XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
+          HIP_TRY(c, k::csr_offsets(sorted_keys, n, (uint32_t)range, (uint32_t*)off, c->stream));
+          p.off = (uint32_t*)off;
+          p.keys = nullptr;
+          p.key_range = (uint32_t)range;
+          return XL_OK;
+        }
+        void* uk;
+        Buf tmp, cnt;
+        XL_TRY(own((size_t)(n + 1) * 4, "index offsets", &off));
+        XL_TRY(own((size_t)n * 4, "index keys", &uk));
+        XL_TRY(dalloc(c, k::compact_offsets_temp_bytes(n), &tmp, "index compaction scratch"));
+        XL_TRY(dalloc(c, 8, &cnt, "count"));
+        HIP_TRY(c, k::compact_offsets(sorted_keys, n, (uint32_t*)uk, (uint32_t*)off, cnt.as<uint32_t>(), tmp.p,
+                                      c->stream));
+        uint32_t nk = 0;
+        XL_TRY(ctl_read(c, cnt.p, 4, &nk));
+        p.off = (uint32_t*)off;
+        p.keys = (const uint32_t*)uk;
+        p.key_range = nk;
+        return XL_OK;
+      };
       // A loaded relation keeps its rows in lexicographic order, so its index
       // by the first column -- plain, or ordered by the second column's
       // values -- is its rows as they are: only the offsets are built, and
@@ -790,13 +825,9 @@ struct Runner {
         Buf keys;
         XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
         HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
-        void* off;
-        XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
-        HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)range, (uint32_t*)off, c->stream));
+        XL_TRY(offsets(keys.as<uint32_t>()));
         for (int j = 0; j < rel->arity; ++j) p.col[j] = rcol[j];
-        p.off = (uint32_t*)off;
         p.key_lo = klo;
-        p.key_range = (uint32_t)range;
         *out = p;
         if (first) *first = ix->first;
         if (cacheable) cache_index(*ix);
@@ -810,15 +841,13 @@ struct Runner {
       XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
       HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
       HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
-      void* off;
-      XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
       uint32_t* sp = nullptr;
       if (ordered) {
         // one sort by (key, order value); the offsets come from the sorted
         // keys.  Degree order reads each order value's degree from the plain
         // index of rel by the order column (its row count as a key there).
         IndexProbe dz{};
-        if (order_kind == 0) XL_TRY(get_index(rel, order_col, &dz));
+        if (order_kind == 0) XL_TRY(get_index(rel, order_col, &dz, -1, nullptr, 0, true));
         Buf k64, k64b;
         XL_TRY(dalloc(c, (size_t)n * 8, &k64, "index order keys"));
         XL_TRY(dalloc(c, (size_t)n * 8, &k64b, "index order keys"));
@@ -847,7 +876,7 @@ struct Runner {
                                      obits + kbits, tmp.p, c->stream, &alt));
         sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
         HIP_TRY(c, k::high_bits(alt ? k64b.as<u64>() : k64.as<u64>(), obits, n, keys.as<uint32_t>(), c->stream));
-        HIP_TRY(c, k::csr_offsets(keys.as<uint32_t>(), n, (uint32_t)range, (uint32_t*)off, c->stream));
+        XL_TRY(offsets(keys.as<uint32_t>()));
       } else {
         Buf keys2;
         XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
@@ -856,7 +885,7 @@ struct Runner {
                                      perm2.as<uint32_t>(), n, kbits, tmp.p, c->stream, &alt));
         const uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
         sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
-        HIP_TRY(c, k::csr_offsets(sk, n, (uint32_t)range, (uint32_t*)off, c->stream));
+        XL_TRY(offsets(sk));
       }
       for (int j = 0; j < rel->arity; ++j) {
         void* cj;
@@ -867,13 +896,10 @@ struct Runner {
       if (ordered && order_kind == 0) {
         void* fp;
         XL_TRY(own((size_t)range * 4, "index first rows", &fp));
-        HIP_TRY(c, k::segment_first((const uint32_t*)off, p.col[order_col], (uint32_t)range, (uint32_t*)fp,
-                                    c->stream));
+        HIP_TRY(c, k::segment_first(p.off, p.col[order_col], (uint32_t)range, (uint32_t*)fp, c->stream));
         ix->first = (uint32_t*)fp;
       }
-      p.off = (uint32_t*)off;
       p.key_lo = klo;
-      p.key_range = (uint32_t)range;
     }
     *out = p;
     if (first) *first = ix->first;
@@ -939,6 +965,12 @@ struct Runner {
     const int64_t r0 = hr->dom_hi[0] - hr->dom_lo[0] + 1;
     const int64_t r1 = hr->nkey == 2 ? hr->dom_hi[1] - hr->dom_lo[1] + 1 : 1;
     if (r0 <= 0 || r0 > ((int64_t)1 << 28) || r1 <= 0 || r1 > ((int64_t)1 << 30)) return;
+    // the dictionary build needs two arrays over the first key's range, and
+    // the arrays one row per dictionary value over the second key's range:
+    // with the budget init_dv applies to the arrays, skip the dense form
+    // before building a dictionary that could not be used
+    const double budget = std::min(8589934592.0, (double)c->arena.capacity() / 4);
+    if ((double)r0 * 8 > budget || (double)r1 * 16.5 > budget) return;
     std::vector<std::pair<Relation*, int>> src;
     for (const RulePlan& p : s.full) {
       if (p.head != h) continue;
@@ -1021,15 +1053,19 @@ struct Runner {
       kp.nkey = hr->nkey;
       int bits0 = 1;
       double dsize = 1;
+      int full = 0;  // key columns whose domain spans all 2^32 values
       for (int j = 0; j < hr->nkey; ++j) {
         Interval iv = d[j].empty() ? Interval{0, 0} : d[j];
         kp.lo[j] = (int32_t)iv.lo;
         const int b = std::max(1, bitlen((uint64_t)(iv.hi - iv.lo)));
         if (j == 0) bits0 = b; else kp.shift = b;
         dsize *= (double)(iv.hi - iv.lo + 1);
+        full += iv.hi - iv.lo == 0xffffffffll;
       }
-      if (hr->nkey == 2 && bits0 + kp.shift > 63)
-        return c->fail(XL_UNSUPPORTED, "key domain of " + h->name + " is wider than 63 bits");
+      // a packed key is all ones (the empty-slot marker of the hash tables)
+      // only for the largest tuple of two key domains of 2^32 values each
+      if (hr->nkey == 2 && full == 2)
+        return c->fail(XL_UNSUPPORTED, "both key columns of " + h->name + " span all 2^32 values");
       hr->kp = kp;
       hr->bits0 = bits0;
       hr->domain = dsize;
@@ -1409,7 +1445,7 @@ struct Runner {
     f.in_cnt = h->fcnt[h->fcur].as<uint32_t>();
     f.in_diff = h->fdiff[h->fcur].as<uint32_t>();
     f.nseg = h->fn;
-    XL_TRY(get_index(p.steps[0].rel, p.steps[0].key_col, &f.idx));
+    XL_TRY(get_index(p.steps[0].rel, p.steps[0].key_col, &f.idx, -1, nullptr, 0, true));
     f.ybind_col = p.carried_ycol;
     f.bits = h->bits.as<uint32_t>();
     f.lo0 = h->kp.lo[0];
@@ -1419,7 +1455,7 @@ struct Runner {
     f.out_diff = h->fdiff[h->fcur ^ 1].as<uint32_t>();
     f.pull_ratio = (uint32_t)c->pull_ratio;
     if (c->pull_ratio) {
-      XL_TRY(get_index(p.steps[0].rel, p.carried_ycol, &f.rev, p.steps[0].key_col, &f.rev_first));
+      XL_TRY(get_index(p.steps[0].rel, p.carried_ycol, &f.rev, p.steps[0].key_col, &f.rev_first, 0, true));
       if (!f.rev_first) return c->fail(XL_DEVICE_ERROR, "pull index without first rows (internal)");
       f.rev_zcol = p.steps[0].key_col;
       if (!h->hasin.p) {
@@ -1443,9 +1479,9 @@ struct Runner {
     a.in_flag = h->gflag[h->gcur].as<uint32_t>();
     a.out_flag = h->gflag[h->gcur ^ 1].as<uint32_t>();
     a.bits = h->bits.as<uint32_t>();
-    XL_TRY(get_index(p.steps[g.s1].rel, g.x_col, &a.e1));
+    XL_TRY(get_index(p.steps[g.s1].rel, g.x_col, &a.e1, -1, nullptr, 0, true));
     a.e1_acol = p.steps[g.s1].key_col;
-    XL_TRY(get_index(p.steps[g.s2].rel, p.steps[g.s2].key_col, &a.push.idx));
+    XL_TRY(get_index(p.steps[g.s2].rel, p.steps[g.s2].key_col, &a.push.idx, -1, nullptr, 0, true));
     a.push.ybind_col = g.y_col;
     a.lo0 = a.push.lo0 = h->kp.lo[0];
     a.lo1 = a.push.lo1 = h->kp.lo[1];
@@ -1630,7 +1666,7 @@ struct Runner {
     }
     if (kcol < 0) return nullptr;
     for (const auto& ix : indexes)
-      if (ix->rel == p.driver && ix->col == kcol) return ix.get();
+      if (ix->rel == p.driver && ix->col == kcol && !ix->probe.keys) return ix.get();
     return nullptr;
   }
 
@@ -1669,7 +1705,7 @@ struct Runner {
     q.range1 = (uint32_t)h->range1;
     q.nrank = (uint32_t)h->nrank_d;
     q.lo1 = h->kp.lo[1];
-    XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev));
+    XL_TRY(get_index(sp.rel, p.carried_ycol, &q.rev, -1, nullptr, 0, true));
     for (int j = 0; j < sp.rel->arity; ++j) q.rev.act[j] = sp.act[j];
     q.rev.act[p.carried_ycol].kind = CA_NONE;  // Y is bound from the key
     q.zcol = sp.key_col;
@@ -1795,7 +1831,7 @@ struct Runner {
     const int fast = affine_value(p, &fcol);
     const int64_t nsd = h->nrank_d * h->range1;
     IndexProbe fwd{};
-    XL_TRY(get_index(sp.rel, sp.key_col, &fwd));
+    XL_TRY(get_index(sp.rel, sp.key_col, &fwd, -1, nullptr, 0, true));
     const int B = c->batched_rounds;
     Buf acc, rounds, list, tmp;
     XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
@@ -1905,7 +1941,7 @@ struct Runner {
       // marks are the delta presence rows pushed to the out-neighbours (the
       // mark bits are clear: the previous list pass cleared what it listed)
       IndexProbe fwd{};
-      XL_TRY(get_index(sp.rel, sp.key_col, &fwd));
+      XL_TRY(get_index(sp.rel, sp.key_col, &fwd, -1, nullptr, 0, true));
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
       HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
                                    h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));

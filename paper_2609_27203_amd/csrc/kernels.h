@@ -41,6 +41,12 @@ hipError_t minmax_i32(const int32_t* col, int64_t n, int32_t* out, hipStream_t s
 // key[i] = col[i] - lo as unsigned.
 hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hipStream_t s);
 // off[k] = first i with sorted[i] >= k, for k in [0, range].
+// Compacted index offsets from n ascending keys: keys[0 .. *count) receive
+// the distinct keys, off[0 .. *count] the first row of each and n (keys and
+// off must hold n and n + 1 values; *count is written on the device).
+size_t compact_offsets_temp_bytes(int64_t n);
+hipError_t compact_offsets(const uint32_t* sorted, int64_t n, uint32_t* keys, uint32_t* off, uint32_t* count,
+                           void* temp, hipStream_t s);
 hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
                        hipStream_t s);
 // key[i] = (sorted[i] << 16) | (0xffff - min(deg(zcol[perm[i]]), 0xffff)), deg

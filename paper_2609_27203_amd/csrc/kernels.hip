@@ -391,6 +391,38 @@ hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32
   return hipGetLastError();
 }
 
+// Compacted offsets: row i starts a segment when flag[i] (its key differs
+// from row i - 1's); the segment's number is pos[i] (the exclusive scan of
+// the flags), its key sorted[i] and its first row i; the last row closes the
+// array with off[number of segments] = n.
+__global__ void segment_keys_k(const uint32_t* sorted, const uint32_t* flag, const uint32_t* pos, int64_t n,
+                               uint32_t* keys, uint32_t* off) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t f = flag[i], p = pos[i];
+    if (f) {
+      keys[p] = sorted[i];
+      off[p] = (uint32_t)i;
+    }
+    if (i == n - 1) off[p + f] = (uint32_t)n;
+  }
+}
+size_t compact_offsets_temp_bytes(int64_t n) { return ((size_t)n * 8 + 255) / 256 * 256 + scan_temp_bytes(n); }
+hipError_t compact_offsets(const uint32_t* sorted, int64_t n, uint32_t* keys, uint32_t* off, uint32_t* count,
+                           void* temp, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  uint32_t* flag = (uint32_t*)temp;
+  uint32_t* pos = flag + n;
+  void* scan_tmp = (char*)temp + ((size_t)n * 8 + 255) / 256 * 256;
+  const uint32_t* cols[1] = {sorted};
+  hipError_t e = row_change_flags(cols, 1, n, flag, s);
+  if (e != hipSuccess) return e;
+  e = scan_exclusive_u32(flag, pos, n, count, scan_tmp, s);
+  if (e != hipSuccess) return e;
+  segment_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, flag, pos, n, keys, off);
+  return hipGetLastError();
+}
+
 // key[i] = (sorted[i] << 16) | (0xffff - min(deg(z), 0xffff)) with z =
 // zcol[perm[i]] and deg(z) = off[z - klo + 1] - off[z - klo] (0 outside the
 // key range): sorting by it keeps the key order and puts, inside each key's
@@ -1399,15 +1431,21 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     if (HAS_INDEX) {
       uint32_t beg = 0, deg = 0, beg2 = 0, deg2 = 1;
       if (ok) {
-        const uint32_t kk = getv(v, a.idx.key_slot) - (uint32_t)a.idx.key_lo;
-        if (kk < a.idx.key_range) {
+        uint32_t kk;
+        if (index_segment(a.idx, getv(v, a.idx.key_slot), &kk)) {
           beg = a.idx.off[kk];
           deg = a.idx.off[kk + 1] - beg;
+          // the wave's match count must stay below 2^32: a key with 2^26 or
+          // more rows is refused (the host reports it as unsupported)
+          if (deg >= (1u << 26)) {
+            atomicOr(&a.emit.counters[CNT_FATAL], 32ull);
+            deg = 0;
+          }
         }
         if (a.has_idx2) {
-          const uint32_t k2 = getv(v, a.idx2.key_slot) - (uint32_t)a.idx2.key_lo;
+          uint32_t k2;
           deg2 = 0;
-          if (k2 < a.idx2.key_range) {
+          if (index_segment(a.idx2, getv(v, a.idx2.key_slot), &k2)) {
             beg2 = a.idx2.off[k2];
             deg2 = a.idx2.off[k2 + 1] - beg2;
           }

@@ -21,8 +21,8 @@ constexpr int WC_THREADS = 256;
 constexpr int WC_WAVES = WC_THREADS / 64;
 
 __device__ __forceinline__ uint32_t seg_len(const IndexProbe& ix, uint32_t v, uint32_t* beg) {
-  const uint32_t kk = v - (uint32_t)ix.key_lo;
-  if (kk >= ix.key_range) {
+  uint32_t kk;
+  if (!index_segment(ix, v, &kk)) {
     *beg = 0;
     return 0;
   }

@@ -126,3 +126,21 @@ def test_full_same_generation_every_row():
     assert np.array_equal(x.astype(np.int64) * n + y, keys)
     assert stats["derived_tuples"] == len(keys)
     _check_digest("same_generation", wl, rels)
+
+
+def test_join_over_the_full_rmat_closure():
+    """A later stratum joins the 128.9 M-row closure by its second column (an
+    index built by sorting the whole relation, beyond 2^25 rows):
+    into(Z) :- edge(_, Y), path(Z, Y) holds every node with a path row, since
+    every path ends with an edge into its last node."""
+    base = W.tc_rmat()
+    rules = W.TC_RULES + "into(Z) :- edge(_,Y), path(Z,Y).\n"
+    wl = W.Workload("rmat_later_join", rules, base.edb, {"path": ("i32", "i32"), "into": ("i32",)})
+    print("case: full R-MAT closure joined by its second column", flush=True)
+    rels, stats, ctx = engine_run(wl, workspace_bytes=32 << 30)
+    ctx.close()
+    src, dst = wl.edb["edge"][1]
+    n = 1 << base.params["scale"]
+    m = CERT.reached_matrix(CERT.closure_bits(n, src, dst)[0], n)
+    CERT.check_closure_rows(m, *rels["path"])
+    assert np.array_equal(rels["into"][0], np.flatnonzero(m.any(axis=1)).astype(np.int32))
