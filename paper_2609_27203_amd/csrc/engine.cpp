@@ -1419,22 +1419,35 @@ struct Runner {
     return XL_OK;
   }
 
+  // Fatal flags of a stage launch: 32 is a join key with 2^26 or more rows
+  // (the kernel's 32-bit match count per wavefront), anything else internal.
+  xl_status stage_fatal(u64 flags, const char* internal) {
+    if (flags & 32)
+      return c->fail(XL_UNSUPPORTED, "a join key matches 2^26 or more rows of an indexed relation");
+    return c->fail(XL_DEVICE_ERROR, internal);
+  }
+
   xl_status counted_pass(StageArgs& a, int64_t* total, Buf* offs) {
     const int64_t nchunks = (a.src.n + 63) / 64;
     Buf cnt, tmp, tot;
     XL_TRY(dalloc(c, (size_t)nchunks * 8, &cnt, "chunk counts"));
     XL_TRY(dalloc(c, (size_t)nchunks * 8, offs, "chunk offsets"));
     XL_TRY(dalloc(c, k::scan_temp_bytes(nchunks), &tmp, "scan scratch"));
-    XL_TRY(dalloc(c, 8, &tot, "count"));
+    XL_TRY(dalloc(c, 16, &tot, "count"));
     StageArgs ca = a;
     ca.emit.mode = EM_COUNT;
     ca.emit.chunk_cnt = cnt.as<u64>();
+    ca.emit.counters = c->dcounters;
+    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     HIP_TRY(c, k::stage_launch(ca, c->stream, 1 << 16));
     HIP_TRY(c, k::scan_exclusive_u64(cnt.as<u64>(), offs->as<u64>(), nchunks, tot.as<u64>(), tmp.p,
                                      c->stream));
-    u64 t = 0;
-    XL_TRY(ctl_read(c, tot.p, 8, &t));
-    *total = (int64_t)t;
+    // the total and the fatal flags in one read
+    HIP_TRY(c, hipMemcpyAsync(tot.as<u64>() + 1, c->dcounters + CNT_FATAL, 8, hipMemcpyDeviceToDevice, c->stream));
+    u64 t[2] = {0, 0};
+    XL_TRY(ctl_read(c, tot.p, 16, t));
+    if (t[1]) return stage_fatal(t[1], "stage count pass failed (internal)");
+    *total = (int64_t)t[0];
     return XL_OK;
   }
 
@@ -1975,7 +1988,7 @@ struct Runner {
       HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
       XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
-      if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "key outside the dense domain (internal)");
+      if (cnt[CNT_FATAL]) return stage_fatal(cnt[CNT_FATAL], "key outside the dense domain (internal)");
       if (c->profile) {
         float ms = 0;
         HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
@@ -2405,6 +2418,7 @@ struct Runner {
         HIP_TRY(c, k::stage_launch(a, c->stream, 1 << 16));
         u64 cnt[CNT_N];
         XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+        if (cnt[CNT_FATAL]) return stage_fatal(cnt[CNT_FATAL], "count key outside the head domain (internal)");
         cands += (int64_t)cnt[CNT_CANDIDATES];
         return XL_OK;
       }
@@ -2513,8 +2527,8 @@ struct Runner {
         if (product && cnt[CNT_FATAL] == 16) {
           refused = true;  // some product rows were skipped: the rule runs again unfused below
         } else if (cnt[CNT_FATAL]) {
-          return c->fail(XL_DEVICE_ERROR, h->dv ? "key outside the dense domain (internal)"
-                                                : "hash table probe exhausted or row list overflow (internal)");
+          return stage_fatal(cnt[CNT_FATAL], h->dv ? "key outside the dense domain (internal)"
+                                                   : "hash table probe exhausted or row list overflow (internal)");
         }
         cands += (int64_t)cnt[CNT_CANDIDATES];
         if (h->dense) {

@@ -676,6 +676,27 @@ def test_sparse_and_wide_node_ids(name, span):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+def test_join_key_with_2_26_rows_is_refused():
+    """One key holding 2^26 rows of the indexed relation would overflow the
+    stage kernel's 32-bit match count per wavefront: the run reports
+    XL_UNSUPPORTED (the kernel skips that key's matches, so nothing is read
+    out of bounds), and one row fewer runs."""
+    from paper_2609_27203_amd import xlh
+    for n, ok in (((1 << 26) - 1, True), (1 << 26, False)):
+        v = np.arange(n, dtype=np.int32)
+        wl = W.Workload("hub", "out(V) :- d(K), e(K, V), V < 3.",
+                        {"d": (("i32",), [np.zeros(1, np.int32)]), "e": (("i32", "i32"), [np.zeros(n, np.int32), v])},
+                        {"out": ("i32",)})
+        print(f"case: hub key with {n} rows", flush=True)
+        if ok:
+            rels, _, _ = engine_run(wl, workspace_bytes=8 << 30)
+            assert rels["out"][0].tolist() == [0, 1, 2]
+        else:
+            with pytest.raises(xlh.XlError) as ei:
+                engine_run(wl, workspace_bytes=8 << 30)
+            assert ei.value.status_name == "XL_UNSUPPORTED" and "2^26" in str(ei.value)
+
+
 def test_sparse_ids_self_join_and_later_stratum():
     """Self-joined recursion and a later join over the finished closure, with
     sparse ids: the head snapshots and the closure are indexed compacted."""
