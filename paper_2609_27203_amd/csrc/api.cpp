@@ -8,7 +8,7 @@
 using namespace xlh;
 
 namespace {
-constexpr size_t PINNED_BYTES = 4096;
+constexpr size_t PINNED_BYTES = CTL_BYTES;
 constexpr int STATIC_MAX_DEVICES = 64;
 }  // namespace
 
@@ -69,6 +69,7 @@ xl_status xl_context_create(int device, void* hip_stream, void* workspace, size_
       return XL_DEVICE_ERROR;
     }
     c->dcounters = (unsigned long long*)c->arena.alloc(8 * CNT_N);
+    c->dcheck = (unsigned long long*)c->arena.alloc(8);
   }
   *out = c;
   return XL_OK;
@@ -91,6 +92,7 @@ xl_status xl_context_create_static(int device, void* hip_stream, xl_context** ou
   c->pinned = c->ctl;
   c->arena.init((char*)g_static_ptr[device], XL_STATIC_WORKSPACE_BYTES);
   c->dcounters = (unsigned long long*)c->arena.alloc(8 * CNT_N);
+  c->dcheck = (unsigned long long*)c->arena.alloc(8);
   g_static_held[device] = true;
   *out = c;
   return XL_OK;

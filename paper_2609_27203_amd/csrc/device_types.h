@@ -114,6 +114,13 @@ enum Counter : int32_t {
   CNT_N = 8
 };
 
+// Internal consistency flags a run's kernels may set (Context::dcheck); any
+// set bit fails the run with XL_DEVICE_ERROR.
+enum CheckBit : unsigned long long {
+  CHECK_BITMAP_ROWS = 1,    // a dense head's bitmap holds a different row count than its receipt
+  CHECK_COUNT_DOMAIN = 2,   // a count key outside the head's planned domain
+};
+
 struct EmitSpec {
   int32_t mode;
   KeyPack key;

@@ -136,6 +136,7 @@ xl_status dalloc(Context* c, size_t bytes, Buf* b, const char* what) {
 }
 
 xl_status ctl_read(Context* c, const void* dev, size_t bytes, void* host) {
+  if (bytes > CTL_CHECK_OFFSET) return c->fail(XL_DEVICE_ERROR, "control read larger than the control block (internal)");
   HIP_TRY(c, hipMemcpyAsync(c->pinned, dev, bytes, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   memcpy(host, c->pinned, bytes);
@@ -730,7 +731,10 @@ struct Runner {
           HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0,
                                            off.as<uint32_t>() + h->range0, tmp.p, c->stream));
           HIP_TRY(c, k::bits_to_rows(h->bits.as<uint32_t>(), h->range0, h->row_words, off.as<uint32_t>(),
-                                     h->kp.lo[0], h->kp.lo[1], (uint32_t*)snap[0], (uint32_t*)snap[1], c->stream));
+                                     h->kp.lo[0], h->kp.lo[1], (uint32_t*)snap[0], (uint32_t*)snap[1], n,
+                                     c->stream));
+          HIP_TRY(c, k::check_eq(off.as<uint32_t>() + h->range0, (uint32_t)n, c->dcheck, CHECK_BITMAP_ROWS,
+                                 c->stream));
         } else {
           const int64_t nbits = (h->range0 + 31) / 32 * 32;
           XL_TRY(dalloc(c, k::bits_list_temp_bytes(nbits), &tmp, "compaction scratch"));
@@ -1582,27 +1586,34 @@ struct Runner {
     f.in_diff = h->dbits.as<uint32_t>();
     f.nseg = h->range0;
     f.out_cnt = f.out_diff = nullptr;
-    constexpr size_t HDR = 16;
+    // one block, one read: the work queue, largest round and cap overflow in
+    // a 256-byte block of their own (every workgroup's atomic on the queue
+    // word is on the path to its next key, so no other counter shares its
+    // cache line), the kernel's counters, then the new tuples of each round
+    constexpr size_t HDR = 256, CNTB = 256, BLOCK = HDR + CNTB + 8 * XL_STATS_ROUNDS;
+    static_assert(8 * CNT_N <= CNTB, "counters fit their block");
     Buf rs;
-    XL_TRY(dalloc(c, HDR + 8 * XL_STATS_ROUNDS, &rs, "round counters"));
-    HIP_TRY(c, hipMemsetAsync(rs.p, 0, HDR + 8 * XL_STATS_ROUNDS, c->stream));
+    XL_TRY(dalloc(c, BLOCK, &rs, "round counters"));
+    HIP_TRY(c, hipMemsetAsync(rs.p, 0, BLOCK, c->stream));
     f.queue = rs.as<uint32_t>();
     f.max_round = rs.as<uint32_t>() + 1;
     f.overflow = rs.as<uint32_t>() + 2;
-    f.round_new = (unsigned long long*)((char*)rs.p + HDR);
+    f.counters = (unsigned long long*)((char*)rs.p + HDR);
+    f.round_new = (unsigned long long*)((char*)rs.p + HDR + CNTB);
     f.round_slots = XL_STATS_ROUNDS;
     f.max_rounds = (uint32_t)std::min<int64_t>(max_iterations, 0xffffffffll);
-    HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
     HIP_TRY(c, k::frontier_resident(f, 0, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
-    u64 cnt[CNT_N];
-    XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
+    std::vector<unsigned char> blk(BLOCK);
+    XL_TRY(ctl_read(c, rs.p, BLOCK, blk.data()));
     uint32_t hdr[4];
-    XL_TRY(ctl_read(c, rs.p, HDR, hdr));
+    u64 cnt[CNT_N];
+    memcpy(hdr, blk.data(), sizeof(hdr));
+    memcpy(cnt, blk.data() + HDR, sizeof(cnt));
     const uint32_t rounds = hdr[1];
     std::vector<u64> per((size_t)XL_STATS_ROUNDS, 0);
-    if (rounds) XL_TRY(ctl_read(c, f.round_new, 8 * std::min<size_t>(rounds, XL_STATS_ROUNDS), per.data()));
+    memcpy(per.data(), blk.data() + HDR + CNTB, 8 * (size_t)XL_STATS_ROUNDS);
     cands += (int64_t)cnt[CNT_CANDIDATES];
     if (c->profile) {
       float ms = 0;
@@ -2402,12 +2413,8 @@ struct Runner {
       if (h->dcount) {
         const DevIndex* dx = degree_index(p);
         if (dx) {  // the group's count is the index degree of its key
-          HIP_TRY(c, hipMemsetAsync(c->dcounters, 0, 8 * CNT_N, c->stream));
           HIP_TRY(c, k::index_degree_add(dx->probe.off, dx->probe.key_range, dx->probe.key_lo, h->kp.lo[0],
-                                         (uint32_t)h->range0, h->counts.as<uint32_t>(), c->dcounters, c->stream));
-          u64 cnt[CNT_N];
-          XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
-          if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "count key outside the head domain (internal)");
+                                         (uint32_t)h->range0, h->counts.as<uint32_t>(), c->dcheck, c->stream));
           cands += src.n;
           return XL_OK;
         }
@@ -2832,15 +2839,17 @@ struct Runner {
       HIP_TRY(c, k::row_popcount(h->bits.as<uint32_t>(), h->range0, h->row_words, cnt.as<uint32_t>(), c->stream));
       HIP_TRY(c, k::scan_exclusive_u32(cnt.as<uint32_t>(), off.as<uint32_t>(), h->range0,
                                        off.as<uint32_t>() + h->range0, tmp.p, c->stream));
-      uint32_t n = 0;
-      XL_TRY(ctl_read(c, off.as<uint32_t>() + h->range0, 4, &n));
-      if ((int64_t)n != h->keys) return c->fail(XL_DEVICE_ERROR, "bitmap row count mismatch (internal)");
+      // the receipt's count is the row count; the bitmap's own total is
+      // compared on the device (flag read at the end of the run), and the
+      // rows are written only up to the allocated count
+      const int64_t n = h->keys;
+      HIP_TRY(c, k::check_eq(off.as<uint32_t>() + h->range0, (uint32_t)n, c->dcheck, CHECK_BITMAP_ROWS, c->stream));
       h->rows[0].reset();
       h->rows[1].reset();
       Buf out[2];
-      for (int j = 0; j < 2; ++j) XL_TRY(dalloc(c, (size_t)std::max<uint32_t>(n, 1) * 4, &out[j], "relation column"));
+      for (int j = 0; j < 2; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
       HIP_TRY(c, k::bits_to_rows(h->bits.as<uint32_t>(), h->range0, h->row_words, off.as<uint32_t>(), h->kp.lo[0],
-                                 h->kp.lo[1], out[0].as<uint32_t>(), out[1].as<uint32_t>(), c->stream));
+                                 h->kp.lo[1], out[0].as<uint32_t>(), out[1].as<uint32_t>(), n, c->stream));
       relation_free_storage(r);
       for (int j = 0; j < 2; ++j) r->col[j] = (uint32_t*)out[j].keep();
       r->nrows = n;
@@ -3152,6 +3161,7 @@ xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st)
   HIP_TRY(c, hipEventCreate(&e0));
   HIP_TRY(c, hipEventCreate(&e1));
   HIP_TRY(c, hipEventRecord(e0, c->stream));
+  HIP_TRY(c, hipMemsetAsync(c->dcheck, 0, 8, c->stream));
   xl_status s = XL_OK;
   {
     Runner run{c, p, st};
@@ -3165,8 +3175,19 @@ xl_status run_program(Program* p, int64_t max_iterations, xl_fixpoint_stats* st)
     }
     st->candidates_total = run.cands;
   }
+  // the consistency flags ride on the run's final synchronization: the copy
+  // into the control block's last word is complete once e1 is
+  unsigned long long* check_host = (unsigned long long*)((char*)c->pinned + CTL_CHECK_OFFSET);
+  *check_host = 0;
+  (void)hipMemcpyAsync(check_host, c->dcheck, 8, hipMemcpyDeviceToHost, c->stream);
   (void)hipEventRecord(e1, c->stream);
   (void)hipEventSynchronize(e1);
+  if (s == XL_OK && *check_host) {
+    const unsigned long long f = *check_host;
+    s = c->fail(XL_DEVICE_ERROR, std::string("internal consistency check failed:") +
+                                     (f & CHECK_BITMAP_ROWS ? " bitmap row count" : "") +
+                                     (f & CHECK_COUNT_DOMAIN ? " count key outside the head domain" : ""));
+  }
   float ms = 0;
   (void)hipEventElapsedTime(&ms, e0, e1);
   (void)hipEventDestroy(e0);

@@ -85,6 +85,11 @@ struct CachedIndex {
   uint64_t last_run = 0;
 };
 
+// The host control block (8192 bytes, pinned): control reads use its first
+// CTL_CHECK_OFFSET bytes, the run's consistency flags its last word.
+constexpr size_t CTL_BYTES = 8192;
+constexpr size_t CTL_CHECK_OFFSET = CTL_BYTES - 64;
+
 struct Context {
   int device = -1;
   hipStream_t stream = nullptr;
@@ -92,6 +97,9 @@ struct Context {
   std::string err;
   void* pinned = nullptr;                  // host control block
   unsigned long long* dcounters = nullptr; // device counters (arena)
+  // internal consistency flags (arena word, CHECK_* bits) that kernels set
+  // during a run; read once with the run's final synchronization
+  unsigned long long* dcheck = nullptr;
   std::vector<Relation*> rels;
   std::vector<Program*> progs;
   int hash_min_log2 = 22;

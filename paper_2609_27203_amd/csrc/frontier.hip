@@ -561,11 +561,12 @@ hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words,
 
 // Relation rows (x, y) of every set bit, in ascending (x, y) order: bitmap row
 // r holds x = lo0 + r and starts at off[r].  Each chunk of 256 words is
-// decoded into LDS first so the column writes are coalesced.
+// decoded into LDS first so the column writes are coalesced.  Rows at
+// positions cap and beyond are not written (the columns hold cap rows).
 __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int64_t nrows,
                                                       uint32_t row_words, const uint32_t* off,
                                                       int32_t lo0, int32_t lo1, uint32_t* c0,
-                                                      uint32_t* c1) {
+                                                      uint32_t* c1, u64 cap) {
   __shared__ uint32_t stage[256 * 32];
   __shared__ uint32_t s_w[4];
   for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
@@ -580,8 +581,10 @@ __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int6
       for (uint32_t b = d; b; b &= b - 1) stage[pos++] = (uint32_t)lo1 + wi * 32u + (uint32_t)(__ffs(b) - 1);
       __syncthreads();
       for (uint32_t i = threadIdx.x; i < n; i += 256) {
-        c0[out + i] = x;
-        c1[out + i] = stage[i];
+        if (out + i < cap) {
+          c0[out + i] = x;
+          c1[out + i] = stage[i];
+        }
       }
       out += n;
       __syncthreads();
@@ -589,10 +592,10 @@ __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int6
   }
 }
 hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
-                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s) {
+                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, int64_t cap, hipStream_t s) {
   if (nrows <= 0) return hipSuccess;
   bits_to_rows_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, off,
-                                                                            lo0, lo1, c0, c1);
+                                                                            lo0, lo1, c0, c1, (u64)cap);
   return hipGetLastError();
 }
 

@@ -137,7 +137,7 @@ hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32
 hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
                         hipStream_t s);
 hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
-                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, hipStream_t s);
+                        int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, int64_t cap, hipStream_t s);
 // out row sg = bitmap row (x[sg] - lo0)
 hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t* x, int32_t lo0, int64_t nseg,
                        uint32_t* out, hipStream_t s);
@@ -195,8 +195,9 @@ hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
-                            uint32_t head_range, uint32_t* counts, u64* counters,
-                            hipStream_t s);
+                            uint32_t head_range, uint32_t* counts, u64* check, hipStream_t s);
+// *check |= bit when the device value *v differs from expected.
+hipError_t check_eq(const uint32_t* v, uint32_t expected, u64* check, u64 bit, hipStream_t s);
 // out[i] = in[i] + add
 hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, hipStream_t s);
 

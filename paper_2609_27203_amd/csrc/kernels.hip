@@ -2456,7 +2456,7 @@ hipError_t add_u32(const uint32_t* in, uint32_t add, uint32_t* out, int64_t n, h
 // key, so no two threads touch one counter; a key with rows outside the head's
 // domain raises the fatal counter.
 __global__ void index_degree_add_k(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
-                                   uint32_t head_range, uint32_t* counts, u64* counters) {
+                                   uint32_t head_range, uint32_t* counts, u64* check) {
   for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < key_range; i += gridDim.x * blockDim.x) {
     const uint32_t d = off[i + 1] - off[i];
     if (!d) continue;
@@ -2464,14 +2464,23 @@ __global__ void index_degree_add_k(const uint32_t* off, uint32_t key_range, int3
     if (hk < head_range)
       counts[hk] += d;
     else
-      atomicAdd(&counters[CNT_FATAL], 1ull);
+      atomicOr(check, (u64)CHECK_COUNT_DOMAIN);
   }
 }
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,
-                            uint32_t head_range, uint32_t* counts, u64* counters, hipStream_t s) {
+                            uint32_t head_range, uint32_t* counts, u64* check, hipStream_t s) {
   if (key_range == 0) return hipSuccess;
   index_degree_add_k<<<grid_for(key_range, 256, 65536), 256, 0, s>>>(off, key_range, key_lo, head_lo,
-                                                                      head_range, counts, counters);
+                                                                      head_range, counts, check);
+  return hipGetLastError();
+}
+
+// *check |= bit when *v differs from expected (one thread).
+__global__ void check_eq_k(const uint32_t* v, uint32_t expected, u64* check, u64 bit) {
+  if (threadIdx.x == 0 && *v != expected) atomicOr(check, bit);
+}
+hipError_t check_eq(const uint32_t* v, uint32_t expected, u64* check, u64 bit, hipStream_t s) {
+  check_eq_k<<<1, 64, 0, s>>>(v, expected, check, bit);
   return hipGetLastError();
 }
 
