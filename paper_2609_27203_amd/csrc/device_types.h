@@ -180,6 +180,11 @@ struct StageArgs {
   uint32_t consts[MAXK];
   NegTable neg[MAXNEG];
   EmitSpec emit;
+  // batched rounds: the driver rows are [src_range[0], src_range[1]) of the
+  // src columns (read on the device; src.n only bounds the grid), and the
+  // launch does nothing once an earlier launch of the batch overflowed
+  // (emit.counters[CNT_OVERFLOW]); null: rows [0, src.n)
+  const unsigned long long* src_range;
 };
 
 // One round of a carried-value rule over a dense sum/logsumexp head, for the

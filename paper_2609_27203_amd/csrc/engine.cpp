@@ -1757,6 +1757,152 @@ struct Runner {
   // Batched gathered rounds: each round gets its own counter block, so
   // `batched_rounds` rounds run per host read; rounds past the fixpoint find
   // no flagged delta row and change nothing.
+  // ------------------------------------------------------------ batched set rounds
+  // A recursive stratum with one set head held in a hash table (row list +
+  // open-addressing set), whose delta variants each run in one stage-kernel
+  // launch over the head's delta (one index step, or two fused into a
+  // product) and join only relations outside the stratum, runs
+  // batched_rounds rounds per host read: the head's row list is append-only,
+  // so round j's delta is the rows between two boundaries that a one-thread
+  // kernel records on the device after each round, and every launch reads
+  // its driver range from there.  The batch shares one set of counters and
+  // one load limit; a launch that crosses the limit (or refuses a product
+  // row) sets the overflow flag, after which the rest of the batch does
+  // nothing and the host re-runs that round the ordinary way (growing the
+  // table; insert-if-absent keeps the partial round's rows valid).  Passes,
+  // per-pass delta sizes and the iteration cap are those of the host loop.
+  const u64* batch_range = nullptr;
+  u64* batch_counters = nullptr;
+  u64 batch_row_base = 0, batch_limit = 0;
+  int batch_grid = EMIT_GRID;  // workgroups of a batched launch (its waves bound the slack)
+
+  bool batched_sets(const Stratum& s) {
+    if (c->batched_rounds <= 0 || heads.size() != 1 || s.variants.empty()) return false;
+    HeadRun* h = heads[0].get();
+    if (!h->is_set || h->dense || h->frontier || h->gathered || h->dv) return false;
+    for (const RulePlan& p : s.variants) {
+      if (!p.driver_delta || p.driver != h->rel || p.wcoj || head_of(p.head) != h) return false;
+      for (const StepPlan& sp : p.steps)
+        if (head_of(sp.rel)) return false;
+      if (p.steps.size() > 2) return false;
+      if (p.steps.size() == 2) {
+        std::vector<MicroOp> pops;
+        std::vector<uint32_t> pconsts;
+        if (!c->product_joins || !product_plan(p, h, &pops, &pconsts)) return false;
+      }
+    }
+    return true;
+  }
+
+  xl_status run_sets_batched(Stratum& s, HeadRun* h, int64_t max_iterations) {
+    const int B = c->batched_rounds;
+    constexpr size_t CNTB = 256;
+    static_assert(8 * CNT_N <= CNTB, "counters fit their block");
+    Buf blk;  // the batch's counters, then the round boundaries
+    XL_TRY(dalloc(c, CNTB + 8 * (size_t)(B + 2), &blk, "batch counters"));
+    u64* counters = blk.as<u64>();
+    u64* bnd = (u64*)((char*)blk.p + CNTB);
+    std::vector<unsigned char> host(CNTB + 8 * (size_t)(B + 2));
+    int64_t pass = 0;
+    while (h->dend > h->dbeg) {
+      if (pass >= max_iterations)
+        return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                   " reached before the fixpoint");
+      // every wavefront of the launch that crosses the limit may still insert
+      // one batch: the grid takes at most a quarter of the table as slack
+      // (whatever the round's delta size, which is unknown here)
+      const int64_t waves =
+          std::max<int64_t>(256, std::min<int64_t>((int64_t)EMIT_GRID * 4, h->cap / 4 / WAVE_SLACK)) / 4 * 4;
+      batch_grid = (int)(waves / 4);
+      const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
+      if (h->keys >= max_keys) {
+        XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + WAVE_SLACK * waves + 1024)));
+        continue;
+      }
+      const int K = (int)std::min<int64_t>(B, max_iterations - pass);
+      HIP_TRY(c, hipMemsetAsync(counters, 0, CNTB, c->stream));
+      HIP_TRY(c, k::batch_init(bnd, B + 2, (u64)h->dbeg, (u64)h->dend, c->stream));
+      batch_counters = counters;
+      batch_row_base = (u64)h->nrows;
+      batch_limit = (u64)(max_keys - h->keys);
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+      for (int j = 1; j <= K; ++j) {
+        batch_range = bnd + (j - 1);
+        for (RulePlan& p : s.variants) {
+          const xl_status e = eval_plan(p);
+          if (e != XL_OK) {
+            batch_range = nullptr;
+            return e;
+          }
+        }
+        HIP_TRY(c, k::batch_mark(bnd, j, counters, batch_row_base, c->stream));
+      }
+      batch_range = nullptr;
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+      XL_TRY(ctl_read(c, blk.p, CNTB + 8 * (size_t)(K + 2), host.data()));
+      u64 cnt[CNT_N];
+      memcpy(cnt, host.data(), sizeof(cnt));
+      const u64* b = (const u64*)(host.data() + CNTB);
+      if (cnt[CNT_FATAL] & ~16ull) return stage_fatal(cnt[CNT_FATAL], "hash table probe exhausted or row list overflow (internal)");
+      cands += (int64_t)cnt[CNT_CANDIDATES];
+      if (c->profile) {
+        float ms = 0;
+        HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+        st->emit_ms += ms;
+        st->emit_launches += (int64_t)K * (int64_t)s.variants.size();
+        st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+        st->emit_new += (int64_t)cnt[CNT_APPENDED];
+      }
+      h->nrows = (int64_t)batch_row_base + (int64_t)cnt[CNT_APPENDED];
+      h->keys += (int64_t)cnt[CNT_APPENDED];
+      if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+        return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                                 std::to_string(h->rel->max_rows));
+      int done = 0;
+      bool empty = false;
+      for (int j = 1; j <= K && b[j + 1] != ~0ull; ++j) {
+        ++done;
+        ++pass;
+        st->iterations++;
+        const int64_t d = (int64_t)(b[j + 1] - b[j]);
+        record(d);
+        st->new_tuples_total += d;
+        if (d == 0) {
+          empty = true;
+          break;
+        }
+      }
+      if (empty) {
+        h->dbeg = h->dend = h->nrows;
+        break;
+      }
+      if (done == K) {
+        h->dbeg = (int64_t)b[K];
+        h->dend = (int64_t)b[K + 1];
+        continue;
+      }
+      // round done + 1 stopped early: re-run it the ordinary way (its driver
+      // is [b[done], b[done + 1]); the rows it appended before stopping are
+      // the start of its delta)
+      if (pass >= max_iterations)
+        return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                   " reached before the fixpoint");
+      const int64_t round_begin = (int64_t)b[done + 1];
+      h->dbeg = (int64_t)b[done];
+      h->dend = round_begin;
+      begin_round(h);
+      for (RulePlan& p : s.variants) XL_TRY(eval_plan(p));
+      ++pass;
+      st->iterations++;
+      const int64_t d = h->nrows - round_begin;
+      record(d);
+      st->new_tuples_total += d;
+      h->dbeg = round_begin;
+      h->dend = h->nrows;
+    }
+    return XL_OK;
+  }
+
   bool batched_gather(const Stratum& s) {
     return c->batched_rounds > 0 && heads.size() == 1 && heads[0]->gathered && heads[0]->gather_ready &&
            s.variants.size() == 1 && s.variants[0].driver_delta && head_of(s.variants[0].head) == heads[0].get();
@@ -2338,6 +2484,10 @@ struct Runner {
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
+    if (batch_range && p.driver_delta) {  // batched set rounds: the delta range is on the device
+      for (int j = 0; j < h->nkey; ++j) src.col[j] = h->rows[j].as<uint32_t>();
+      src.n = h->rows_cap;  // bounds the grid only
+    }
     if (src.n == 0) return XL_OK;
     std::vector<MicroOp> pops;
     std::vector<uint32_t> pconsts;
@@ -2464,6 +2614,22 @@ struct Runner {
       // set / min / max: single pass with insert-or-improve, retried after growth
       for (int attempt = 0;; ++attempt) {
         if (attempt > 8) return c->fail(XL_DEVICE_ERROR, "hash table growth did not converge");
+        if (batch_range) {
+          // batched set rounds: the driver range, the append base, the load
+          // limit and the counters belong to the batch; nothing is read back
+          a.src_range = batch_range;
+          a.emit.counters = batch_counters;
+          a.emit.limit = batch_limit;
+          a.emit.mask = (u64)h->cap - 1;
+          a.emit.mode = EM_SET;
+          a.emit.table = h->table.as<u64>();
+          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
+          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
+          a.emit.row_base = batch_row_base;
+          a.emit.row_cap = h->rows_cap;
+          HIP_TRY(c, k::stage_launch(a, c->stream, batch_grid));
+          break;
+        }
         if (nst == 0 || ks == 0) {  // the driver may live in this head's row list
           Source s2 = resolve_driver(p);
           for (int j = 0; j < a.src.ncols && ks == 0; ++j) a.src.col[j] = s2.col[j];
@@ -3088,6 +3254,10 @@ struct Runner {
     }
     if (s.recursive && total > 0 && batched_gather(s)) {
       XL_TRY(run_gather_batched(s.variants[0], heads[0].get(), max_iterations));
+      total = 0;
+    }
+    if (s.recursive && total > 0 && batched_sets(s)) {
+      XL_TRY(run_sets_batched(s, heads[0].get(), max_iterations));
       total = 0;
     }
     if (s.recursive && total > 0 && resident_frontier(s)) {

@@ -83,6 +83,9 @@ hipError_t compact_u32(const uint32_t* src, const uint32_t* flag, const uint32_t
                        uint32_t* dst, int64_t n, hipStream_t s);
 
 // ---- join / project / emit stage ----
+// Batched set rounds (see the kernels' comment): bnd holds n entries.
+hipError_t batch_init(u64* bnd, int n, u64 b0, u64 b1, hipStream_t s);
+hipError_t batch_mark(u64* bnd, int j, const u64* counters, u64 base, hipStream_t s);
 hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap);
 
 // ---- hash tables ----

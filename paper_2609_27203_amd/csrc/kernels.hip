@@ -1405,7 +1405,12 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DMIN;
   __shared__ uint32_t s_out[STAGED ? ST_WAVES : 1][2][STAGED ? OUTB : 1];
   const int lane = lane_id(), w = threadIdx.x >> 6;
-  const int64_t nchunks = (a.src.n + 63) / 64;
+  int64_t src_n = a.src.n, src_base = 0;
+  if (a.src_range) {  // batched rounds: the round's delta range lives on the device
+    src_base = (int64_t)a.src_range[0];
+    src_n = a.emit.counters[CNT_OVERFLOW] ? 0 : (int64_t)a.src_range[1] - src_base;
+  }
+  const int64_t nchunks = (src_n + 63) / 64;
   const int64_t nwaves = (int64_t)gridDim.x * ST_WAVES;
   EmitState st;
   st.stop = false;
@@ -1426,8 +1431,8 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     st.out_base = (MODE == EM_MAT) ? a.emit.chunk_off[chunk] + (u64)a.emit.mat_base : 0;
     const int64_t row = chunk * 64 + lane;
     Regs v = (Regs)(0u);
-    bool ok = row < a.src.n;
-    if (ok) ok = bind_cols(a.src, row, v);
+    bool ok = row < src_n;
+    if (ok) ok = bind_cols(a.src, src_base + row, v);
     if (HAS_INDEX) {
       uint32_t beg = 0, deg = 0, beg2 = 0, deg2 = 1;
       if (ok) {
@@ -1453,6 +1458,8 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
           // 2^24 products is refused (the host then runs the two steps apart)
           if ((u64)deg * deg2 >= (1u << 24)) {
             atomicOr(&a.emit.counters[CNT_FATAL], 16ull);
+            // batched rounds stop here, so the host re-runs this round apart
+            if (a.src_range) atomicOr(&a.emit.counters[CNT_OVERFLOW], 1ull);
             deg = 0;
           } else {
             deg *= deg2;
@@ -1549,6 +1556,26 @@ static void launch_mode(const StageArgs& a, unsigned grid, hipStream_t s) {
     case 2: launch_ops<MODE, 2>(a, grid, s); break;
     default: launch_ops<MODE, 1>(a, grid, s); break;
   }
+}
+
+// Batched rounds of a set head over its append-only row list: bnd[j] is the
+// row count after round j - 1 of the batch (bnd[0], bnd[1] bound the first
+// round's delta, later entries start as ~0).  After round j's launches,
+// bnd[j + 1] = base + rows appended in the batch so far, unless a launch of
+// the batch overflowed (the entry then stays ~0 and the host re-runs round j).
+__global__ void batch_init_k(u64* bnd, int n, u64 b0, u64 b1) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) bnd[i] = i == 0 ? b0 : i == 1 ? b1 : ~0ull;
+}
+__global__ void batch_mark_k(u64* bnd, int j, const u64* counters, u64 base) {
+  if (threadIdx.x == 0 && !counters[CNT_OVERFLOW]) bnd[j + 1] = base + counters[CNT_APPENDED];
+}
+hipError_t batch_init(u64* bnd, int n, u64 b0, u64 b1, hipStream_t s) {
+  batch_init_k<<<1, 256, 0, s>>>(bnd, n, b0, b1);
+  return hipGetLastError();
+}
+hipError_t batch_mark(u64* bnd, int j, const u64* counters, u64 base, hipStream_t s) {
+  batch_mark_k<<<1, 64, 0, s>>>(bnd, j, counters, base);
+  return hipGetLastError();
 }
 
 hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {

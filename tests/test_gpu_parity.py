@@ -438,6 +438,53 @@ def test_subtraction_rules_match_oracle(name, index_mode):
     assert stats["derived_tuples"] == sum(len(r[1][0]) for r in ref.relations.values())
 
 
+@pytest.mark.parametrize("growth", [False, True])
+@pytest.mark.parametrize("batch", [1, 4, 64])
+@pytest.mark.parametrize("name", ["tc_uniform", "tc_rmat_count", "same_generation"])
+def test_hash_set_rounds_batched(name, batch, growth):
+    """Set heads held in hash tables (index mode 1) run batch rounds per host
+    read, with the delta range on the device; with a tiny initial table the
+    batches overflow and the host re-runs the round that stopped.  Rows,
+    per-pass delta sizes and pass counts equal the round-by-round loop's."""
+    wl = W.small_workloads()[name]()
+    print(f"case: batched hash set rounds {name} batch={batch} growth={growth}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    opts = {"index_mode": 1, "batched_rounds": batch}
+    if growth:
+        opts["hash_min_log2"] = 10
+    rels, stats, _ = engine_run(wl, options=opts)
+    _compare(wl, rels, ref)
+    base = engine_run(wl, options={"index_mode": 1, "batched_rounds": 0})[1]
+    assert stats["delta_rows"] == base["delta_rows"] and stats["iterations"] == base["iterations"]
+    if growth:
+        assert stats["table_grows"] > 0
+
+
+@pytest.mark.parametrize("batch", [0, 4, 64])
+def test_hash_set_rounds_cap_and_round_count(batch):
+    """A chain of n nodes closes in n - 1 passes: the iteration cap ends the
+    run with XL_CONVERGENCE_FAILURE at the same pass batched or not, and with
+    64 rounds per read the control bytes read do not grow with the number of
+    rounds (chains of 20 and 50 nodes)."""
+    from paper_2609_27203_amd import xlh
+    reads = {}
+    for n in (20, 50):
+        src = np.arange(n - 1, dtype=np.int32)
+        wl = W.Workload(f"chain{n}", W.TC_RULES, _edges(src, src + 1), {"path": ("i32", "i32")})
+        print(f"case: hash chain n={n} batch={batch}", flush=True)
+        opts = {"index_mode": 1, "batched_rounds": batch}
+        rels, stats, _ = engine_run(wl, options=opts, workspace_bytes=256 << 20)
+        assert len(rels["path"][0]) == n * (n - 1) // 2
+        assert stats["iterations"] == n - 1 and stats["delta_rows"] == list(range(n - 1, -1, -1))
+        reads[n] = stats["control_bytes_read"]
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, options=opts, max_iterations=n - 2, workspace_bytes=256 << 20)
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+        engine_run(wl, options=opts, max_iterations=n - 1, workspace_bytes=256 << 20)
+    if batch == 64:
+        assert reads[20] == reads[50]
+
+
 @pytest.mark.parametrize("batch", [0, 1, 4, 64])
 @pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
 def test_min_rounds_tiled_and_untiled(tiles, batch):
