@@ -227,13 +227,15 @@ xl_status xl_context_create_static(int device, void* hip_stream, xl_context** ou
  *                     device array read once per batch; rounds past the
  *                     fixpoint change nothing (default 4; 0 = one round and
  *                     two host reads per pass; at most 64)
- *   "gather_rounds"   1 = a recursive rule h(X,Y) :- e1(X,A), h(A,B), e2(Y,B)
+ *   "gather_rounds"   a recursive rule h(X,Y) :- e1(X,A), h(A,B), e2(Y,B)
  *                     with nothing else (same generation's shape) over a dense
- *                     set head runs gathered rounds: one workgroup per head
- *                     row X stages it in LDS and sets there the Y values of
- *                     e2 for the B bits of the delta rows of X's A values,
- *                     writing back only changed words (default); 0 = the
- *                     generic join of each delta tuple
+ *                     set head runs gathered rounds: 1 = one workgroup per
+ *                     delta row A builds the Y values of e2 for its B bits
+ *                     once in LDS and ORs their nonzero words into the head
+ *                     rows of A's X values (default); 2 = one workgroup per
+ *                     head row X stages it in LDS and sets there the Y values
+ *                     for the delta rows of its A values, writing back only
+ *                     changed words; 0 = the generic join of each delta tuple
  *   "product_joins"   1 = a rule whose two join steps are both keyed by
  *                     variables of the driver row (into a set head) runs as
  *                     one launch over the product of the two match lists

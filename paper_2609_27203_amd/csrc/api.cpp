@@ -128,7 +128,7 @@ xl_status xl_context_set_option(xl_context* c, const char* key, int64_t value) {
     return XL_OK;
   }
   if (!strcmp(key, "gather_rounds")) {
-    if (value != 0 && value != 1) return c->fail(XL_INVALID_ARGUMENT, "gather_rounds must be 0 or 1");
+    if (value < 0 || value > 2) return c->fail(XL_INVALID_ARGUMENT, "gather_rounds must be 0, 1 or 2");
     c->gather_rounds = (int)value;
     return XL_OK;
   }

@@ -332,6 +332,17 @@ struct GatherArgs {
   uint32_t row_words;
   int64_t range0;
   unsigned long long* counters;  // CNT_CANDIDATES, CNT_APPENDED
+  // by_a: one workgroup per flagged delta row A instead of per head row X;
+  // e1a is e1 indexed by its A column, e1_xcol the column holding X.  Every
+  // delta row r keeps word bounds: its bits lie in words [lo[r], hi[r])
+  // (empty: lo = row_words, hi = 0); the next round's bounds only widen.
+  int32_t by_a;
+  IndexProbe e1a;
+  int32_t e1_xcol;
+  const uint32_t* in_lo;
+  const uint32_t* in_hi;
+  uint32_t* out_lo;
+  uint32_t* out_hi;
 };
 
 

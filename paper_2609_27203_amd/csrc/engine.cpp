@@ -583,6 +583,7 @@ struct HeadRun {
   bool gathered = false;
   bool gather_ready = false;
   Buf gbits, gflag[2];
+  Buf gbound[2];  // word bounds of the delta rows of dbits / gbits: lo[range0] then hi[range0]
   int gcur = 0;
   Buf hasin;                    // Y values with an in-edge (pull direction)
   int fcur = 0;
@@ -1177,6 +1178,9 @@ struct Runner {
       for (int b = 0; b < 2; ++b) {
         XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->gflag[b], "delta row flags"));
         HIP_TRY(c, hipMemsetAsync(h->gflag[b].p, 0, (size_t)std::max<int64_t>(h->range0, 1) * 4, c->stream));
+        XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 8, &h->gbound[b], "delta row bounds"));
+        HIP_TRY(c, k::fill_bounds(h->gbound[b].as<uint32_t>(), h->gbound[b].as<uint32_t>() + h->range0, h->range0,
+                                  (uint32_t)h->row_words, 0u, c->stream));
       }
     }
     if (h->frontier && !h->resident) {
@@ -1498,6 +1502,15 @@ struct Runner {
     a.bits = h->bits.as<uint32_t>();
     XL_TRY(get_index(p.steps[g.s1].rel, g.x_col, &a.e1, -1, nullptr, 0, true));
     a.e1_acol = p.steps[g.s1].key_col;
+    a.by_a = c->gather_rounds == 1;
+    if (a.by_a) {
+      XL_TRY(get_index(p.steps[g.s1].rel, a.e1_acol, &a.e1a, -1, nullptr, 0, true));
+      a.e1_xcol = g.x_col;
+      a.in_lo = h->gbound[h->gcur].as<uint32_t>();
+      a.in_hi = a.in_lo + h->range0;
+      a.out_lo = h->gbound[h->gcur ^ 1].as<uint32_t>();
+      a.out_hi = a.out_lo + h->range0;
+    }
     XL_TRY(get_index(p.steps[g.s2].rel, p.steps[g.s2].key_col, &a.push.idx, -1, nullptr, 0, true));
     a.push.ybind_col = g.y_col;
     a.lo0 = a.push.lo0 = h->kp.lo[0];
@@ -1518,7 +1531,8 @@ struct Runner {
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
     // the consumed delta becomes the next round's output buffer
     HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(), h->gflag[h->gcur].as<uint32_t>(),
-                                     h->range0, h->row_words, c->stream));
+                                     h->range0, h->row_words, a.by_a ? h->gbound[h->gcur].as<uint32_t>() : nullptr,
+                                     a.by_a ? h->gbound[h->gcur].as<uint32_t>() + h->range0 : nullptr, c->stream));
     u64 cnt[CNT_N];
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
     cands += (int64_t)cnt[CNT_CANDIDATES];
@@ -1940,7 +1954,10 @@ struct Runner {
         HIP_TRY(c, k::gather_round(a, c->stream));
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
         HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(),
-                                         h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words, c->stream));
+                                         h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words,
+                                         a.by_a ? h->gbound[h->gcur].as<uint32_t>() : nullptr,
+                                         a.by_a ? h->gbound[h->gcur].as<uint32_t>() + h->range0 : nullptr,
+                                         c->stream));
         h->gcur ^= 1;
       }
       std::vector<u64> cnt((size_t)nb * CNT_N);  // at most 64 blocks of 64 B: one control read
@@ -2774,9 +2791,13 @@ struct Runner {
       if (h->gathered) {  // seed round: its new tuples in dbits are the first delta rows
         h->gather_ready = true;
         h->gcur = 0;
-        if (h->round_new)
+        if (h->round_new) {
           HIP_TRY(c, k::row_popcount(h->dbits.as<uint32_t>(), h->range0, h->row_words, h->gflag[0].as<uint32_t>(),
                                      c->stream));
+          // the seed's delta rows may hold bits anywhere
+          HIP_TRY(c, k::fill_bounds(h->gbound[0].as<uint32_t>(), h->gbound[0].as<uint32_t>() + h->range0, h->range0,
+                                    0u, (uint32_t)h->row_words, c->stream));
+        }
         return XL_OK;
       }
       if (h->resident) {  // the resident launch reads the seed's delta rows from dbits

@@ -110,7 +110,8 @@ struct Context {
   int wcoj_shorter = 1;       // triangle joins: 1 probe the shorter list, 0 always b's (binary-join order)
   int product_joins = 1;      // two driver-keyed index steps in one launch (0: materialize between them)
   int batched_rounds = 4;     // tiled min/max strata: rounds per host read (0: one round at a time)
-  int gather_rounds = 1;      // h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B): 1 gathered rounds, 0 generic
+  int gather_rounds = 1;      // h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B): gathered rounds, 1 one
+                              // workgroup per delta row A, 2 per head row X; 0 the generic join
   int dense_tiles = 0;  // tiled min/max rounds: 0 auto, k tiles per rank, -1 off
   int64_t control_bytes = 0;
   uint64_t generations = 0;      // source of Relation::generation values

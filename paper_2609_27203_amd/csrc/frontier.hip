@@ -516,26 +516,221 @@ __global__ __launch_bounds__(FR_THREADS) void gather_round_k(GatherArgs g) {
   }
 }
 
-hipError_t gather_round(const GatherArgs& a, hipStream_t s) {
-  if (a.range0 <= 0) return hipSuccess;
-  const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 2048);
-  gather_round_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
-  return hipGetLastError();
-}
-
-__global__ void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words) {
-  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
-    if (!flag[r]) continue;  // (uniform)
-    uint32_t* row = bits + (u64)r * row_words;
-    for (uint32_t i = threadIdx.x; i < row_words; i += blockDim.x) row[i] = 0u;
-    __syncthreads();  // every thread has read the flag before it is cleared
-    if (threadIdx.x == 0) flag[r] = 0u;
+// Gathered round by delta row (GatherArgs::by_a).  Every X that e1 pairs
+// with A receives the same Y values from A's delta row: the union U(A) of
+// e2's Y lists over the B bits of the delta row (words [in_lo, in_hi) only)
+// is built once in LDS with the wave-balanced push expansion of the frontier
+// kernels, its nonzero words are listed in order, and each such word is ORed
+// into the head row of every X of A with one device atomic whose old value
+// gives the bits new to X; those go to X's next delta row (several A may reach
+// one X, so that is an atomic too), raise X's flag and widen its word bounds.
+// The work is the words the round touches, not whole rows.
+__global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
+  extern __shared__ uint32_t lds[];
+  const uint32_t W = g.row_words;
+  uint32_t* U = lds;       // union of this A's Y values: zero between delta rows
+  uint32_t* tw = lds + W;  // indexes of U's nonzero words, ascending
+  __shared__ FrontierShared L;
+  __shared__ uint32_t s_umin, s_umax;
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  u64 cands = 0, fresh = 0;
+  const FrontierArgs& a = g.push;
+  const uint32_t* ycol = a.idx.col[a.ybind_col];
+  const uint32_t* xcol = g.e1a.col[g.e1_xcol];
+  uint32_t* zlist = L.zlist;
+  auto& s_excl = L.s_excl;
+  auto& s_beg = L.s_beg;
+  for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) U[i] = 0u;
+  if (threadIdx.x == 0) {
+    s_umin = 0xffffffffu;
+    s_umax = 0u;
+  }
+  __syncthreads();
+  for (int64_t ar64 = blockIdx.x; ar64 < g.range0; ar64 += gridDim.x) {
+    const uint32_t ar = (uint32_t)ar64;
+    if (!g.in_flag[ar]) continue;  // (uniform: no delta row)
+    const uint32_t kk = (uint32_t)g.lo0 + ar - (uint32_t)g.e1a.key_lo;
+    uint32_t b1 = 0, n1 = 0;
+    if (kk < g.e1a.key_range) {
+      b1 = g.e1a.off[kk];
+      n1 = g.e1a.off[kk + 1] - b1;
+    }
+    if (n1 == 0) continue;  // (uniform: no X pairs with A)
+    const uint32_t* frow = g.in_bits + (u64)ar * W;
+    const uint32_t we = min(g.in_hi[ar], W);
+    uint32_t umin = 0xffffffffu, umax = 0u;  // this lane's words of U touched
+    for (uint32_t cb = g.in_lo[ar]; cb < we;) {
+      // decode words [cb, cb + 512) of the delta row, two per thread, cut so
+      // the B list holds at most FR_ZCAP values
+      const uint32_t w0 = cb + 2u * threadIdx.x;
+      const uint32_t d0 = w0 < we ? frow[w0] : 0u, d1 = w0 + 1 < we ? frow[w0 + 1] : 0u;
+      const uint32_t c = __popc(d0) + __popc(d1);
+      uint32_t tot;
+      uint32_t pos = block_excl_scan_u32(c, &tot, L.s_w);
+      if (pos + c <= FR_ZCAP) {
+        for (uint32_t bits = d0; bits; bits &= bits - 1)
+          zlist[pos++] = (uint32_t)a.lo1 + w0 * 32u + (uint32_t)(__ffs(bits) - 1);
+        for (uint32_t bits = d1; bits; bits &= bits - 1)
+          zlist[pos++] = (uint32_t)a.lo1 + (w0 + 1) * 32u + (uint32_t)(__ffs(bits) - 1);
+      } else if (pos <= FR_ZCAP) {
+        L.s_cut[0] = pos;
+        L.s_cut[1] = 2u * threadIdx.x;
+      }
+      __syncthreads();
+      const uint32_t nz = tot <= FR_ZCAP ? tot : L.s_cut[0];
+      cb += tot <= FR_ZCAP ? 2u * FR_THREADS : L.s_cut[1];
+      // each B's Y list: rows of 64 or more by the whole wavefront, smaller
+      // ones through a scan and a six-step owner search
+      for (uint32_t j0 = 0; j0 < nz; j0 += FR_WAVES * 64) {
+        const uint32_t r = j0 + (uint32_t)lane * FR_WAVES + (uint32_t)w;
+        uint32_t beg = 0, deg = 0;
+        if (r < nz) {
+          const uint32_t k2 = zlist[r] - (uint32_t)a.idx.key_lo;
+          if (k2 < a.idx.key_range) {
+            beg = a.idx.off[k2];
+            deg = a.idx.off[k2 + 1] - beg;
+          }
+        }
+        const bool big = deg >= 64;
+        u64 bigm = __ballot(big);
+        const uint32_t sdeg = big ? 0u : deg;
+        const uint32_t incl = wave_incl_scan(sdeg);
+        const uint32_t total = __shfl(incl, 63, 64);
+        s_excl[w][lane] = incl - sdeg;
+        s_beg[w][lane] = beg;
+        wave_lds_sync();
+        if (lane == 0) cands += total;
+        while (bigm) {
+          const int rb = __ffsll((long long)bigm) - 1;
+          bigm &= bigm - 1;
+          const uint32_t bb = __shfl(beg, rb, 64), bd = __shfl(deg, rb, 64);
+          if (lane == 0) cands += bd;
+          for (uint32_t k = lane; k < bd; k += 64) {
+            const uint32_t y = ycol[bb + k] - (uint32_t)a.lo1;
+            const uint32_t bit = 1u << (y & 31);
+            umin = min(umin, y >> 5);
+            umax = max(umax, y >> 5);
+            if (!(U[y >> 5] & bit)) atomicOr(&U[y >> 5], bit);
+          }
+        }
+        for (uint32_t b0 = 0; b0 < total; b0 += 64) {
+          const uint32_t j = b0 + lane;
+          if (j < total) {
+            int q = 0;
+#pragma unroll
+            for (int step = 32; step > 0; step >>= 1)
+              if (s_excl[w][q + step] <= j) q += step;
+            const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
+            const uint32_t bit = 1u << (y & 31);
+            umin = min(umin, y >> 5);
+            umax = max(umax, y >> 5);
+            if (!(U[y >> 5] & bit)) atomicOr(&U[y >> 5], bit);
+          }
+        }
+        wave_lds_sync();
+      }
+      __syncthreads();
+    }
+    if (umin <= umax) {
+      atomicMin(&s_umin, umin);
+      atomicMax(&s_umax, umax);
+    }
+    __syncthreads();
+    // U's nonzero words, in order, within the touched range
+    const uint32_t lo = s_umin, hi = s_umin <= s_umax ? min(s_umax + 1u, W) : s_umin;
+    const uint32_t span = hi > lo ? hi - lo : 0u;
+    const uint32_t per = (span + FR_THREADS - 1) / FR_THREADS;
+    const uint32_t p0 = lo + threadIdx.x * per, p1 = min(hi, p0 + per);
+    uint32_t cnt = 0;
+    for (uint32_t i = p0; i < p1; ++i) cnt += U[i] != 0u;
+    uint32_t nt;
+    uint32_t pos = block_excl_scan_u32(cnt, &nt, L.s_w);
+    for (uint32_t i = p0; i < p1; ++i)
+      if (U[i]) tw[pos++] = i;
+    __syncthreads();
+    uint32_t nb = 0;
+    const uint32_t total = n1 * nt;  // below 2^32: X values times row words
+    for (uint32_t p = threadIdx.x; p < total; p += FR_THREADS) {
+      const uint32_t q = p / nt, k = p - q * nt, wi = tw[k];
+      const uint32_t xr = xcol[b1 + q] - (uint32_t)g.lo0;
+      if ((int64_t)xr >= g.range0) continue;  // outside the head's rows (not planned)
+      if (k == 0) {  // X's next delta row may get bits in these words
+        atomicMin(&g.out_lo[xr], tw[0]);
+        atomicMax(&g.out_hi[xr], tw[nt - 1] + 1u);
+      }
+      const uint32_t u = U[wi];
+      const u64 at = (u64)xr * W + wi;
+      const uint32_t nw = u & ~atomicOr(g.bits + at, u);
+      if (nw) {
+        atomicOr(g.out_bits + at, nw);
+        g.out_flag[xr] = 1u;
+        nb += (uint32_t)__popc(nw);
+      }
+    }
+    fresh += nb;
+    __syncthreads();  // every word of U is read before it is cleared
+    for (uint32_t i = threadIdx.x; i < nt; i += FR_THREADS) U[tw[i]] = 0u;
+    if (threadIdx.x == 0) {
+      s_umin = 0xffffffffu;
+      s_umax = 0u;
+    }
+    __syncthreads();
+  }
+  const u64 c = wave_incl_scan_t<u64>(cands), fr = wave_incl_scan_t<u64>(fresh);
+  if (lane == 63) {
+    if (c) atomicAdd(&g.counters[CNT_CANDIDATES], c);
+    if (fr) atomicAdd(&g.counters[CNT_APPENDED], fr);
   }
 }
 
-hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, hipStream_t s) {
+hipError_t gather_round(const GatherArgs& a, hipStream_t s) {
+  if (a.range0 <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 2048);
+  if (a.by_a)
+    gather_by_a_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
+  else
+    gather_round_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
+  return hipGetLastError();
+}
+
+// Empty the flagged rows (only their words [lo, hi) when bounds are kept,
+// which are then reset to empty) and their flags.
+__global__ void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words,
+                                     uint32_t* lo, uint32_t* hi) {
+  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    if (!flag[r]) continue;  // (uniform)
+    uint32_t* row = bits + (u64)r * row_words;
+    const uint32_t b = lo ? lo[r] : 0u, e = lo ? min(hi[r], row_words) : row_words;
+    for (uint32_t i = b + threadIdx.x; i < e; i += blockDim.x) row[i] = 0u;
+    __syncthreads();  // every thread has read the flag and bounds before they are reset
+    if (threadIdx.x == 0) {
+      flag[r] = 0u;
+      if (lo) {
+        lo[r] = row_words;
+        hi[r] = 0u;
+      }
+    }
+  }
+}
+
+hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, uint32_t* lo,
+                              uint32_t* hi, hipStream_t s) {
   if (nrows <= 0) return hipSuccess;
-  clear_flagged_rows_k<<<(unsigned)std::min<int64_t>(nrows, 4096), 256, 0, s>>>(bits, flag, nrows, row_words);
+  clear_flagged_rows_k<<<(unsigned)std::min<int64_t>(nrows, 4096), 256, 0, s>>>(bits, flag, nrows, row_words, lo,
+                                                                                hi);
+  return hipGetLastError();
+}
+
+// lo[r] = vlo, hi[r] = vhi for every row.
+__global__ void fill_bounds_k(uint32_t* lo, uint32_t* hi, int64_t n, uint32_t vlo, uint32_t vhi) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+    lo[r] = vlo;
+    hi[r] = vhi;
+  }
+}
+hipError_t fill_bounds(uint32_t* lo, uint32_t* hi, int64_t n, uint32_t vlo, uint32_t vhi, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  fill_bounds_k<<<grid_for(n, 256, 4096), 256, 0, s>>>(lo, hi, n, vlo, vhi);
   return hipGetLastError();
 }
 

@@ -135,7 +135,10 @@ hipError_t frontier_resident(const FrontierArgs& a, unsigned grid, hipStream_t s
 // One gathered round (see GatherArgs).
 hipError_t gather_round(const GatherArgs& a, hipStream_t s);
 // Zero the flagged rows of a [nrows][row_words] bitmap and their flags.
-hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, hipStream_t s);
+hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, uint32_t* lo,
+                              uint32_t* hi, hipStream_t s);
+// lo[r] = vlo, hi[r] = vhi for r < n (word bounds of delta rows).
+hipError_t fill_bounds(uint32_t* lo, uint32_t* hi, int64_t n, uint32_t vlo, uint32_t vhi, hipStream_t s);
 hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s);
 hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
                         hipStream_t s);

@@ -812,13 +812,15 @@ def _gather_workload(variant):
     return W.Workload(variant, rules, edb, {"h": ("i32", "i32")}), "h"
 
 
-@pytest.mark.parametrize("gather,batch", [(0, 4), (1, 0), (1, 1), (1, 4), (1, 64)])
+@pytest.mark.parametrize("gather,batch", [(0, 4), (1, 0), (1, 1), (1, 4), (1, 64), (2, 0), (2, 4)])
 @pytest.mark.parametrize("variant", ["sg", "sg_reordered", "dag", "dag_swapped", "func"])
 def test_gathered_rounds(variant, gather, batch):
-    """h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) in gathered rounds (head row
-    X staged in LDS, the Y values of the B bits of its A values' delta rows
-    set there; one round or 1, 4 or 64 rounds per host read) and in the
-    generic join: the oracle's rows and per-round delta sizes either way,
+    """h(X,Y) :- e1(X,A), delta h(A,B), e2(Y,B) in gathered rounds (1: per
+    delta row A, the union of its Y values ORed into the rows of A's X
+    values; 2: head row X staged in LDS, the Y values of the B bits of its A
+    values' delta rows set there; one round or 1, 4 or 64 rounds per host
+    read) and in the generic join: the oracle's rows and per-round delta
+    sizes either way,
     also over random graphs where an X has many A (several
     delta rows per head row, one delta row read for many X), where e1 is a
     random function (one A per X, cycles), and with the columns and atoms in
