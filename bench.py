@@ -66,7 +66,7 @@ KERNEL = {
     "front": "frontier_resident_k",
     "emit": "dense_min_tile_k",
     "pull": "dense_pull_k",
-    "gather": "gather_round_k",
+    "gather": "gather_by_a_k",
     "wcoj": "wcoj_probe_k",
 }
 KERNEL_DOC = {
@@ -75,8 +75,9 @@ KERNEL_DOC = {
     "emit": "dense_min_tile_k (one workgroup per source and tile of targets, the tile's values in LDS: "
             "delta rows expanded through the (tile, Z) index, min folded in LDS)",
     "pull": "dense_pull_k (fold of each marked key's in-edges against the delta, keys ordered by target)",
-    "gather": "gather_round_k (per head row X staged in LDS: the delta rows of X's A values pushed "
-              "through e2, test-and-set in LDS, changed words written back)",
+    "gather": "gather_by_a_k (one workgroup per delta row A: the union of e2's Y lists over A's B bits "
+              "built once in LDS, its nonzero words ORed into the head rows of A's X values with device "
+              "atomics whose old values give the next delta words)",
     "wcoj": "wcoj_probe_k (count and materialize passes: each driver row's shorter Z list probed into "
             "the longer)",
 }
