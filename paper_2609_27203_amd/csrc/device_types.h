@@ -101,6 +101,8 @@ enum EmitMode : int32_t {
   EM_DMIN = 6,    // atomic improvement in a dense value array over (dictionary rank of
                   // the first key) x (second key); improved slots to delta
   EM_MARK = 7,    // set the bit of the same dense slot (keys that receive a contribution)
+  EM_HAGG = 8,    // sum/logsumexp contributions of a round folded per key in a keyed table's
+                  // accumulator array (acc[slot]); the slots touched in the round to delta
 };
 
 // Device-side counters of one emission (cleared per round).
@@ -147,10 +149,20 @@ struct EmitSpec {
   // EM_DCOUNT: counter of the same index, with row_bits = the second key's range
   uint32_t* bits;
   unsigned long long row_bits;
-  // EM_MINMAX
+  // EM_MINMAX / EM_HAGG
   Slot16* table16;
   uint32_t round;
-  uint32_t* delta_idx;       // EM_MINMAX / EM_DMIN: improved slots of this round
+  uint32_t* delta_idx;       // EM_MINMAX / EM_DMIN: improved slots of this round; EM_HAGG: touched slots
+  // EM_MINMAX / EM_DMIN / EM_HAGG: delta_idx positions from delta_lim on are
+  // not written and the launch overflows (0: no limit)
+  unsigned long long delta_lim;
+  // EM_HAGG: one accumulator per table slot, at the fold's identity between
+  // rounds (integer sum: the low 32 bits; f32 sum: an f64 sum; logsumexp:
+  // an f64 log-sum); a key inserted in the round takes agg_identity as its
+  // full-relation value until the round's end merges the accumulator
+  unsigned long long* acc;
+  int32_t fold_kind;
+  uint32_t agg_identity;
   // EM_DMIN: slot = dmap[k0 - lo0] * row_bits + (k1 - lo1) of the value array
   // `bits`; dpres marks slots holding a value, dchg slots already listed in
   // this round's delta.

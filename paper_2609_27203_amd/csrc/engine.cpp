@@ -1355,6 +1355,18 @@ struct Runner {
     u64 cnt[CNT_N];
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
     if (cnt[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "hash table rebuild failed");
+    if (h->is_minmax && h->didx_n > 0) {
+      // the slots listed for the current round moved: list the slots stamped
+      // with the round again (in slot order)
+      Buf tmp, tot;
+      XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
+      XL_TRY(dalloc(c, 8, &tot, "count"));
+      HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(), h->cap,
+                                    tot.as<uint32_t>(), tmp.p, c->stream));
+      uint32_t n2 = 0;
+      XL_TRY(ctl_read(c, tot.p, 4, &n2));
+      h->didx_n = (int64_t)n2;
+    }
     return XL_OK;
   }
 
@@ -1789,6 +1801,16 @@ struct Runner {
   u64* batch_counters = nullptr;
   u64 batch_row_base = 0, batch_limit = 0;
   int batch_grid = EMIT_GRID;  // workgroups of a batched launch (its waves bound the slack)
+  // batched keyed value rounds: the batch's delta rows and slot list (one
+  // position space: the first delta at [0, base), each round's slots and rows
+  // after it), its capacity past the base, the round's stamp and the
+  // accumulators of hashed folds
+  uint32_t* batch_rows[3] = {nullptr, nullptr, nullptr};
+  int64_t batch_rows_cap = 0;
+  uint32_t* batch_idx = nullptr;
+  u64 batch_delta_lim = 0;
+  uint32_t batch_round = 0;
+  u64* batch_acc = nullptr;
 
   bool batched_sets(const Stratum& s) {
     if (c->batched_rounds <= 0 || heads.size() != 1 || s.variants.empty()) return false;
@@ -1913,6 +1935,208 @@ struct Runner {
       st->new_tuples_total += d;
       h->dbeg = round_begin;
       h->dend = h->nrows;
+    }
+    return XL_OK;
+  }
+
+  // Batched rounds of a min/max or sum/logsumexp head held in a keyed hash
+  // table (index mode 1, or key domains too wide for the dense forms): the
+  // stratum's delta variants each run in one stage launch and join only
+  // relations outside the stratum.  Min/max candidates improve table values
+  // (EM_MINMAX); sum/logsumexp candidates fold into one accumulator per slot
+  // (EM_HAGG).  Either way the slots a round touches are listed once (round
+  // stamps) after the batch's earlier rounds, and a range kernel turns them
+  // into the next delta rows at the same positions (for hashed folds it also
+  // merges the round into the full relation and resets the accumulators),
+  // so every size stays on the device until the batch's one read.
+  bool batched_values(const Stratum& s) {
+    if (c->batched_rounds <= 0 || heads.size() != 1 || s.variants.empty()) return false;
+    HeadRun* h = heads[0].get();
+    if (h->is_set || h->dense || h->dv || h->ds || h->tiled || h->frontier || h->gathered || h->dcount) return false;
+    const int vt = h->rel->types[h->nkey];
+    const bool hashed = h->is_sortagg && (h->fold == k::FOLD_SUM || h->fold == k::FOLD_LSE) &&
+                        (vt == T_I32 || vt == T_F32);
+    if (!h->is_minmax && !hashed) return false;
+    for (const RulePlan& p : s.variants) {
+      if (!p.driver_delta || p.driver != h->rel || p.wcoj || head_of(p.head) != h) return false;
+      for (const StepPlan& sp : p.steps)
+        if (head_of(sp.rel)) return false;
+      if (p.steps.size() > 2) return false;
+      if (p.steps.size() == 2) {
+        std::vector<MicroOp> pops;
+        std::vector<uint32_t> pconsts;
+        if (!c->product_joins || !product_plan(p, h, &pops, &pconsts)) return false;
+      }
+    }
+    return true;
+  }
+
+  // Copy n delta rows (key columns and value) from position `from` of the
+  // columns src into the head's delta rows.
+  xl_status take_delta_rows(HeadRun* h, uint32_t* const* src, int64_t from, int64_t n) {
+    XL_TRY(ensure_drow(h, std::max<int64_t>(n, 1)));
+    for (int j = 0; j <= h->nkey && n > 0; ++j)
+      HIP_TRY(c, hipMemcpyAsync(h->drow[j].p, src[j] + from, (size_t)n * 4, hipMemcpyDeviceToDevice, c->stream));
+    h->dn = n;
+    return XL_OK;
+  }
+
+  xl_status run_values_batched(Stratum& s, HeadRun* h, int64_t max_iterations) {
+    const int B = c->batched_rounds;
+    const bool hashed = !h->is_minmax;
+    const int vt = h->rel->types[h->nkey];
+    constexpr size_t CNTB = 256;
+    static_assert(8 * CNT_N <= CNTB, "counters fit their block");
+    Buf blk;  // the batch's counters, then the round boundaries
+    XL_TRY(dalloc(c, CNTB + 8 * (size_t)(B + 2), &blk, "batch counters"));
+    u64* counters = blk.as<u64>();
+    u64* bnd = (u64*)((char*)blk.p + CNTB);
+    std::vector<unsigned char> host(CNTB + 8 * (size_t)(B + 2));
+    Buf acc, bidx, brow[3];
+    int64_t acc_cap = 0, bcap = 0;
+    int64_t pass = 0;
+    while (h->dn > 0) {
+      if (pass >= max_iterations)
+        return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                   " reached before the fixpoint");
+      const int64_t waves =
+          std::max<int64_t>(256, std::min<int64_t>((int64_t)EMIT_GRID * 4, h->cap / 4 / WAVE_SLACK)) / 4 * 4;
+      batch_grid = (int)(waves / 4);
+      const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
+      if (h->keys >= max_keys) {
+        XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + WAVE_SLACK * waves + 1024)));
+        continue;
+      }
+      if (hashed && acc_cap != h->cap) {  // accumulators follow the table's slots (all at identity here)
+        acc.reset();
+        XL_TRY(dalloc(c, (size_t)h->cap * 8, &acc, "fold accumulators"));
+        HIP_TRY(c, k::acc_fill(acc.as<u64>(), h->cap, vt, h->fold, c->stream));
+        acc_cap = h->cap;
+      }
+      // a round touches each key at most once: the table's capacity past the
+      // first delta holds a batch of typical rounds; more overflows the batch
+      const int64_t need = h->dn + std::max<int64_t>(h->cap, 4096);
+      if (bcap < need) {
+        bidx.reset();
+        XL_TRY(dalloc(c, (size_t)need * 4, &bidx, "batch delta slots"));
+        for (int j = 0; j <= h->nkey; ++j) {
+          brow[j].reset();
+          XL_TRY(dalloc(c, (size_t)need * 4, &brow[j], "batch delta rows"));
+        }
+        bcap = need;
+      }
+      uint32_t* rows[3] = {brow[0].as<uint32_t>(), h->nkey == 2 ? brow[1].as<uint32_t>() : nullptr,
+                           brow[h->nkey].as<uint32_t>()};
+      uint32_t* cols[3] = {brow[0].as<uint32_t>(), brow[1].as<uint32_t>(), brow[2].as<uint32_t>()};
+      for (int j = 0; j <= h->nkey; ++j)
+        HIP_TRY(c, hipMemcpyAsync(brow[j].p, h->drow[j].p, (size_t)h->dn * 4, hipMemcpyDeviceToDevice, c->stream));
+      const int K = (int)std::min<int64_t>(B, max_iterations - pass);
+      const int64_t dn0 = h->dn;
+      HIP_TRY(c, hipMemsetAsync(counters, 0, CNTB, c->stream));
+      HIP_TRY(c, k::batch_init(bnd, B + 2, 0ull, (u64)dn0, c->stream));
+      batch_counters = counters;
+      batch_row_base = (u64)dn0;
+      batch_limit = (u64)(max_keys - h->keys);
+      for (int j = 0; j <= h->nkey; ++j) batch_rows[j] = brow[j].as<uint32_t>();
+      batch_rows_cap = bcap;
+      batch_idx = bidx.as<uint32_t>();
+      batch_delta_lim = (u64)(bcap - dn0);
+      batch_acc = hashed ? acc.as<u64>() : nullptr;
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
+      for (int j = 1; j <= K; ++j) {
+        batch_range = bnd + (j - 1);
+        batch_round = h->round + (uint32_t)j;
+        for (RulePlan& p : s.variants) {
+          const xl_status e = eval_plan(p);
+          if (e != XL_OK) {
+            batch_range = nullptr;
+            return e;
+          }
+        }
+        HIP_TRY(c, k::batch_mark(bnd, j, counters, (u64)dn0, c->stream));
+        HIP_TRY(c, k::table16_rows_range(h->table.as<Slot16>(), batch_acc, bidx.as<uint32_t>(), bnd, j, bcap,
+                                         h->kp, vt, h->fold, rows[0], rows[1], rows[2], c->stream));
+      }
+      batch_range = nullptr;
+      batch_acc = nullptr;
+      if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+      XL_TRY(ctl_read(c, blk.p, CNTB + 8 * (size_t)(K + 2), host.data()));
+      u64 cnt[CNT_N];
+      memcpy(cnt, host.data(), sizeof(cnt));
+      const u64* b = (const u64*)(host.data() + CNTB);
+      if (cnt[CNT_FATAL] & ~16ull) return stage_fatal(cnt[CNT_FATAL], "hash table probe exhausted (internal)");
+      cands += (int64_t)cnt[CNT_CANDIDATES];
+      if (c->profile) {
+        float ms = 0;
+        HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
+        st->emit_ms += ms;
+        st->emit_launches += (int64_t)K * (int64_t)s.variants.size();
+        st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
+        st->emit_new += (int64_t)cnt[CNT_INSERTED];
+      }
+      h->keys += (int64_t)cnt[CNT_INSERTED];
+      if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+        return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                                 std::to_string(h->rel->max_rows));
+      int done = 0;
+      bool empty = false;
+      for (int j = 1; j <= K && b[j + 1] != ~0ull; ++j) {
+        ++done;
+        ++pass;
+        st->iterations++;
+        const int64_t d = (int64_t)(b[j + 1] - b[j]);
+        record(d);
+        st->new_tuples_total += d;
+        if (d == 0) {
+          empty = true;
+          break;
+        }
+      }
+      h->round += (uint32_t)done;
+      if (empty) {
+        h->dn = 0;
+        break;
+      }
+      if (done == K) {  // the last round's rows are the next delta
+        XL_TRY(take_delta_rows(h, cols, (int64_t)b[K], (int64_t)(b[K + 1] - b[K])));
+        continue;
+      }
+      // Round done + 1 stopped early (table load limit, slot list capacity
+      // or a refused product row): re-run it the ordinary way from its driver
+      // rows [b[done], b[done + 1]).
+      if (pass >= max_iterations)
+        return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
+                                                   " reached before the fixpoint");
+      XL_TRY(take_delta_rows(h, cols, (int64_t)b[done], (int64_t)(b[done + 1] - b[done])));
+      const uint32_t rid = h->round + 1;  // the stopped round's stamp
+      if (hashed) {
+        // its contributions so far are dropped (the run below folds them all
+        // again, under a new stamp, by the sorted path); keys it inserted
+        // hold the identity until that run's merge
+        HIP_TRY(c, k::acc_fill(acc.as<u64>(), acc_cap, vt, h->fold, c->stream));
+        h->round = rid;
+        begin_round(h);
+      } else {
+        // its improvements stay in the table: list the slots it stamped and
+        // let the run below add the rest
+        h->round = rid - 1;
+        begin_round(h);
+        Buf tmp, tot;
+        XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
+        XL_TRY(dalloc(c, 8, &tot, "count"));
+        HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(), h->cap,
+                                      tot.as<uint32_t>(), tmp.p, c->stream));
+        uint32_t n2 = 0;
+        XL_TRY(ctl_read(c, tot.p, 4, &n2));
+        h->didx_n = (int64_t)n2;
+      }
+      for (RulePlan& p : s.variants) XL_TRY(eval_plan(p));
+      ++pass;
+      st->iterations++;
+      int64_t d = 0;
+      XL_TRY(finish_round(h, &d));
+      record(d);
+      st->new_tuples_total += d;
     }
     return XL_OK;
   }
@@ -2501,9 +2725,14 @@ struct Runner {
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
-    if (batch_range && p.driver_delta) {  // batched set rounds: the delta range is on the device
-      for (int j = 0; j < h->nkey; ++j) src.col[j] = h->rows[j].as<uint32_t>();
-      src.n = h->rows_cap;  // bounds the grid only
+    if (batch_range && p.driver_delta) {  // batched rounds: the delta range is on the device
+      if (h->is_set) {
+        for (int j = 0; j < h->nkey; ++j) src.col[j] = h->rows[j].as<uint32_t>();
+        src.n = h->rows_cap;  // bounds the grid only
+      } else {
+        for (int j = 0; j <= h->nkey; ++j) src.col[j] = batch_rows[j];
+        src.n = batch_rows_cap;
+      }
     }
     if (src.n == 0) return XL_OK;
     std::vector<MicroOp> pops;
@@ -2577,6 +2806,35 @@ struct Runner {
       a.emit.key.shift = h->kp.shift;
       a.emit.val_slot = (int8_t)p.val_slot;
       a.emit.val_type = p.val_type;
+      if (batch_range) {
+        // batched rounds: the driver range, the append base, the load limit
+        // and the counters belong to the batch; nothing is read back
+        a.src_range = batch_range;
+        a.emit.counters = batch_counters;
+        a.emit.limit = batch_limit;
+        a.emit.mask = (u64)h->cap - 1;
+        if (h->is_set) {
+          a.emit.mode = EM_SET;
+          a.emit.table = h->table.as<u64>();
+          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
+          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
+          a.emit.row_base = batch_row_base;
+          a.emit.row_cap = h->rows_cap;
+        } else {
+          a.emit.mode = h->is_minmax ? EM_MINMAX : EM_HAGG;
+          a.emit.table16 = h->table.as<Slot16>();
+          a.emit.is_max = h->agg == Agg::MAX;
+          a.emit.round = batch_round;
+          a.emit.delta_idx = batch_idx + batch_row_base;
+          a.emit.delta_lim = batch_delta_lim;
+          a.emit.acc = batch_acc;
+          a.emit.fold_kind = h->fold;
+          a.emit.agg_identity = h->fold == k::FOLD_LSE ? 0xff800000u : 0u;  // -inf, or zero
+        }
+        HIP_TRY(c, k::stage_launch(a, c->stream, batch_grid));
+        if (product) break;  // the one launch covered both steps
+        continue;
+      }
       if (h->dcount) {
         const DevIndex* dx = degree_index(p);
         if (dx) {  // the group's count is the index degree of its key
@@ -2631,22 +2889,6 @@ struct Runner {
       // set / min / max: single pass with insert-or-improve, retried after growth
       for (int attempt = 0;; ++attempt) {
         if (attempt > 8) return c->fail(XL_DEVICE_ERROR, "hash table growth did not converge");
-        if (batch_range) {
-          // batched set rounds: the driver range, the append base, the load
-          // limit and the counters belong to the batch; nothing is read back
-          a.src_range = batch_range;
-          a.emit.counters = batch_counters;
-          a.emit.limit = batch_limit;
-          a.emit.mask = (u64)h->cap - 1;
-          a.emit.mode = EM_SET;
-          a.emit.table = h->table.as<u64>();
-          a.emit.row_col[0] = h->rows[0].as<uint32_t>();
-          a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
-          a.emit.row_base = batch_row_base;
-          a.emit.row_cap = h->rows_cap;
-          HIP_TRY(c, k::stage_launch(a, c->stream, batch_grid));
-          break;
-        }
         if (nst == 0 || ks == 0) {  // the driver may live in this head's row list
           Source s2 = resolve_driver(p);
           for (int j = 0; j < a.src.ncols && ks == 0; ++j) a.src.col[j] = s2.col[j];
@@ -2735,17 +2977,7 @@ struct Runner {
           return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
                                                    std::to_string(h->rel->max_rows));
         if (!cnt[CNT_OVERFLOW]) break;
-        XL_TRY(grow(h, h->keys * 2 + 1));
-        if (h->is_minmax) {  // slot indices moved: rebuild this round's delta list
-          Buf tmp, tot;
-          XL_TRY(dalloc(c, k::compact_temp_bytes(h->cap), &tmp, "compaction scratch"));
-          XL_TRY(dalloc(c, 8, &tot, "count"));
-          HIP_TRY(c, k::table16_stamped(h->table.as<Slot16>(), h->cap, h->round, h->didx.as<uint32_t>(), h->cap,
-                                        tot.as<uint32_t>(), tmp.p, c->stream));
-          uint32_t n2 = 0;
-          XL_TRY(ctl_read(c, tot.p, 4, &n2));
-          h->didx_n = (int64_t)n2;
-        }
+        XL_TRY(grow(h, h->keys * 2 + 1));  // (lists this round's min/max slots again)
       }
       if (product) break;  // the one launch covered both steps
     }
@@ -3279,6 +3511,10 @@ struct Runner {
     }
     if (s.recursive && total > 0 && batched_sets(s)) {
       XL_TRY(run_sets_batched(s, heads[0].get(), max_iterations));
+      total = 0;
+    }
+    if (s.recursive && total > 0 && batched_values(s)) {
+      XL_TRY(run_values_batched(s, heads[0].get(), max_iterations));
       total = 0;
     }
     if (s.recursive && total > 0 && resident_frontier(s)) {

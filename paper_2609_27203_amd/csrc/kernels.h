@@ -105,6 +105,15 @@ hipError_t table16_stamped(const Slot16* t, int64_t cap, uint32_t round, uint32_
 hipError_t table16_rows_from_idx(const Slot16* t, const uint32_t* idx, int64_t n, KeyPack kp,
                                  int type, int fold_kind, uint32_t* k0, uint32_t* k1,
                                  uint32_t* v, hipStream_t s);
+// Delta rows of one batched keyed-table round, from the slot list positions
+// [bnd[j], bnd[j + 1]) held on the device (max_n bounds them, for the grid);
+// with acc (hashed sum/logsumexp) also the round's merge into the full
+// relation and the accumulators' reset.
+hipError_t table16_rows_range(Slot16* t, unsigned long long* acc, const uint32_t* idx, const unsigned long long* bnd,
+                              int j, int64_t max_n, KeyPack kp, int type, int fold_kind, uint32_t* k0,
+                              uint32_t* k1, uint32_t* v, hipStream_t s);
+// Set n accumulators of hashed sum/logsumexp folds to the fold's identity.
+hipError_t acc_fill(unsigned long long* acc, int64_t n, int type, int fold_kind, hipStream_t s);
 hipError_t table16_compact(const Slot16* t, int64_t cap, KeyPack kp, int type, int fold_kind,
                            uint32_t* k0, uint32_t* k1, uint32_t* v, int64_t out_cap, uint32_t* total,
                            void* temp, hipStream_t s);

@@ -1115,6 +1115,45 @@ __device__ __forceinline__ bool eval_ops(KernArgs& a, Regs& u) {
   return run_ops(a, u);
 }
 
+// Accumulators of hashed sum/logsumexp folds (EM_HAGG), one 64-bit word per
+// table slot.  Integer sums add modulo 2^32 in the low word (the result of
+// any order); f32 sums add in f64 and logsumexp folds in f64 with
+// max + log1p(exp(-|a - b|)), so the order in which a round's contributions
+// arrive moves the f64 result by a few units of its last place, far below
+// the f32 rounding applied when the round ends.
+__device__ __forceinline__ double lse2d(double a, double b) {
+  if (a == -HUGE_VAL) return b;
+  if (b == -HUGE_VAL) return a;
+  return fmax(a, b) + log1p(exp(-fabs(a - b)));
+}
+__device__ __forceinline__ u64 acc_identity(int type, int fold_kind) {
+  if (fold_kind == FOLD_LSE) return (u64)__double_as_longlong(-HUGE_VAL);
+  (void)type;
+  return 0ull;  // integer 0 in the low word, or f64 +0.0
+}
+__device__ __forceinline__ void acc_add(u64* acc, uint32_t x, int type, int fold_kind) {
+  if (fold_kind == FOLD_LSE) {
+    const double v = (double)__uint_as_float(x);
+    if (v == -HUGE_VAL) return;
+    u64 old = *acc;
+    for (;;) {
+      const u64 nv = (u64)__double_as_longlong(lse2d(__longlong_as_double((long long)old), v));
+      const u64 prev = atomicCAS(acc, old, nv);
+      if (prev == old) break;
+      old = prev;
+    }
+  } else if (type == T_F32) {
+    atomicAdd(reinterpret_cast<double*>(acc), (double)__uint_as_float(x));
+  } else {
+    atomicAdd(reinterpret_cast<uint32_t*>(acc), x);
+  }
+}
+// The round's fold of one key, as the value type's bits.
+__device__ __forceinline__ uint32_t acc_value(u64 a, int type, int fold_kind) {
+  if (fold_kind == FOLD_LSE || type == T_F32) return __float_as_uint((float)__longlong_as_double((long long)a));
+  return (uint32_t)a;
+}
+
 // Rows produced by EM_SET / EM_BITSET / EM_MINMAX are staged in a per-wave
 // LDS buffer and written out with one counter reservation per flush, so a
 // launch issues one global atomic per OUTB rows instead of one per 64.
@@ -1144,7 +1183,7 @@ __device__ __forceinline__ void flush_rows(KernArgs& a, EmitState& st) {
   typedef XL_KARG const EmitSpec KEmit;
   KEmit& e = a.emit;
   const int lane = lane_id();
-  if ((MODE == EM_MINMAX || MODE == EM_DMIN) && st.ins_pend) {
+  if ((MODE == EM_MINMAX || MODE == EM_DMIN || MODE == EM_HAGG) && st.ins_pend) {
     u64 b = 0;
     if (lane == 0) {
       b = atomicAdd(&e.counters[CNT_INSERTED], (u64)st.ins_pend);
@@ -1157,16 +1196,17 @@ __device__ __forceinline__ void flush_rows(KernArgs& a, EmitState& st) {
   if (st.buf_n == 0) return;
   wave_lds_sync();
   u64 base = 0;
+  constexpr bool SLOTS = MODE == EM_MINMAX || MODE == EM_DMIN || MODE == EM_HAGG;
   if (lane == 0) {
     base = atomicAdd(&e.counters[CNT_APPENDED], (u64)st.buf_n);
-    if (MODE != EM_MINMAX && MODE != EM_DMIN && base + st.buf_n > e.limit)
+    if (SLOTS ? e.delta_lim && base + st.buf_n > e.delta_lim : base + st.buf_n > e.limit)
       atomicOr(&e.counters[CNT_OVERFLOW], 1ull);
   }
   base = shfl_u64(base, 0);
-  if (MODE != EM_MINMAX && MODE != EM_DMIN && base + st.buf_n > e.limit) st.stop = true;
+  if (SLOTS ? e.delta_lim && base + st.buf_n > e.delta_lim : base + st.buf_n > e.limit) st.stop = true;
   for (uint32_t i = lane; i < st.buf_n; i += 64) {
-    if (MODE == EM_MINMAX || MODE == EM_DMIN) {
-      e.delta_idx[base + i] = st.buf0[i];
+    if (SLOTS) {
+      if (!e.delta_lim || base + i < e.delta_lim) e.delta_idx[base + i] = st.buf0[i];
     } else {
       const u64 p = (u64)e.row_base + base + i;
       if (p < (u64)e.row_cap) {
@@ -1368,7 +1408,7 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
     }
     return;
   }
-  if (MODE == EM_MINMAX) {
+  if (MODE == EM_MINMAX || MODE == EM_HAGG) {
     bool ins = false, app = false;
     u64 slot = ~0ull;
     if (act) {
@@ -1376,9 +1416,16 @@ __device__ __forceinline__ void emit(KernArgs& a, const Regs& u, bool act,
                                                              getv(u, e.key.slot[1])),
                                  &ins, e.counters);
       if (slot != ~0ull) {
-        const uint32_t enc = fold_encode(getv(u, e.val_slot), e.val_type, e.is_max);
-        const uint32_t old = atomicMin(&e.table16[slot].val, enc);
-        if (ins || enc < old) app = atomicExch(&e.table16[slot].stamp, e.round) != e.round;
+        if (MODE == EM_MINMAX) {
+          const uint32_t enc = fold_encode(getv(u, e.val_slot), e.val_type, e.is_max);
+          const uint32_t old = atomicMin(&e.table16[slot].val, enc);
+          if (ins || enc < old) app = atomicExch(&e.table16[slot].stamp, e.round) != e.round;
+        } else {
+          // the full-relation value is only read by the round's merge
+          if (ins) e.table16[slot].val = e.agg_identity;
+          acc_add(e.acc + slot, getv(u, e.val_slot), e.val_type, e.fold_kind);
+          app = atomicExch(&e.table16[slot].stamp, e.round) != e.round;
+        }
       }
     }
     st.ins_pend += (uint32_t)__popcll(__ballot(ins));
@@ -1402,7 +1449,8 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
   __shared__ uint32_t s_beg[ST_WAVES][64];
   __shared__ uint32_t s_beg2[ST_WAVES][64], s_deg2[ST_WAVES][64];
   __shared__ uint32_t s_v[ST_WAVES][MAXV][64];
-  constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DMIN;
+  constexpr bool STAGED = MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DMIN ||
+                         MODE == EM_HAGG;
   __shared__ uint32_t s_out[STAGED ? ST_WAVES : 1][2][STAGED ? OUTB : 1];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   int64_t src_n = a.src.n, src_base = 0;
@@ -1506,7 +1554,7 @@ __global__ __launch_bounds__(ST_THREADS) void stage_k(StageArgs by_value) {
     if (MODE == EM_COUNT && lane == 0) a.emit.chunk_cnt[chunk] = st.running;
   }
   if (MODE == EM_SET || MODE == EM_BITSET || MODE == EM_MINMAX || MODE == EM_DCOUNT || MODE == EM_DMIN ||
-      MODE == EM_MARK) {
+      MODE == EM_MARK || MODE == EM_HAGG) {
     // one atomic per workgroup: a shared counter hit by every wave serializes
     __shared__ u64 s_cands[ST_WAVES], s_new[ST_WAVES];
     u64 nw = 0;
@@ -1590,6 +1638,7 @@ hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
     case EM_BITSET: launch_mode<EM_BITSET>(a, grid, s); break;
     case EM_DMIN: launch_mode<EM_DMIN>(a, grid, s); break;
     case EM_MARK: launch_mode<EM_MARK>(a, grid, s); break;
+    case EM_HAGG: launch_mode<EM_HAGG>(a, grid, s); break;
     default: launch_mode<EM_MINMAX>(a, grid, s); break;
   }
   return hipGetLastError();
@@ -1722,6 +1771,61 @@ __device__ __forceinline__ float lse2(float a, float b) {
   if (b == -INFINITY) return a;
   const float m = fmaxf(a, b);
   return m + log1pf(expf(-fabsf(a - b)));
+}
+
+// Delta rows of batched keyed-table rounds: list positions [bnd[j], bnd[j + 1])
+// (read on the device; ~0 as the end: the round overflowed, nothing to do)
+// hold the slots the round touched; row i is written for position i.  With
+// acc (hashed sum/logsumexp), each slot's accumulator is the round's fold of
+// its key: it becomes the row's value, is merged into the slot's full-relation
+// value and is reset to the identity; otherwise (min/max) the row takes the
+// slot's value.  Each slot appears once in a round's list, so no two threads
+// touch one slot.
+__global__ void table16_rows_range_k(Slot16* t, u64* acc, const uint32_t* idx, const u64* bnd, int j,
+                                     KeyPack kp, int type, int fold_kind, uint32_t* k0, uint32_t* k1,
+                                     uint32_t* v) {
+  const u64 lo = bnd[j], hi = bnd[j + 1];
+  if (hi == ~0ull) return;
+  const u64 ident = acc ? acc_identity(type, fold_kind) : 0ull;
+  for (u64 i = lo + (u64)blockIdx.x * blockDim.x + threadIdx.x; i < hi; i += (u64)gridDim.x * blockDim.x) {
+    const uint32_t slot = idx[i];
+    const Slot16 s = t[slot];
+    uint32_t a, b;
+    unpack_key(kp, s.key, &a, &b);
+    k0[i] = a;
+    if (k1) k1[i] = b;
+    if (acc) {
+      const uint32_t d = acc_value(acc[slot], type, fold_kind);
+      acc[slot] = ident;
+      uint32_t r;
+      if (fold_kind == FOLD_LSE) r = __float_as_uint(lse2(__uint_as_float(s.val), __uint_as_float(d)));
+      else if (type == T_F32) r = __float_as_uint(__fadd_rn(__uint_as_float(s.val), __uint_as_float(d)));
+      else r = s.val + d;
+      t[slot].val = r;
+      v[i] = d;
+    } else {
+      v[i] = stored_value(s.val, type, fold_kind);
+    }
+  }
+}
+hipError_t table16_rows_range(Slot16* t, unsigned long long* acc, const uint32_t* idx, const unsigned long long* bnd,
+                              int j, int64_t max_n, KeyPack kp, int type, int fold_kind, uint32_t* k0,
+                              uint32_t* k1, uint32_t* v, hipStream_t s) {
+  if (max_n <= 0) return hipSuccess;
+  table16_rows_range_k<<<grid_for(max_n, 256, 4096), 256, 0, s>>>(t, acc, idx, bnd, j, kp, type, fold_kind, k0,
+                                                                 k1, v);
+  return hipGetLastError();
+}
+
+__global__ void acc_fill_k(u64* acc, int64_t n, int type, int fold_kind) {
+  const u64 ident = acc_identity(type, fold_kind);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    acc[i] = ident;
+}
+hipError_t acc_fill(unsigned long long* acc, int64_t n, int type, int fold_kind, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  acc_fill_k<<<grid_for(n, 256, 8192), 256, 0, s>>>(acc, n, type, fold_kind);
+  return hipGetLastError();
 }
 
 // Fold a contribution into a full-relation slot this thread owns; returns

@@ -1,5 +1,7 @@
 """Full-size parity: every row of the five full-size workloads, in the
-launch configuration the benchmark times (default options, index mode 0).
+launch configuration the benchmark times (default options, index mode 0)
+and with every derived relation in hash tables (index mode 1: the generic
+keyed-table paths and their batched rounds).
 
 Each result is decided twice, by independent routes:
 * a certificate from a textbook routine computed here on the CPU
@@ -27,17 +29,29 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
 DIGESTS = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "full_digests.json")))
 
 _RUNS = {}
+_CLOSURES = {}
 
 
-def _full(name, workspace_gb):
-    """The engine's full-size result (one run per workload and session)."""
-    if name not in _RUNS:
+def _full(name, workspace_gb, index_mode=0):
+    """The engine's full-size result (one run per workload, index mode and
+    session; a new run frees the previous one's rows)."""
+    key = (name, index_mode)
+    if key not in _RUNS:
+        _RUNS.clear()
         wl = W.full_workloads()[name]()
-        print(f"case: full {name} {wl.digest()[:12]}", flush=True)
-        rels, stats, ctx = engine_run(wl, workspace_bytes=workspace_gb << 30)
+        print(f"case: full {name} index_mode={index_mode} {wl.digest()[:12]}", flush=True)
+        rels, stats, ctx = engine_run(wl, workspace_bytes=workspace_gb << 30, options={"index_mode": index_mode})
         ctx.close()
-        _RUNS[name] = (wl, rels, stats)
-    return _RUNS[name]
+        _RUNS[key] = (wl, rels, stats)
+    return _RUNS[key]
+
+
+def _closure(name, n, src, dst):
+    """Breadth-first-search closure matrix and level sizes (cached per workload)."""
+    if name not in _CLOSURES:
+        reached, levels = CERT.closure_bits(n, src, dst)
+        _CLOSURES[name] = (CERT.reached_matrix(reached, n), levels)
+    return _CLOSURES[name]
 
 
 def _check_digest(name, wl, rels):
@@ -52,26 +66,27 @@ def _levels(sizes):
     return [sizes[0]] + [b - a for a, b in zip(sizes, sizes[1:])]
 
 
-def test_full_tc_uniform_every_row():
-    wl, rels, stats = _full("tc_uniform", 4)
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_full_tc_uniform_every_row(index_mode):
+    wl, rels, stats = _full("tc_uniform", 4, index_mode)
     src, dst = wl.edb["edge"][1]
     n = wl.params["n_nodes"]
-    reached, levels = CERT.closure_bits(n, src, dst)
-    CERT.check_closure_rows(CERT.reached_matrix(reached, n), *rels["path"])
+    m, levels = _closure("tc_uniform", n, src, dst)
+    CERT.check_closure_rows(m, *rels["path"])
     assert stats["delta_rows"] == levels and stats["iterations"] == len(levels) - 1
     _check_digest("tc_uniform", wl, rels)
     assert _levels(DIGESTS["tc_uniform"]["path_sizes"]) == levels
 
 
-def test_full_tc_rmat_count_every_row():
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_full_tc_rmat_count_every_row(index_mode):
     """The headline workload: all 128.9 M closure rows, all reach counts,
     the per-pass delta sizes and the derived-tuple count the benchmark
     reports."""
-    wl, rels, stats = _full("tc_rmat_count", 32)
+    wl, rels, stats = _full("tc_rmat_count", 32, index_mode)
     src, dst = wl.edb["edge"][1]
     n = 1 << wl.params["scale"]
-    reached, levels = CERT.closure_bits(n, src, dst)
-    m = CERT.reached_matrix(reached, n)
+    m, levels = _closure("tc_rmat_count", n, src, dst)
     CERT.check_closure_rows(m, *rels["path"])
     cnt = m.sum(axis=1)
     rc = rels["reach_count"]
@@ -83,20 +98,22 @@ def test_full_tc_rmat_count_every_row():
     assert _levels(DIGESTS["tc_rmat_count"]["path_sizes"]) == levels
 
 
-def test_full_sssp_every_row():
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_full_sssp_every_row(index_mode):
     """All 64 sources, bit for bit: the binary32 Bellman equations hold for
     every node, and the rows' digest is the oracle's."""
-    wl, rels, _ = _full("sssp", 8)
+    wl, rels, _ = _full("sssp", 8, index_mode)
     src, dst, w = wl.edb["edge"][1]
     sources = np.sort(wl.edb["source"][1][0])
     CERT.bellman_check(wl.params["n_nodes"], src, dst, w, sources, *rels["dist"])
     _check_digest("sssp", wl, rels)
 
 
-def test_full_lse_every_row_forward_pass():
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_full_lse_every_row_forward_pass(index_mode):
     """All 256 sources: every row within 1e-5 * max(1, |ref|) of the float64
     forward pass, and exactly the (source, node) pairs joined by a path."""
-    wl, rels, _ = _full("lse_dag", 8)
+    wl, rels, _ = _full("lse_dag", 8, index_mode)
     src, dst, w = wl.edb["edge"][1]
     L, K = wl.params["n_layers"], wl.params["width"]
     sources = np.sort(wl.edb["source"][1][0])
@@ -118,8 +135,9 @@ def test_full_lse_oracle_sampled_sources(part):
                          ref.relations["score"][1], " (oracle-sampled sources)", tol=(LSE_TOL, 1.0))
 
 
-def test_full_same_generation_every_row():
-    wl, rels, stats = _full("same_generation", 8)
+@pytest.mark.parametrize("index_mode", [0, 1])
+def test_full_same_generation_every_row(index_mode):
+    wl, rels, stats = _full("same_generation", 8, index_mode)
     x, y = rels["sg"]
     n = len(wl.params["depth"])
     keys = CERT.same_generation_keys(wl.edb["parent"][1][0], wl.params["depth"], wl.params["root"], n)

@@ -485,6 +485,96 @@ def test_hash_set_rounds_cap_and_round_count(batch):
         assert reads[20] == reads[50]
 
 
+def _value_workload(name):
+    """A min/max/sum/logsumexp workload over the small layered DAG or the small
+    SSSP graph (the aggregate heads of the batched keyed-table rounds)."""
+    if name in ("sssp", "lse_dag"):
+        return W.small_workloads()[name]()
+    base = W.small_workloads()["lse_dag"]()
+    if name in PULL_RULES:
+        rules, idb = PULL_RULES[name]
+        return W.Workload(name, rules, base.edb, idb)
+    rules, idb = SUBTRACT_RULES[name]
+    src, dst, _ = base.edb["edge"][1]
+    edb = dict(base.edb)
+    edb["iedge"] = (("i32", "i32", "i32"), [src, dst, ((src * 7 + dst * 3) % 9 + 1).astype(np.int32)])
+    return W.Workload(name, rules, {k: v for k, v in edb.items() if k + "(" in rules}, idb)
+
+
+def _compare_values(wl, rels, ref, where=""):
+    for rel, types in wl.idb.items():
+        tol = value_tolerance(wl.rules, rel)
+        assert_same_relation(rel, types, rels[rel], ref.relations[rel][1], where,
+                             tol=tol if tol[0] == LSE_TOL else (0.0, 0.0))
+
+
+@pytest.mark.parametrize("growth", [False, True])
+@pytest.mark.parametrize("batch", [1, 4, 64])
+@pytest.mark.parametrize("name", ["sssp", "lse_dag", "npaths", "max_i32", "score_filtered"])
+def test_hash_value_rounds_batched(name, batch, growth):
+    """Min/max and sum/logsumexp heads held in hash tables (index mode 1) run
+    batch rounds per host read: min/max candidates improve table values,
+    sum/logsumexp candidates fold into per-slot accumulators, and each round's
+    touched slots become the next delta on the device.  With a tiny initial
+    table the batches overflow and the host re-runs the round that stopped.
+    Min/max and integer sums match the oracle bit for bit, logsumexp within
+    its tolerance; per-pass delta sizes and pass counts equal the
+    round-by-round loop's."""
+    wl = _value_workload(name)
+    print(f"case: batched hash value rounds {name} batch={batch} growth={growth}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    opts = {"index_mode": 1, "batched_rounds": batch}
+    if growth:
+        opts["hash_min_log2"] = 10
+    rels, stats, _ = engine_run(wl, options=opts)
+    _compare_values(wl, rels, ref)
+    base = engine_run(wl, options={"index_mode": 1, "batched_rounds": 0})[1]
+    assert stats["delta_rows"] == base["delta_rows"] and stats["iterations"] == base["iterations"]
+    if growth:
+        assert stats["table_grows"] > 0
+
+
+CHAIN_VALUE_RULES = {
+    "min": (W.SSSP_RULES, {"dist": ("i32", "i32", "f32")}),
+    "lse": (W.LSE_RULES, {"score": ("i32", "i32", "f32")}),
+    "sum": (PULL_RULES["npaths"][0], {"npaths": ("i32", "i32", "i32")}),
+}
+
+
+@pytest.mark.parametrize("batch", [0, 4, 64])
+@pytest.mark.parametrize("kind", list(CHAIN_VALUE_RULES))
+def test_hash_value_rounds_cap_and_round_count(kind, batch):
+    """A chain of n nodes from one source takes one pass per edge: in index
+    mode 1 the iteration cap ends the run with XL_CONVERGENCE_FAILURE at the
+    same pass batched or not, and with 64 rounds per read the control bytes
+    read do not grow with the number of rounds (chains of 20 and 50 nodes)."""
+    from paper_2609_27203_amd import xlh
+    rules, idb = CHAIN_VALUE_RULES[kind]
+    reads = {}
+    for n in (20, 50):
+        src = np.arange(n - 1, dtype=np.int32)
+        w = np.full(n - 1, -0.5 if kind == "lse" else 1.5, np.float32)
+        edb = {"source": (("i32",), [np.array([0], np.int32)]),
+               "edge": (("i32", "i32", "f32"), [src, src + 1, w])}
+        wl = W.Workload(f"{kind}_chain{n}", rules, edb, idb)
+        print(f"case: hash value chain {kind} n={n} batch={batch}", flush=True)
+        ref = evaluate(wl.rules, wl.edb, wl.idb)
+        opts = {"index_mode": 1, "batched_rounds": batch}
+        rels, stats, _ = engine_run(wl, options=opts, workspace_bytes=256 << 20)
+        _compare_values(wl, rels, ref)
+        base = engine_run(wl, options={"index_mode": 1, "batched_rounds": 0}, workspace_bytes=256 << 20)[1]
+        passes = stats["iterations"]
+        assert passes == base["iterations"] and stats["delta_rows"] == base["delta_rows"]
+        assert passes >= n - 1
+        reads[n] = stats["control_bytes_read"]
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, options=opts, max_iterations=passes - 1, workspace_bytes=256 << 20)
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+        engine_run(wl, options=opts, max_iterations=passes, workspace_bytes=256 << 20)
+    if batch == 64:
+        assert reads[20] == reads[50]
+
+
 @pytest.mark.parametrize("batch", [0, 1, 4, 64])
 @pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
 def test_min_rounds_tiled_and_untiled(tiles, batch):
