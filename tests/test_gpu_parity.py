@@ -575,6 +575,34 @@ def test_hash_value_rounds_cap_and_round_count(kind, batch):
         assert reads[20] == reads[50]
 
 
+@pytest.mark.parametrize("batch", [0, 4, 64])
+def test_hash_same_generation_rounds_and_control_reads(batch):
+    """Same generation in hash tables (index mode 1; the recursive rule joins
+    both parent steps in one product launch): over two parallel chains under
+    one root, pass k derives the pairs at depth k + 1, so the pass count
+    grows with the depth while, at 64 rounds per read, the control bytes
+    read do not (depths 10 and 30)."""
+    reads = {}
+    for depth in (10, 30):
+        # node 0 is the root; chain a: 1..depth, chain b: depth+1..2*depth
+        a = np.arange(1, depth + 1, dtype=np.int32)
+        b = a + depth
+        child = np.concatenate([a, b])
+        par = np.concatenate([np.concatenate([[0], a[:-1]]), np.concatenate([[0], b[:-1]])]).astype(np.int32)
+        wl = W.Workload(f"comb{depth}", W.SG_RULES, {"parent": (("i32", "i32"), [child, par])},
+                        {"sg": ("i32", "i32")})
+        print(f"case: hash same generation comb depth={depth} batch={batch}", flush=True)
+        ref = evaluate(wl.rules, wl.edb, wl.idb)
+        rels, stats, _ = engine_run(wl, options={"index_mode": 1, "batched_rounds": batch},
+                                    workspace_bytes=256 << 20)
+        _compare(wl, rels, ref)
+        assert len(rels["sg"][0]) == 2 * depth
+        assert stats["iterations"] == depth and stats["delta_rows"] == [2] * depth + [0]
+        reads[depth] = stats["control_bytes_read"]
+    if batch == 64:
+        assert reads[10] == reads[30]
+
+
 @pytest.mark.parametrize("batch", [0, 1, 4, 64])
 @pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
 def test_min_rounds_tiled_and_untiled(tiles, batch):
