@@ -619,6 +619,12 @@ struct HeadRun {
   uint32_t tile = 0, ntiles = 0;
   // key-column domains (bounds recorded on the materialized relation)
   int64_t dom_lo[2] = {0, 0}, dom_hi[2] = {0, 0};
+  // batched rounds: this head's counters and round boundaries on the device
+  // (row counts of its row list, or positions of the batch's slot list), the
+  // base its emissions append at and its load limit
+  u64* b_cnt = nullptr;
+  u64* b_bnd = nullptr;
+  u64 b_base = 0, b_limit = 0;
 };
 
 struct Runner {
@@ -1797,9 +1803,7 @@ struct Runner {
   // nothing and the host re-runs that round the ordinary way (growing the
   // table; insert-if-absent keeps the partial round's rows valid).  Passes,
   // per-pass delta sizes and the iteration cap are those of the host loop.
-  const u64* batch_range = nullptr;
-  u64* batch_counters = nullptr;
-  u64 batch_row_base = 0, batch_limit = 0;
+  int batch_j = 0;              // round of the batch being enqueued (1-based; 0: not batching)
   int batch_grid = EMIT_GRID;  // workgroups of a batched launch (its waves bound the slack)
   // batched keyed value rounds: the batch's delta rows and slot list (one
   // position space: the first delta at [0, base), each round's slots and rows
@@ -1812,12 +1816,20 @@ struct Runner {
   uint32_t batch_round = 0;
   u64* batch_acc = nullptr;
 
+  // Batched rounds of set heads held in hash tables (row list + set): every
+  // head of the stratum (one, or several in mutual recursion) is a hash set,
+  // and each delta variant runs in one stage launch over its driver head's
+  // delta and joins only relations outside the stratum.
   bool batched_sets(const Stratum& s) {
-    if (c->batched_rounds <= 0 || heads.size() != 1 || s.variants.empty()) return false;
-    HeadRun* h = heads[0].get();
-    if (!h->is_set || h->dense || h->frontier || h->gathered || h->dv) return false;
+    if (c->batched_rounds <= 0 || heads.empty() || heads.size() > (size_t)k::MAX_BATCH_HEADS || s.variants.empty())
+      return false;
+    for (auto& hp : heads) {
+      const HeadRun* h = hp.get();
+      if (!h->is_set || h->dense || h->frontier || h->gathered || h->dv) return false;
+    }
     for (const RulePlan& p : s.variants) {
-      if (!p.driver_delta || p.driver != h->rel || p.wcoj || head_of(p.head) != h) return false;
+      HeadRun* h = head_of(p.head);
+      if (!p.driver_delta || !head_of(p.driver) || p.wcoj || !h) return false;
       for (const StepPlan& sp : p.steps)
         if (head_of(sp.rel)) return false;
       if (p.steps.size() > 2) return false;
@@ -1830,77 +1842,108 @@ struct Runner {
     return true;
   }
 
-  xl_status run_sets_batched(Stratum& s, HeadRun* h, int64_t max_iterations) {
+  xl_status run_sets_batched(Stratum& s, int64_t max_iterations) {
     const int B = c->batched_rounds;
+    const int nh = (int)heads.size();
     constexpr size_t CNTB = 256;
     static_assert(8 * CNT_N <= CNTB, "counters fit their block");
-    Buf blk;  // the batch's counters, then the round boundaries
-    XL_TRY(dalloc(c, CNTB + 8 * (size_t)(B + 2), &blk, "batch counters"));
-    u64* counters = blk.as<u64>();
-    u64* bnd = (u64*)((char*)blk.p + CNTB);
-    std::vector<unsigned char> host(CNTB + 8 * (size_t)(B + 2));
+    const size_t per = CNTB + 8 * (size_t)(B + 2);  // one head's counters, then its round boundaries
+    Buf blk;
+    XL_TRY(dalloc(c, per * nh, &blk, "batch counters"));
+    std::vector<unsigned char> host(per * nh);
+    auto hcnt = [&](int q) { return (const u64*)(host.data() + per * q); };
+    auto hbnd = [&](int q) { return (const u64*)(host.data() + per * q + CNTB); };
+    for (int q = 0; q < nh; ++q) {
+      heads[q]->b_cnt = (u64*)((char*)blk.p + per * q);
+      heads[q]->b_bnd = (u64*)((char*)blk.p + per * q + CNTB);
+    }
+    auto any_delta = [&]() {
+      for (auto& h : heads)
+        if (h->dend > h->dbeg) return true;
+      return false;
+    };
     int64_t pass = 0;
-    while (h->dend > h->dbeg) {
+    while (any_delta()) {
       if (pass >= max_iterations)
         return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
                                                    " reached before the fixpoint");
-      // every wavefront of the launch that crosses the limit may still insert
-      // one batch: the grid takes at most a quarter of the table as slack
-      // (whatever the round's delta size, which is unknown here)
-      const int64_t waves =
-          std::max<int64_t>(256, std::min<int64_t>((int64_t)EMIT_GRID * 4, h->cap / 4 / WAVE_SLACK)) / 4 * 4;
+      // every wavefront of a launch that crosses its head's limit may still
+      // insert one batch: the grid takes at most a quarter of the smallest
+      // table as slack (whatever the round's delta size, unknown here)
+      int64_t waves = (int64_t)EMIT_GRID * 4;
+      for (auto& h : heads) waves = std::min<int64_t>(waves, h->cap / 4 / WAVE_SLACK);
+      waves = std::max<int64_t>(256, waves) / 4 * 4;
       batch_grid = (int)(waves / 4);
-      const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
-      if (h->keys >= max_keys) {
-        XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + WAVE_SLACK * waves + 1024)));
-        continue;
+      bool grown = false;
+      for (auto& hp : heads) {
+        HeadRun* h = hp.get();
+        const int64_t max_keys = std::min<int64_t>(h->cap / 2, h->cap - WAVE_SLACK * waves - 1024);
+        if (h->keys >= max_keys) {
+          XL_TRY(grow(h, std::max<int64_t>(h->keys * 2, h->keys + WAVE_SLACK * waves + 1024)));
+          grown = true;
+        }
+        h->b_limit = (u64)std::max<int64_t>(0, max_keys - h->keys);
       }
+      if (grown) continue;
       const int K = (int)std::min<int64_t>(B, max_iterations - pass);
-      HIP_TRY(c, hipMemsetAsync(counters, 0, CNTB, c->stream));
-      HIP_TRY(c, k::batch_init(bnd, B + 2, (u64)h->dbeg, (u64)h->dend, c->stream));
-      batch_counters = counters;
-      batch_row_base = (u64)h->nrows;
-      batch_limit = (u64)(max_keys - h->keys);
+      HIP_TRY(c, hipMemsetAsync(blk.p, 0, per * nh, c->stream));
+      k::BatchMarks marks{};
+      marks.n = nh;
+      for (int q = 0; q < nh; ++q) {
+        HeadRun* h = heads[q].get();
+        HIP_TRY(c, k::batch_init(h->b_bnd, B + 2, (u64)h->dbeg, (u64)h->dend, c->stream));
+        h->b_base = (u64)h->nrows;
+        marks.bnd[q] = h->b_bnd;
+        marks.cnt[q] = h->b_cnt;
+        marks.base[q] = h->b_base;
+      }
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
       for (int j = 1; j <= K; ++j) {
-        batch_range = bnd + (j - 1);
+        batch_j = j;
         for (RulePlan& p : s.variants) {
           const xl_status e = eval_plan(p);
           if (e != XL_OK) {
-            batch_range = nullptr;
+            batch_j = 0;
             return e;
           }
         }
-        HIP_TRY(c, k::batch_mark(bnd, j, counters, batch_row_base, c->stream));
+        HIP_TRY(c, k::batch_mark_heads(marks, j, c->stream));
       }
-      batch_range = nullptr;
+      batch_j = 0;
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
-      XL_TRY(ctl_read(c, blk.p, CNTB + 8 * (size_t)(K + 2), host.data()));
-      u64 cnt[CNT_N];
-      memcpy(cnt, host.data(), sizeof(cnt));
-      const u64* b = (const u64*)(host.data() + CNTB);
-      if (cnt[CNT_FATAL] & ~16ull) return stage_fatal(cnt[CNT_FATAL], "hash table probe exhausted or row list overflow (internal)");
-      cands += (int64_t)cnt[CNT_CANDIDATES];
+      XL_TRY(ctl_read(c, blk.p, per * nh, host.data()));
+      u64 emitted = 0, candidates = 0;
+      for (int q = 0; q < nh; ++q) {
+        HeadRun* h = heads[q].get();
+        const u64* cnt = hcnt(q);
+        if (cnt[CNT_FATAL] & ~16ull)
+          return stage_fatal(cnt[CNT_FATAL], "hash table probe exhausted or row list overflow (internal)");
+        candidates += cnt[CNT_CANDIDATES];
+        emitted += cnt[CNT_APPENDED];
+        h->nrows = (int64_t)h->b_base + (int64_t)cnt[CNT_APPENDED];
+        h->keys += (int64_t)cnt[CNT_APPENDED];
+        if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
+          return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
+                                                   std::to_string(h->rel->max_rows));
+      }
+      cands += (int64_t)candidates;
       if (c->profile) {
         float ms = 0;
         HIP_TRY(c, hipEventElapsedTime(&ms, ev[0], ev[1]));
         st->emit_ms += ms;
         st->emit_launches += (int64_t)K * (int64_t)s.variants.size();
-        st->emit_candidates += (int64_t)cnt[CNT_CANDIDATES];
-        st->emit_new += (int64_t)cnt[CNT_APPENDED];
+        st->emit_candidates += (int64_t)candidates;
+        st->emit_new += (int64_t)emitted;
       }
-      h->nrows = (int64_t)batch_row_base + (int64_t)cnt[CNT_APPENDED];
-      h->keys += (int64_t)cnt[CNT_APPENDED];
-      if (h->rel->max_rows > 0 && h->keys > h->rel->max_rows)
-        return c->fail(XL_CAPACITY_EXCEEDED, "relation " + h->rel->name + " exceeds its max_rows " +
-                                                 std::to_string(h->rel->max_rows));
+      // the marks are all or nothing: a round is complete for every head or for none
       int done = 0;
       bool empty = false;
-      for (int j = 1; j <= K && b[j + 1] != ~0ull; ++j) {
+      for (int j = 1; j <= K && hbnd(0)[j + 1] != ~0ull; ++j) {
         ++done;
         ++pass;
         st->iterations++;
-        const int64_t d = (int64_t)(b[j + 1] - b[j]);
+        int64_t d = 0;
+        for (int q = 0; q < nh; ++q) d += (int64_t)(hbnd(q)[j + 1] - hbnd(q)[j]);
         record(d);
         st->new_tuples_total += d;
         if (d == 0) {
@@ -1909,32 +1952,42 @@ struct Runner {
         }
       }
       if (empty) {
-        h->dbeg = h->dend = h->nrows;
+        for (auto& h : heads) h->dbeg = h->dend = h->nrows;
         break;
       }
       if (done == K) {
-        h->dbeg = (int64_t)b[K];
-        h->dend = (int64_t)b[K + 1];
+        for (int q = 0; q < nh; ++q) {
+          heads[q]->dbeg = (int64_t)hbnd(q)[K];
+          heads[q]->dend = (int64_t)hbnd(q)[K + 1];
+        }
         continue;
       }
-      // round done + 1 stopped early: re-run it the ordinary way (its driver
-      // is [b[done], b[done + 1]); the rows it appended before stopping are
-      // the start of its delta)
+      // round done + 1 stopped early: re-run it the ordinary way (each head's
+      // driver is [b[done], b[done + 1]); the rows its stopped launches
+      // appended are the start of its delta, and insert-if-absent keeps them)
       if (pass >= max_iterations)
         return c->fail(XL_CONVERGENCE_FAILURE, "iteration cap " + std::to_string(max_iterations) +
                                                    " reached before the fixpoint");
-      const int64_t round_begin = (int64_t)b[done + 1];
-      h->dbeg = (int64_t)b[done];
-      h->dend = round_begin;
-      begin_round(h);
+      std::vector<int64_t> rb(nh);
+      for (int q = 0; q < nh; ++q) {
+        HeadRun* h = heads[q].get();
+        rb[q] = (int64_t)hbnd(q)[done + 1];
+        h->dbeg = (int64_t)hbnd(q)[done];
+        h->dend = rb[q];
+        begin_round(h);
+      }
       for (RulePlan& p : s.variants) XL_TRY(eval_plan(p));
       ++pass;
       st->iterations++;
-      const int64_t d = h->nrows - round_begin;
+      int64_t d = 0;
+      for (int q = 0; q < nh; ++q) {
+        HeadRun* h = heads[q].get();
+        d += h->nrows - rb[q];
+        h->dbeg = rb[q];
+        h->dend = h->nrows;
+      }
       record(d);
       st->new_tuples_total += d;
-      h->dbeg = round_begin;
-      h->dend = h->nrows;
     }
     return XL_OK;
   }
@@ -2034,9 +2087,10 @@ struct Runner {
       const int64_t dn0 = h->dn;
       HIP_TRY(c, hipMemsetAsync(counters, 0, CNTB, c->stream));
       HIP_TRY(c, k::batch_init(bnd, B + 2, 0ull, (u64)dn0, c->stream));
-      batch_counters = counters;
-      batch_row_base = (u64)dn0;
-      batch_limit = (u64)(max_keys - h->keys);
+      h->b_cnt = counters;
+      h->b_bnd = bnd;
+      h->b_base = (u64)dn0;
+      h->b_limit = (u64)(max_keys - h->keys);
       for (int j = 0; j <= h->nkey; ++j) batch_rows[j] = brow[j].as<uint32_t>();
       batch_rows_cap = bcap;
       batch_idx = bidx.as<uint32_t>();
@@ -2044,12 +2098,12 @@ struct Runner {
       batch_acc = hashed ? acc.as<u64>() : nullptr;
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
       for (int j = 1; j <= K; ++j) {
-        batch_range = bnd + (j - 1);
+        batch_j = j;
         batch_round = h->round + (uint32_t)j;
         for (RulePlan& p : s.variants) {
           const xl_status e = eval_plan(p);
           if (e != XL_OK) {
-            batch_range = nullptr;
+            batch_j = 0;
             return e;
           }
         }
@@ -2057,7 +2111,7 @@ struct Runner {
         HIP_TRY(c, k::table16_rows_range(h->table.as<Slot16>(), batch_acc, bidx.as<uint32_t>(), bnd, j, bcap,
                                          h->kp, vt, h->fold, rows[0], rows[1], rows[2], c->stream));
       }
-      batch_range = nullptr;
+      batch_j = 0;
       batch_acc = nullptr;
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
       XL_TRY(ctl_read(c, blk.p, CNTB + 8 * (size_t)(K + 2), host.data()));
@@ -2725,10 +2779,11 @@ struct Runner {
     const int nst = (int)p.steps.size();
     const int nkst = nst > 0 ? nst : 1;
     Source src = resolve_driver(p);
-    if (batch_range && p.driver_delta) {  // batched rounds: the delta range is on the device
-      if (h->is_set) {
-        for (int j = 0; j < h->nkey; ++j) src.col[j] = h->rows[j].as<uint32_t>();
-        src.n = h->rows_cap;  // bounds the grid only
+    HeadRun* hd = batch_j && p.driver_delta ? head_of(p.driver) : nullptr;
+    if (hd) {  // batched rounds: the delta range is on the device
+      if (hd->is_set) {
+        for (int j = 0; j < hd->nkey; ++j) src.col[j] = hd->rows[j].as<uint32_t>();
+        src.n = hd->rows_cap;  // bounds the grid only
       } else {
         for (int j = 0; j <= h->nkey; ++j) src.col[j] = batch_rows[j];
         src.n = batch_rows_cap;
@@ -2806,26 +2861,26 @@ struct Runner {
       a.emit.key.shift = h->kp.shift;
       a.emit.val_slot = (int8_t)p.val_slot;
       a.emit.val_type = p.val_type;
-      if (batch_range) {
-        // batched rounds: the driver range, the append base, the load limit
-        // and the counters belong to the batch; nothing is read back
-        a.src_range = batch_range;
-        a.emit.counters = batch_counters;
-        a.emit.limit = batch_limit;
+      if (hd) {
+        // batched rounds: the driver's delta range, the target's append base,
+        // load limit and counters belong to the batch; nothing is read back
+        a.src_range = hd->b_bnd + (batch_j - 1);
+        a.emit.counters = h->b_cnt;
+        a.emit.limit = h->b_limit;
         a.emit.mask = (u64)h->cap - 1;
         if (h->is_set) {
           a.emit.mode = EM_SET;
           a.emit.table = h->table.as<u64>();
           a.emit.row_col[0] = h->rows[0].as<uint32_t>();
           a.emit.row_col[1] = h->nkey == 2 ? h->rows[1].as<uint32_t>() : h->rows[0].as<uint32_t>();
-          a.emit.row_base = batch_row_base;
+          a.emit.row_base = h->b_base;
           a.emit.row_cap = h->rows_cap;
         } else {
           a.emit.mode = h->is_minmax ? EM_MINMAX : EM_HAGG;
           a.emit.table16 = h->table.as<Slot16>();
           a.emit.is_max = h->agg == Agg::MAX;
           a.emit.round = batch_round;
-          a.emit.delta_idx = batch_idx + batch_row_base;
+          a.emit.delta_idx = batch_idx + h->b_base;
           a.emit.delta_lim = batch_delta_lim;
           a.emit.acc = batch_acc;
           a.emit.fold_kind = h->fold;
@@ -3510,7 +3565,7 @@ struct Runner {
       total = 0;
     }
     if (s.recursive && total > 0 && batched_sets(s)) {
-      XL_TRY(run_sets_batched(s, heads[0].get(), max_iterations));
+      XL_TRY(run_sets_batched(s, max_iterations));
       total = 0;
     }
     if (s.recursive && total > 0 && batched_values(s)) {

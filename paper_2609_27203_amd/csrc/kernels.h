@@ -86,6 +86,18 @@ hipError_t compact_u32(const uint32_t* src, const uint32_t* flag, const uint32_t
 // Batched set rounds (see the kernels' comment): bnd holds n entries.
 hipError_t batch_init(u64* bnd, int n, u64 b0, u64 b1, hipStream_t s);
 hipError_t batch_mark(u64* bnd, int j, const u64* counters, u64 base, hipStream_t s);
+// Batched rounds of several set heads: after round j, unless a launch of
+// any head overflowed (then every head's overflow flag is raised, so later
+// rounds of the batch do nothing for all of them), bnd[h][j + 1] = base[h] +
+// rows appended to head h in the batch so far.
+constexpr int MAX_BATCH_HEADS = 8;
+struct BatchMarks {
+  u64* bnd[MAX_BATCH_HEADS];
+  u64* cnt[MAX_BATCH_HEADS];
+  u64 base[MAX_BATCH_HEADS];
+  int n;
+};
+hipError_t batch_mark_heads(const BatchMarks& m, int j, hipStream_t s);
 hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap);
 
 // ---- hash tables ----

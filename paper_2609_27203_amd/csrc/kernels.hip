@@ -1625,6 +1625,20 @@ hipError_t batch_mark(u64* bnd, int j, const u64* counters, u64 base, hipStream_
   batch_mark_k<<<1, 64, 0, s>>>(bnd, j, counters, base);
   return hipGetLastError();
 }
+__global__ void batch_mark_heads_k(BatchMarks m, int j) {
+  if (threadIdx.x != 0) return;
+  u64 any = 0;
+  for (int h = 0; h < m.n; ++h) any |= m.cnt[h][CNT_OVERFLOW];
+  for (int h = 0; h < m.n; ++h) {
+    if (any) m.cnt[h][CNT_OVERFLOW] = 1ull;
+    else m.bnd[h][j + 1] = m.base[h] + m.cnt[h][CNT_APPENDED];
+  }
+}
+hipError_t batch_mark_heads(const BatchMarks& m, int j, hipStream_t s) {
+  if (m.n <= 0 || m.n > MAX_BATCH_HEADS) return hipErrorInvalidValue;
+  batch_mark_heads_k<<<1, 64, 0, s>>>(m, j);
+  return hipGetLastError();
+}
 
 hipError_t stage_launch(const StageArgs& a, hipStream_t s, int grid_cap) {
   if (a.src.n <= 0) return hipSuccess;

@@ -575,6 +575,67 @@ def test_hash_value_rounds_cap_and_round_count(kind, batch):
         assert reads[20] == reads[50]
 
 
+PARITY_RULES = """
+odd(X,Y) :- edge(X,Y).
+even(X,Y) :- odd(X,Z), edge(Z,Y).
+odd(X,Y) :- even(X,Z), edge(Z,Y).
+"""
+PARITY_IDB = {"odd": ("i32", "i32"), "even": ("i32", "i32")}
+
+
+@pytest.mark.parametrize("growth", [False, True])
+@pytest.mark.parametrize("batch", [1, 4, 64])
+@pytest.mark.parametrize("name", ["tc_uniform", "tc_rmat_count"])
+def test_hash_mutual_recursion_batched(name, batch, growth):
+    """Two set heads in one recursive stratum (walks of odd and of even
+    length: each head's delta drives the other's rule), held in hash tables
+    and batched: one row list, counter block and boundary list per head,
+    rounds marked complete for both heads or for neither.  With a tiny
+    initial table the batches overflow and the host re-runs the stopped
+    round for both heads.  Rows, per-pass delta sizes and pass counts equal
+    the round-by-round loop's; index mode 0 agrees too."""
+    base = W.small_workloads()[name]()
+    wl = W.Workload(f"parity_{name}", PARITY_RULES, {"edge": base.edb["edge"]}, PARITY_IDB)
+    print(f"case: batched mutual recursion {name} batch={batch} growth={growth}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    opts = {"index_mode": 1, "batched_rounds": batch}
+    if growth:
+        opts["hash_min_log2"] = 10
+    rels, stats, _ = engine_run(wl, options=opts)
+    _compare(wl, rels, ref)
+    round_by_round = engine_run(wl, options={"index_mode": 1, "batched_rounds": 0})[1]
+    assert stats["delta_rows"] == round_by_round["delta_rows"]
+    assert stats["iterations"] == round_by_round["iterations"]
+    if growth:
+        assert stats["table_grows"] > 0
+    _compare(wl, engine_run(wl, options={"index_mode": 0})[0], ref, " (index mode 0)")
+
+
+@pytest.mark.parametrize("batch", [0, 4, 64])
+def test_hash_mutual_recursion_cap_and_control_reads(batch):
+    """Odd/even walks along a chain of n nodes take n - 1 passes: the cap ends
+    the run with XL_CONVERGENCE_FAILURE at the same pass batched or not, and
+    at 64 rounds per read the control bytes read do not grow with the number
+    of rounds (chains of 20 and 50 nodes)."""
+    from paper_2609_27203_amd import xlh
+    reads = {}
+    for n in (20, 50):
+        src = np.arange(n - 1, dtype=np.int32)
+        wl = W.Workload(f"parity_chain{n}", PARITY_RULES, _edges(src, src + 1), PARITY_IDB)
+        print(f"case: mutual recursion chain n={n} batch={batch}", flush=True)
+        opts = {"index_mode": 1, "batched_rounds": batch}
+        rels, stats, _ = engine_run(wl, options=opts, workspace_bytes=256 << 20)
+        assert len(rels["odd"][0]) + len(rels["even"][0]) == n * (n - 1) // 2
+        assert stats["iterations"] == n - 1 and stats["delta_rows"] == list(range(n - 1, -1, -1))
+        reads[n] = stats["control_bytes_read"]
+        with pytest.raises(xlh.XlError) as ei:
+            engine_run(wl, options=opts, max_iterations=n - 2, workspace_bytes=256 << 20)
+        assert ei.value.status_name == "XL_CONVERGENCE_FAILURE"
+        engine_run(wl, options=opts, max_iterations=n - 1, workspace_bytes=256 << 20)
+    if batch == 64:
+        assert reads[20] == reads[50]
+
+
 @pytest.mark.parametrize("batch", [0, 4, 64])
 def test_hash_same_generation_rounds_and_control_reads(batch):
     """Same generation in hash tables (index mode 1; the recursive rule joins
