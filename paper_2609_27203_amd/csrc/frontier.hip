@@ -520,32 +520,38 @@ __global__ __launch_bounds__(FR_THREADS) void gather_round_k(GatherArgs g) {
 // with A receives the same Y values from A's delta row: the union U(A) of
 // e2's Y lists over the B bits of the delta row (words [in_lo, in_hi) only)
 // is built once in LDS with the wave-balanced push expansion of the frontier
-// kernels, its nonzero words are listed in order, and each such word is ORed
-// into the head row of every X of A with one device atomic whose old value
-// gives the bits new to X; those go to X's next delta row (several A may reach
-// one X, so that is an atomic too), raise X's flag and widen its word bounds.
-// The work is the words the round touches, not whole rows.
-__global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
-  extern __shared__ uint32_t lds[];
+// kernels, and each nonzero word of U is ORed into the head row of every X
+// of A with one device atomic whose old value gives the bits new to X; those
+// go to X's next delta row (several A may reach one X, so that is an atomic
+// too), raise X's flag and widen its word bounds.  One wavefront per
+// workgroup handles one delta row at a time: a row's work is a chain of
+// dependent global accesses (flag, word range, delta words, e2 offsets, Y
+// lists, X list, atomics), most rows on a forest are small, and rows in
+// flight, not threads per row, set the pace.
+constexpr uint32_t GA_STEP = 16;             // delta words decoded per step
+constexpr uint32_t GA_ZCAP = GA_STEP * 32;   // B values listed per step, at most
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+  for (int k = 32; k > 0; k >>= 1) x = min(x, (uint32_t)__shfl_xor(x, k, 64));
+  return x;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  for (int k = 32; k > 0; k >>= 1) x = max(x, (uint32_t)__shfl_xor(x, k, 64));
+  return x;
+}
+
+__global__ __launch_bounds__(64) void gather_by_a_k(GatherArgs g) {
+  extern __shared__ uint32_t U[];  // union of this A's Y values: zero between delta rows
+  __shared__ uint32_t zlist[GA_ZCAP];
+  __shared__ uint32_t s_excl[64], s_beg[64];
   const uint32_t W = g.row_words;
-  uint32_t* U = lds;       // union of this A's Y values: zero between delta rows
-  uint32_t* tw = lds + W;  // indexes of U's nonzero words, ascending
-  __shared__ FrontierShared L;
-  __shared__ uint32_t s_umin, s_umax;
-  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const int lane = lane_id();
   u64 cands = 0, fresh = 0;
   const FrontierArgs& a = g.push;
   const uint32_t* ycol = a.idx.col[a.ybind_col];
   const uint32_t* xcol = g.e1a.col[g.e1_xcol];
-  uint32_t* zlist = L.zlist;
-  auto& s_excl = L.s_excl;
-  auto& s_beg = L.s_beg;
-  for (uint32_t i = threadIdx.x; i < W; i += FR_THREADS) U[i] = 0u;
-  if (threadIdx.x == 0) {
-    s_umin = 0xffffffffu;
-    s_umax = 0u;
-  }
-  __syncthreads();
+  for (uint32_t i = lane; i < W; i += 64) U[i] = 0u;
+  wave_lds_sync();
   for (int64_t ar64 = blockIdx.x; ar64 < g.range0; ar64 += gridDim.x) {
     const uint32_t ar = (uint32_t)ar64;
     if (!g.in_flag[ar]) continue;  // (uniform: no delta row)
@@ -559,30 +565,21 @@ __global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
     const uint32_t* frow = g.in_bits + (u64)ar * W;
     const uint32_t we = min(g.in_hi[ar], W);
     uint32_t umin = 0xffffffffu, umax = 0u;  // this lane's words of U touched
-    for (uint32_t cb = g.in_lo[ar]; cb < we;) {
-      // decode words [cb, cb + 512) of the delta row, two per thread, cut so
-      // the B list holds at most FR_ZCAP values
-      const uint32_t w0 = cb + 2u * threadIdx.x;
-      const uint32_t d0 = w0 < we ? frow[w0] : 0u, d1 = w0 + 1 < we ? frow[w0 + 1] : 0u;
-      const uint32_t c = __popc(d0) + __popc(d1);
-      uint32_t tot;
-      uint32_t pos = block_excl_scan_u32(c, &tot, L.s_w);
-      if (pos + c <= FR_ZCAP) {
-        for (uint32_t bits = d0; bits; bits &= bits - 1)
-          zlist[pos++] = (uint32_t)a.lo1 + w0 * 32u + (uint32_t)(__ffs(bits) - 1);
-        for (uint32_t bits = d1; bits; bits &= bits - 1)
-          zlist[pos++] = (uint32_t)a.lo1 + (w0 + 1) * 32u + (uint32_t)(__ffs(bits) - 1);
-      } else if (pos <= FR_ZCAP) {
-        L.s_cut[0] = pos;
-        L.s_cut[1] = 2u * threadIdx.x;
-      }
-      __syncthreads();
-      const uint32_t nz = tot <= FR_ZCAP ? tot : L.s_cut[0];
-      cb += tot <= FR_ZCAP ? 2u * FR_THREADS : L.s_cut[1];
+    for (uint32_t cb = g.in_lo[ar]; cb < we; cb += GA_STEP) {
+      // the B values of delta words [cb, cb + GA_STEP), in order
+      const uint32_t wi = cb + (uint32_t)lane;
+      const uint32_t d = lane < (int)GA_STEP && wi < we ? frow[wi] : 0u;
+      const uint32_t c = __popc(d);
+      const uint32_t incl = wave_incl_scan(c);
+      const uint32_t nz = __shfl(incl, 63, 64);
+      uint32_t pos = incl - c;
+      for (uint32_t bits = d; bits; bits &= bits - 1)
+        zlist[pos++] = (uint32_t)a.lo1 + wi * 32u + (uint32_t)(__ffs(bits) - 1);
+      wave_lds_sync();
       // each B's Y list: rows of 64 or more by the whole wavefront, smaller
       // ones through a scan and a six-step owner search
-      for (uint32_t j0 = 0; j0 < nz; j0 += FR_WAVES * 64) {
-        const uint32_t r = j0 + (uint32_t)lane * FR_WAVES + (uint32_t)w;
+      for (uint32_t j0 = 0; j0 < nz; j0 += 64) {
+        const uint32_t r = j0 + (uint32_t)lane;
         uint32_t beg = 0, deg = 0;
         if (r < nz) {
           const uint32_t k2 = zlist[r] - (uint32_t)a.idx.key_lo;
@@ -594,10 +591,10 @@ __global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
         const bool big = deg >= 64;
         u64 bigm = __ballot(big);
         const uint32_t sdeg = big ? 0u : deg;
-        const uint32_t incl = wave_incl_scan(sdeg);
-        const uint32_t total = __shfl(incl, 63, 64);
-        s_excl[w][lane] = incl - sdeg;
-        s_beg[w][lane] = beg;
+        const uint32_t sincl = wave_incl_scan(sdeg);
+        const uint32_t total = __shfl(sincl, 63, 64);
+        s_excl[lane] = sincl - sdeg;
+        s_beg[lane] = beg;
         wave_lds_sync();
         if (lane == 0) cands += total;
         while (bigm) {
@@ -619,8 +616,8 @@ __global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
             int q = 0;
 #pragma unroll
             for (int step = 32; step > 0; step >>= 1)
-              if (s_excl[w][q + step] <= j) q += step;
-            const uint32_t y = ycol[s_beg[w][q] + (j - s_excl[w][q])] - (uint32_t)a.lo1;
+              if (s_excl[q + step] <= j) q += step;
+            const uint32_t y = ycol[s_beg[q] + (j - s_excl[q])] - (uint32_t)a.lo1;
             const uint32_t bit = 1u << (y & 31);
             umin = min(umin, y >> 5);
             umax = max(umax, y >> 5);
@@ -629,52 +626,37 @@ __global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
         }
         wave_lds_sync();
       }
-      __syncthreads();
     }
-    if (umin <= umax) {
-      atomicMin(&s_umin, umin);
-      atomicMax(&s_umax, umax);
-    }
-    __syncthreads();
-    // U's nonzero words, in order, within the touched range
-    const uint32_t lo = s_umin, hi = s_umin <= s_umax ? min(s_umax + 1u, W) : s_umin;
-    const uint32_t span = hi > lo ? hi - lo : 0u;
-    const uint32_t per = (span + FR_THREADS - 1) / FR_THREADS;
-    const uint32_t p0 = lo + threadIdx.x * per, p1 = min(hi, p0 + per);
-    uint32_t cnt = 0;
-    for (uint32_t i = p0; i < p1; ++i) cnt += U[i] != 0u;
-    uint32_t nt;
-    uint32_t pos = block_excl_scan_u32(cnt, &nt, L.s_w);
-    for (uint32_t i = p0; i < p1; ++i)
-      if (U[i]) tw[pos++] = i;
-    __syncthreads();
+    umin = wave_min_u32(umin);
+    umax = wave_max_u32(umax);
+    if (umin > umax) continue;  // (uniform: no Y value; U is still zero)
+    const uint32_t hi = min(umax + 1u, W);
     uint32_t nb = 0;
-    const uint32_t total = n1 * nt;  // below 2^32: X values times row words
-    for (uint32_t p = threadIdx.x; p < total; p += FR_THREADS) {
-      const uint32_t q = p / nt, k = p - q * nt, wi = tw[k];
+    for (uint32_t q = 0; q < n1; ++q) {
       const uint32_t xr = xcol[b1 + q] - (uint32_t)g.lo0;
       if ((int64_t)xr >= g.range0) continue;  // outside the head's rows (not planned)
-      if (k == 0) {  // X's next delta row may get bits in these words
-        atomicMin(&g.out_lo[xr], tw[0]);
-        atomicMax(&g.out_hi[xr], tw[nt - 1] + 1u);
+      if (lane == 0) {  // X's next delta row may get bits in these words
+        atomicMin(&g.out_lo[xr], umin);
+        atomicMax(&g.out_hi[xr], hi);
       }
-      const uint32_t u = U[wi];
-      const u64 at = (u64)xr * W + wi;
-      const uint32_t nw = u & ~atomicOr(g.bits + at, u);
-      if (nw) {
-        atomicOr(g.out_bits + at, nw);
-        g.out_flag[xr] = 1u;
-        nb += (uint32_t)__popc(nw);
+      bool any = false;
+      for (uint32_t wi = umin + (uint32_t)lane; wi < hi; wi += 64) {
+        const uint32_t u = U[wi];
+        if (!u) continue;
+        const u64 at = (u64)xr * W + wi;
+        const uint32_t nw = u & ~atomicOr(g.bits + at, u);
+        if (nw) {
+          atomicOr(g.out_bits + at, nw);
+          nb += (uint32_t)__popc(nw);
+          any = true;
+        }
       }
+      if (__ballot(any) && lane == 0) g.out_flag[xr] = 1u;
     }
     fresh += nb;
-    __syncthreads();  // every word of U is read before it is cleared
-    for (uint32_t i = threadIdx.x; i < nt; i += FR_THREADS) U[tw[i]] = 0u;
-    if (threadIdx.x == 0) {
-      s_umin = 0xffffffffu;
-      s_umax = 0u;
-    }
-    __syncthreads();
+    wave_lds_sync();  // every word of U is read before it is cleared
+    for (uint32_t wi = umin + (uint32_t)lane; wi < hi; wi += 64) U[wi] = 0u;
+    wave_lds_sync();
   }
   const u64 c = wave_incl_scan_t<u64>(cands), fr = wave_incl_scan_t<u64>(fresh);
   if (lane == 63) {
@@ -685,11 +667,20 @@ __global__ __launch_bounds__(FR_THREADS) void gather_by_a_k(GatherArgs g) {
 
 hipError_t gather_round(const GatherArgs& a, hipStream_t s) {
   if (a.range0 <= 0) return hipSuccess;
-  const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 2048);
-  if (a.by_a)
-    gather_by_a_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
-  else
+  if (a.by_a) {
+    // eight single-wavefront workgroups per compute unit: measured on the
+    // 20,000-node forest, 2,048 wavefronts take 0.60 ms per run against 0.71
+    // with 1,024, 0.66 with 3,072 and 0.94 with 8,192
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 8 * (int64_t)std::max(cus, 1));
+    gather_by_a_k<<<grid, 64, (size_t)a.row_words * sizeof(uint32_t), s>>>(a);
+  } else {
+    const unsigned grid = (unsigned)std::min<int64_t>(a.range0, 2048);
     gather_round_k<<<grid, FR_THREADS, (size_t)a.row_words * 2 * sizeof(uint32_t), s>>>(a);
+  }
   return hipGetLastError();
 }
 
@@ -762,23 +753,40 @@ __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int6
                                                       uint32_t row_words, const uint32_t* off,
                                                       int32_t lo0, int32_t lo1, uint32_t* c0,
                                                       uint32_t* c1, u64 cap) {
-  __shared__ uint32_t stage[256 * 32];
+  __shared__ __align__(16) uint32_t stage[256 * 32 + 4];
   __shared__ uint32_t s_w[4];
   for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
     const uint32_t* row = bits + (u64)r * row_words;
     u64 out = off[r];
     const uint32_t x = (uint32_t)lo0 + (uint32_t)r;
+    const uint4 xq = make_uint4(x, x, x, x);
     for (uint32_t cb = 0; cb < row_words; cb += 256) {
       const uint32_t wi = cb + threadIdx.x;
       const uint32_t d = wi < row_words ? row[wi] : 0u;
+      // value i of the chunk goes to stage[sh + i] and to output position
+      // out + i, so stage index s and position out - sh + s agree modulo 4:
+      // whole quads are one 16-byte LDS read and two 16-byte stores
+      const uint32_t sh = (uint32_t)(out & 3u);
       uint32_t n;
-      uint32_t pos = block_excl_scan_u32(__popc(d), &n, s_w);
+      uint32_t pos = sh + block_excl_scan_u32(__popc(d), &n, s_w);
       for (uint32_t b = d; b; b &= b - 1) stage[pos++] = (uint32_t)lo1 + wi * 32u + (uint32_t)(__ffs(b) - 1);
       __syncthreads();
-      for (uint32_t i = threadIdx.x; i < n; i += 256) {
-        if (out + i < cap) {
-          c0[out + i] = x;
-          c1[out + i] = stage[i];
+      const uint32_t end = sh + n;
+      const u64 base = out - sh;
+      for (uint32_t q = threadIdx.x; q < (end + 3u) / 4u; q += 256) {
+        const uint32_t s0 = 4u * q;
+        const u64 p = base + s0;
+        if (s0 >= sh && s0 + 4u <= end && p + 4u <= cap) {
+          *reinterpret_cast<uint4*>(c1 + p) = *reinterpret_cast<const uint4*>(stage + s0);
+          *reinterpret_cast<uint4*>(c0 + p) = xq;
+        } else {
+#pragma unroll
+          for (uint32_t k = 0; k < 4u; ++k) {
+            if (s0 + k >= sh && s0 + k < end && p + k < cap) {
+              c0[p + k] = x;
+              c1[p + k] = stage[s0 + k];
+            }
+          }
         }
       }
       out += n;
