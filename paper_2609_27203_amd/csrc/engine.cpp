@@ -2298,11 +2298,10 @@ struct Runner {
     IndexProbe fwd{};
     XL_TRY(get_index(sp.rel, sp.key_col, &fwd, -1, nullptr, 0, true));
     const int B = c->batched_rounds;
-    Buf acc, rounds, list, tmp;
+    Buf acc, rounds, list;
     XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
     XL_TRY(dalloc(c, (size_t)B * 4, &rounds, "round delta sizes"));
     XL_TRY(dalloc(c, (size_t)nsd * 4, &list, "marked keys"));
-    XL_TRY(dalloc(c, k::bits_list_temp_bytes(nsd), &tmp, "compaction scratch"));
     HIP_TRY(c, hipMemsetAsync(acc.p, 0, 8 * CNT_N, c->stream));
     std::vector<hipEvent_t> evs;
     if (c->profile) {
@@ -2323,12 +2322,12 @@ struct Runner {
         break;
       }
       const int nb = (int)std::min<int64_t>(B, max_iterations - pass);
+      HIP_TRY(c, hipMemsetAsync(rounds.p, 0, (size_t)nb * 4, c->stream));
       for (int r = 0; r < nb; ++r) {
         uint32_t* nr = rounds.as<uint32_t>() + r;
         HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
                                      h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
-        HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, nullptr, nr, tmp.p, false, c->stream));
-        HIP_TRY(c, k::bits_list(h->dchg.as<uint32_t>(), nsd, list.as<uint32_t>(), nr, tmp.p, true, c->stream));
+        HIP_TRY(c, k::bits_list_waves(h->dchg.as<uint32_t>(), nsd, list.as<uint32_t>(), nr, c->stream));
         DensePullArgs q{};
         XL_TRY(pull_args(p, h, fast, fcol, q));
         q.list = list.as<uint32_t>();

@@ -187,6 +187,7 @@ hipError_t dense_delta_rows(const uint32_t* idx, int64_t n, const uint32_t* vals
 // in two calls on the same temp (write=false counts into *total; write=true
 // writes the list and clears the bits).
 size_t bits_list_temp_bytes(int64_t nbits);
+hipError_t bits_list_waves(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, hipStream_t s);
 hipError_t bits_list(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, void* temp, bool write,
                      hipStream_t s);
 hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);

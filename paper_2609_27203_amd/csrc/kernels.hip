@@ -1704,6 +1704,51 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
   }
 }
 
+// Marked slots -> slot list in one pass, clearing the marks: each wavefront
+// takes 256 consecutive words (four per lane, lane-major, so the loads
+// coalesce), reserves its entries with one atomic on *total and writes them
+// in word order.  The list is ascending within each wavefront's range and
+// the ranges land in any order: for consumers that take each listed key on
+// its own (the dense pull folds every key's in-edges itself).  *total must
+// be zero before the launch.
+constexpr int LW_WORDS = 4;
+__global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t nw, uint32_t* list, uint32_t* total) {
+  const int lane = lane_id();
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  for (int64_t w0 = (((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6) * 64 * LW_WORDS; w0 < nw;
+       w0 += nwaves * 64 * LW_WORDS) {
+    uint32_t d[LW_WORDS], c[LW_WORDS], run[LW_WORDS], all = 0;
+#pragma unroll
+    for (int k = 0; k < LW_WORDS; ++k) {
+      const int64_t wi = w0 + k * 64 + lane;
+      d[k] = wi < nw ? bits[wi] : 0u;
+      c[k] = (uint32_t)__popc(d[k]);
+      const uint32_t incl = wave_incl_scan(c[k]);
+      run[k] = all + incl - c[k];
+      all += __shfl(incl, 63, 64);
+    }
+    if (all == 0) continue;  // (wave-uniform)
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(total, all);
+    base = __shfl(base, 0, 64);
+#pragma unroll
+    for (int k = 0; k < LW_WORDS; ++k) {
+      if (!d[k]) continue;
+      const int64_t wi = w0 + k * 64 + lane;
+      bits[wi] = 0u;
+      uint32_t p = base + run[k];
+      for (uint32_t b = d[k]; b; b &= b - 1) list[p++] = (uint32_t)wi * 32u + (uint32_t)(__ffs(b) - 1);
+    }
+  }
+}
+hipError_t bits_list_waves(uint32_t* bits, int64_t nbits, uint32_t* list, uint32_t* total, hipStream_t s) {
+  const int64_t nw = (nbits + 31) / 32;
+  if (nw <= 0) return hipSuccess;
+  const int64_t waves = (nw + 64 * LW_WORDS - 1) / (64 * LW_WORDS);
+  bits_list_waves_k<<<(unsigned)std::min<int64_t>((waves + 3) / 4, 2048), 256, 0, s>>>(bits, nw, list, total);
+  return hipGetLastError();
+}
+
 // Rows (k0, k1) of the set bits of a dense key bitmap, in bit order: bit b
 // is k0 = lo0 + b / row_bits, k1 = lo1 + b % row_bits (one key: k0 = lo0 + b).
 // Optionally clears the words it read (a delta bitmap).  A workgroup owns
