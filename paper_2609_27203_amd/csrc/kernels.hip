@@ -225,15 +225,37 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter_k(const K* kin, const u
     wave_lds_sync();
   }
   __syncthreads();
+  // the tile's keys in output order in LDS (digit, then wave, then rank), so
+  // each digit's run goes out as consecutive stores
+  __shared__ K sk[RS_TILE];
+  __shared__ uint32_t sv[RS_TILE];
+  __shared__ uint32_t toff[256], s_w[RS_WAVES];
+  {
+    uint32_t t = 0;
+    for (int ww = 0; ww < RS_WAVES; ++ww) t += cnt[ww][threadIdx.x];
+    uint32_t tot;
+    toff[threadIdx.x] = block_excl_scan_u32(t, &tot, s_w);
+  }
+  __syncthreads();
 #pragma unroll
   for (int i = 0; i < RS_ITEMS; ++i) {
     const uint32_t d = dig[i];
     if (d == 0xffffffffu) continue;
     uint32_t pre = 0;
     for (int ww = 0; ww < w; ++ww) pre += cnt[ww][d];
-    const uint32_t pos = off[(size_t)d * nblocks + blockIdx.x] + pre + rank[i];
-    kout[pos] = key[i];
-    if (vout) vout[pos] = val[i];
+    const uint32_t lp = toff[d] + pre + rank[i];
+    sk[lp] = key[i];
+    sv[lp] = val[i];
+  }
+  __syncthreads();
+  const int64_t t0 = (int64_t)blockIdx.x * RS_TILE;
+  const uint32_t tile_n = (uint32_t)min((int64_t)RS_TILE, n - t0);
+  for (uint32_t q = threadIdx.x; q < tile_n; q += RS_THREADS) {
+    const K k = sk[q];
+    const uint32_t d = (uint32_t)(k >> shift) & dmask;
+    const uint32_t pos = off[(size_t)d * nblocks + blockIdx.x] + (q - toff[d]);
+    kout[pos] = k;
+    if (vout) vout[pos] = sv[q];
   }
 }
 
