@@ -22,6 +22,11 @@ constexpr uint32_t FR_ZCAP = 4096;  // Z (or Y) values decoded per step
 constexpr int FR_PROBE = 4;         // in-edges a pulling lane loads at once: one aligned 16-B block
 constexpr int FR_UNROLL = 8;        // first in-edges a pulling lane tests together
 constexpr uint32_t FR_LONG = 64;    // longer remaining in-edge lists are scanned by the whole wave
+// A round pulls only while the delta holds at least 1/FR_PULL_BETA of the
+// row's bits (besides pull_ratio * |delta| >= unreached targets): a small
+// delta pushes, as in direction-optimizing breadth-first search, since a
+// pull would re-test the in-edges of targets it cannot reach.
+constexpr uint32_t FR_PULL_BETA = 64;
 
 
 // Workgroup totals of two per-thread counts (one barrier pair).
@@ -298,7 +303,8 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_round_k(FrontierArgs a) {
     }
     uint32_t tnd, tnu;
     block_sum2(nd, nu, &tnd, &tnu, L.s_w, L.s_w2);
-    const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
+    const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu &&
+                      (u64)tnd * FR_PULL_BETA >= (u64)W * 32u;
     frontier_expand(a, old_row, new_row, f_row, pull, L, cands);
     // next delta row = new bits; write back the changed words of row x
     uint32_t nnew = 0;
@@ -388,7 +394,8 @@ __global__ __launch_bounds__(FR_THREADS) void frontier_resident_k(FrontierArgs a
         ++round;                       // this round finds nothing and ends x's passes
         break;
       }
-      const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu;
+      const bool pull = a.pull_ratio && (u64)a.pull_ratio * tnd >= (u64)tnu &&
+                        (u64)tnd * FR_PULL_BETA >= (u64)W * 32u;
       frontier_expand(a, old_row, new_row, f_row, pull, L, cands);
       // the new bits become the next delta; the row takes them
       nd = 0;
