@@ -18,7 +18,9 @@ Prints one JSON line:
   duration and the 8 TB/s peak.  `frac_algorithmic` prices the same launch
   in the method's own units: 12 B per join-output candidate (each derived
   (x, z) times the out-degree of z, whether the kernel pushes or pulls) and
-  24 B per new tuple;
+  24 B per new tuple.  `achievable_peak` is a 4 GiB device-to-device copy's
+  rate on this device.  `on_chip` prices the kernel's examined candidates
+  against the rate of its per-candidate step alone (csrc/ceiling.hip);
 * per_config: the five workloads (and the triangle join), each 3 warm-up and
   10 timed runs (median, min, max), with the same two fractions for its
   dominant kernel and for the whole run;
@@ -214,6 +216,8 @@ def per_config(args, W, xlh, torch):
         med = statistics.median(ev)
         f = fractions(name, wl, ctx, stats, med)
         derived = stats[-1]["derived_tuples"]
+        if f["units"].get("C"):
+            f["join_output_candidates_per_s"] = f["units"]["C"] / (med * 1e-3)
         res[name] = {"workload": DESCRIPTIONS[name], "derived_tuples": derived,
                      "iterations": stats[-1]["iterations"],
                      "ms_per_run": {"median": med, "min": min(ev), "max": max(ev),
@@ -235,6 +239,26 @@ def per_config(args, W, xlh, torch):
 # head), over the headline graph's edge target column.
 # ---------------------------------------------------------------------------
 FRONTIER_LDS_BYTES = 18944 + 3 * 2048
+
+
+def copy_bandwidth(torch, gib=4):
+    """Achievable HBM bandwidth on this device: a plain device-to-device copy
+    of `gib` GiB (read + write bytes over the best of three event-timed runs)."""
+    n = gib << 30
+    x = torch.empty(n, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    x.fill_(1)
+    best = 0.0
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        y.copy_(x)
+        e1.record()
+        e1.synchronize()
+        best = max(best, 2 * n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del x, y
+    torch.cuda.empty_cache()
+    return best
 
 
 def candidate_ceiling(col, torch):
@@ -589,8 +613,11 @@ def main():
     del ctx, prog
     torch.cuda.empty_cache()
 
+    achievable = copy_bandwidth(torch)
     roofline = {"bound": "hbm", "achieved": f["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": f["frac"], "traffic": f["traffic"],
+                "achievable_peak": achievable,
+                "frac_of_achievable": f["achieved"] / achievable if f["achieved"] else None,
                 "achieved_algorithmic": f["achieved_algorithmic"], "frac_algorithmic": f["frac_algorithmic"],
                 "algorithmic_bytes_per_launch": f["algorithmic_bytes_per_launch"],
                 "kernel": f["kernel"], "launches_per_step": f["launches_per_run"],
