@@ -24,9 +24,9 @@ Prints one JSON line:
 * per_config: the five workloads (and the triangle join), each 3 warm-up and
   10 timed runs (median, min, max), with the same two fractions for its
   dominant kernel and for the whole run;
-* cpu_baseline: the CPU oracle on a bounded sample of each workload, run in
-  parallel on the host's cores (one process per core, each evaluating its
-  own share of the sampled first keys).
+* cpu_baseline: the CPU oracle's semi-naive mode on a bounded sample of each
+  workload, run in parallel on the host's cores (one process per core, each
+  evaluating its own share of the sampled first keys).
 """
 from __future__ import annotations
 
@@ -286,25 +286,26 @@ def candidate_ceiling(col, torch):
 
 
 # ---------------------------------------------------------------------------
-# CPU baseline: the oracle, unchanged, on a bounded sample of each workload.
+# CPU baseline: the oracle's semi-naive mode, unchanged, on a bounded sample
+# of each workload.
 # Each worker process evaluates its own share of the sampled first keys
 # (sources, nodes or driver values); the wall time spans the first start to
 # the last end of the workers' evaluations.
 # ---------------------------------------------------------------------------
-CPU_SAMPLE = {  # first keys per worker
+CPU_SAMPLE = {  # first keys per worker (about one to two seconds of one core each)
     "tc_uniform": None,        # all sources, split over the workers
-    "tc_rmat_count": 16,
+    "tc_rmat_count": 32,
     "sssp": 1,
-    "lse_dag": 2,
-    "same_generation": 400,
-    "triangle": 2000,
+    "lse_dag": 4,
+    "same_generation": 800,
+    "triangle": 4000,
 }
 _WL_CACHE = {}
 
 
 def _cpu_job(job):
     name, part, nparts, seed = job
-    from oracle import evaluate
+    from oracle.seminaive import evaluate_semi_naive as evaluate
     from paper_2609_27203_amd import workloads as W
     if name not in _WL_CACHE:
         _WL_CACHE[name] = W.full_workloads()[name]()
@@ -365,9 +366,9 @@ def cpu_baselines(names, workers):
             keys = sum(p[1] for p in parts)
             wall = max(p[3] for p in parts) - min(p[2] for p in parts)
             out[name] = {"value": rows / wall, "unit": "derived tuples/s", "cores": workers, "kind": "oracle",
-                         "sample": f"naive evaluation (numpy) of {keys} sampled first keys of the full "
-                                   f"workload, split over {workers} processes: {rows} derived rows in "
-                                   f"{wall:.2f} s wall",
+                         "sample": f"semi-naive evaluation (the oracle's Algorithm 1 mode, numpy) of {keys} "
+                                   f"sampled first keys of the full workload, split over {workers} processes: "
+                                   f"{rows} derived rows in {wall:.2f} s wall",
                          "host": f"{cpu_model()}; {len(os.sched_getaffinity(0))} cores visible"}
             print(f"cpu {name}: {rows / wall:.4g} tuples/s", file=sys.stderr, flush=True)
     return out

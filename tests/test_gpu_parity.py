@@ -392,13 +392,19 @@ low(S,Y,min(D)) :- low(S,Z,D1), edge(Z,Y,W), D is D1 - W.
 high(S,S,max(D)) :- source(S), D is 0.
 high(S,Y,max(D)) :- high(S,Z,D1), iedge(Z,Y,K), D is D1 - K.
 """, {"high": ("i32", "i32", "i32")}),
-    # sum over derivations of C1 - K (the dense pull's one-subtract form)
+    # a sum seeded through subtraction (a recursive sum carries its value
+    # unchanged: a subtracted term would act once per pass, not once)
     "sum_i32": ("""
 ws(S,Y,sum(C)) :- source(S), iedge(S,Y,K), C is 0 - K.
-ws(S,Y,sum(C)) :- ws(S,Z,C1), iedge(Z,Y,K), C is C1 - K.
+ws(S,Y,sum(C)) :- ws(S,Z,C1), iedge(Z,Y,_), C is C1.
 """, {"ws": ("i32", "i32", "i32")}),
-    # logsumexp of P1 - W
+    # logsumexp of P1 - W (the dense pull's one-subtract form: a log-domain product)
     "lse_f32": ("""
+score(S,Y,logsumexp(P)) :- source(S), edge(S,Y,P).
+score(S,Y,logsumexp(P)) :- score(S,Z,P1), edge(Z,Y,W), P is P1 - W.
+""", {"score": ("i32", "i32", "f32")}),
+    # logsumexp of P1 - W - 1 (the general form)
+    "lse_f32_terms": ("""
 score(S,Y,logsumexp(P)) :- source(S), edge(S,Y,P).
 score(S,Y,logsumexp(P)) :- score(S,Z,P1), edge(Z,Y,W), P is P1 - W - 1.0.
 """, {"score": ("i32", "i32", "f32")}),

@@ -136,6 +136,19 @@ def test_self_join_gets_one_delta_variant_per_recursive_atom():
      "h(X,Y,Z) :- e(X,Y), e(Y,Z), e(X,Z).\nh(X,Y,Z) :- e(Y,X), e(Y,Z), e(X,Z).", "XL_UNSUPPORTED"),
     ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Z) :- e(X,Y), e(Y,Z), h(X,Z,Y).", "XL_UNSUPPORTED"),
     ({"e": I2, "h": ("i32", "i32", "i32")}, "h(X,Y,Y) :- e(X,Y), e(Y,Y), e(X,Y).", "XL_UNSUPPORTED"),
+    # a recursive sum carries the recursive atom's value unchanged, a
+    # recursive logsumexp adds terms to it, and neither compares it: folding
+    # each pass's contributions then gives the naive fixpoint's values
+    ({"w": ("i32", "i32", "i32"), "s": ("i32", "i32", "i32")},
+     "s(X,Y,sum(C)) :- w(X,Y,C).\ns(X,Y,sum(C)) :- s(X,Z,C1), w(Z,Y,K), C is C1 - K.", "XL_UNSUPPORTED"),
+    ({"w": ("i32", "i32", "i32"), "s": ("i32", "i32", "i32")},
+     "s(X,Y,sum(C)) :- w(X,Y,C).\ns(X,Y,sum(C)) :- s(X,Z,C1), w(Z,Y,C).", "XL_UNSUPPORTED"),
+    ({"w": ("i32", "i32", "i32"), "s": ("i32", "i32", "i32")},
+     "s(X,Y,sum(C)) :- w(X,Y,C).\ns(X,Y,sum(C)) :- s(X,Z,C1), w(Z,Y,_), C1 > 3, C is C1.", "XL_UNSUPPORTED"),
+    ({"w": W3, "s": W3}, "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), w(Z,Y,W), P is W - P1.",
+     "XL_UNSUPPORTED"),
+    ({"w": W3, "s": W3}, "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,_), w(Z,Y,P).",
+     "XL_UNSUPPORTED"),
 ])
 def test_rejected_programs(rels, text, status):
     c = _ctx(rels)
@@ -212,3 +225,19 @@ def test_options():
                  ("product_joins", 3), ("batched_rounds", 65)]:
         with pytest.raises(xlh.XlError):
             c.set_option(k, v)
+
+
+@pytest.mark.parametrize("text", [
+    "s(X,Y,sum(C)) :- w(X,Y,C).\ns(X,Y,sum(C)) :- s(X,Z,C1), w(Z,Y,_), C is C1.",
+    "s(X,Y,sum(C1)) :- w(X,Y,C1).\ns(X,Y,sum(C1)) :- s(X,Z,C1), w(Z,Y,K), K > 0.",
+])
+def test_recursive_path_sums_are_accepted(text):
+    _ctx({"w": ("i32", "i32", "i32"), "s": ("i32", "i32", "i32")}).compile(text)
+
+
+@pytest.mark.parametrize("text", [
+    "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), w(Z,Y,W), P is P1 + W.",
+    "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), w(Z,Y,W), W > -2.0, P is P1 - W - 1.0.",
+])
+def test_recursive_log_domain_products_are_accepted(text):
+    _ctx({"w": W3, "s": W3}).compile(text)
