@@ -26,8 +26,13 @@
  * sum and logsumexp only when every recursive rule of the stratum is linear
  * (the delta of round k holds the fold of the contributions derived from the
  * delta of round k-1, and the full relation accumulates them -- finite only
- * when derivations are acyclic, otherwise the iteration cap is reached);
- * count never (XL_UNSUPPORTED).
+ * when derivations are acyclic, otherwise the iteration cap is reached) and
+ * carries the recursive atom's value through a semiring product: a
+ * recursive sum takes that value unchanged (C is C1), a recursive logsumexp
+ * that value plus other terms (P is P1 + W), and neither compares it or
+ * tests it in a negated literal -- the forms for which accumulating the
+ * rounds gives the naive fixpoint's values; count never.  Every other
+ * recursive aggregate rule is XL_UNSUPPORTED at compile time.
  *
  * Memory.  The caller owns a device workspace and a HIP stream; the library
  * sub-allocates every relation, index, hash table and delta buffer from that
