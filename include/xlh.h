@@ -21,8 +21,11 @@
  * merge, until every delta is empty.
  *
  * Aggregates inside recursion go beyond the paper (its stratifier rejects
- * them, Sec. 3.5).  They are accepted as follows: min and max in any
- * recursive rule (the delta holds keys that are new or strictly improved);
+ * them, Sec. 3.5).  They are accepted as follows: min and max when each
+ * recursive rule uses each recursive atom's value at most once, added into
+ * the head's value (D is D1 + W, D is D1 + D2), and neither compares it nor
+ * tests it in a negated literal (a monotone tropical product; the delta
+ * holds keys that are new or strictly improved);
  * sum and logsumexp only when every recursive rule of the stratum is linear
  * (the delta of round k holds the fold of the contributions derived from the
  * delta of round k-1, and the full relation accumulates them -- finite only

@@ -861,48 +861,61 @@ xl_status compile_program(Context* ctx, const char* text, Program** out) {
         if (ha == Agg::SUM || ha == Agg::LSE)
           return bad(XL_UNSUPPORTED, "rule '" + r.text + "': sum and logsumexp need linear recursion (one recursive atom)");
       }
-      // A recursive sum/logsumexp rule must carry the recursive atom's value
-      // through a semiring product, so that folding each pass's contributions
-      // into the relation gives the fixpoint's value: for sum the head's
-      // value is that value itself (path sums), for logsumexp that value
-      // plus other terms (a log-domain product).  A term added to a sum, or
-      // a comparison on the carried value, would act once per pass in which
-      // the key's value changes instead of once.
-      if (rec.size() == 1) {
+      // A recursive aggregate rule must carry each recursive atom's value
+      // through a semiring product, so that folding each pass's
+      // contributions into the relation gives the naive fixpoint's values:
+      // for sum the head's value is that value itself (path sums); for
+      // logsumexp that value plus other terms (a product in the log domain);
+      // for min and max each recursive atom's value at most once, added
+      // (a tropical product; min and max are idempotent, so passes that
+      // re-derive a key change nothing).  A term added to a sum, a value that
+      // enters with a minus sign, or a comparison or negated literal on a
+      // carried value would act once per pass in which a key's value changes
+      // instead of on the fixpoint's value.
+      {
         const Agg ha = prog->head_agg(ctx->find(r.head));
-        if (ha == Agg::SUM || ha == Agg::LSE) {
-          const AtomAst& ra = r.atoms[rec[0]];
-          const Term& vt = ra.args.back();
-          const std::string why = "rule '" + r.text + "': a recursive " + (ha == Agg::SUM ? "sum" : "logsumexp") +
-                                  " must carry the recursive atom's value ";
-          if (vt.kind != Term::VAR)
-            return bad(XL_UNSUPPORTED, why + "(its value column holds no variable)");
-          bool ok = r.agg_var == vt.name;
-          for (const auto& as : r.assigns) {
-            int uses = 0, plus = 0;
-            for (const auto& pt : as.parts)
-              if (pt.second.kind == Term::VAR && pt.second.name == vt.name) {
-                ++uses;
-                plus += pt.first > 0;
-              }
-            if (as.var == r.agg_var) {
-              if (ha == Agg::SUM) ok = as.parts.size() == 1 && uses == 1 && plus == 1;
-              else ok = uses == 1 && plus == 1;
-            } else if (uses) {
-              ok = false;  // the carried value feeds another variable
-              break;
+        if (!rec.empty() && ha != Agg::NONE && ha != Agg::COUNT) {
+          const char* an = ha == Agg::SUM ? "sum" : ha == Agg::LSE ? "logsumexp" : ha == Agg::MIN ? "min" : "max";
+          const std::string why = "rule '" + r.text + "': a recursive " + an + " must carry the recursive atom's value ";
+          const char* form = ha == Agg::SUM ? "unchanged (C is C1)"
+                             : ha == Agg::LSE ? "plus other terms (P is P1 + ...)"
+                                              : "at most once, added (D is D1 + ...)";
+          for (int k : rec) {
+            const Term& vt = r.atoms[k].args.back();
+            if (vt.kind != Term::VAR) {
+              if (ha == Agg::SUM || ha == Agg::LSE) return bad(XL_UNSUPPORTED, why + "(its value column holds no variable)");
+              continue;
             }
+            int uses = r.agg_var == vt.name ? 1 : 0, plus = uses;
+            size_t nparts = 1;
+            for (const auto& as : r.assigns) {
+              int u = 0, pl = 0;
+              for (const auto& pt : as.parts)
+                if (pt.second.kind == Term::VAR && pt.second.name == vt.name) {
+                  ++u;
+                  pl += pt.first > 0;
+                }
+              if (as.var == r.agg_var) {
+                uses += u;
+                plus += pl;
+                nparts = as.parts.size();
+              } else if (u) {
+                return bad(XL_UNSUPPORTED, why + form);  // it feeds another variable
+              }
+            }
+            bool ok = uses == plus && uses <= 1;
+            if (ha == Agg::SUM) ok = ok && uses == 1 && nparts == 1;
+            if (ha == Agg::LSE) ok = ok && uses == 1;
+            if (!ok) return bad(XL_UNSUPPORTED, why + form);
+            for (const auto& cmp : r.cmps)
+              if ((cmp.lhs.kind == Term::VAR && cmp.lhs.name == vt.name) ||
+                  (cmp.rhs.kind == Term::VAR && cmp.rhs.name == vt.name))
+                return bad(XL_UNSUPPORTED, why + "without comparing it");
+            for (const auto& ng : r.negs)
+              for (const auto& t : ng.args)
+                if (t.kind == Term::VAR && t.name == vt.name)
+                  return bad(XL_UNSUPPORTED, why + "without testing it in a negated literal");
           }
-          if (!ok)
-            return bad(XL_UNSUPPORTED, why + (ha == Agg::SUM ? "unchanged (C is C1)" : "plus other terms (P is P1 + ...)"));
-          for (const auto& cmp : r.cmps)
-            if ((cmp.lhs.kind == Term::VAR && cmp.lhs.name == vt.name) ||
-                (cmp.rhs.kind == Term::VAR && cmp.rhs.name == vt.name))
-              return bad(XL_UNSUPPORTED, why + "without comparing it");
-          for (const auto& ng : r.negs)
-            for (const auto& t : ng.args)
-              if (t.kind == Term::VAR && t.name == vt.name)
-                return bad(XL_UNSUPPORTED, why + "without testing it in a negated literal");
         }
       }
       RulePlan full;

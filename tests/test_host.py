@@ -149,6 +149,13 @@ def test_self_join_gets_one_delta_variant_per_recursive_atom():
      "XL_UNSUPPORTED"),
     ({"w": W3, "s": W3}, "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,_), w(Z,Y,P).",
      "XL_UNSUPPORTED"),
+    # min and max: each carried value at most once, added, and not compared
+    ({"w": W3, "d": W3}, "d(X,Y,min(D)) :- w(X,Y,D).\nd(X,Y,min(D)) :- d(X,Z,D1), w(Z,Y,W), D is W - D1.",
+     "XL_UNSUPPORTED"),
+    ({"w": W3, "d": W3}, "d(X,Y,min(D)) :- w(X,Y,D).\nd(X,Y,min(D)) :- d(X,Z,D1), w(Z,Y,W), D1 > 1.0, D is D1 + W.",
+     "XL_UNSUPPORTED"),
+    ({"w": W3, "d": W3}, "d(X,Y,max(D)) :- w(X,Y,D).\nd(X,Y,max(D)) :- d(X,Z,D1), w(Z,Y,_), D is D1 + D1.",
+     "XL_UNSUPPORTED"),
 ])
 def test_rejected_programs(rels, text, status):
     c = _ctx(rels)
@@ -236,6 +243,9 @@ def test_recursive_path_sums_are_accepted(text):
 
 
 @pytest.mark.parametrize("text", [
+    "s(X,Y,min(P)) :- w(X,Y,P).\ns(X,Y,min(P)) :- s(X,Z,P1), w(Z,Y,W), P is P1 - W.",
+    "s(X,Y,max(P)) :- w(X,Y,P).\ns(X,Y,max(P)) :- s(X,Z,_), w(Z,Y,P).",
+    "s(X,Y,min(P)) :- w(X,Y,P).\ns(X,Y,min(P)) :- s(X,Z,P1), s(Z,Y,P2), P is P1 + P2.",
     "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), w(Z,Y,W), P is P1 + W.",
     "s(X,Y,logsumexp(P)) :- w(X,Y,P).\ns(X,Y,logsumexp(P)) :- s(X,Z,P1), w(Z,Y,W), W > -2.0, P is P1 - W - 1.0.",
 ])
