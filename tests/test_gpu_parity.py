@@ -671,13 +671,14 @@ def test_hash_same_generation_rounds_and_control_reads(batch):
 
 
 @pytest.mark.parametrize("batch", [0, 1, 4, 64])
-@pytest.mark.parametrize("tiles", [-1, 0, 1, 7])
+@pytest.mark.parametrize("tiles", [-1, 0, 1, 7, 94])
 def test_min_rounds_tiled_and_untiled(tiles, batch):
     """Carried min rule over a dense head: one workgroup per (source, tile of
     targets) with the tile in LDS (1 tile, 7 uneven tiles, the automatic
-    choice) or the untiled emission (-1), tiled rounds enqueued one at a
-    time or in batches of 1, 4 or 64 per host read; all match the oracle bit
-    for bit and give the same per-round delta sizes and pass count."""
+    choice, 94 tiles of 32 slots) or the untiled emission (-1), tiled rounds
+    enqueued one at a time or in batches of 1, 4 or 64 per host read; all
+    match the oracle bit for bit and give the same per-round delta sizes and
+    pass count."""
     wl = W.small_workloads()["sssp"]()
     print(f"case: min tiles={tiles} batch={batch}", flush=True)
     ref = evaluate(wl.rules, wl.edb, wl.idb)
