@@ -144,6 +144,8 @@ xl_status ctl_read(Context* c, const void* dev, size_t bytes, void* host) {
   return XL_OK;
 }
 
+constexpr int64_t BOUNDS_ONE_MAX = 65536;  // columns this short take one workgroup for their bounds
+
 int bitlen(uint64_t x) {  // bits needed to represent values 0..x
   int b = 0;
   while (x) {
@@ -590,6 +592,7 @@ struct HeadRun {
   int64_t fn = 0, fnew = 0;
   // dense count heads: one counter per key of the domain
   bool dcount = false;
+  bool vbounds = false;  // the value column's bounds were read with the rows
   Buf counts;
   int64_t range1 = 1;
   // dense value heads (min/max): value array over (rank of the first key in
@@ -3262,12 +3265,16 @@ struct Runner {
       r->lo[j] = (int32_t)h->dom_lo[j];
       r->hi[j] = (int32_t)h->dom_hi[j];
     }
-    if (h->nkey < r->arity && r->types[h->nkey] == T_I32) {
+    if (h->nkey < r->arity && r->types[h->nkey] == T_I32 && !h->vbounds) {
       Buf mm;
       XL_TRY(dalloc(c, 8, &mm, "bounds"));
-      const int32_t init[2] = {INT32_MAX, INT32_MIN};
-      HIP_TRY(c, hipMemcpyAsync(mm.p, init, 8, hipMemcpyHostToDevice, c->stream));
-      HIP_TRY(c, k::minmax_i32((const int32_t*)r->col[h->nkey], r->nrows, mm.as<int32_t>(), c->stream));
+      if (r->nrows <= BOUNDS_ONE_MAX) {
+        HIP_TRY(c, k::bounds_one((const int32_t*)r->col[h->nkey], nullptr, r->nrows, mm.as<int32_t>(), c->stream));
+      } else {
+        HIP_TRY(c, hipMemsetD32Async(mm.as<int32_t>(), INT32_MAX, 1, c->stream));
+        HIP_TRY(c, hipMemsetD32Async(mm.as<int32_t>() + 1, INT32_MIN, 1, c->stream));
+        HIP_TRY(c, k::minmax_i32((const int32_t*)r->col[h->nkey], r->nrows, mm.as<int32_t>(), c->stream));
+      }
       int32_t out[2];
       XL_TRY(ctl_read(c, mm.p, 8, out));
       r->lo[h->nkey] = out[0];
@@ -3343,7 +3350,35 @@ struct Runner {
       const int64_t n = h->range0 * h->range1;
       Buf tmp, tot;
       XL_TRY(dalloc(c, k::compact_temp_bytes(n), &tmp, "compaction scratch"));
-      XL_TRY(dalloc(c, 8, &tot, "count"));
+      XL_TRY(dalloc(c, 16, &tot, "count"));
+      if (n <= BOUNDS_ONE_MAX) {
+        // few slots: the rows go to columns sized for every slot, and their
+        // count and the value column's bounds come back in one read
+        Buf out[3];
+        for (int j = 0; j <= h->nkey; ++j) XL_TRY(dalloc(c, (size_t)std::max<int64_t>(n, 1) * 4, &out[j], "relation column"));
+        HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->kp, out[0].as<uint32_t>(),
+                                  h->nkey == 2 ? out[1].as<uint32_t>() : nullptr, out[h->nkey].as<uint32_t>(),
+                                  std::max<int64_t>(n, 1), tot.as<uint32_t>(), tmp.p, c->stream));
+        const bool i32 = r->types[h->nkey] == T_I32;
+        if (i32)
+          HIP_TRY(c, k::bounds_one(out[h->nkey].as<int32_t>(), tot.as<uint32_t>(), n, tot.as<int32_t>() + 1,
+                                   c->stream));
+        int32_t t[3] = {0, 0, 0};
+        XL_TRY(ctl_read(c, tot.p, i32 ? 12 : 4, t));
+        const uint32_t m = (uint32_t)t[0];
+        relation_free_storage(r);
+        for (int j = 0; j <= h->nkey; ++j) r->col[j] = (uint32_t*)out[j].keep();
+        r->nrows = (int64_t)m;
+        h->keys = (int64_t)m;
+        if (i32 && m > 0) {
+          r->lo[h->nkey] = t[1];
+          r->hi[h->nkey] = t[2];
+          h->vbounds = true;
+        }
+        if (r->max_rows > 0 && r->nrows > r->max_rows)
+          return c->fail(XL_CAPACITY_EXCEEDED, "relation " + r->name + " exceeds its max_rows");
+        return XL_OK;
+      }
       HIP_TRY(c, k::dcount_rows(h->counts.as<uint32_t>(), n, h->range1, h->kp, nullptr, nullptr, nullptr, 0,
                                 tot.as<uint32_t>(), tmp.p, c->stream));
       uint32_t m = 0;

@@ -38,6 +38,7 @@ hipError_t ordered_key(const uint32_t* col, int type, const uint32_t* perm, uint
 // out[0] = min, out[1] = max over an i32 column (out must be initialised by caller
 // to {INT32_MAX, INT32_MIN}).
 hipError_t minmax_i32(const int32_t* col, int64_t n, int32_t* out, hipStream_t s);
+hipError_t bounds_one(const int32_t* col, const uint32_t* count, int64_t cap, int32_t* out, hipStream_t s);
 // key[i] = col[i] - lo as unsigned.
 hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hipStream_t s);
 // off[k] = first i with sorted[i] >= k, for k in [0, range].

@@ -87,6 +87,47 @@ __global__ __launch_bounds__(SC_THREADS) void scan_apply_k(const T* in, T* out, 
   if (total && blockIdx.x == gridDim.x - 1 && threadIdx.x == SC_THREADS - 1) *total = pre;
 }
 
+// Arrays up to SC_ONE_MAX elements are scanned by one workgroup walking its
+// tiles in order (one launch instead of three: for a few tens of thousands
+// of elements the launches, not the bytes, set the time).
+constexpr int SC_ONE_THREADS = 1024;
+constexpr int64_t SC_ONE_MAX = 65536;
+
+template <typename T>
+__global__ __launch_bounds__(SC_ONE_THREADS) void scan_one_k(const T* in, T* out, int64_t n, T* total) {
+  __shared__ T s_w[SC_ONE_THREADS / 64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  T carry = 0;
+  for (int64_t b = 0; b < n; b += (int64_t)SC_ONE_THREADS * SC_ITEMS) {
+    const int64_t base = b + (int64_t)threadIdx.x * SC_ITEMS;
+    T v[SC_ITEMS];
+    T acc = 0;
+#pragma unroll
+    for (int i = 0; i < SC_ITEMS; ++i) {
+      v[i] = base + i < n ? in[base + i] : (T)0;
+      acc += v[i];
+    }
+    const T incl = wave_incl_scan_t<T>(acc);
+    if (lane == 63) s_w[w] = incl;
+    __syncthreads();
+    T pre = carry, tot = 0;
+    for (int i = 0; i < SC_ONE_THREADS / 64; ++i) {
+      const T y = s_w[i];
+      if (i < w) pre += y;
+      tot += y;
+    }
+    __syncthreads();
+    pre += incl - acc;
+#pragma unroll
+    for (int i = 0; i < SC_ITEMS; ++i) {
+      if (base + i < n) out[base + i] = pre;
+      pre += v[i];
+    }
+    carry += tot;
+  }
+  if (total && threadIdx.x == 0) *total = carry;
+}
+
 size_t scan_temp_bytes(int64_t n) {
   size_t bytes = 0;
   int64_t m = n;
@@ -105,6 +146,10 @@ static hipError_t scan_rec(const T* in, T* out, int64_t n, T* total, char* temp,
   }
   if (n <= SC_TILE) {
     scan_apply_k<T><<<1, SC_THREADS, 0, s>>>(in, out, n, nullptr, total);
+    return hipGetLastError();
+  }
+  if (n <= SC_ONE_MAX) {
+    scan_one_k<T><<<1, SC_ONE_THREADS, 0, s>>>(in, out, n, total);
     return hipGetLastError();
   }
   int64_t nb = (n + SC_TILE - 1) / SC_TILE;
@@ -383,6 +428,41 @@ __global__ void minmax_k(const int32_t* col, int64_t n, int32_t* out) {
 }
 hipError_t minmax_i32(const int32_t* col, int64_t n, int32_t* out, hipStream_t s) {
   minmax_k<<<grid_for(n, 256, 2048), 256, 0, s>>>(col, n, out);
+  return hipGetLastError();
+}
+
+// out = {min, max} of col[0, m), m = *count (at most cap) or cap when count
+// is null; {INT32_MAX, INT32_MIN} for no rows.  One workgroup, no
+// initialized output: for short columns (a few tens of thousands of rows).
+__global__ __launch_bounds__(1024) void bounds_one_k(const int32_t* col, const uint32_t* count, int64_t cap,
+                                                     int32_t* out) {
+  const int64_t m = count ? min((int64_t)*count, cap) : cap;
+  int32_t lo = INT32_MAX, hi = INT32_MIN;
+  for (int64_t i = threadIdx.x; i < m; i += 1024) {
+    lo = min(lo, col[i]);
+    hi = max(hi, col[i]);
+  }
+  for (int d = 32; d > 0; d >>= 1) {
+    lo = min(lo, __shfl_xor(lo, d, 64));
+    hi = max(hi, __shfl_xor(hi, d, 64));
+  }
+  __shared__ int32_t s_lo[16], s_hi[16];
+  if (lane_id() == 0) {
+    s_lo[threadIdx.x >> 6] = lo;
+    s_hi[threadIdx.x >> 6] = hi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 16; ++k) {
+      lo = min(lo, s_lo[k]);
+      hi = max(hi, s_hi[k]);
+    }
+    out[0] = lo;
+    out[1] = hi;
+  }
+}
+hipError_t bounds_one(const int32_t* col, const uint32_t* count, int64_t cap, int32_t* out, hipStream_t s) {
+  bounds_one_k<<<1, 1024, 0, s>>>(col, count, cap, out);
   return hipGetLastError();
 }
 
