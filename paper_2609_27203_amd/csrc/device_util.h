@@ -1,6 +1,9 @@
 // Wavefront and workgroup helpers shared by the HIP sources (wave64).
 #pragma once
 #include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <vector>
 #include <stdint.h>
 
 #include "kernels.h"
@@ -101,6 +104,41 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t x, uint32_t* to
   __syncthreads();
   *total = tot;
   return pre + incl - x;
+}
+
+// Workgroups of `threads` threads and `lds` dynamic LDS bytes of kernel k
+// that the current device keeps resident at once.
+// The answer is cached per (kernel, shape, device): a round-by-round launch
+// asks again every round.
+template <typename Kernel>
+static inline hipError_t resident_blocks(Kernel k, int threads, size_t lds, int* out) {
+  struct Entry {
+    const void* k;
+    int threads;
+    size_t lds;
+    int dev, blocks;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  {
+    std::lock_guard<std::mutex> g(mu);
+    for (const Entry& c : cache)
+      if (c.k == (const void*)k && c.threads == threads && c.lds == lds && c.dev == dev) {
+        *out = c.blocks;
+        return hipSuccess;
+      }
+  }
+  int cus = 0, per_cu = 0;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, lds);
+  if (e != hipSuccess) return e;
+  *out = std::max(1, cus * std::max(1, per_cu));
+  std::lock_guard<std::mutex> g(mu);
+  cache.push_back(Entry{(const void*)k, threads, lds, dev, *out});
+  return hipSuccess;
 }
 
 }  // namespace k

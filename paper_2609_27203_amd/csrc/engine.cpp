@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <functional>
 #include <memory>
 
 #include "engine.h"
@@ -1807,6 +1808,8 @@ struct Runner {
   // table; insert-if-absent keeps the partial round's rows valid).  Passes,
   // per-pass delta sizes and the iteration cap are those of the host loop.
   int batch_j = 0;              // round of the batch being enqueued (1-based; 0: not batching)
+  // run by the next stage launch after the launch and before its count read
+  std::function<xl_status()> before_count_read;
   int batch_grid = EMIT_GRID;  // workgroups of a batched launch (its waves bound the slack)
   // batched keyed value rounds: the batch's delta rows and slot list (one
   // position space: the first delta at [0, base), each round's slots and rows
@@ -3002,6 +3005,11 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
         HIP_TRY(c, k::stage_launch(a, c->stream, EMIT_GRID));
         if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
+        if (before_count_read) {  // work that does not need this launch's counts, enqueued before waiting for them
+          const auto f = std::move(before_count_read);
+          before_count_read = nullptr;
+          XL_TRY(f());
+        }
         u64 cnt[CNT_N];
         XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
         if (c->profile) {
@@ -3576,7 +3584,22 @@ struct Runner {
     XL_TRY(setup_heads(s));
     for (auto& h : heads) begin_round(h.get());
     XL_TRY(snapshot_head_indexes(s.full));
+    // A stratum that runs as one resident frontier launch builds that
+    // launch's indexes (inputs only) while its seed round runs: the host's
+    // launches then overlap the seed kernel instead of following its count
+    // read.
+    struct ClearHook {
+      std::function<xl_status()>& f;
+      ~ClearHook() { f = nullptr; }
+    } clear_hook{before_count_read};
+    if (s.recursive && heads.size() == 1 && heads[0]->resident && s.variants.size() == 1 &&
+        s.variants[0].driver_delta && head_of(s.variants[0].head) == heads[0].get())
+      before_count_read = [this, &s]() {
+        FrontierArgs f{};
+        return frontier_args(s.variants[0], heads[0].get(), f);
+      };
     for (RulePlan& p : s.full) XL_TRY(eval_plan(p));
+    before_count_read = nullptr;
     int64_t total = 0;
     for (auto& h : heads) {
       int64_t d = 0;

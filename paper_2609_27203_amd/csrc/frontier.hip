@@ -435,13 +435,10 @@ hipError_t frontier_resident(const FrontierArgs& a, unsigned grid, hipStream_t s
   if (!a.queue || !a.max_round || !a.overflow || !a.round_new || a.round_slots == 0) return hipErrorInvalidValue;
   const size_t lds = (size_t)a.row_words * 3 * sizeof(uint32_t);
   if (grid == 0) {
-    int dev = 0, cus = 0, per_cu = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess)
-      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, frontier_resident_k, FR_THREADS, lds);
+    int blocks = 0;
+    const hipError_t e = resident_blocks(frontier_resident_k, FR_THREADS, lds, &blocks);
     if (e != hipSuccess) return e;
-    grid = (unsigned)std::max(1, cus * std::max(1, per_cu));
+    grid = (unsigned)blocks;
   }
   grid = (unsigned)std::min<int64_t>(grid, a.nseg);
   frontier_resident_k<<<grid, FR_THREADS, lds, s>>>(a);

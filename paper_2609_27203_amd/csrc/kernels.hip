@@ -11,18 +11,6 @@
 namespace xlh {
 namespace k {
 
-// Workgroups of `threads` threads and `lds` dynamic LDS bytes of kernel k
-// that the current device keeps resident at once.
-template <typename Kernel>
-static hipError_t resident_blocks(Kernel k, int threads, size_t lds, int* out) {
-  int dev = 0, cus = 0, per_cu = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, threads, lds);
-  if (e != hipSuccess) return e;
-  *out = std::max(1, cus * std::max(1, per_cu));
-  return hipSuccess;
-}
 
 // ============================================================ scan
 constexpr int SC_THREADS = 256;
@@ -90,7 +78,10 @@ __global__ __launch_bounds__(SC_THREADS) void scan_apply_k(const T* in, T* out, 
 // Arrays up to SC_ONE_MAX elements are scanned by one workgroup walking its
 // tiles in order (one launch instead of three: for a few tens of thousands
 // of elements the launches, not the bytes, set the time).
+// Each thread owns SC_ONE_ITEMS consecutive elements of a tile, so one load
+// instruction of a wavefront covers a contiguous 1 KB (u32).
 constexpr int SC_ONE_THREADS = 1024;
+constexpr int SC_ONE_ITEMS = 4;
 constexpr int64_t SC_ONE_MAX = 65536;
 
 template <typename T>
@@ -98,12 +89,12 @@ __global__ __launch_bounds__(SC_ONE_THREADS) void scan_one_k(const T* in, T* out
   __shared__ T s_w[SC_ONE_THREADS / 64];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   T carry = 0;
-  for (int64_t b = 0; b < n; b += (int64_t)SC_ONE_THREADS * SC_ITEMS) {
-    const int64_t base = b + (int64_t)threadIdx.x * SC_ITEMS;
-    T v[SC_ITEMS];
+  for (int64_t b = 0; b < n; b += (int64_t)SC_ONE_THREADS * SC_ONE_ITEMS) {
+    const int64_t base = b + (int64_t)threadIdx.x * SC_ONE_ITEMS;
+    T v[SC_ONE_ITEMS];
     T acc = 0;
 #pragma unroll
-    for (int i = 0; i < SC_ITEMS; ++i) {
+    for (int i = 0; i < SC_ONE_ITEMS; ++i) {
       v[i] = base + i < n ? in[base + i] : (T)0;
       acc += v[i];
     }
@@ -119,7 +110,7 @@ __global__ __launch_bounds__(SC_ONE_THREADS) void scan_one_k(const T* in, T* out
     __syncthreads();
     pre += incl - acc;
 #pragma unroll
-    for (int i = 0; i < SC_ITEMS; ++i) {
+    for (int i = 0; i < SC_ONE_ITEMS; ++i) {
       if (base + i < n) out[base + i] = pre;
       pre += v[i];
     }
