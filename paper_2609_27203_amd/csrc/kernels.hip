@@ -1802,23 +1802,29 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
 // coalesce), reserves its entries with one atomic on *total and writes them
 // in word order.  The list is ascending within each wavefront's range and
 // the ranges land in any order: for consumers that take each listed key on
-// its own (the dense pull folds every key's in-edges itself).  *total must
-// be zero before the launch.
+// its own (the dense pull folds every key's in-edges itself).  Each word
+// column's entries are staged in LDS (entry o at o + o / 32, so the lanes of
+// a nearly full column write different banks) and go out with consecutive
+// lanes on consecutive entries.  *total must be zero before the launch.
 constexpr int LW_WORDS = 4;
+constexpr int LW_STAGE = 64 * 32 + 64;  // one column's entries, padded
 __global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t nw, uint32_t* list, uint32_t* total) {
+  __shared__ uint32_t stage_all[4][LW_STAGE];
   const int lane = lane_id();
+  uint32_t* stage = stage_all[threadIdx.x >> 6];
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   for (int64_t w0 = (((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6) * 64 * LW_WORDS; w0 < nw;
        w0 += nwaves * 64 * LW_WORDS) {
-    uint32_t d[LW_WORDS], c[LW_WORDS], run[LW_WORDS], all = 0;
+    uint32_t d[LW_WORDS], run[LW_WORDS], cnt[LW_WORDS], all = 0;
 #pragma unroll
     for (int k = 0; k < LW_WORDS; ++k) {
       const int64_t wi = w0 + k * 64 + lane;
       d[k] = wi < nw ? bits[wi] : 0u;
-      c[k] = (uint32_t)__popc(d[k]);
-      const uint32_t incl = wave_incl_scan(c[k]);
-      run[k] = all + incl - c[k];
-      all += __shfl(incl, 63, 64);
+      const uint32_t c = (uint32_t)__popc(d[k]);
+      const uint32_t incl = wave_incl_scan(c);
+      run[k] = incl - c;
+      cnt[k] = __shfl(incl, 63, 64);
+      all += cnt[k];
     }
     if (all == 0) continue;  // (wave-uniform)
     uint32_t base = 0;
@@ -1826,11 +1832,17 @@ __global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t
     base = __shfl(base, 0, 64);
 #pragma unroll
     for (int k = 0; k < LW_WORDS; ++k) {
-      if (!d[k]) continue;
+      if (cnt[k] == 0) continue;  // (wave-uniform)
       const int64_t wi = w0 + k * 64 + lane;
-      bits[wi] = 0u;
-      uint32_t p = base + run[k];
-      for (uint32_t b = d[k]; b; b &= b - 1) list[p++] = (uint32_t)wi * 32u + (uint32_t)(__ffs(b) - 1);
+      if (d[k]) {
+        bits[wi] = 0u;
+        uint32_t o = run[k];
+        for (uint32_t b = d[k]; b; b &= b - 1, ++o) stage[o + (o >> 5)] = (uint32_t)wi * 32u + (uint32_t)(__ffs(b) - 1);
+      }
+      wave_lds_sync();
+      for (uint32_t o = (uint32_t)lane; o < cnt[k]; o += 64) list[base + o] = stage[o + (o >> 5)];
+      base += cnt[k];
+      wave_lds_sync();
     }
   }
 }
