@@ -846,19 +846,47 @@ __global__ __launch_bounds__(CP_THREADS) void compact_count_k(CompactArgs a) {
   if (threadIdx.x == 0) a.range_cnt[blockIdx.x] = tot;
 }
 
+// Each step ranks its 256 items by wavefront ballots and one exchange of
+// the four wavefront totals: one barrier per step, the exchange words
+// alternating between steps so that a step's writes never meet the previous
+// step's reads.
 __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
+  __shared__ uint32_t s_wc[2][CP_THREADS / 64];
   const int64_t base = (int64_t)blockIdx.x * a.rlen;
+  const int w = threadIdx.x >> 6;
+  // dense slots below 2^32 (the dense forms' limit) split with 32-bit division
+  const bool narrow = a.n <= (int64_t)0xffffffffll && a.nrank <= (int64_t)0xffffffffll &&
+                      a.range1 <= (int64_t)0xffffffffll;
   uint32_t out = a.range_off[blockIdx.x];
   for (int64_t k = 0; k < a.rlen / CP_THREADS; ++k) {
     const int64_t i = base + k * CP_THREADS + threadIdx.x;
     const bool keep = cp_keep(a, i);
-    uint32_t tot;
-    const uint32_t p = out + block_excl_scan<uint32_t>(keep ? 1u : 0u, &tot);
+    const u64 m = __ballot(keep);
+    uint32_t* wc = s_wc[k & 1];
+    if (lane_id() == 0) wc[w] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int j = 0; j < CP_THREADS / 64; ++j) {
+      const uint32_t c = wc[j];
+      pre += j < w ? c : 0u;
+      tot += c;
+    }
+    const uint32_t p = out + pre + (uint32_t)__popcll(m & lanemask_lt());
     if (keep && p < (u64)a.out_cap) {
       if (a.kind == CK_STAMP) {
         a.k0[p] = (uint32_t)i;
       } else if (a.kind == CK_DENSE) {
-        const int64_t rk = a.nrank ? i % a.nrank : i / a.range1, yb = a.nrank ? i / a.nrank : i % a.range1;
+        int64_t rk, yb;
+        if (narrow) {
+          const uint32_t i32 = (uint32_t)i, d = (uint32_t)(a.nrank ? a.nrank : a.range1);
+          const uint32_t q = i32 / d, r = i32 - q * d;
+          rk = a.nrank ? r : q;
+          yb = a.nrank ? q : r;
+        } else {
+          rk = a.nrank ? i % a.nrank : i / a.range1;
+          yb = a.nrank ? i / a.nrank : i % a.range1;
+        }
         a.k0[p] = a.dict[rk];
         if (a.k1) a.k1[p] = (uint32_t)yb + (uint32_t)a.kp.lo[1];
         a.v[p] = stored_value(a.counts[i], a.type, a.fold_kind);
