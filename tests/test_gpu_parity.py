@@ -848,6 +848,25 @@ def test_empty_edb():
     assert stats["iterations"] == 0
 
 
+@pytest.mark.parametrize("resident", [0, 1])
+def test_closure_and_count_over_many_first_keys(resident):
+    """20,000 first keys in chains of 8 nodes (a ragged last chain): the
+    per-key row counts are scanned by one workgroup walking 4,096-value
+    tiles (4,097 to 65,536 values), and the count head, 20,000 slots, is
+    compacted in one pass with its row count and value bounds in one read."""
+    n, chain = 20_000, 8
+    src = np.array([i for i in range(n - 1) if (i + 1) % chain], np.int64)
+    wl = W.Workload("chains", W.TC_COUNT_RULES, _edges(src, src + 1),
+                    {"path": ("i32", "i32"), "reach_count": ("i32", "i32")})
+    print(f"case: chains n={n} resident={resident}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"frontier_resident": resident})
+    _compare(wl, rels, ref)
+    assert stats["iterations"] == chain - 1
+    counts = rels["reach_count"][1]
+    assert counts.min() == 1 and counts.max() == chain - 1
+
+
 def test_self_loop_and_duplicates():
     wl = W.Workload("loops", W.TC_RULES, _edges([0, 0, 1, 1, 2], [0, 1, 2, 2, 0]), {"path": ("i32", "i32")})
     ref = evaluate(wl.rules, wl.edb, wl.idb)
