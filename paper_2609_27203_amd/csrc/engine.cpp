@@ -849,23 +849,18 @@ struct Runner {
         indexes.push_back(std::move(ix));
         return XL_OK;
       }
-      Buf keys, perm, perm2, tmp;
-      XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+      Buf perm, perm2, tmp;
       XL_TRY(dalloc(c, (size_t)n * 4, &perm, "index permutation"));
       XL_TRY(dalloc(c, (size_t)n * 4, &perm2, "index permutation"));
       XL_TRY(dalloc(c, k::radix_temp_bytes(n), &tmp, "sort scratch"));
-      HIP_TRY(c, k::sub_lo(rcol[col], klo, keys.as<uint32_t>(), n, c->stream));
-      HIP_TRY(c, k::iota_u32(perm.as<uint32_t>(), n, c->stream));
       uint32_t* sp = nullptr;
       if (ordered) {
-        // one sort by (key, order value); the offsets come from the sorted
-        // keys.  Degree order reads each order value's degree from the plain
+        // one sort by (key, order value), of 32-bit composite keys when
+        // both parts fit; the offsets come from the sorted keys' high bits.
+        // Degree order reads each order value's degree from the plain
         // index of rel by the order column (its row count as a key there).
         IndexProbe dz{};
         if (order_kind == 0) XL_TRY(get_index(rel, order_col, &dz, -1, nullptr, 0, true));
-        Buf k64, k64b;
-        XL_TRY(dalloc(c, (size_t)n * 8, &k64, "index order keys"));
-        XL_TRY(dalloc(c, (size_t)n * 8, &k64b, "index order keys"));
         // value order: the order column's bounds when known (a finished
         // relation, or a key column of a head), else the whole int32 range
         int32_t vlo = INT32_MIN;
@@ -879,22 +874,43 @@ struct Runner {
             vlo = (int32_t)oh->dom_lo[order_col];
             vbits = std::max(1, bitlen((uint64_t)(oh->dom_hi[order_col] - oh->dom_lo[order_col])));
           }
-          HIP_TRY(c, k::value_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], vlo, vbits, n,
-                                         k64.as<u64>(), c->stream));
-        } else {
-          HIP_TRY(c, k::degree_order_keys(keys.as<uint32_t>(), nullptr, rcol[order_col], dz.key_lo, dz.key_range,
-                                          dz.off, n, k64.as<u64>(), c->stream));
         }
         const int obits = order_kind == 1 ? vbits : 16;
+        const bool wide = obits + kbits > 32;
+        const size_t kw = wide ? 8 : 4;
+        Buf ka, kb;
+        XL_TRY(dalloc(c, (size_t)n * kw, &ka, "index order keys"));
+        XL_TRY(dalloc(c, (size_t)n * kw, &kb, "index order keys"));
+        HIP_TRY(c, k::order_keys(rcol[col], klo, rcol[order_col], order_kind == 1 ? vlo : dz.key_lo, obits,
+                                 order_kind == 1 ? nullptr : dz.off, dz.key_range, n, ka.p, wide,
+                                 perm.as<uint32_t>(), c->stream));
         int alt = 0;
-        HIP_TRY(c, k::radix_sort_u64(k64.as<u64>(), perm.as<uint32_t>(), k64b.as<u64>(), perm2.as<uint32_t>(), n,
-                                     obits + kbits, tmp.p, c->stream, &alt));
+        if (wide)
+          HIP_TRY(c, k::radix_sort_u64(ka.as<u64>(), perm.as<uint32_t>(), kb.as<u64>(), perm2.as<uint32_t>(), n,
+                                       obits + kbits, tmp.p, c->stream, &alt));
+        else
+          HIP_TRY(c, k::radix_sort_u32(ka.as<uint32_t>(), perm.as<uint32_t>(), kb.as<uint32_t>(),
+                                       perm2.as<uint32_t>(), n, obits + kbits, tmp.p, c->stream, &alt));
         sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
-        HIP_TRY(c, k::high_bits(alt ? k64b.as<u64>() : k64.as<u64>(), obits, n, keys.as<uint32_t>(), c->stream));
-        XL_TRY(offsets(keys.as<uint32_t>()));
+        const void* sk = alt ? kb.p : ka.p;
+        if (!compact) {
+          void* off;
+          XL_TRY(own((size_t)(range + 1) * 4, "index offsets", &off));
+          HIP_TRY(c, k::csr_offsets_high(sk, wide, obits, n, (uint32_t)range, (uint32_t*)off, c->stream));
+          p.off = (uint32_t*)off;
+          p.keys = nullptr;
+          p.key_range = (uint32_t)range;
+        } else {
+          Buf keys;
+          XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
+          HIP_TRY(c, k::high_bits(sk, wide, obits, n, keys.as<uint32_t>(), c->stream));
+          XL_TRY(offsets(keys.as<uint32_t>()));
+        }
       } else {
-        Buf keys2;
+        Buf keys, keys2;
+        XL_TRY(dalloc(c, (size_t)n * 4, &keys, "index keys"));
         XL_TRY(dalloc(c, (size_t)n * 4, &keys2, "index keys"));
+        HIP_TRY(c, k::keys_perm(rcol[col], klo, n, keys.as<uint32_t>(), perm.as<uint32_t>(), c->stream));
         int alt = 0;
         HIP_TRY(c, k::radix_sort_u32(keys.as<uint32_t>(), perm.as<uint32_t>(), keys2.as<uint32_t>(),
                                      perm2.as<uint32_t>(), n, kbits, tmp.p, c->stream, &alt));
@@ -902,12 +918,14 @@ struct Runner {
         sp = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
         XL_TRY(offsets(sk));
       }
+      uint32_t* cols[MAXC] = {};
       for (int j = 0; j < rel->arity; ++j) {
         void* cj;
         XL_TRY(own((size_t)n * 4, "index column", &cj));
-        HIP_TRY(c, k::gather_u32(rcol[j], sp, (uint32_t*)cj, n, c->stream));
-        p.col[j] = (uint32_t*)cj;
+        cols[j] = (uint32_t*)cj;
+        p.col[j] = cols[j];
       }
+      HIP_TRY(c, k::gather_cols(rcol, cols, rel->arity, sp, n, c->stream));
       if (ordered && order_kind == 0) {
         void* fp;
         XL_TRY(own((size_t)range * 4, "index first rows", &fp));
@@ -2552,12 +2570,14 @@ struct Runner {
                                  n, std::max(1, key_bits), tmp.p, c->stream, &alt));
     uint32_t* sk = alt ? keys2.as<uint32_t>() : keys.as<uint32_t>();
     uint32_t* spm = alt ? perm2.as<uint32_t>() : perm.as<uint32_t>();
+    uint32_t* tc[MAXC] = {};
     for (int j = 0; j < e->arity; ++j) {
       h->tcols.push_back(std::make_unique<Buf>());
       XL_TRY(dalloc(c, (size_t)n * 4, h->tcols.back().get(), "tiled index column"));
-      HIP_TRY(c, k::gather_u32(e->col[j], spm, h->tcols.back()->as<uint32_t>(), n, c->stream));
-      q.col[j] = h->tcols.back()->as<uint32_t>();
+      tc[j] = h->tcols.back()->as<uint32_t>();
+      q.col[j] = tc[j];
     }
+    HIP_TRY(c, k::gather_cols(e->col, tc, e->arity, spm, n, c->stream));
     if (presorted)  // the whole keys of the rows in their new order
       HIP_TRY(c, k::tile_keys(q.col[zc], q.col[p.carried_ycol], n, e->lo[zc], h->kp.lo[1], h->tile, h->ntiles,
                               (uint32_t)zr, false, sk, c->stream));

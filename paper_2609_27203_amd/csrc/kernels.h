@@ -32,6 +32,11 @@ hipError_t radix_sort_u64(u64* keys, uint32_t* vals, u64* keys_alt, uint32_t* va
 hipError_t iota_u32(uint32_t* out, int64_t n, hipStream_t s);
 hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n,
                       hipStream_t s);
+// dst[j][i] = src[j][perm[i]] for the ncols (<= MAXC) columns, one launch.
+hipError_t gather_cols(const uint32_t* const* src, uint32_t* const* dst, int ncols, const uint32_t* perm, int64_t n,
+                       hipStream_t s);
+// key[i] = col[i] - lo (unsigned) and perm[i] = i.
+hipError_t keys_perm(const uint32_t* col, int32_t lo, int64_t n, uint32_t* key, uint32_t* perm, hipStream_t s);
 // Order-preserving u32 image of a column: i32 signed order, f32 totalOrder.
 hipError_t ordered_key(const uint32_t* col, int type, const uint32_t* perm, uint32_t* out,
                        int64_t n, hipStream_t s);
@@ -50,21 +55,23 @@ hipError_t compact_offsets(const uint32_t* sorted, int64_t n, uint32_t* keys, ui
                            void* temp, hipStream_t s);
 hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
                        hipStream_t s);
-// key[i] = (sorted[i] << 16) | (0xffff - min(deg(zcol[perm[i]]), 0xffff)), deg
-// read from the CSR offsets off over keys [klo, klo + range); perm may be
-// null (identity), also in value_order_keys.
-hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol, int32_t klo,
-                             uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s);
+// The same over the high bits (key >> shift) of ascending 32-bit (wide
+// false) or 64-bit keys.
+hipError_t csr_offsets_high(const void* sorted, bool wide, int shift, int64_t n, uint32_t range, uint32_t* off,
+                            hipStream_t s);
+// Composite keys of an ordered index, 32-bit (wide false) or 64-bit, and
+// perm[i] = i: (kcol[i] - klo) << obits | order part, the order part being
+// 0xffff - min(deg(ocol[i]), 0xffff) with deg from the CSR offsets doff over
+// [olo, olo + drange) (degree order, obits 16), or ocol[i] - olo when doff is
+// null (value order, int32 values in [olo, olo + 2^obits)).
+hipError_t order_keys(const uint32_t* kcol, int32_t klo, const uint32_t* ocol, int32_t olo, int obits,
+                      const uint32_t* doff, uint32_t drange, int64_t n, void* key, bool wide, uint32_t* perm,
+                      hipStream_t s);
 // out[k] = col[off[k]] for keys k in [0, range) with rows, 0xffffffff otherwise.
 hipError_t segment_first(const uint32_t* off, const uint32_t* col, uint32_t range, uint32_t* out, hipStream_t s);
 // Packed keys of a negation table: c0[i], or (c0[i] << 32) | c1[i].
 hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key, hipStream_t s);
-// key[i] = (sorted[i] << vbits) | (vcol[perm[i]] - vlo) (unsigned), for int32
-// values in [vlo, vlo + 2^vbits): sorting by it keeps the key order and
-// orders each key's rows by the value.  vlo = INT32_MIN, vbits = 32 covers
-// every int32.
-hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
-                            int vbits, int64_t n, u64* key, hipStream_t s);
+
 // ---- worst-case-optimal triangle join (see WcojArgs) ----
 constexpr int WC_CHUNK = 256;  // items per wavefront chunk
 hipError_t wcoj_work(const WcojArgs& a, hipStream_t s);
@@ -74,8 +81,8 @@ hipError_t nonzero_flags(const uint32_t* v, int64_t n, uint32_t* flag, hipStream
 hipError_t wcoj_compact(const uint32_t* work, const uint32_t* pos, int64_t n, uint32_t* crow,
                         unsigned long long* cw, hipStream_t s);
 hipError_t wcoj_probe(const WcojArgs& a, bool materialize, hipStream_t s);
-// out[i] = key[i] >> shift
-hipError_t high_bits(const u64* key, int shift, int64_t n, uint32_t* out, hipStream_t s);
+// out[i] = key[i] >> shift, over 32-bit (wide false) or 64-bit keys
+hipError_t high_bits(const void* key, bool wide, int shift, int64_t n, uint32_t* out, hipStream_t s);
 // flag[i] = 1 if row i differs (bitwise) from row i-1 in any column (or i == 0).
 hipError_t row_change_flags(const uint32_t* const* cols, int ncols, int64_t n, uint32_t* flag,
                             hipStream_t s);

@@ -373,6 +373,45 @@ hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, 
   return hipGetLastError();
 }
 
+struct ColPtrsIn { const uint32_t* c[MAXC]; };
+struct ColPtrsOut { uint32_t* c[MAXC]; };
+
+// dst.c[j][i] = src.c[j][perm[i]] for every column j < ncols, one launch.
+__global__ void gather_cols_k(ColPtrsIn src, ColPtrsOut dst, int ncols, const uint32_t* perm, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t p = perm[i];
+    for (int j = 0; j < ncols; ++j) dst.c[j][i] = src.c[j][p];
+  }
+}
+hipError_t gather_cols(const uint32_t* const* src, uint32_t* const* dst, int ncols, const uint32_t* perm, int64_t n,
+                       hipStream_t s) {
+  if (n <= 0 || ncols <= 0) return hipSuccess;
+  if (ncols > MAXC) return hipErrorInvalidValue;
+  ColPtrsIn a{};
+  ColPtrsOut b{};
+  for (int j = 0; j < ncols; ++j) {
+    a.c[j] = src[j];
+    b.c[j] = dst[j];
+  }
+  gather_cols_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(a, b, ncols, perm, n);
+  return hipGetLastError();
+}
+
+// key[i] = col[i] - lo (unsigned) and perm[i] = i, one launch.
+__global__ void keys_perm_k(const uint32_t* col, int32_t lo, int64_t n, uint32_t* key, uint32_t* perm) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    key[i] = col[i] - (uint32_t)lo;
+    perm[i] = (uint32_t)i;
+  }
+}
+hipError_t keys_perm(const uint32_t* col, int32_t lo, int64_t n, uint32_t* key, uint32_t* perm, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  keys_perm_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(col, lo, n, key, perm);
+  return hipGetLastError();
+}
+
 __device__ __forceinline__ uint32_t order_bits(uint32_t x, int type) {
   if (type == T_F32) return x ^ ((x >> 31) ? 0xffffffffu : 0x80000000u);  // totalOrder
   return x ^ 0x80000000u;                                                  // signed int
@@ -467,20 +506,31 @@ hipError_t sub_lo(const uint32_t* col, int32_t lo, uint32_t* out, int64_t n, hip
   return hipGetLastError();
 }
 
-__global__ void csr_offsets_k(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off) {
+template <typename K>
+__global__ void csr_offsets_k(const K* sorted, int shift, int64_t n, uint32_t range, uint32_t* off) {
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k <= (int64_t)range;
        k += (int64_t)gridDim.x * blockDim.x) {
-    int64_t lo = 0, hi = n;  // first i with sorted[i] >= k
+    int64_t lo = 0, hi = n;  // first i with sorted[i] >> shift >= k
     while (lo < hi) {
       int64_t mid = (lo + hi) >> 1;
-      if ((int64_t)sorted[mid] < k) lo = mid + 1; else hi = mid;
+      if ((int64_t)(sorted[mid] >> shift) < k) lo = mid + 1; else hi = mid;
     }
     off[k] = (uint32_t)lo;
   }
 }
 hipError_t csr_offsets(const uint32_t* sorted, int64_t n, uint32_t range, uint32_t* off,
                        hipStream_t s) {
-  csr_offsets_k<<<grid_for((int64_t)range + 1, 256, 65536), 256, 0, s>>>(sorted, n, range, off);
+  csr_offsets_k<uint32_t><<<grid_for((int64_t)range + 1, 256, 65536), 256, 0, s>>>(sorted, 0, n, range, off);
+  return hipGetLastError();
+}
+hipError_t csr_offsets_high(const void* sorted, bool wide, int shift, int64_t n, uint32_t range, uint32_t* off,
+                            hipStream_t s) {
+  if (wide)
+    csr_offsets_k<u64><<<grid_for((int64_t)range + 1, 256, 65536), 256, 0, s>>>((const u64*)sorted, shift, n, range,
+                                                                                 off);
+  else
+    csr_offsets_k<uint32_t><<<grid_for((int64_t)range + 1, 256, 65536), 256, 0, s>>>((const uint32_t*)sorted, shift,
+                                                                                      n, range, off);
   return hipGetLastError();
 }
 
@@ -516,23 +566,37 @@ hipError_t compact_offsets(const uint32_t* sorted, int64_t n, uint32_t* keys, ui
   return hipGetLastError();
 }
 
-// key[i] = (sorted[i] << 16) | (0xffff - min(deg(z), 0xffff)) with z =
-// zcol[perm[i]] and deg(z) = off[z - klo + 1] - off[z - klo] (0 outside the
-// key range): sorting by it keeps the key order and puts, inside each key's
-// segment, the rows whose z has the most rows first.
-__global__ void degree_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol,
-                                    int32_t klo, uint32_t range, const uint32_t* off, int64_t n, u64* key) {
+// Composite sort key of row i of an ordered index and perm[i] = i, one
+// launch: the key column's image kcol[i] - klo in the high bits, below it
+// (obits bits) the order part -- degree order: 0xffff - min(deg(z), 0xffff)
+// with z = ocol[i] and deg(z) = doff[z - olo + 1] - doff[z - olo] (0
+// outside [olo, olo + drange)), so the rows whose z has the most rows come
+// first; value order: ocol[i] - olo.  Sorting by it keeps the key order.
+template <typename K>
+__global__ void order_keys_k(const uint32_t* kcol, int32_t klo, const uint32_t* ocol, int32_t olo, int obits,
+                             const uint32_t* doff, uint32_t drange, int64_t n, K* key, uint32_t* perm) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t kz = zcol[perm ? perm[i] : i] - (uint32_t)klo;
-    const uint32_t deg = kz < range ? off[kz + 1] - off[kz] : 0u;
-    key[i] = ((u64)sorted[i] << 16) | (0xffffu - (deg < 0xffffu ? deg : 0xffffu));
+    const uint32_t o = ocol[i] - (uint32_t)olo;
+    uint32_t part = o;
+    if (doff) {
+      const uint32_t deg = o < drange ? doff[o + 1] - doff[o] : 0u;
+      part = 0xffffu - (deg < 0xffffu ? deg : 0xffffu);
+    }
+    key[i] = ((K)(kcol[i] - (uint32_t)klo) << obits) | (K)part;
+    perm[i] = (uint32_t)i;
   }
 }
-hipError_t degree_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* zcol, int32_t klo,
-                             uint32_t range, const uint32_t* off, int64_t n, u64* key, hipStream_t s) {
+hipError_t order_keys(const uint32_t* kcol, int32_t klo, const uint32_t* ocol, int32_t olo, int obits,
+                      const uint32_t* doff, uint32_t drange, int64_t n, void* key, bool wide, uint32_t* perm,
+                      hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  degree_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, zcol, klo, range, off, n, key);
+  if (wide)
+    order_keys_k<u64><<<grid_for(n, 256, 65536), 256, 0, s>>>(kcol, klo, ocol, olo, obits, doff, drange, n, (u64*)key,
+                                                              perm);
+  else
+    order_keys_k<uint32_t><<<grid_for(n, 256, 65536), 256, 0, s>>>(kcol, klo, ocol, olo, obits, doff, drange, n,
+                                                                   (uint32_t*)key, perm);
   return hipGetLastError();
 }
 
@@ -563,28 +627,19 @@ hipError_t neg_keys(const uint32_t* c0, const uint32_t* c1, int64_t n, u64* key,
   return hipGetLastError();
 }
 
-__global__ void value_order_keys_k(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
-                                   int vbits, int64_t n, u64* key) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    key[i] = ((u64)sorted[i] << vbits) | (u64)(vcol[perm ? perm[i] : i] - (uint32_t)vlo);
-}
-hipError_t value_order_keys(const uint32_t* sorted, const uint32_t* perm, const uint32_t* vcol, int32_t vlo,
-                            int vbits, int64_t n, u64* key, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  value_order_keys_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(sorted, perm, vcol, vlo, vbits, n, key);
-  return hipGetLastError();
-}
-
 // out[i] = key[i] >> shift
-__global__ void high_bits_k(const u64* key, int shift, int64_t n, uint32_t* out) {
+template <typename K>
+__global__ void high_bits_k(const K* key, int shift, int64_t n, uint32_t* out) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     out[i] = (uint32_t)(key[i] >> shift);
 }
-hipError_t high_bits(const u64* key, int shift, int64_t n, uint32_t* out, hipStream_t s) {
+hipError_t high_bits(const void* key, bool wide, int shift, int64_t n, uint32_t* out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  high_bits_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(key, shift, n, out);
+  if (wide)
+    high_bits_k<u64><<<grid_for(n, 256, 65536), 256, 0, s>>>((const u64*)key, shift, n, out);
+  else
+    high_bits_k<uint32_t><<<grid_for(n, 256, 65536), 256, 0, s>>>((const uint32_t*)key, shift, n, out);
   return hipGetLastError();
 }
 
