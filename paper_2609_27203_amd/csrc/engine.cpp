@@ -1169,7 +1169,7 @@ struct Runner {
 
   xl_status alloc_table(HeadRun* h, int64_t cap, Buf* out) {
     XL_TRY(dalloc(c, (size_t)cap * slot_bytes(h), out, "hash table"));
-    HIP_TRY(c, hipMemsetAsync(out->p, 0xff, (size_t)cap * slot_bytes(h), c->stream));
+    HIP_TRY(c, k::fill_bytes(out->p, 0xff, (size_t)cap * slot_bytes(h), c->stream));
     return XL_OK;
   }
 
@@ -1184,9 +1184,9 @@ struct Runner {
                                            : (double)((h->range0 + 31) / 32) * 32.0;
     const size_t bytes = (size_t)(total_bits / 8);
     XL_TRY(dalloc(c, bytes, &h->bits, "dense key bitmap"));
-    HIP_TRY(c, hipMemsetAsync(h->bits.p, 0, bytes, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->bits.p, 0, bytes, c->stream));
     XL_TRY(dalloc(c, bytes, &h->dbits, "dense delta bitmap"));
-    HIP_TRY(c, hipMemsetAsync(h->dbits.p, 0, bytes, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->dbits.p, 0, bytes, c->stream));
     // the row list only holds loaded rows (the seed scans them); derived
     // tuples live in the bitmap and each round's delta in dbits
     h->rows_cap = std::max<int64_t>(h->preloaded, 1);
@@ -1203,7 +1203,7 @@ struct Runner {
     h->dbeg = h->dend = 0;
     if (h->gathered) {
       XL_TRY(dalloc(c, bytes, &h->gbits, "dense delta bitmap"));
-      HIP_TRY(c, hipMemsetAsync(h->gbits.p, 0, bytes, c->stream));
+      HIP_TRY(c, k::fill_bytes(h->gbits.p, 0, bytes, c->stream));
       for (int b = 0; b < 2; ++b) {
         XL_TRY(dalloc(c, (size_t)std::max<int64_t>(h->range0, 1) * 4, &h->gflag[b], "delta row flags"));
         HIP_TRY(c, hipMemsetAsync(h->gflag[b].p, 0, (size_t)std::max<int64_t>(h->range0, 1) * 4, c->stream));
@@ -1226,7 +1226,7 @@ struct Runner {
   xl_status init_dcount(HeadRun* h) {
     const size_t bytes = (size_t)h->range0 * (size_t)h->range1 * 4;
     XL_TRY(dalloc(c, bytes, &h->counts, "dense counters"));
-    HIP_TRY(c, hipMemsetAsync(h->counts.p, 0, bytes, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->counts.p, 0, bytes, c->stream));
     return XL_OK;
   }
 
@@ -1273,9 +1273,9 @@ struct Runner {
     XL_TRY(dalloc(c, ns * 4, &h->dvals, "dense values"));
     XL_TRY(dalloc(c, nw * 4, &h->dpres, "dense presence bits"));
     XL_TRY(dalloc(c, nw * 4, &h->dchg, "dense delta bits"));
-    HIP_TRY(c, hipMemsetAsync(h->dvals.p, 0xff, ns * 4, c->stream));
-    HIP_TRY(c, hipMemsetAsync(h->dpres.p, 0, nw * 4, c->stream));
-    HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nw * 4, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->dvals.p, 0xff, ns * 4, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->dpres.p, 0, nw * 4, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->dchg.p, 0, nw * 4, c->stream));
     if (h->tiled) XL_TRY(dalloc(c, (size_t)(n0 + 1) * 4, &h->roff, "delta rows per rank"));
     if (h->ds) {
       // target-major delta slots with whole words per target: y * nrank_d + rank
@@ -1285,9 +1285,9 @@ struct Runner {
       XL_TRY(dalloc(c, nwd * 4, &h->dcur_pres, "dense delta bits"));
       XL_TRY(dalloc(c, nwd * 4, &h->dnext_pres, "dense delta bits"));
       XL_TRY(dalloc(c, nwd * 4, &h->dchg, "dense delta marks"));
-      HIP_TRY(c, hipMemsetAsync(h->dcur_pres.p, 0, nwd * 4, c->stream));
-      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, nwd * 4, c->stream));
-      HIP_TRY(c, hipMemsetAsync(h->dchg.p, 0, nwd * 4, c->stream));
+      HIP_TRY(c, k::fill_bytes(h->dcur_pres.p, 0, nwd * 4, c->stream));
+      HIP_TRY(c, k::fill_bytes(h->dnext_pres.p, 0, nwd * 4, c->stream));
+      HIP_TRY(c, k::fill_bytes(h->dchg.p, 0, nwd * 4, c->stream));
     } else {
       XL_TRY(dalloc(c, ns * 4, &h->didx, "delta slot list"));
     }
@@ -1718,7 +1718,7 @@ struct Runner {
     XL_TRY(ctl_read(c, tot.p, 4, &nseg));
     HIP_TRY(c, k::gather_rows(h->dbits.as<uint32_t>(), h->row_words, h->fx.as<uint32_t>(), h->kp.lo[0], nseg,
                               h->fdiff[h->fcur].as<uint32_t>(), c->stream));
-    HIP_TRY(c, hipMemsetAsync(h->dbits.p, 0, (size_t)h->range0 * h->row_words * 4, c->stream));
+    HIP_TRY(c, k::fill_bytes(h->dbits.p, 0, (size_t)h->range0 * h->row_words * 4, c->stream));
     h->fn = nseg;
     return XL_OK;
   }
@@ -2364,7 +2364,7 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
         std::swap(h->dcur.p, h->dnext.p);
         std::swap(h->dcur_pres.p, h->dnext_pres.p);
-        HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)(nsd / 32) * 4, c->stream));
+        HIP_TRY(c, k::fill_bytes(h->dnext_pres.p, 0, (size_t)(nsd / 32) * 4, c->stream));
       }
       std::vector<uint32_t> n(nb);
       XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));
@@ -3164,7 +3164,7 @@ struct Runner {
       h->dn = h->pull_n;
       std::swap(h->dcur.p, h->dnext.p);
       std::swap(h->dcur_pres.p, h->dnext_pres.p);
-      HIP_TRY(c, hipMemsetAsync(h->dnext_pres.p, 0, (size_t)(h->nrank_d * h->range1 / 32) * 4, c->stream));
+      HIP_TRY(c, k::fill_bytes(h->dnext_pres.p, 0, (size_t)(h->nrank_d * h->range1 / 32) * 4, c->stream));
       *delta = h->dn;
       return XL_OK;
     }

@@ -29,6 +29,8 @@ hipError_t radix_sort_u64(u64* keys, uint32_t* vals, u64* keys_alt, uint32_t* va
                           int64_t n, int bits, void* temp, hipStream_t s, int* in_alt);
 
 // ---- small helpers ----
+// hipMemsetAsync's result; a kernel of 16-byte stores for 1 MB and more.
+hipError_t fill_bytes(void* p, int byte, size_t bytes, hipStream_t s);
 hipError_t iota_u32(uint32_t* out, int64_t n, hipStream_t s);
 hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n,
                       hipStream_t s);

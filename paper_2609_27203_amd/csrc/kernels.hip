@@ -78,43 +78,59 @@ __global__ __launch_bounds__(SC_THREADS) void scan_apply_k(const T* in, T* out, 
 // Arrays up to SC_ONE_MAX elements are scanned by one workgroup walking its
 // tiles in order (one launch instead of three: for a few tens of thousands
 // of elements the launches, not the bytes, set the time).
-// Each thread owns SC_ONE_ITEMS consecutive elements of a tile, so one load
-// instruction of a wavefront covers a contiguous 1 KB (u32).
+// Each thread owns SC_ONE_ITEMS consecutive elements of each of SC_ONE_SUB
+// sub-tiles, so one load instruction of a wavefront covers a contiguous 1 KB
+// (u32); a step loads all four sub-tiles at once and ranks them with one
+// workgroup scan of four sums per thread.
 constexpr int SC_ONE_THREADS = 1024;
 constexpr int SC_ONE_ITEMS = 4;
+constexpr int SC_ONE_SUB = 4;
 constexpr int64_t SC_ONE_MAX = 65536;
 
 template <typename T>
 __global__ __launch_bounds__(SC_ONE_THREADS) void scan_one_k(const T* in, T* out, int64_t n, T* total) {
-  __shared__ T s_w[SC_ONE_THREADS / 64];
+  __shared__ T s_w[SC_ONE_SUB][SC_ONE_THREADS / 64];
   const int lane = lane_id(), w = threadIdx.x >> 6;
+  constexpr int64_t SUB = (int64_t)SC_ONE_THREADS * SC_ONE_ITEMS;
   T carry = 0;
-  for (int64_t b = 0; b < n; b += (int64_t)SC_ONE_THREADS * SC_ONE_ITEMS) {
-    const int64_t base = b + (int64_t)threadIdx.x * SC_ONE_ITEMS;
-    T v[SC_ONE_ITEMS];
-    T acc = 0;
+  for (int64_t b = 0; b < n; b += SUB * SC_ONE_SUB) {
+    T v[SC_ONE_SUB][SC_ONE_ITEMS], acc[SC_ONE_SUB], incl[SC_ONE_SUB];
 #pragma unroll
-    for (int i = 0; i < SC_ONE_ITEMS; ++i) {
-      v[i] = base + i < n ? in[base + i] : (T)0;
-      acc += v[i];
-    }
-    const T incl = wave_incl_scan_t<T>(acc);
-    if (lane == 63) s_w[w] = incl;
-    __syncthreads();
-    T pre = carry, tot = 0;
-    for (int i = 0; i < SC_ONE_THREADS / 64; ++i) {
-      const T y = s_w[i];
-      if (i < w) pre += y;
-      tot += y;
-    }
-    __syncthreads();
-    pre += incl - acc;
+    for (int k = 0; k < SC_ONE_SUB; ++k) {
+      const int64_t base = b + k * SUB + (int64_t)threadIdx.x * SC_ONE_ITEMS;
+      acc[k] = 0;
 #pragma unroll
-    for (int i = 0; i < SC_ONE_ITEMS; ++i) {
-      if (base + i < n) out[base + i] = pre;
-      pre += v[i];
+      for (int i = 0; i < SC_ONE_ITEMS; ++i) {
+        v[k][i] = base + i < n ? in[base + i] : (T)0;
+        acc[k] += v[k][i];
+      }
     }
-    carry += tot;
+#pragma unroll
+    for (int k = 0; k < SC_ONE_SUB; ++k) {
+      incl[k] = wave_incl_scan_t<T>(acc[k]);
+      if (lane == 63) s_w[k][w] = incl[k];
+    }
+    __syncthreads();
+    T run = carry;
+#pragma unroll
+    for (int k = 0; k < SC_ONE_SUB; ++k) {
+      T pre = 0, tot = 0;
+      for (int j = 0; j < SC_ONE_THREADS / 64; ++j) {
+        const T y = s_w[k][j];
+        if (j < w) pre += y;
+        tot += y;
+      }
+      T o = run + pre + incl[k] - acc[k];
+      const int64_t base = b + k * SUB + (int64_t)threadIdx.x * SC_ONE_ITEMS;
+#pragma unroll
+      for (int i = 0; i < SC_ONE_ITEMS; ++i) {
+        if (base + i < n) out[base + i] = o;
+        o += v[k][i];
+      }
+      run += tot;
+    }
+    __syncthreads();
+    carry = run;
   }
   if (total && threadIdx.x == 0) *total = carry;
 }
@@ -370,6 +386,22 @@ __global__ void gather_k(const uint32_t* src, const uint32_t* perm, uint32_t* ds
 hipError_t gather_u32(const uint32_t* src, const uint32_t* perm, uint32_t* dst, int64_t n,
                       hipStream_t s) {
   gather_k<<<grid_for(n, 256, 65536), 256, 0, s>>>(src, perm, dst, n);
+  return hipGetLastError();
+}
+
+// Byte fill with 16-byte stores (large clears of bitmaps and value arrays):
+// n16 aligned quads, then the ntail bytes after them.
+__global__ void fill_k(uint4* p, int64_t n16, uint32_t v, uint8_t* tail, int ntail) {
+  const uint4 q = make_uint4(v, v, v, v);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = q;
+  if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = (uint8_t)v;
+}
+hipError_t fill_bytes(void* p, int byte, size_t bytes, hipStream_t s) {
+  if (bytes < ((size_t)1 << 20) || ((uintptr_t)p & 15u)) return hipMemsetAsync(p, byte, bytes, s);
+  const int64_t n16 = (int64_t)(bytes / 16);
+  const uint32_t v = (uint32_t)(byte & 0xff) * 0x01010101u;
+  fill_k<<<grid_for(n16, 256, 8192), 256, 0, s>>>((uint4*)p, n16, v, (uint8_t*)p + n16 * 16, (int)(bytes % 16));
   return hipGetLastError();
 }
 
