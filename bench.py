@@ -581,7 +581,7 @@ def main():
         copy_calibration()
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: this build runs on one "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the engine runs on one "
               "GPU only (the multi-GPU partitioning is a design, not code)", file=sys.stderr)
         sys.exit(2)
 

@@ -3,7 +3,7 @@ own T_P pieces.
 
 TEST INFRASTRUCTURE ONLY, like datalog.py: nothing in the engine imports it;
 the test suite checks it against the naive definition, and the benchmark's
-CPU-baseline leg times it (SURVEY's "semi-naive mode on all host cores").
+CPU-baseline leg times it on all host cores.
 
 Per stratum (strongly connected component of the IDB dependency graph, in
 dependency order):
