@@ -22,8 +22,9 @@ Prints one JSON line:
   rate on this device.  `on_chip` prices the kernel's examined candidates
   against the rate of its per-candidate step alone (csrc/ceiling.hip);
 * per_config: the five workloads (and the triangle join), each 3 warm-up and
-  10 timed runs (median, min, max), with the same two fractions for its
-  dominant kernel and for the whole run;
+  10 timed runs (median, min, max; without the engine's per-launch events),
+  with the same two fractions for its dominant kernel (launch durations
+  from three further runs with the events) and for the whole run;
 * cpu_baseline: the CPU oracle's semi-naive mode on a bounded sample of each
   workload, run in parallel on the host's cores (one process per core, each
   evaluating its own share of the sampled first keys).
@@ -197,11 +198,15 @@ def fractions(name, wl, ctx, stats_list, ms_run):
 
 
 def per_config(args, W, xlh, torch):
+    """Each workload: warm-up runs, then the timed runs without the engine's
+    per-launch events (ms per run), then three runs with them (the dominant
+    kernel's launch durations)."""
     res = {}
     for name in CONFIGS:
         wl = W.full_workloads()[name]()
         ctx, prog = make_context(wl, args, xlh)
         ev, wall, stats = [], [], []
+        ctx.set_option("profile", 0)
         for i in range(args.config_warmup + args.config_runs):
             for n in wl.idb:
                 ctx.relations[n].clear()
@@ -212,7 +217,11 @@ def per_config(args, W, xlh, torch):
             if i >= args.config_warmup:
                 wall.append(1e3 * (time.perf_counter() - t0))
                 ev.append(s["ms_total"])
-                stats.append(s)
+        ctx.set_option("profile", 1)
+        for _ in range(3):
+            for n in wl.idb:
+                ctx.relations[n].clear()
+            stats.append(prog.run())
         med = statistics.median(ev)
         f = fractions(name, wl, ctx, stats, med)
         derived = stats[-1]["derived_tuples"]
