@@ -764,9 +764,11 @@ __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int6
     u64 out = off[r];
     const uint32_t x = (uint32_t)lo0 + (uint32_t)r;
     const uint4 xq = make_uint4(x, x, x, x);
+    uint32_t dn = threadIdx.x < row_words ? row[threadIdx.x] : 0u;
     for (uint32_t cb = 0; cb < row_words; cb += 256) {
       const uint32_t wi = cb + threadIdx.x;
-      const uint32_t d = wi < row_words ? row[wi] : 0u;
+      const uint32_t d = dn;
+      dn = wi + 256 < row_words ? row[wi + 256] : 0u;  // the next step's word, loaded ahead
       // value i of the chunk goes to stage[sh + i] and to output position
       // out + i, so stage index s and position out - sh + s agree modulo 4:
       // whole quads are one 16-byte LDS read and two 16-byte stores
