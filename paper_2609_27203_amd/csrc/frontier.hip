@@ -730,22 +730,30 @@ hipError_t fill_bounds(uint32_t* lo, uint32_t* hi, int64_t n, uint32_t vlo, uint
 }
 
 // Number of set bits in each bitmap row.
+// One wavefront per row: four word loads in flight per lane, then a
+// shuffle reduction (no barriers).
 __global__ __launch_bounds__(256) void row_popcount_k(const uint32_t* bits, int64_t nrows,
                                                       uint32_t row_words, uint32_t* cnt) {
-  __shared__ uint32_t s_w[4];
-  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+  const uint32_t lane = (uint32_t)lane_id();
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < nrows; r += (int64_t)gridDim.x * 4) {
     const uint32_t* row = bits + (u64)r * row_words;
     uint32_t c = 0;
-    for (uint32_t i = threadIdx.x; i < row_words; i += 256) c += __popc(row[i]);
-    uint32_t tot;
-    block_excl_scan_u32(c, &tot, s_w);
-    if (threadIdx.x == 0) cnt[r] = tot;
+    for (uint32_t i = lane; i < row_words; i += 256) {
+      uint32_t w[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) w[k] = i + 64u * k < row_words ? row[i + 64u * k] : 0u;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) c += (uint32_t)__popc(w[k]);
+    }
+    for (int k = 32; k > 0; k >>= 1) c += __shfl_xor(c, k, 64);
+    if (lane == 0) cnt[r] = c;
   }
 }
 hipError_t row_popcount(const uint32_t* bits, int64_t nrows, uint32_t row_words, uint32_t* cnt,
                         hipStream_t s) {
   if (nrows <= 0) return hipSuccess;
-  row_popcount_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, cnt);
+  row_popcount_k<<<(unsigned)std::min<int64_t>((nrows + 3) / 4, 1 << 16), 256, 0, s>>>(bits, nrows, row_words,
+                                                                                      cnt);
   return hipGetLastError();
 }
 
