@@ -690,15 +690,19 @@ hipError_t gather_round(const GatherArgs& a, hipStream_t s) {
 
 // Empty the flagged rows (only their words [lo, hi) when bounds are kept,
 // which are then reset to empty) and their flags.
-__global__ void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words,
-                                     uint32_t* lo, uint32_t* hi) {
-  for (int64_t r = blockIdx.x; r < nrows; r += gridDim.x) {
-    if (!flag[r]) continue;  // (uniform)
+// One wavefront per row: most rows are not flagged, so the rows a wavefront
+// visits one after another (a flag load each) are kept few.  Every lane has
+// read the flag and the bounds before lane 0 resets them (one wavefront, in
+// program order).
+__global__ __launch_bounds__(256) void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nrows,
+                                                            uint32_t row_words, uint32_t* lo, uint32_t* hi) {
+  const uint32_t lane = (uint32_t)lane_id();
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < nrows; r += (int64_t)gridDim.x * 4) {
+    if (!flag[r]) continue;  // (uniform within the wavefront)
     uint32_t* row = bits + (u64)r * row_words;
     const uint32_t b = lo ? lo[r] : 0u, e = lo ? min(hi[r], row_words) : row_words;
-    for (uint32_t i = b + threadIdx.x; i < e; i += blockDim.x) row[i] = 0u;
-    __syncthreads();  // every thread has read the flag and bounds before they are reset
-    if (threadIdx.x == 0) {
+    for (uint32_t i = b + lane; i < e; i += 64) row[i] = 0u;
+    if (lane == 0) {
       flag[r] = 0u;
       if (lo) {
         lo[r] = row_words;
@@ -711,8 +715,8 @@ __global__ void clear_flagged_rows_k(uint32_t* bits, uint32_t* flag, int64_t nro
 hipError_t clear_flagged_rows(uint32_t* bits, uint32_t* flag, int64_t nrows, uint32_t row_words, uint32_t* lo,
                               uint32_t* hi, hipStream_t s) {
   if (nrows <= 0) return hipSuccess;
-  clear_flagged_rows_k<<<(unsigned)std::min<int64_t>(nrows, 4096), 256, 0, s>>>(bits, flag, nrows, row_words, lo,
-                                                                                hi);
+  clear_flagged_rows_k<<<(unsigned)std::min<int64_t>((nrows + 3) / 4, 8192), 256, 0, s>>>(bits, flag, nrows,
+                                                                                         row_words, lo, hi);
   return hipGetLastError();
 }
 
