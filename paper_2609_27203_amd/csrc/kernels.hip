@@ -2522,8 +2522,16 @@ __global__ __launch_bounds__(MK_THREADS) void dense_delta_bits_k(uint32_t* chg, 
     __syncthreads();
     for (uint32_t r = threadIdx.x; r < tot; r += MK_THREADS) {
       const u64 slot = base + stage[r];
-      k0[p + r] = dict[slot / range1];
-      k1[p + r] = (uint32_t)lo1 + (uint32_t)(slot % range1);
+      uint32_t rk, y;
+      if (nw <= (int64_t)(0xffffffffu / 32u)) {  // slots below 2^32: 32-bit division
+        rk = (uint32_t)slot / range1;
+        y = (uint32_t)slot - rk * range1;
+      } else {
+        rk = (uint32_t)(slot / range1);
+        y = (uint32_t)(slot % range1);
+      }
+      k0[p + r] = dict[rk];
+      k1[p + r] = (uint32_t)lo1 + y;
       v[p + r] = stored_value(vals[slot], type, fold_kind);
     }
     p += tot;
