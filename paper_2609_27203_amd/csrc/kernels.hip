@@ -980,8 +980,9 @@ __global__ __launch_bounds__(CP_THREADS) void compact_write_k(CompactArgs a) {
         a.v[p] = stored_value(a.counts[i], a.type, a.fold_kind);
       } else if (a.kind == CK_COUNTER) {
         if (a.kp.nkey == 2) {
-          a.k0[p] = (uint32_t)(i / a.range1) + (uint32_t)a.kp.lo[0];
-          a.k1[p] = (uint32_t)(i % a.range1) + (uint32_t)a.kp.lo[1];
+          const uint32_t q = narrow ? (uint32_t)i / (uint32_t)a.range1 : (uint32_t)(i / a.range1);
+          a.k0[p] = q + (uint32_t)a.kp.lo[0];
+          a.k1[p] = (uint32_t)(i - (int64_t)q * a.range1) + (uint32_t)a.kp.lo[1];
         } else {
           a.k0[p] = (uint32_t)i + (uint32_t)a.kp.lo[0];
         }
@@ -1996,8 +1997,14 @@ __global__ __launch_bounds__(MK_THREADS) void bits_keys_k(uint32_t* bits, int64_
     for (uint32_t r = threadIdx.x; r < tot; r += MK_THREADS) {
       const u64 bi = base + stage[r];
       if (nkey == 2) {
-        c0[p + r] = (uint32_t)lo0 + (uint32_t)(bi / row_bits);
-        c1[p + r] = (uint32_t)lo1 + (uint32_t)(bi % row_bits);
+        if (nw <= (int64_t)(0xffffffffu / 32u) && row_bits <= 0xffffffffu) {  // 32-bit division
+          const uint32_t q = (uint32_t)bi / (uint32_t)row_bits;
+          c0[p + r] = (uint32_t)lo0 + q;
+          c1[p + r] = (uint32_t)lo1 + ((uint32_t)bi - q * (uint32_t)row_bits);
+        } else {
+          c0[p + r] = (uint32_t)lo0 + (uint32_t)(bi / row_bits);
+          c1[p + r] = (uint32_t)lo1 + (uint32_t)(bi % row_bits);
+        }
       } else {
         c0[p + r] = (uint32_t)lo0 + (uint32_t)bi;
       }
