@@ -1915,15 +1915,17 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
 }
 
 // Marked slots -> slot list in one pass, clearing the marks: each wavefront
-// takes 256 consecutive words (four per lane, lane-major, so the loads
-// coalesce), reserves its entries with one atomic on *total and writes them
+// takes 128 consecutive words (two per lane, lane-major, so the loads
+// coalesce; a wavefront's word columns go out one after another, so short
+// wavefronts finish sooner), reserves its entries with one atomic on *total
+// and writes them
 // in word order.  The list is ascending within each wavefront's range and
 // the ranges land in any order: for consumers that take each listed key on
 // its own (the dense pull folds every key's in-edges itself).  Each word
 // column's entries are staged in LDS (entry o at o + o / 32, so the lanes of
 // a nearly full column write different banks) and go out with consecutive
 // lanes on consecutive entries.  *total must be zero before the launch.
-constexpr int LW_WORDS = 4;
+constexpr int LW_WORDS = 2;
 constexpr int LW_STAGE = 64 * 32 + 64;  // one column's entries, padded
 __global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t nw, uint32_t* list, uint32_t* total) {
   __shared__ uint32_t stage_all[4][LW_STAGE];
