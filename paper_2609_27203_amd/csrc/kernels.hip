@@ -2482,7 +2482,14 @@ __global__ void dense_mark_out_k(IndexProbe fwd, int ycol, int32_t lo1, uint32_t
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t p = pres[i];
     if (!p) continue;
-    const uint32_t zb = (uint32_t)(i / wpr), wd = (uint32_t)(i % wpr);
+    uint32_t zb, wd;
+    if (n <= (int64_t)0xffffffffll) {  // 32-bit division
+      zb = (uint32_t)i / wpr;
+      wd = (uint32_t)i - zb * wpr;
+    } else {
+      zb = (uint32_t)(i / wpr);
+      wd = (uint32_t)(i % wpr);
+    }
     const uint32_t kk = zb + (uint32_t)lo1 - (uint32_t)fwd.key_lo;
     if (kk >= fwd.key_range) continue;
     const uint32_t e1 = fwd.off[kk + 1];
