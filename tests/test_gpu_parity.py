@@ -216,6 +216,25 @@ def test_triangle_join_edge_cases():
             _compare(wl, rels, ref)
 
 
+@pytest.mark.parametrize("rules", ["tri(Z,X,Y) :- s(Y,Z), r(X,Y), t(Z,X).",
+                                   "tri(X,Y,Z) :- t(Z,X), s(Z,Y), r(Y,X)."])
+def test_triangle_value_order_keys_of_exactly_32_bits(rules):
+    """Indexes sorted by (key, value) whose key and value columns each span
+    exactly 2^16 values: the composite sort keys take all 32 bits of the
+    32-bit form (relations the rule reads in another column order than the
+    one they are stored in are sorted, not read as they are)."""
+    big = 65535
+    rels3 = {"r": ([0, 5, big, 7, 1], [1, 2, 3, big, big]),
+             "s": ([1, 2, 3, big, 0, 0], [0, big, 9, 7, big, 1]),
+             "t": ([0, 5, big, 0, 7], [0, big, 9, big, 7])}
+    wl = _tri_case(rels3, rules)
+    print(f"case: triangle 32-bit order keys {rules!r}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    assert len(ref.relations["tri"][1][0]) > 0
+    rels, _, _ = engine_run(wl, workspace_bytes=256 << 20)
+    _compare(wl, rels, ref)
+
+
 def test_triangle_full_size_sampled_and_sound():
     """The 3 x 65,536-row fixture: rows of 400 sampled driver rows against the
     oracle, every triple satisfying all three atoms, strictly ascending
