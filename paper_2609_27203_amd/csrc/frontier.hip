@@ -812,11 +812,68 @@ __global__ __launch_bounds__(256) void bits_to_rows_k(const uint32_t* bits, int6
     }
   }
 }
+// The same with one wavefront per row (four rows per workgroup, no
+// workgroup barriers): for sparse bitmaps, where a row's steps write few
+// rows each and the barriers of the workgroup form would set the pace.
+__global__ __launch_bounds__(256) void bits_to_rows_wave_k(const uint32_t* bits, int64_t nrows,
+                                                           uint32_t row_words, const uint32_t* off,
+                                                           int32_t lo0, int32_t lo1, uint32_t* c0,
+                                                           uint32_t* c1, u64 cap) {
+  __shared__ __align__(16) uint32_t stage_all[4][64 * 32 + 4];
+  const uint32_t lane = (uint32_t)lane_id();
+  uint32_t* stage = stage_all[threadIdx.x >> 6];
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < nrows; r += (int64_t)gridDim.x * 4) {
+    const uint32_t* row = bits + (u64)r * row_words;
+    u64 out = off[r];
+    const uint32_t x = (uint32_t)lo0 + (uint32_t)r;
+    const uint4 xq = make_uint4(x, x, x, x);
+    uint32_t dn = lane < row_words ? row[lane] : 0u;
+    for (uint32_t cb = 0; cb < row_words; cb += 64) {
+      const uint32_t wi = cb + lane;
+      const uint32_t d = dn;
+      dn = wi + 64 < row_words ? row[wi + 64] : 0u;
+      const uint32_t sh = (uint32_t)(out & 3u);
+      const uint32_t c = (uint32_t)__popc(d);
+      const uint32_t incl = wave_incl_scan(c);
+      const uint32_t n = __shfl(incl, 63, 64);
+      uint32_t pos = sh + incl - c;
+      for (uint32_t b = d; b; b &= b - 1) stage[pos++] = (uint32_t)lo1 + wi * 32u + (uint32_t)(__ffs(b) - 1);
+      wave_lds_sync();
+      const uint32_t end = sh + n;
+      const u64 base = out - sh;
+      for (uint32_t q = lane; q < (end + 3u) / 4u; q += 64) {
+        const uint32_t s0 = 4u * q;
+        const u64 p = base + s0;
+        if (s0 >= sh && s0 + 4u <= end && p + 4u <= cap) {
+          *reinterpret_cast<uint4*>(c1 + p) = *reinterpret_cast<const uint4*>(stage + s0);
+          *reinterpret_cast<uint4*>(c0 + p) = xq;
+        } else {
+#pragma unroll
+          for (uint32_t k = 0; k < 4u; ++k) {
+            if (s0 + k >= sh && s0 + k < end && p + k < cap) {
+              c0[p + k] = x;
+              c1[p + k] = stage[s0 + k];
+            }
+          }
+        }
+      }
+      out += n;
+      wave_lds_sync();
+    }
+  }
+}
 hipError_t bits_to_rows(const uint32_t* bits, int64_t nrows, uint32_t row_words, const uint32_t* off,
                         int32_t lo0, int32_t lo1, uint32_t* c0, uint32_t* c1, int64_t cap, hipStream_t s) {
   if (nrows <= 0) return hipSuccess;
-  bits_to_rows_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, off,
-                                                                            lo0, lo1, c0, c1, (u64)cap);
+  // fewer than a quarter of the bits set (cap is the row total): one
+  // wavefront per row (same generation's 17%: -3%; the R-MAT closure's
+  // 48% takes 3% longer that way)
+  if ((double)cap * 4.0 < (double)nrows * row_words * 32.0)
+    bits_to_rows_wave_k<<<(unsigned)std::min<int64_t>((nrows + 3) / 4, 1 << 16), 256, 0, s>>>(
+        bits, nrows, row_words, off, lo0, lo1, c0, c1, (u64)cap);
+  else
+    bits_to_rows_k<<<(unsigned)std::min<int64_t>(nrows, 1 << 16), 256, 0, s>>>(bits, nrows, row_words, off, lo0,
+                                                                              lo1, c0, c1, (u64)cap);
   return hipGetLastError();
 }
 
