@@ -135,6 +135,111 @@ __global__ __launch_bounds__(SC_ONE_THREADS) void scan_one_k(const T* in, T* out
   if (total && threadIdx.x == 0) *total = carry;
 }
 
+// Arrays of SC_TILE+1 to SC_WIDE_MAX elements, 16-byte aligned and written
+// to a separate array: one launch of one workgroup per tile.  Each workgroup
+// sums every element before its tile itself (at most SC_WIDE_MAX elements,
+// read with 16-byte loads issued a batch at a time) instead of waiting for
+// the tiles before it, so no workgroup depends on another.  Within a tile,
+// thread t owns one 16-byte vector of each of four sub-tiles (one load
+// instruction of a wavefront covers a contiguous 1 KB) and the four sums per
+// thread are ranked by one workgroup scan.
+constexpr int SC_W_THREADS = 1024;
+constexpr int SC_W_SUB = 4;
+constexpr int SC_W_BATCH = 16;
+constexpr int64_t SC_WIDE_MAX = 131072;
+
+template <typename T>
+struct alignas(16) ScVec {
+  T e[16 / sizeof(T)];
+};
+
+template <typename T>
+__global__ __launch_bounds__(SC_W_THREADS) void scan_wide_k(const T* in, T* out, int64_t n, T* total) {
+  constexpr int PER = 16 / sizeof(T);
+  constexpr int64_t SUBV = SC_W_THREADS;                  // vectors per sub-tile
+  constexpr int64_t TILE = SUBV * SC_W_SUB * PER;         // elements per workgroup
+  __shared__ T s_w[SC_W_SUB][SC_W_THREADS / 64];
+  __shared__ T s_p[SC_W_THREADS / 64];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const ScVec<T>* inv = (const ScVec<T>*)in;
+  ScVec<T>* outv = (ScVec<T>*)out;
+  const int64_t v0 = (int64_t)blockIdx.x * (TILE / PER);  // first vector of the tile
+  ScVec<T> v[SC_W_SUB];
+  T acc[SC_W_SUB];
+#pragma unroll
+  for (int k = 0; k < SC_W_SUB; ++k) {
+    const int64_t vi = v0 + k * SUBV + threadIdx.x;
+    const int64_t e0 = vi * PER;
+    if (e0 + PER <= n) {
+      v[k] = inv[vi];
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) v[k].e[i] = e0 + i < n ? in[e0 + i] : (T)0;
+    }
+    acc[k] = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[k] += v[k].e[i];
+  }
+  // the elements before the tile: whole vectors, since the tile starts at a
+  // multiple of TILE elements
+  T pre = 0;
+  for (int64_t q0 = threadIdx.x; q0 < v0; q0 += (int64_t)SC_W_THREADS * SC_W_BATCH) {
+    ScVec<T> x[SC_W_BATCH];
+#pragma unroll
+    for (int u = 0; u < SC_W_BATCH; ++u) {
+      const int64_t q = q0 + (int64_t)u * SC_W_THREADS;
+      if (q < v0) {
+        x[u] = inv[q];
+      } else {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) x[u].e[i] = 0;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SC_W_BATCH; ++u)
+#pragma unroll
+      for (int i = 0; i < PER; ++i) pre += x[u].e[i];
+  }
+  T incl[SC_W_SUB];
+#pragma unroll
+  for (int k = 0; k < SC_W_SUB; ++k) {
+    incl[k] = wave_incl_scan_t<T>(acc[k]);
+    if (lane == 63) s_w[k][w] = incl[k];
+  }
+  const T pw = wave_incl_scan_t<T>(pre);
+  if (lane == 63) s_p[w] = pw;
+  __syncthreads();
+  T run = 0;
+  for (int j = 0; j < SC_W_THREADS / 64; ++j) run += s_p[j];
+#pragma unroll
+  for (int k = 0; k < SC_W_SUB; ++k) {
+    T before = 0, tot = 0;
+    for (int j = 0; j < SC_W_THREADS / 64; ++j) {
+      const T y = s_w[k][j];
+      if (j < w) before += y;
+      tot += y;
+    }
+    T o = run + before + incl[k] - acc[k];
+    const int64_t vi = v0 + k * SUBV + threadIdx.x;
+    const int64_t e0 = vi * PER;
+    ScVec<T> r;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      r.e[i] = o;
+      o += v[k].e[i];
+    }
+    if (e0 + PER <= n) {
+      outv[vi] = r;
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        if (e0 + i < n) out[e0 + i] = r.e[i];
+    }
+    run += tot;
+  }
+  if (total && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *total = run;
+}
+
 size_t scan_temp_bytes(int64_t n) {
   size_t bytes = 0;
   int64_t m = n;
@@ -153,6 +258,15 @@ static hipError_t scan_rec(const T* in, T* out, int64_t n, T* total, char* temp,
   }
   if (n <= SC_TILE) {
     scan_apply_k<T><<<1, SC_THREADS, 0, s>>>(in, out, n, nullptr, total);
+    return hipGetLastError();
+  }
+  // the one-launch wide form reads elements of other tiles, so it needs a
+  // separate output array; both arrays 16-byte aligned for its vector loads
+  const uintptr_t ia = (uintptr_t)in, oa = (uintptr_t)out;
+  const bool apart = oa >= ia + (uintptr_t)n * sizeof(T) || ia >= oa + (uintptr_t)n * sizeof(T);
+  if (n <= SC_WIDE_MAX && apart && ((ia | oa) & 15) == 0) {
+    constexpr int64_t tile = (int64_t)SC_W_THREADS * SC_W_SUB * (16 / sizeof(T));
+    scan_wide_k<T><<<(unsigned)((n + tile - 1) / tile), SC_W_THREADS, 0, s>>>(in, out, n, total);
     return hipGetLastError();
   }
   if (n <= SC_ONE_MAX) {
