@@ -425,6 +425,104 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter_k(const K* kin, const u
   }
 }
 
+// Inputs of at most SS_MAX keys are sorted by one workgroup in LDS: every
+// 8-bit pass of the same stable LSD order runs in one launch instead of
+// three launches per pass.  Wavefront w owns positions [256w, 256w + 256),
+// four 64-key runs; a pass ranks each key among the equal digits of its
+// wavefront with the ballot match used by the scatter above, offsets each
+// (digit, wavefront) count in digit-major order, and scatters the keys to
+// their new positions in LDS.  The result is written back in place.
+constexpr int SS_THREADS = 1024;
+constexpr int SS_WAVES = SS_THREADS / 64;
+constexpr int SS_ITEMS = 4;
+constexpr int64_t SS_MAX = (int64_t)SS_THREADS * SS_ITEMS;
+
+template <typename K>
+__global__ __launch_bounds__(SS_THREADS) void sort_small_k(K* keys, uint32_t* vals, int n, int bits) {
+  __shared__ K sk[SS_MAX];
+  __shared__ uint32_t sv[SS_MAX];
+  __shared__ uint32_t cnt[SS_WAVES][256];
+  __shared__ uint32_t s_w[SS_WAVES];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  K key[SS_ITEMS];
+  uint32_t val[SS_ITEMS];
+#pragma unroll
+  for (int j = 0; j < SS_ITEMS; ++j) {
+    const int p = w * 64 * SS_ITEMS + j * 64 + lane;
+    key[j] = p < n ? keys[p] : (K)0;
+    val[j] = (p < n && vals) ? vals[p] : 0u;
+  }
+  for (int shift = 0; shift < bits; shift += 8) {
+    const int nbits = bits - shift < 8 ? bits - shift : 8;
+    const uint32_t dmask = (1u << nbits) - 1u;
+    for (int i = threadIdx.x; i < SS_WAVES * 256; i += SS_THREADS) (&cnt[0][0])[i] = 0;
+    __syncthreads();
+    uint32_t rank[SS_ITEMS], dig[SS_ITEMS];
+#pragma unroll
+    for (int j = 0; j < SS_ITEMS; ++j) {
+      const bool valid = w * 64 * SS_ITEMS + j * 64 + lane < n;
+      const uint32_t d = (uint32_t)(key[j] >> shift) & dmask;
+      u64 peers = __ballot(valid);
+      for (int b = 0; b < nbits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const u64 bal = __ballot(bit);
+        peers &= bit ? bal : ~bal;
+      }
+      if (!valid) peers = 0;
+      const uint32_t lt = __popcll(peers & lanemask_lt());
+      const uint32_t before = cnt[w][d];
+      wave_lds_sync();
+      rank[j] = before + lt;
+      dig[j] = d;
+      if (valid && lt == 0) cnt[w][d] = before + (uint32_t)__popcll(peers);
+      wave_lds_sync();
+    }
+    __syncthreads();
+    // digit d's total, then the digit-major offsets of every (digit, wavefront)
+    uint32_t tot = 0;
+    if (threadIdx.x < 256)
+      for (int ww = 0; ww < SS_WAVES; ++ww) tot += cnt[ww][threadIdx.x];
+    const uint32_t incl = wave_incl_scan_t<uint32_t>(tot);
+    if (lane == 63) s_w[w] = incl;
+    __syncthreads();
+    uint32_t run = incl - tot;
+    for (int ww = 0; ww < w; ++ww) run += s_w[ww];
+    if (threadIdx.x < 256)
+      for (int ww = 0; ww < SS_WAVES; ++ww) {
+        const uint32_t c = cnt[ww][threadIdx.x];
+        cnt[ww][threadIdx.x] = run;
+        run += c;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SS_ITEMS; ++j) {
+      if (w * 64 * SS_ITEMS + j * 64 + lane < n) {
+        const uint32_t pos = cnt[w][dig[j]] + rank[j];
+        sk[pos] = key[j];
+        sv[pos] = val[j];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SS_ITEMS; ++j) {
+      const int p = w * 64 * SS_ITEMS + j * 64 + lane;
+      if (p < n) {
+        key[j] = sk[p];
+        val[j] = sv[p];
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < SS_ITEMS; ++j) {
+    const int p = w * 64 * SS_ITEMS + j * 64 + lane;
+    if (p < n) {
+      keys[p] = key[j];
+      if (vals) vals[p] = val[j];
+    }
+  }
+}
+
 static int64_t rs_tile(int64_t n) { return (int64_t)RS_THREADS * (n < RS_SMALL_N ? RS_SMALL_ITEMS : 16); }
 
 size_t radix_temp_bytes(int64_t n) {
@@ -439,6 +537,10 @@ static hipError_t radix_sort_t(K* keys, uint32_t* vals, K* keys_alt, uint32_t* v
                                int64_t n, int bits, void* temp, hipStream_t s, int* in_alt) {
   *in_alt = 0;
   if (n <= 1 || bits <= 0) return hipSuccess;
+  if (n <= SS_MAX) {
+    sort_small_k<K><<<1, SS_THREADS, 0, s>>>(keys, vals, (int)n, bits);
+    return hipGetLastError();
+  }
   const bool small = n < RS_SMALL_N;
   const uint32_t nb = (uint32_t)((n + rs_tile(n) - 1) / rs_tile(n));
   uint32_t* hist = (uint32_t*)temp;
