@@ -668,7 +668,7 @@ struct Runner {
   // Index of rel by column col.  With order_col >= 0 the rows of each key are
   // further ordered: order_kind 0 by how many rows of rel have the order_col
   // value in column order_col (its out-degree when rel is an edge relation
-  // indexed by its target), most first by power-of-two class -- the
+  // indexed by its target), most first by base-8 class -- the
   // frontier pull scans in-edges
   // in that order, so that edges from well-connected sources, the likeliest
   // to be in a delta, come first; order_kind 1 by the int32 value itself
@@ -876,7 +876,7 @@ struct Runner {
             vbits = std::max(1, bitlen((uint64_t)(oh->dom_hi[order_col] - oh->dom_lo[order_col])));
           }
         }
-        const int obits = order_kind == 1 ? vbits : 5;  // degree order: power-of-two classes
+        const int obits = order_kind == 1 ? vbits : 2;  // degree order: four base-8 classes
         const bool wide = obits + kbits > 32;
         const size_t kw = wide ? 8 : 4;
         Buf ka, kb;

@@ -63,8 +63,8 @@ hipError_t csr_offsets_high(const void* sorted, bool wide, int shift, int64_t n,
                             hipStream_t s);
 // Composite keys of an ordered index, 32-bit (wide false) or 64-bit, and
 // perm[i] = i: (kcol[i] - klo) << obits | order part, the order part being
-// 31 - bitlen(deg(ocol[i])) with deg from the CSR offsets doff over [olo,
-// olo + drange) (degree order by power-of-two class, obits 5), or ocol[i] -
+// 3 - min(3, bitlen(deg(ocol[i])) / 3) with deg from the CSR offsets doff
+// over [olo, olo + drange) (degree order by base-8 class, obits 2), or ocol[i] -
 // olo when doff is null (value order, int32 values in [olo, olo + 2^obits)).
 hipError_t order_keys(const uint32_t* kcol, int32_t klo, const uint32_t* ocol, int32_t olo, int obits,
                       const uint32_t* doff, uint32_t drange, int64_t n, void* key, bool wide, uint32_t* perm,

@@ -816,10 +816,11 @@ hipError_t compact_offsets(const uint32_t* sorted, int64_t n, uint32_t* keys, ui
 
 // Composite sort key of row i of an ordered index and perm[i] = i, one
 // launch: the key column's image kcol[i] - klo in the high bits, below it
-// (obits bits) the order part -- degree order: 31 - bitlen(deg(z)) with z =
-// ocol[i] and deg(z) = doff[z - olo + 1] - doff[z - olo] (0 outside [olo,
-// olo + drange)), so the rows whose z has the most rows come first, by
-// power-of-two class (5 bits; rows of one class keep their order); value
+// (obits bits) the order part -- degree order: 3 - min(3, bitlen(deg(z)) / 3)
+// with z = ocol[i] and deg(z) = doff[z - olo + 1] - doff[z - olo] (0 outside
+// [olo, olo + drange)), so the rows whose z has the most rows come first, by
+// base-8 class (2 bits: at least 256 rows, 32 to 255, 4 to 31, fewer; rows
+// of one class keep their order); value
 // order: ocol[i] - olo.  Sorting by it keeps the key order.
 template <typename K>
 __global__ void order_keys_k(const uint32_t* kcol, int32_t klo, const uint32_t* ocol, int32_t olo, int obits,
@@ -830,7 +831,7 @@ __global__ void order_keys_k(const uint32_t* kcol, int32_t klo, const uint32_t* 
     uint32_t part = o;
     if (doff) {
       const uint32_t deg = o < drange ? doff[o + 1] - doff[o] : 0u;
-      part = 31u - (deg ? 32u - (uint32_t)__clz(deg) : 0u);
+      part = 3u - min(3u, (deg ? 32u - (uint32_t)__clz(deg) : 0u) / 3u);
     }
     key[i] = ((K)(kcol[i] - (uint32_t)klo) << obits) | (K)part;
     perm[i] = (uint32_t)i;
