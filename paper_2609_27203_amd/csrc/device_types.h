@@ -272,6 +272,7 @@ struct DenseTileArgs {
   uint32_t* pres;
   uint32_t* chg;
   unsigned long long* counters;  // CNT_CANDIDATES, CNT_INSERTED (new keys), CNT_APPENDED (improved keys)
+  uint32_t* tcnt;         // [n0 * ntiles] or null: improved slots of each (rank, tile) this round
 };
 
 // Closure-shaped recursive rule head(X, Y) :- delta head(X, Z), e(Z, Y) over a

@@ -2617,8 +2617,17 @@ struct Runner {
 
   // Delta rows of a tiled head from its delta bits, grouped by rank (count
   // and write passes; the write pass also fills roff); the row total goes to
-  // *total on the device.
-  xl_status tile_delta_rows(HeadRun* h, uint32_t* total, Buf* ltmp) {
+  // *total on the device.  With tcnt (the round's per-tile counts) one
+  // launch that sums the counts itself replaces both passes.
+  xl_status tile_delta_rows(HeadRun* h, uint32_t* total, Buf* ltmp, const uint32_t* tcnt) {
+    if (tcnt) {
+      HIP_TRY(c, k::tile_delta_rows(h->dchg.as<uint32_t>(), tcnt, (uint32_t)h->n0, h->ntiles, h->tile,
+                                    (uint32_t)h->range1, h->dvals.as<uint32_t>(), h->dict.as<uint32_t>(), h->kp.lo[1],
+                                    h->rel->types[h->nkey], h->fold, h->drow[0].as<uint32_t>(),
+                                    h->drow[1].as<uint32_t>(), h->drow[2].as<uint32_t>(), h->roff.as<uint32_t>(),
+                                    total, c->stream));
+      return XL_OK;
+    }
     const int64_t ns = std::max<int64_t>(h->n0, 1) * h->range1;
     for (bool write : {false, true})
       HIP_TRY(c, k::dense_delta_from_bits(h->dchg.as<uint32_t>(), ns, (uint32_t)h->range1, h->dvals.as<uint32_t>(),
@@ -2663,10 +2672,17 @@ struct Runner {
     DenseTileArgs a{};
     XL_TRY(tile_args(p, h, a));
     const int B = c->batched_rounds;
-    Buf acc, rounds, ltmp;
+    Buf acc, rounds, ltmp, tcnt;
     XL_TRY(dalloc(c, 8 * CNT_N, &acc, "round counters"));
     XL_TRY(dalloc(c, (size_t)B * 4, &rounds, "round delta sizes"));
     XL_TRY(dalloc(c, k::bits_list_temp_bytes(ns), &ltmp, "compaction scratch"));
+    // one-launch delta rows from per-tile counts when the tiles are few
+    // enough for each listing workgroup to sum the counts before its tile
+    const uint64_t nwork = (uint64_t)h->n0 * h->ntiles;
+    if (h->n0 > 0 && nwork <= k::TL_MAX_WORK && h->tile <= k::TL_MAX_TILE && h->range1 % 32 == 0) {
+      XL_TRY(dalloc(c, (size_t)nwork * 4, &tcnt, "tile delta counts"));
+      a.tcnt = tcnt.as<uint32_t>();
+    }
     HIP_TRY(c, hipMemsetAsync(acc.p, 0, 8 * CNT_N, c->stream));
     a.counters = acc.as<unsigned long long>();
     std::vector<hipEvent_t> evs;
@@ -2692,7 +2708,7 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
         HIP_TRY(c, k::dense_min_tiles(a, c->stream));
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
-        XL_TRY(tile_delta_rows(h, rounds.as<uint32_t>() + r, &ltmp));
+        XL_TRY(tile_delta_rows(h, rounds.as<uint32_t>() + r, &ltmp, a.tcnt));
       }
       std::vector<uint32_t> n(nb);
       XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));

@@ -230,6 +230,18 @@ size_t dense_tile_lds_bytes(uint32_t tile);
 hipError_t tile_keys(const uint32_t* zc, const uint32_t* yc, int64_t n, int32_t zlo, int32_t lo1, uint32_t tile,
                      uint32_t ntiles, uint32_t zr, bool tile_only, uint32_t* key, hipStream_t s);
 hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s);
+// The same delta rows in one launch after a tile round that wrote tcnt
+// ([n0 * ntiles] improved slots per (rank, tile), DenseTileArgs::tcnt): one
+// workgroup per tile sums the counts of the tiles before it itself.  Fills
+// roff[0 .. n0] and *total; clears the delta bits.  Needs n0 * ntiles <=
+// TL_MAX_WORK, tile <= TL_MAX_TILE, tile and range1 multiples of 32
+// (hipErrorInvalidValue otherwise).
+constexpr uint32_t TL_MAX_WORK = 8192;
+constexpr uint32_t TL_MAX_TILE = 32768;
+hipError_t tile_delta_rows(uint32_t* chg, const uint32_t* tcnt, uint32_t n0, uint32_t ntiles, uint32_t tile,
+                           uint32_t range1, const uint32_t* vals, const uint32_t* dict, int32_t lo1, int type,
+                           int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v, uint32_t* roff, uint32_t* total,
+                           hipStream_t s);
 // counts[key_lo + i - head_lo] += off[i + 1] - off[i] for every i < key_range
 // with rows; a key outside [head_lo, head_lo + head_range) bumps CNT_FATAL.
 hipError_t index_degree_add(const uint32_t* off, uint32_t key_range, int32_t key_lo, int32_t head_lo,

@@ -2804,6 +2804,7 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
   uint32_t* tchg = lds + a.tile;         // improved in this round
   uint32_t* tpres = tchg + a.tile / 32;  // presence before the round
   __shared__ uint32_t s_excl[DT_WAVES][64], s_beg[DT_WAVES][64], s_z[DT_WAVES][64], s_d[DT_WAVES][64];
+  __shared__ uint32_t s_tc[DT_WAVES];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const uint32_t* ycol = a.idx.col[a.ycol];
   u64 cands = 0;
@@ -2886,6 +2887,7 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
     // write back the improved slots; new keys get their presence bit
     for (uint32_t i = threadIdx.x; i < tw; i += DT_THREADS)
       if ((tchg[i >> 5] >> (i & 31)) & 1u) a.vals[base + i] = tv[i];
+    uint32_t item = 0;
     for (uint32_t i = threadIdx.x; i < tw / 32; i += DT_THREADS) {
       const uint32_t c = tchg[i];
       if (!c) continue;
@@ -2893,9 +2895,19 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
       const uint32_t fresh = c & ~tpres[i];
       if (fresh) a.pres[base / 32 + i] = tpres[i] | fresh;
       ins += (uint32_t)__popc(fresh);
-      imp += (uint32_t)__popc(c);
+      item += (uint32_t)__popc(c);
+    }
+    imp += item;
+    if (a.tcnt) {
+      for (int k = 32; k > 0; k >>= 1) item += __shfl_xor(item, k, 64);
+      if (lane == 0) s_tc[w] = item;
     }
     __syncthreads();
+    if (a.tcnt && threadIdx.x == 0) {  // s_tc is next written after this item's tile loads and barrier
+      uint32_t tc = 0;
+      for (int i = 0; i < DT_WAVES; ++i) tc += s_tc[i];
+      a.tcnt[b] = tc;
+    }
   }
   // one atomic per workgroup for each count
   __shared__ u64 s_c[DT_WAVES], s_i[DT_WAVES], s_m[DT_WAVES];
@@ -2948,6 +2960,75 @@ hipError_t dense_min_tiles(const DenseTileArgs& a, hipStream_t s) {
   const uint32_t nwork = a.n0 * a.ntiles;
   if (nwork == 0) return hipSuccess;
   dense_min_tile_k<<<std::min<uint32_t>(nwork, 65536), DT_THREADS, dense_tile_lds_bytes(a.tile), s>>>(a);
+  return hipGetLastError();
+}
+
+// Delta rows of a tiled round in one launch, from the per-(rank, tile)
+// counts of improved slots that the round's tile kernel wrote: workgroup b
+// lists tile b (one delta bit word per thread, the tile's words in one step)
+// after summing the counts of the tiles before it itself, so no count pass
+// or scan launch precedes it.  Rows come out in slot order (rank-major, as
+// the two-pass form writes them) and the delta bits are cleared; workgroup
+// b also writes its rank's first row when it holds the rank's first tile,
+// and the last one writes roff[n0] and the total.
+constexpr int TL_THREADS = 1024;
+__global__ __launch_bounds__(TL_THREADS) void tile_delta_rows_k(uint32_t* chg, const uint32_t* tcnt, uint32_t nwork,
+                                                                uint32_t ntiles, uint32_t tile, uint32_t range1,
+                                                                const uint32_t* vals, const uint32_t* dict,
+                                                                int32_t lo1, int type, int fold_kind, uint32_t* k0,
+                                                                uint32_t* k1, uint32_t* v, uint32_t* roff,
+                                                                uint32_t* total) {
+  extern __shared__ uint32_t stage[];  // tile entries: slot offsets within the tile
+  __shared__ uint32_t s_w[TL_THREADS / 64];
+  const uint32_t b = blockIdx.x, r = b / ntiles, t = b - r * ntiles;
+  uint32_t acc = 0;
+  for (uint32_t i = threadIdx.x; i < b; i += TL_THREADS) acc += tcnt[i];
+  uint32_t p;
+  block_excl_scan_u32(acc, &p, s_w);
+  const uint32_t own = tcnt[b];
+  if (threadIdx.x == 0) {
+    if (t == 0) roff[r] = p;
+    if (b == nwork - 1) {
+      roff[r + 1] = p + own;
+      *total = p + own;
+    }
+  }
+  if (own == 0) return;  // the tile kernel wrote no delta bit in this tile
+  const uint32_t y0 = t * tile;
+  const uint32_t tw = min(tile, range1 - y0);
+  const u64 base = (u64)r * range1 + y0;  // a multiple of 32
+  const uint32_t nwt = tw / 32;
+  const uint32_t key0 = dict[r];
+  for (uint32_t w0 = 0; w0 < nwt; w0 += TL_THREADS) {
+    const uint32_t wi = w0 + threadIdx.x;
+    const uint32_t d = wi < nwt ? chg[base / 32 + wi] : 0u;
+    uint32_t tot;
+    uint32_t q = block_excl_scan_u32((uint32_t)__popc(d), &tot, s_w);
+    if (d) {
+      chg[base / 32 + wi] = 0u;
+      for (uint32_t bb = d; bb; bb &= bb - 1) stage[q++] = (wi - w0) * 32u + (uint32_t)(__ffs(bb) - 1);
+    }
+    __syncthreads();
+    for (uint32_t e = threadIdx.x; e < tot; e += TL_THREADS) {
+      const uint32_t y = w0 * 32u + stage[e];
+      k0[p + e] = key0;
+      k1[p + e] = (uint32_t)lo1 + y0 + y;
+      v[p + e] = stored_value(vals[base + y], type, fold_kind);
+    }
+    p += tot;
+    __syncthreads();
+  }
+}
+hipError_t tile_delta_rows(uint32_t* chg, const uint32_t* tcnt, uint32_t n0, uint32_t ntiles, uint32_t tile,
+                           uint32_t range1, const uint32_t* vals, const uint32_t* dict, int32_t lo1, int type,
+                           int fold_kind, uint32_t* k0, uint32_t* k1, uint32_t* v, uint32_t* roff, uint32_t* total,
+                           hipStream_t s) {
+  const uint32_t nwork = n0 * ntiles;
+  if (nwork == 0 || nwork > TL_MAX_WORK || tile % 32 != 0 || range1 % 32 != 0 || tile > TL_MAX_TILE)
+    return hipErrorInvalidValue;
+  const uint32_t stage = std::min<uint32_t>(tile, (uint32_t)TL_THREADS * 32u);
+  tile_delta_rows_k<<<nwork, TL_THREADS, (size_t)stage * 4, s>>>(chg, tcnt, nwork, ntiles, tile, range1, vals, dict,
+                                                                 lo1, type, fold_kind, k0, k1, v, roff, total);
   return hipGetLastError();
 }
 
