@@ -2350,8 +2350,11 @@ struct Runner {
       HIP_TRY(c, hipMemsetAsync(rounds.p, 0, (size_t)nb * 4, c->stream));
       for (int r = 0; r < nb; ++r) {
         uint32_t* nr = rounds.as<uint32_t>() + r;
+        // the mark pass also clears the presence bits this round's pull
+        // writes (the round before last's, no longer read)
         HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
-                                     h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+                                     h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(),
+                                     h->dnext_pres.as<uint32_t>(), c->stream));
         HIP_TRY(c, k::bits_list_waves(h->dchg.as<uint32_t>(), nsd, list.as<uint32_t>(), nr, c->stream));
         DensePullArgs q{};
         XL_TRY(pull_args(p, h, fast, fcol, q));
@@ -2364,7 +2367,6 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
         std::swap(h->dcur.p, h->dnext.p);
         std::swap(h->dcur_pres.p, h->dnext_pres.p);
-        HIP_TRY(c, k::fill_bytes(h->dnext_pres.p, 0, (size_t)(nsd / 32) * 4, c->stream));
       }
       std::vector<uint32_t> n(nb);
       XL_TRY(ctl_read(c, rounds.p, (size_t)nb * 4, n.data()));
@@ -2390,6 +2392,8 @@ struct Runner {
       delta = n[done - 1];
     }
     destroy_events();
+    // the next presence bits are clear between rounds everywhere else
+    HIP_TRY(c, k::fill_bytes(h->dnext_pres.p, 0, (size_t)(nsd / 32) * 4, c->stream));
     u64 tot[CNT_N];
     XL_TRY(ctl_read(c, acc.p, sizeof(tot), tot));
     if (tot[CNT_FATAL]) return c->fail(XL_DEVICE_ERROR, "marked key without a contribution (internal)");
@@ -2433,7 +2437,7 @@ struct Runner {
       XL_TRY(get_index(sp.rel, sp.key_col, &fwd, -1, nullptr, 0, true));
       if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
       HIP_TRY(c, k::dense_mark_out(fwd, p.carried_ycol, h->kp.lo[1], (uint32_t)h->range1, (uint32_t)h->nrank_d,
-                                   h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), c->stream));
+                                   h->dcur_pres.as<uint32_t>(), h->dchg.as<uint32_t>(), nullptr, c->stream));
       if (c->profile) {
         HIP_TRY(c, hipEventRecord(ev[1], c->stream));
         HIP_TRY(c, hipEventSynchronize(ev[1]));

@@ -204,8 +204,10 @@ hipError_t dense_pull(const DensePullArgs& a, hipStream_t s);
 // Marks (target-major, nrank a multiple of 32) of the keys that receive a
 // contribution from the delta presence bits pres, pushed through e's index by
 // its Z column (fwd; ycol = e's Y column); mark must be all zero on entry.
+// clear (optional, the same range1 * nrank / 32 words as pres, not aliasing
+// pres or mark) is zeroed in the same launch.
 hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t nrank,
-                          const uint32_t* pres, uint32_t* mark, hipStream_t s);
+                          const uint32_t* pres, uint32_t* mark, uint32_t* clear, hipStream_t s);
 // Rows of the set bits of a dense key bitmap in bit order (two calls on the
 // same temp as bits_list; temp sized by bits_list_temp_bytes); clear = zero
 // the words read.

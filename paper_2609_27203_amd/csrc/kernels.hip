@@ -2692,12 +2692,15 @@ hipError_t dense_apply_rows(const uint32_t* c0, const uint32_t* c1, const uint32
 // every nonzero word w of z's delta presence row is ORed into word w of the
 // mark row of each out-neighbour y of z (mark all zero on entry).  Only the
 // delta's words cost more than one load; reading every target's in-edges
-// instead took three times as long on the layered DAG.
+// instead took three times as long on the layered DAG.  Word i of clear, an
+// array of the same shape (the presence bits the coming pull writes), is
+// zeroed by the thread that reads word i of pres.
 __global__ void dense_mark_out_k(IndexProbe fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t wpr,
-                                 const uint32_t* pres, uint32_t* mark) {
+                                 const uint32_t* pres, uint32_t* mark, uint32_t* clear) {
   const int64_t n = (int64_t)range1 * wpr;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t p = pres[i];
+    if (clear) clear[i] = 0u;
     if (!p) continue;
     uint32_t zb, wd;
     if (n <= (int64_t)0xffffffffll) {  // 32-bit division
@@ -2717,11 +2720,12 @@ __global__ void dense_mark_out_k(IndexProbe fwd, int ycol, int32_t lo1, uint32_t
   }
 }
 hipError_t dense_mark_out(const IndexProbe& fwd, int ycol, int32_t lo1, uint32_t range1, uint32_t nrank,
-                          const uint32_t* pres, uint32_t* mark, hipStream_t s) {
+                          const uint32_t* pres, uint32_t* mark, uint32_t* clear, hipStream_t s) {
   const uint32_t wpr = nrank / 32;
   if (range1 == 0 || wpr == 0 || nrank % 32 != 0) return hipErrorInvalidValue;
+  if (clear && (clear == pres || clear == mark)) return hipErrorInvalidValue;
   dense_mark_out_k<<<grid_for((int64_t)range1 * wpr, 256, 65536), 256, 0, s>>>(fwd, ycol, lo1, range1, wpr, pres,
-                                                                              mark);
+                                                                              mark, clear);
   return hipGetLastError();
 }
 
