@@ -331,8 +331,8 @@ struct FrontierArgs {
 // only read (rows are shared by all X of one A) and cleared by
 // clear_flagged_rows after the round.
 struct GatherArgs {
-  const uint32_t* in_bits;  // [range0][row_words] this round's delta
-  const uint32_t* in_flag;  // [range0]
+  uint32_t* in_bits;        // [range0][row_words] this round's delta (by_a: emptied as read)
+  uint32_t* in_flag;        // [range0]
   uint32_t* out_bits;       // [range0][row_words] next delta (zero on entry)
   uint32_t* out_flag;       // [range0] (zero on entry)
   uint32_t* bits;           // the head's membership bitmap
@@ -349,11 +349,13 @@ struct GatherArgs {
   // e1a is e1 indexed by its A column, e1_xcol the column holding X.  Every
   // delta row r keeps word bounds: its bits lie in words [lo[r], hi[r])
   // (empty: lo = row_words, hi = 0); the next round's bounds only widen.
+  // The by_a kernel also empties each delta row it reads (its nonzero words,
+  // its flag and its bounds), so no clearing pass follows the round.
   int32_t by_a;
   IndexProbe e1a;
   int32_t e1_xcol;
-  const uint32_t* in_lo;
-  const uint32_t* in_hi;
+  uint32_t* in_lo;
+  uint32_t* in_hi;
   uint32_t* out_lo;
   uint32_t* out_hi;
 };

@@ -1570,10 +1570,12 @@ struct Runner {
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[0], c->stream));
     HIP_TRY(c, k::gather_round(a, c->stream));
     if (c->profile) HIP_TRY(c, hipEventRecord(ev[1], c->stream));
-    // the consumed delta becomes the next round's output buffer
-    HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(), h->gflag[h->gcur].as<uint32_t>(),
-                                     h->range0, h->row_words, a.by_a ? h->gbound[h->gcur].as<uint32_t>() : nullptr,
-                                     a.by_a ? h->gbound[h->gcur].as<uint32_t>() + h->range0 : nullptr, c->stream));
+    // the consumed delta becomes the next round's output buffer (the by-row
+    // kernel empties each delta row it reads itself)
+    if (!a.by_a)
+      HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(),
+                                       h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words, nullptr, nullptr,
+                                       c->stream));
     u64 cnt[CNT_N];
     XL_TRY(ctl_read(c, c->dcounters, sizeof(cnt), cnt));
     cands += (int64_t)cnt[CNT_CANDIDATES];
@@ -2256,11 +2258,10 @@ struct Runner {
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r], c->stream));
         HIP_TRY(c, k::gather_round(a, c->stream));
         if (c->profile) HIP_TRY(c, hipEventRecord(evs[2 * r + 1], c->stream));
-        HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(),
-                                         h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words,
-                                         a.by_a ? h->gbound[h->gcur].as<uint32_t>() : nullptr,
-                                         a.by_a ? h->gbound[h->gcur].as<uint32_t>() + h->range0 : nullptr,
-                                         c->stream));
+        if (!a.by_a)  // the by-row kernel empties each delta row it reads itself
+          HIP_TRY(c, k::clear_flagged_rows((h->gcur ? h->gbits : h->dbits).as<uint32_t>(),
+                                           h->gflag[h->gcur].as<uint32_t>(), h->range0, h->row_words, nullptr,
+                                           nullptr, c->stream));
         h->gcur ^= 1;
       }
       std::vector<u64> cnt((size_t)nb * CNT_N);  // at most 64 blocks of 64 B: one control read

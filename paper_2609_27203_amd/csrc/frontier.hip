@@ -531,7 +531,10 @@ __global__ __launch_bounds__(FR_THREADS) void gather_round_k(GatherArgs g) {
 // workgroup handles one delta row at a time: a row's work is a chain of
 // dependent global accesses (flag, word range, delta words, e2 offsets, Y
 // lists, X list, atomics), most rows on a forest are small, and rows in
-// flight, not threads per row, set the pace.
+// flight, not threads per row, set the pace.  The wavefront that reads delta
+// row A is the only one that touches it in the round, so it also empties it:
+// each nonzero word as it is read, then A's flag and bounds, which every
+// lane has read before lane 0 resets them.
 constexpr uint32_t GA_STEP = 16;             // delta words decoded per step
 constexpr uint32_t GA_ZCAP = GA_STEP * 32;   // B values listed per step, at most
 
@@ -559,20 +562,29 @@ __global__ __launch_bounds__(64) void gather_by_a_k(GatherArgs g) {
   for (int64_t ar64 = blockIdx.x; ar64 < g.range0; ar64 += gridDim.x) {
     const uint32_t ar = (uint32_t)ar64;
     if (!g.in_flag[ar]) continue;  // (uniform: no delta row)
+    uint32_t* frow = g.in_bits + (u64)ar * W;
+    const uint32_t wb = g.in_lo[ar], we = min(g.in_hi[ar], W);
     const uint32_t kk = (uint32_t)g.lo0 + ar - (uint32_t)g.e1a.key_lo;
     uint32_t b1 = 0, n1 = 0;
     if (kk < g.e1a.key_range) {
       b1 = g.e1a.off[kk];
       n1 = g.e1a.off[kk + 1] - b1;
     }
-    if (n1 == 0) continue;  // (uniform: no X pairs with A)
-    const uint32_t* frow = g.in_bits + (u64)ar * W;
-    const uint32_t we = min(g.in_hi[ar], W);
+    if (n1 == 0) {  // (uniform: no X pairs with A) empty the row unread
+      for (uint32_t wi = wb + (uint32_t)lane; wi < we; wi += 64) frow[wi] = 0u;
+      if (lane == 0) {
+        g.in_flag[ar] = 0u;
+        g.in_lo[ar] = W;
+        g.in_hi[ar] = 0u;
+      }
+      continue;
+    }
     uint32_t umin = 0xffffffffu, umax = 0u;  // this lane's words of U touched
-    for (uint32_t cb = g.in_lo[ar]; cb < we; cb += GA_STEP) {
+    for (uint32_t cb = wb; cb < we; cb += GA_STEP) {
       // the B values of delta words [cb, cb + GA_STEP), in order
       const uint32_t wi = cb + (uint32_t)lane;
       const uint32_t d = lane < (int)GA_STEP && wi < we ? frow[wi] : 0u;
+      if (d) frow[wi] = 0u;
       const uint32_t c = __popc(d);
       const uint32_t incl = wave_incl_scan(c);
       const uint32_t nz = __shfl(incl, 63, 64);
@@ -630,6 +642,11 @@ __global__ __launch_bounds__(64) void gather_by_a_k(GatherArgs g) {
         }
         wave_lds_sync();
       }
+    }
+    if (lane == 0) {  // the row is empty now; every lane read wb and we above
+      g.in_flag[ar] = 0u;
+      g.in_lo[ar] = W;
+      g.in_hi[ar] = 0u;
     }
     umin = wave_min_u32(umin);
     umax = wave_max_u32(umax);
