@@ -886,6 +886,41 @@ def test_closure_and_count_over_many_first_keys(resident):
     assert counts.min() == 1 and counts.max() == chain - 1
 
 
+@pytest.mark.parametrize("resident", [0, 1])
+def test_closure_seeded_by_two_rules(resident):
+    """The seed round of the closure has two rules (edge, then a second edge
+    relation): the resident launch starts only after both have inserted, so
+    paths that begin with an edge of the second relation are found too."""
+    rng = np.random.default_rng(17)
+    edb = _edges(rng.integers(0, 300, 1200), rng.integers(0, 300, 1200))
+    edb["extra"] = (("i32", "i32"), [rng.integers(0, 300, 400).astype(np.int32),
+                                     rng.integers(0, 300, 400).astype(np.int32)])
+    rules = ("path(X, Y) :- edge(X, Y).\npath(X, Y) :- extra(X, Y).\n"
+             "path(X, Z) :- path(X, Y), edge(Y, Z).")
+    wl = W.Workload("two_seeds", rules, edb, {"path": ("i32", "i32")})
+    print(f"case: closure seeded by two rules resident={resident}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"frontier_resident": resident, "profile": 1})
+    _compare(wl, rels, ref)
+    assert stats["iterations"] == len(ref.sizes["path"]) - 1
+    assert stats["front_launches"] == (1 if resident else stats["iterations"])
+
+
+@pytest.mark.parametrize("resident", [0, 1])
+def test_closure_whose_seed_derives_nothing(resident):
+    """A seed rule whose filter rejects every edge: the closure stays empty,
+    no round runs, and the count stratum after it sees no rows."""
+    wl = W.Workload("empty_seed", "path(X, Y) :- edge(X, Y), X > 1000.\n"
+                                  "path(X, Z) :- path(X, Y), edge(Y, Z).\n"
+                                  "reach_count(X, count(Y)) :- path(X, Y).",
+                    _edges([1, 2, 3, 4], [2, 3, 4, 1]), {"path": ("i32", "i32"), "reach_count": ("i32", "i32")})
+    print(f"case: closure with an empty seed resident={resident}", flush=True)
+    ref = evaluate(wl.rules, wl.edb, wl.idb)
+    rels, stats, _ = engine_run(wl, options={"frontier_resident": resident}, workspace_bytes=256 << 20)
+    _compare(wl, rels, ref)   # both relations empty, as in the oracle
+    assert stats["iterations"] == 0
+
+
 def test_self_loop_and_duplicates():
     wl = W.Workload("loops", W.TC_RULES, _edges([0, 0, 1, 1, 2], [0, 1, 2, 2, 0]), {"path": ("i32", "i32")})
     ref = evaluate(wl.rules, wl.edb, wl.idb)
