@@ -911,19 +911,24 @@ hipError_t gather_rows(const uint32_t* bits, uint32_t row_words, const uint32_t*
 }
 
 // hasin bit (y - lo1) for y in [lo1, lo1 + 32 * words): y has an in-edge in
-// the index of e by its Y column.
+// the index of e by its Y column.  One lane per y and one ballot per 64 y:
+// lanes 0 and 32 write the wavefront's two words.
 __global__ void hasin_bits_k(IndexProbe rev, int32_t lo1, uint32_t words, uint32_t* out) {
-  for (uint32_t wi = blockIdx.x * blockDim.x + threadIdx.x; wi < words; wi += gridDim.x * blockDim.x) {
-    uint32_t m = 0;
-    for (int b = 0; b < 32; ++b) {
-      const uint32_t kk = (uint32_t)lo1 + wi * 32u + (uint32_t)b - (uint32_t)rev.key_lo;
-      if (kk < rev.key_range && rev.off[kk + 1] > rev.off[kk]) m |= 1u << b;
-    }
-    out[wi] = m;
+  const uint32_t lane = (uint32_t)lane_id();
+  const u64 n = (u64)words * 32u;
+  const u64 waves = (u64)gridDim.x * (blockDim.x / 64);
+  for (u64 base = ((u64)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6)) * 64; base < n; base += waves * 64) {
+    const u64 y = base + lane;
+    const uint32_t kk = (uint32_t)lo1 + (uint32_t)y - (uint32_t)rev.key_lo;
+    const bool has = y < n && kk < rev.key_range && rev.off[kk + 1] > rev.off[kk];
+    const u64 m = __ballot(has);
+    const u64 wi = base / 32;
+    if (lane == 0) out[wi] = (uint32_t)m;
+    if (lane == 32 && wi + 1 < words) out[wi + 1] = (uint32_t)(m >> 32);
   }
 }
 hipError_t hasin_bits(const IndexProbe& rev, int32_t lo1, uint32_t words, uint32_t* out, hipStream_t s) {
-  hasin_bits_k<<<grid_for(words, 256, 4096), 256, 0, s>>>(rev, lo1, words, out);
+  hasin_bits_k<<<grid_for((int64_t)words * 32, 256, 4096), 256, 0, s>>>(rev, lo1, words, out);
   return hipGetLastError();
 }
 
