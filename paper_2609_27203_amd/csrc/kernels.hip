@@ -2816,6 +2816,11 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
   const uint32_t nwork = a.n0 * a.ntiles;
   for (uint32_t b = blockIdx.x; b < nwork; b += gridDim.x) {
     const uint32_t r = b / a.ntiles, t = b % a.ntiles;
+    const uint32_t rb = a.roff[r], re = a.roff[r + 1];
+    if (rb == re) {  // (uniform) no delta row of this rank: the tile cannot change
+      if (a.tcnt && threadIdx.x == 0) a.tcnt[b] = 0u;
+      continue;
+    }
     const uint32_t y0 = t * a.tile;
     const uint32_t tw = min(a.tile, a.range1 - y0);
     const u64 base = (u64)r * a.range1 + y0;  // first slot (a multiple of 32)
@@ -2826,7 +2831,6 @@ __global__ __launch_bounds__(DT_THREADS) void dense_min_tile_k(DenseTileArgs by_
     }
     __syncthreads();
     const uint32_t s = a.dict[r];
-    const uint32_t rb = a.roff[r], re = a.roff[r + 1];
     for (uint32_t r0 = rb + (uint32_t)w * 64; r0 < re; r0 += DT_WAVES * 64) {
       const uint32_t j = r0 + (uint32_t)lane;
       uint32_t beg = 0, deg = 0, z = 0, d1 = 0;
