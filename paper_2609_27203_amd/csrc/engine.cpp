@@ -3538,15 +3538,18 @@ struct Runner {
       return XL_OK;
     };
     if (a.na == 0 || p.tri_brel->nrows == 0 || p.tri_crel->nrows == 0) return finish(0);
-    Buf work, flag_pos, crow, cw, cofs, tmp, tot;
+    Buf work, flags, flag_pos, crow, cw, cofs, tmp, tot;
     XL_TRY(dalloc(c, (size_t)a.na * 4, &work, "triangle work"));
+    XL_TRY(dalloc(c, (size_t)a.na * 4, &flags, "triangle row flags"));
     XL_TRY(dalloc(c, (size_t)a.na * 4, &flag_pos, "triangle row positions"));
     XL_TRY(dalloc(c, std::max(k::scan_temp_bytes(a.na), k::scan_temp_bytes(a.na + 1)), &tmp, "scan scratch"));
     XL_TRY(dalloc(c, 16, &tot, "count"));
     a.work = work.as<uint32_t>();
     HIP_TRY(c, k::wcoj_work(a, c->stream));
-    HIP_TRY(c, k::nonzero_flags(work.as<uint32_t>(), a.na, flag_pos.as<uint32_t>(), c->stream));
-    HIP_TRY(c, k::scan_exclusive_u32(flag_pos.as<uint32_t>(), flag_pos.as<uint32_t>(), a.na, tot.as<uint32_t>(), tmp.p,
+    // flags and positions in separate arrays: the scan then takes its
+    // one-launch form (it reads other tiles' flags)
+    HIP_TRY(c, k::nonzero_flags(work.as<uint32_t>(), a.na, flags.as<uint32_t>(), c->stream));
+    HIP_TRY(c, k::scan_exclusive_u32(flags.as<uint32_t>(), flag_pos.as<uint32_t>(), a.na, tot.as<uint32_t>(), tmp.p,
                                      c->stream));
     uint32_t nz = 0;
     XL_TRY(ctl_read(c, tot.p, 4, &nz));
