@@ -2134,9 +2134,10 @@ __global__ __launch_bounds__(MK_THREADS) void bits_list_k(uint32_t* bits, int64_
 // Marked slots -> slot list in one pass, clearing the marks: each wavefront
 // takes 128 consecutive words (two per lane, lane-major, so the loads
 // coalesce; a wavefront's word columns go out one after another, so short
-// wavefronts finish sooner), reserves its entries with one atomic on *total
-// and writes them
-// in word order.  The list is ascending within each wavefront's range and
+// wavefronts finish sooner); the four wavefronts of a workgroup reserve
+// their entries with one atomic on *total (one per wavefront put thousands
+// of same-address atomics in line) and each writes its entries in word
+// order.  The list is ascending within each wavefront's range and
 // the ranges land in any order: for consumers that take each listed key on
 // its own (the dense pull folds every key's in-edges itself).  Each word
 // column's entries are staged in LDS (entry o at o + o / 32, so the lanes of
@@ -2146,11 +2147,12 @@ constexpr int LW_WORDS = 2;
 constexpr int LW_STAGE = 64 * 32 + 64;  // one column's entries, padded
 __global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t nw, uint32_t* list, uint32_t* total) {
   __shared__ uint32_t stage_all[4][LW_STAGE];
-  const int lane = lane_id();
-  uint32_t* stage = stage_all[threadIdx.x >> 6];
-  const int64_t nwaves = (int64_t)gridDim.x * 4;
-  for (int64_t w0 = (((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6) * 64 * LW_WORDS; w0 < nw;
-       w0 += nwaves * 64 * LW_WORDS) {
+  __shared__ uint32_t s_all[4], s_base[4];
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+  uint32_t* stage = stage_all[wv];
+  // workgroup-uniform steps (the reservation takes two barriers)
+  for (int64_t g0 = (int64_t)blockIdx.x * 4 * 64 * LW_WORDS; g0 < nw; g0 += (int64_t)gridDim.x * 4 * 64 * LW_WORDS) {
+    const int64_t w0 = g0 + (int64_t)wv * 64 * LW_WORDS;
     uint32_t d[LW_WORDS], run[LW_WORDS], cnt[LW_WORDS], all = 0;
 #pragma unroll
     for (int k = 0; k < LW_WORDS; ++k) {
@@ -2162,10 +2164,20 @@ __global__ __launch_bounds__(256) void bits_list_waves_k(uint32_t* bits, int64_t
       cnt[k] = __shfl(incl, 63, 64);
       all += cnt[k];
     }
-    if (all == 0) continue;  // (wave-uniform)
-    uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(total, all);
-    base = __shfl(base, 0, 64);
+    if (lane == 0) s_all[wv] = all;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const uint32_t a0 = s_all[0], a1 = s_all[1], a2 = s_all[2], a3 = s_all[3];
+      const uint32_t sum = a0 + a1 + a2 + a3;
+      const uint32_t b = sum ? atomicAdd(total, sum) : 0u;
+      s_base[0] = b;
+      s_base[1] = b + a0;
+      s_base[2] = b + a0 + a1;
+      s_base[3] = b + a0 + a1 + a2;
+    }
+    __syncthreads();
+    if (all == 0) continue;  // (wave-uniform; the next step's barriers come after s_base is read)
+    uint32_t base = s_base[wv];
 #pragma unroll
     for (int k = 0; k < LW_WORDS; ++k) {
       if (cnt[k] == 0) continue;  // (wave-uniform)
